@@ -1,0 +1,236 @@
+/*
+ * gnnshap.h - C ABI of the GNNShap coalition-evaluation path for one AMD
+ * Instinct MI355X (gfx950).
+ *
+ * GNNShap (Akkas & Azad, arXiv 2401.04829) explains the prediction of a GNN
+ * for one target node v by a Shapley value for every directed edge of v's
+ * pruned computational graph.  Alg. 1 of the paper has four steps; each has
+ * an entry point here:
+ *
+ *   1. gnnshap_extract_subgraph   prune the l-hop computational graph (Sec. 3.2)
+ *   2. gnnshap_plan_samples       size classes and weights (eq. 4-6, Alg. 2)
+ *      gnnshap_sample_coalitions  coalition masks and weights (Alg. 3, App. C.1)
+ *   3. gnnshap_eval_coalitions    masked GCN predictions (Sec. 3.4)
+ *   4. gnnshap_solve_wls          constrained weighted least squares (eq. 2-3, Sec. 3.5)
+ *
+ * Conventions shared by every call:
+ *   - "[dev]" pointers are device memory of the current HIP device, "[host]"
+ *     pointers host memory.  Every buffer is owned by the caller; the library
+ *     allocates nothing (scratch space comes from the *_workspace queries,
+ *     which report the byte size of a caller-owned device buffer).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  All device work
+ *     is enqueued on it and is asynchronous, except where a call says it
+ *     blocks.
+ *   - Return value: a gnnshap_status.  No C++ exception crosses the ABI.  On
+ *     GNNSHAP_EINVAL or GNNSHAP_ECAPACITY nothing is written except the sizes
+ *     a call reports.  gnnshap_last_error() gives a thread-local message about
+ *     the last failure.
+ *   - All floating-point device data is fp32, row-major.
+ */
+#ifndef GNNSHAP_H
+#define GNNSHAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum gnnshap_status {
+  GNNSHAP_OK = 0,
+  GNNSHAP_EINVAL = 1,       /* invalid argument */
+  GNNSHAP_ECAPACITY = 2,    /* a caller buffer or workspace is too small; sizes reported */
+  GNNSHAP_EHIP = 3,         /* a HIP runtime call failed */
+  GNNSHAP_ESINGULAR = 4,    /* reserved: the solver reports pivots through `info` */
+  GNNSHAP_EUNSUPPORTED = 5  /* valid but outside what this build implements */
+};
+
+#define GNNSHAP_MAX_HOPS 8
+#define GNNSHAP_MAX_LAYERS 8
+#define GNNSHAP_MAX_CLASSES 1024
+
+const char* gnnshap_status_str(int status);
+const char* gnnshap_last_error(void);
+int gnnshap_version(void); /* major*10000 + minor*100 + patch */
+
+/* ------------------------------------------------------------------------ */
+/* Graph: in-CSR of a simple directed graph (row = destination).            */
+/* The sources of the edges u -> w are indices[indptr[w] .. indptr[w+1]),   */
+/* ascending, without duplicates or self loops.                             */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int64_t num_nodes;
+  int64_t num_edges;
+  const int64_t* indptr;   /* [dev] num_nodes + 1 */
+  const int32_t* indices;  /* [dev] num_edges */
+} gnnshap_graph;
+
+/* ------------------------------------------------------------------------ */
+/* 1. Pruned computational graph (Sec. 3.2 and App. A; Fig. 2).             */
+/*                                                                          */
+/* dist(u) = length of the shortest directed path u -> ... -> v.  With l =  */
+/* num_hops, the players are the edges whose message reaches v within l     */
+/* layers: E_c = {(u -> w) : dist(w) <= l-1}; the nodes are V_c = {u :      */
+/* dist(u) <= l}.  Local node ids sort V_c by (dist, global id): v is local */
+/* node 0 and the nodes within j hops are the prefix [0, hop_ptr[j+1]).     */
+/* Players are ordered by (local destination, source global id); the        */
+/* players entering local node x are [dst_ptr[x], dst_ptr[x+1]) for         */
+/* x < num_dst = hop_ptr[l] (the nodes within l-1 hops).  Players           */
+/* 0 .. indeg(v)-1 are the in-edges of v.                                   */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t num_hops;        /* in: l, 1 .. GNNSHAP_MAX_HOPS */
+  int32_t reserved;
+  int64_t cap_nodes;       /* in: capacity of node_gid (and of dst_ptr minus one) */
+  int64_t cap_edges;       /* in: capacity of edge_src, edge_dst, edge_gid */
+  int32_t* node_gid;       /* [dev] out: global id of local node i, i < num_nodes */
+  int32_t* dst_ptr;        /* [dev] out: num_dst + 1 player offsets */
+  int32_t* edge_src;       /* [dev] out: local source of player p */
+  int32_t* edge_dst;       /* [dev] out: local destination of player p */
+  int64_t* edge_gid;       /* [dev] out: position of player p in indices[] */
+  int64_t num_nodes;       /* out: |V_c| */
+  int64_t num_edges;       /* out: M = |E_c| (number of players) */
+  int64_t num_dst;         /* out: |H_{l-1}| */
+  int64_t hop_ptr[GNNSHAP_MAX_HOPS + 2]; /* out: hop_ptr[0..l+1] */
+} gnnshap_subgraph;
+
+/* Bytes of device workspace for graphs of `num_nodes` nodes. */
+int gnnshap_extract_workspace(int64_t num_nodes, size_t* bytes);
+
+/* Extracts the computational graph of `target`.  `ws` must be zero-filled
+ * before its first use; every call that returns (with any status) leaves it
+ * zero-filled again, so it can be reused across calls without clearing.
+ * BLOCKS the host: the sizes (num_nodes, num_edges, ...) are returned in *sg
+ * after a synchronisation of `stream`.  If cap_nodes or cap_edges is too
+ * small, returns GNNSHAP_ECAPACITY with the required sizes in *sg and writes
+ * no output array.  EINVAL: null pointers, target out of range, bad hops. */
+int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
+                             gnnshap_subgraph* sg, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* 2. Coalition sampling (Sec. 3.3, eq. 4-6, Alg. 2-3, App. C.1).           */
+/*                                                                          */
+/* Size class c (1 <= c <= M/2) holds the coalitions of size c and, through */
+/* complements, of size M-c; omega_c = kappa_c (M-1)/(c(M-c)) with kappa_c  */
+/* = 2, or 1 for the middle class c = M/2 of even M (eq. 4).  Classes are   */
+/* enumerated in ascending c while their eq. 5 share of the pairs left is   */
+/* at least their number of coalitions (Sec. 3.3.1 surplus redistribution); */
+/* the remaining pairs are spread over the other classes in proportion to   */
+/* omega (eq. 5), largest remainder, ties to the smaller c.  Enumerated     */
+/* rows carry the Kernel-SHAP weight (eq. 3) divided by sum(rho); all random */
+/* rows carry one common weight (Alg. 2).  Rows [0, k/2) are                */
+/* representatives: enumerated classes first (lexicographic rank order),    */
+/* then random classes (Floyd's algorithm on Philox4x32-10 draws: draw s of */
+/* row i uses counter (s/4, i, stream_lo, stream_hi), key (seed_lo,         */
+/* seed_hi), word s%4, mapped to [0, j] as (u*(j+1))>>32).  Row i + k/2 is   */
+/* the complement of row i.                                                 */
+/*                                                                          */
+/* Mask layout: row b is words_per_row = ceil(M/64) uint64 words; player j  */
+/* is bit j%64 of word b*words_per_row + j/64; padding bits are zero.       */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t size;            /* coalition size c of the representative rows */
+  int32_t full;            /* 1 = enumerated in rank order, 0 = random */
+  int64_t row_begin;       /* first representative row of the class */
+  int64_t row_count;       /* number of representative rows */
+  double weight;           /* weight of each row of the class and of its complement */
+} gnnshap_class;
+
+typedef struct {
+  int64_t num_players;     /* in: M >= 2 */
+  int64_t num_samples;     /* in: p >= 2, even (the budget) */
+  uint64_t seed;           /* in: Philox key */
+  uint64_t stream_id;      /* in: Philox stream (e.g. the target's global id) */
+  int64_t num_rows;        /* out: k <= p rows actually produced (even) */
+  int64_t words_per_row;   /* out: ceil(M/64) */
+  int64_t num_classes;     /* out: number of gnnshap_class records */
+  int64_t random_begin;    /* out: first random representative row */
+  double full_fraction;    /* out: total weight of the enumerated rows */
+  double random_weight;    /* out: weight of every random row (0 if none) */
+} gnnshap_sample_plan;
+
+/* Host-only, pure.  Fills *plan's outputs and classes[0 .. num_classes).
+ * If `classes` is NULL or cap_classes < num_classes, returns
+ * GNNSHAP_ECAPACITY with the outputs of *plan filled.  EINVAL: M < 2, odd
+ * or non-positive p, or more than 2^31 rows. */
+int gnnshap_plan_samples(gnnshap_sample_plan* plan, gnnshap_class* classes,
+                         int64_t cap_classes);
+
+/* Bytes of device workspace for gnnshap_sample_coalitions. */
+int gnnshap_sample_workspace(const gnnshap_sample_plan* plan, size_t* bytes);
+
+/* Writes masks[num_rows * words_per_row] and weights[num_rows] (fp32, the
+ * rounding of the fp64 class weight).  `classes` is the host table filled
+ * by gnnshap_plan_samples; it is copied to `ws` on `stream` and must stay
+ * unchanged until that copy has run.  EUNSUPPORTED: M too large for the
+ * on-chip row buffer (M > 131072). */
+int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
+                              const gnnshap_class* classes,
+                              uint64_t* masks, float* weights,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* 3. Masked GCN predictions (Sec. 3.4, GCN of Sec. 4.2).                   */
+/*                                                                          */
+/* For coalition S: A_S[w,u] = 1 iff (u -> w) in S; deg_S(x) = 1 + in-degree */
+/* of x under S; Ahat_S = D^-1/2 (A_S + I) D^-1/2; H^0 = X[V_c];            */
+/* H^l = Ahat_S H^(l-1) W_l + b_l with ReLU after every layer but the last; */
+/* y = H^L[v, target_class].  Coalitions without an in-edge of v are not    */
+/* evaluated: their value is f(empty) (Sec. 3.4.1, exact).                  */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t num_layers;            /* L, 1 .. GNNSHAP_MAX_LAYERS */
+  int32_t reserved;
+  const int32_t* dims;           /* [host] L + 1 widths: dims[0] = feature width d,
+                                    dims[L] = number of classes C */
+  const float* const* W;         /* [host] L [dev] pointers; W_l is dims[l] x dims[l+1] */
+  const float* const* b;         /* [host] L [dev] pointers, or NULL entries / NULL = zero bias */
+} gnnshap_gcn;
+
+/* Bytes of device workspace for evaluating k coalitions of subgraph sg. */
+int gnnshap_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_gcn* m,
+                           int64_t k, size_t* bytes);
+
+/* y[b] = f(S_b) for b < k.  X is the [dev] feature matrix of the whole graph
+ * (num_nodes x dims[0]).  target_class >= 0 selects the explained logit;
+ * -1 selects argmax_c f(E_c)[c] (ties to the lowest c), computed on the
+ * device and written to *class_out if class_out is not NULL ([dev] int32).
+ * f_empty_full[0] = f(empty), f_empty_full[1] = f(E_c) ([dev] 2 floats). */
+int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m,
+                            const float* X, int32_t target_class,
+                            const uint64_t* masks, int64_t k,
+                            int64_t words_per_row, float* y,
+                            float* f_empty_full, int32_t* class_out,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* 4. Constrained Kernel-SHAP least squares (eq. 2-3, Alg. 1, Sec. 3.5).    */
+/*                                                                          */
+/* phi = argmin sum_b w_b (y_b - f(empty) - m_b . phi)^2 subject to         */
+/* sum(phi) = f(E_c) - f(empty) (efficiency; eq. 3's infinite weights at    */
+/* the empty and full coalitions), over the rows of a plan.  Solved as the  */
+/* projected system (P G P + gamma 11^T/M) psi = P(r - Delta/M G 1),        */
+/* phi = Delta/M + psi, P = I - 11^T/M, with G = M^T W M built from exact   */
+/* integer coalition counts and factored by Cholesky.                       */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace for a plan. */
+int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes);
+
+/* phi[M] from the plan's masks, the predictions y[k] and f_empty_full[2]
+ * (all [dev]).  `classes` as for gnnshap_sample_coalitions.  *info ([dev]
+ * int32) receives 0, or j > 0 if the j-th pivot (1-based) of the Cholesky
+ * factorisation was not positive (phi is then not meaningful; this happens
+ * when the sampled rows do not determine phi). */
+int gnnshap_solve_wls(const gnnshap_sample_plan* plan,
+                      const gnnshap_class* classes, const uint64_t* masks,
+                      const float* y, const float* f_empty_full, float* phi,
+                      int32_t* info, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GNNSHAP_H */

@@ -42,10 +42,16 @@ SATURATE = 1 << 62
 
 
 def binom_sat(n, r):
-    """C(n, r) saturated at 2^62 (exact integers)."""
+    """C(n, r) saturated at 2^62 (exact integers below that)."""
     if r < 0 or r > n:
         return 0
-    return min(math.comb(n, r), SATURATE)
+    r = min(r, n - r)
+    v = 1
+    for i in range(1, r + 1):
+        v = v * (n - r + i) // i          # C(n-r+i, i), exact at every step
+        if v >= SATURATE:
+            return SATURATE
+    return v
 
 
 def class_tables(M):
@@ -56,7 +62,9 @@ def class_tables(M):
         kappa = 2.0 if paired else 1.0
         rho = float(M - 1) / (float(c) * float(M - c))      # eq. 4
         omega = kappa * rho
-        n_rows = binom_sat(M, c) if paired else min(math.comb(M, c) // 2, SATURATE)
+        n_rows = binom_sat(M, c)
+        if not paired:
+            n_rows = n_rows if n_rows >= SATURATE else n_rows // 2
         out.append((c, kappa, omega, n_rows))
     return out
 
@@ -157,25 +165,27 @@ def unrank(M, c, q):
 def floyd_rows(M, c, rows, seed, stream):
     """Floyd's random c-subsets of {0..M-1} for representative rows `rows`.
 
-    Vectorised over rows; the c steps run in order, exactly as Floyd's
-    algorithm prescribes for each row.  Returns a bool array [len(rows), M].
+    `c` is one size or one size per row.  Vectorised over rows; for each row
+    the c steps run in order, exactly as Floyd's algorithm prescribes.
+    Returns a bool array [len(rows), M].
     """
     rows = np.asarray(rows, dtype=np.uint64)
     nr = rows.shape[0]
+    cs = np.broadcast_to(np.asarray(c, dtype=np.int64), (nr,))
     sel = np.zeros((nr, M), dtype=bool)
     seed_lo, seed_hi = seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF
     st_lo, st_hi = stream & 0xFFFFFFFF, (stream >> 32) & 0xFFFFFFFF
-    ar = np.arange(nr)
     words = None
-    for s in range(c):
+    for s in range(int(cs.max()) if nr else 0):
+        act = np.flatnonzero(cs > s)              # rows that still take a step
         if s % 4 == 0:
             words = philox4x32_10_np(np.uint64(s // 4), rows, st_lo, st_hi, seed_lo, seed_hi)
-        u = words[s % 4]
-        j = M - c + s
-        t = ((u * np.uint64(j + 1)) >> np.uint64(32)).astype(np.int64)   # uniform in [0, j]
-        hit = sel[ar, t]
+        u = words[s % 4][act]
+        j = M - cs[act] + s
+        t = ((u * (j + 1).astype(np.uint64)) >> np.uint64(32)).astype(np.int64)   # uniform in [0, j]
+        hit = sel[act, t]
         pick = np.where(hit, j, t)
-        sel[ar, pick] = True
+        sel[act, pick] = True
     return sel
 
 
@@ -184,14 +194,17 @@ def sample(pl, seed, stream):
     M, k, half = pl["M"], pl["k"], pl["half"]
     masks = np.zeros((k, M), dtype=bool)
     w = np.zeros(k, dtype=np.float64)
+    sizes = np.zeros(half, dtype=np.int64)
     for cl in pl["classes"]:
         r0, n, c = cl["row_begin"], cl["row_count"], cl["c"]
         if cl["full"]:
             for q in range(n):
                 masks[r0 + q, unrank(M, c, q)] = True
-        else:
-            masks[r0:r0 + n] = floyd_rows(M, c, np.arange(r0, r0 + n), seed, stream)
+        sizes[r0:r0 + n] = c
         w[r0:r0 + n] = cl["weight"]
+    rb = pl["random_begin"]
+    if rb < half:
+        masks[rb:half] = floyd_rows(M, sizes[rb:half], np.arange(rb, half), seed, stream)
     masks[half:] = ~masks[:half]                      # complement pairing
     w[half:] = w[:half]
     return masks, w
@@ -212,3 +225,24 @@ def unpack(words, M):
     k = words.shape[0]
     by = words.view(np.uint8).reshape(k, -1)
     return np.unpackbits(by, axis=1, bitorder="little")[:, :M].astype(bool)
+
+
+def sample_rows(pl, rows, seed, stream):
+    """Masks (bool [len(rows), M]) and weights of selected rows of the plan,
+    each built by its own definition: an unranked subset, a Floyd subset, or
+    the complement of its representative row."""
+    M, half = pl["M"], pl["half"]
+    rows = np.asarray(rows, dtype=np.int64)
+    rep = np.where(rows >= half, rows - half, rows)
+    out = np.zeros((rows.size, M), dtype=bool)
+    w = np.zeros(rows.size, dtype=np.float64)
+    starts = np.array([cl["row_begin"] for cl in pl["classes"]])
+    for t, r in enumerate(rep):
+        cl = pl["classes"][int(np.searchsorted(starts, r, side="right")) - 1]
+        if cl["full"]:
+            out[t, unrank(M, cl["c"], int(r - cl["row_begin"]))] = True
+        else:
+            out[t] = floyd_rows(M, cl["c"], np.array([r]), seed, stream)[0]
+        w[t] = cl["weight"]
+    out[rows >= half] = ~out[rows >= half]
+    return out, w

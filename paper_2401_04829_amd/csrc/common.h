@@ -1,0 +1,60 @@
+// Internal helpers shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "gnnshap.h"
+
+namespace gnnshap {
+
+// Records a thread-local message and returns `status`.
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+// Bump allocator over a caller-owned workspace.  With base == nullptr it only
+// measures, so the *_workspace queries and the calls share one layout.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  size_t bytes() const { return (off + 255) & ~size_t(255); }
+};
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Grid size for grid-stride loops: enough blocks to fill 256 CUs several times.
+inline unsigned grid_for(int64_t items, int block, int64_t cap = 8192) {
+  int64_t g = ceil_div(items, block);
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return static_cast<unsigned>(g);
+}
+
+}  // namespace gnnshap
+
+#define GS_HIP(call)                                                                     \
+  do {                                                                                   \
+    hipError_t gs_e_ = (call);                                                           \
+    if (gs_e_ != hipSuccess)                                                             \
+      return ::gnnshap::fail(GNNSHAP_EHIP, "%s failed: %s (%s:%d)", #call,              \
+                             hipGetErrorString(gs_e_), __FILE__, __LINE__);              \
+  } while (0)
+
+#define GS_LAUNCHED() GS_HIP(hipGetLastError())
+
+#define GS_TRY_BEGIN try {
+#define GS_TRY_END                                                               \
+  }                                                                              \
+  catch (...) {                                                                  \
+    return ::gnnshap::fail(GNNSHAP_EHIP, "unexpected C++ exception");            \
+  }

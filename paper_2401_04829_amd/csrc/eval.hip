@@ -1,0 +1,580 @@
+// Masked GCN predictions for a batch of coalitions (Sec. 3.4 of the GNNShap
+// paper; the GCN of Sec. 4.2).
+//
+// Layer l of the GCN under coalition S, at a node x within l-1 hops of v:
+//   H^l[x] = act( d_x^-1/2 ( sum_{(u->x) in S} d_u^-1/2 Z^l[u] + d_x^-1/2 Z^l[x] ) + b_l ),
+//   Z^l = H^(l-1) W_l,  d = 1 + in-degree under S.
+// Only what reaches the target is computed: layer l is needed at the nodes
+// within L-l hops.  Nodes at the computational graph's outer boundary (dist
+// = hops) have no players entering them, so their representations do not
+// depend on S; they are computed once per target ("constant" rows), as is
+// Z^1 = X[V_c] W_1.  Everything else is per coalition:
+//   degrees   popcount of the mask bits of each destination's player range;
+//   aggregate a tile of 32 coalitions x one destination x a feature slice
+//             per block: the constant source rows of a chunk of 64 players
+//             are staged in LDS once and reused by all 32 coalitions;
+//   transform (L >= 3) the per-coalition rows times W_l;
+//   final     the target's logit, y = d_v^-1/2 (sum d_u^-1/2 H[u].w + d_v^-1/2 H[v].w) + b.
+// Coalitions without an in-edge of v are not evaluated (Sec. 3.4.1): their
+// value is f(empty), which is exact.  f(empty) and f(E_c) come from two extra
+// rows (no players / all players) run through the same kernels first.
+#include "common.h"
+
+namespace {
+
+constexpr int kTB = 32;          // coalitions per aggregation block
+constexpr int kChunkE = 64;      // players staged per step
+constexpr size_t kTileBudget = size_t(1) << 30;  // bytes of per-coalition scratch
+
+struct Shape {
+  int L = 0, hops = 0;
+  int64_t n_nodes = 0, n_dst = 0, bnd0 = 0, bnd1 = 0;  // boundary rows [bnd0, bnd1)
+  int dims[GNNSHAP_MAX_LAYERS + 1] = {};
+  int64_t nd[GNNSHAP_MAX_LAYERS + 1] = {};  // rows of H^j that depend on S: [0, nd[j])
+  bool bnd[GNNSHAP_MAX_LAYERS + 1] = {};    // H^j is needed at the boundary rows
+  int64_t tile = 0;                          // coalitions per pass
+  int64_t k = 0, wpr = 0;
+};
+
+struct Ws {
+  int32_t* ctl;        // [0] class, [1] live count
+  uint64_t* sp_masks;  // 2 rows: no players, all players
+  int32_t* sp_rows;    // {0, 1}
+  float* sp_y;         // 2 x C
+  int32_t* live_rows;  // k
+  uint8_t* live_flag;  // k
+  float* Zc[GNNSHAP_MAX_LAYERS + 1];  // constant Z^j rows (n_nodes x dims[j])
+  float* Bc[GNNSHAP_MAX_LAYERS + 1];  // constant H^j rows at the boundary
+  float* dinv;                        // tile x n_dst
+  float* Hb[GNNSHAP_MAX_LAYERS + 1];  // tile x nd[j] x dims[j]
+  float* Zb[GNNSHAP_MAX_LAYERS + 1];  // tile x nd[j-1] x dims[j]
+};
+
+int64_t per_row_bytes(const Shape& s) {
+  int64_t b = s.n_dst;
+  for (int j = 1; j < s.L; ++j) b += s.nd[j] * s.dims[j];
+  for (int j = 2; j < s.L; ++j) b += s.nd[j - 1] * s.dims[j];
+  return 4 * b;
+}
+
+Ws carve(gnnshap::Carver& c, const Shape& s) {
+  Ws w{};
+  const int C = s.dims[s.L];
+  w.ctl = c.take<int32_t>(8);
+  w.sp_masks = c.take<uint64_t>(2 * s.wpr);
+  w.sp_rows = c.take<int32_t>(2);
+  w.sp_y = c.take<float>(2 * C);
+  w.live_rows = c.take<int32_t>(s.k);
+  w.live_flag = c.take<uint8_t>(s.k);
+  w.Zc[1] = c.take<float>(s.n_nodes * s.dims[1]);
+  for (int j = 1; j < s.L; ++j) {
+    if (!s.bnd[j]) continue;
+    w.Bc[j] = c.take<float>(s.n_nodes * s.dims[j]);
+    if (j + 1 < s.L) w.Zc[j + 1] = c.take<float>(s.n_nodes * s.dims[j + 1]);
+  }
+  w.dinv = c.take<float>(s.tile * s.n_dst);
+  for (int j = 1; j < s.L; ++j) w.Hb[j] = c.take<float>(s.tile * s.nd[j] * s.dims[j]);
+  for (int j = 2; j < s.L; ++j) w.Zb[j] = c.take<float>(s.tile * s.nd[j - 1] * s.dims[j]);
+  return w;
+}
+
+int make_shape(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, Shape* out) {
+  if (!sg || !m || !m->dims) return gnnshap::fail(GNNSHAP_EINVAL, "null subgraph or model");
+  Shape s;
+  s.L = m->num_layers;
+  s.hops = sg->num_hops;
+  if (s.L < 1 || s.L > GNNSHAP_MAX_LAYERS) return gnnshap::fail(GNNSHAP_EINVAL, "num_layers out of range");
+  if (s.hops < 1 || s.hops > GNNSHAP_MAX_HOPS) return gnnshap::fail(GNNSHAP_EINVAL, "num_hops out of range");
+  for (int j = 0; j <= s.L; ++j) {
+    s.dims[j] = m->dims[j];
+    if (s.dims[j] < 1 || s.dims[j] > (1 << 20)) return gnnshap::fail(GNNSHAP_EINVAL, "bad layer width");
+  }
+  if (s.dims[s.L] > GNNSHAP_MAX_CLASSES) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "too many classes");
+  s.n_nodes = sg->num_nodes;
+  s.n_dst = sg->num_dst;
+  if (s.n_nodes < 1 || s.n_dst < 1 || s.n_dst > s.n_nodes || sg->hop_ptr[s.hops] != s.n_dst ||
+      sg->hop_ptr[s.hops + 1] != s.n_nodes || sg->num_edges < 1)
+    return gnnshap::fail(GNNSHAP_EINVAL, "subgraph sizes are inconsistent");
+  s.bnd0 = sg->hop_ptr[s.hops];
+  s.bnd1 = sg->hop_ptr[s.hops + 1];
+  s.nd[0] = 0;
+  for (int j = 1; j <= s.L; ++j) {
+    const int r = std::min(s.L - j, s.hops - 1);
+    s.nd[j] = sg->hop_ptr[r + 1];
+    s.bnd[j] = (s.L - j) >= s.hops && s.bnd1 > s.bnd0;
+  }
+  s.k = k;
+  s.wpr = (sg->num_edges + 63) / 64;
+  const int64_t prb = per_row_bytes(s);
+  int64_t t = static_cast<int64_t>(kTileBudget / static_cast<size_t>(prb > 0 ? prb : 1));
+  if (t > k) t = k;
+  if (t >= kTB) t -= t % kTB;
+  if (t < 2) t = 2;
+  s.tile = t;
+  *out = s;
+  return GNNSHAP_OK;
+}
+
+__device__ inline int64_t rows_in_pass(const int32_t* dyn_count, int64_t dyn_off, int64_t cap) {
+  if (!dyn_count) return cap;
+  int64_t r = static_cast<int64_t>(*dyn_count) - dyn_off;
+  return r < 0 ? 0 : (r > cap ? cap : r);
+}
+
+__global__ void k_init(int32_t* ctl, uint64_t* sp_masks, int32_t* sp_rows, int64_t wpr, int64_t M) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t < 8) ctl[t] = 0;
+  if (t < 2) sp_rows[t] = static_cast<int32_t>(t);
+  for (int64_t w = t; w < wpr; w += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    sp_masks[w] = 0;
+    const int64_t lo = w * 64;
+    const int64_t nb = M - lo >= 64 ? 64 : M - lo;
+    sp_masks[wpr + w] = nb >= 64 ? ~uint64_t(0) : ((uint64_t(1) << nb) - 1);
+  }
+}
+
+// C[m, :] = op(A[row(m), :]) B for m in [m0, m0 + rows), 64x64 tiles, fp32.
+// row(m) = arow ? arow[m] : m; op(a) = relu(a + abias) if abias else a.
+__global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64_t lda,
+                                              const int32_t* __restrict__ arow,
+                                              const float* __restrict__ abias,
+                                              const float* __restrict__ B, int64_t ldb,
+                                              float* __restrict__ C, int64_t ldc, int64_t m0,
+                                              int64_t rows, int64_t N, int64_t K,
+                                              const int32_t* dyn_count, int64_t dyn_off,
+                                              int64_t dyn_cap, int64_t dyn_mult) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64];
+  if (dyn_count) {
+    const int64_t r = rows_in_pass(dyn_count, dyn_off, dyn_cap) * dyn_mult;
+    if (r < rows) rows = r;
+  }
+  const int64_t mb = m0 + static_cast<int64_t>(blockIdx.x) * 64;
+  if (mb >= m0 + rows) return;
+  const int64_t nb = static_cast<int64_t>(blockIdx.y) * 64;
+  const int tid = threadIdx.x;
+  const int ty = tid / 16, tx = tid % 16;
+  float acc[4][4] = {};
+  for (int64_t k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + i * 256;
+      const int r = idx / 16, kk = idx % 16;
+      const int64_t m = mb + r;
+      float a = 0.f;
+      if (m < m0 + rows && k0 + kk < K) {
+        const int64_t ar = arow ? static_cast<int64_t>(arow[m]) : m;
+        a = A[ar * lda + k0 + kk];
+        if (abias) a = fmaxf(a + abias[k0 + kk], 0.f);
+      }
+      As[kk][r] = a;
+      const int kb = idx / 64, nn = idx % 64;
+      float b = 0.f;
+      if (k0 + kb < K && nb + nn < N) b = B[(k0 + kb) * ldb + nb + nn];
+      Bs[kb][nn] = b;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = As[kk][ty * 4 + i];
+        b[i] = Bs[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int jn = 0; jn < 4; ++jn) acc[i][jn] += a[i] * b[jn];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = mb + ty * 4 + i;
+    if (m >= m0 + rows) continue;
+#pragma unroll
+    for (int jn = 0; jn < 4; ++jn) {
+      const int64_t n = nb + tx * 4 + jn;
+      if (n < N) C[m * ldc + n] = acc[i][jn];
+    }
+  }
+}
+
+__global__ void k_bias_relu(const float* __restrict__ Z, const float* __restrict__ bias,
+                            float* __restrict__ H, int64_t r0, int64_t r1, int h) {
+  const int64_t total = (r1 - r0) * h;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t idx = r0 * h + t;
+    const float bb = bias ? bias[t % h] : 0.f;
+    H[idx] = fmaxf(Z[idx] + bb, 0.f);
+  }
+}
+
+// dinv[b, x] = (1 + popcount of row b's bits in player range of x)^-1/2.
+__global__ void __launch_bounds__(256) k_degrees(const uint64_t* __restrict__ masks, int64_t wpr,
+                                                 const int32_t* __restrict__ rows, int64_t row_off,
+                                                 int64_t cap, const int32_t* dyn_count,
+                                                 const int32_t* __restrict__ dst_ptr, int64_t n_dst,
+                                                 float* __restrict__ dinv) {
+  const int64_t nr = rows_in_pass(dyn_count, row_off, cap);
+  const int64_t total = nr * n_dst;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t b = t / n_dst, x = t % n_dst;
+    const uint64_t* mrow = masks + static_cast<int64_t>(rows[row_off + b]) * wpr;
+    const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+    int cnt = 0;
+    for (int64_t w = e0 >> 6; w <= ((e1 - 1) >> 6) && e1 > e0; ++w) {
+      uint64_t word = mrow[w];
+      const int64_t lo = w * 64;
+      if (e0 > lo) word &= ~uint64_t(0) << (e0 - lo);
+      if (e1 < lo + 64) word &= (uint64_t(1) << (e1 - lo)) - 1;
+      cnt += __popcll(word);
+    }
+    dinv[t] = rsqrtf(1.0f + static_cast<float>(cnt));
+  }
+}
+
+// Masked aggregation of layer j for a tile of kTB coalitions, one destination
+// x and one feature slice of width 8*FPT.  Thread (tb, fg): coalition tb,
+// features fs0 + fg*FPT .. +FPT.
+template <int FPT>
+__global__ void __launch_bounds__(256) k_aggregate(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows,
+    int64_t row_off, int64_t cap, const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr,
+    const int32_t* __restrict__ edge_src, int64_t n_dst, const float* __restrict__ dinv,
+    const float* __restrict__ Zc, const float* __restrict__ Zb, int64_t nd_prev,
+    const float* __restrict__ bias, float* __restrict__ Hout, int64_t nd_out, int h,
+    int64_t n_tiles, int n_slices) {
+  constexpr int FS = 8 * FPT;
+  __shared__ float zs[kChunkE][FS];
+  __shared__ int32_t ss[kChunkE];
+  const int64_t nr = rows_in_pass(dyn_count, row_off, cap);
+  int64_t bid = blockIdx.x;
+  const int slice = static_cast<int>(bid % n_slices);
+  bid /= n_slices;
+  const int64_t tile = bid % n_tiles;
+  const int64_t x = bid / n_tiles;
+  if (tile * kTB >= nr) return;
+  const int tid = threadIdx.x;
+  const int tb = tid >> 3, fg = tid & 7;
+  const int64_t b = tile * kTB + tb;
+  const bool valid = b < nr;
+  const int fs0 = slice * FS;
+  const int f0 = fs0 + fg * FPT;
+  const uint64_t* mrow = valid ? masks + static_cast<int64_t>(rows[row_off + b]) * wpr : masks;
+  const float* drow = dinv + (valid ? b : 0) * n_dst;
+  const float* zbrow = Zb ? Zb + (valid ? b : 0) * nd_prev * h : nullptr;
+  float acc[FPT];
+#pragma unroll
+  for (int i = 0; i < FPT; ++i) acc[i] = 0.f;
+  const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+  for (int64_t ec = e0; ec < e1; ec += kChunkE) {
+    const int n = static_cast<int>(e1 - ec < kChunkE ? e1 - ec : kChunkE);
+    if (tid < n) ss[tid] = edge_src[ec + tid];
+    __syncthreads();
+    for (int idx = tid; idx < n * FS; idx += 256) {
+      const int e = idx / FS, f = idx % FS;
+      const int32_t u = ss[e];
+      zs[e][f] = (u >= nd_prev && fs0 + f < h) ? Zc[static_cast<int64_t>(u) * h + fs0 + f] : 0.f;
+    }
+    uint64_t bits = 0;
+    if (valid) {
+      const int64_t w0 = ec >> 6;
+      const int sh = static_cast<int>(ec & 63);
+      bits = mrow[w0] >> sh;
+      if (sh && w0 + 1 < wpr) bits |= mrow[w0 + 1] << (64 - sh);
+      if (n < 64) bits &= (uint64_t(1) << n) - 1;
+    }
+    __syncthreads();
+    while (bits) {
+      const int e = __ffsll(static_cast<long long>(bits)) - 1;
+      bits &= bits - 1;
+      const int32_t u = ss[e];
+      const float coef = u < n_dst ? drow[u] : 1.0f;
+      if (u < nd_prev) {
+        const float* zr = zbrow + static_cast<int64_t>(u) * h;
+#pragma unroll
+        for (int i = 0; i < FPT; ++i)
+          if (f0 + i < h) acc[i] += coef * zr[f0 + i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < FPT; ++i) acc[i] += coef * zs[e][fg * FPT + i];
+      }
+    }
+    __syncthreads();
+  }
+  if (!valid) return;
+  const float dx = drow[x];
+  const float* zx = x < nd_prev ? zbrow + x * h : Zc + x * h;
+  float* out = Hout + (b * nd_out + x) * h;
+#pragma unroll
+  for (int i = 0; i < FPT; ++i) {
+    const int f = f0 + i;
+    if (f < h) {
+      const float v = dx * (acc[i] + dx * zx[f]) + (bias ? bias[f] : 0.f);
+      out[f] = fmaxf(v, 0.f);
+    }
+  }
+}
+
+// The target's logit for each coalition of the pass: one wavefront per row.
+// T(u) = u < nd_last ? Hb[b, u] : Hc[u] (width h); y = d_v^-1/2 (sum_{S} d_u^-1/2
+// T(u).w_c + d_v^-1/2 T(v).w_c) + b_c.  With one layer T(u).w_c = Z^1[u, c].
+__global__ void __launch_bounds__(256) k_final(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows,
+    int64_t row_off, int64_t cap, const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr,
+    const int32_t* __restrict__ edge_src, int64_t n_dst, const float* __restrict__ dinv,
+    const float* __restrict__ Hb, const float* __restrict__ Hc, int64_t nd_last, int h,
+    const float* __restrict__ WL, const float* __restrict__ bL, int C, bool one_layer,
+    const int32_t* __restrict__ ctl, bool all_classes, float* __restrict__ y_rows,
+    float* __restrict__ y_all) {
+  const int64_t nr = rows_in_pass(dyn_count, row_off, cap);
+  const int lane = threadIdx.x & 63;
+  const int64_t b = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  if (b >= nr) return;
+  const int64_t row = rows[row_off + b];
+  const uint64_t* mrow = masks + row * wpr;
+  const float* drow = dinv + b * n_dst;
+  const float dv = drow[0];
+  const int64_t e1 = dst_ptr[1];
+  const int c_lo = all_classes ? 0 : ctl[0];
+  const int c_hi = all_classes ? C : c_lo + 1;
+  for (int c = c_lo; c < c_hi; ++c) {
+    float acc = 0.f;
+    for (int64_t e = 0; e < e1; ++e) {
+      if (!((mrow[e >> 6] >> (e & 63)) & 1)) continue;
+      const int32_t u = edge_src[e];
+      const float coef = u < n_dst ? drow[u] : 1.0f;
+      if (one_layer) {
+        if (lane == 0) acc += coef * Hc[static_cast<int64_t>(u) * C + c];
+      } else {
+        const float* t = u < nd_last ? Hb + (b * nd_last + u) * h : Hc + static_cast<int64_t>(u) * h;
+        float d = 0.f;
+        for (int f = lane; f < h; f += 64) d += t[f] * WL[static_cast<int64_t>(f) * C + c];
+        acc += coef * d;
+      }
+    }
+    {
+      if (one_layer) {
+        if (lane == 0) acc += dv * Hc[c];
+      } else {
+        const float* t = 0 < nd_last ? Hb + (b * nd_last) * h : Hc;
+        float d = 0.f;
+        for (int f = lane; f < h; f += 64) d += t[f] * WL[static_cast<int64_t>(f) * C + c];
+        acc += dv * d;
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    const float yv = dv * acc + (bL ? bL[c] : 0.f);
+    if (lane == 0) {
+      if (all_classes) y_all[b * C + c] = yv;
+      else y_rows[row] = yv;
+    }
+  }
+}
+
+__global__ void k_pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
+                             int32_t* class_out, float* f_empty_full) {
+  int c = requested;
+  if (c < 0) {
+    c = 0;
+    for (int i = 1; i < C; ++i)
+      if (sp_y[C + i] > sp_y[C + c]) c = i;
+  }
+  ctl[0] = c;
+  if (class_out) *class_out = c;
+  f_empty_full[0] = sp_y[c];
+  f_empty_full[1] = sp_y[C + c];
+}
+
+// A coalition is evaluated only if it holds an in-edge of v (players [0, indeg v)).
+__global__ void __launch_bounds__(256) k_live(const uint64_t* __restrict__ masks, int64_t wpr,
+                                              int64_t k, const int32_t* __restrict__ dst_ptr,
+                                              int32_t* ctl, int32_t* live_rows, uint8_t* live_flag) {
+  const int lane = threadIdx.x & 63;
+  const int64_t indeg = dst_ptr[1];
+  const int64_t nwords = (indeg + 63) >> 6;
+  for (int64_t b0 = static_cast<int64_t>(blockIdx.x) * blockDim.x; b0 < k;
+       b0 += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t b = b0 + threadIdx.x;
+    bool live = false;
+    if (b < k) {
+      const uint64_t* mrow = masks + b * wpr;
+      for (int64_t w = 0; w < nwords; ++w) {
+        uint64_t word = mrow[w];
+        const int64_t rem = indeg - w * 64;
+        if (rem < 64) word &= (uint64_t(1) << rem) - 1;
+        if (word) {
+          live = true;
+          break;
+        }
+      }
+      live_flag[b] = live ? 1 : 0;
+    }
+    const uint64_t bal = __ballot(live);
+    if (bal) {
+      int base = 0;
+      if (lane == 0) base = atomicAdd(&ctl[1], __popcll(bal));
+      base = __shfl(base, 0);
+      if (live) live_rows[base + __popcll(bal & ((1ull << lane) - 1ull))] = static_cast<int32_t>(b);
+    }
+  }
+}
+
+__global__ void k_fill_pruned(const uint8_t* __restrict__ live_flag, int64_t k,
+                              const float* __restrict__ f_empty_full, float* __restrict__ y) {
+  const float f0 = f_empty_full[0];
+  for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < k;
+       b += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    if (!live_flag[b]) y[b] = f0;
+}
+
+int launch_gemm(hipStream_t s, const float* A, int64_t lda, const int32_t* arow, const float* abias,
+                const float* B, int64_t ldb, float* C, int64_t ldc, int64_t m0, int64_t rows, int64_t N,
+                int64_t K, const int32_t* dyn = nullptr, int64_t dyn_off = 0, int64_t dyn_cap = 0,
+                int64_t dyn_mult = 0) {
+  if (rows <= 0) return GNNSHAP_OK;
+  dim3 grid(static_cast<unsigned>(gnnshap::ceil_div(rows, 64)), static_cast<unsigned>(gnnshap::ceil_div(N, 64)));
+  k_gemm<<<grid, 256, 0, s>>>(A, lda, arow, abias, B, ldb, C, ldc, m0, rows, N, K, dyn, dyn_off,
+                              dyn_cap, dyn_mult);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int launch_aggregate(hipStream_t s, int h, const uint64_t* masks, int64_t wpr, const int32_t* rows,
+                     int64_t row_off, int64_t cap, const int32_t* dyn, const gnnshap_subgraph* sg,
+                     const Shape& sh, const float* dinv, const float* Zc, const float* Zb,
+                     int64_t nd_prev, const float* bias, float* Hout, int64_t nd_out) {
+  int fpt = 16;
+  while (fpt > 1 && 8 * (fpt / 2) >= h) fpt /= 2;
+  const int fs = 8 * fpt;
+  const int64_t n_tiles = gnnshap::ceil_div(cap, kTB);
+  const int n_slices = static_cast<int>(gnnshap::ceil_div(h, fs));
+  const int64_t blocks = n_tiles * nd_out * n_slices;
+  if (blocks > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "aggregation grid too large");
+  const unsigned g = static_cast<unsigned>(blocks);
+#define GS_AGG(F)                                                                                  \
+  k_aggregate<F><<<g, 256, 0, s>>>(masks, wpr, rows, row_off, cap, dyn, sg->dst_ptr, sg->edge_src, \
+                                   sh.n_dst, dinv, Zc, Zb, nd_prev, bias, Hout, nd_out, h, n_tiles, \
+                                   n_slices)
+  switch (fpt) {
+    case 1: GS_AGG(1); break;
+    case 2: GS_AGG(2); break;
+    case 4: GS_AGG(4); break;
+    case 8: GS_AGG(8); break;
+    default: GS_AGG(16); break;
+  }
+#undef GS_AGG
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+// Runs degrees -> layers 1..L-1 -> final for `cap` rows (or a device count).
+int run_pass(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn* m, const Shape& sh,
+             const Ws& w, const uint64_t* masks, const int32_t* rows, int64_t row_off, int64_t cap,
+             const int32_t* dyn, bool all_classes, float* y_rows) {
+  const int L = sh.L;
+  k_degrees<<<gnnshap::grid_for(cap * sh.n_dst, 256), 256, 0, s>>>(masks, sh.wpr, rows, row_off, cap,
+                                                                    dyn, sg->dst_ptr, sh.n_dst, w.dinv);
+  GS_LAUNCHED();
+  for (int j = 1; j < L; ++j) {
+    const float* Zb = j >= 2 ? w.Zb[j] : nullptr;
+    const float* bias = m->b ? m->b[j - 1] : nullptr;
+    if (int st = launch_aggregate(s, sh.dims[j], masks, sh.wpr, rows, row_off, cap, dyn, sg, sh, w.dinv,
+                                  w.Zc[j], Zb, sh.nd[j - 1], bias, w.Hb[j], sh.nd[j]))
+      return st;
+    if (j + 1 < L) {
+      if (int st = launch_gemm(s, w.Hb[j], sh.dims[j], nullptr, nullptr, m->W[j], sh.dims[j + 1], w.Zb[j + 1],
+                               sh.dims[j + 1], 0, cap * sh.nd[j], sh.dims[j + 1], sh.dims[j], dyn, row_off,
+                               cap, sh.nd[j]))
+        return st;
+    }
+  }
+  const int C = sh.dims[L];
+  const bool one = L == 1;
+  const float* Hb = one ? nullptr : w.Hb[L - 1];
+  const float* Hc = one ? w.Zc[1] : w.Bc[L - 1];
+  const int64_t nd_last = one ? 0 : sh.nd[L - 1];
+  const int h = one ? 1 : sh.dims[L - 1];
+  k_final<<<static_cast<unsigned>(gnnshap::ceil_div(cap, 4)), 256, 0, s>>>(
+      masks, sh.wpr, rows, row_off, cap, dyn, sg->dst_ptr, sg->edge_src, sh.n_dst, w.dinv, Hb, Hc,
+      nd_last, h, m->W[L - 1], m->b ? m->b[L - 1] : nullptr, C, one, w.ctl, all_classes, y_rows, w.sp_y);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k,
+                                      size_t* bytes) {
+  gnnshap::clear_error();
+  if (!bytes || k < 1) return gnnshap::fail(GNNSHAP_EINVAL, "bad arguments");
+  Shape sh;
+  if (int st = make_shape(sg, m, k, &sh)) return st;
+  gnnshap::Carver c(nullptr);
+  carve(c, sh);
+  *bytes = c.bytes();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X,
+                                       int32_t target_class, const uint64_t* masks, int64_t k,
+                                       int64_t words_per_row, float* y, float* f_empty_full,
+                                       int32_t* class_out, void* ws, size_t ws_bytes, void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (k < 1) return gnnshap::fail(GNNSHAP_EINVAL, "k must be >= 1");
+  Shape sh;
+  if (int st = make_shape(sg, m, k, &sh)) return st;
+  if (!X || !masks || !y || !f_empty_full || !ws || !m->W) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  for (int l = 0; l < sh.L; ++l)
+    if (!m->W[l]) return gnnshap::fail(GNNSHAP_EINVAL, "null weight matrix %d", l);
+  if (!sg->node_gid || !sg->dst_ptr || !sg->edge_src) return gnnshap::fail(GNNSHAP_EINVAL, "null subgraph arrays");
+  if (words_per_row != sh.wpr) return gnnshap::fail(GNNSHAP_EINVAL, "words_per_row != ceil(M/64)");
+  if (target_class >= sh.dims[sh.L] || target_class < -1) return gnnshap::fail(GNNSHAP_EINVAL, "target_class out of range");
+  if (k > INT32_MAX) return gnnshap::fail(GNNSHAP_EINVAL, "k too large");
+  gnnshap::Carver need(nullptr);
+  carve(need, sh);
+  if (ws_bytes < need.bytes()) return gnnshap::fail(GNNSHAP_ECAPACITY, "eval workspace needs %zu bytes", need.bytes());
+  gnnshap::Carver cv(ws);
+  const Ws w = carve(cv, sh);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int L = sh.L;
+
+  k_init<<<gnnshap::grid_for(sh.wpr, 256, 64), 256, 0, s>>>(w.ctl, w.sp_masks, w.sp_rows, sh.wpr, sg->num_edges);
+  GS_LAUNCHED();
+  // Constant rows: Z^1 = X[V_c] W_1, then the boundary chain.
+  if (int st = launch_gemm(s, X, sh.dims[0], sg->node_gid, nullptr, m->W[0], sh.dims[1], w.Zc[1], sh.dims[1], 0,
+                           sh.n_nodes, sh.dims[1], sh.dims[0]))
+    return st;
+  for (int j = 1; j < L; ++j) {
+    if (!sh.bnd[j]) continue;
+    k_bias_relu<<<gnnshap::grid_for((sh.bnd1 - sh.bnd0) * sh.dims[j], 256, 1024), 256, 0, s>>>(
+        w.Zc[j], m->b ? m->b[j - 1] : nullptr, w.Bc[j], sh.bnd0, sh.bnd1, sh.dims[j]);
+    GS_LAUNCHED();
+    if (j + 1 < L) {
+      if (int st = launch_gemm(s, w.Bc[j], sh.dims[j], nullptr, nullptr, m->W[j], sh.dims[j + 1], w.Zc[j + 1],
+                               sh.dims[j + 1], sh.bnd0, sh.bnd1 - sh.bnd0, sh.dims[j + 1], sh.dims[j]))
+        return st;
+    }
+  }
+  // f(empty) and f(E_c) for every class, then the explained class.
+  if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
+  k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
+  GS_LAUNCHED();
+  // Prediction pruning, then the live coalitions in passes of sh.tile rows.
+  k_live<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(masks, sh.wpr, k, sg->dst_ptr, w.ctl, w.live_rows,
+                                                         w.live_flag);
+  GS_LAUNCHED();
+  for (int64_t off = 0; off < k; off += sh.tile) {
+    const int64_t cap = std::min(sh.tile, k - off);
+    if (int st = run_pass(s, sg, m, sh, w, masks, w.live_rows, off, cap, w.ctl + 1, false, y)) return st;
+  }
+  k_fill_pruned<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(w.live_flag, k, f_empty_full, y);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+  GS_TRY_END
+}

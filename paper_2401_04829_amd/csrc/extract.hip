@@ -1,0 +1,311 @@
+// Pruned computational graph of a target node (Sec. 3.2 and App. A of the
+// GNNShap paper): BFS over in-edges to depth l, local ids by (dist, global
+// id), players = in-edges of the nodes within l-1 hops, in CSR order.
+//
+// Device steps: one launch per BFS level (wave per frontier node, wave-
+// aggregated queue appends), a two-pass compaction of the visited marks in
+// global-id order (which yields the (dist, id) order without a sort), a scan
+// of the destinations' in-degrees, then the player arrays.  The host waits
+// once, to learn the sizes.
+#include "common.h"
+
+namespace {
+
+constexpr int kLevels = GNNSHAP_MAX_HOPS + 1;  // dist 0 .. MAX_HOPS
+constexpr int kPerThread = 16;
+constexpr int kChunk = 256 * kPerThread;      // marks per compaction block
+constexpr int kCounters = 32;                 // int64: [0, kLevels) level sizes, [kLevels] = M
+
+struct Ws {
+  int32_t* mark;      // N: dist + 1, 0 = unvisited (zero between calls)
+  int32_t* local_of;  // N: local id of a visited node
+  int32_t* queue;     // N: BFS queue, level by level
+  int32_t* sorted;    // N: visited nodes by (dist, id)
+  int32_t* dstptr;    // N + 1
+  int64_t* counters;  // kCounters
+  int32_t* bcount;    // nblk * kLevels
+};
+
+Ws carve(gnnshap::Carver& c, int64_t n) {
+  Ws w;
+  const int64_t nblk = gnnshap::ceil_div(n, kChunk);
+  w.mark = c.take<int32_t>(n);
+  w.local_of = c.take<int32_t>(n);
+  w.queue = c.take<int32_t>(n);
+  w.sorted = c.take<int32_t>(n);
+  w.dstptr = c.take<int32_t>(n + 1);
+  w.counters = c.take<int64_t>(kCounters);
+  w.bcount = c.take<int32_t>(nblk * kLevels);
+  return w;
+}
+
+__global__ void k_init(int32_t* mark, int32_t* queue, int64_t* counters, int64_t v) {
+  for (int i = 0; i < kCounters; ++i) counters[i] = 0;
+  counters[0] = 1;
+  mark[v] = 1;
+  queue[0] = static_cast<int32_t>(v);
+}
+
+// Expands BFS level `level`: frontier = queue[begin, begin + counters[level]).
+__global__ void __launch_bounds__(256) k_expand(const int64_t* __restrict__ indptr,
+                                                const int32_t* __restrict__ indices,
+                                                int32_t* mark, int32_t* queue,
+                                                int64_t* counters, int level) {
+  int64_t begin = 0;
+  for (int i = 0; i < level; ++i) begin += counters[i];
+  const int64_t size = counters[level];
+  const int64_t end = begin + size;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = (static_cast<int64_t>(gridDim.x) * blockDim.x) >> 6;
+  for (int64_t f = wave; f < size; f += nwaves) {
+    const int32_t w = queue[begin + f];
+    const int64_t e0 = indptr[w], e1 = indptr[w + 1];
+    for (int64_t e = e0; e < e1; e += 64) {
+      bool win = false;
+      int32_t u = 0;
+      if (e + lane < e1) {
+        u = indices[e + lane];
+        win = atomicCAS(&mark[u], 0, level + 2) == 0;
+      }
+      const uint64_t bal = __ballot(win);
+      if (bal) {
+        unsigned long long base = 0;
+        if (lane == 0)
+          base = atomicAdd(reinterpret_cast<unsigned long long*>(&counters[level + 1]),
+                           static_cast<unsigned long long>(__popcll(bal)));
+        base = __shfl(base, 0);
+        if (win) {
+          const int rank = __popcll(bal & ((1ull << lane) - 1ull));
+          queue[end + static_cast<int64_t>(base) + rank] = u;
+        }
+      }
+    }
+  }
+}
+
+// Per block of kChunk marks: number of visited nodes of each level.
+__global__ void __launch_bounds__(256) k_count_levels(const int32_t* __restrict__ mark, int64_t n,
+                                                      int32_t* bcount, int levels) {
+  __shared__ int cnt[kLevels];
+  if (threadIdx.x < kLevels) cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kChunk + threadIdx.x * kPerThread;
+  int m[kPerThread];
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) m[i] = (base + i < n) ? mark[base + i] : 0;
+  for (int l = 0; l < levels; ++l) {
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) c += (m[i] == l + 1);
+    if (c) atomicAdd(&cnt[l], c);
+  }
+  __syncthreads();
+  if (threadIdx.x < levels) bcount[static_cast<int64_t>(blockIdx.x) * kLevels + threadIdx.x] = cnt[threadIdx.x];
+}
+
+// Writes the visited nodes in (level, id) order: sorted[pos] = id, local_of[id] = pos.
+__global__ void __launch_bounds__(256) k_scatter_levels(const int32_t* __restrict__ mark, int64_t n,
+                                                        const int32_t* __restrict__ bcount,
+                                                        const int64_t* __restrict__ counters,
+                                                        int levels, int32_t* sorted,
+                                                        int32_t* local_of) {
+  __shared__ int64_t off[kLevels];
+  __shared__ int scan[256];
+  const int tid = threadIdx.x;
+  if (tid < levels) {
+    int64_t hb = 0;
+    for (int i = 0; i < tid; ++i) hb += counters[i];
+    int64_t s = 0;
+    for (int64_t b = 0; b < blockIdx.x; ++b) s += bcount[b * kLevels + tid];
+    off[tid] = hb + s;
+  }
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kChunk + tid * kPerThread;
+  int m[kPerThread];
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) m[i] = (base + i < n) ? mark[base + i] : 0;
+  __syncthreads();
+  for (int l = 0; l < levels; ++l) {
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) c += (m[i] == l + 1);
+    scan[tid] = c;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {   // inclusive Hillis-Steele scan
+      const int v = tid >= d ? scan[tid - d] : 0;
+      __syncthreads();
+      scan[tid] += v;
+      __syncthreads();
+    }
+    int64_t pos = off[l] + scan[tid] - c;
+#pragma unroll
+    for (int i = 0; i < kPerThread; ++i) {
+      if (m[i] == l + 1) {
+        const int32_t gid = static_cast<int32_t>(base + i);
+        sorted[pos] = gid;
+        local_of[gid] = static_cast<int32_t>(pos);
+        ++pos;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// dstptr = exclusive scan of the in-degrees of the nodes within hops-1 hops;
+// counters[kLevels] = M.  One block.
+__global__ void __launch_bounds__(1024) k_dst_ptr(const int64_t* __restrict__ indptr,
+                                                  const int32_t* __restrict__ sorted,
+                                                  int64_t* counters, int hops, int32_t* dstptr) {
+  __shared__ int64_t buf[1024];
+  __shared__ int64_t carry;
+  const int tid = threadIdx.x;
+  int64_t n_dst = 0;
+  for (int i = 0; i < hops; ++i) n_dst += counters[i];
+  if (tid == 0) {
+    carry = 0;
+    dstptr[0] = 0;
+  }
+  __syncthreads();
+  for (int64_t b0 = 0; b0 < n_dst; b0 += 1024) {
+    const int64_t x = b0 + tid;
+    int64_t deg = 0;
+    if (x < n_dst) {
+      const int32_t g = sorted[x];
+      deg = indptr[g + 1] - indptr[g];
+    }
+    buf[tid] = deg;
+    __syncthreads();
+    for (int d = 1; d < 1024; d <<= 1) {
+      const int64_t v = tid >= d ? buf[tid - d] : 0;
+      __syncthreads();
+      buf[tid] += v;
+      __syncthreads();
+    }
+    if (x < n_dst) dstptr[x + 1] = static_cast<int32_t>(carry + buf[tid]);
+    __syncthreads();
+    if (tid == 1023) carry += buf[1023];
+    __syncthreads();
+  }
+  if (tid == 0) counters[kLevels] = carry;
+}
+
+__global__ void __launch_bounds__(256) k_fill_edges(const int64_t* __restrict__ indptr,
+                                                    const int32_t* __restrict__ indices,
+                                                    const int32_t* __restrict__ sorted,
+                                                    const int32_t* __restrict__ local_of,
+                                                    const int32_t* __restrict__ dstptr,
+                                                    int64_t n_dst, int32_t* edge_src,
+                                                    int32_t* edge_dst, int64_t* edge_gid) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = (static_cast<int64_t>(gridDim.x) * blockDim.x) >> 6;
+  for (int64_t x = wave; x < n_dst; x += nwaves) {
+    const int32_t g = sorted[x];
+    const int64_t e0 = indptr[g];
+    const int64_t deg = indptr[g + 1] - e0;
+    const int64_t out = dstptr[x];
+    for (int64_t j = lane; j < deg; j += 64) {
+      const int64_t e = e0 + j;
+      edge_src[out + j] = local_of[indices[e]];
+      edge_dst[out + j] = static_cast<int32_t>(x);
+      edge_gid[out + j] = e;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) k_cleanup(int32_t* mark, const int32_t* __restrict__ queue,
+                                                 int64_t count) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    mark[queue[i]] = 0;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_extract_workspace(int64_t num_nodes, size_t* bytes) {
+  gnnshap::clear_error();
+  if (!bytes || num_nodes < 1) return gnnshap::fail(GNNSHAP_EINVAL, "bad arguments");
+  gnnshap::Carver c(nullptr);
+  carve(c, num_nodes);
+  *bytes = c.bytes();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
+                                        gnnshap_subgraph* sg, void* ws, size_t ws_bytes,
+                                        void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (!g || !sg || !ws) return gnnshap::fail(GNNSHAP_EINVAL, "null graph, subgraph or workspace");
+  if (!g->indptr || !g->indices) return gnnshap::fail(GNNSHAP_EINVAL, "null graph arrays");
+  const int64_t n = g->num_nodes;
+  if (n < 1 || n > INT32_MAX) return gnnshap::fail(GNNSHAP_EINVAL, "num_nodes out of range");
+  if (g->num_edges < 0) return gnnshap::fail(GNNSHAP_EINVAL, "num_edges < 0");
+  if (target < 0 || target >= n) return gnnshap::fail(GNNSHAP_EINVAL, "target out of range");
+  const int hops = sg->num_hops;
+  if (hops < 1 || hops > GNNSHAP_MAX_HOPS) return gnnshap::fail(GNNSHAP_EINVAL, "num_hops out of range");
+  gnnshap::Carver need(nullptr);
+  carve(need, n);
+  if (ws_bytes < need.bytes())
+    return gnnshap::fail(GNNSHAP_ECAPACITY, "extract workspace needs %zu bytes", need.bytes());
+  gnnshap::Carver c(ws);
+  const Ws w = carve(c, n);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int levels = hops + 1;
+  const int64_t nblk = gnnshap::ceil_div(n, kChunk);
+
+  k_init<<<1, 1, 0, s>>>(w.mark, w.queue, w.counters, target);
+  GS_LAUNCHED();
+  for (int l = 0; l < hops; ++l) {
+    k_expand<<<512, 256, 0, s>>>(g->indptr, g->indices, w.mark, w.queue, w.counters, l);
+    GS_LAUNCHED();
+  }
+  k_count_levels<<<static_cast<unsigned>(nblk), 256, 0, s>>>(w.mark, n, w.bcount, levels);
+  GS_LAUNCHED();
+  k_scatter_levels<<<static_cast<unsigned>(nblk), 256, 0, s>>>(w.mark, n, w.bcount, w.counters,
+                                                                levels, w.sorted, w.local_of);
+  GS_LAUNCHED();
+  k_dst_ptr<<<1, 1024, 0, s>>>(g->indptr, w.sorted, w.counters, hops, w.dstptr);
+  GS_LAUNCHED();
+
+  int64_t h[kCounters];
+  GS_HIP(hipMemcpyAsync(h, w.counters, sizeof(h), hipMemcpyDeviceToHost, s));
+  GS_HIP(hipStreamSynchronize(s));
+
+  int64_t nodes = 0;
+  sg->hop_ptr[0] = 0;
+  for (int l = 0; l < levels; ++l) {
+    nodes += h[l];
+    sg->hop_ptr[l + 1] = nodes;
+  }
+  for (int l = levels + 1; l < GNNSHAP_MAX_HOPS + 2; ++l) sg->hop_ptr[l] = nodes;
+  const int64_t n_dst = sg->hop_ptr[hops];
+  const int64_t m = h[kLevels];
+  sg->num_nodes = nodes;
+  sg->num_dst = n_dst;
+  sg->num_edges = m;
+
+  int status = GNNSHAP_OK;
+  if (m > INT32_MAX) {
+    status = gnnshap::fail(GNNSHAP_EUNSUPPORTED, "more than 2^31 players");
+  } else if (nodes > sg->cap_nodes || m > sg->cap_edges) {
+    status = gnnshap::fail(GNNSHAP_ECAPACITY, "subgraph needs %lld nodes and %lld edges",
+                           (long long)nodes, (long long)m);
+  } else if (!sg->node_gid || !sg->dst_ptr || (m > 0 && (!sg->edge_src || !sg->edge_dst || !sg->edge_gid))) {
+    status = gnnshap::fail(GNNSHAP_EINVAL, "null subgraph output arrays");
+  }
+  if (status == GNNSHAP_OK) {
+    GS_HIP(hipMemcpyAsync(sg->node_gid, w.sorted, nodes * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+    GS_HIP(hipMemcpyAsync(sg->dst_ptr, w.dstptr, (n_dst + 1) * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+    if (m > 0) {
+      k_fill_edges<<<gnnshap::grid_for(n_dst * 64, 256, 4096), 256, 0, s>>>(
+          g->indptr, g->indices, w.sorted, w.local_of, w.dstptr, n_dst, sg->edge_src,
+          sg->edge_dst, sg->edge_gid);
+      GS_LAUNCHED();
+    }
+  }
+  k_cleanup<<<gnnshap::grid_for(nodes, 256, 1024), 256, 0, s>>>(w.mark, w.queue, nodes);
+  GS_LAUNCHED();
+  return status;
+  GS_TRY_END
+}

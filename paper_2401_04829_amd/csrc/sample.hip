@@ -1,0 +1,231 @@
+// Coalition sampler (Sec. 3.3.2, Alg. 3 and App. C.1 of the GNNShap paper).
+//
+// One wavefront per representative row.  The row is built as a bitset in
+// LDS, then the row and its complement are written as packed uint64 words.
+// Enumerated classes unrank their lexicographic index; random classes run
+// Floyd's algorithm on Philox4x32-10 draws, 64 steps at a time: every lane
+// takes one step, lanes whose draw cannot interact with an earlier step of
+// the same chunk decide at once, the others are replayed in step order, so
+// the result is exactly the sequential algorithm's.
+#include "common.h"
+
+namespace {
+
+static_assert(sizeof(gnnshap_class) == 32, "class record layout");
+constexpr int64_t kMaxPlayers = 131072;  // 3 bitsets of M bits in 48 KiB of LDS
+
+struct Ws {
+  gnnshap_class* classes;
+};
+
+Ws carve(gnnshap::Carver& c, int64_t ncls) {
+  Ws w;
+  w.classes = c.take<gnnshap_class>(ncls > 0 ? ncls : 1);
+  return w;
+}
+
+// Philox4x32-10 (Salmon et al., SC'11).
+__device__ inline void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3,
+                                     uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c0), lo0 = 0xD2511F53u * c0;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c2), lo1 = 0xCD9E8D57u * c2;
+    const uint32_t n0 = hi1 ^ c1 ^ k0;
+    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+}
+
+// C(n, r), saturating at 2^62 (the unranked classes only need values < 2^32).
+__device__ inline uint64_t binom(int64_t n, int64_t r) {
+  if (r < 0 || r > n) return 0;
+  if (r > n - r) r = n - r;
+  uint64_t v = 1;
+  for (int64_t i = 1; i <= r; ++i) {
+    const uint64_t f = static_cast<uint64_t>(n - r + i);
+    if (v > (uint64_t(1) << 62) / f) return uint64_t(1) << 62;
+    v = v * f / static_cast<uint64_t>(i);
+  }
+  return v;
+}
+
+__device__ inline void set_bit(uint32_t* bs, int64_t j) { bs[j >> 5] |= 1u << (j & 31); }
+
+__global__ void __launch_bounds__(64) k_sample(const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                               int64_t half, int64_t M, int64_t wpr, uint32_t seed_lo,
+                                               uint32_t seed_hi, uint32_t st_lo, uint32_t st_hi,
+                                               uint64_t* __restrict__ masks,
+                                               float* __restrict__ weights) {
+  extern __shared__ uint32_t lds[];
+  const int64_t nw = 2 * wpr;           // 32-bit words per bitset
+  uint32_t* S = lds;                    // the row being built
+  uint32_t* D1 = S + nw;                // draws seen once in the current chunk
+  uint32_t* D2 = D1 + nw;               // draws seen twice or more
+  const int lane = threadIdx.x;
+  for (int64_t w = lane; w < nw; w += 64) {
+    D1[w] = 0;
+    D2[w] = 0;
+  }
+  for (int64_t i = blockIdx.x; i < half; i += gridDim.x) {
+    int64_t lo = 0, hi = ncls - 1;      // last class starting at or before row i
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (cls[mid].row_begin <= i) lo = mid; else hi = mid - 1;
+    }
+    const int64_t c = cls[lo].size;
+    const int full = cls[lo].full;
+    const int64_t rank = i - cls[lo].row_begin;
+    const float wt = static_cast<float>(cls[lo].weight);
+    for (int64_t w = lane; w < nw; w += 64) S[w] = 0;
+    __syncthreads();
+    if (full) {
+      if (lane == 0) {
+        // rank-th c-subset in lexicographic order: for each position, skip
+        // whole blocks of subsets with one binary search (hockey-stick sums).
+        uint64_t q = static_cast<uint64_t>(rank);
+        int64_t x = 0;
+        for (int64_t jj = 1; jj <= c; ++jj) {
+          const int64_t r = c - jj;
+          const uint64_t top = binom(M - x, r + 1);
+          int64_t a = x, b = M - r - 1;
+          while (a < b) {
+            const int64_t mid = (a + b + 1) >> 1;
+            if (top - binom(M - mid, r + 1) <= q) a = mid; else b = mid - 1;
+          }
+          q -= top - binom(M - a, r + 1);
+          set_bit(S, a);
+          x = a + 1;
+        }
+      }
+    } else {
+      for (int64_t base = 0; base < c; base += 64) {
+        const int64_t s = base + lane;
+        const bool act = s < c;
+        const int64_t j = M - c + s;
+        uint32_t t = 0;
+        if (act) {
+          uint32_t c0 = static_cast<uint32_t>(s >> 2), c1 = static_cast<uint32_t>(i), c2 = st_lo, c3 = st_hi;
+          philox4x32_10(c0, c1, c2, c3, seed_lo, seed_hi);
+          const int sel = static_cast<int>(s & 3);
+          const uint32_t u = sel == 0 ? c0 : sel == 1 ? c1 : sel == 2 ? c2 : c3;
+          t = static_cast<uint32_t>((static_cast<uint64_t>(u) * static_cast<uint64_t>(j + 1)) >> 32);
+        }
+        const int64_t wd = t >> 5;
+        const uint32_t bit = 1u << (t & 31);
+        if (act) {
+          const uint32_t old = atomicOr(&D1[wd], bit);
+          if (old & bit) atomicOr(&D2[wd], bit);
+        }
+        __syncthreads();
+        const bool dup = act && (D2[wd] & bit);
+        const bool hits_j = act && static_cast<int64_t>(t) >= M - c + base && static_cast<int64_t>(t) < j;
+        const bool dirty = dup || hits_j;
+        const bool in = act && !dirty && (S[wd] & bit);
+        __syncthreads();
+        if (act && !dirty) {
+          const int64_t ins = in ? j : static_cast<int64_t>(t);
+          atomicOr(&S[ins >> 5], 1u << (ins & 31));
+        }
+        __syncthreads();
+        uint64_t todo = __ballot(dirty);
+        while (todo) {                     // replay the interacting steps in order
+          const int l = __ffsll(static_cast<long long>(todo)) - 1;
+          todo &= todo - 1;
+          const uint32_t tl = __shfl(t, l);
+          if (lane == 0) {
+            const int64_t jl = M - c + base + l;
+            const bool inl = S[tl >> 5] & (1u << (tl & 31));
+            set_bit(S, inl ? jl : static_cast<int64_t>(tl));
+          }
+          __syncthreads();
+        }
+        if (act) {
+          D1[wd] = 0;
+          D2[wd] = 0;
+        }
+        __syncthreads();
+      }
+    }
+    __syncthreads();
+    const uint64_t tail = (M & 63) ? ((uint64_t(1) << (M & 63)) - 1) : ~uint64_t(0);
+    for (int64_t w = lane; w < wpr; w += 64) {
+      const uint64_t word = static_cast<uint64_t>(S[2 * w]) | (static_cast<uint64_t>(S[2 * w + 1]) << 32);
+      const uint64_t valid = (w == wpr - 1) ? tail : ~uint64_t(0);
+      masks[i * wpr + w] = word;
+      masks[(i + half) * wpr + w] = ~word & valid;
+    }
+    if (lane == 0) {
+      weights[i] = wt;
+      weights[i + half] = wt;
+    }
+    __syncthreads();
+  }
+}
+
+int check_plan(const gnnshap_sample_plan* plan) {
+  if (!plan) return gnnshap::fail(GNNSHAP_EINVAL, "plan is NULL");
+  if (plan->num_players < 2 || plan->num_rows < 2 || (plan->num_rows % 2) ||
+      plan->words_per_row != (plan->num_players + 63) / 64 || plan->num_classes < 1)
+    return gnnshap::fail(GNNSHAP_EINVAL, "plan is not the output of gnnshap_plan_samples");
+  return GNNSHAP_OK;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_sample_workspace(const gnnshap_sample_plan* plan, size_t* bytes) {
+  gnnshap::clear_error();
+  if (!bytes) return gnnshap::fail(GNNSHAP_EINVAL, "bytes is NULL");
+  if (int st = check_plan(plan)) return st;
+  gnnshap::Carver c(nullptr);
+  carve(c, plan->num_classes);
+  *bytes = c.bytes();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
+                                         const gnnshap_class* classes, uint64_t* masks,
+                                         float* weights, void* ws, size_t ws_bytes,
+                                         void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (int st = check_plan(plan)) return st;
+  if (!classes || !masks || !weights || !ws) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  const int64_t M = plan->num_players;
+  if (M > kMaxPlayers)
+    return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "sampler supports up to %lld players", (long long)kMaxPlayers);
+  gnnshap::Carver need(nullptr);
+  carve(need, plan->num_classes);
+  if (ws_bytes < need.bytes())
+    return gnnshap::fail(GNNSHAP_ECAPACITY, "sample workspace needs %zu bytes", need.bytes());
+  // The table must describe consecutive first-half rows.
+  int64_t row = 0;
+  for (int64_t i = 0; i < plan->num_classes; ++i) {
+    if (classes[i].row_begin != row || classes[i].row_count < 1 || classes[i].size < 1 ||
+        2 * static_cast<int64_t>(classes[i].size) > M)
+      return gnnshap::fail(GNNSHAP_EINVAL, "class table inconsistent at record %lld", (long long)i);
+    row += classes[i].row_count;
+  }
+  const int64_t half = plan->num_rows / 2;
+  if (row != half) return gnnshap::fail(GNNSHAP_EINVAL, "class table does not cover k/2 rows");
+  gnnshap::Carver c(ws);
+  const Ws w = carve(c, plan->num_classes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class),
+                        hipMemcpyHostToDevice, s));
+  const int64_t wpr = plan->words_per_row;
+  const size_t lds = static_cast<size_t>(3 * 2 * wpr) * sizeof(uint32_t);
+  const unsigned grid = static_cast<unsigned>(half < 65536 ? half : 65536);
+  k_sample<<<grid, 64, lds, s>>>(w.classes, plan->num_classes, half, M, wpr,
+                                 static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
+                                 static_cast<uint32_t>(plan->stream_id),
+                                 static_cast<uint32_t>(plan->stream_id >> 32), masks, weights);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+  GS_TRY_END
+}

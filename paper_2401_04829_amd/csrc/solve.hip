@@ -1,0 +1,589 @@
+// Constrained Kernel-SHAP weighted least squares (eq. 2-3, Alg. 1 step 5 and
+// Sec. 3.5 of the GNNShap paper).
+//
+// Minimise sum_b w_b (y_b - f0 - m_b.phi)^2 subject to sum(phi) = Delta =
+// f(E_c) - f0.  With phi = Delta/M 1 + psi, 1.psi = 0 and P = I - 11^T/M the
+// normal equations become  (P G P + gamma 11^T/M) psi = P (r - Delta/M G 1),
+// G = sum_b w_b m_b m_b^T, r = sum_b w_b (y_b - f0) m_b; the shift gamma =
+// tr(PGP)/(M-1) makes the system positive definite without changing psi.
+//
+// The plan's structure makes G exact and cheap:
+//   * a row and its complement give P(m m^T + mbar mbar^T)P = 2 P m m^T P;
+//   * an enumerated class of size c contributes w_c kappa_c C(M-2, c-1) P
+//     (all c-subsets: diagonal C(M-1,c-1), off-diagonal C(M-2,c-2));
+//   * the random rows share one weight w_r, so their part is 2 w_r P C_R P
+//     with C_R the integer co-occurrence counts of the random representative
+//     rows, computed exactly by popcounts on a bit-transposed copy.
+// Then a blocked right-looking Cholesky (64-wide panels) and two blocked
+// triangular solves.  The right-hand side is accumulated in fp64.
+#include <cmath>
+#include <vector>
+
+#include "common.h"
+
+namespace {
+
+constexpr int kNB = 64;
+
+struct Ws {
+  gnnshap_class* classes;
+  uint64_t* T;       // nrb x M: bit b of T[rb, j] = player j in random row rb*64+b
+  float* G;          // M x M (int32 counts first, then the system, lower part factored)
+  int64_t* usum;     // M: row sums of the counts
+  double* scal;      // [0] trace, [1] sigma, [2] gamma, [3] delta, [4] f0
+  double* part;      // nch x M partial right-hand sides
+  double* dz;        // half
+  float* rhs;        // M
+  float* x;          // M
+};
+
+constexpr int kMaxChunks = 256;
+
+int64_t n_chunks(int64_t half) {
+  int64_t c = gnnshap::ceil_div(half, 64);
+  return c < 1 ? 1 : (c > kMaxChunks ? kMaxChunks : c);
+}
+
+Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
+  Ws w;
+  const int64_t M = p->num_players;
+  const int64_t half = p->num_rows / 2;
+  const int64_t kr = half - p->random_begin;
+  const int64_t nrb = gnnshap::ceil_div(kr, 64);
+  w.classes = c.take<gnnshap_class>(p->num_classes > 0 ? p->num_classes : 1);
+  w.T = c.take<uint64_t>((nrb > 0 ? nrb : 1) * M);
+  w.G = c.take<float>(M * M);
+  w.usum = c.take<int64_t>(M);
+  w.scal = c.take<double>(16);
+  w.part = c.take<double>(n_chunks(half) * M);
+  w.dz = c.take<double>(half);
+  w.rhs = c.take<float>(M);
+  w.x = c.take<float>(M);
+  return w;
+}
+
+// T[rb, j]: transpose 64 rows x 64 players with ballots.  One wave per (rb, word).
+__global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ masks, int64_t wpr,
+                                                  int64_t row0, int64_t nrows, int64_t M,
+                                                  uint64_t* __restrict__ T) {
+  const int lane = threadIdx.x;
+  const int64_t rb = blockIdx.x;
+  const int64_t w = blockIdx.y;
+  const int64_t r = rb * 64 + lane;
+  const uint64_t word = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
+  uint64_t mine = 0;
+#pragma unroll 8
+  for (int p = 0; p < 64; ++p) {
+    const uint64_t bal = __ballot((word >> p) & 1);
+    if (lane == p) mine = bal;
+  }
+  const int64_t j = w * 64 + lane;
+  if (j < M) T[rb * M + j] = mine;
+}
+
+// Counts C[i, j] = sum_rb popcount(T[rb, i] & T[rb, j]) for 64x64 tiles with J >= I,
+// stored in both halves.
+__global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M,
+                                              int32_t* __restrict__ C) {
+  const int64_t I = blockIdx.y, J = blockIdx.x;
+  if (J < I) return;
+  __shared__ uint64_t Ti[16][64];
+  __shared__ uint64_t Tj[16][64];
+  const int tid = threadIdx.x;
+  const int ty = tid / 16, tx = tid % 16;
+  int acc[4][4] = {};
+  for (int64_t k0 = 0; k0 < nrb; k0 += 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + q * 256;
+      const int kk = idx / 64, c = idx % 64;
+      const int64_t i = I * 64 + c, j = J * 64 + c;
+      const bool kin = k0 + kk < nrb;
+      Ti[kk][c] = (kin && i < M) ? T[(k0 + kk) * M + i] : 0;
+      Tj[kk][c] = (kin && j < M) ? T[(k0 + kk) * M + j] : 0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < 16; ++kk) {
+      uint64_t a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[q] = Ti[kk][ty * 4 + q];
+        b[q] = Tj[kk][tx * 4 + q];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[q][r] += __popcll(a[q] & b[r]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t i = I * 64 + ty * 4 + q;
+    if (i >= M) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t j = J * 64 + tx * 4 + r;
+      if (j >= M) continue;
+      C[i * M + j] = acc[q][r];
+      C[j * M + i] = acc[q][r];
+    }
+  }
+}
+
+// usum[i] = sum_j C[i, j]; one wave per row.
+__global__ void __launch_bounds__(256) k_rowsum(const int32_t* __restrict__ C, int64_t M,
+                                                int64_t* __restrict__ usum) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  if (i >= M) return;
+  long long s = 0;
+  for (int64_t j = lane; j < M; j += 64) s += C[i * M + j];
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane == 0) usum[i] = s;
+}
+
+// scal: trace and sigma of the counts (exact), gamma, Delta, f0.  One block.
+__global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, const int64_t* __restrict__ usum,
+                                                 int64_t M, bool has_random, double alpha, double wr,
+                                                 const float* __restrict__ fef, double* scal) {
+  __shared__ long long st[256], ss[256];
+  const int tid = threadIdx.x;
+  long long tr = 0, sg = 0;
+  if (has_random)
+    for (int64_t i = tid; i < M; i += 256) {
+      tr += C[i * M + i];
+      sg += usum[i];
+    }
+  st[tid] = tr;
+  ss[tid] = sg;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if (tid < off) {
+      st[tid] += st[tid + off];
+      ss[tid] += ss[tid + off];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const double Md = static_cast<double>(M);
+    const double trace = static_cast<double>(st[0]);
+    const double sigma = static_cast<double>(ss[0]);
+    const double tr_pgp = alpha * (Md - 1.0) + 2.0 * wr * (trace - sigma / Md);
+    scal[0] = trace;
+    scal[1] = sigma;
+    scal[2] = tr_pgp / (Md - 1.0);
+    scal[3] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
+    scal[4] = static_cast<double>(fef[0]);
+  }
+}
+
+// In place: counts (int32) -> G~ (fp32), lower and upper.
+__global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restrict__ usum, int64_t M,
+                                               bool has_random, double alpha, double wr,
+                                               const double* __restrict__ scal) {
+  const double Md = static_cast<double>(M);
+  const double sigma = scal[1], gamma = scal[2];
+  const int64_t total = M * M;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t i = t / M, j = t % M;
+    double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
+    if (has_random) {
+      const double cij = static_cast<double>(reinterpret_cast<const int32_t*>(G)[t]);
+      v += 2.0 * wr * (cij - static_cast<double>(usum[i] + usum[j]) / Md + sigma / (Md * Md));
+    }
+    G[t] = static_cast<float>(v);
+  }
+}
+
+// dz[b] = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|), for b < half.
+__global__ void __launch_bounds__(256) k_dz(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
+                                            int64_t M, const float* __restrict__ y,
+                                            const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                            const double* __restrict__ scal, double* __restrict__ dz) {
+  const double Md = static_cast<double>(M);
+  const double delta = scal[3], f0 = scal[4];
+  for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < half;
+       b += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    int64_t lo = 0, hi = ncls - 1;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (cls[mid].row_begin <= b) lo = mid; else hi = mid - 1;
+    }
+    const double w = cls[lo].weight;
+    int64_t pc = 0;
+    for (int64_t q = 0; q < wpr; ++q) pc += __popcll(masks[b * wpr + q]);
+    const double z1 = w * (static_cast<double>(y[b]) - f0 - delta / Md * static_cast<double>(pc));
+    const double z2 = w * (static_cast<double>(y[b + half]) - f0 - delta / Md * static_cast<double>(M - pc));
+    dz[b] = z1 - z2;
+  }
+}
+
+// Partial right-hand sides: part[ch, j] = sum_{b in chunk ch} dz[b] m_bj.
+__global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ masks, int64_t wpr,
+                                                  int64_t half, int64_t M, const double* __restrict__ dz,
+                                                  int64_t rows_per_chunk, double* __restrict__ part) {
+  __shared__ double dzs[256];
+  const int tid = threadIdx.x;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per_chunk;
+  const int64_t r1 = r0 + rows_per_chunk < half ? r0 + rows_per_chunk : half;
+  for (int64_t j0 = 0; j0 < M; j0 += 256) {
+    const int64_t j = j0 + tid;
+    double acc = 0.0;
+    for (int64_t b0 = r0; b0 < r1; b0 += 256) {
+      const int nb = static_cast<int>(r1 - b0 < 256 ? r1 - b0 : 256);
+      __syncthreads();
+      if (tid < nb) dzs[tid] = dz[b0 + tid];
+      __syncthreads();
+      if (j < M) {
+        const uint64_t* col = masks + b0 * wpr + (j >> 6);
+        const int sh = static_cast<int>(j & 63);
+        for (int q = 0; q < nb; ++q)
+          if ((col[q * wpr] >> sh) & 1) acc += dzs[q];
+      }
+    }
+    if (j < M) part[static_cast<int64_t>(blockIdx.x) * M + j] = acc;
+  }
+}
+
+// rhs = P (sum of the partials); one block.
+__global__ void __launch_bounds__(1024) k_rhs_finish(const double* __restrict__ part, int64_t nch, int64_t M,
+                                                     float* __restrict__ rhs, double* scal) {
+  __shared__ double red[1024];
+  const int tid = threadIdx.x;
+  double s = 0.0;
+  for (int64_t j = tid; j < M; j += 1024) {
+    double v = 0.0;
+    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
+    s += v;
+  }
+  red[tid] = s;
+  __syncthreads();
+  for (int off = 512; off > 0; off >>= 1) {
+    if (tid < off) red[tid] += red[tid + off];
+    __syncthreads();
+  }
+  const double mean = red[0] / static_cast<double>(M);
+  for (int64_t j = tid; j < M; j += 1024) {
+    double v = 0.0;
+    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
+    rhs[j] = static_cast<float>(v - mean);
+  }
+}
+
+__global__ void k_zero_info(int32_t* info) { *info = 0; }
+
+// Cholesky of the diagonal block jb (in LDS); records the first bad pivot.
+__global__ void __launch_bounds__(256) k_potrf(float* G, int64_t M, int64_t jb, int32_t* info) {
+  __shared__ float A[kNB][kNB + 1];
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  const int tid = threadIdx.x;
+  for (int t = tid; t < n * n; t += 256) {
+    const int i = t / n, j = t % n;
+    A[i][j] = G[(o + i) * M + o + j];
+  }
+  __syncthreads();
+  for (int k = 0; k < n; ++k) {
+    float piv = A[k][k];
+    if (!(piv > 0.f)) {
+      if (tid == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
+      piv = 1.f;
+    }
+    const float lkk = sqrtf(piv);
+    __syncthreads();
+    if (tid == 0) A[k][k] = lkk;
+    for (int i = k + 1 + tid; i < n; i += 256) A[i][k] = A[i][k] / lkk;
+    __syncthreads();
+    for (int t = tid; t < (n - k - 1) * (n - k - 1); t += 256) {
+      const int i = k + 1 + t / (n - k - 1), j = k + 1 + t % (n - k - 1);
+      if (j <= i) A[i][j] -= A[i][k] * A[j][k];
+    }
+    __syncthreads();
+  }
+  for (int t = tid; t < n * n; t += 256) {
+    const int i = t / n, j = t % n;
+    G[(o + i) * M + o + j] = j <= i ? A[i][j] : 0.f;
+  }
+}
+
+// Panel: rows of block ib > jb: X <- X L_jj^-T.  One thread per row.
+__global__ void __launch_bounds__(64) k_trsm(float* G, int64_t M, int64_t jb) {
+  __shared__ float L[kNB][kNB + 1];
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  const int tid = threadIdx.x;
+  for (int t = tid; t < n * n; t += 64) {
+    const int i = t / n, j = t % n;
+    L[i][j] = G[(o + i) * M + o + j];
+  }
+  __syncthreads();
+  const int64_t r = o + n + static_cast<int64_t>(blockIdx.x) * 64 + tid;
+  if (r >= M) return;
+  float x[kNB];
+  float* row = G + r * M + o;
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) x[c] = c < n ? row[c] : 0.f;
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) {
+    if (c < n) {
+      float v = x[c];
+      for (int k = 0; k < c; ++k) v -= x[k] * L[c][k];
+      x[c] = v / L[c][c];
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+    if (c < n) row[c] = x[c];
+}
+
+// Trailing update of tile (ib, kb), jb < kb <= ib: A_ib,kb -= L_ib,jb L_kb,jb^T.
+__global__ void __launch_bounds__(256) k_syrk(float* G, int64_t M, int64_t jb) {
+  const int64_t ib = jb + 1 + blockIdx.y, kb = jb + 1 + blockIdx.x;
+  if (kb > ib) return;
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const int tid = threadIdx.x;
+  const int ty = tid / 16, tx = tid % 16;
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < n; k0 += 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + q * 256;
+      const int r = idx / 16, kk = idx % 16;
+      const int64_t gi = ib * kNB + r, gk = kb * kNB + r;
+      const bool kin = k0 + kk < n;
+      As[kk][r] = (kin && gi < M) ? G[gi * M + o + k0 + kk] : 0.f;
+      Bs[kk][r] = (kin && gk < M) ? G[gk * M + o + k0 + kk] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[q] = As[kk][ty * 4 + q];
+        b[q] = Bs[kk][tx * 4 + q];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[q][r] += a[q] * b[r];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t i = ib * kNB + ty * 4 + q;
+    if (i >= M) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t j = kb * kNB + tx * 4 + r;
+      if (j < M && j <= i) G[i * M + j] -= acc[q][r];
+    }
+  }
+}
+
+// Forward substitution on diagonal block jb: x_j = L_jj^-1 rhs_j (one wave).
+__global__ void __launch_bounds__(64) k_trsv_lower(const float* __restrict__ G, int64_t M, int64_t jb,
+                                                   const float* __restrict__ rhs, float* __restrict__ x) {
+  __shared__ float xs[kNB];
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  const int lane = threadIdx.x;
+  for (int c = 0; c < n; ++c) {
+    float v = lane < c ? G[(o + c) * M + o + lane] * xs[lane] : 0.f;
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) xs[c] = (rhs[o + c] - v) / G[(o + c) * M + o + c];
+    __syncthreads();
+  }
+  if (lane < n) x[o + lane] = xs[lane];
+}
+
+// rhs[i] -= sum_{k in block jb} L[i, k] x[k] for rows i after block jb.
+__global__ void __launch_bounds__(256) k_update_lower(const float* __restrict__ G, int64_t M, int64_t jb,
+                                                      const float* __restrict__ x, float* __restrict__ rhs) {
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  const int64_t i = o + n + static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  float v = 0.f;
+  for (int k = 0; k < n; ++k) v += G[i * M + o + k] * x[o + k];
+  rhs[i] -= v;
+}
+
+// Backward substitution on diagonal block jb: x_j = L_jj^-T a_j (one wave).
+__global__ void __launch_bounds__(64) k_trsv_upper(const float* __restrict__ G, int64_t M, int64_t jb,
+                                                   const float* __restrict__ a, float* __restrict__ x) {
+  __shared__ float xs[kNB];
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  const int lane = threadIdx.x;
+  for (int c = n - 1; c >= 0; --c) {
+    float v = (lane > c && lane < n) ? G[(o + lane) * M + o + c] * xs[lane] : 0.f;
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) xs[c] = (a[o + c] - v) / G[(o + c) * M + o + c];
+    __syncthreads();
+  }
+  if (lane < n) x[o + lane] = xs[lane];
+}
+
+// a[i] -= sum_{k in block jb} L[k, i] x[k] for rows i before block jb.
+__global__ void __launch_bounds__(256) k_update_upper(const float* __restrict__ G, int64_t M, int64_t jb,
+                                                      const float* __restrict__ x, float* __restrict__ a) {
+  const int64_t o = jb * kNB;
+  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= o) return;
+  float v = 0.f;
+  for (int k = 0; k < n; ++k) v += G[(o + k) * M + i] * x[o + k];
+  a[i] -= v;
+}
+
+__global__ void k_finish(const float* __restrict__ x, int64_t M, const double* __restrict__ scal,
+                         float* __restrict__ phi) {
+  const double base = scal[3] / static_cast<double>(M);
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < M;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    phi[i] = static_cast<float>(base + static_cast<double>(x[i]));
+}
+
+int check_plan(const gnnshap_sample_plan* p, const gnnshap_class* classes) {
+  if (!p) return gnnshap::fail(GNNSHAP_EINVAL, "plan is NULL");
+  if (p->num_players < 2 || p->num_rows < 2 || (p->num_rows % 2) ||
+      p->words_per_row != (p->num_players + 63) / 64 || p->num_classes < 1 || p->random_begin < 0 ||
+      p->random_begin > p->num_rows / 2)
+    return gnnshap::fail(GNNSHAP_EINVAL, "plan is not the output of gnnshap_plan_samples");
+  if (classes) {
+    int64_t row = 0;
+    for (int64_t i = 0; i < p->num_classes; ++i) {
+      if (classes[i].row_begin != row || classes[i].row_count < 1 ||
+          (classes[i].full != 0) != (row < p->random_begin))
+        return gnnshap::fail(GNNSHAP_EINVAL, "class table inconsistent at record %lld", (long long)i);
+      if (!classes[i].full && classes[i].weight != p->random_weight)
+        return gnnshap::fail(GNNSHAP_EINVAL, "random rows must share the plan's random weight");
+      row += classes[i].row_count;
+    }
+    if (row != p->num_rows / 2) return gnnshap::fail(GNNSHAP_EINVAL, "class table does not cover k/2 rows");
+  }
+  return GNNSHAP_OK;
+}
+
+// C(n, r) in fp64 (exact while below 2^53; the enumerated classes stay far below).
+double binom_d(int64_t n, int64_t r) {
+  if (r < 0 || r > n) return 0.0;
+  if (r > n - r) r = n - r;
+  double v = 1.0;
+  for (int64_t i = 1; i <= r; ++i) v = v * static_cast<double>(n - r + i) / static_cast<double>(i);
+  return v;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes) {
+  gnnshap::clear_error();
+  if (!bytes) return gnnshap::fail(GNNSHAP_EINVAL, "bytes is NULL");
+  if (int st = check_plan(plan, nullptr)) return st;
+  gnnshap::Carver c(nullptr);
+  carve(c, plan);
+  *bytes = c.bytes();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_class* classes,
+                                 const uint64_t* masks, const float* y, const float* f_empty_full, float* phi,
+                                 int32_t* info, void* ws, size_t ws_bytes, void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (!classes || !masks || !y || !f_empty_full || !phi || !info || !ws)
+    return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  if (int st = check_plan(plan, classes)) return st;
+  gnnshap::Carver need(nullptr);
+  carve(need, plan);
+  if (ws_bytes < need.bytes()) return gnnshap::fail(GNNSHAP_ECAPACITY, "solve workspace needs %zu bytes", need.bytes());
+  gnnshap::Carver cv(ws);
+  const Ws w = carve(cv, plan);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t M = plan->num_players;
+  const int64_t wpr = plan->words_per_row;
+  const int64_t half = plan->num_rows / 2;
+  const int64_t rb0 = plan->random_begin;
+  const int64_t kr = half - rb0;
+  const bool has_random = kr > 0;
+  const double wr = has_random ? plan->random_weight : 0.0;
+  // Enumerated classes: P (sum over the class and its complements) P = w kappa C(M-2, c-1) P.
+  double alpha = 0.0;
+  for (int64_t i = 0; i < plan->num_classes; ++i) {
+    if (!classes[i].full) continue;
+    const int64_t c = classes[i].size;
+    const double kappa = 2 * c < M ? 2.0 : 1.0;
+    alpha += classes[i].weight * kappa * binom_d(M - 2, c - 1);
+  }
+  GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class), hipMemcpyHostToDevice, s));
+  k_zero_info<<<1, 1, 0, s>>>(info);
+  GS_LAUNCHED();
+  int32_t* counts = reinterpret_cast<int32_t*>(w.G);
+  if (has_random) {
+    const int64_t nrb = gnnshap::ceil_div(kr, 64);
+    k_transpose<<<dim3(static_cast<unsigned>(nrb), static_cast<unsigned>(wpr)), 64, 0, s>>>(masks, wpr, rb0, kr, M, w.T);
+    GS_LAUNCHED();
+    const unsigned nb = static_cast<unsigned>(gnnshap::ceil_div(M, 64));
+    k_gram<<<dim3(nb, nb), 256, 0, s>>>(w.T, nrb, M, counts);
+    GS_LAUNCHED();
+    k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, w.usum);
+    GS_LAUNCHED();
+  }
+  k_scalars<<<1, 256, 0, s>>>(counts, w.usum, M, has_random, alpha, wr, f_empty_full, w.scal);
+  GS_LAUNCHED();
+  k_build<<<gnnshap::grid_for(M * M, 256, 16384), 256, 0, s>>>(w.G, w.usum, M, has_random, alpha, wr, w.scal);
+  GS_LAUNCHED();
+  const int64_t nch = n_chunks(half);
+  const int64_t rpc = gnnshap::ceil_div(half, nch);
+  k_dz<<<gnnshap::grid_for(half, 256, 4096), 256, 0, s>>>(masks, wpr, half, M, y, w.classes, plan->num_classes,
+                                                           w.scal, w.dz);
+  GS_LAUNCHED();
+  k_rhs_part<<<static_cast<unsigned>(nch), 256, 0, s>>>(masks, wpr, half, M, w.dz, rpc, w.part);
+  GS_LAUNCHED();
+  k_rhs_finish<<<1, 1024, 0, s>>>(w.part, nch, M, w.rhs, w.scal);
+  GS_LAUNCHED();
+  // Cholesky G~ = L L^T.
+  const int64_t nblk = gnnshap::ceil_div(M, kNB);
+  for (int64_t jb = 0; jb < nblk; ++jb) {
+    k_potrf<<<1, 256, 0, s>>>(w.G, M, jb, info);
+    GS_LAUNCHED();
+    const int64_t rest = nblk - jb - 1;
+    if (rest > 0) {
+      const int64_t rows = M - (jb + 1) * kNB;
+      k_trsm<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 64)), 64, 0, s>>>(w.G, M, jb);
+      GS_LAUNCHED();
+      k_syrk<<<dim3(static_cast<unsigned>(rest), static_cast<unsigned>(rest)), 256, 0, s>>>(w.G, M, jb);
+      GS_LAUNCHED();
+    }
+  }
+  // L a = rhs (a overwrites x), then L^T psi = a (psi overwrites rhs).
+  for (int64_t jb = 0; jb < nblk; ++jb) {
+    k_trsv_lower<<<1, 64, 0, s>>>(w.G, M, jb, w.rhs, w.x);
+    GS_LAUNCHED();
+    const int64_t rows = M - (jb + 1) * kNB;
+    if (rows > 0) {
+      k_update_lower<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 256)), 256, 0, s>>>(w.G, M, jb, w.x, w.rhs);
+      GS_LAUNCHED();
+    }
+  }
+  for (int64_t jb = nblk - 1; jb >= 0; --jb) {
+    k_trsv_upper<<<1, 64, 0, s>>>(w.G, M, jb, w.x, w.rhs);
+    GS_LAUNCHED();
+    if (jb > 0) {
+      k_update_upper<<<static_cast<unsigned>(gnnshap::ceil_div(jb * kNB, 256)), 256, 0, s>>>(w.G, M, jb, w.rhs, w.x);
+      GS_LAUNCHED();
+    }
+  }
+  k_finish<<<gnnshap::grid_for(M, 256, 1024), 256, 0, s>>>(w.rhs, M, w.scal, phi);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+  GS_TRY_END
+}

@@ -1,0 +1,156 @@
+"""Torch-facing driver of the four C-ABI calls for one graph and one GCN.
+
+Torch provides device memory and the stream; every computation runs in
+libgnnshap.so.  Buffers are caller-owned torch tensors and grow on demand.
+"""
+import ctypes
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib as L
+
+
+def _vp(t):
+    return ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+
+
+class _Buffer:
+    """Grow-only device byte buffer used as a library workspace."""
+
+    def __init__(self, device):
+        self.device = device
+        self.t = None
+
+    def get(self, nbytes):
+        nbytes = max(int(nbytes), 256)
+        if self.t is None or self.t.numel() < nbytes:
+            self.t = None
+            self.t = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self.t
+
+
+@dataclass
+class Subgraph:
+    sg: L.gnnshap_subgraph      # sizes (host struct, pointers into the arrays below)
+    node_gid: torch.Tensor      # int32 [n']
+    dst_ptr: torch.Tensor       # int32 [num_dst + 1]
+    edge_src: torch.Tensor      # int32 [M]
+    edge_dst: torch.Tensor      # int32 [M]
+    edge_gid: torch.Tensor      # int64 [M]
+
+    @property
+    def num_edges(self):
+        return self.sg.num_edges
+
+    @property
+    def hop_ptr(self):
+        return [self.sg.hop_ptr[i] for i in range(self.sg.num_hops + 2)]
+
+
+@dataclass
+class Explanation:
+    target: int
+    sub: Subgraph
+    plan: L.gnnshap_sample_plan
+    classes: object             # ctypes array of gnnshap_class
+    masks: torch.Tensor         # int64 [k, wpr] (uint64 bit patterns)
+    weights: torch.Tensor       # float32 [k]
+    y: torch.Tensor             # float32 [k]
+    f_empty_full: torch.Tensor  # float32 [2]
+    cls: torch.Tensor           # int32 [1]
+    phi: torch.Tensor           # float32 [M]
+    info: torch.Tensor          # int32 [1]
+
+
+class Explainer:
+    def __init__(self, indptr, indices, X, weights, biases, hops, device="cuda"):
+        L.load()
+        self.device = torch.device(device)
+        dev = self.device
+        self.indptr = torch.as_tensor(indptr, dtype=torch.int64).to(dev).contiguous()
+        self.indices = torch.as_tensor(indices, dtype=torch.int32).to(dev).contiguous()
+        self.X = torch.as_tensor(X, dtype=torch.float32).to(dev).contiguous()
+        self.W = [torch.as_tensor(w, dtype=torch.float32).to(dev).contiguous() for w in weights]
+        self.b = [None if b is None else torch.as_tensor(b, dtype=torch.float32).to(dev).contiguous() for b in biases]
+        self.hops = int(hops)
+        self.dims = [int(self.X.shape[1])] + [int(w.shape[1]) for w in self.W]
+        n = self.indptr.numel() - 1
+        self.graph = L.gnnshap_graph(num_nodes=n, num_edges=self.indices.numel(),
+                                     indptr=self.indptr.data_ptr(), indices=self.indices.data_ptr())
+        nl = len(self.W)
+        self._dims = (ctypes.c_int32 * (nl + 1))(*self.dims)
+        self._Wp = (ctypes.c_void_p * nl)(*[w.data_ptr() for w in self.W])
+        self._bp = (ctypes.c_void_p * nl)(*[0 if b is None else b.data_ptr() for b in self.b])
+        self.model = L.gnnshap_gcn(num_layers=nl, dims=self._dims, W=self._Wp, b=self._bp)
+        self.extract_ws = torch.zeros(L.gnnshap_extract_workspace(n), dtype=torch.uint8, device=dev)
+        self._cap_nodes = 0
+        self._cap_edges = 0
+        self._sub = None
+        self.ws_sample = _Buffer(dev)
+        self.ws_eval = _Buffer(dev)
+        self.ws_solve = _Buffer(dev)
+
+    def stream(self):
+        return ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream)
+
+    def _grow(self, nodes, edges):
+        dev = self.device
+        self._cap_nodes = max(int(nodes * 1.25) + 16, self._cap_nodes)
+        self._cap_edges = max(int(edges * 1.25) + 64, self._cap_edges)
+        self._sub = dict(
+            node_gid=torch.empty(self._cap_nodes, dtype=torch.int32, device=dev),
+            dst_ptr=torch.empty(self._cap_nodes + 1, dtype=torch.int32, device=dev),
+            edge_src=torch.empty(self._cap_edges, dtype=torch.int32, device=dev),
+            edge_dst=torch.empty(self._cap_edges, dtype=torch.int32, device=dev),
+            edge_gid=torch.empty(self._cap_edges, dtype=torch.int64, device=dev))
+
+    def extract(self, target):
+        """gnnshap_extract_subgraph (blocks the host: returns the sizes)."""
+        if self._sub is None:
+            self._grow(1024, 8192)
+        while True:
+            b = self._sub
+            sg = L.gnnshap_subgraph(num_hops=self.hops, cap_nodes=self._cap_nodes, cap_edges=self._cap_edges,
+                                    node_gid=b["node_gid"].data_ptr(), dst_ptr=b["dst_ptr"].data_ptr(),
+                                    edge_src=b["edge_src"].data_ptr(), edge_dst=b["edge_dst"].data_ptr(),
+                                    edge_gid=b["edge_gid"].data_ptr())
+            st = L.gnnshap_extract_subgraph(self.graph, int(target), sg, _vp(self.extract_ws),
+                                            self.extract_ws.numel(), self.stream())
+            if st == L.OK:
+                break
+            self._grow(sg.num_nodes, sg.num_edges)
+        n, m, nd = sg.num_nodes, sg.num_edges, sg.num_dst
+        # the arrays stay valid until the next extract(); callers copy what they keep
+        return Subgraph(sg=sg, node_gid=b["node_gid"][:n], dst_ptr=b["dst_ptr"][:nd + 1],
+                        edge_src=b["edge_src"][:m], edge_dst=b["edge_dst"][:m], edge_gid=b["edge_gid"][:m])
+
+    def explain(self, target, num_samples, seed, target_class=-1, stream_id=None):
+        """Alg. 1 for one target: extract, plan, sample, evaluate, solve."""
+        sub = self.extract(target)
+        M = sub.sg.num_edges
+        if M < 2:
+            raise ValueError(f"target {target} has {M} players; at least 2 are needed")
+        plan, classes = L.gnnshap_plan_samples(M, int(num_samples), int(seed),
+                                               int(target if stream_id is None else stream_id))
+        return self.run(sub, plan, classes, target_class, target)
+
+    def run(self, sub, plan, classes, target_class=-1, target=-1):
+        dev, s = self.device, self.stream()
+        k, wpr, M = plan.num_rows, plan.words_per_row, plan.num_players
+        masks = torch.empty((k, wpr), dtype=torch.int64, device=dev)
+        weights = torch.empty(k, dtype=torch.float32, device=dev)
+        ws = self.ws_sample.get(L.gnnshap_sample_workspace(plan))
+        L.gnnshap_sample_coalitions(plan, classes, _vp(masks), _vp(weights), _vp(ws), ws.numel(), s)
+        y = torch.empty(k, dtype=torch.float32, device=dev)
+        fef = torch.empty(2, dtype=torch.float32, device=dev)
+        cls = torch.empty(1, dtype=torch.int32, device=dev)
+        ws = self.ws_eval.get(L.gnnshap_eval_workspace(sub.sg, self.model, k))
+        L.gnnshap_eval_coalitions(sub.sg, self.model, _vp(self.X), int(target_class), _vp(masks), k, wpr, _vp(y),
+                                  _vp(fef), _vp(cls), _vp(ws), ws.numel(), s)
+        phi = torch.empty(M, dtype=torch.float32, device=dev)
+        info = torch.empty(1, dtype=torch.int32, device=dev)
+        ws = self.ws_solve.get(L.gnnshap_solve_workspace(plan))
+        L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws), ws.numel(), s)
+        return Explanation(target=target, sub=sub, plan=plan, classes=classes, masks=masks, weights=weights, y=y,
+                           f_empty_full=fef, cls=cls, phi=phi, info=info)

@@ -1,0 +1,288 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Bars: subgraph arrays and masks bit-exact; weights equal to the fp32 rounding
+of the oracle's fp64 weights; coalition values within 1e-4 of
+max(|y|, |f(E_c)|, |f(empty)|); Shapley values within 1e-3 of max|phi|.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import gcn, sampler, subgraph, wls, shapley
+from tests.gpu_util import (explainer_for, masks_np, require_gpu, sample_on_gpu, y_tolerance)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _small_cfg(seed, n, e, dims, hops, bias="random"):
+    indptr, indices = W.random_digraph(n, e, seed=seed, symmetric=True)
+    X = W.gaussian_features(n, dims[0], seed + 7)
+    Ws, bs = W.glorot_gcn(dims, seed + 9, bias=bias)
+    return dict(indptr=indptr, indices=indices, X=X, weights=Ws, biases=bs, hops=hops)
+
+
+def _check_subgraph(got, ref):
+    assert got.sg.num_nodes == ref["num_nodes"] and got.sg.num_edges == ref["num_edges"]
+    assert got.hop_ptr == ref["hop_ptr"].tolist()
+    np.testing.assert_array_equal(got.node_gid.cpu().numpy(), ref["node_gid"])
+    np.testing.assert_array_equal(got.dst_ptr.cpu().numpy(), ref["dst_ptr"])
+    np.testing.assert_array_equal(got.edge_src.cpu().numpy(), ref["edge_src"])
+    np.testing.assert_array_equal(got.edge_dst.cpu().numpy(), ref["edge_dst"])
+    np.testing.assert_array_equal(got.edge_gid.cpu().numpy(), ref["edge_gid"])
+
+
+# -- 1. computational graph -----------------------------------------------------------
+
+@pytest.mark.parametrize("hops", [1, 2, 3])
+def test_extract_small_graphs_bit_exact(dev, hops):
+    for seed in range(3):
+        cfg = _small_cfg(seed, 60, 150, [4, 8, 3], hops)
+        ex = explainer_for(cfg)
+        for v in range(0, 60, 3):
+            _say("extract small", seed, hops, v)
+            _check_subgraph(ex.extract(v), subgraph.extract(cfg["indptr"], cfg["indices"], v, hops))
+        assert int(ex.extract_ws.count_nonzero()) == 0       # workspace left zero-filled
+
+
+@pytest.mark.parametrize("name", ["tiny", "cora", "pubmed"])
+def test_extract_workload_targets_bit_exact(dev, name):
+    cfg = W.make_config(name)
+    ex = explainer_for(cfg)
+    targets = cfg["targets"] if name != "pubmed" else cfg["targets"][:40]
+    for v in targets:
+        _say("extract", name, v)
+        got = ex.extract(v)
+        ref = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
+        _check_subgraph(got, ref)
+        lo, hi = cfg["m_range"]
+        assert lo <= ref["num_edges"] <= hi
+
+
+def test_extract_capacity_reports_sizes(dev):
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    v = cfg["targets"][0]
+    ref = subgraph.extract(cfg["indptr"], cfg["indices"], v, 2)
+    from paper_2401_04829_amd import _lib as L
+    from paper_2401_04829_amd.explainer import _vp
+    buf = torch.zeros(16, dtype=torch.int64, device=dev)
+    sg = L.gnnshap_subgraph(num_hops=2, cap_nodes=1, cap_edges=1, node_gid=buf.data_ptr(), dst_ptr=buf.data_ptr(),
+                            edge_src=buf.data_ptr(), edge_dst=buf.data_ptr(), edge_gid=buf.data_ptr())
+    st = L.gnnshap_extract_subgraph(ex.graph, v, sg, _vp(ex.extract_ws), ex.extract_ws.numel(),
+                                    torch.cuda.current_stream().cuda_stream)
+    assert st == L.ECAPACITY
+    assert sg.num_nodes == ref["num_nodes"] and sg.num_edges == ref["num_edges"]
+    assert int(buf.count_nonzero()) == 0                      # nothing written
+    assert int(ex.extract_ws.count_nonzero()) == 0
+    _check_subgraph(ex.extract(v), ref)                       # and the next call still works
+
+
+# -- 2. sampler ------------------------------------------------------------------------
+
+SAMPLER_CASES = [(2, 2), (3, 4), (5, 30), (8, 254), (12, 4094), (13, 1000), (20, 10000), (57, 2000),
+                 (60, 2000), (64, 3000), (65, 1554), (128, 5000), (400, 10000), (1000, 6668),
+                 (4000, 25000), (20000, 50000), (30000, 100000)]
+
+
+@pytest.mark.parametrize("M,p", SAMPLER_CASES)
+def test_sampler_bit_exact(dev, M, p):
+    seed, stream = 0x5EED0002 + M, 1000 + p
+    _say("sample", M, p)
+    plan, classes, masks, weights = sample_on_gpu(M, p, seed, stream)
+    pl = sampler.plan(M, p)
+    k = pl["k"]
+    got = masks_np(masks)
+    gw = weights.cpu().numpy()
+    if M <= 4000:
+        ref_m, ref_w = sampler.sample(pl, seed, stream)
+        np.testing.assert_array_equal(got, sampler.pack(ref_m))
+        np.testing.assert_array_equal(gw, ref_w.astype(np.float32))
+    else:
+        rng = np.random.default_rng(M)
+        rows = np.unique(np.concatenate([rng.integers(0, k, 48), [0, k // 2 - 1, k // 2, k - 1]]))
+        ref_m, ref_w = sampler.sample_rows(pl, rows, seed, stream)
+        np.testing.assert_array_equal(got[rows], sampler.pack(ref_m))
+        np.testing.assert_array_equal(gw[rows], ref_w.astype(np.float32))
+        # properties of every row: complement pairing, class sizes
+        half = k // 2
+        pc = np.unpackbits(got.view(np.uint8), axis=1).sum(axis=1)
+        assert (pc[:half] + pc[half:] == M).all()
+        np.testing.assert_array_equal(got[:half] & got[half:], 0)
+
+
+def test_sampler_is_deterministic_and_seeded(dev):
+    _, _, m1, _ = sample_on_gpu(300, 4000, 7, 9)
+    _, _, m2, _ = sample_on_gpu(300, 4000, 7, 9)
+    _, _, m3, _ = sample_on_gpu(300, 4000, 8, 9)
+    assert torch.equal(m1, m2)
+    assert not torch.equal(m1, m3)
+
+
+# -- 3. coalition values -----------------------------------------------------------------
+
+def _oracle_game(cfg, sub_ref, cls):
+    return gcn.Game(sub_ref, cfg["X"], cfg["weights"], cfg["biases"], cls=cls)
+
+
+def _check_eval(cfg, v, p, seed, rows=None, target_class=-1):
+    ex = explainer_for(cfg)
+    res = ex.explain(v, p, seed, target_class=target_class)
+    torch.cuda.synchronize()
+    ref_sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
+    M = ref_sub["num_edges"]
+    game = _oracle_game(cfg, ref_sub, None)
+    full_logits = game.logits(np.ones(M, bool))
+    cls = gcn.predicted_class(full_logits) if target_class < 0 else target_class
+    game.cls = cls
+    f0, f1 = game(np.zeros(M, bool)), float(full_logits[cls])
+    srt = np.sort(full_logits)[::-1]
+    if target_class < 0 and len(srt) > 1 and srt[0] - srt[1] < 1e-5 * max(1.0, abs(srt[0])):
+        pytest.skip("predicted class is a near tie")
+    assert int(res.cls.item()) == cls
+    fef = res.f_empty_full.cpu().numpy()
+    tol0 = y_tolerance(np.array([f0, f1]), f0, f1)
+    assert abs(fef[0] - f0) <= tol0[0] and abs(fef[1] - f1) <= tol0[1]
+    pl = sampler.plan(M, p)
+    k = pl["k"]
+    if rows is None:
+        rows = np.arange(k)
+    ref_m, _ = sampler.sample_rows(pl, rows, seed, v) if len(rows) < k else sampler.sample(pl, seed, v)
+    got_m = masks_np(res.masks)[rows]
+    np.testing.assert_array_equal(got_m, sampler.pack(ref_m))
+    y_ref = game.values(ref_m)
+    y_gpu = res.y.cpu().numpy()[rows].astype(np.float64)
+    err = np.abs(y_gpu - y_ref)
+    tol = y_tolerance(y_ref, f0, f1)
+    bad = np.flatnonzero(err > tol)
+    assert bad.size == 0, f"target {v}: {bad.size} rows off, worst {err.max():.3e} vs tol {tol[bad[0]]:.3e}"
+    # pruned rows hold exactly f(empty) as computed on the device
+    deg_v = ref_sub["dst_ptr"][1]
+    pruned = ~ref_m[:, :deg_v].any(axis=1)
+    assert (y_gpu[pruned] == fef[0]).all()
+    return res, game, (f0, f1, cls)
+
+
+def test_eval_tiny_all_rows(dev):
+    cfg = W.make_config("tiny")
+    _say("eval tiny")
+    _check_eval(cfg, cfg["targets"][0], cfg["p"], cfg["seed"])
+
+
+@pytest.mark.parametrize("L_hops", [(1, 1), (1, 2), (2, 1), (2, 2), (2, 3), (3, 1), (3, 2), (3, 3)])
+def test_eval_small_graphs_layers_and_hops(dev, L_hops):
+    nl, hops = L_hops
+    dims = [6, 16, 8, 5][:nl] + [4]
+    for seed in range(2):
+        cfg = _small_cfg(10 + seed, 50, 140, dims, hops)
+        for v in range(0, 50, 7):
+            M = subgraph.extract(cfg["indptr"], cfg["indices"], v, hops)["num_edges"]
+            if M < 2:
+                continue
+            _say("eval small", nl, hops, seed, v, M)
+            _check_eval(cfg, v, 600, 99)
+
+
+def test_eval_fixed_class_and_wide_layers(dev):
+    cfg = _small_cfg(31, 80, 400, [20, 130, 70, 9], 2)
+    for v in (1, 5):
+        _say("eval wide", v)
+        _check_eval(cfg, v, 800, 3, target_class=4)
+
+
+def test_eval_cora_all_targets_sampled_rows(dev):
+    cfg = W.make_config("cora")
+    rng = np.random.default_rng(0)
+    for v in cfg["targets"]:
+        _say("eval cora", v)
+        k = sampler.plan(subgraph.extract(cfg["indptr"], cfg["indices"], v, 2)["num_edges"], cfg["p"])["k"]
+        rows = np.unique(np.concatenate([rng.integers(0, k, 40), [0, k - 1]]))
+        _check_eval(cfg, v, cfg["p"], cfg["seed"], rows=rows)
+
+
+def test_eval_pubmed_sampled_rows(dev):
+    cfg = W.make_config("pubmed")
+    rng = np.random.default_rng(1)
+    for v in cfg["targets"][:6]:
+        _say("eval pubmed", v)
+        k = sampler.plan(subgraph.extract(cfg["indptr"], cfg["indices"], v, 3)["num_edges"], cfg["p"])["k"]
+        rows = np.unique(np.concatenate([rng.integers(0, k, 16), [0, k - 1]]))
+        _check_eval(cfg, v, cfg["p"], cfg["seed"], rows=rows)
+
+
+# -- 4. least squares ---------------------------------------------------------------------
+
+def _phi_close(phi_gpu, phi_ref, rel=1e-3):
+    scale = np.abs(phi_ref).max()
+    err = np.abs(phi_gpu - phi_ref).max()
+    assert err <= rel * scale, f"max |phi err| {err:.3e} > {rel:.0e} * {scale:.3e}"
+
+
+def test_solve_end_to_end_tiny_and_cora(dev):
+    for name, targets in (("tiny", None), ("cora", 6)):
+        cfg = W.make_config(name)
+        for v in (cfg["targets"] if targets is None else cfg["targets"][:targets]):
+            _say("solve", name, v)
+            res, game, (f0, f1, cls) = _check_eval(cfg, v, cfg["p"], cfg["seed"])
+            assert int(res.info.item()) == 0
+            pl = sampler.plan(res.plan.num_players, cfg["p"])
+            m, w = sampler.sample(pl, cfg["seed"], v)
+            phi_ref = wls.kernel_shap(m, w, game.values(m), f0, f1)
+            phi = res.phi.cpu().numpy().astype(np.float64)
+            _phi_close(phi, phi_ref)
+            assert abs(phi.sum() - float(res.f_empty_full[1] - res.f_empty_full[0])) < 1e-4 * max(1.0, abs(f1 - f0))
+
+
+@pytest.mark.parametrize("M", [2, 3, 5, 8, 10])
+def test_solve_exhaustive_equals_exact_shapley(dev, M):
+    """Every coalition enumerated: Kernel SHAP = eq. 1 (checked on a synthetic game)."""
+    from paper_2401_04829_amd import _lib as L
+    from paper_2401_04829_amd.explainer import _vp
+    rng = np.random.default_rng(M)
+    table = rng.normal(size=1 << M)
+    vals = table.copy()
+    exact = shapley.exact_shapley(vals, M)
+    p = 2 ** M - 2
+    plan, classes, masks, _ = sample_on_gpu(M, p, 1, 2)
+    mb = sampler.unpack(masks_np(masks), M)
+    codes = (mb * (1 << np.arange(M))).sum(axis=1)
+    y = torch.tensor(vals[codes], dtype=torch.float32, device=dev)
+    fef = torch.tensor([vals[0], vals[-1]], dtype=torch.float32, device=dev)
+    phi = torch.empty(M, dtype=torch.float32, device=dev)
+    info = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(L.gnnshap_solve_workspace(plan), dtype=torch.uint8, device=dev)
+    L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws), ws.numel(),
+                        torch.cuda.current_stream().cuda_stream)
+    assert int(info.item()) == 0
+    _phi_close(phi.cpu().numpy().astype(np.float64), exact, rel=1e-4)
+
+
+@pytest.mark.parametrize("M,p", [(20, 10000), (60, 2000), (400, 10000), (1000, 6668), (4000, 25000)])
+def test_solve_recovers_additive_game(dev, M, p):
+    """y = f0 + m.a has phi = a exactly for any determined sample set."""
+    from paper_2401_04829_amd import _lib as L
+    from paper_2401_04829_amd.explainer import _vp
+    _say("additive", M, p)
+    plan, classes, masks, _ = sample_on_gpu(M, p, 5, 6)
+    rng = np.random.default_rng(M)
+    a = rng.normal(size=M)
+    f0 = 0.25
+    mb = torch.tensor(sampler.unpack(masks_np(masks), M), dtype=torch.float64, device=dev)
+    y = (f0 + mb @ torch.tensor(a, device=dev)).float()
+    fef = torch.tensor([f0, f0 + a.sum()], dtype=torch.float32, device=dev)
+    phi = torch.empty(M, dtype=torch.float32, device=dev)
+    info = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(L.gnnshap_solve_workspace(plan), dtype=torch.uint8, device=dev)
+    L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws), ws.numel(),
+                        torch.cuda.current_stream().cuda_stream)
+    assert int(info.item()) == 0
+    _phi_close(phi.cpu().numpy().astype(np.float64), a)

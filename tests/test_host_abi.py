@@ -1,0 +1,97 @@
+"""CPU tests of the C-ABI library: it loads, exports every declared symbol,
+and its host-only logic (the sample plan, argument checks, workspace
+queries) agrees with the oracle.  No device work is launched."""
+import ctypes
+import math
+
+import numpy as np
+import pytest
+
+from oracle import sampler
+from paper_2401_04829_amd import _lib as L
+
+
+def test_library_exports_every_declared_function():
+    lib = L.load()
+    names = L.header_functions()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(L._SIGNATURES) == set(names)
+    assert lib.gnnshap_version() >= 100
+    for st in range(6):
+        assert lib.gnnshap_status_str(st)
+
+
+@pytest.mark.parametrize("M,p", [(2, 2), (3, 4), (5, 30), (8, 254), (12, 4094), (13, 8190), (17, 2000),
+                                 (20, 10000), (33, 5000), (57, 2000), (60, 2000), (64, 3000), (65, 777 * 2),
+                                 (400, 10000), (1000, 3334 * 2), (4000, 25000), (12345, 50000), (30000, 100000)])
+def test_plan_matches_oracle_bit_for_bit(M, p):
+    plan, classes = L.gnnshap_plan_samples(M, p, 1, 2)
+    ref = sampler.plan(M, p)
+    assert plan.num_rows == ref["k"]
+    assert plan.words_per_row == math.ceil(M / 64)
+    assert plan.random_begin == ref["random_begin"]
+    assert plan.num_classes == len(ref["classes"])
+    assert plan.full_fraction == ref["full_fraction"]          # exact fp64 equality
+    assert plan.random_weight == ref["random_weight"]
+    for got, want in zip(classes, ref["classes"]):
+        assert got.size == want["c"]
+        assert bool(got.full) == want["full"]
+        assert got.row_begin == want["row_begin"]
+        assert got.row_count == want["row_count"]
+        assert got.weight == want["weight"]
+
+
+def test_plan_errors_and_size_query():
+    lib = L.load()
+    plan = L.gnnshap_sample_plan(num_players=1, num_samples=10)
+    assert lib.gnnshap_plan_samples(ctypes.byref(plan), None, 0) == L.EINVAL
+    plan = L.gnnshap_sample_plan(num_players=10, num_samples=11)
+    assert lib.gnnshap_plan_samples(ctypes.byref(plan), None, 0) == L.EINVAL
+    plan = L.gnnshap_sample_plan(num_players=10, num_samples=0)
+    assert lib.gnnshap_plan_samples(ctypes.byref(plan), None, 0) == L.EINVAL
+    assert lib.gnnshap_plan_samples(None, None, 0) == L.EINVAL
+    plan = L.gnnshap_sample_plan(num_players=400, num_samples=10000)
+    assert lib.gnnshap_plan_samples(ctypes.byref(plan), None, 0) == L.ECAPACITY
+    assert plan.num_classes > 0 and plan.num_rows == 10000
+    assert "class table" in lib.gnnshap_last_error().decode()
+
+
+def test_workspace_queries_and_argument_checks():
+    lib = L.load()
+    n = ctypes.c_size_t()
+    assert lib.gnnshap_extract_workspace(2708, ctypes.byref(n)) == L.OK and n.value >= 5 * 4 * 2708
+    assert lib.gnnshap_extract_workspace(0, ctypes.byref(n)) == L.EINVAL
+    plan, classes = L.gnnshap_plan_samples(400, 10000, 1, 2)
+    assert L.gnnshap_sample_workspace(plan) >= plan.num_classes * 32
+    need = L.gnnshap_solve_workspace(plan)
+    assert need >= 400 * 400 * 4
+    bad = L.gnnshap_sample_plan(num_players=400, num_samples=10000)    # not planned
+    assert lib.gnnshap_sample_workspace(ctypes.byref(bad), ctypes.byref(n)) == L.EINVAL
+    assert lib.gnnshap_solve_workspace(ctypes.byref(bad), ctypes.byref(n)) == L.EINVAL
+    # eval: a consistent 2-hop subgraph description and a 2-layer model
+    sg = L.gnnshap_subgraph(num_hops=2, num_nodes=10, num_edges=12, num_dst=4)
+    for i, v in enumerate([0, 1, 4, 10, 10, 10, 10, 10, 10, 10]):
+        sg.hop_ptr[i] = v
+    dims = (ctypes.c_int32 * 3)(8, 16, 3)
+    W = (ctypes.c_void_p * 2)(1, 1)
+    model = L.gnnshap_gcn(num_layers=2, dims=dims, W=W, b=None)
+    assert L.gnnshap_eval_workspace(sg, model, 100) > 0
+    assert lib.gnnshap_eval_workspace(ctypes.byref(sg), ctypes.byref(model), 0, ctypes.byref(n)) == L.EINVAL
+    sg.hop_ptr[2] = 5                                                   # inconsistent with num_dst
+    assert lib.gnnshap_eval_workspace(ctypes.byref(sg), ctypes.byref(model), 100, ctypes.byref(n)) == L.EINVAL
+    sg.hop_ptr[2] = 4
+    # invalid arguments are rejected before any device work
+    assert lib.gnnshap_eval_coalitions(ctypes.byref(sg), ctypes.byref(model), None, 0, None, 10, 1, None, None,
+                                       None, None, 0, None) == L.EINVAL
+    assert lib.gnnshap_sample_coalitions(ctypes.byref(plan), classes, None, None, None, 0, None) == L.EINVAL
+    assert lib.gnnshap_solve_wls(ctypes.byref(plan), classes, None, None, None, None, None, None, 0,
+                                 None) == L.EINVAL
+    g = L.gnnshap_graph(num_nodes=10, num_edges=0, indptr=1, indices=1)
+    sub = L.gnnshap_subgraph(num_hops=2)
+    assert lib.gnnshap_extract_subgraph(ctypes.byref(g), 10, ctypes.byref(sub), 1, 10 ** 6, None) == L.EINVAL
+    sub.num_hops = 9
+    assert lib.gnnshap_extract_subgraph(ctypes.byref(g), 0, ctypes.byref(sub), 1, 10 ** 6, None) == L.EINVAL
+    sub.num_hops = 2
+    assert lib.gnnshap_extract_subgraph(ctypes.byref(g), 0, ctypes.byref(sub), 1, 16, None) == L.ECAPACITY
