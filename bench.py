@@ -73,6 +73,7 @@ def main():
     def step():
         ks = 0
         last = None
+        ex.prepare()                 # X W_1 once per step, shared by every target
         for v in targets:
             r = ex.explain(v, cfg["p"], cfg["seed"])
             ks += r.plan.num_rows

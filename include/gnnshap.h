@@ -187,7 +187,17 @@ typedef struct {
                                     dims[L] = number of classes C */
   const float* const* W;         /* [host] L [dev] pointers; W_l is dims[l] x dims[l+1] */
   const float* const* b;         /* [host] L [dev] pointers, or NULL entries / NULL = zero bias */
+  const float* XW1;              /* [dev] optional num_nodes x dims[1]: X W_1 for every node of the
+                                    graph (gnnshap_transform_features); NULL = computed from X */
 } gnnshap_gcn;
+
+/* Z = X W for every node (fp32; X [dev] n x d, W [dev] d x h, Z [dev] n x h, row-major).
+ * The first GCN layer transforms each node's features independently of the
+ * coalition (Sec. 3.4.2: the coalitions of a batch share the node features),
+ * so X W_1 is computed once per graph and model and passed as
+ * gnnshap_gcn.XW1; each explanation then gathers the rows of its subgraph. */
+int gnnshap_transform_features(const float* X, int64_t n, int32_t d, const float* W, int32_t h,
+                               float* Z, void* stream);
 
 /* Bytes of device workspace for evaluating k coalitions of subgraph sg. */
 int gnnshap_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_gcn* m,

@@ -41,7 +41,7 @@ class gnnshap_sample_plan(ctypes.Structure):
 
 class gnnshap_gcn(ctypes.Structure):
     _fields_ = [("num_layers", c_i32), ("reserved", c_i32), ("dims", ctypes.POINTER(c_i32)),
-                ("W", ctypes.POINTER(c_vp)), ("b", ctypes.POINTER(c_vp))]
+                ("W", ctypes.POINTER(c_vp)), ("b", ctypes.POINTER(c_vp)), ("XW1", c_vp)]
 
 
 _P = ctypes.POINTER
@@ -60,6 +60,7 @@ _SIGNATURES = {
                                               _P(ctypes.c_size_t)]),
     "gnnshap_eval_coalitions": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp,
                                                c_i64, c_i64, c_vp, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_transform_features": (ctypes.c_int, [c_vp, c_i64, c_i32, c_vp, c_i32, c_vp, c_vp]),
     "gnnshap_solve_workspace": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(ctypes.c_size_t)]),
     "gnnshap_solve_wls": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(gnnshap_class), c_vp, c_vp, c_vp, c_vp,
                                          c_vp, c_vp, ctypes.c_size_t, c_vp]),
@@ -151,6 +152,10 @@ def gnnshap_eval_coalitions(sg, model, X_ptr, target_class, masks_ptr, k, wpr, y
                             ws_bytes, stream):
     check(load().gnnshap_eval_coalitions(ctypes.byref(sg), ctypes.byref(model), X_ptr, target_class, masks_ptr, k,
                                          wpr, y_ptr, fef_ptr, cls_ptr, ws_ptr, ws_bytes, stream), "eval_coalitions")
+
+
+def gnnshap_transform_features(X_ptr, n, d, W_ptr, h, Z_ptr, stream):
+    check(load().gnnshap_transform_features(X_ptr, n, d, W_ptr, h, Z_ptr, stream), "transform_features")
 
 
 def gnnshap_solve_workspace(plan):

@@ -40,6 +40,15 @@ inline unsigned grid_for(int64_t items, int block, int64_t cap = 8192) {
   return static_cast<unsigned>(g);
 }
 
+// Largest dynamic LDS allocation one workgroup may request on the current device.
+inline int max_lds_bytes() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 65536;
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0) v = 65536;
+  return v;
+}
+
 }  // namespace gnnshap
 
 #define GS_HIP(call)                                                                     \

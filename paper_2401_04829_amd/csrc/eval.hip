@@ -134,7 +134,9 @@ __global__ void k_init(int32_t* ctl, uint64_t* sp_masks, int32_t* sp_rows, int64
 }
 
 // C[m, :] = op(A[row(m), :]) B for m in [m0, m0 + rows), 64x64 tiles, fp32.
-// row(m) = arow ? arow[m] : m; op(a) = relu(a + abias) if abias else a.
+// row(m) = arow ? arow[m] : m; op(a) = relu(a + abias) if abias else a.  The
+// next 16-wide K slice is fetched into registers while the current one is
+// multiplied.
 __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64_t lda,
                                               const int32_t* __restrict__ arow,
                                               const float* __restrict__ abias,
@@ -154,33 +156,48 @@ __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64
   const int64_t nb = static_cast<int64_t>(blockIdx.y) * 64;
   const int tid = threadIdx.x;
   const int ty = tid / 16, tx = tid % 16;
+  const int kk = tid % 16, kb0 = tid / 64, nn = tid % 64;
+  const float* arp[4];
+  bool aok[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = mb + tid / 16 + 16 * i;
+    aok[i] = m < m0 + rows;
+    const int64_t ar = aok[i] ? (arow ? static_cast<int64_t>(arow[m]) : m) : 0;
+    arp[i] = A + ar * lda;
+  }
+  const bool nok = nb + nn < N;
+  float ra[4], rb[4];
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float a = 0.f;
+      if (aok[i] && k0 + kk < K) {
+        a = arp[i][k0 + kk];
+        if (abias) a = fmaxf(a + abias[k0 + kk], 0.f);
+      }
+      ra[i] = a;
+      const int64_t kr = k0 + kb0 + 4 * i;
+      rb[i] = (kr < K && nok) ? B[kr * ldb + nb + nn] : 0.f;
+    }
+  };
   float acc[4][4] = {};
+  fetch(0);
   for (int64_t k0 = 0; k0 < K; k0 += 16) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int idx = tid + i * 256;
-      const int r = idx / 16, kk = idx % 16;
-      const int64_t m = mb + r;
-      float a = 0.f;
-      if (m < m0 + rows && k0 + kk < K) {
-        const int64_t ar = arow ? static_cast<int64_t>(arow[m]) : m;
-        a = A[ar * lda + k0 + kk];
-        if (abias) a = fmaxf(a + abias[k0 + kk], 0.f);
-      }
-      As[kk][r] = a;
-      const int kb = idx / 64, nn = idx % 64;
-      float b = 0.f;
-      if (k0 + kb < K && nb + nn < N) b = B[(k0 + kb) * ldb + nb + nn];
-      Bs[kb][nn] = b;
+      As[kk][tid / 16 + 16 * i] = ra[i];
+      Bs[kb0 + 4 * i][nn] = rb[i];
     }
     __syncthreads();
+    if (k0 + 16 < K) fetch(k0 + 16);
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
+    for (int q = 0; q < 16; ++q) {
       float a[4], b[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        a[i] = As[kk][ty * 4 + i];
-        b[i] = Bs[kk][tx * 4 + i];
+        a[i] = As[q][ty * 4 + i];
+        b[i] = Bs[q][tx * 4 + i];
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -198,6 +215,17 @@ __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64
       const int64_t n = nb + tx * 4 + jn;
       if (n < N) C[m * ldc + n] = acc[i][jn];
     }
+  }
+}
+
+// Zc[u, :] = XW1[node_gid[u], :]
+__global__ void k_gather_rows(const float* __restrict__ src, const int32_t* __restrict__ idx, int64_t n, int h,
+                              float* __restrict__ dst) {
+  const int64_t total = n * h;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t u = t / h, f = t % h;
+    dst[t] = src[static_cast<int64_t>(idx[u]) * h + f];
   }
 }
 
@@ -376,6 +404,140 @@ __global__ void __launch_bounds__(256) k_final(
   }
 }
 
+// Two-layer GCN with hops >= 2, one launch per pass: a block takes `tbr` <=
+// kTB coalitions and runs, in LDS,
+//   degrees  dinv[b, x] for every destination x;
+//   layer 1  at every x in H_1: masked aggregation of Z^1 = X W_1 rows
+//            (staged 64 players at a time), ReLU, then t[b, x, c] =
+//            H^1[b, x] . W_2[:, c] for the explained class (or every class);
+//   layer 2  y = d_v^-1/2 (sum_{(u->v) in S} d_u^-1/2 t[u] + d_v^-1/2 t[v]) + b_2.
+template <int FPT>
+__global__ void __launch_bounds__(256) k_eval_l2(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t row_off,
+    int64_t cap, const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr,
+    const int32_t* __restrict__ edge_src, int64_t n_dst, int64_t n1, const float* __restrict__ Zc,
+    const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
+    const int32_t* __restrict__ ctl, bool all_classes, int tbr, float* __restrict__ y_rows,
+    float* __restrict__ y_all) {
+  constexpr int FS = 8 * FPT;
+  extern __shared__ __align__(16) float sm[];
+  const int ncls = all_classes ? C : 1;
+  float* dinv = sm;                                   // tbr x n_dst
+  float* tt = dinv + tbr * n_dst;                     // tbr x n1 x ncls
+  float* zs = tt + tbr * n1 * ncls;                   // 64 x FS
+  int32_t* ss = reinterpret_cast<int32_t*>(zs + kChunkE * FS);
+  const int64_t nr = rows_in_pass(dyn_count, row_off, cap);
+  const int64_t b_base = static_cast<int64_t>(blockIdx.x) * tbr;
+  if (b_base >= nr) return;
+  const int tid = threadIdx.x;
+  const int tb = tid >> 3, fg = tid & 7;
+  const int64_t b = b_base + tb;
+  const bool valid = tb < tbr && b < nr;
+  const uint64_t* mrow = valid ? masks + static_cast<int64_t>(rows[row_off + b]) * wpr : masks;
+  const int c0 = all_classes ? 0 : ctl[0];
+
+  // degrees
+  for (int64_t t = tid; t < static_cast<int64_t>(tbr) * n_dst; t += 256) {
+    const int64_t bb = t / n_dst, x = t % n_dst;
+    float d = 1.0f;
+    if (b_base + bb < nr) {
+      const uint64_t* mr = masks + static_cast<int64_t>(rows[row_off + b_base + bb]) * wpr;
+      const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+      int cnt = 0;
+      for (int64_t w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+        uint64_t word = mr[w];
+        const int64_t lo = w * 64;
+        if (e0 > lo) word &= ~uint64_t(0) << (e0 - lo);
+        if (e1 < lo + 64) word &= (uint64_t(1) << (e1 - lo)) - 1;
+        cnt += __popcll(word);
+      }
+      d = rsqrtf(1.0f + static_cast<float>(cnt));
+    }
+    dinv[t] = d;
+  }
+  for (int64_t t = tid; t < static_cast<int64_t>(tbr) * n1 * ncls; t += 256) tt[t] = 0.f;
+  __syncthreads();
+  const float* drow = dinv + (valid ? tb : 0) * n_dst;
+
+  // layer 1 at every node of H_1, folded into the class logits
+  for (int64_t x = 0; x < n1; ++x) {
+    const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+    const float dx = drow[x];
+    for (int fs0 = 0; fs0 < h; fs0 += FS) {
+      const int f0 = fs0 + fg * FPT;
+      float acc[FPT];
+#pragma unroll
+      for (int i = 0; i < FPT; ++i) acc[i] = 0.f;
+      for (int64_t ec = e0; ec < e1; ec += kChunkE) {
+        const int n = static_cast<int>(e1 - ec < kChunkE ? e1 - ec : kChunkE);
+        __syncthreads();
+        if (tid < n) ss[tid] = edge_src[ec + tid];
+        __syncthreads();
+        for (int idx = tid; idx < n * FS; idx += 256) {
+          const int e = idx / FS, f = idx % FS;
+          zs[idx] = fs0 + f < h ? Zc[static_cast<int64_t>(ss[e]) * h + fs0 + f] : 0.f;
+        }
+        uint64_t bits = 0;
+        if (valid) {
+          const int64_t w0 = ec >> 6;
+          const int sh = static_cast<int>(ec & 63);
+          bits = mrow[w0] >> sh;
+          if (sh && w0 + 1 < wpr) bits |= mrow[w0 + 1] << (64 - sh);
+          if (n < 64) bits &= (uint64_t(1) << n) - 1;
+        }
+        __syncthreads();
+        while (bits) {
+          const int e = __ffsll(static_cast<long long>(bits)) - 1;
+          bits &= bits - 1;
+          const int32_t u = ss[e];
+          const float coef = u < n_dst ? drow[u] : 1.0f;
+#pragma unroll
+          for (int i = 0; i < FPT; ++i) acc[i] += coef * zs[e * FS + fg * FPT + i];
+        }
+      }
+      float hv[FPT];
+#pragma unroll
+      for (int i = 0; i < FPT; ++i) {
+        const int f = f0 + i;
+        hv[i] = f < h ? fmaxf(dx * (acc[i] + dx * Zc[x * h + f]) + (b1 ? b1[f] : 0.f), 0.f) : 0.f;
+      }
+      for (int ci = 0; ci < ncls; ++ci) {
+        float p = 0.f;
+#pragma unroll
+        for (int i = 0; i < FPT; ++i)
+          if (f0 + i < h) p += hv[i] * W2[static_cast<int64_t>(f0 + i) * C + c0 + ci];
+        p += __shfl_xor(p, 1);
+        p += __shfl_xor(p, 2);
+        p += __shfl_xor(p, 4);
+        if (valid && fg == 0) tt[(tb * n1 + x) * ncls + ci] += p;
+      }
+    }
+  }
+  __syncthreads();
+
+  // layer 2 at the target
+  const int64_t indeg = dst_ptr[1];
+  for (int t = tid; t < tbr * ncls; t += 256) {
+    const int bb = t / ncls, ci = t % ncls;
+    const int64_t bg = b_base + bb;
+    if (bg >= nr) continue;
+    const int64_t row = rows[row_off + bg];
+    const uint64_t* mr = masks + row * wpr;
+    const float* dr = dinv + bb * n_dst;
+    const float dv = dr[0];
+    float acc = 0.f;
+    for (int64_t e = 0; e < indeg; ++e) {
+      if (!((mr[e >> 6] >> (e & 63)) & 1)) continue;
+      const int32_t u = edge_src[e];
+      acc += dr[u] * tt[(bb * n1 + u) * ncls + ci];
+    }
+    acc += dv * tt[(bb * n1) * ncls + ci];
+    const float yv = dv * acc + (b2 ? b2[c0 + ci] : 0.f);
+    if (all_classes) y_all[bg * C + ci] = yv;
+    else y_rows[row] = yv;
+  }
+}
+
 __global__ void k_pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
                              int32_t* class_out, float* f_empty_full) {
   int c = requested;
@@ -473,9 +635,56 @@ int launch_aggregate(hipStream_t s, int h, const uint64_t* masks, int64_t wpr, c
 }
 
 // Runs degrees -> layers 1..L-1 -> final for `cap` rows (or a device count).
+size_t fused_lds_bytes(const Shape& sh, int64_t tbr, int ncls, int fs) {
+  return sizeof(float) * (static_cast<size_t>(tbr) * sh.n_dst + static_cast<size_t>(tbr) * sh.nd[1] * ncls +
+                          static_cast<size_t>(kChunkE) * fs) + sizeof(int32_t) * kChunkE;
+}
+
+int feature_split(int h) {
+  int fpt = 16;
+  while (fpt > 1 && 8 * (fpt / 2) >= h) fpt /= 2;
+  return fpt;
+}
+
+// The fused two-layer kernel applies when its LDS fits; returns false otherwise.
+bool fused_l2_ok(const Shape& sh, int64_t cap, bool all_classes) {
+  if (sh.L != 2 || sh.hops < 2) return false;
+  const int64_t tbr = cap < kTB ? cap : kTB;
+  const int fs = 8 * feature_split(sh.dims[1]);
+  return fused_lds_bytes(sh, tbr, all_classes ? sh.dims[2] : 1, fs) <= 65536;
+}
+
+int launch_fused_l2(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn* m, const Shape& sh, const Ws& w,
+                    const uint64_t* masks, const int32_t* rows, int64_t row_off, int64_t cap, const int32_t* dyn,
+                    bool all_classes, float* y_rows) {
+  const int tbr = static_cast<int>(cap < kTB ? cap : kTB);
+  const int h = sh.dims[1], C = sh.dims[2];
+  const int fpt = feature_split(h);
+  const size_t lds = fused_lds_bytes(sh, tbr, all_classes ? C : 1, 8 * fpt);
+  const unsigned g = static_cast<unsigned>(gnnshap::ceil_div(cap, tbr));
+  const float* b1 = m->b ? m->b[0] : nullptr;
+  const float* b2 = m->b ? m->b[1] : nullptr;
+#define GS_L2(F)                                                                                          \
+  k_eval_l2<F><<<g, 256, lds, s>>>(masks, sh.wpr, rows, row_off, cap, dyn, sg->dst_ptr, sg->edge_src,      \
+                                   sh.n_dst, sh.nd[1], w.Zc[1], b1, m->W[1], b2, h, C, w.ctl, all_classes, \
+                                   tbr, y_rows, w.sp_y)
+  switch (fpt) {
+    case 1: GS_L2(1); break;
+    case 2: GS_L2(2); break;
+    case 4: GS_L2(4); break;
+    case 8: GS_L2(8); break;
+    default: GS_L2(16); break;
+  }
+#undef GS_L2
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
 int run_pass(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn* m, const Shape& sh,
              const Ws& w, const uint64_t* masks, const int32_t* rows, int64_t row_off, int64_t cap,
              const int32_t* dyn, bool all_classes, float* y_rows) {
+  if (fused_l2_ok(sh, cap, all_classes))
+    return launch_fused_l2(s, sg, m, sh, w, masks, rows, row_off, cap, dyn, all_classes, y_rows);
   const int L = sh.L;
   k_degrees<<<gnnshap::grid_for(cap * sh.n_dst, 256), 256, 0, s>>>(masks, sh.wpr, rows, row_off, cap,
                                                                     dyn, sg->dst_ptr, sh.n_dst, w.dinv);
@@ -529,7 +738,8 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   if (k < 1) return gnnshap::fail(GNNSHAP_EINVAL, "k must be >= 1");
   Shape sh;
   if (int st = make_shape(sg, m, k, &sh)) return st;
-  if (!X || !masks || !y || !f_empty_full || !ws || !m->W) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  if ((!X && !m->XW1) || !masks || !y || !f_empty_full || !ws || !m->W)
+    return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
   for (int l = 0; l < sh.L; ++l)
     if (!m->W[l]) return gnnshap::fail(GNNSHAP_EINVAL, "null weight matrix %d", l);
   if (!sg->node_gid || !sg->dst_ptr || !sg->edge_src) return gnnshap::fail(GNNSHAP_EINVAL, "null subgraph arrays");
@@ -546,10 +756,15 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
 
   k_init<<<gnnshap::grid_for(sh.wpr, 256, 64), 256, 0, s>>>(w.ctl, w.sp_masks, w.sp_rows, sh.wpr, sg->num_edges);
   GS_LAUNCHED();
-  // Constant rows: Z^1 = X[V_c] W_1, then the boundary chain.
-  if (int st = launch_gemm(s, X, sh.dims[0], sg->node_gid, nullptr, m->W[0], sh.dims[1], w.Zc[1], sh.dims[1], 0,
-                           sh.n_nodes, sh.dims[1], sh.dims[0]))
+  // Constant rows: Z^1 = X[V_c] W_1 (gathered from X W_1 when given), then the boundary chain.
+  if (m->XW1) {
+    k_gather_rows<<<gnnshap::grid_for(sh.n_nodes * sh.dims[1], 256, 2048), 256, 0, s>>>(m->XW1, sg->node_gid,
+                                                                                        sh.n_nodes, sh.dims[1], w.Zc[1]);
+    GS_LAUNCHED();
+  } else if (int st = launch_gemm(s, X, sh.dims[0], sg->node_gid, nullptr, m->W[0], sh.dims[1], w.Zc[1], sh.dims[1],
+                                  0, sh.n_nodes, sh.dims[1], sh.dims[0])) {
     return st;
+  }
   for (int j = 1; j < L; ++j) {
     if (!sh.bnd[j]) continue;
     k_bias_relu<<<gnnshap::grid_for((sh.bnd1 - sh.bnd0) * sh.dims[j], 256, 1024), 256, 0, s>>>(
@@ -576,5 +791,17 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   k_fill_pruned<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(w.live_flag, k, f_empty_full, y);
   GS_LAUNCHED();
   return GNNSHAP_OK;
+  GS_TRY_END
+}
+
+extern "C" int gnnshap_transform_features(const float* X, int64_t n, int32_t d, const float* W, int32_t h, float* Z,
+                                          void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (!X || !W || !Z) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  if (n < 1 || d < 1 || h < 1) return gnnshap::fail(GNNSHAP_EINVAL, "bad sizes");
+  if (gnnshap::ceil_div(n, 64) > INT32_MAX || gnnshap::ceil_div(h, 64) > 65535)
+    return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "matrix too large");
+  return launch_gemm(static_cast<hipStream_t>(stream), X, d, nullptr, nullptr, W, h, Z, h, 0, n, h, d);
   GS_TRY_END
 }

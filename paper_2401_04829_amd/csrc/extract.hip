@@ -213,11 +213,20 @@ __global__ void __launch_bounds__(256) k_fill_edges(const int64_t* __restrict__ 
   }
 }
 
-__global__ void __launch_bounds__(256) k_cleanup(int32_t* mark, const int32_t* __restrict__ queue,
-                                                 int64_t count) {
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    mark[queue[i]] = 0;
+// Restores the zero state of everything a call touched.
+__global__ void __launch_bounds__(256) k_cleanup(Ws w, int64_t count, int64_t n_dst, int64_t nbc) {
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t step = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t i = t0; i < count; i += step) {
+    const int32_t g = w.queue[i];
+    w.mark[g] = 0;
+    w.local_of[g] = 0;
+    w.queue[i] = 0;
+    w.sorted[i] = 0;
+  }
+  for (int64_t i = t0; i <= n_dst; i += step) w.dstptr[i] = 0;
+  for (int64_t i = t0; i < nbc; i += step) w.bcount[i] = 0;
+  for (int64_t i = t0; i < kCounters; i += step) w.counters[i] = 0;
 }
 
 }  // namespace
@@ -304,7 +313,8 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
       GS_LAUNCHED();
     }
   }
-  k_cleanup<<<gnnshap::grid_for(nodes, 256, 1024), 256, 0, s>>>(w.mark, w.queue, nodes);
+  k_cleanup<<<gnnshap::grid_for(std::max(nodes, nblk * kLevels), 256, 1024), 256, 0, s>>>(w, nodes, n_dst,
+                                                                                         nblk * kLevels);
   GS_LAUNCHED();
   return status;
   GS_TRY_END

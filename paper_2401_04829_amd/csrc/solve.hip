@@ -32,7 +32,6 @@ struct Ws {
   int64_t* usum;     // M: row sums of the counts
   double* scal;      // [0] trace, [1] sigma, [2] gamma, [3] delta, [4] f0
   double* part;      // nch x M partial right-hand sides
-  double* dz;        // half
   float* rhs;        // M
   float* x;          // M
 };
@@ -56,7 +55,6 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   w.usum = c.take<int64_t>(M);
   w.scal = c.take<double>(16);
   w.part = c.take<double>(n_chunks(half) * M);
-  w.dz = c.take<double>(half);
   w.rhs = c.take<float>(M);
   w.x = c.take<float>(M);
   return w;
@@ -198,44 +196,40 @@ __global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restri
   }
 }
 
-// dz[b] = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|), for b < half.
-__global__ void __launch_bounds__(256) k_dz(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
-                                            int64_t M, const float* __restrict__ y,
-                                            const gnnshap_class* __restrict__ cls, int64_t ncls,
-                                            const double* __restrict__ scal, double* __restrict__ dz) {
-  const double Md = static_cast<double>(M);
-  const double delta = scal[3], f0 = scal[4];
-  for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < half;
-       b += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-    int64_t lo = 0, hi = ncls - 1;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (cls[mid].row_begin <= b) lo = mid; else hi = mid - 1;
-    }
-    const double w = cls[lo].weight;
-    int64_t pc = 0;
-    for (int64_t q = 0; q < wpr; ++q) pc += __popcll(masks[b * wpr + q]);
-    const double z1 = w * (static_cast<double>(y[b]) - f0 - delta / Md * static_cast<double>(pc));
-    const double z2 = w * (static_cast<double>(y[b + half]) - f0 - delta / Md * static_cast<double>(M - pc));
-    dz[b] = z1 - z2;
-  }
-}
-
-// Partial right-hand sides: part[ch, j] = sum_{b in chunk ch} dz[b] m_bj.
+// Partial right-hand sides: part[ch, j] = sum_{b in chunk ch} dz_b m_bj with
+// dz_b = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|), b < half.
 __global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ masks, int64_t wpr,
-                                                  int64_t half, int64_t M, const double* __restrict__ dz,
-                                                  int64_t rows_per_chunk, double* __restrict__ part) {
+                                                  int64_t half, int64_t M, const float* __restrict__ y,
+                                                  const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                                  const float* __restrict__ fef, int64_t rows_per_chunk,
+                                                  double* __restrict__ part) {
   __shared__ double dzs[256];
   const int tid = threadIdx.x;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per_chunk;
   const int64_t r1 = r0 + rows_per_chunk < half ? r0 + rows_per_chunk : half;
+  const double Md = static_cast<double>(M);
+  const double f0 = static_cast<double>(fef[0]);
+  const double delta = static_cast<double>(fef[1]) - f0;
   for (int64_t j0 = 0; j0 < M; j0 += 256) {
     const int64_t j = j0 + tid;
     double acc = 0.0;
     for (int64_t b0 = r0; b0 < r1; b0 += 256) {
       const int nb = static_cast<int>(r1 - b0 < 256 ? r1 - b0 : 256);
       __syncthreads();
-      if (tid < nb) dzs[tid] = dz[b0 + tid];
+      if (tid < nb) {
+        const int64_t b = b0 + tid;
+        int64_t lo = 0, hi = ncls - 1;
+        while (lo < hi) {
+          const int64_t mid = (lo + hi + 1) >> 1;
+          if (cls[mid].row_begin <= b) lo = mid; else hi = mid - 1;
+        }
+        const double w = cls[lo].weight;
+        int64_t pc = 0;
+        for (int64_t q = 0; q < wpr; ++q) pc += __popcll(masks[b * wpr + q]);
+        const double z1 = w * (static_cast<double>(y[b]) - f0 - delta / Md * static_cast<double>(pc));
+        const double z2 = w * (static_cast<double>(y[b + half]) - f0 - delta / Md * static_cast<double>(M - pc));
+        dzs[tid] = z1 - z2;
+      }
       __syncthreads();
       if (j < M) {
         const uint64_t* col = masks + b0 * wpr + (j >> 6);
@@ -275,38 +269,228 @@ __global__ void __launch_bounds__(1024) k_rhs_finish(const double* __restrict__ 
 
 __global__ void k_zero_info(int32_t* info) { *info = 0; }
 
-// Cholesky of the diagonal block jb (in LDS); records the first bad pivot.
-__global__ void __launch_bounds__(256) k_potrf(float* G, int64_t M, int64_t jb, int32_t* info) {
-  __shared__ float A[kNB][kNB + 1];
+__device__ inline float bcast(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Cholesky of the nbe x nbe diagonal block at (o, o) by one wavefront: lane r
+// holds row o + r in registers; column k's pivot and entries are broadcast
+// with readlane.  Records the first non-positive pivot (1-based) in *info and
+// continues with a unit pivot.
+template <int NB>
+__device__ inline void chol_diag_wave(float* A, int64_t lda, int64_t o, int nbe, int32_t* info) {
+  const int lane = threadIdx.x & 63;
+  const bool own = lane < nbe;
+  float a[NB];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) a[c] = (own && c <= lane && c < nbe) ? A[(o + lane) * lda + o + c] : 0.f;
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    if (k < nbe) {
+      float piv = bcast(a[k], k);
+      if (!(piv > 0.f)) {
+        if (lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
+        piv = 1.f;
+      }
+      const float lkk = sqrtf(piv);
+      if (lane == k) a[k] = lkk;
+      else if (lane > k) a[k] = a[k] / lkk;
+#pragma unroll
+      for (int j = k + 1; j < NB; ++j) {
+        if (j < nbe) {
+          const float ljk = bcast(a[k], j);
+          if (lane >= j) a[j] -= a[k] * ljk;
+        }
+      }
+    }
+  }
+  if (own) {
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+      if (c < nbe) A[(o + lane) * lda + o + c] = c <= lane ? a[c] : 0.f;
+  }
+}
+
+// Cholesky of diagonal block jb of the multi-block path (one wavefront).
+__global__ void __launch_bounds__(64) k_potrf(float* G, int64_t M, int64_t jb, int32_t* info) {
   const int64_t o = jb * kNB;
   const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
+  chol_diag_wave<kNB>(G, M, o, n, info);
+}
+
+// Small systems (M <= kSmallM) in one workgroup: assemble G~ and the
+// right-hand side, factor (32-wide blocks), forward and backward solve, phi.
+// The matrix lives in LDS when it fits (kLds), else in the global buffer.
+constexpr int kSmallM = 512;
+constexpr int kSB = 32;
+
+template <bool kLds>
+__global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool has_random, double alpha,
+                                                     double wr, const float* __restrict__ fef,
+                                                     const double* __restrict__ part, int64_t nch,
+                                                     int32_t* info, float* __restrict__ phi) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  double* dv = reinterpret_cast<double*>(smem);      // M: row sums, then the raw right-hand side
+  float* rhs = reinterpret_cast<float*>(dv + M);     // M
+  float* xv = rhs + M;                               // M
+  float* A = kLds ? xv + M : G;
+  __shared__ double red[2][4];
+  __shared__ double sc[4];
   const int tid = threadIdx.x;
-  for (int t = tid; t < n * n; t += 256) {
-    const int i = t / n, j = t % n;
-    A[i][j] = G[(o + i) * M + o + j];
+  const int nt = blockDim.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int32_t* C = reinterpret_cast<const int32_t*>(G);
+  const double Md = static_cast<double>(M);
+  if (tid == 0) *info = 0;
+
+  // 1. row sums and trace of the counts
+  double trl = 0.0, sgl = 0.0;
+  if (has_random) {
+    for (int64_t i = tid; i < M; i += nt) {
+      long long sum = 0;
+      for (int64_t j = 0; j < M; ++j) sum += C[i * M + j];
+      dv[i] = static_cast<double>(sum);
+      trl += static_cast<double>(C[i * M + i]);
+      sgl += static_cast<double>(sum);
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    trl += __shfl_xor(trl, off);
+    sgl += __shfl_xor(sgl, off);
+  }
+  if (lane == 0) {
+    red[0][wave] = trl;
+    red[1][wave] = sgl;
   }
   __syncthreads();
-  for (int k = 0; k < n; ++k) {
-    float piv = A[k][k];
-    if (!(piv > 0.f)) {
-      if (tid == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
-      piv = 1.f;
+  if (tid == 0) {
+    double tr = 0.0, sg = 0.0;
+    for (int w = 0; w < nt / 64; ++w) {
+      tr += red[0][w];
+      sg += red[1][w];
     }
-    const float lkk = sqrtf(piv);
+    const double tr_pgp = alpha * (Md - 1.0) + 2.0 * wr * (tr - sg / Md);
+    sc[0] = sg;
+    sc[1] = tr_pgp / (Md - 1.0);
+    sc[2] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
+  }
+  __syncthreads();
+  const double sigma = sc[0], gamma = sc[1], delta = sc[2];
+
+  // 2. lower triangle of G~ = alpha P + 2 wr P C P + gamma 11^T/M
+  for (int64_t t = tid; t < M * M; t += nt) {
+    const int64_t i = t / M, j = t % M;
+    if (j > i) continue;
+    double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
+    if (has_random) v += 2.0 * wr * (static_cast<double>(C[t]) - (dv[i] + dv[j]) / Md + sigma / (Md * Md));
+    A[t] = static_cast<float>(v);
+  }
+  __syncthreads();
+
+  // 3. right-hand side P r
+  double sl = 0.0;
+  for (int64_t j = tid; j < M; j += nt) {
+    double v = 0.0;
+    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
+    dv[j] = v;
+    sl += v;
+  }
+  for (int off = 32; off > 0; off >>= 1) sl += __shfl_xor(sl, off);
+  if (lane == 0) red[0][wave] = sl;
+  __syncthreads();
+  if (tid == 0) {
+    double t = 0.0;
+    for (int w = 0; w < nt / 64; ++w) t += red[0][w];
+    sc[3] = t / Md;
+  }
+  __syncthreads();
+  for (int64_t j = tid; j < M; j += nt) rhs[j] = static_cast<float>(dv[j] - sc[3]);
+  __syncthreads();
+
+  // 4. Cholesky, 32-wide blocks
+  for (int64_t o = 0; o < M; o += kSB) {
+    const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
+    if (wave == 0) chol_diag_wave<kSB>(A, M, o, nbe, info);
     __syncthreads();
-    if (tid == 0) A[k][k] = lkk;
-    for (int i = k + 1 + tid; i < n; i += 256) A[i][k] = A[i][k] / lkk;
+    for (int64_t i = o + nbe + tid; i < M; i += nt) {
+      float x[kSB];
+#pragma unroll
+      for (int c = 0; c < kSB; ++c) x[c] = c < nbe ? A[i * M + o + c] : 0.f;
+#pragma unroll
+      for (int c = 0; c < kSB; ++c) {
+        if (c < nbe) {
+          float v = x[c];
+#pragma unroll
+          for (int k = 0; k < c; ++k) v -= x[k] * A[(o + c) * M + o + k];
+          x[c] = v / A[(o + c) * M + o + c];
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < kSB; ++c)
+        if (c < nbe) A[i * M + o + c] = x[c];
+    }
     __syncthreads();
-    for (int t = tid; t < (n - k - 1) * (n - k - 1); t += 256) {
-      const int i = k + 1 + t / (n - k - 1), j = k + 1 + t % (n - k - 1);
-      if (j <= i) A[i][j] -= A[i][k] * A[j][k];
+    const int64_t T = M - o - nbe;
+    for (int64_t t = tid; t < T * T; t += nt) {
+      const int64_t i = o + nbe + t / T, j = o + nbe + t % T;
+      if (j > i) continue;
+      float acc = 0.f;
+      for (int c = 0; c < nbe; ++c) acc += A[i * M + o + c] * A[j * M + o + c];
+      A[i * M + j] -= acc;
     }
     __syncthreads();
   }
-  for (int t = tid; t < n * n; t += 256) {
-    const int i = t / n, j = t % n;
-    G[(o + i) * M + o + j] = j <= i ? A[i][j] : 0.f;
+
+  // 5. forward substitution L x = rhs
+  for (int64_t o = 0; o < M; o += kSB) {
+    const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
+    if (wave == 0) {
+      float b = lane < nbe ? rhs[o + lane] : 0.f;
+#pragma unroll
+      for (int k = 0; k < kSB; ++k) {
+        if (k < nbe) {
+          const float xk = bcast(b, k) / A[(o + k) * M + o + k];
+          if (lane == k) b = xk;
+          else if (lane > k && lane < nbe) b -= A[(o + lane) * M + o + k] * xk;
+        }
+      }
+      if (lane < nbe) xv[o + lane] = b;
+    }
+    __syncthreads();
+    for (int64_t i = o + nbe + tid; i < M; i += nt) {
+      float acc = 0.f;
+      for (int c = 0; c < nbe; ++c) acc += A[i * M + o + c] * xv[o + c];
+      rhs[i] -= acc;
+    }
+    __syncthreads();
   }
+
+  // 6. backward substitution L^T z = x (z overwrites rhs)
+  for (int64_t o = ((M - 1) / kSB) * kSB; o >= 0; o -= kSB) {
+    const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
+    if (wave == 0) {
+      float b = lane < nbe ? xv[o + lane] : 0.f;
+#pragma unroll
+      for (int k = kSB - 1; k >= 0; --k) {
+        if (k < nbe) {
+          const float zk = bcast(b, k) / A[(o + k) * M + o + k];
+          if (lane == k) b = zk;
+          else if (lane < k) b -= A[(o + k) * M + o + lane] * zk;
+        }
+      }
+      if (lane < nbe) rhs[o + lane] = b;
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < o; i += nt) {
+      float acc = 0.f;
+      for (int c = 0; c < nbe; ++c) acc += A[(o + c) * M + i] * rhs[o + c];
+      xv[i] -= acc;
+    }
+    __syncthreads();
+  }
+
+  // 7. phi = Delta/M + psi
+  for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rhs[i]));
 }
 
 // Panel: rows of block ib > jb: X <- X L_jj^-T.  One thread per row.
@@ -524,8 +708,6 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     alpha += classes[i].weight * kappa * binom_d(M - 2, c - 1);
   }
   GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class), hipMemcpyHostToDevice, s));
-  k_zero_info<<<1, 1, 0, s>>>(info);
-  GS_LAUNCHED();
   int32_t* counts = reinterpret_cast<int32_t*>(w.G);
   if (has_random) {
     const int64_t nrb = gnnshap::ceil_div(kr, 64);
@@ -534,6 +716,37 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     const unsigned nb = static_cast<unsigned>(gnnshap::ceil_div(M, 64));
     k_gram<<<dim3(nb, nb), 256, 0, s>>>(w.T, nrb, M, counts);
     GS_LAUNCHED();
+  }
+  const int64_t nch = n_chunks(half);
+  const int64_t rpc = gnnshap::ceil_div(half, nch);
+  k_rhs_part<<<static_cast<unsigned>(nch), 256, 0, s>>>(masks, wpr, half, M, y, w.classes, plan->num_classes,
+                                                         f_empty_full, rpc, w.part);
+  GS_LAUNCHED();
+
+  if (M <= kSmallM) {
+    // one workgroup: assembly, factorisation, both solves
+    const size_t vec_bytes = static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float));
+    const size_t mat_bytes = static_cast<size_t>(M) * M * sizeof(float);
+    bool in_lds = false;
+    if (vec_bytes + mat_bytes <= static_cast<size_t>(gnnshap::max_lds_bytes())) {
+      in_lds = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_solve_small<true>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   static_cast<int>(vec_bytes + mat_bytes)) == hipSuccess;
+      (void)hipGetLastError();
+    }
+    if (in_lds)
+      k_solve_small<true><<<1, 256, vec_bytes + mat_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full,
+                                                                 w.part, nch, info, phi);
+    else
+      k_solve_small<false><<<1, 256, vec_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full, w.part, nch,
+                                                      info, phi);
+    GS_LAUNCHED();
+    return GNNSHAP_OK;
+  }
+
+  k_zero_info<<<1, 1, 0, s>>>(info);
+  GS_LAUNCHED();
+  if (has_random) {
     k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, w.usum);
     GS_LAUNCHED();
   }
@@ -541,19 +754,12 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   GS_LAUNCHED();
   k_build<<<gnnshap::grid_for(M * M, 256, 16384), 256, 0, s>>>(w.G, w.usum, M, has_random, alpha, wr, w.scal);
   GS_LAUNCHED();
-  const int64_t nch = n_chunks(half);
-  const int64_t rpc = gnnshap::ceil_div(half, nch);
-  k_dz<<<gnnshap::grid_for(half, 256, 4096), 256, 0, s>>>(masks, wpr, half, M, y, w.classes, plan->num_classes,
-                                                           w.scal, w.dz);
-  GS_LAUNCHED();
-  k_rhs_part<<<static_cast<unsigned>(nch), 256, 0, s>>>(masks, wpr, half, M, w.dz, rpc, w.part);
-  GS_LAUNCHED();
   k_rhs_finish<<<1, 1024, 0, s>>>(w.part, nch, M, w.rhs, w.scal);
   GS_LAUNCHED();
   // Cholesky G~ = L L^T.
   const int64_t nblk = gnnshap::ceil_div(M, kNB);
   for (int64_t jb = 0; jb < nblk; ++jb) {
-    k_potrf<<<1, 256, 0, s>>>(w.G, M, jb, info);
+    k_potrf<<<1, 64, 0, s>>>(w.G, M, jb, info);
     GS_LAUNCHED();
     const int64_t rest = nblk - jb - 1;
     if (rest > 0) {

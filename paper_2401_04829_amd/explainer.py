@@ -82,7 +82,8 @@ class Explainer:
         self._dims = (ctypes.c_int32 * (nl + 1))(*self.dims)
         self._Wp = (ctypes.c_void_p * nl)(*[w.data_ptr() for w in self.W])
         self._bp = (ctypes.c_void_p * nl)(*[0 if b is None else b.data_ptr() for b in self.b])
-        self.model = L.gnnshap_gcn(num_layers=nl, dims=self._dims, W=self._Wp, b=self._bp)
+        self.model = L.gnnshap_gcn(num_layers=nl, dims=self._dims, W=self._Wp, b=self._bp, XW1=None)
+        self.XW1 = None
         self.extract_ws = torch.zeros(L.gnnshap_extract_workspace(n), dtype=torch.uint8, device=dev)
         self._cap_nodes = 0
         self._cap_edges = 0
@@ -90,6 +91,15 @@ class Explainer:
         self.ws_sample = _Buffer(dev)
         self.ws_eval = _Buffer(dev)
         self.ws_solve = _Buffer(dev)
+
+    def prepare(self):
+        """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
+        n = self.X.shape[0]
+        if self.XW1 is None:
+            self.XW1 = torch.empty((n, self.dims[1]), dtype=torch.float32, device=self.device)
+        L.gnnshap_transform_features(_vp(self.X), n, self.dims[0], _vp(self.W[0]), self.dims[1], _vp(self.XW1),
+                                     self.stream())
+        self.model.XW1 = self.XW1.data_ptr()
 
     def stream(self):
         return ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream)
@@ -127,6 +137,8 @@ class Explainer:
 
     def explain(self, target, num_samples, seed, target_class=-1, stream_id=None):
         """Alg. 1 for one target: extract, plan, sample, evaluate, solve."""
+        if self.XW1 is None:
+            self.prepare()
         sub = self.extract(target)
         M = sub.sg.num_edges
         if M < 2:

@@ -199,6 +199,45 @@ def test_eval_fixed_class_and_wide_layers(dev):
         _check_eval(cfg, v, 800, 3, target_class=4)
 
 
+def test_eval_hub_target_unfused_path(dev):
+    """A target with 300 in-neighbours: the two-layer kernel's LDS tables do not
+    fit, so the layered kernels run; both must agree with the oracle."""
+    n = 400
+    src = list(range(1, 301)) + [int(x) for x in np.random.default_rng(3).integers(1, n, 600)]
+    dst = [0] * 300 + [int(x) for x in np.random.default_rng(4).integers(1, n, 600)]
+    indptr, indices = W.in_csr_from_pairs(n, np.array(src), np.array(dst))
+    X = W.gaussian_features(n, 12, 5)
+    Ws, bs = W.glorot_gcn([12, 16, 5], 6, bias="random")
+    cfg = dict(indptr=indptr, indices=indices, X=X, weights=Ws, biases=bs, hops=2)
+    rng = np.random.default_rng(9)
+    M = subgraph.extract(indptr, indices, 0, 2)["num_edges"]
+    k = sampler.plan(M, 3000)["k"]
+    _check_eval(cfg, 0, 3000, 21, rows=np.unique(rng.integers(0, k, 64)))
+
+
+def test_transform_features_and_unfused_first_layer(dev):
+    """gnnshap_transform_features against fp64 numpy, and evaluation with
+    X W_1 gathered vs computed from X per call."""
+    from paper_2401_04829_amd import _lib as L
+    from paper_2401_04829_amd.explainer import _vp
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    ex.prepare()
+    torch.cuda.synchronize()
+    ref = cfg["X"].astype(np.float64) @ cfg["weights"][0].astype(np.float64)
+    got = ex.XW1.cpu().numpy()
+    assert np.abs(got - ref).max() <= 1e-5 * max(1.0, np.abs(ref).max())
+    v = cfg["targets"][3]
+    r1 = ex.explain(v, cfg["p"], cfg["seed"])
+    y1 = r1.y.clone()
+    ex.model.XW1 = None
+    r2 = ex.run(ex.extract(v), r1.plan, r1.classes, -1, v)
+    ex.model.XW1 = ex.XW1.data_ptr()
+    torch.cuda.synchronize()
+    d = (r2.y - y1).abs().max().item()
+    assert d <= 1e-5 * max(1.0, y1.abs().max().item())
+
+
 def test_eval_cora_all_targets_sampled_rows(dev):
     cfg = W.make_config("cora")
     rng = np.random.default_rng(0)
