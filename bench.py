@@ -29,6 +29,7 @@ def parse():
     ap.add_argument("--config", default="cora")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--streams", type=int, default=8)
     return ap.parse_args()
 
 
@@ -71,14 +72,9 @@ def main():
     targets = cfg["targets"]
 
     def step():
-        ks = 0
-        last = None
         ex.prepare()                 # X W_1 once per step, shared by every target
-        for v in targets:
-            r = ex.explain(v, cfg["p"], cfg["seed"])
-            ks += r.plan.num_rows
-            last = r
-        return ks, last
+        res = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=args.streams)
+        return sum(r.plan.num_rows for r in res), res
 
     for _ in range(args.warmup):
         step()

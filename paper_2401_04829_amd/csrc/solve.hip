@@ -334,6 +334,7 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
   float* rhs = reinterpret_cast<float*>(dv + M);     // M
   float* xv = rhs + M;                               // M
   float* A = kLds ? xv + M : G;
+  float* P = xv + M;                                 // global-matrix mode: panel rows (<= kSmallM x kSB)
   __shared__ double red[2][4];
   __shared__ double sc[4];
   const int tid = threadIdx.x;
@@ -407,36 +408,67 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
   for (int64_t j = tid; j < M; j += nt) rhs[j] = static_cast<float>(dv[j] - sc[3]);
   __syncthreads();
 
-  // 4. Cholesky, 32-wide blocks
+  // 4. Cholesky, 32-wide blocks.  The panel below the diagonal block is solved
+  // row by row (right-looking over its 32 columns) and kept in LDS (P), the
+  // trailing triangle is updated in 4x4 register tiles.
   for (int64_t o = 0; o < M; o += kSB) {
     const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
     if (wave == 0) chol_diag_wave<kSB>(A, M, o, nbe, info);
     __syncthreads();
-    for (int64_t i = o + nbe + tid; i < M; i += nt) {
+    const int64_t r0 = o + nbe;                      // first trailing row
+    const int64_t T = M - r0;
+    const float* Pb = kLds ? A + r0 * M + o : P;     // panel row i at Pb[(i - r0) * ps + c]
+    const int64_t ps = kLds ? M : kSB;
+    for (int64_t i = r0 + tid; i < M; i += nt) {
       float x[kSB];
 #pragma unroll
       for (int c = 0; c < kSB; ++c) x[c] = c < nbe ? A[i * M + o + c] : 0.f;
 #pragma unroll
       for (int c = 0; c < kSB; ++c) {
         if (c < nbe) {
-          float v = x[c];
+          x[c] = x[c] / A[(o + c) * M + o + c];
 #pragma unroll
-          for (int k = 0; k < c; ++k) v -= x[k] * A[(o + c) * M + o + k];
-          x[c] = v / A[(o + c) * M + o + c];
+          for (int q = c + 1; q < kSB; ++q)
+            if (q < nbe) x[q] -= x[c] * A[(o + q) * M + o + c];
         }
       }
 #pragma unroll
-      for (int c = 0; c < kSB; ++c)
-        if (c < nbe) A[i * M + o + c] = x[c];
+      for (int c = 0; c < kSB; ++c) {
+        if (c < nbe) {
+          A[i * M + o + c] = x[c];
+          if (!kLds) P[(i - r0) * kSB + c] = x[c];
+        }
+      }
     }
     __syncthreads();
-    const int64_t T = M - o - nbe;
-    for (int64_t t = tid; t < T * T; t += nt) {
-      const int64_t i = o + nbe + t / T, j = o + nbe + t % T;
-      if (j > i) continue;
-      float acc = 0.f;
-      for (int c = 0; c < nbe; ++c) acc += A[i * M + o + c] * A[j * M + o + c];
-      A[i * M + j] -= acc;
+    const int64_t T4 = (T + 3) / 4;
+    for (int64_t t = tid; t < T4 * T4; t += nt) {
+      const int64_t I = t / T4, J = t % T4;
+      if (J > I) continue;
+      float acc[4][4] = {};
+      for (int c = 0; c < nbe; ++c) {
+        float pa[4], pb[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t ri = 4 * I + q, rj = 4 * J + q;
+          pa[q] = ri < T ? Pb[ri * ps + c] : 0.f;
+          pb[q] = rj < T ? Pb[rj * ps + c] : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[q][r] += pa[q] * pb[r];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t i = r0 + 4 * I + q;
+        if (i >= M) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t j = r0 + 4 * J + r;
+          if (j <= i) A[i * M + j] -= acc[q][r];
+        }
+      }
     }
     __syncthreads();
   }
@@ -727,21 +759,28 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     // one workgroup: assembly, factorisation, both solves
     const size_t vec_bytes = static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float));
     const size_t mat_bytes = static_cast<size_t>(M) * M * sizeof(float);
-    bool in_lds = false;
-    if (vec_bytes + mat_bytes <= static_cast<size_t>(gnnshap::max_lds_bytes())) {
-      in_lds = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_solve_small<true>),
-                                   hipFuncAttributeMaxDynamicSharedMemorySize,
-                                   static_cast<int>(vec_bytes + mat_bytes)) == hipSuccess;
+    const size_t panel_bytes = static_cast<size_t>(M) * kSB * sizeof(float);
+    const int lds_max = gnnshap::max_lds_bytes();
+    auto fits = [&](const void* fn, size_t bytes) {
+      if (bytes > static_cast<size_t>(lds_max)) return false;
+      if (bytes <= 65536) return true;
+      const bool ok = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                          static_cast<int>(bytes)) == hipSuccess;
       (void)hipGetLastError();
-    }
-    if (in_lds)
+      return ok;
+    };
+    if (fits(reinterpret_cast<const void*>(&k_solve_small<true>), vec_bytes + mat_bytes)) {
       k_solve_small<true><<<1, 256, vec_bytes + mat_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full,
                                                                  w.part, nch, info, phi);
-    else
-      k_solve_small<false><<<1, 256, vec_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full, w.part, nch,
-                                                      info, phi);
-    GS_LAUNCHED();
-    return GNNSHAP_OK;
+      GS_LAUNCHED();
+      return GNNSHAP_OK;
+    }
+    if (fits(reinterpret_cast<const void*>(&k_solve_small<false>), vec_bytes + panel_bytes)) {
+      k_solve_small<false><<<1, 256, vec_bytes + panel_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full,
+                                                                    w.part, nch, info, phi);
+      GS_LAUNCHED();
+      return GNNSHAP_OK;
+    }
   }
 
   k_zero_info<<<1, 1, 0, s>>>(info);

@@ -147,22 +147,93 @@ class Explainer:
                                                int(target if stream_id is None else stream_id))
         return self.run(sub, plan, classes, target_class, target)
 
-    def run(self, sub, plan, classes, target_class=-1, target=-1):
+    def explain_many(self, targets, num_samples, seed, target_class=-1, n_streams=8):
+        """Alg. 1 for many targets, pipelined: extraction (the only call that
+        waits for the device) runs on its own stream while earlier targets'
+        sampling, evaluation and solve run on `n_streams` compute streams, so
+        independent targets overlap on the GPU.  Returns one Explanation per
+        target; their device tensors are complete once the default stream has
+        synchronised (the compute streams are joined to it at the end)."""
+        if self.XW1 is None:
+            self.prepare()
+        main = torch.cuda.current_stream(self.device)
+        ext = self._pipe_streams(n_streams)
+        ext_stream, lanes = ext
+        ext_stream.wait_stream(main)
+        for st in lanes:
+            st.wait_stream(main)
+        out = []
+        for t, v in enumerate(targets):
+            lane = lanes[t % len(lanes)]
+            slot = self._slots[t % len(lanes)]
+            # the slot's subgraph buffers are rewritten: wait for its previous target
+            ext_stream.wait_stream(lane)
+            with torch.cuda.stream(ext_stream):
+                sub = self._extract_into(slot, v)
+            M = sub.sg.num_edges
+            if M < 2:
+                raise ValueError(f"target {v} has {M} players; at least 2 are needed")
+            plan, classes = L.gnnshap_plan_samples(M, int(num_samples), int(seed), int(v))
+            with torch.cuda.stream(lane):
+                out.append(self.run(sub, plan, classes, target_class, v, slot=slot))
+        for st in lanes:
+            main.wait_stream(st)
+        return out
+
+    def _pipe_streams(self, n):
+        if getattr(self, "_pipe", None) is None or len(self._pipe[1]) != n:
+            self._pipe = (torch.cuda.Stream(self.device), [torch.cuda.Stream(self.device) for _ in range(n)])
+            self._slots = [dict(sub=None, cap_nodes=0, cap_edges=0, ws_sample=_Buffer(self.device),
+                                ws_eval=_Buffer(self.device), ws_solve=_Buffer(self.device)) for _ in range(n)]
+        return self._pipe
+
+    def _extract_into(self, slot, target):
+        dev = self.device
+        while True:
+            if slot["sub"] is None:
+                slot["cap_nodes"], slot["cap_edges"] = 1024, 8192
+            b = slot["sub"]
+            if b is None or b["node_gid"].numel() < slot["cap_nodes"] or b["edge_src"].numel() < slot["cap_edges"]:
+                cn, ce = slot["cap_nodes"], slot["cap_edges"]
+                b = slot["sub"] = dict(
+                    node_gid=torch.empty(cn, dtype=torch.int32, device=dev),
+                    dst_ptr=torch.empty(cn + 1, dtype=torch.int32, device=dev),
+                    edge_src=torch.empty(ce, dtype=torch.int32, device=dev),
+                    edge_dst=torch.empty(ce, dtype=torch.int32, device=dev),
+                    edge_gid=torch.empty(ce, dtype=torch.int64, device=dev))
+            sg = L.gnnshap_subgraph(num_hops=self.hops, cap_nodes=b["node_gid"].numel(),
+                                    cap_edges=b["edge_src"].numel(), node_gid=b["node_gid"].data_ptr(),
+                                    dst_ptr=b["dst_ptr"].data_ptr(), edge_src=b["edge_src"].data_ptr(),
+                                    edge_dst=b["edge_dst"].data_ptr(), edge_gid=b["edge_gid"].data_ptr())
+            st = L.gnnshap_extract_subgraph(self.graph, int(target), sg, _vp(self.extract_ws),
+                                            self.extract_ws.numel(), self.stream())
+            if st == L.OK:
+                break
+            slot["cap_nodes"] = max(int(sg.num_nodes * 1.25) + 16, slot["cap_nodes"])
+            slot["cap_edges"] = max(int(sg.num_edges * 1.25) + 64, slot["cap_edges"])
+        n, m, nd = sg.num_nodes, sg.num_edges, sg.num_dst
+        return Subgraph(sg=sg, node_gid=b["node_gid"][:n], dst_ptr=b["dst_ptr"][:nd + 1],
+                        edge_src=b["edge_src"][:m], edge_dst=b["edge_dst"][:m], edge_gid=b["edge_gid"][:m])
+
+    def run(self, sub, plan, classes, target_class=-1, target=-1, slot=None):
         dev, s = self.device, self.stream()
+        ws_sample = slot["ws_sample"] if slot else self.ws_sample
+        ws_eval = slot["ws_eval"] if slot else self.ws_eval
+        ws_solve = slot["ws_solve"] if slot else self.ws_solve
         k, wpr, M = plan.num_rows, plan.words_per_row, plan.num_players
         masks = torch.empty((k, wpr), dtype=torch.int64, device=dev)
         weights = torch.empty(k, dtype=torch.float32, device=dev)
-        ws = self.ws_sample.get(L.gnnshap_sample_workspace(plan))
+        ws = ws_sample.get(L.gnnshap_sample_workspace(plan))
         L.gnnshap_sample_coalitions(plan, classes, _vp(masks), _vp(weights), _vp(ws), ws.numel(), s)
         y = torch.empty(k, dtype=torch.float32, device=dev)
         fef = torch.empty(2, dtype=torch.float32, device=dev)
         cls = torch.empty(1, dtype=torch.int32, device=dev)
-        ws = self.ws_eval.get(L.gnnshap_eval_workspace(sub.sg, self.model, k))
+        ws = ws_eval.get(L.gnnshap_eval_workspace(sub.sg, self.model, k))
         L.gnnshap_eval_coalitions(sub.sg, self.model, _vp(self.X), int(target_class), _vp(masks), k, wpr, _vp(y),
                                   _vp(fef), _vp(cls), _vp(ws), ws.numel(), s)
         phi = torch.empty(M, dtype=torch.float32, device=dev)
         info = torch.empty(1, dtype=torch.int32, device=dev)
-        ws = self.ws_solve.get(L.gnnshap_solve_workspace(plan))
+        ws = ws_solve.get(L.gnnshap_solve_workspace(plan))
         L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws), ws.numel(), s)
         return Explanation(target=target, sub=sub, plan=plan, classes=classes, masks=masks, weights=weights, y=y,
                            f_empty_full=fef, cls=cls, phi=phi, info=info)

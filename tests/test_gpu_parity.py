@@ -238,6 +238,24 @@ def test_transform_features_and_unfused_first_layer(dev):
     assert d <= 1e-5 * max(1.0, y1.abs().max().item())
 
 
+def test_pipelined_targets_match_sequential(dev):
+    """explain_many (extraction on its own stream, targets spread over compute
+    streams) gives bit-identical masks, values and phi to explain()."""
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    targets = cfg["targets"]
+    many = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=8)
+    torch.cuda.synchronize()
+    for v, r in zip(targets, many):
+        _say("pipelined", v)
+        one = ex.explain(v, cfg["p"], cfg["seed"])
+        torch.cuda.synchronize()
+        assert torch.equal(one.masks, r.masks)
+        assert torch.equal(one.y, r.y)
+        assert torch.equal(one.phi, r.phi)
+        assert int(r.info.item()) == 0
+
+
 def test_eval_cora_all_targets_sampled_rows(dev):
     cfg = W.make_config("cora")
     rng = np.random.default_rng(0)
