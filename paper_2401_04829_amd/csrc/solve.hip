@@ -39,7 +39,7 @@ struct Ws {
 constexpr int kMaxChunks = 256;
 
 int64_t n_chunks(int64_t half) {
-  int64_t c = gnnshap::ceil_div(half, 64);
+  int64_t c = gnnshap::ceil_div(half, 256);
   return c < 1 ? 1 : (c > kMaxChunks ? kMaxChunks : c);
 }
 
@@ -318,41 +318,95 @@ __global__ void __launch_bounds__(64) k_potrf(float* G, int64_t M, int64_t jb, i
   chol_diag_wave<kNB>(G, M, o, n, info);
 }
 
-// Small systems (M <= kSmallM) in one workgroup: assemble G~ and the
-// right-hand side, factor (32-wide blocks), forward and backward solve, phi.
-// The matrix lives in LDS when it fits (kLds), else in the global buffer.
-constexpr int kSmallM = 512;
+// Small systems in one workgroup, the lower triangle of G~ packed in LDS
+// (row i starts at i(i+1)/2): assemble G~ from the counts and the right-hand
+// side from the partial sums, factor (32-wide blocks: one wavefront factors
+// the diagonal block in registers, the panel rows are solved right-looking,
+// the trailing triangle is updated in 4x4 register tiles), then the forward
+// and backward solves and phi.
 constexpr int kSB = 32;
 
-template <bool kLds>
-__global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool has_random, double alpha,
-                                                     double wr, const float* __restrict__ fef,
+__device__ inline int64_t tri(int64_t i, int64_t j) { return ((i * (i + 1)) >> 1) + j; }
+
+// Cholesky of the diagonal block at (o, o) of a packed lower triangle.
+__device__ inline void chol_diag_wave_packed(float* A, int64_t o, int nbe, int32_t* info) {
+  const int lane = threadIdx.x & 63;
+  const bool own = lane < nbe;
+  float a[kSB];
+#pragma unroll
+  for (int c = 0; c < kSB; ++c) a[c] = (own && c <= lane && c < nbe) ? A[tri(o + lane, o + c)] : 0.f;
+#pragma unroll
+  for (int k = 0; k < kSB; ++k) {
+    if (k < nbe) {
+      float piv = bcast(a[k], k);
+      if (!(piv > 0.f)) {
+        if (lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
+        piv = 1.f;
+      }
+      const float lkk = sqrtf(piv);
+      if (lane == k) a[k] = lkk;
+      else if (lane > k) a[k] = a[k] / lkk;
+#pragma unroll
+      for (int j = k + 1; j < kSB; ++j) {
+        if (j < nbe) {
+          const float ljk = bcast(a[k], j);
+          if (lane >= j) a[j] -= a[k] * ljk;
+        }
+      }
+    }
+  }
+  if (own) {
+#pragma unroll
+    for (int c = 0; c < kSB; ++c)
+      if (c < nbe && c <= lane) A[tri(o + lane, o + c)] = a[c];
+  }
+}
+
+size_t small_lds_bytes(int64_t M) {
+  return static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float)) +
+         static_cast<size_t>((M * (M + 1)) / 2) * sizeof(float);
+}
+
+__global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__ C, int64_t M, bool has_random,
+                                                     double alpha, double wr, const float* __restrict__ fef,
                                                      const double* __restrict__ part, int64_t nch,
                                                      int32_t* info, float* __restrict__ phi) {
   extern __shared__ __align__(16) unsigned char smem[];
   double* dv = reinterpret_cast<double*>(smem);      // M: row sums, then the raw right-hand side
   float* rhs = reinterpret_cast<float*>(dv + M);     // M
   float* xv = rhs + M;                               // M
-  float* A = kLds ? xv + M : G;
-  float* P = xv + M;                                 // global-matrix mode: panel rows (<= kSmallM x kSB)
+  float* A = xv + M;                                 // packed lower triangle
   __shared__ double red[2][4];
   __shared__ double sc[4];
   const int tid = threadIdx.x;
   const int nt = blockDim.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int32_t* C = reinterpret_cast<const int32_t*>(G);
   const double Md = static_cast<double>(M);
   if (tid == 0) *info = 0;
 
-  // 1. row sums and trace of the counts
+  // 1. counts -> LDS (lower part, exact as floats below 2^24), row sums, trace
   double trl = 0.0, sgl = 0.0;
   if (has_random) {
-    for (int64_t i = tid; i < M; i += nt) {
+    for (int64_t i = wave; i < M; i += nt / 64) {
       long long sum = 0;
-      for (int64_t j = 0; j < M; ++j) sum += C[i * M + j];
-      dv[i] = static_cast<double>(sum);
-      trl += static_cast<double>(C[i * M + i]);
-      sgl += static_cast<double>(sum);
+      for (int64_t j0 = 0; j0 < M; j0 += 512) {
+        int32_t v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int64_t j = j0 + q * 64 + lane;
+          v[q] = j < M ? C[i * M + j] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int64_t j = j0 + q * 64 + lane;
+          sum += v[q];
+          if (j <= i) A[tri(i, j)] = static_cast<float>(v[q]);
+          if (j == i) trl += static_cast<double>(v[q]);
+        }
+      }
+      for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+      if (lane == 0) dv[i] = static_cast<double>(sum);
+      sgl += lane == 0 ? static_cast<double>(sum) : 0.0;
     }
   }
   for (int off = 32; off > 0; off >>= 1) {
@@ -378,21 +432,29 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
   __syncthreads();
   const double sigma = sc[0], gamma = sc[1], delta = sc[2];
 
-  // 2. lower triangle of G~ = alpha P + 2 wr P C P + gamma 11^T/M
-  for (int64_t t = tid; t < M * M; t += nt) {
-    const int64_t i = t / M, j = t % M;
-    if (j > i) continue;
-    double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
-    if (has_random) v += 2.0 * wr * (static_cast<double>(C[t]) - (dv[i] + dv[j]) / Md + sigma / (Md * Md));
-    A[t] = static_cast<float>(v);
+  // 2. G~ = alpha P + 2 wr P C P + gamma 11^T/M, lower triangle in place
+  const int64_t ntri = (M * (M + 1)) / 2;
+  for (int64_t i = 0, base = 0; i < M; base += i + 1, ++i) {
+    for (int64_t j = tid; j <= i; j += nt) {
+      double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
+      if (has_random) v += 2.0 * wr * (static_cast<double>(A[base + j]) - (dv[i] + dv[j]) / Md + sigma / (Md * Md));
+      A[base + j] = static_cast<float>(v);
+    }
   }
+  (void)ntri;
   __syncthreads();
 
-  // 3. right-hand side P r
+  // 3. right-hand side P r from the partial sums (8 loads in flight per thread)
   double sl = 0.0;
   for (int64_t j = tid; j < M; j += nt) {
     double v = 0.0;
-    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
+    for (int64_t c0 = 0; c0 < nch; c0 += 8) {
+      double t[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) t[q] = c0 + q < nch ? part[(c0 + q) * M + j] : 0.0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v += t[q];
+    }
     dv[j] = v;
     sl += v;
   }
@@ -408,37 +470,30 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
   for (int64_t j = tid; j < M; j += nt) rhs[j] = static_cast<float>(dv[j] - sc[3]);
   __syncthreads();
 
-  // 4. Cholesky, 32-wide blocks.  The panel below the diagonal block is solved
-  // row by row (right-looking over its 32 columns) and kept in LDS (P), the
-  // trailing triangle is updated in 4x4 register tiles.
+  // 4. Cholesky
   for (int64_t o = 0; o < M; o += kSB) {
     const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
-    if (wave == 0) chol_diag_wave<kSB>(A, M, o, nbe, info);
+    if (wave == 0) chol_diag_wave_packed(A, o, nbe, info);
     __syncthreads();
-    const int64_t r0 = o + nbe;                      // first trailing row
+    const int64_t r0 = o + nbe;
     const int64_t T = M - r0;
-    const float* Pb = kLds ? A + r0 * M + o : P;     // panel row i at Pb[(i - r0) * ps + c]
-    const int64_t ps = kLds ? M : kSB;
     for (int64_t i = r0 + tid; i < M; i += nt) {
       float x[kSB];
+      const int64_t bi = tri(i, o);
 #pragma unroll
-      for (int c = 0; c < kSB; ++c) x[c] = c < nbe ? A[i * M + o + c] : 0.f;
+      for (int c = 0; c < kSB; ++c) x[c] = c < nbe ? A[bi + c] : 0.f;
 #pragma unroll
       for (int c = 0; c < kSB; ++c) {
         if (c < nbe) {
-          x[c] = x[c] / A[(o + c) * M + o + c];
+          x[c] = x[c] / A[tri(o + c, o + c)];
 #pragma unroll
           for (int q = c + 1; q < kSB; ++q)
-            if (q < nbe) x[q] -= x[c] * A[(o + q) * M + o + c];
+            if (q < nbe) x[q] -= x[c] * A[tri(o + q, o + c)];
         }
       }
 #pragma unroll
-      for (int c = 0; c < kSB; ++c) {
-        if (c < nbe) {
-          A[i * M + o + c] = x[c];
-          if (!kLds) P[(i - r0) * kSB + c] = x[c];
-        }
-      }
+      for (int c = 0; c < kSB; ++c)
+        if (c < nbe) A[bi + c] = x[c];
     }
     __syncthreads();
     const int64_t T4 = (T + 3) / 4;
@@ -446,13 +501,19 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
       const int64_t I = t / T4, J = t % T4;
       if (J > I) continue;
       float acc[4][4] = {};
+      int64_t pi[4], pj[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t ri = r0 + 4 * I + q, rj = r0 + 4 * J + q;
+        pi[q] = ri < M ? tri(ri, o) : -1;
+        pj[q] = rj < M ? tri(rj, o) : -1;
+      }
       for (int c = 0; c < nbe; ++c) {
         float pa[4], pb[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int64_t ri = 4 * I + q, rj = 4 * J + q;
-          pa[q] = ri < T ? Pb[ri * ps + c] : 0.f;
-          pb[q] = rj < T ? Pb[rj * ps + c] : 0.f;
+          pa[q] = pi[q] >= 0 ? A[pi[q] + c] : 0.f;
+          pb[q] = pj[q] >= 0 ? A[pj[q] + c] : 0.f;
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q)
@@ -466,7 +527,7 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t j = r0 + 4 * J + r;
-          if (j <= i) A[i * M + j] -= acc[q][r];
+          if (j <= i) A[tri(i, j)] -= acc[q][r];
         }
       }
     }
@@ -481,9 +542,9 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
 #pragma unroll
       for (int k = 0; k < kSB; ++k) {
         if (k < nbe) {
-          const float xk = bcast(b, k) / A[(o + k) * M + o + k];
+          const float xk = bcast(b, k) / A[tri(o + k, o + k)];
           if (lane == k) b = xk;
-          else if (lane > k && lane < nbe) b -= A[(o + lane) * M + o + k] * xk;
+          else if (lane > k && lane < nbe) b -= A[tri(o + lane, o + k)] * xk;
         }
       }
       if (lane < nbe) xv[o + lane] = b;
@@ -491,7 +552,8 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
     __syncthreads();
     for (int64_t i = o + nbe + tid; i < M; i += nt) {
       float acc = 0.f;
-      for (int c = 0; c < nbe; ++c) acc += A[i * M + o + c] * xv[o + c];
+      const int64_t bi = tri(i, o);
+      for (int c = 0; c < nbe; ++c) acc += A[bi + c] * xv[o + c];
       rhs[i] -= acc;
     }
     __syncthreads();
@@ -505,9 +567,9 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
 #pragma unroll
       for (int k = kSB - 1; k >= 0; --k) {
         if (k < nbe) {
-          const float zk = bcast(b, k) / A[(o + k) * M + o + k];
+          const float zk = bcast(b, k) / A[tri(o + k, o + k)];
           if (lane == k) b = zk;
-          else if (lane < k) b -= A[(o + k) * M + o + lane] * zk;
+          else if (lane < k) b -= A[tri(o + k, o + lane)] * zk;
         }
       }
       if (lane < nbe) rhs[o + lane] = b;
@@ -515,7 +577,7 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
     __syncthreads();
     for (int64_t i = tid; i < o; i += nt) {
       float acc = 0.f;
-      for (int c = 0; c < nbe; ++c) acc += A[(o + c) * M + i] * rhs[o + c];
+      for (int c = 0; c < nbe; ++c) acc += A[tri(o + c, i)] * rhs[o + c];
       xv[i] -= acc;
     }
     __syncthreads();
@@ -523,6 +585,70 @@ __global__ void __launch_bounds__(256) k_solve_small(float* G, int64_t M, bool h
 
   // 7. phi = Delta/M + psi
   for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rhs[i]));
+}
+
+// Both triangular solves and phi in one workgroup, for a factor in global
+// memory (multi-block path): forward L x = rhs, backward L^T z = x.
+__global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G, int64_t M,
+                                                    float* __restrict__ rhs, float* __restrict__ x,
+                                                    const double* __restrict__ scal, float* __restrict__ phi) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int64_t o = 0; o < M; o += 64) {
+    const int nbe = static_cast<int>(M - o < 64 ? M - o : 64);
+    if (wave == 0) {
+      float b = lane < nbe ? rhs[o + lane] : 0.f;
+      float lrow[64];
+#pragma unroll
+      for (int k = 0; k < 64; ++k) lrow[k] = (lane < nbe && k < nbe && k < lane) ? G[(o + lane) * M + o + k] : 0.f;
+#pragma unroll
+      for (int k = 0; k < 64; ++k) {
+        if (k < nbe) {
+          const float xk = bcast(b, k) / G[(o + k) * M + o + k];
+          if (lane == k) b = xk;
+          else if (lane > k) b -= lrow[k] * xk;
+        }
+      }
+      if (lane < nbe) x[o + lane] = b;
+    }
+    __syncthreads();
+    for (int64_t i = o + nbe + tid; i < M; i += nt) {
+      float acc = 0.f;
+      const float* row = G + i * M + o;
+#pragma unroll 8
+      for (int c = 0; c < nbe; ++c) acc += row[c] * x[o + c];
+      rhs[i] -= acc;
+    }
+    __syncthreads();
+  }
+  for (int64_t o = ((M - 1) / 64) * 64; o >= 0; o -= 64) {
+    const int nbe = static_cast<int>(M - o < 64 ? M - o : 64);
+    if (wave == 0) {
+      float b = lane < nbe ? x[o + lane] : 0.f;
+      float lcol[64];
+#pragma unroll
+      for (int k = 0; k < 64; ++k) lcol[k] = (lane < nbe && k < nbe && k > lane) ? G[(o + k) * M + o + lane] : 0.f;
+#pragma unroll
+      for (int k = 63; k >= 0; --k) {
+        if (k < nbe) {
+          const float zk = bcast(b, k) / G[(o + k) * M + o + k];
+          if (lane == k) b = zk;
+          else if (lane < k) b -= lcol[k] * zk;
+        }
+      }
+      if (lane < nbe) rhs[o + lane] = b;
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < o; i += nt) {
+      float acc = 0.f;
+#pragma unroll 8
+      for (int c = 0; c < nbe; ++c) acc += G[(o + c) * M + i] * rhs[o + c];
+      x[i] -= acc;
+    }
+    __syncthreads();
+  }
+  const double base = scal[3] / static_cast<double>(M);
+  for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(base + static_cast<double>(rhs[i]));
 }
 
 // Panel: rows of block ib > jb: X <- X L_jj^-T.  One thread per row.
@@ -545,9 +671,10 @@ __global__ void __launch_bounds__(64) k_trsm(float* G, int64_t M, int64_t jb) {
 #pragma unroll
   for (int c = 0; c < kNB; ++c) {
     if (c < n) {
-      float v = x[c];
-      for (int k = 0; k < c; ++k) v -= x[k] * L[c][k];
-      x[c] = v / L[c][c];
+      x[c] = x[c] / L[c][c];
+#pragma unroll
+      for (int q = c + 1; q < kNB; ++q)
+        if (q < n) x[q] -= x[c] * L[q][c];
     }
   }
 #pragma unroll
@@ -755,29 +882,18 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
                                                          f_empty_full, rpc, w.part);
   GS_LAUNCHED();
 
-  if (M <= kSmallM) {
-    // one workgroup: assembly, factorisation, both solves
-    const size_t vec_bytes = static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float));
-    const size_t mat_bytes = static_cast<size_t>(M) * M * sizeof(float);
-    const size_t panel_bytes = static_cast<size_t>(M) * kSB * sizeof(float);
-    const int lds_max = gnnshap::max_lds_bytes();
-    auto fits = [&](const void* fn, size_t bytes) {
-      if (bytes > static_cast<size_t>(lds_max)) return false;
-      if (bytes <= 65536) return true;
-      const bool ok = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                          static_cast<int>(bytes)) == hipSuccess;
+  const size_t small_bytes = small_lds_bytes(M);
+  if (small_bytes <= static_cast<size_t>(gnnshap::max_lds_bytes())) {
+    // one workgroup: assembly, factorisation, both solves, phi
+    bool ok = small_bytes <= 65536;
+    if (!ok) {
+      ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_solve_small), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               static_cast<int>(small_bytes)) == hipSuccess;
       (void)hipGetLastError();
-      return ok;
-    };
-    if (fits(reinterpret_cast<const void*>(&k_solve_small<true>), vec_bytes + mat_bytes)) {
-      k_solve_small<true><<<1, 256, vec_bytes + mat_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full,
-                                                                 w.part, nch, info, phi);
-      GS_LAUNCHED();
-      return GNNSHAP_OK;
     }
-    if (fits(reinterpret_cast<const void*>(&k_solve_small<false>), vec_bytes + panel_bytes)) {
-      k_solve_small<false><<<1, 256, vec_bytes + panel_bytes, s>>>(w.G, M, has_random, alpha, wr, f_empty_full,
-                                                                    w.part, nch, info, phi);
+    if (ok) {
+      k_solve_small<<<1, 256, small_bytes, s>>>(counts, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
+                                                phi);
       GS_LAUNCHED();
       return GNNSHAP_OK;
     }
@@ -809,25 +925,8 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
       GS_LAUNCHED();
     }
   }
-  // L a = rhs (a overwrites x), then L^T psi = a (psi overwrites rhs).
-  for (int64_t jb = 0; jb < nblk; ++jb) {
-    k_trsv_lower<<<1, 64, 0, s>>>(w.G, M, jb, w.rhs, w.x);
-    GS_LAUNCHED();
-    const int64_t rows = M - (jb + 1) * kNB;
-    if (rows > 0) {
-      k_update_lower<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 256)), 256, 0, s>>>(w.G, M, jb, w.x, w.rhs);
-      GS_LAUNCHED();
-    }
-  }
-  for (int64_t jb = nblk - 1; jb >= 0; --jb) {
-    k_trsv_upper<<<1, 64, 0, s>>>(w.G, M, jb, w.x, w.rhs);
-    GS_LAUNCHED();
-    if (jb > 0) {
-      k_update_upper<<<static_cast<unsigned>(gnnshap::ceil_div(jb * kNB, 256)), 256, 0, s>>>(w.G, M, jb, w.rhs, w.x);
-      GS_LAUNCHED();
-    }
-  }
-  k_finish<<<gnnshap::grid_for(M, 256, 1024), 256, 0, s>>>(w.rhs, M, w.scal, phi);
+  // L x = rhs, L^T psi = x, phi = Delta/M + psi (one workgroup)
+  k_trsv_both<<<1, 1024, 0, s>>>(w.G, M, w.rhs, w.x, w.scal, phi);
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END
