@@ -14,16 +14,21 @@
 //   * the random rows share one weight w_r, so their part is 2 w_r P C_R P
 //     with C_R the integer co-occurrence counts of the random representative
 //     rows, computed exactly by popcounts on a bit-transposed copy.
-// Then a blocked right-looking Cholesky (64-wide panels) and two blocked
-// triangular solves.  The right-hand side is accumulated in fp64.
+// Systems whose lower triangle fits in LDS are assembled, factored and solved
+// by one workgroup; larger ones use a blocked right-looking Cholesky over the
+// whole GPU (64-wide panels) and one workgroup for the two triangular solves.
+// Diagonal blocks are factored by one wavefront holding a row per lane in
+// registers; tail blocks are padded with the identity so every inner loop
+// runs without per-lane branches.  The right-hand side is accumulated in fp64.
 #include <cmath>
-#include <vector>
 
 #include "common.h"
 
 namespace {
 
-constexpr int kNB = 64;
+constexpr int kNB = 64;   // panel width, multi-block path
+constexpr int kSB = 32;   // panel width, one-workgroup path
+constexpr int kMaxChunks = 256;
 
 struct Ws {
   gnnshap_class* classes;
@@ -34,9 +39,8 @@ struct Ws {
   double* part;      // nch x M partial right-hand sides
   float* rhs;        // M
   float* x;          // M
+  float* Ld;         // kNB x kNB padded diagonal factor + kNB reciprocal pivots
 };
-
-constexpr int kMaxChunks = 256;
 
 int64_t n_chunks(int64_t half) {
   int64_t c = gnnshap::ceil_div(half, 256);
@@ -57,7 +61,46 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   w.part = c.take<double>(n_chunks(half) * M);
   w.rhs = c.take<float>(M);
   w.x = c.take<float>(M);
+  w.Ld = c.take<float>(kNB * kNB + kNB);
   return w;
+}
+
+__device__ inline float bcast(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// a[lane] without a dynamic register index: unrolled selects.
+template <int NB>
+__device__ inline float lane_entry(const float (&a)[NB]) {
+  const int lane = threadIdx.x & 63;
+  float d = 1.f;
+#pragma unroll
+  for (int c = 0; c < NB; ++c) d = c == lane ? a[c] : d;
+  return d;
+}
+
+// Cholesky of an NB x NB lower block held by one wavefront, row `lane` in
+// a[] (rows and columns past the real block are the identity).  Column k:
+// broadcast the pivot, scale the column, rank-1 update of the later
+// columns.  Entries above each lane's diagonal are left undefined.  The
+// first non-positive pivot (1-based, offset o) goes to *info and is replaced
+// by 1.
+template <int NB>
+__device__ inline void chol_regs(float (&a)[NB], int64_t o, int32_t* info) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    float piv = bcast(a[k], k);
+    if (!(piv > 0.f)) {
+      if (lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
+      piv = 1.f;
+    }
+    // lane k holds the pivot itself: piv / sqrt(piv) = sqrt(piv), so one
+    // scaling serves the diagonal and the column below it
+    a[k] *= 1.0f / sqrtf(piv);
+#pragma unroll
+    for (int j = k + 1; j < NB; ++j) a[j] -= a[k] * bcast(a[k], j);
+  }
 }
 
 // T[rb, j]: transpose 64 rows x 64 players with ballots.  One wave per (rb, word).
@@ -267,100 +310,9 @@ __global__ void __launch_bounds__(1024) k_rhs_finish(const double* __restrict__ 
   }
 }
 
-__global__ void k_zero_info(int32_t* info) { *info = 0; }
-
-__device__ inline float bcast(float v, int lane) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
-}
-
-// Cholesky of the nbe x nbe diagonal block at (o, o) by one wavefront: lane r
-// holds row o + r in registers; column k's pivot and entries are broadcast
-// with readlane.  Records the first non-positive pivot (1-based) in *info and
-// continues with a unit pivot.
-template <int NB>
-__device__ inline void chol_diag_wave(float* A, int64_t lda, int64_t o, int nbe, int32_t* info) {
-  const int lane = threadIdx.x & 63;
-  const bool own = lane < nbe;
-  float a[NB];
-#pragma unroll
-  for (int c = 0; c < NB; ++c) a[c] = (own && c <= lane && c < nbe) ? A[(o + lane) * lda + o + c] : 0.f;
-#pragma unroll
-  for (int k = 0; k < NB; ++k) {
-    if (k < nbe) {
-      float piv = bcast(a[k], k);
-      if (!(piv > 0.f)) {
-        if (lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
-        piv = 1.f;
-      }
-      const float lkk = sqrtf(piv);
-      if (lane == k) a[k] = lkk;
-      else if (lane > k) a[k] = a[k] / lkk;
-#pragma unroll
-      for (int j = k + 1; j < NB; ++j) {
-        if (j < nbe) {
-          const float ljk = bcast(a[k], j);
-          if (lane >= j) a[j] -= a[k] * ljk;
-        }
-      }
-    }
-  }
-  if (own) {
-#pragma unroll
-    for (int c = 0; c < NB; ++c)
-      if (c < nbe) A[(o + lane) * lda + o + c] = c <= lane ? a[c] : 0.f;
-  }
-}
-
-// Cholesky of diagonal block jb of the multi-block path (one wavefront).
-__global__ void __launch_bounds__(64) k_potrf(float* G, int64_t M, int64_t jb, int32_t* info) {
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  chol_diag_wave<kNB>(G, M, o, n, info);
-}
-
-// Small systems in one workgroup, the lower triangle of G~ packed in LDS
-// (row i starts at i(i+1)/2): assemble G~ from the counts and the right-hand
-// side from the partial sums, factor (32-wide blocks: one wavefront factors
-// the diagonal block in registers, the panel rows are solved right-looking,
-// the trailing triangle is updated in 4x4 register tiles), then the forward
-// and backward solves and phi.
-constexpr int kSB = 32;
-
+// One-workgroup path: the lower triangle of G~ packed in LDS (row i at
+// i(i+1)/2).
 __device__ inline int64_t tri(int64_t i, int64_t j) { return ((i * (i + 1)) >> 1) + j; }
-
-// Cholesky of the diagonal block at (o, o) of a packed lower triangle.
-__device__ inline void chol_diag_wave_packed(float* A, int64_t o, int nbe, int32_t* info) {
-  const int lane = threadIdx.x & 63;
-  const bool own = lane < nbe;
-  float a[kSB];
-#pragma unroll
-  for (int c = 0; c < kSB; ++c) a[c] = (own && c <= lane && c < nbe) ? A[tri(o + lane, o + c)] : 0.f;
-#pragma unroll
-  for (int k = 0; k < kSB; ++k) {
-    if (k < nbe) {
-      float piv = bcast(a[k], k);
-      if (!(piv > 0.f)) {
-        if (lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
-        piv = 1.f;
-      }
-      const float lkk = sqrtf(piv);
-      if (lane == k) a[k] = lkk;
-      else if (lane > k) a[k] = a[k] / lkk;
-#pragma unroll
-      for (int j = k + 1; j < kSB; ++j) {
-        if (j < nbe) {
-          const float ljk = bcast(a[k], j);
-          if (lane >= j) a[j] -= a[k] * ljk;
-        }
-      }
-    }
-  }
-  if (own) {
-#pragma unroll
-    for (int c = 0; c < kSB; ++c)
-      if (c < nbe && c <= lane) A[tri(o + lane, o + c)] = a[c];
-  }
-}
 
 size_t small_lds_bytes(int64_t M) {
   return static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float)) +
@@ -376,6 +328,9 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   float* rhs = reinterpret_cast<float*>(dv + M);     // M
   float* xv = rhs + M;                               // M
   float* A = xv + M;                                 // packed lower triangle
+  __shared__ float Blk[kSB][kSB + 1];                // staging of the current diagonal block
+  __shared__ float Ld[kSB][kSB + 1];                 // padded diagonal factor of the current block
+  __shared__ float rd[kSB];                          // its reciprocal pivots
   __shared__ double red[2][4];
   __shared__ double sc[4];
   const int tid = threadIdx.x;
@@ -384,7 +339,7 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   const double Md = static_cast<double>(M);
   if (tid == 0) *info = 0;
 
-  // 1. counts -> LDS (lower part, exact as floats below 2^24), row sums, trace
+  // 1. counts -> LDS (lower part; exact as floats below 2^24), row sums, trace
   double trl = 0.0, sgl = 0.0;
   if (has_random) {
     for (int64_t i = wave; i < M; i += nt / 64) {
@@ -394,14 +349,15 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           const int64_t j = j0 + q * 64 + lane;
-          v[q] = j < M ? C[i * M + j] : 0;
+          v[q] = C[i * M + (j < M ? j : 0)];
+          v[q] = j < M ? v[q] : 0;
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           const int64_t j = j0 + q * 64 + lane;
           sum += v[q];
           if (j <= i) A[tri(i, j)] = static_cast<float>(v[q]);
-          if (j == i) trl += static_cast<double>(v[q]);
+          trl += j == i ? static_cast<double>(v[q]) : 0.0;
         }
       }
       for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
@@ -433,7 +389,6 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   const double sigma = sc[0], gamma = sc[1], delta = sc[2];
 
   // 2. G~ = alpha P + 2 wr P C P + gamma 11^T/M, lower triangle in place
-  const int64_t ntri = (M * (M + 1)) / 2;
   for (int64_t i = 0, base = 0; i < M; base += i + 1, ++i) {
     for (int64_t j = tid; j <= i; j += nt) {
       double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
@@ -441,7 +396,6 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
       A[base + j] = static_cast<float>(v);
     }
   }
-  (void)ntri;
   __syncthreads();
 
   // 3. right-hand side P r from the partial sums (8 loads in flight per thread)
@@ -451,9 +405,9 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
     for (int64_t c0 = 0; c0 < nch; c0 += 8) {
       double t[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) t[q] = c0 + q < nch ? part[(c0 + q) * M + j] : 0.0;
+      for (int q = 0; q < 8; ++q) t[q] = part[(c0 + q < nch ? c0 + q : 0) * M + j];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v += t[q];
+      for (int q = 0; q < 8; ++q) v += c0 + q < nch ? t[q] : 0.0;
     }
     dv[j] = v;
     sl += v;
@@ -470,30 +424,51 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   for (int64_t j = tid; j < M; j += nt) rhs[j] = static_cast<float>(dv[j] - sc[3]);
   __syncthreads();
 
-  // 4. Cholesky
+  // 4. Cholesky, 32-wide blocks
   for (int64_t o = 0; o < M; o += kSB) {
     const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
-    if (wave == 0) chol_diag_wave_packed(A, o, nbe, info);
+    for (int t = tid; t < kSB * kSB; t += nt) {      // padded block: identity past nbe
+      const int r = t / kSB, c = t % kSB;
+      Blk[r][c] = (r < nbe && c <= r) ? A[tri(o + r, o + c)] : (r == c ? 1.f : 0.f);
+    }
     __syncthreads();
+    if (wave == 0) {
+      float a[kSB];
+#pragma unroll
+      for (int c = 0; c < kSB; ++c) a[c] = Blk[lane & (kSB - 1)][c];
+      chol_regs<kSB>(a, o, info);
+      if (lane < kSB) {
+#pragma unroll
+        for (int c = 0; c < kSB; ++c) Blk[lane][c] = a[c];
+      }
+    }
+    __syncthreads();
+    for (int t = tid; t < kSB * kSB; t += nt) {
+      const int r = t / kSB, c = t % kSB;
+      const float v = c <= r ? Blk[r][c] : 0.f;
+      Ld[r][c] = v;
+      if (c == r) rd[r] = 1.0f / v;
+      if (r < nbe && c <= r) A[tri(o + r, o + c)] = v;
+    }
+    __syncthreads();
+    // rows below exist only when the diagonal block is full (nbe == kSB)
     const int64_t r0 = o + nbe;
     const int64_t T = M - r0;
     for (int64_t i = r0 + tid; i < M; i += nt) {
       float x[kSB];
       const int64_t bi = tri(i, o);
 #pragma unroll
-      for (int c = 0; c < kSB; ++c) x[c] = c < nbe ? A[bi + c] : 0.f;
+      for (int c = 0; c < kSB; ++c) x[c] = A[bi + c];
 #pragma unroll
       for (int c = 0; c < kSB; ++c) {
-        if (c < nbe) {
-          x[c] = x[c] / A[tri(o + c, o + c)];
+        x[c] *= rd[c];
 #pragma unroll
-          for (int q = c + 1; q < kSB; ++q)
-            if (q < nbe) x[q] -= x[c] * A[tri(o + q, o + c)];
-        }
+        for (int q = c + 1; q < kSB; ++q) x[q] -= x[c] * Ld[q][c];
+        __builtin_amdgcn_sched_barrier(0);   // column by column: keeps register pressure low
       }
 #pragma unroll
       for (int c = 0; c < kSB; ++c)
-        if (c < nbe) A[bi + c] = x[c];
+        A[bi + c] = x[c];
     }
     __syncthreads();
     const int64_t T4 = (T + 3) / 4;
@@ -502,18 +477,21 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
       if (J > I) continue;
       float acc[4][4] = {};
       int64_t pi[4], pj[4];
+      bool oi[4], oj[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int64_t ri = r0 + 4 * I + q, rj = r0 + 4 * J + q;
-        pi[q] = ri < M ? tri(ri, o) : -1;
-        pj[q] = rj < M ? tri(rj, o) : -1;
+        oi[q] = ri < M;
+        oj[q] = rj < M;
+        pi[q] = oi[q] ? tri(ri, o) : 0;
+        pj[q] = oj[q] ? tri(rj, o) : 0;
       }
       for (int c = 0; c < nbe; ++c) {
         float pa[4], pb[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          pa[q] = pi[q] >= 0 ? A[pi[q] + c] : 0.f;
-          pb[q] = pj[q] >= 0 ? A[pj[q] + c] : 0.f;
+          pa[q] = oi[q] ? A[pi[q] + c] : 0.f;
+          pb[q] = oj[q] ? A[pj[q] + c] : 0.f;
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q)
@@ -534,20 +512,26 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
     __syncthreads();
   }
 
-  // 5. forward substitution L x = rhs
+  // 5. forward substitution L x = rhs (one wavefront per diagonal block)
   for (int64_t o = 0; o < M; o += kSB) {
     const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
+    // strictly lower part of the diagonal block and its reciprocal pivots
+    for (int t = tid; t < kSB * kSB; t += nt) {
+      const int r = t / kSB, c = t % kSB;
+      Blk[r][c] = (r < nbe && c < r) ? A[tri(o + r, o + c)] : 0.f;
+      if (c == r) rd[r] = r < nbe ? 1.0f / A[tri(o + r, o + r)] : 1.f;
+    }
+    __syncthreads();
     if (wave == 0) {
+      // b_k is final once the columns before k are applied: x_k = b_k / L_kk
+      const int rl = lane & (kSB - 1);
       float b = lane < nbe ? rhs[o + lane] : 0.f;
+      float lr[kSB];
 #pragma unroll
-      for (int k = 0; k < kSB; ++k) {
-        if (k < nbe) {
-          const float xk = bcast(b, k) / A[tri(o + k, o + k)];
-          if (lane == k) b = xk;
-          else if (lane > k && lane < nbe) b -= A[tri(o + lane, o + k)] * xk;
-        }
-      }
-      if (lane < nbe) xv[o + lane] = b;
+      for (int c = 0; c < kSB; ++c) lr[c] = Blk[rl][c];
+#pragma unroll
+      for (int k = 0; k < kSB; ++k) b -= lr[k] * (bcast(b, k) * rd[k]);
+      if (lane < nbe) xv[o + lane] = b * rd[rl];
     }
     __syncthreads();
     for (int64_t i = o + nbe + tid; i < M; i += nt) {
@@ -562,17 +546,22 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   // 6. backward substitution L^T z = x (z overwrites rhs)
   for (int64_t o = ((M - 1) / kSB) * kSB; o >= 0; o -= kSB) {
     const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
+    // Blk[r][k] = L[o+k][o+r] for k > r (the strictly upper part of L_jj^T)
+    for (int t = tid; t < kSB * kSB; t += nt) {
+      const int r = t / kSB, k = t % kSB;
+      Blk[r][k] = (k < nbe && r < k) ? A[tri(o + k, o + r)] : 0.f;
+      if (k == r) rd[r] = r < nbe ? 1.0f / A[tri(o + r, o + r)] : 1.f;
+    }
+    __syncthreads();
     if (wave == 0) {
+      const int rl = lane & (kSB - 1);
       float b = lane < nbe ? xv[o + lane] : 0.f;
+      float lc[kSB];
 #pragma unroll
-      for (int k = kSB - 1; k >= 0; --k) {
-        if (k < nbe) {
-          const float zk = bcast(b, k) / A[tri(o + k, o + k)];
-          if (lane == k) b = zk;
-          else if (lane < k) b -= A[tri(o + k, o + lane)] * zk;
-        }
-      }
-      if (lane < nbe) rhs[o + lane] = b;
+      for (int k = 0; k < kSB; ++k) lc[k] = Blk[rl][k];
+#pragma unroll
+      for (int k = kSB - 1; k >= 0; --k) b -= lc[k] * (bcast(b, k) * rd[k]);
+      if (lane < nbe) rhs[o + lane] = b * rd[rl];
     }
     __syncthreads();
     for (int64_t i = tid; i < o; i += nt) {
@@ -587,99 +576,58 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rhs[i]));
 }
 
-// Both triangular solves and phi in one workgroup, for a factor in global
-// memory (multi-block path): forward L x = rhs, backward L^T z = x.
-__global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G, int64_t M,
-                                                    float* __restrict__ rhs, float* __restrict__ x,
-                                                    const double* __restrict__ scal, float* __restrict__ phi) {
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  for (int64_t o = 0; o < M; o += 64) {
-    const int nbe = static_cast<int>(M - o < 64 ? M - o : 64);
-    if (wave == 0) {
-      float b = lane < nbe ? rhs[o + lane] : 0.f;
-      float lrow[64];
-#pragma unroll
-      for (int k = 0; k < 64; ++k) lrow[k] = (lane < nbe && k < nbe && k < lane) ? G[(o + lane) * M + o + k] : 0.f;
-#pragma unroll
-      for (int k = 0; k < 64; ++k) {
-        if (k < nbe) {
-          const float xk = bcast(b, k) / G[(o + k) * M + o + k];
-          if (lane == k) b = xk;
-          else if (lane > k) b -= lrow[k] * xk;
-        }
-      }
-      if (lane < nbe) x[o + lane] = b;
-    }
-    __syncthreads();
-    for (int64_t i = o + nbe + tid; i < M; i += nt) {
-      float acc = 0.f;
-      const float* row = G + i * M + o;
-#pragma unroll 8
-      for (int c = 0; c < nbe; ++c) acc += row[c] * x[o + c];
-      rhs[i] -= acc;
-    }
-    __syncthreads();
-  }
-  for (int64_t o = ((M - 1) / 64) * 64; o >= 0; o -= 64) {
-    const int nbe = static_cast<int>(M - o < 64 ? M - o : 64);
-    if (wave == 0) {
-      float b = lane < nbe ? x[o + lane] : 0.f;
-      float lcol[64];
-#pragma unroll
-      for (int k = 0; k < 64; ++k) lcol[k] = (lane < nbe && k < nbe && k > lane) ? G[(o + k) * M + o + lane] : 0.f;
-#pragma unroll
-      for (int k = 63; k >= 0; --k) {
-        if (k < nbe) {
-          const float zk = bcast(b, k) / G[(o + k) * M + o + k];
-          if (lane == k) b = zk;
-          else if (lane < k) b -= lcol[k] * zk;
-        }
-      }
-      if (lane < nbe) rhs[o + lane] = b;
-    }
-    __syncthreads();
-    for (int64_t i = tid; i < o; i += nt) {
-      float acc = 0.f;
-#pragma unroll 8
-      for (int c = 0; c < nbe; ++c) acc += G[(o + c) * M + i] * rhs[o + c];
-      x[i] -= acc;
-    }
-    __syncthreads();
-  }
-  const double base = scal[3] / static_cast<double>(M);
-  for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(base + static_cast<double>(rhs[i]));
-}
+__global__ void k_zero_info(int32_t* info) { *info = 0; }
 
-// Panel: rows of block ib > jb: X <- X L_jj^-T.  One thread per row.
-__global__ void __launch_bounds__(64) k_trsm(float* G, int64_t M, int64_t jb) {
-  __shared__ float L[kNB][kNB + 1];
+// Multi-block path, diagonal block jb: one wavefront factors it in registers,
+// writes L_jj back (zeros above the diagonal) and the padded factor with its
+// reciprocal pivots to Ld for the panel kernel.
+__global__ void __launch_bounds__(64) k_potrf(float* G, int64_t M, int64_t jb, int32_t* info, float* Ld) {
   const int64_t o = jb * kNB;
   const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  const int tid = threadIdx.x;
-  for (int t = tid; t < n * n; t += 64) {
-    const int i = t / n, j = t % n;
-    L[i][j] = G[(o + i) * M + o + j];
+  const int lane = threadIdx.x;
+  const bool own = lane < n;
+  float a[kNB];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) {
+    const bool real = own && c < n && c <= lane;
+    const float v = G[real ? (o + lane) * M + o + c : 0];
+    a[c] = real ? v : (c == lane ? 1.f : 0.f);
   }
+  chol_regs<kNB>(a, o, info);
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) Ld[lane * kNB + c] = c <= lane ? a[c] : 0.f;
+  Ld[kNB * kNB + lane] = 1.0f / lane_entry(a);
+  if (own) {
+#pragma unroll
+    for (int c = 0; c < kNB; ++c)
+      if (c < n) G[(o + lane) * M + o + c] = c <= lane ? a[c] : 0.f;
+  }
+}
+
+// Panel: rows below block jb, X <- X L_jj^-T, one thread per row, right-looking.
+__global__ void __launch_bounds__(256) k_trsm(float* G, int64_t M, int64_t jb, const float* __restrict__ Ld) {
+  __shared__ float L[kNB][kNB + 1];
+  __shared__ float rd[kNB];
+  const int64_t o = jb * kNB;
+  const int tid = threadIdx.x;
+  for (int t = tid; t < kNB * kNB; t += 256) L[t / kNB][t % kNB] = Ld[t];
+  if (tid < kNB) rd[tid] = Ld[kNB * kNB + tid];
   __syncthreads();
-  const int64_t r = o + n + static_cast<int64_t>(blockIdx.x) * 64 + tid;
+  const int64_t r = o + kNB + static_cast<int64_t>(blockIdx.x) * 256 + tid;
   if (r >= M) return;
   float x[kNB];
   float* row = G + r * M + o;
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) x[c] = c < n ? row[c] : 0.f;
+  for (int c = 0; c < kNB; ++c) x[c] = row[c];
 #pragma unroll
   for (int c = 0; c < kNB; ++c) {
-    if (c < n) {
-      x[c] = x[c] / L[c][c];
+    x[c] *= rd[c];
 #pragma unroll
-      for (int q = c + 1; q < kNB; ++q)
-        if (q < n) x[q] -= x[c] * L[q][c];
-    }
+    for (int q = c + 1; q < kNB; ++q) x[q] -= x[c] * L[q][c];
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
-  for (int c = 0; c < kNB; ++c)
-    if (c < n) row[c] = x[c];
+  for (int c = 0; c < kNB; ++c) row[c] = x[c];
 }
 
 // Trailing update of tile (ib, kb), jb < kb <= ib: A_ib,kb -= L_ib,jb L_kb,jb^T.
@@ -731,68 +679,69 @@ __global__ void __launch_bounds__(256) k_syrk(float* G, int64_t M, int64_t jb) {
   }
 }
 
-// Forward substitution on diagonal block jb: x_j = L_jj^-1 rhs_j (one wave).
-__global__ void __launch_bounds__(64) k_trsv_lower(const float* __restrict__ G, int64_t M, int64_t jb,
-                                                   const float* __restrict__ rhs, float* __restrict__ x) {
-  __shared__ float xs[kNB];
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  const int lane = threadIdx.x;
-  for (int c = 0; c < n; ++c) {
-    float v = lane < c ? G[(o + c) * M + o + lane] * xs[lane] : 0.f;
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if (lane == 0) xs[c] = (rhs[o + c] - v) / G[(o + c) * M + o + c];
+// Multi-block path: both triangular solves and phi in one workgroup.
+__global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G, int64_t M,
+                                                    float* __restrict__ rhs, float* __restrict__ x,
+                                                    const double* __restrict__ scal, float* __restrict__ phi) {
+  __shared__ float Blk[kNB][kNB + 1];
+  __shared__ float rd[kNB];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int64_t o = 0; o < M; o += kNB) {
+    const int nbe = static_cast<int>(M - o < kNB ? M - o : kNB);
+    for (int t = tid; t < kNB * kNB; t += nt) {      // strictly lower part of L_jj
+      const int r = t / kNB, c = t % kNB;
+      Blk[r][c] = (r < nbe && c < r) ? G[(o + r) * M + o + c] : 0.f;
+      if (c == r) rd[r] = r < nbe ? 1.0f / G[(o + r) * M + o + r] : 1.f;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      float b = lane < nbe ? rhs[o + lane] : 0.f;
+      float lr[kNB];
+#pragma unroll
+      for (int c = 0; c < kNB; ++c) lr[c] = Blk[lane][c];
+#pragma unroll
+      for (int k = 0; k < kNB; ++k) b -= lr[k] * (bcast(b, k) * rd[k]);
+      if (lane < nbe) x[o + lane] = b * rd[lane];
+    }
+    __syncthreads();
+    for (int64_t i = o + nbe + tid; i < M; i += nt) {
+      float acc = 0.f;
+      const float* row = G + i * M + o;
+#pragma unroll 8
+      for (int c = 0; c < nbe; ++c) acc += row[c] * x[o + c];
+      rhs[i] -= acc;
+    }
     __syncthreads();
   }
-  if (lane < n) x[o + lane] = xs[lane];
-}
-
-// rhs[i] -= sum_{k in block jb} L[i, k] x[k] for rows i after block jb.
-__global__ void __launch_bounds__(256) k_update_lower(const float* __restrict__ G, int64_t M, int64_t jb,
-                                                      const float* __restrict__ x, float* __restrict__ rhs) {
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  const int64_t i = o + n + static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= M) return;
-  float v = 0.f;
-  for (int k = 0; k < n; ++k) v += G[i * M + o + k] * x[o + k];
-  rhs[i] -= v;
-}
-
-// Backward substitution on diagonal block jb: x_j = L_jj^-T a_j (one wave).
-__global__ void __launch_bounds__(64) k_trsv_upper(const float* __restrict__ G, int64_t M, int64_t jb,
-                                                   const float* __restrict__ a, float* __restrict__ x) {
-  __shared__ float xs[kNB];
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  const int lane = threadIdx.x;
-  for (int c = n - 1; c >= 0; --c) {
-    float v = (lane > c && lane < n) ? G[(o + lane) * M + o + c] * xs[lane] : 0.f;
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if (lane == 0) xs[c] = (a[o + c] - v) / G[(o + c) * M + o + c];
+  for (int64_t o = ((M - 1) / kNB) * kNB; o >= 0; o -= kNB) {
+    const int nbe = static_cast<int>(M - o < kNB ? M - o : kNB);
+    for (int t = tid; t < kNB * kNB; t += nt) {      // Blk[r][k] = L[o+k][o+r], k > r
+      const int r = t / kNB, k = t % kNB;
+      Blk[r][k] = (k < nbe && r < k) ? G[(o + k) * M + o + r] : 0.f;
+      if (k == r) rd[r] = r < nbe ? 1.0f / G[(o + r) * M + o + r] : 1.f;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      float b = lane < nbe ? x[o + lane] : 0.f;
+      float lc[kNB];
+#pragma unroll
+      for (int k = 0; k < kNB; ++k) lc[k] = Blk[lane][k];
+#pragma unroll
+      for (int k = kNB - 1; k >= 0; --k) b -= lc[k] * (bcast(b, k) * rd[k]);
+      if (lane < nbe) rhs[o + lane] = b * rd[lane];
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < o; i += nt) {
+      float acc = 0.f;
+#pragma unroll 8
+      for (int c = 0; c < nbe; ++c) acc += G[(o + c) * M + i] * rhs[o + c];
+      x[i] -= acc;
+    }
     __syncthreads();
   }
-  if (lane < n) x[o + lane] = xs[lane];
-}
-
-// a[i] -= sum_{k in block jb} L[k, i] x[k] for rows i before block jb.
-__global__ void __launch_bounds__(256) k_update_upper(const float* __restrict__ G, int64_t M, int64_t jb,
-                                                      const float* __restrict__ x, float* __restrict__ a) {
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= o) return;
-  float v = 0.f;
-  for (int k = 0; k < n; ++k) v += G[(o + k) * M + i] * x[o + k];
-  a[i] -= v;
-}
-
-__global__ void k_finish(const float* __restrict__ x, int64_t M, const double* __restrict__ scal,
-                         float* __restrict__ phi) {
   const double base = scal[3] / static_cast<double>(M);
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < M;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    phi[i] = static_cast<float>(base + static_cast<double>(x[i]));
+  for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(base + static_cast<double>(rhs[i]));
 }
 
 int check_plan(const gnnshap_sample_plan* p, const gnnshap_class* classes) {
@@ -884,7 +833,6 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
 
   const size_t small_bytes = small_lds_bytes(M);
   if (small_bytes <= static_cast<size_t>(gnnshap::max_lds_bytes())) {
-    // one workgroup: assembly, factorisation, both solves, phi
     bool ok = small_bytes <= 65536;
     if (!ok) {
       ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_solve_small), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -911,21 +859,19 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   GS_LAUNCHED();
   k_rhs_finish<<<1, 1024, 0, s>>>(w.part, nch, M, w.rhs, w.scal);
   GS_LAUNCHED();
-  // Cholesky G~ = L L^T.
   const int64_t nblk = gnnshap::ceil_div(M, kNB);
   for (int64_t jb = 0; jb < nblk; ++jb) {
-    k_potrf<<<1, 64, 0, s>>>(w.G, M, jb, info);
+    k_potrf<<<1, 64, 0, s>>>(w.G, M, jb, info, w.Ld);
     GS_LAUNCHED();
     const int64_t rest = nblk - jb - 1;
     if (rest > 0) {
       const int64_t rows = M - (jb + 1) * kNB;
-      k_trsm<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 64)), 64, 0, s>>>(w.G, M, jb);
+      k_trsm<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 256)), 256, 0, s>>>(w.G, M, jb, w.Ld);
       GS_LAUNCHED();
       k_syrk<<<dim3(static_cast<unsigned>(rest), static_cast<unsigned>(rest)), 256, 0, s>>>(w.G, M, jb);
       GS_LAUNCHED();
     }
   }
-  // L x = rhs, L^T psi = x, phi = Delta/M + psi (one workgroup)
   k_trsv_both<<<1, 1024, 0, s>>>(w.G, M, w.rhs, w.x, w.scal, phi);
   GS_LAUNCHED();
   return GNNSHAP_OK;
