@@ -30,6 +30,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--streams", type=int, default=8)
+    ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0,
+                    help="bytes of a plain device copy run before the steps (counter calibration)")
     return ap.parse_args()
 
 
@@ -55,6 +58,82 @@ def cpu_baseline(cfg, seconds):
                       f"extract+sample+fp64 GCN per coalition+lstsq) in {dt:.1f} s, 1 thread"}
 
 
+# Peaks (MI355X): HBM3E 8 TB/s; fp32 VALU without packed-fp32 instructions
+# (this build disables them): 256 CUs x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
+# = 78.6 TFLOP/s; 32-bit integer VALU ops at the same issue rate: 39.3 Tops/s.
+HBM_PEAK_GBS = 8000.0
+VALU_FP32_TFLOPS = 78.6
+VALU_INT_TOPS = 39.3
+SMALL_SOLVE_LDS = 163840      # LDS of one workgroup on gfx950: the one-workgroup solve's limit
+
+
+def _small_solve(M):
+    return M * 16 + (M * (M + 1) // 2) * 4 <= SMALL_SOLVE_LDS
+
+
+def work_model(kernel, results, dims):
+    """Algorithmic work of the timed kernel over one step: (amount, unit, bound, peak).
+
+    k_solve_small  M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
+    k_eval_l2      (k/2) M h useful MACs per target (complement pairs cover every
+                   player-feature product once) + the layer-2 dot products
+    k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
+                   per 64 rows and pair
+    k_sample       k x ceil(M/64) x 8 bytes of masks + 4 k bytes of weights written
+    k_rhs_part     (k/2) x ceil(M/64) x 8 bytes of masks + 4 k bytes of y read
+    """
+    h = dims[1]
+    tot = 0.0
+    for r in results:
+        M, k = r.plan.num_players, r.plan.num_rows
+        wpr = r.plan.words_per_row
+        kr = k // 2 - r.plan.random_begin
+        if kernel == "k_solve_small":
+            if _small_solve(M):
+                tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
+        elif kernel == "k_eval_l2":
+            n1 = r.sub.sg.hop_ptr[2]
+            tot += 2.0 * ((k / 2.0) * M * h + k * n1 * h)
+        elif kernel == "k_gram":
+            tot += (kr / 64.0) * M * (M + 1) / 2.0
+        elif kernel == "k_sample":
+            tot += k * wpr * 8.0 + 4.0 * k
+        elif kernel == "k_rhs_part":
+            tot += (k / 2.0) * wpr * 8.0 + 4.0 * k
+    if kernel in ("k_sample", "k_rhs_part"):
+        return tot, "GB/s", "hbm", HBM_PEAK_GBS
+    if kernel == "k_gram":
+        return tot, "Tops/s", "alu", VALU_INT_TOPS
+    return tot, "TFLOP/s", "alu", VALU_FP32_TFLOPS
+
+
+CANDIDATES = ["k_solve_small", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"]
+
+
+def roofline(step, lib, dims):
+    """Times each candidate kernel with HIP events over one step, picks the
+    one with the largest total and relates its algorithmic work to its
+    average launch duration."""
+    import torch
+    best = None
+    for name in CANDIDATES:
+        lib.gnnshap_timing_begin(name)
+        _, res = step()
+        torch.cuda.synchronize()
+        ms, n = lib.gnnshap_timing_end()
+        if n and (best is None or ms > best[1]):
+            best = (name, ms, n, res)
+    name, ms, n, res = best
+    amount, unit, bound, peak = work_model(name, res, dims)
+    avg_s = ms / 1e3 / n
+    per_launch = amount / n
+    scale = 1e9 if unit == "GB/s" else 1e12
+    achieved = per_launch / avg_s / scale
+    return {"kernel": name, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+            "frac": achieved / peak, "traffic": None, "launches": n, "avg_launch_us": 1e3 * ms / n,
+            "work_per_launch": per_launch}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -75,6 +154,15 @@ def main():
         ex.prepare()                 # X W_1 once per step, shared by every target
         res = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=args.streams)
         return sum(r.plan.num_rows for r in res), res
+
+    if args.copy_probe:
+        # a plain device copy of known size, for calibrating HBM byte counters
+        n = args.copy_probe // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
     for _ in range(args.warmup):
         step()
@@ -118,6 +206,9 @@ def main():
         "roofline": None,
         "cpu_baseline": None,
     }
+    if not args.no_roofline:
+        from paper_2401_04829_amd import _lib
+        out["roofline"] = roofline(step, _lib, cfg["dims"])
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out))

@@ -239,6 +239,22 @@ int gnnshap_solve_wls(const gnnshap_sample_plan* plan,
                       const float* y, const float* f_empty_full, float* phi,
                       int32_t* info, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Diagnostics: HIP-event timing of one kernel.                             */
+/* ------------------------------------------------------------------------ */
+
+/* Arms timing for the kernels whose name starts with `kernel_name` (e.g.
+ * "k_solve_small", "k_eval_l2"): every later launch of such a kernel, from
+ * any entry point, is bracketed by two HIP events recorded on the launch's
+ * own stream.  EINVAL if the name is empty or timing is already armed. */
+int gnnshap_timing_begin(const char* kernel_name);
+
+/* Disarms timing, waits for the recorded events and returns the summed
+ * kernel time in milliseconds and the number of timed launches.  Timing
+ * adds two event records per timed launch; not for concurrent use from
+ * several host threads. */
+int gnnshap_timing_end(double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -64,6 +64,8 @@ _SIGNATURES = {
     "gnnshap_solve_workspace": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(ctypes.c_size_t)]),
     "gnnshap_solve_wls": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(gnnshap_class), c_vp, c_vp, c_vp, c_vp,
                                          c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_timing_begin": (ctypes.c_int, [ctypes.c_char_p]),
+    "gnnshap_timing_end": (ctypes.c_int, [_P(ctypes.c_double), _P(c_i64)]),
 }
 
 _lib = None
@@ -162,6 +164,17 @@ def gnnshap_solve_workspace(plan):
     n = ctypes.c_size_t()
     check(load().gnnshap_solve_workspace(ctypes.byref(plan), ctypes.byref(n)), "solve_workspace")
     return n.value
+
+
+def gnnshap_timing_begin(kernel_name):
+    check(load().gnnshap_timing_begin(kernel_name.encode()), "timing_begin")
+
+
+def gnnshap_timing_end():
+    """Returns (total milliseconds, number of timed launches)."""
+    ms, n = ctypes.c_double(), c_i64()
+    check(load().gnnshap_timing_end(ctypes.byref(ms), ctypes.byref(n)), "timing_end")
+    return ms.value, n.value
 
 
 def gnnshap_solve_wls(plan, classes, masks_ptr, y_ptr, fef_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):

@@ -40,6 +40,21 @@ inline unsigned grid_for(int64_t items, int block, int64_t cap = 8192) {
   return static_cast<unsigned>(g);
 }
 
+// Brackets one kernel launch with two HIP events on the launch's stream when
+// gnnshap_timing_begin() armed a name that prefixes `name`; inert otherwise.
+class KernelTimer {
+ public:
+  KernelTimer(const char* name, hipStream_t s);
+  ~KernelTimer();
+  KernelTimer(const KernelTimer&) = delete;
+  KernelTimer& operator=(const KernelTimer&) = delete;
+
+ private:
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+  hipEvent_t stop_ = nullptr;
+};
+
 // Largest dynamic LDS allocation one workgroup may request on the current device.
 inline int max_lds_bytes() {
   int dev = 0;
@@ -60,6 +75,9 @@ inline int max_lds_bytes() {
   } while (0)
 
 #define GS_LAUNCHED() GS_HIP(hipGetLastError())
+
+// Scope guard timing the launch(es) in the enclosing block.
+#define GS_TIMED(name, stream) ::gnnshap::KernelTimer gs_kernel_timer_(name, stream)
 
 #define GS_TRY_BEGIN try {
 #define GS_TRY_END                                                               \

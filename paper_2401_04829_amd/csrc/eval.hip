@@ -600,6 +600,7 @@ int launch_gemm(hipStream_t s, const float* A, int64_t lda, const int32_t* arow,
                 int64_t dyn_mult = 0) {
   if (rows <= 0) return GNNSHAP_OK;
   dim3 grid(static_cast<unsigned>(gnnshap::ceil_div(rows, 64)), static_cast<unsigned>(gnnshap::ceil_div(N, 64)));
+  GS_TIMED("k_gemm", s);
   k_gemm<<<grid, 256, 0, s>>>(A, lda, arow, abias, B, ldb, C, ldc, m0, rows, N, K, dyn, dyn_off,
                               dyn_cap, dyn_mult);
   GS_LAUNCHED();
@@ -618,6 +619,7 @@ int launch_aggregate(hipStream_t s, int h, const uint64_t* masks, int64_t wpr, c
   const int64_t blocks = n_tiles * nd_out * n_slices;
   if (blocks > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "aggregation grid too large");
   const unsigned g = static_cast<unsigned>(blocks);
+  GS_TIMED("k_aggregate", s);
 #define GS_AGG(F)                                                                                  \
   k_aggregate<F><<<g, 256, 0, s>>>(masks, wpr, rows, row_off, cap, dyn, sg->dst_ptr, sg->edge_src, \
                                    sh.n_dst, dinv, Zc, Zb, nd_prev, bias, Hout, nd_out, h, n_tiles, \
@@ -668,6 +670,7 @@ int launch_fused_l2(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn
   k_eval_l2<F><<<g, 256, lds, s>>>(masks, sh.wpr, rows, row_off, cap, dyn, sg->dst_ptr, sg->edge_src,      \
                                    sh.n_dst, sh.nd[1], w.Zc[1], b1, m->W[1], b2, h, C, w.ctl, all_classes, \
                                    tbr, y_rows, w.sp_y)
+  GS_TIMED("k_eval_l2", s);
   switch (fpt) {
     case 1: GS_L2(1); break;
     case 2: GS_L2(2); break;

@@ -266,7 +266,10 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
   k_init<<<1, 1, 0, s>>>(w.mark, w.queue, w.counters, target);
   GS_LAUNCHED();
   for (int l = 0; l < hops; ++l) {
-    k_expand<<<512, 256, 0, s>>>(g->indptr, g->indices, w.mark, w.queue, w.counters, l);
+    {
+      GS_TIMED("k_expand", s);
+      k_expand<<<512, 256, 0, s>>>(g->indptr, g->indices, w.mark, w.queue, w.counters, l);
+    }
     GS_LAUNCHED();
   }
   k_count_levels<<<static_cast<unsigned>(nblk), 256, 0, s>>>(w.mark, n, w.bcount, levels);

@@ -221,10 +221,13 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
   const int64_t wpr = plan->words_per_row;
   const size_t lds = static_cast<size_t>(3 * 2 * wpr) * sizeof(uint32_t);
   const unsigned grid = static_cast<unsigned>(half < 65536 ? half : 65536);
-  k_sample<<<grid, 64, lds, s>>>(w.classes, plan->num_classes, half, M, wpr,
-                                 static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
-                                 static_cast<uint32_t>(plan->stream_id),
-                                 static_cast<uint32_t>(plan->stream_id >> 32), masks, weights);
+  {
+    GS_TIMED("k_sample", s);
+    k_sample<<<grid, 64, lds, s>>>(w.classes, plan->num_classes, half, M, wpr,
+                                   static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
+                                   static_cast<uint32_t>(plan->stream_id),
+                                   static_cast<uint32_t>(plan->stream_id >> 32), masks, weights);
+  }
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END

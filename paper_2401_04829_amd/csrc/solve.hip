@@ -819,16 +819,25 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   int32_t* counts = reinterpret_cast<int32_t*>(w.G);
   if (has_random) {
     const int64_t nrb = gnnshap::ceil_div(kr, 64);
-    k_transpose<<<dim3(static_cast<unsigned>(nrb), static_cast<unsigned>(wpr)), 64, 0, s>>>(masks, wpr, rb0, kr, M, w.T);
+    {
+      GS_TIMED("k_transpose", s);
+      k_transpose<<<dim3(static_cast<unsigned>(nrb), static_cast<unsigned>(wpr)), 64, 0, s>>>(masks, wpr, rb0, kr, M, w.T);
+    }
     GS_LAUNCHED();
     const unsigned nb = static_cast<unsigned>(gnnshap::ceil_div(M, 64));
-    k_gram<<<dim3(nb, nb), 256, 0, s>>>(w.T, nrb, M, counts);
+    {
+      GS_TIMED("k_gram", s);
+      k_gram<<<dim3(nb, nb), 256, 0, s>>>(w.T, nrb, M, counts);
+    }
     GS_LAUNCHED();
   }
   const int64_t nch = n_chunks(half);
   const int64_t rpc = gnnshap::ceil_div(half, nch);
-  k_rhs_part<<<static_cast<unsigned>(nch), 256, 0, s>>>(masks, wpr, half, M, y, w.classes, plan->num_classes,
-                                                         f_empty_full, rpc, w.part);
+  {
+    GS_TIMED("k_rhs_part", s);
+    k_rhs_part<<<static_cast<unsigned>(nch), 256, 0, s>>>(masks, wpr, half, M, y, w.classes, plan->num_classes,
+                                                           f_empty_full, rpc, w.part);
+  }
   GS_LAUNCHED();
 
   const size_t small_bytes = small_lds_bytes(M);
@@ -840,8 +849,11 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
       (void)hipGetLastError();
     }
     if (ok) {
-      k_solve_small<<<1, 256, small_bytes, s>>>(counts, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
-                                                phi);
+      {
+        GS_TIMED("k_solve_small", s);
+        k_solve_small<<<1, 256, small_bytes, s>>>(counts, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
+                                                  phi);
+      }
       GS_LAUNCHED();
       return GNNSHAP_OK;
     }
@@ -861,18 +873,30 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   GS_LAUNCHED();
   const int64_t nblk = gnnshap::ceil_div(M, kNB);
   for (int64_t jb = 0; jb < nblk; ++jb) {
-    k_potrf<<<1, 64, 0, s>>>(w.G, M, jb, info, w.Ld);
+    {
+      GS_TIMED("k_potrf", s);
+      k_potrf<<<1, 64, 0, s>>>(w.G, M, jb, info, w.Ld);
+    }
     GS_LAUNCHED();
     const int64_t rest = nblk - jb - 1;
     if (rest > 0) {
       const int64_t rows = M - (jb + 1) * kNB;
-      k_trsm<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 256)), 256, 0, s>>>(w.G, M, jb, w.Ld);
+      {
+        GS_TIMED("k_trsm", s);
+        k_trsm<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 256)), 256, 0, s>>>(w.G, M, jb, w.Ld);
+      }
       GS_LAUNCHED();
-      k_syrk<<<dim3(static_cast<unsigned>(rest), static_cast<unsigned>(rest)), 256, 0, s>>>(w.G, M, jb);
+      {
+        GS_TIMED("k_syrk", s);
+        k_syrk<<<dim3(static_cast<unsigned>(rest), static_cast<unsigned>(rest)), 256, 0, s>>>(w.G, M, jb);
+      }
       GS_LAUNCHED();
     }
   }
-  k_trsv_both<<<1, 1024, 0, s>>>(w.G, M, w.rhs, w.x, w.scal, phi);
+  {
+    GS_TIMED("k_trsv_both", s);
+    k_trsv_both<<<1, 1024, 0, s>>>(w.G, M, w.rhs, w.x, w.scal, phi);
+  }
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END
