@@ -130,8 +130,27 @@ def roofline(step, lib, dims):
     scale = 1e9 if unit == "GB/s" else 1e12
     achieved = per_launch / avg_s / scale
     return {"kernel": name, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-            "frac": achieved / peak, "traffic": None, "launches": n, "avg_launch_us": 1e3 * ms / n,
-            "work_per_launch": per_launch}
+            "frac": achieved / peak, "traffic": measured_traffic(name), "launches": n,
+            "avg_launch_us": 1e3 * ms / n, "work_per_launch": per_launch}
+
+
+def measured_traffic(kernel):
+    """HBM bytes per dispatch from the committed counter summary
+    (profiles/hbm_traffic.json: FETCH_SIZE and WRITE_SIZE scaled by a copy of
+    known size), or None when the kernel's source changed since then."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(kernel)
+        if rec is None:
+            return None
+        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != rec["source_sha256"]:
+                return None
+        return rec["hbm_bytes_per_dispatch"]
+    except (OSError, ValueError, KeyError):
+        return None
 
 
 def main():
