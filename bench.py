@@ -29,7 +29,7 @@ def parse():
     ap.add_argument("--config", default="cora")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--streams", type=int, default=8)
+    ap.add_argument("--streams", type=int, default=3)
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="bytes of a plain device copy run before the steps (counter calibration)")

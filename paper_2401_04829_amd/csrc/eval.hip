@@ -107,8 +107,8 @@ int make_shape(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, Shap
   s.wpr = (sg->num_edges + 63) / 64;
   const int64_t prb = per_row_bytes(s);
   int64_t t = static_cast<int64_t>(kTileBudget / static_cast<size_t>(prb > 0 ? prb : 1));
-  if (t > k) t = k;
-  if (t >= kTB) t -= t % kTB;
+  if (t >= k) t = k;                 // one pass covers every row
+  else if (t >= kTB) t -= t % kTB;
   if (t < 2) t = 2;
   s.tile = t;
   *out = s;

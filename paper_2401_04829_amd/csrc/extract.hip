@@ -229,6 +229,154 @@ __global__ void __launch_bounds__(256) k_cleanup(Ws w, int64_t count, int64_t n_
   for (int64_t i = t0; i < kCounters; i += step) w.counters[i] = 0;
 }
 
+// Inclusive scan of v over the 1024 threads of a block (Hillis-Steele in LDS).
+__device__ inline int64_t block_scan_1024(int64_t v, int64_t* buf) {
+  const int tid = threadIdx.x;
+  buf[tid] = v;
+  __syncthreads();
+  for (int d = 1; d < 1024; d <<= 1) {
+    const int64_t t = tid >= d ? buf[tid - d] : 0;
+    __syncthreads();
+    buf[tid] += t;
+    __syncthreads();
+  }
+  const int64_t r = buf[tid];
+  __syncthreads();
+  return r;
+}
+
+constexpr int64_t kOneBlockNodes = int64_t(1) << 18;
+
+// The whole extraction in one workgroup (graphs of at most kOneBlockNodes
+// nodes): BFS levels with a queue in the workspace, the level compaction in
+// global-id order, the degree scan, the player arrays when they fit the
+// caller's capacities, and the reset of the workspace.  counters[0..hops]
+// receive the level sizes, counters[kLevels] = M, counters[kLevels + 1] = 1 if
+// the arrays were written.
+__global__ void __launch_bounds__(1024) k_extract_one(const int64_t* __restrict__ indptr,
+                                                      const int32_t* __restrict__ indices, int64_t n,
+                                                      int64_t v, int hops, Ws w, int64_t cap_nodes,
+                                                      int64_t cap_edges, int32_t* node_gid, int32_t* dst_ptr,
+                                                      int32_t* edge_src, int32_t* edge_dst, int64_t* edge_gid) {
+  __shared__ int64_t lvl[kLevels + 2];     // queue offsets of the levels
+  __shared__ unsigned int qcount;
+  __shared__ int64_t buf[1024];
+  __shared__ int64_t carry;
+  __shared__ int ok;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) {
+    w.mark[v] = 1;
+    w.queue[0] = static_cast<int32_t>(v);
+    qcount = 1;
+    lvl[0] = 0;
+    lvl[1] = 1;
+  }
+  __syncthreads();
+  // BFS over in-edges, one wavefront per frontier node
+  for (int level = 0; level < hops; ++level) {
+    const int64_t b0 = lvl[level], b1 = lvl[level + 1];
+    for (int64_t f = b0 + wave; f < b1; f += 16) {
+      const int32_t node = w.queue[f];
+      const int64_t e0 = indptr[node], e1 = indptr[node + 1];
+      for (int64_t e = e0; e < e1; e += 64) {
+        bool win = false;
+        int32_t u = 0;
+        if (e + lane < e1) {
+          u = indices[e + lane];
+          win = atomicCAS(&w.mark[u], 0, level + 2) == 0;
+        }
+        const uint64_t bal = __ballot(win);
+        if (bal) {
+          unsigned int base = 0;
+          if (lane == 0) base = atomicAdd(&qcount, static_cast<unsigned int>(__popcll(bal)));
+          base = __shfl(base, 0);
+          if (win) w.queue[base + __popcll(bal & ((1ull << lane) - 1ull))] = u;
+        }
+      }
+    }
+    __syncthreads();
+    if (tid == 0) lvl[level + 2] = qcount;
+    __syncthreads();
+  }
+  const int64_t nodes = lvl[hops + 1];
+  const int64_t n_dst = lvl[hops];
+  // level compaction in global-id order: thread t scans marks [t*chunk, (t+1)*chunk)
+  const int64_t chunk = (n + 1023) / 1024;
+  const int64_t m0 = tid * chunk;
+  const int64_t m1 = m0 + chunk < n ? m0 + chunk : n;
+  for (int l = 0; l <= hops; ++l) {
+    int64_t c = 0;
+    for (int64_t i = m0; i < m1; ++i) c += w.mark[i] == l + 1;
+    int64_t pos = lvl[l] + block_scan_1024(c, buf) - c;
+    for (int64_t i = m0; i < m1 && c > 0; ++i) {
+      if (w.mark[i] == l + 1) {
+        w.sorted[pos] = static_cast<int32_t>(i);
+        w.local_of[i] = static_cast<int32_t>(pos);
+        ++pos;
+        --c;
+      }
+    }
+  }
+  __syncthreads();
+  // player offsets: exclusive scan of the in-degrees of the first n_dst nodes
+  if (tid == 0) {
+    carry = 0;
+    w.dstptr[0] = 0;
+  }
+  __syncthreads();
+  for (int64_t x0 = 0; x0 < n_dst; x0 += 1024) {
+    const int64_t x = x0 + tid;
+    int64_t deg = 0;
+    if (x < n_dst) {
+      const int32_t g = w.sorted[x];
+      deg = indptr[g + 1] - indptr[g];
+    }
+    const int64_t incl = block_scan_1024(deg, buf);
+    if (x < n_dst) w.dstptr[x + 1] = static_cast<int32_t>(carry + incl);
+    __syncthreads();
+    if (tid == 1023) carry += incl;
+    __syncthreads();
+  }
+  const int64_t m = carry;
+  if (tid == 0) ok = nodes <= cap_nodes && m <= cap_edges && m <= INT32_MAX;
+  __syncthreads();
+  if (ok) {
+    for (int64_t i = tid; i < nodes; i += 1024) node_gid[i] = w.sorted[i];
+    for (int64_t i = tid; i <= n_dst; i += 1024) dst_ptr[i] = w.dstptr[i];
+    for (int64_t x = wave; x < n_dst; x += 16) {
+      const int32_t g = w.sorted[x];
+      const int64_t e0 = indptr[g];
+      const int64_t deg = indptr[g + 1] - e0;
+      const int64_t out = w.dstptr[x];
+      for (int64_t j = lane; j < deg; j += 64) {
+        const int64_t e = e0 + j;
+        edge_src[out + j] = w.local_of[indices[e]];
+        edge_dst[out + j] = static_cast<int32_t>(x);
+        edge_gid[out + j] = e;
+      }
+    }
+  }
+  if (tid == 0) {
+    for (int l = 0; l <= hops; ++l) w.counters[l] = lvl[l + 1] - lvl[l];
+    w.counters[kLevels] = m;
+    w.counters[kLevels + 1] = ok;
+  }
+  __syncthreads();
+  // back to the zero state (the counters are cleared after the host copy)
+  for (int64_t i = tid; i < nodes; i += 1024) {
+    const int32_t g = w.queue[i];
+    w.mark[g] = 0;
+    w.local_of[g] = 0;
+    w.queue[i] = 0;
+    w.sorted[i] = 0;
+  }
+  for (int64_t i = tid; i <= n_dst; i += 1024) w.dstptr[i] = 0;
+}
+
+__global__ void k_zero_counters(int64_t* counters) {
+  if (threadIdx.x < kCounters) counters[threadIdx.x] = 0;
+}
+
 }  // namespace
 
 extern "C" int gnnshap_extract_workspace(int64_t num_nodes, size_t* bytes) {
@@ -262,6 +410,38 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int levels = hops + 1;
   const int64_t nblk = gnnshap::ceil_div(n, kChunk);
+
+  if (n <= kOneBlockNodes) {
+    if ((sg->cap_nodes > 0 && (!sg->node_gid || !sg->dst_ptr)) ||
+        (sg->cap_edges > 0 && (!sg->edge_src || !sg->edge_dst || !sg->edge_gid)))
+      return gnnshap::fail(GNNSHAP_EINVAL, "null subgraph output arrays");
+    {
+      GS_TIMED("k_extract_one", s);
+      k_extract_one<<<1, 1024, 0, s>>>(g->indptr, g->indices, n, target, hops, w, sg->cap_nodes, sg->cap_edges,
+                                       sg->node_gid, sg->dst_ptr, sg->edge_src, sg->edge_dst, sg->edge_gid);
+    }
+    GS_LAUNCHED();
+    int64_t h[kCounters];
+    GS_HIP(hipMemcpyAsync(h, w.counters, sizeof(h), hipMemcpyDeviceToHost, s));
+    k_zero_counters<<<1, 64, 0, s>>>(w.counters);
+    GS_LAUNCHED();
+    GS_HIP(hipStreamSynchronize(s));
+    int64_t nodes = 0;
+    sg->hop_ptr[0] = 0;
+    for (int l = 0; l < levels; ++l) {
+      nodes += h[l];
+      sg->hop_ptr[l + 1] = nodes;
+    }
+    for (int l = levels + 1; l < GNNSHAP_MAX_HOPS + 2; ++l) sg->hop_ptr[l] = nodes;
+    sg->num_nodes = nodes;
+    sg->num_dst = sg->hop_ptr[hops];
+    sg->num_edges = h[kLevels];
+    if (h[kLevels] > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "more than 2^31 players");
+    if (!h[kLevels + 1])
+      return gnnshap::fail(GNNSHAP_ECAPACITY, "subgraph needs %lld nodes and %lld edges", (long long)nodes,
+                           (long long)h[kLevels]);
+    return GNNSHAP_OK;
+  }
 
   k_init<<<1, 1, 0, s>>>(w.mark, w.queue, w.counters, target);
   GS_LAUNCHED();

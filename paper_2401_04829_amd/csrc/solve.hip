@@ -267,8 +267,7 @@ __global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ m
           if (cls[mid].row_begin <= b) lo = mid; else hi = mid - 1;
         }
         const double w = cls[lo].weight;
-        int64_t pc = 0;
-        for (int64_t q = 0; q < wpr; ++q) pc += __popcll(masks[b * wpr + q]);
+        const int64_t pc = cls[lo].size;               // |S_b|: representatives have their class size
         const double z1 = w * (static_cast<double>(y[b]) - f0 - delta / Md * static_cast<double>(pc));
         const double z2 = w * (static_cast<double>(y[b + half]) - f0 - delta / Md * static_cast<double>(M - pc));
         dzs[tid] = z1 - z2;

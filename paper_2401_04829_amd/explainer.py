@@ -1,7 +1,7 @@
-"""Torch-facing driver of the four C-ABI calls for one graph and one GCN.
+"""Torch-facing driver of the C-ABI calls for one graph and one GCN.
 
-Torch provides device memory and the stream; every computation runs in
-libgnnshap.so.  Buffers are caller-owned torch tensors and grow on demand.
+Torch provides device memory and streams; every computation runs in
+libgnnshap.so.  Buffers are caller-owned torch tensors.
 """
 import ctypes
 from dataclasses import dataclass
@@ -32,7 +32,7 @@ class _Buffer:
 
 @dataclass
 class Subgraph:
-    sg: L.gnnshap_subgraph      # sizes (host struct, pointers into the arrays below)
+    sg: L.gnnshap_subgraph      # sizes (host struct; pointers into the arrays below)
     node_gid: torch.Tensor      # int32 [n']
     dst_ptr: torch.Tensor       # int32 [num_dst + 1]
     edge_src: torch.Tensor      # int32 [M]
@@ -85,12 +85,12 @@ class Explainer:
         self.model = L.gnnshap_gcn(num_layers=nl, dims=self._dims, W=self._Wp, b=self._bp, XW1=None)
         self.XW1 = None
         self.extract_ws = torch.zeros(L.gnnshap_extract_workspace(n), dtype=torch.uint8, device=dev)
-        self._cap_nodes = 0
-        self._cap_edges = 0
+        self._cap = [1024, 8192]                 # node and edge capacity of new subgraph buffers
         self._sub = None
         self.ws_sample = _Buffer(dev)
         self.ws_eval = _Buffer(dev)
         self.ws_solve = _Buffer(dev)
+        self._pipe = None
 
     def prepare(self):
         """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
@@ -104,36 +104,41 @@ class Explainer:
     def stream(self):
         return ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream)
 
-    def _grow(self, nodes, edges):
+    def _new_sub_buffers(self):
         dev = self.device
-        self._cap_nodes = max(int(nodes * 1.25) + 16, self._cap_nodes)
-        self._cap_edges = max(int(edges * 1.25) + 64, self._cap_edges)
-        self._sub = dict(
-            node_gid=torch.empty(self._cap_nodes, dtype=torch.int32, device=dev),
-            dst_ptr=torch.empty(self._cap_nodes + 1, dtype=torch.int32, device=dev),
-            edge_src=torch.empty(self._cap_edges, dtype=torch.int32, device=dev),
-            edge_dst=torch.empty(self._cap_edges, dtype=torch.int32, device=dev),
-            edge_gid=torch.empty(self._cap_edges, dtype=torch.int64, device=dev))
+        cn, ce = self._cap
+        return dict(node_gid=torch.empty(cn, dtype=torch.int32, device=dev),
+                    dst_ptr=torch.empty(cn + 1, dtype=torch.int32, device=dev),
+                    edge_src=torch.empty(ce, dtype=torch.int32, device=dev),
+                    edge_dst=torch.empty(ce, dtype=torch.int32, device=dev),
+                    edge_gid=torch.empty(ce, dtype=torch.int64, device=dev))
 
-    def extract(self, target):
-        """gnnshap_extract_subgraph (blocks the host: returns the sizes)."""
-        if self._sub is None:
-            self._grow(1024, 8192)
+    def _extract(self, target, bufs):
+        """gnnshap_extract_subgraph into `bufs` (grown and retried on ECAPACITY);
+        blocks the host until the sizes are known."""
         while True:
-            b = self._sub
-            sg = L.gnnshap_subgraph(num_hops=self.hops, cap_nodes=self._cap_nodes, cap_edges=self._cap_edges,
-                                    node_gid=b["node_gid"].data_ptr(), dst_ptr=b["dst_ptr"].data_ptr(),
-                                    edge_src=b["edge_src"].data_ptr(), edge_dst=b["edge_dst"].data_ptr(),
-                                    edge_gid=b["edge_gid"].data_ptr())
+            b = bufs
+            sg = L.gnnshap_subgraph(num_hops=self.hops, cap_nodes=b["node_gid"].numel(),
+                                    cap_edges=b["edge_src"].numel(), node_gid=b["node_gid"].data_ptr(),
+                                    dst_ptr=b["dst_ptr"].data_ptr(), edge_src=b["edge_src"].data_ptr(),
+                                    edge_dst=b["edge_dst"].data_ptr(), edge_gid=b["edge_gid"].data_ptr())
             st = L.gnnshap_extract_subgraph(self.graph, int(target), sg, _vp(self.extract_ws),
                                             self.extract_ws.numel(), self.stream())
             if st == L.OK:
                 break
-            self._grow(sg.num_nodes, sg.num_edges)
+            self._cap = [max(int(sg.num_nodes * 1.25) + 16, self._cap[0]),
+                         max(int(sg.num_edges * 1.25) + 64, self._cap[1])]
+            bufs.clear()
+            bufs.update(self._new_sub_buffers())
         n, m, nd = sg.num_nodes, sg.num_edges, sg.num_dst
-        # the arrays stay valid until the next extract(); callers copy what they keep
         return Subgraph(sg=sg, node_gid=b["node_gid"][:n], dst_ptr=b["dst_ptr"][:nd + 1],
                         edge_src=b["edge_src"][:m], edge_dst=b["edge_dst"][:m], edge_gid=b["edge_gid"][:m])
+
+    def extract(self, target):
+        """The computational graph of one target (arrays valid until the next extract())."""
+        if self._sub is None:
+            self._sub = self._new_sub_buffers()
+        return self._extract(target, self._sub)
 
     def explain(self, target, num_samples, seed, target_class=-1, stream_id=None):
         """Alg. 1 for one target: extract, plan, sample, evaluate, solve."""
@@ -147,79 +152,46 @@ class Explainer:
                                                int(target if stream_id is None else stream_id))
         return self.run(sub, plan, classes, target_class, target)
 
-    def explain_many(self, targets, num_samples, seed, target_class=-1, n_streams=8):
-        """Alg. 1 for many targets, pipelined: extraction (the only call that
-        waits for the device) runs on its own stream while earlier targets'
-        sampling, evaluation and solve run on `n_streams` compute streams, so
-        independent targets overlap on the GPU.  Returns one Explanation per
-        target; their device tensors are complete once the default stream has
-        synchronised (the compute streams are joined to it at the end)."""
+    def explain_many(self, targets, num_samples, seed, target_class=-1, n_streams=3):
+        """Alg. 1 for many targets.  Extraction (the only call that waits for
+        the device) runs on its own stream into fresh buffers, so it never
+        waits for compute; each target's sampling, evaluation and solve are
+        enqueued on one of `n_streams` compute streams, so independent targets
+        overlap on the GPU.  The compute streams are joined to the current
+        stream before returning; results are complete once it synchronises."""
         if self.XW1 is None:
             self.prepare()
         main = torch.cuda.current_stream(self.device)
-        ext = self._pipe_streams(n_streams)
-        ext_stream, lanes = ext
-        ext_stream.wait_stream(main)
+        if self._pipe is None or len(self._pipe[1]) != n_streams:
+            self._pipe = (torch.cuda.Stream(self.device), [torch.cuda.Stream(self.device) for _ in range(n_streams)],
+                          [(_Buffer(self.device), _Buffer(self.device), _Buffer(self.device))
+                           for _ in range(n_streams)])
+        ext, lanes, wss = self._pipe
+        ext.wait_stream(main)
         for st in lanes:
             st.wait_stream(main)
         out = []
         for t, v in enumerate(targets):
-            lane = lanes[t % len(lanes)]
-            slot = self._slots[t % len(lanes)]
-            # the slot's subgraph buffers are rewritten: wait for its previous target
-            ext_stream.wait_stream(lane)
-            with torch.cuda.stream(ext_stream):
-                sub = self._extract_into(slot, v)
+            lane, ws = lanes[t % n_streams], wss[t % n_streams]
+            with torch.cuda.stream(ext):
+                bufs = self._new_sub_buffers()
+                sub = self._extract(v, bufs)
+            for tensor in bufs.values():
+                tensor.record_stream(lane)
             M = sub.sg.num_edges
             if M < 2:
                 raise ValueError(f"target {v} has {M} players; at least 2 are needed")
             plan, classes = L.gnnshap_plan_samples(M, int(num_samples), int(seed), int(v))
             with torch.cuda.stream(lane):
-                out.append(self.run(sub, plan, classes, target_class, v, slot=slot))
+                out.append(self.run(sub, plan, classes, target_class, v, workspaces=ws))
         for st in lanes:
             main.wait_stream(st)
         return out
 
-    def _pipe_streams(self, n):
-        if getattr(self, "_pipe", None) is None or len(self._pipe[1]) != n:
-            self._pipe = (torch.cuda.Stream(self.device), [torch.cuda.Stream(self.device) for _ in range(n)])
-            self._slots = [dict(sub=None, cap_nodes=0, cap_edges=0, ws_sample=_Buffer(self.device),
-                                ws_eval=_Buffer(self.device), ws_solve=_Buffer(self.device)) for _ in range(n)]
-        return self._pipe
-
-    def _extract_into(self, slot, target):
-        dev = self.device
-        while True:
-            if slot["sub"] is None:
-                slot["cap_nodes"], slot["cap_edges"] = 1024, 8192
-            b = slot["sub"]
-            if b is None or b["node_gid"].numel() < slot["cap_nodes"] or b["edge_src"].numel() < slot["cap_edges"]:
-                cn, ce = slot["cap_nodes"], slot["cap_edges"]
-                b = slot["sub"] = dict(
-                    node_gid=torch.empty(cn, dtype=torch.int32, device=dev),
-                    dst_ptr=torch.empty(cn + 1, dtype=torch.int32, device=dev),
-                    edge_src=torch.empty(ce, dtype=torch.int32, device=dev),
-                    edge_dst=torch.empty(ce, dtype=torch.int32, device=dev),
-                    edge_gid=torch.empty(ce, dtype=torch.int64, device=dev))
-            sg = L.gnnshap_subgraph(num_hops=self.hops, cap_nodes=b["node_gid"].numel(),
-                                    cap_edges=b["edge_src"].numel(), node_gid=b["node_gid"].data_ptr(),
-                                    dst_ptr=b["dst_ptr"].data_ptr(), edge_src=b["edge_src"].data_ptr(),
-                                    edge_dst=b["edge_dst"].data_ptr(), edge_gid=b["edge_gid"].data_ptr())
-            st = L.gnnshap_extract_subgraph(self.graph, int(target), sg, _vp(self.extract_ws),
-                                            self.extract_ws.numel(), self.stream())
-            if st == L.OK:
-                break
-            slot["cap_nodes"] = max(int(sg.num_nodes * 1.25) + 16, slot["cap_nodes"])
-            slot["cap_edges"] = max(int(sg.num_edges * 1.25) + 64, slot["cap_edges"])
-        n, m, nd = sg.num_nodes, sg.num_edges, sg.num_dst
-        return Subgraph(sg=sg, node_gid=b["node_gid"][:n], dst_ptr=b["dst_ptr"][:nd + 1],
-                        edge_src=b["edge_src"][:m], edge_dst=b["edge_dst"][:m], edge_gid=b["edge_gid"][:m])
-
-    def run(self, sub, plan, classes, target_class=-1, target=-1, slot=None):
+    def run(self, sub, plan, classes, target_class=-1, target=-1, workspaces=None):
+        """Sample, evaluate and solve on the current stream."""
         dev, s = self.device, self.stream()
-        ws_sample = slot["ws_sample"] if slot else self.ws_sample
-        ws_eval = slot["ws_eval"] if slot else self.ws_eval
-        ws_solve = slot["ws_solve"] if slot else self.ws_solve
+        ws_sample, ws_eval, ws_solve = workspaces or (self.ws_sample, self.ws_eval, self.ws_solve)
         k, wpr, M = plan.num_rows, plan.words_per_row, plan.num_players
         masks = torch.empty((k, wpr), dtype=torch.int64, device=dev)
         weights = torch.empty(k, dtype=torch.float32, device=dev)

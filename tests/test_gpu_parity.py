@@ -68,6 +68,22 @@ def test_extract_workload_targets_bit_exact(dev, name):
         assert lo <= ref["num_edges"] <= hi
 
 
+def test_extract_large_graph_multiblock_path(dev):
+    """Graphs above 2^18 nodes take the multi-block extraction kernels."""
+    n = 300_000
+    indptr, indices = W.random_digraph(n, 1_200_000, seed=77, symmetric=True)
+    cfg = dict(indptr=indptr, indices=indices, X=np.zeros((n, 4), np.float32),
+               weights=[np.zeros((4, 2), np.float32)], biases=[None], hops=2)
+    ex = explainer_for(cfg)
+    rng = np.random.default_rng(5)
+    for v in rng.integers(0, n, 12):
+        for hops in (1, 2, 3):
+            _say("extract large", int(v), hops)
+            ex.hops = hops
+            _check_subgraph(ex.extract(int(v)), subgraph.extract(indptr, indices, int(v), hops))
+    assert int(ex.extract_ws.count_nonzero()) == 0
+
+
 def test_extract_capacity_reports_sizes(dev):
     cfg = W.make_config("cora")
     ex = explainer_for(cfg)
