@@ -678,16 +678,21 @@ __global__ void __launch_bounds__(256) k_syrk(float* G, int64_t M, int64_t jb) {
   }
 }
 
-// Multi-block path: both triangular solves and phi in one workgroup.
-__global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G, int64_t M,
-                                                    float* __restrict__ rhs, float* __restrict__ x,
-                                                    const double* __restrict__ scal, float* __restrict__ phi) {
+// Multi-block path, triangular solves by segments [s0, s1) of at most kSeg
+// rows: one workgroup substitutes inside a segment (64-row blocks, one
+// wavefront per diagonal block); multi-block GEMVs carry a segment's
+// contribution to the rows outside it.
+constexpr int64_t kSeg = 2048;
+
+// Forward: x[s0:s1) = L[s0:s1, s0:s1)^-1 rhs[s0:s1) (rhs holds the earlier segments' updates).
+__global__ void __launch_bounds__(1024) k_trsv_fwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
+                                                   float* __restrict__ rhs, float* __restrict__ x) {
   __shared__ float Blk[kNB][kNB + 1];
   __shared__ float rd[kNB];
   const int tid = threadIdx.x, nt = blockDim.x;
   const int wave = tid >> 6, lane = tid & 63;
-  for (int64_t o = 0; o < M; o += kNB) {
-    const int nbe = static_cast<int>(M - o < kNB ? M - o : kNB);
+  for (int64_t o = s0; o < s1; o += kNB) {
+    const int nbe = static_cast<int>(s1 - o < kNB ? s1 - o : kNB);
     for (int t = tid; t < kNB * kNB; t += nt) {      // strictly lower part of L_jj
       const int r = t / kNB, c = t % kNB;
       Blk[r][c] = (r < nbe && c < r) ? G[(o + r) * M + o + c] : 0.f;
@@ -704,7 +709,7 @@ __global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G,
       if (lane < nbe) x[o + lane] = b * rd[lane];
     }
     __syncthreads();
-    for (int64_t i = o + nbe + tid; i < M; i += nt) {
+    for (int64_t i = o + nbe + tid; i < s1; i += nt) {
       float acc = 0.f;
       const float* row = G + i * M + o;
 #pragma unroll 8
@@ -713,8 +718,29 @@ __global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G,
     }
     __syncthreads();
   }
-  for (int64_t o = ((M - 1) / kNB) * kNB; o >= 0; o -= kNB) {
-    const int nbe = static_cast<int>(M - o < kNB ? M - o : kNB);
+}
+
+// rhs[i] -= L[i, s0:s1) x[s0:s1) for i >= s1; one wavefront per row.
+__global__ void __launch_bounds__(256) k_gemv_fwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
+                                                  const float* __restrict__ x, float* __restrict__ rhs) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = s1 + ((static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6);
+  if (i >= M) return;
+  float acc = 0.f;
+  for (int64_t c = s0 + lane; c < s1; c += 64) acc += G[i * M + c] * x[c];
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) rhs[i] -= acc;
+}
+
+// Backward: z[s0:s1) = L[s0:s1, s0:s1)^-T x[s0:s1) into rhs (x holds the later segments' updates).
+__global__ void __launch_bounds__(1024) k_trsv_bwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
+                                                   float* __restrict__ x, float* __restrict__ rhs) {
+  __shared__ float Blk[kNB][kNB + 1];
+  __shared__ float rd[kNB];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int64_t o = s0 + ((s1 - s0 - 1) / kNB) * kNB; o >= s0; o -= kNB) {
+    const int nbe = static_cast<int>(s1 - o < kNB ? s1 - o : kNB);
     for (int t = tid; t < kNB * kNB; t += nt) {      // Blk[r][k] = L[o+k][o+r], k > r
       const int r = t / kNB, k = t % kNB;
       Blk[r][k] = (k < nbe && r < k) ? G[(o + k) * M + o + r] : 0.f;
@@ -731,7 +757,7 @@ __global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G,
       if (lane < nbe) rhs[o + lane] = b * rd[lane];
     }
     __syncthreads();
-    for (int64_t i = tid; i < o; i += nt) {
+    for (int64_t i = s0 + tid; i < o; i += nt) {
       float acc = 0.f;
 #pragma unroll 8
       for (int c = 0; c < nbe; ++c) acc += G[(o + c) * M + i] * rhs[o + c];
@@ -739,8 +765,24 @@ __global__ void __launch_bounds__(1024) k_trsv_both(const float* __restrict__ G,
     }
     __syncthreads();
   }
+}
+
+// x[i] -= sum_{c in [s0, s1)} L[c, i] z[c] for i < s0; one thread per row (coalesced over i).
+__global__ void __launch_bounds__(256) k_gemv_bwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
+                                                  const float* __restrict__ z, float* __restrict__ x) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= s0) return;
+  float acc = 0.f;
+  for (int64_t c = s0; c < s1; ++c) acc += G[c * M + i] * z[c];
+  x[i] -= acc;
+}
+
+__global__ void k_finish(const float* __restrict__ z, int64_t M, const double* __restrict__ scal,
+                         float* __restrict__ phi) {
   const double base = scal[3] / static_cast<double>(M);
-  for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(base + static_cast<double>(rhs[i]));
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < M;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    phi[i] = static_cast<float>(base + static_cast<double>(z[i]));
 }
 
 int check_plan(const gnnshap_sample_plan* p, const gnnshap_class* classes) {
@@ -892,10 +934,33 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
       GS_LAUNCHED();
     }
   }
-  {
-    GS_TIMED("k_trsv_both", s);
-    k_trsv_both<<<1, 1024, 0, s>>>(w.G, M, w.rhs, w.x, w.scal, phi);
+  // L x = rhs, L^T psi = x (psi into rhs), phi = Delta/M + psi
+  for (int64_t s0 = 0; s0 < M; s0 += kSeg) {
+    const int64_t s1 = std::min(M, s0 + kSeg);
+    {
+      GS_TIMED("k_trsv", s);
+      k_trsv_fwd<<<1, 1024, 0, s>>>(w.G, M, s0, s1, w.rhs, w.x);
+    }
+    GS_LAUNCHED();
+    if (s1 < M) {
+      k_gemv_fwd<<<static_cast<unsigned>(gnnshap::ceil_div((M - s1) * 64, 256)), 256, 0, s>>>(w.G, M, s0, s1, w.x,
+                                                                                             w.rhs);
+      GS_LAUNCHED();
+    }
   }
+  for (int64_t s0 = ((M - 1) / kSeg) * kSeg; s0 >= 0; s0 -= kSeg) {
+    const int64_t s1 = std::min(M, s0 + kSeg);
+    {
+      GS_TIMED("k_trsv", s);
+      k_trsv_bwd<<<1, 1024, 0, s>>>(w.G, M, s0, s1, w.x, w.rhs);
+    }
+    GS_LAUNCHED();
+    if (s0 > 0) {
+      k_gemv_bwd<<<static_cast<unsigned>(gnnshap::ceil_div(s0, 256)), 256, 0, s>>>(w.G, M, s0, s1, w.rhs, w.x);
+      GS_LAUNCHED();
+    }
+  }
+  k_finish<<<gnnshap::grid_for(M, 256, 1024), 256, 0, s>>>(w.rhs, M, w.scal, phi);
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END

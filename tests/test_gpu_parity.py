@@ -150,8 +150,8 @@ def _oracle_game(cfg, sub_ref, cls):
     return gcn.Game(sub_ref, cfg["X"], cfg["weights"], cfg["biases"], cls=cls)
 
 
-def _check_eval(cfg, v, p, seed, rows=None, target_class=-1):
-    ex = explainer_for(cfg)
+def _check_eval(cfg, v, p, seed, rows=None, target_class=-1, ex=None):
+    ex = ex or explainer_for(cfg)
     res = ex.explain(v, p, seed, target_class=target_class)
     torch.cuda.synchronize()
     ref_sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
@@ -359,3 +359,95 @@ def test_solve_recovers_additive_game(dev, M, p):
                         torch.cuda.current_stream().cuda_stream)
     assert int(info.item()) == 0
     _phi_close(phi.cpu().numpy().astype(np.float64), a)
+
+
+# -- 5. full-size workloads ---------------------------------------------------------------
+
+def _unpack_rows(masks, M, r0, r1):
+    """Rows [r0, r1) of packed masks as fp64 0/1 on the device (test-side arithmetic)."""
+    sh = torch.arange(64, device=masks.device, dtype=torch.int64)
+    bits = (masks[r0:r1].unsqueeze(-1) >> sh) & 1
+    return bits.reshape(r1 - r0, -1)[:, :M].to(torch.float64)
+
+
+def _solve_phi(res, y, f0, f1):
+    from paper_2401_04829_amd import _lib as L
+    from paper_2401_04829_amd.explainer import _vp
+    dev = res.masks.device
+    M = res.plan.num_players
+    fef = torch.tensor([f0, f1], dtype=torch.float32, device=dev)
+    phi = torch.empty(M, dtype=torch.float32, device=dev)
+    info = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(L.gnnshap_solve_workspace(res.plan), dtype=torch.uint8, device=dev)
+    L.gnnshap_solve_wls(res.plan, res.classes, _vp(res.masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws),
+                        ws.numel(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert int(info.item()) == 0
+    return phi.cpu().numpy().astype(np.float64)
+
+
+def _normal_equation_residual(res, phi, f0, chunk=1024):
+    """r = X^T W (y - f0 - X phi) for the sampled rows X and their kernel
+    weights W, and the row sums of |X^T W X|, in fp64 on the device.  The
+    efficiency-constrained least squares optimum has r = lambda * 1."""
+    M, k = res.plan.num_players, res.plan.num_rows
+    dev = res.masks.device
+    ph = torch.tensor(phi, dtype=torch.float64, device=dev)
+    r = torch.zeros(M, dtype=torch.float64, device=dev)
+    gsum = torch.zeros(M, dtype=torch.float64, device=dev)
+    for r0 in range(0, k, chunk):
+        r1 = min(k, r0 + chunk)
+        X = _unpack_rows(res.masks, M, r0, r1)
+        w = res.weights[r0:r1].double()
+        e = res.y[r0:r1].double() - f0 - X @ ph
+        r += X.T @ (w * e)
+        gsum += X.T @ (w * X.sum(dim=1))
+    return r.cpu().numpy(), gsum.cpu().numpy()
+
+
+def _full_size_targets(cfg, picks):
+    ms = sorted((W.player_count(cfg["indptr"], cfg["indices"], v, cfg["hops"]), v) for v in cfg["targets"])
+    idx = sorted({int(round(x)) for x in np.linspace(0, len(ms) - 1, picks)})
+    return [ms[i][1] for i in idx]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,picks", [("arxiv", 3), ("reddit", 2)])
+def test_full_size_workload(dev, name, picks):
+    """At the full sizes of the two large workloads (2-hop graphs of 5k..30k
+    players, 50,000 / 100,000 coalitions): extraction bit-exact, sampled
+    masks bit-exact, sampled coalition values within the y bar, and phi
+    checked by properties that hold at any size: efficiency, the constrained
+    normal equations of the least squares, and exact recovery of an additive
+    game on the same coalitions."""
+    _say("full size", name, "building the workload")
+    cfg = W.make_config(name)
+    ex = explainer_for(cfg)
+    rng = np.random.default_rng(5)
+    for v in _full_size_targets(cfg, picks):
+        ref_sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
+        M = ref_sub["num_edges"]
+        pl = sampler.plan(M, cfg["p"])
+        k = pl["k"]
+        rows = np.unique(np.concatenate([rng.integers(0, k, 12), [0, 1, k // 2 - 1, k // 2, k - 1]]))
+        _say("full size", name, "target", v, "M", M, "k", k)
+        res, game, (f0, f1, cls) = _check_eval(cfg, v, cfg["p"], cfg["seed"], rows=rows, ex=ex)
+        _check_subgraph(ex.extract(v), ref_sub)
+        assert int(res.info.item()) == 0
+        phi = res.phi.cpu().numpy().astype(np.float64)
+        fef = res.f_empty_full.cpu().numpy().astype(np.float64)
+        delta = fef[1] - fef[0]
+        assert abs(phi.sum() - delta) <= 1e-4 * max(1.0, abs(delta)) + 1e-3 * np.abs(phi).max()
+        # first-order optimality: r - mean(r) = -(G d - mean(G d)) for d = phi - phi*,
+        # so the phi bar bounds it by 2 * 1e-3 max|phi| * (largest row sum of G)
+        r, gsum = _normal_equation_residual(res, phi, fef[0])
+        dev_r = np.abs(r - r.mean()).max()
+        assert dev_r <= 2e-3 * np.abs(phi).max() * gsum.max(), (dev_r, np.abs(phi).max(), gsum.max())
+        # an additive game on the same coalitions has phi = a
+        a = np.random.default_rng(M).normal(size=M)
+        at = torch.tensor(a, dtype=torch.float64, device=res.masks.device)
+        y_add = torch.cat([(0.25 + _unpack_rows(res.masks, M, r0, min(k, r0 + 1024)) @ at)
+                           for r0 in range(0, k, 1024)]).float()
+        _phi_close(_solve_phi(res, y_add, 0.25, 0.25 + a.sum()), a)
+        del res, y_add
+        torch.cuda.empty_cache()

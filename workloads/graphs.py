@@ -11,17 +11,20 @@ def _unique_pairs(a, b, n):
 
 
 def _draw_exact(n, n_pairs, draw, rng):
-    """Draws candidate pairs with `draw(count)` until exactly n_pairs distinct
-    undirected pairs exist; keeps a seeded random subset of the last batch."""
+    """Draws candidate pairs with `draw(count)` until at least n_pairs distinct
+    undirected pairs exist, then keeps a seeded random subset of exactly
+    n_pairs.  Returns (lo, hi), sorted by (lo, hi)."""
     keys = np.zeros(0, dtype=np.uint64)
+    batch = int(n_pairs * 1.3) + 1024
     while keys.size < n_pairs:
-        need = n_pairs - keys.size
-        a, b = draw(int(need * 1.3) + 1024)
+        a, b = draw(batch)
         new = _unique_pairs(a, b, n)
-        new = np.setdiff1d(new, keys, assume_unique=True)
-        if new.size > need:
-            new = rng.choice(new, size=need, replace=False)
-        keys = np.union1d(keys, new)
+        keys = new if keys.size == 0 else np.union1d(keys, new)
+        batch = int((n_pairs - keys.size) * 2) + 1024
+    if keys.size > n_pairs:
+        pick = rng.permutation(keys.size)[:n_pairs]
+        pick.sort()
+        keys = keys[pick]
     lo = (keys // np.uint64(n)).astype(np.int64)
     hi = (keys % np.uint64(n)).astype(np.int64)
     return lo, hi
@@ -49,36 +52,45 @@ def chung_lu_pairs(n, n_pairs, exponent, seed):
     return perm[lo], perm[hi]
 
 
+def _categorical(rng, prob, count):
+    """`count` i.i.d. draws from the categorical distribution `prob`: the
+    multinomial counts of every category, repeated and shuffled (the same law
+    as independent draws, with sequential memory access)."""
+    counts = rng.multinomial(count, prob)
+    idx = np.repeat(np.arange(prob.size, dtype=np.int64), counts)
+    rng.shuffle(idx)
+    return idx
+
+
 def dcsbm_pairs(n, n_pairs, n_blocks, p_in, degree_weights, seed):
     """Degree-corrected stochastic block model.
 
-    Nodes are split into `n_blocks` communities of near-equal size; an edge
-    endpoint is drawn with probability proportional to `degree_weights`; with
-    probability p_in the second endpoint is drawn from the first endpoint's
-    community (again by weight), otherwise from the whole graph.  Exactly
-    `n_pairs` distinct undirected pairs.  Returns (lo, hi) int64 arrays.
+    Nodes are split into `n_blocks` communities (node i in community
+    i mod n_blocks); an edge endpoint is drawn with probability proportional
+    to `degree_weights`; with probability p_in the second endpoint is drawn
+    from the first endpoint's community (again by weight), otherwise from the
+    whole graph.  Exactly `n_pairs` distinct undirected pairs.  Returns
+    (lo, hi) int64 arrays.
     """
     rng = np.random.Generator(np.random.PCG64(seed))
     w = np.asarray(degree_weights, dtype=np.float64)
+    prob = w / w.sum()
     block = np.arange(n) % n_blocks
-    order = np.argsort(block, kind="stable")            # nodes grouped by block
-    starts = np.searchsorted(block[order], np.arange(n_blocks + 1))
-    wcum_all = np.cumsum(w)
-    wcum_all /= wcum_all[-1]
-    w_sorted = w[order]
-    cum_sorted = np.cumsum(w_sorted)
+    members = [np.flatnonzero(block == c) for c in range(n_blocks)]
+    member_prob = [w[m] / w[m].sum() for m in members]
 
     def draw(count):
-        a = np.minimum(np.searchsorted(wcum_all, rng.random(count), side="right"), n - 1)
-        b = np.minimum(np.searchsorted(wcum_all, rng.random(count), side="right"), n - 1)
-        intra = rng.random(count) < p_in
+        a = _categorical(rng, prob, count)
+        b = _categorical(rng, prob, count)
+        intra = np.flatnonzero(rng.random(count) < p_in)
         ba = block[a[intra]]
-        s0, s1 = starts[ba], starts[ba + 1]
-        c0 = np.where(s0 > 0, cum_sorted[np.maximum(s0 - 1, 0)], 0.0)
-        c1 = cum_sorted[s1 - 1]
-        r = c0 + rng.random(ba.size) * (c1 - c0)
-        pos = np.minimum(np.searchsorted(cum_sorted, r, side="right"), s1 - 1)
-        b[intra] = order[pos]
+        by_block = np.argsort(ba, kind="stable")
+        counts = np.bincount(ba, minlength=n_blocks)
+        off = 0
+        for c in range(n_blocks):
+            sel = intra[by_block[off:off + counts[c]]]
+            b[sel] = members[c][_categorical(rng, member_prob[c], int(counts[c]))]
+            off += counts[c]
         return a, b
 
     lo, hi = _draw_exact(n, n_pairs, draw, rng)
@@ -100,10 +112,23 @@ def in_csr_from_directed(n, src, dst):
 
 
 def in_csr_from_pairs(n, lo, hi):
-    """Symmetric in-CSR: both directions of every undirected pair."""
-    src = np.concatenate([lo, hi])
-    dst = np.concatenate([hi, lo])
-    return in_csr_from_directed(n, src, dst)
+    """Symmetric in-CSR: both directions of every undirected pair (self loops
+    and repeated pairs dropped)."""
+    lo = np.asarray(lo, dtype=np.int64)
+    hi = np.asarray(hi, dtype=np.int64)
+    if lo.size and (lo == hi).any():
+        keep = lo != hi
+        lo, hi = lo[keep], hi[keep]
+    # sort by (dst, src) with one key sort; dedupe only when a repeat exists
+    key = np.concatenate([hi * np.int64(n) + lo, lo * np.int64(n) + hi])
+    key.sort()
+    if key.size > 1 and (key[1:] == key[:-1]).any():
+        key = np.unique(key)
+    d = key // n
+    s = key % n
+    indptr = np.zeros(n + 1, dtype=np.int64)
+    np.cumsum(np.bincount(d, minlength=n), out=indptr[1:])
+    return indptr, s.astype(np.int32)
 
 
 def random_digraph(n, n_edges, seed, symmetric=False):
