@@ -115,7 +115,7 @@ int make_shape(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, Shap
   return GNNSHAP_OK;
 }
 
-__device__ inline int64_t rows_in_pass(const int32_t* dyn_count, int64_t dyn_off, int64_t cap) {
+__device__ __forceinline__ int64_t rows_in_pass(const int32_t* dyn_count, int64_t dyn_off, int64_t cap) {
   if (!dyn_count) return cap;
   int64_t r = static_cast<int64_t>(*dyn_count) - dyn_off;
   return r < 0 ? 0 : (r > cap ? cap : r);

@@ -230,7 +230,7 @@ __global__ void __launch_bounds__(256) k_cleanup(Ws w, int64_t count, int64_t n_
 }
 
 // Inclusive scan of v over the 1024 threads of a block (Hillis-Steele in LDS).
-__device__ inline int64_t block_scan_1024(int64_t v, int64_t* buf) {
+__device__ __forceinline__ int64_t block_scan_1024(int64_t v, int64_t* buf) {
   const int tid = threadIdx.x;
   buf[tid] = v;
   __syncthreads();

@@ -25,7 +25,7 @@ Ws carve(gnnshap::Carver& c, int64_t ncls) {
 }
 
 // Philox4x32-10 (Salmon et al., SC'11).
-__device__ inline void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3,
+__device__ __forceinline__ void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3,
                                      uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
@@ -43,7 +43,7 @@ __device__ inline void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32_t& c2, u
 }
 
 // C(n, r), saturating at 2^62 (the unranked classes only need values < 2^32).
-__device__ inline uint64_t binom(int64_t n, int64_t r) {
+__device__ __forceinline__ uint64_t binom(int64_t n, int64_t r) {
   if (r < 0 || r > n) return 0;
   if (r > n - r) r = n - r;
   uint64_t v = 1;
@@ -55,7 +55,7 @@ __device__ inline uint64_t binom(int64_t n, int64_t r) {
   return v;
 }
 
-__device__ inline void set_bit(uint32_t* bs, int64_t j) { bs[j >> 5] |= 1u << (j & 31); }
+__device__ __forceinline__ void set_bit(uint32_t* bs, int64_t j) { bs[j >> 5] |= 1u << (j & 31); }
 
 __global__ void __launch_bounds__(64) k_sample(const gnnshap_class* __restrict__ cls, int64_t ncls,
                                                int64_t half, int64_t M, int64_t wpr, uint32_t seed_lo,

@@ -15,36 +15,54 @@
 //     with C_R the integer co-occurrence counts of the random representative
 //     rows, computed exactly by popcounts on a bit-transposed copy.
 // Systems whose lower triangle fits in LDS are assembled, factored and solved
-// by one workgroup; larger ones use a blocked right-looking Cholesky over the
-// whole GPU (64-wide panels) and one workgroup for the two triangular solves.
-// Diagonal blocks are factored by one wavefront holding a row per lane in
-// registers; tail blocks are padded with the identity so every inner loop
-// runs without per-lane branches.  The right-hand side is accumulated in fp64.
+// by one workgroup.  Larger ones use a blocked right-looking Cholesky over the
+// whole GPU with 128-wide panels: one workgroup factors the diagonal block and
+// inverts its factor, then the panel solve (a product with that inverse) and
+// the trailing update run as fp32 MFMA GEMMs.  The triangular solves go by
+// 256-row segments whose triangle sits in LDS, with multi-block GEMVs carrying
+// each segment to the rows outside it.  The right-hand side is accumulated in
+// fp64.
 #include <cmath>
 
 #include "common.h"
 
 namespace {
 
-constexpr int kNB = 64;   // panel width, multi-block path
-constexpr int kSB = 32;   // panel width, one-workgroup path
+constexpr int kPB = 128;       // panel width, multi-block Cholesky
+constexpr int kTB = 64;        // diagonal block of the triangular solves (one wavefront)
+constexpr int kSB = 32;        // panel width, one-workgroup path
+constexpr int64_t kSeg = 256;  // segment of the triangular solves (its triangle in LDS)
 constexpr int kMaxChunks = 256;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 struct Ws {
   gnnshap_class* classes;
   uint64_t* T;       // nrb x M: bit b of T[rb, j] = player j in random row rb*64+b
-  float* G;          // M x M (int32 counts first, then the system, lower part factored)
+  float* G;          // M rows of ld floats (int32 counts first, then the system, lower part factored)
   int64_t* usum;     // M: row sums of the counts
   double* scal;      // [0] trace, [1] sigma, [2] gamma, [3] delta, [4] f0
+  double* dz;        // half: z_b - z_{b+half}
   double* part;      // nch x M partial right-hand sides
+  double* dv;        // M: summed right-hand side before centring
+  double* bsum;      // per-block sums of dv
   float* rhs;        // M
   float* x;          // M
-  float* Ld;         // kNB x kNB padded diagonal factor + kNB reciprocal pivots
+  float* Winv;       // kPB x kPB inverse of the current diagonal factor
 };
 
-int64_t n_chunks(int64_t half) {
-  int64_t c = gnnshap::ceil_div(half, 256);
-  return c < 1 ? 1 : (c > kMaxChunks ? kMaxChunks : c);
+// Row stride of G: a multiple of 64 floats keeps every row 256-byte aligned.
+int64_t ld_of(int64_t M) { return gnnshap::ceil_div(M, 64) * 64; }
+
+// Row chunks of the right-hand side: enough wavefronts (word columns x chunks)
+// to fill the GPU, at least 64 rows per chunk.
+int64_t n_chunks(int64_t half, int64_t wpr) {
+  int64_t c = gnnshap::ceil_div(2048, wpr);
+  const int64_t by_rows = gnnshap::ceil_div(half, 64);
+  if (c > by_rows) c = by_rows;
+  if (c > kMaxChunks) c = kMaxChunks;
+  return c < 1 ? 1 : c;
 }
 
 Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
@@ -55,23 +73,32 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   const int64_t nrb = gnnshap::ceil_div(kr, 64);
   w.classes = c.take<gnnshap_class>(p->num_classes > 0 ? p->num_classes : 1);
   w.T = c.take<uint64_t>((nrb > 0 ? nrb : 1) * M);
-  w.G = c.take<float>(M * M);
+  w.G = c.take<float>(M * ld_of(M));
   w.usum = c.take<int64_t>(M);
   w.scal = c.take<double>(16);
-  w.part = c.take<double>(n_chunks(half) * M);
+  w.dz = c.take<double>(half);
+  w.part = c.take<double>(n_chunks(half, p->words_per_row) * M);
+  w.dv = c.take<double>(M);
+  w.bsum = c.take<double>(gnnshap::ceil_div(M, 256));
   w.rhs = c.take<float>(M);
   w.x = c.take<float>(M);
-  w.Ld = c.take<float>(kNB * kNB + kNB);
+  w.Winv = c.take<float>(kPB * kPB);
   return w;
 }
 
-__device__ inline float bcast(float v, int lane) {
+__device__ __forceinline__ float bcast(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
 }
 
 // a[lane] without a dynamic register index: unrolled selects.
 template <int NB>
-__device__ inline float lane_entry(const float (&a)[NB]) {
+__device__ __forceinline__ float lane_entry(const float (&a)[NB]) {
   const int lane = threadIdx.x & 63;
   float d = 1.f;
 #pragma unroll
@@ -86,7 +113,7 @@ __device__ inline float lane_entry(const float (&a)[NB]) {
 // first non-positive pivot (1-based, offset o) goes to *info and is replaced
 // by 1.
 template <int NB>
-__device__ inline void chol_regs(float (&a)[NB], int64_t o, int32_t* info) {
+__device__ __forceinline__ void chol_regs(float (&a)[NB], int64_t o, int32_t* info) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int k = 0; k < NB; ++k) {
@@ -123,8 +150,8 @@ __global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ m
 }
 
 // Counts C[i, j] = sum_rb popcount(T[rb, i] & T[rb, j]) for 64x64 tiles with J >= I,
-// stored in both halves.
-__global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M,
+// stored in both halves (row stride ld).
+__global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
                                               int32_t* __restrict__ C) {
   const int64_t I = blockIdx.y, J = blockIdx.x;
   if (J < I) return;
@@ -167,34 +194,34 @@ __global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, in
     for (int r = 0; r < 4; ++r) {
       const int64_t j = J * 64 + tx * 4 + r;
       if (j >= M) continue;
-      C[i * M + j] = acc[q][r];
-      C[j * M + i] = acc[q][r];
+      C[i * ld + j] = acc[q][r];
+      C[j * ld + i] = acc[q][r];
     }
   }
 }
 
 // usum[i] = sum_j C[i, j]; one wave per row.
-__global__ void __launch_bounds__(256) k_rowsum(const int32_t* __restrict__ C, int64_t M,
+__global__ void __launch_bounds__(256) k_rowsum(const int32_t* __restrict__ C, int64_t M, int64_t ld,
                                                 int64_t* __restrict__ usum) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
   if (i >= M) return;
   long long s = 0;
-  for (int64_t j = lane; j < M; j += 64) s += C[i * M + j];
+  for (int64_t j = lane; j < M; j += 64) s += C[i * ld + j];
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
   if (lane == 0) usum[i] = s;
 }
 
 // scal: trace and sigma of the counts (exact), gamma, Delta, f0.  One block.
 __global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, const int64_t* __restrict__ usum,
-                                                 int64_t M, bool has_random, double alpha, double wr,
+                                                 int64_t M, int64_t ld, bool has_random, double alpha, double wr,
                                                  const float* __restrict__ fef, double* scal) {
   __shared__ long long st[256], ss[256];
   const int tid = threadIdx.x;
   long long tr = 0, sg = 0;
   if (has_random)
     for (int64_t i = tid; i < M; i += 256) {
-      tr += C[i * M + i];
+      tr += C[i * ld + i];
       sg += usum[i];
     }
   st[tid] = tr;
@@ -220,105 +247,124 @@ __global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, 
   }
 }
 
-// In place: counts (int32) -> G~ (fp32), lower and upper.
-__global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restrict__ usum, int64_t M,
+// In place: counts (int32) -> G~ (fp32) on the lower triangle (the factorisation reads nothing else).
+__global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restrict__ usum, int64_t M, int64_t ld,
                                                bool has_random, double alpha, double wr,
                                                const double* __restrict__ scal) {
   const double Md = static_cast<double>(M);
+  const double inv_m = 1.0 / Md;
   const double sigma = scal[1], gamma = scal[2];
-  const int64_t total = M * M;
-  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
-       t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-    const int64_t i = t / M, j = t % M;
-    double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
+  const double base = -alpha * inv_m + gamma * inv_m + (has_random ? 2.0 * wr * sigma * inv_m * inv_m : 0.0);
+  const double wr2 = 2.0 * wr;
+  const int64_t i = blockIdx.x;          // one block per row
+  for (int64_t j = threadIdx.x; j <= i; j += blockDim.x) {
+    double v = base + (i == j ? alpha : 0.0);
     if (has_random) {
-      const double cij = static_cast<double>(reinterpret_cast<const int32_t*>(G)[t]);
-      v += 2.0 * wr * (cij - static_cast<double>(usum[i] + usum[j]) / Md + sigma / (Md * Md));
+      const double cij = static_cast<double>(reinterpret_cast<const int32_t*>(G)[i * ld + j]);
+      v += wr2 * (cij - static_cast<double>(usum[i] + usum[j]) * inv_m);
     }
-    G[t] = static_cast<float>(v);
+    G[i * ld + j] = static_cast<float>(v);
   }
 }
 
-// Partial right-hand sides: part[ch, j] = sum_{b in chunk ch} dz_b m_bj with
-// dz_b = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|), b < half.
-__global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ masks, int64_t wpr,
-                                                  int64_t half, int64_t M, const float* __restrict__ y,
-                                                  const gnnshap_class* __restrict__ cls, int64_t ncls,
-                                                  const float* __restrict__ fef, int64_t rows_per_chunk,
-                                                  double* __restrict__ part) {
-  __shared__ double dzs[256];
-  const int tid = threadIdx.x;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rows_per_chunk;
-  const int64_t r1 = r0 + rows_per_chunk < half ? r0 + rows_per_chunk : half;
+// dz_b = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|) for b < half; a
+// representative row has its class's size, its complement M minus that.
+__global__ void __launch_bounds__(256) k_dz(const float* __restrict__ y, int64_t half, int64_t M,
+                                            const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                            const float* __restrict__ fef, double* __restrict__ dz) {
+  const int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (b >= half) return;
   const double Md = static_cast<double>(M);
   const double f0 = static_cast<double>(fef[0]);
   const double delta = static_cast<double>(fef[1]) - f0;
-  for (int64_t j0 = 0; j0 < M; j0 += 256) {
-    const int64_t j = j0 + tid;
-    double acc = 0.0;
-    for (int64_t b0 = r0; b0 < r1; b0 += 256) {
-      const int nb = static_cast<int>(r1 - b0 < 256 ? r1 - b0 : 256);
-      __syncthreads();
-      if (tid < nb) {
-        const int64_t b = b0 + tid;
-        int64_t lo = 0, hi = ncls - 1;
-        while (lo < hi) {
-          const int64_t mid = (lo + hi + 1) >> 1;
-          if (cls[mid].row_begin <= b) lo = mid; else hi = mid - 1;
-        }
-        const double w = cls[lo].weight;
-        const int64_t pc = cls[lo].size;               // |S_b|: representatives have their class size
-        const double z1 = w * (static_cast<double>(y[b]) - f0 - delta / Md * static_cast<double>(pc));
-        const double z2 = w * (static_cast<double>(y[b + half]) - f0 - delta / Md * static_cast<double>(M - pc));
-        dzs[tid] = z1 - z2;
-      }
-      __syncthreads();
-      if (j < M) {
-        const uint64_t* col = masks + b0 * wpr + (j >> 6);
-        const int sh = static_cast<int>(j & 63);
-        for (int q = 0; q < nb; ++q)
-          if ((col[q * wpr] >> sh) & 1) acc += dzs[q];
-      }
-    }
-    if (j < M) part[static_cast<int64_t>(blockIdx.x) * M + j] = acc;
+  int64_t lo = 0, hi = ncls - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (cls[mid].row_begin <= b) lo = mid; else hi = mid - 1;
   }
+  const double w = cls[lo].weight;
+  const int64_t pc = cls[lo].size;
+  const double z1 = w * (static_cast<double>(y[b]) - f0 - delta / Md * static_cast<double>(pc));
+  const double z2 = w * (static_cast<double>(y[b + half]) - f0 - delta / Md * static_cast<double>(M - pc));
+  dz[b] = z1 - z2;
 }
 
-// rhs = P (sum of the partials); one block.
-__global__ void __launch_bounds__(1024) k_rhs_finish(const double* __restrict__ part, int64_t nch, int64_t M,
-                                                     float* __restrict__ rhs, double* scal) {
-  __shared__ double red[1024];
-  const int tid = threadIdx.x;
-  double s = 0.0;
-  for (int64_t j = tid; j < M; j += 1024) {
-    double v = 0.0;
-    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
-    s += v;
+// Partial right-hand sides: part[ch, j] = sum_{b in chunk ch} dz_b m_bj.  A
+// wavefront owns one 64-player word column and the rows of one chunk: each
+// row's word and dz_b are wave-uniform (scalar loads) and every lane tests
+// its own bit.
+__global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
+                                                  int64_t M, const double* __restrict__ dz, int64_t rows_per_chunk,
+                                                  double* __restrict__ part) {
+  const int lane = threadIdx.x & 63;
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (w >= wpr) return;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * rows_per_chunk;
+  const int64_t r1 = r0 + rows_per_chunk < half ? r0 + rows_per_chunk : half;
+  const uint64_t* col = masks + w;
+  double acc = 0.0;
+  int64_t b = r0;
+  for (; b + 8 <= r1; b += 8) {
+    uint64_t m[8];
+    double d[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      m[q] = col[(b + q) * wpr];
+      d[q] = dz[b + q];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc += ((m[q] >> lane) & 1) ? d[q] : 0.0;
   }
-  red[tid] = s;
+  for (; b < r1; ++b) acc += ((col[b * wpr] >> lane) & 1) ? dz[b] : 0.0;
+  const int64_t j = w * 64 + lane;
+  if (j < M) part[static_cast<int64_t>(blockIdx.y) * M + j] = acc;
+}
+
+// dv[j] = sum over chunks of part[., j] (fixed order); bsum[block] = sum of its dv.
+__global__ void __launch_bounds__(256) k_rhs_reduce(const double* __restrict__ part, int64_t nch, int64_t M,
+                                                    double* __restrict__ dv, double* __restrict__ bsum) {
+  __shared__ double red[256];
+  const int tid = threadIdx.x;
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + tid;
+  double v = 0.0;
+  if (j < M) {
+    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
+    dv[j] = v;
+  }
+  red[tid] = v;
   __syncthreads();
-  for (int off = 512; off > 0; off >>= 1) {
+  for (int off = 128; off > 0; off >>= 1) {
     if (tid < off) red[tid] += red[tid + off];
     __syncthreads();
   }
-  const double mean = red[0] / static_cast<double>(M);
-  for (int64_t j = tid; j < M; j += 1024) {
-    double v = 0.0;
-    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
-    rhs[j] = static_cast<float>(v - mean);
+  if (tid == 0) bsum[blockIdx.x] = red[0];
+}
+
+// rhs = P dv: subtract the mean (every block sums bsum in the same order).
+__global__ void __launch_bounds__(256) k_rhs_center(const double* __restrict__ dv, const double* __restrict__ bsum,
+                                                    int64_t nb, int64_t M, float* __restrict__ rhs) {
+  __shared__ double mean;
+  if (threadIdx.x == 0) {
+    double s = 0.0;
+    for (int64_t b = 0; b < nb; ++b) s += bsum[b];
+    mean = s / static_cast<double>(M);
   }
+  __syncthreads();
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j < M) rhs[j] = static_cast<float>(dv[j] - mean);
 }
 
 // One-workgroup path: the lower triangle of G~ packed in LDS (row i at
 // i(i+1)/2).
-__device__ inline int64_t tri(int64_t i, int64_t j) { return ((i * (i + 1)) >> 1) + j; }
+__device__ __forceinline__ int64_t tri(int64_t i, int64_t j) { return ((i * (i + 1)) >> 1) + j; }
 
 size_t small_lds_bytes(int64_t M) {
   return static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float)) +
          static_cast<size_t>((M * (M + 1)) / 2) * sizeof(float);
 }
 
-__global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__ C, int64_t M, bool has_random,
+__global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__ C, int64_t ldc, int64_t M,
+                                                     bool has_random,
                                                      double alpha, double wr, const float* __restrict__ fef,
                                                      const double* __restrict__ part, int64_t nch,
                                                      int32_t* info, float* __restrict__ phi) {
@@ -348,7 +394,7 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           const int64_t j = j0 + q * 64 + lane;
-          v[q] = C[i * M + (j < M ? j : 0)];
+          v[q] = C[i * ldc + (j < M ? j : 0)];
           v[q] = j < M ? v[q] : 0;
         }
 #pragma unroll
@@ -577,204 +623,427 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
 
 __global__ void k_zero_info(int32_t* info) { *info = 0; }
 
-// Multi-block path, diagonal block jb: one wavefront factors it in registers,
-// writes L_jj back (zeros above the diagonal) and the padded factor with its
-// reciprocal pivots to Ld for the panel kernel.
-__global__ void __launch_bounds__(64) k_potrf(float* G, int64_t M, int64_t jb, int32_t* info, float* Ld) {
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  const int lane = threadIdx.x;
-  const bool own = lane < n;
-  float a[kNB];
+// ---- multi-block path: diagonal blocks --------------------------------------------------
+
+constexpr int kHP = 68;                                  // LDS pitch of a 64x64 block (16-byte rows)
+constexpr int kHB = 64 * kHP;                            // floats per block
+constexpr size_t kPotrfLds = (5 * kHB + 64) * sizeof(float);
+
+// One wavefront: Cholesky of a 64x64 block held row `lane` per lane in a[]
+// (rows past the real block are the identity).  Column k goes through LDS
+// (`col`, 64 floats): every lane reads the pivot and the entries below it as
+// 16-byte broadcasts and applies the rank-1 update to its row.  Entries above
+// the diagonal are left undefined.  The first non-positive pivot (1-based,
+// offset o) goes to *info and is replaced by 1.
+__device__ __forceinline__ void chol_wave(float (&a)[64], float* col, int64_t o, int32_t* info) {
+  const int lane = threadIdx.x & 63;
+  int bad = 0;
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) {
-    const bool real = own && c < n && c <= lane;
-    const float v = G[real ? (o + lane) * M + o + c : 0];
-    a[c] = real ? v : (c == lane ? 1.f : 0.f);
+  for (int k = 0; k < 64; ++k) {
+    col[lane] = a[k];
+    __builtin_amdgcn_wave_barrier();
+    float cv[64];
+#pragma unroll
+    for (int j4 = k & ~3; j4 < 64; j4 += 4) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(col + j4);
+      cv[j4] = q[0];
+      cv[j4 + 1] = q[1];
+      cv[j4 + 2] = q[2];
+      cv[j4 + 3] = q[3];
+    }
+    const bool ok = cv[k] > 0.f;
+    bad = (bad == 0 && !ok) ? k + 1 : bad;
+    const float rs = 1.0f / sqrtf(ok ? cv[k] : 1.f);
+    a[k] *= rs;                    // L[lane][k] (lane k: sqrt of the pivot)
+    const float t = a[k] * rs;     // L[lane][k] / L[k][k]: L[j][k] = col[j] rs
+#pragma unroll
+    for (int j = k + 1; j < 64; ++j) a[j] -= t * cv[j];
+    __builtin_amdgcn_wave_barrier();
   }
-  chol_regs<kNB>(a, o, info);
+  if (bad != 0 && lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + bad));
+}
+
+// One wavefront: column `lane` of W = L^-1 into w[] from Lt = L^T (pitch kHP)
+// by right-looking forward substitution; row p of Lt is read as 16-byte
+// broadcasts.  Entries above the diagonal come out exactly zero.
+__device__ __forceinline__ void inv_wave(const float* Lt, float (&w)[64]) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) Ld[lane * kNB + c] = c <= lane ? a[c] : 0.f;
-  Ld[kNB * kNB + lane] = 1.0f / lane_entry(a);
-  if (own) {
+  for (int c = 0; c < 64; ++c) w[c] = c == lane ? 1.f : 0.f;
 #pragma unroll
-    for (int c = 0; c < kNB; ++c)
-      if (c < n) G[(o + lane) * M + o + c] = c <= lane ? a[c] : 0.f;
+  for (int p = 0; p < 64; ++p) {
+    const float* row = Lt + p * kHP;
+    float rv[64];
+#pragma unroll
+    for (int j4 = p & ~3; j4 < 64; j4 += 4) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(row + j4);
+      rv[j4] = q[0];
+      rv[j4 + 1] = q[1];
+      rv[j4 + 2] = q[2];
+      rv[j4 + 3] = q[3];
+    }
+    w[p] *= 1.0f / rv[p];
+    const float u = w[p];
+#pragma unroll
+    for (int i = p + 1; i < 64; ++i) w[i] -= rv[i] * u;
   }
 }
 
-// Panel: rows below block jb, X <- X L_jj^-T, one thread per row, right-looking.
-__global__ void __launch_bounds__(256) k_trsm(float* G, int64_t M, int64_t jb, const float* __restrict__ Ld) {
-  __shared__ float L[kNB][kNB + 1];
-  __shared__ float rd[kNB];
-  const int64_t o = jb * kNB;
-  const int tid = threadIdx.x;
-  for (int t = tid; t < kNB * kNB; t += 256) L[t / kNB][t % kNB] = Ld[t];
-  if (tid < kNB) rd[tid] = Ld[kNB * kNB + tid];
+// One wavefront: S (64x64, pitch kHP) <- L = chol(S) (zeros above the
+// diagonal) and Wb <- L^-1, using Wb for L^T on the way.
+__device__ __forceinline__ void chol_inv64(float* S, float* Wb, float* col, int64_t o, int32_t* info) {
+  const int lane = threadIdx.x & 63;
+  {
+    float a[64];
+#pragma unroll
+    for (int c4 = 0; c4 < 64; c4 += 4) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(S + lane * kHP + c4);
+      a[c4] = q[0];
+      a[c4 + 1] = q[1];
+      a[c4 + 2] = q[2];
+      a[c4 + 3] = q[3];
+    }
+    chol_wave(a, col, o, info);
+#pragma unroll
+    for (int c = 0; c < 64; ++c) {
+      const float v = c <= lane ? a[c] : 0.f;
+      S[lane * kHP + c] = v;
+      Wb[c * kHP + lane] = v;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  float w[64];
+  inv_wave(Wb, w);
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int i = 0; i < 64; ++i) Wb[i * kHP + lane] = w[i];
+}
+
+// D = alpha op(X, Y) + beta D on 64x64 LDS blocks, op = X Y^T (kNT) or X Y;
+// four wavefronts, one 32x32 quadrant each, fp32 MFMA 32x32x2 on two
+// accumulator chains.  Lane half h feeds k in [32h, 32h+32), so each MFMA sums
+// k and k+32.  D may alias X or Y: the products are complete before D is
+// written.
+template <bool kNT>
+__device__ __forceinline__ void mm64(const float* X, const float* Y, float* D, float alpha, float beta) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int qr = wave >> 1, qc = wave & 1, h = lane >> 5, rl = lane & 31;
+  f32x16 acc0 = {}, acc1 = {};
+  const float* xr = X + (qr * 32 + rl) * kHP + h * 32;
+#pragma unroll
+  for (int s = 0; s < 32; s += 4) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(xr + s);
+    f32x4 b;
+    if (kNT) {
+      b = *reinterpret_cast<const f32x4*>(Y + (qc * 32 + rl) * kHP + h * 32 + s);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) b[e] = Y[(h * 32 + s + e) * kHP + qc * 32 + rl];
+    }
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], acc1, 0, 0, 0);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[2], b[2], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[3], b[3], acc1, 0, 0, 0);
+  }
   __syncthreads();
-  const int64_t r = o + kNB + static_cast<int64_t>(blockIdx.x) * 256 + tid;
-  if (r >= M) return;
-  float x[kNB];
-  float* row = G + r * M + o;
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) x[c] = row[c];
-#pragma unroll
-  for (int c = 0; c < kNB; ++c) {
-    x[c] *= rd[c];
-#pragma unroll
-    for (int q = c + 1; q < kNB; ++q) x[q] -= x[c] * L[q][c];
-    __builtin_amdgcn_sched_barrier(0);
+  for (int r = 0; r < 16; ++r) {
+    float* d = D + (qr * 32 + 8 * (r >> 2) + 4 * h + (r & 3)) * kHP + qc * 32 + rl;
+    const float v = acc0[r] + acc1[r];
+    *d = beta == 0.f ? alpha * v : beta * *d + alpha * v;
   }
-#pragma unroll
-  for (int c = 0; c < kNB; ++c) row[c] = x[c];
+  __syncthreads();
 }
 
-// Trailing update of tile (ib, kb), jb < kb <= ib: A_ib,kb -= L_ib,jb L_kb,jb^T.
-__global__ void __launch_bounds__(256) k_syrk(float* G, int64_t M, int64_t jb) {
-  const int64_t ib = jb + 1 + blockIdx.y, kb = jb + 1 + blockIdx.x;
-  if (kb > ib) return;
-  __shared__ float As[16][64 + 4];
-  __shared__ float Bs[16][64 + 4];
-  const int tid = threadIdx.x;
-  const int ty = tid / 16, tx = tid % 16;
-  const int64_t o = jb * kNB;
-  const int n = static_cast<int>(M - o < kNB ? M - o : kNB);
-  float acc[4][4] = {};
-  for (int k0 = 0; k0 < n; k0 += 16) {
+// Diagonal block at (o, o), kPB wide (identity past M), factored by 64-wide
+// halves with the inverse built alongside:
+//   L11 = chol(A11), W11 = L11^-1, L21 = A21 W11^T, A22 -= L21 L21^T,
+//   L22 = chol(A22), W22 = L22^-1, W21 = -W22 (L21 W11).
+// L goes back to the lower part of G, W = L^-1 (zero above the diagonal) to Winv.
+__global__ void __launch_bounds__(256) k_potrf(float* G, int64_t ld, int64_t M, int64_t o, int32_t* info,
+                                               float* __restrict__ Winv) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* S0 = reinterpret_cast<float*>(smem);  // A11 -> L11, later L21 W11
+  float* S1 = S0 + kHB;                        // W11
+  float* S2 = S1 + kHB;                        // A21 -> L21, later W21
+  float* S3 = S2 + kHB;                        // A22 -> L22
+  float* S4 = S3 + kHB;                        // W22
+  float* col = S4 + kHB;
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const int64_t n = M - o < kPB ? M - o : kPB;
+  {
+    // all 64 loads of a thread in flight before the LDS stores
+    float v[kPB * kPB / 256];
+#pragma unroll
+    for (int q = 0; q < kPB * kPB / 256; ++q) {
+      const int t = tid + q * 256;
+      const int r = t / kPB, c = t % kPB;
+      v[q] = (r < n && c <= r) ? G[(o + r) * ld + o + c] : (r == c ? 1.f : 0.f);
+    }
+#pragma unroll
+    for (int q = 0; q < kPB * kPB / 256; ++q) {
+      const int t = tid + q * 256;
+      const int r = t / kPB, c = t % kPB;
+      if (r < 64 && c >= 64) continue;
+      float* dst = r < 64 ? S0 + r * kHP + c : (c < 64 ? S2 + (r - 64) * kHP + c : S3 + (r - 64) * kHP + c - 64);
+      *dst = v[q];
+    }
+  }
+  __syncthreads();
+  if (wave == 0) chol_inv64(S0, S1, col, o, info);
+  __syncthreads();
+  mm64<true>(S2, S1, S2, 1.f, 0.f);     // L21
+  mm64<true>(S2, S2, S3, -1.f, 1.f);    // A22 - L21 L21^T
+  for (int t = tid; t < kPB * 64; t += 256) {
+    const int r = t / 64, c = t % 64;
+    if (r < n && c < n && c <= r) G[(o + r) * ld + o + c] = r < 64 ? S0[r * kHP + c] : S2[(r - 64) * kHP + c];
+  }
+  __syncthreads();
+  mm64<false>(S2, S1, S0, 1.f, 0.f);    // L21 W11
+  if (wave == 0) chol_inv64(S3, S4, col, o + 64, info);
+  __syncthreads();
+  mm64<false>(S4, S0, S2, -1.f, 0.f);   // W21
+  for (int t = tid; t < 64 * 64; t += 256) {
+    const int r = t / 64, c = t % 64;
+    if (64 + r < n && 64 + c < n && c <= r) G[(o + 64 + r) * ld + o + 64 + c] = S3[r * kHP + c];
+  }
+  for (int t = tid; t < kPB * kPB; t += 256) {
+    const int r = t / kPB, c = t % kPB;
+    float v;
+    if (r < 64) v = c < 64 ? S1[r * kHP + c] : 0.f;
+    else v = c < 64 ? S2[(r - 64) * kHP + c] : S4[(r - 64) * kHP + c - 64];
+    Winv[t] = v;
+  }
+}
+
+// ---- multi-block path: MFMA GEMM ---------------------------------------------------------
+
+constexpr int kGT = 128;        // output tile edge
+constexpr int kGK = 32;         // K chunk staged in LDS
+constexpr int kGP = kGK + 4;    // LDS row pitch (floats)
+
+// C = beta C + alpha A B^T over 128x128 tiles, fp32 MFMA 32x32x2; rows of A and
+// B are K contiguous floats (K a multiple of 32; lda, ldb multiples of 4 and
+// 16-byte aligned bases).  Four wavefronts own 64x64 quadrants; lane half h
+// feeds k in [16h, 16h+16) of each chunk.  kLower: blockIdx.x enumerates the
+// tiles with J <= I (diagonal tiles written whole).  A may alias C when one
+// tile column covers all of n (the tile reads its rows before writing them).
+template <bool kLower>
+__global__ void __launch_bounds__(256) k_gemm_nt(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
+                                                 int64_t ldc, int64_t m, int64_t n, int64_t K, float alpha,
+                                                 float beta, int64_t tiles_n) {
+  __shared__ __align__(16) float As[kGT * kGP];
+  __shared__ __align__(16) float Bs[kGT * kGP];
+  const int64_t t = blockIdx.x;
+  int64_t I, J;
+  if (kLower) {
+    I = static_cast<int64_t>((sqrt(8.0 * static_cast<double>(t) + 1.0) - 1.0) * 0.5);
+    while (I * (I + 1) / 2 > t) --I;
+    while ((I + 1) * (I + 2) / 2 <= t) ++I;
+    J = t - I * (I + 1) / 2;
+  } else {
+    I = t / tiles_n;
+    J = t % tiles_n;
+  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1, h = lane >> 5, rl = lane & 31;
+  const int64_t i0 = I * kGT, j0 = J * kGT;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = f32x16{};
+  for (int64_t p0 = 0; p0 < K; p0 += kGK) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int idx = tid + q * 256;
-      const int r = idx / 16, kk = idx % 16;
-      const int64_t gi = ib * kNB + r, gk = kb * kNB + r;
-      const bool kin = k0 + kk < n;
-      As[kk][r] = (kin && gi < M) ? G[gi * M + o + k0 + kk] : 0.f;
-      Bs[kk][r] = (kin && gk < M) ? G[gk * M + o + k0 + kk] : 0.f;
+      const int r = idx >> 3, c4 = (idx & 7) << 2;
+      f32x4 va = {0.f, 0.f, 0.f, 0.f}, vb = {0.f, 0.f, 0.f, 0.f};
+      if (i0 + r < m) va = *reinterpret_cast<const f32x4*>(A + (i0 + r) * lda + p0 + c4);
+      if (j0 + r < n) vb = *reinterpret_cast<const f32x4*>(B + (j0 + r) * ldb + p0 + c4);
+      *reinterpret_cast<f32x4*>(As + r * kGP + c4) = va;
+      *reinterpret_cast<f32x4*>(Bs + r * kGP + c4) = vb;
     }
     __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      float a[4], b[4];
+    for (int kk = 0; kk < 16; kk += 4) {
+      f32x4 a[2], b[2];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        a[q] = As[kk][ty * 4 + q];
-        b[q] = Bs[kk][tx * 4 + q];
+      for (int s = 0; s < 2; ++s) {
+        a[s] = *reinterpret_cast<const f32x4*>(As + (wr * 64 + s * 32 + rl) * kGP + h * 16 + kk);
+        b[s] = *reinterpret_cast<const f32x4*>(Bs + (wc * 64 + s * 32 + rl) * kGP + h * 16 + kk);
       }
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int e = 0; e < 4; ++e)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[q][r] += a[q] * b[r];
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int y = 0; y < 2; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[x][e], b[y][e], acc[x][y], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t i = ib * kNB + ty * 4 + q;
-    if (i >= M) continue;
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t j = kb * kNB + tx * 4 + r;
-      if (j < M && j <= i) G[i * M + j] -= acc[q][r];
+    for (int y = 0; y < 2; ++y) {
+      const int64_t col = j0 + wc * 64 + y * 32 + rl;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = i0 + wr * 64 + x * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (row < m && col < n) {
+          float* c = C + row * ldc + col;
+          *c = beta == 0.f ? alpha * acc[x][y][r] : beta * *c + alpha * acc[x][y][r];
+        }
+      }
     }
-  }
 }
 
-// Multi-block path, triangular solves by segments [s0, s1) of at most kSeg
-// rows: one workgroup substitutes inside a segment (64-row blocks, one
-// wavefront per diagonal block); multi-block GEMVs carry a segment's
-// contribution to the rows outside it.
-constexpr int64_t kSeg = 2048;
+// ---- multi-block path: triangular solves ------------------------------------------------
+//
+// Segments [s0, s1) of at most kSeg rows: one workgroup loads the segment's
+// lower triangle into LDS (packed, row i at i(i+1)/2) and substitutes through
+// it in 64-row blocks (one wavefront per diagonal block); multi-block GEMVs
+// then carry the segment's unknowns to the rows outside it.
+
+constexpr size_t kTrsvLds = (kSeg * (kSeg + 1) / 2 + 2 * kSeg) * sizeof(float);
+
+// Packed triangle of rows/cols [s0, s1) and reciprocal pivots, all loads in flight at once.
+__device__ __forceinline__ void load_segment(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t len, float* Ls,
+                                    float* rd) {
+  const int64_t total = len * (len + 1) / 2;
+  constexpr int kPer = (kSeg * (kSeg + 1) / 2 + 1023) / 1024;
+  float v[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int64_t t = threadIdx.x + static_cast<int64_t>(q) * 1024;
+    int64_t i = static_cast<int64_t>((sqrtf(8.f * static_cast<float>(t) + 1.f) - 1.f) * 0.5f);
+    if (i * (i + 1) / 2 > t) --i;
+    if ((i + 1) * (i + 2) / 2 <= t) ++i;
+    const int64_t j = t - i * (i + 1) / 2;
+    v[q] = t < total ? G[(s0 + i) * ld + s0 + j] : 0.f;
+  }
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int64_t t = threadIdx.x + static_cast<int64_t>(q) * 1024;
+    if (t < total) Ls[t] = v[q];
+  }
+  __syncthreads();
+  for (int64_t i = threadIdx.x; i < len; i += blockDim.x) rd[i] = 1.0f / Ls[tri(i, i)];
+  __syncthreads();
+}
 
 // Forward: x[s0:s1) = L[s0:s1, s0:s1)^-1 rhs[s0:s1) (rhs holds the earlier segments' updates).
-__global__ void __launch_bounds__(1024) k_trsv_fwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
-                                                   float* __restrict__ rhs, float* __restrict__ x) {
-  __shared__ float Blk[kNB][kNB + 1];
-  __shared__ float rd[kNB];
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  for (int64_t o = s0; o < s1; o += kNB) {
-    const int nbe = static_cast<int>(s1 - o < kNB ? s1 - o : kNB);
-    for (int t = tid; t < kNB * kNB; t += nt) {      // strictly lower part of L_jj
-      const int r = t / kNB, c = t % kNB;
-      Blk[r][c] = (r < nbe && c < r) ? G[(o + r) * M + o + c] : 0.f;
-      if (c == r) rd[r] = r < nbe ? 1.0f / G[(o + r) * M + o + r] : 1.f;
-    }
-    __syncthreads();
+__global__ void __launch_bounds__(1024) k_trsv_fwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                   const float* __restrict__ rhs, float* __restrict__ x) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* Ls = reinterpret_cast<float*>(smem);
+  float* rd = Ls + kSeg * (kSeg + 1) / 2;
+  float* v = rd + kSeg;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, nw = blockDim.x >> 6;
+  const int64_t len = s1 - s0;
+  for (int64_t t = tid; t < len; t += blockDim.x) v[t] = rhs[s0 + t];
+  load_segment(G, ld, s0, len, Ls, rd);
+  for (int64_t ob = 0; ob < len; ob += kTB) {
+    const int nbe = static_cast<int>(len - ob < kTB ? len - ob : kTB);
     if (wave == 0) {
-      float b = lane < nbe ? rhs[o + lane] : 0.f;
-      float lr[kNB];
+      // b_k is final once the columns before k are applied: x_k = b_k / L_kk
+      const int r = lane < nbe ? lane : 0;
+      float b = lane < nbe ? v[ob + lane] : 0.f;
+      float lr[kTB];
 #pragma unroll
-      for (int c = 0; c < kNB; ++c) lr[c] = Blk[lane][c];
+      for (int c = 0; c < kTB; ++c) lr[c] = (lane < nbe && c < lane) ? Ls[tri(ob + r, ob + c)] : 0.f;
 #pragma unroll
-      for (int k = 0; k < kNB; ++k) b -= lr[k] * (bcast(b, k) * rd[k]);
-      if (lane < nbe) x[o + lane] = b * rd[lane];
+      for (int k = 0; k < kTB; ++k) {
+        const float rk = k < nbe ? rd[ob + k] : 1.f;
+        b -= lr[k] * (bcast(b, k) * rk);
+      }
+      if (lane < nbe) v[ob + lane] = b * rd[ob + lane];
     }
     __syncthreads();
-    for (int64_t i = o + nbe + tid; i < s1; i += nt) {
-      float acc = 0.f;
-      const float* row = G + i * M + o;
-#pragma unroll 8
-      for (int c = 0; c < nbe; ++c) acc += row[c] * x[o + c];
-      rhs[i] -= acc;
+    const float xo = lane < nbe ? v[ob + lane] : 0.f;
+    for (int64_t i = ob + nbe + wave; i < len; i += nw) {
+      const float p = wave_sum(lane < nbe ? Ls[tri(i, ob) + lane] * xo : 0.f);
+      if (lane == 0) v[i] -= p;
     }
     __syncthreads();
   }
+  for (int64_t t = tid; t < len; t += blockDim.x) x[s0 + t] = v[t];
 }
 
-// rhs[i] -= L[i, s0:s1) x[s0:s1) for i >= s1; one wavefront per row.
-__global__ void __launch_bounds__(256) k_gemv_fwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
-                                                  const float* __restrict__ x, float* __restrict__ rhs) {
+// rhs[i] -= L[i, s0:s1) x[s0:s1) for i >= s1; one wavefront per row, four floats per lane.
+__global__ void __launch_bounds__(256) k_gemv_fwd(const float* __restrict__ G, int64_t ld, int64_t M, int64_t s0,
+                                                  int64_t s1, const float* __restrict__ x, float* __restrict__ rhs) {
   const int lane = threadIdx.x & 63;
   const int64_t i = s1 + ((static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6);
   if (i >= M) return;
   float acc = 0.f;
-  for (int64_t c = s0 + lane; c < s1; c += 64) acc += G[i * M + c] * x[c];
-  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  for (int64_t c = s0 + 4 * lane; c < s1; c += 256) {
+    if (c + 4 <= s1) {
+      const f32x4 g = *reinterpret_cast<const f32x4*>(G + i * ld + c);
+      const f32x4 xv = *reinterpret_cast<const f32x4*>(x + c);
+      acc += g[0] * xv[0] + g[1] * xv[1] + g[2] * xv[2] + g[3] * xv[3];
+    } else {
+      for (int64_t e = c; e < s1; ++e) acc += G[i * ld + e] * x[e];
+    }
+  }
+  acc = wave_sum(acc);
   if (lane == 0) rhs[i] -= acc;
 }
 
 // Backward: z[s0:s1) = L[s0:s1, s0:s1)^-T x[s0:s1) into rhs (x holds the later segments' updates).
-__global__ void __launch_bounds__(1024) k_trsv_bwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
-                                                   float* __restrict__ x, float* __restrict__ rhs) {
-  __shared__ float Blk[kNB][kNB + 1];
-  __shared__ float rd[kNB];
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  for (int64_t o = s0 + ((s1 - s0 - 1) / kNB) * kNB; o >= s0; o -= kNB) {
-    const int nbe = static_cast<int>(s1 - o < kNB ? s1 - o : kNB);
-    for (int t = tid; t < kNB * kNB; t += nt) {      // Blk[r][k] = L[o+k][o+r], k > r
-      const int r = t / kNB, k = t % kNB;
-      Blk[r][k] = (k < nbe && r < k) ? G[(o + k) * M + o + r] : 0.f;
-      if (k == r) rd[r] = r < nbe ? 1.0f / G[(o + r) * M + o + r] : 1.f;
-    }
-    __syncthreads();
+__global__ void __launch_bounds__(1024) k_trsv_bwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                   const float* __restrict__ x, float* __restrict__ rhs) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* Ls = reinterpret_cast<float*>(smem);
+  float* rd = Ls + kSeg * (kSeg + 1) / 2;
+  float* v = rd + kSeg;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t len = s1 - s0;
+  for (int64_t t = tid; t < len; t += blockDim.x) v[t] = x[s0 + t];
+  load_segment(G, ld, s0, len, Ls, rd);
+  for (int64_t ob = ((len - 1) / kTB) * kTB; ob >= 0; ob -= kTB) {
+    const int nbe = static_cast<int>(len - ob < kTB ? len - ob : kTB);
     if (wave == 0) {
-      float b = lane < nbe ? x[o + lane] : 0.f;
-      float lc[kNB];
+      // lc[k] = L[ob+k][ob+lane] for k > lane: column `lane` of the block
+      const int r = lane < nbe ? lane : 0;
+      float b = lane < nbe ? v[ob + lane] : 0.f;
+      float lc[kTB];
 #pragma unroll
-      for (int k = 0; k < kNB; ++k) lc[k] = Blk[lane][k];
+      for (int k = 0; k < kTB; ++k) lc[k] = (lane < nbe && k > lane && k < nbe) ? Ls[tri(ob + k, ob + r)] : 0.f;
 #pragma unroll
-      for (int k = kNB - 1; k >= 0; --k) b -= lc[k] * (bcast(b, k) * rd[k]);
-      if (lane < nbe) rhs[o + lane] = b * rd[lane];
+      for (int k = kTB - 1; k >= 0; --k) {
+        const float rk = k < nbe ? rd[ob + k] : 1.f;
+        b -= lc[k] * (bcast(b, k) * rk);
+      }
+      if (lane < nbe) v[ob + lane] = b * rd[ob + lane];
     }
     __syncthreads();
-    for (int64_t i = s0 + tid; i < o; i += nt) {
+    for (int64_t i = tid; i < ob; i += blockDim.x) {
       float acc = 0.f;
-#pragma unroll 8
-      for (int c = 0; c < nbe; ++c) acc += G[(o + c) * M + i] * rhs[o + c];
-      x[i] -= acc;
+      for (int c = 0; c < nbe; ++c) acc += Ls[tri(ob + c, i)] * v[ob + c];
+      v[i] -= acc;
     }
     __syncthreads();
   }
+  for (int64_t t = tid; t < len; t += blockDim.x) rhs[s0 + t] = v[t];
 }
 
-// x[i] -= sum_{c in [s0, s1)} L[c, i] z[c] for i < s0; one thread per row (coalesced over i).
-__global__ void __launch_bounds__(256) k_gemv_bwd(const float* __restrict__ G, int64_t M, int64_t s0, int64_t s1,
+// x[i] -= sum_{c in [s0, s1)} L[c, i] z[c] for i < s0: 64 rows i per block
+// (coalesced over i), the segment split over four thread groups.
+__global__ void __launch_bounds__(256) k_gemv_bwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
                                                   const float* __restrict__ z, float* __restrict__ x) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= s0) return;
+  __shared__ float red[4][64];
+  const int il = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 64 + il;
   float acc = 0.f;
-  for (int64_t c = s0; c < s1; ++c) acc += G[c * M + i] * z[c];
-  x[i] -= acc;
+  if (i < s0) {
+#pragma unroll 8
+    for (int64_t c = s0 + g; c < s1; c += 4) acc += G[c * ld + i] * z[c];
+  }
+  red[g][il] = acc;
+  __syncthreads();
+  if (g == 0 && i < s0) x[i] -= (red[0][il] + red[1][il]) + (red[2][il] + red[3][il]);
 }
 
 __global__ void k_finish(const float* __restrict__ z, int64_t M, const double* __restrict__ scal,
@@ -815,6 +1084,20 @@ double binom_d(int64_t n, int64_t r) {
   return v;
 }
 
+// Whether `kernel` may be launched with `bytes` of dynamic LDS on the current
+// device; above the 64 KiB default, its limit is raised once to the device
+// maximum.
+bool allow_lds(const void* kernel, size_t bytes, bool& raised) {
+  if (bytes <= 65536) return true;
+  const int cap = gnnshap::max_lds_bytes();
+  if (bytes > static_cast<size_t>(cap)) return false;
+  if (!raised) {
+    raised = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, cap) == hipSuccess;
+    (void)hipGetLastError();
+  }
+  return raised;
+}
+
 }  // namespace
 
 extern "C" int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes) {
@@ -842,6 +1125,7 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   const Ws w = carve(cv, plan);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t M = plan->num_players;
+  const int64_t ld = ld_of(M);
   const int64_t wpr = plan->words_per_row;
   const int64_t half = plan->num_rows / 2;
   const int64_t rb0 = plan->random_begin;
@@ -868,82 +1152,88 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     const unsigned nb = static_cast<unsigned>(gnnshap::ceil_div(M, 64));
     {
       GS_TIMED("k_gram", s);
-      k_gram<<<dim3(nb, nb), 256, 0, s>>>(w.T, nrb, M, counts);
+      k_gram<<<dim3(nb, nb), 256, 0, s>>>(w.T, nrb, M, ld, counts);
     }
     GS_LAUNCHED();
   }
-  const int64_t nch = n_chunks(half);
+  const int64_t nch = n_chunks(half, wpr);
   const int64_t rpc = gnnshap::ceil_div(half, nch);
+  k_dz<<<static_cast<unsigned>(gnnshap::ceil_div(half, 256)), 256, 0, s>>>(y, half, M, w.classes, plan->num_classes,
+                                                                           f_empty_full, w.dz);
+  GS_LAUNCHED();
   {
     GS_TIMED("k_rhs_part", s);
-    k_rhs_part<<<static_cast<unsigned>(nch), 256, 0, s>>>(masks, wpr, half, M, y, w.classes, plan->num_classes,
-                                                           f_empty_full, rpc, w.part);
+    k_rhs_part<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(wpr, 4)), static_cast<unsigned>(nch)), 256, 0, s>>>(
+        masks, wpr, half, M, w.dz, rpc, w.part);
   }
   GS_LAUNCHED();
 
   const size_t small_bytes = small_lds_bytes(M);
-  if (small_bytes <= static_cast<size_t>(gnnshap::max_lds_bytes())) {
-    bool ok = small_bytes <= 65536;
-    if (!ok) {
-      ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_solve_small), hipFuncAttributeMaxDynamicSharedMemorySize,
-                               static_cast<int>(small_bytes)) == hipSuccess;
-      (void)hipGetLastError();
+  static bool small_lds = false;
+  if (allow_lds(reinterpret_cast<const void*>(&k_solve_small), small_bytes, small_lds)) {
+    {
+      GS_TIMED("k_solve_small", s);
+      k_solve_small<<<1, 256, small_bytes, s>>>(counts, ld, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
+                                                phi);
     }
-    if (ok) {
-      {
-        GS_TIMED("k_solve_small", s);
-        k_solve_small<<<1, 256, small_bytes, s>>>(counts, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
-                                                  phi);
-      }
-      GS_LAUNCHED();
-      return GNNSHAP_OK;
-    }
+    GS_LAUNCHED();
+    return GNNSHAP_OK;
   }
 
+  static bool potrf_lds = false, fwd_lds = false, bwd_lds = false;
+  if (!allow_lds(reinterpret_cast<const void*>(&k_potrf), kPotrfLds, potrf_lds) ||
+      !allow_lds(reinterpret_cast<const void*>(&k_trsv_fwd), kTrsvLds, fwd_lds) ||
+      !allow_lds(reinterpret_cast<const void*>(&k_trsv_bwd), kTrsvLds, bwd_lds))
+    return gnnshap::fail(GNNSHAP_EHIP, "device cannot give the solver %zu bytes of LDS", kTrsvLds);
   k_zero_info<<<1, 1, 0, s>>>(info);
   GS_LAUNCHED();
   if (has_random) {
-    k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, w.usum);
+    k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, ld, w.usum);
     GS_LAUNCHED();
   }
-  k_scalars<<<1, 256, 0, s>>>(counts, w.usum, M, has_random, alpha, wr, f_empty_full, w.scal);
+  k_scalars<<<1, 256, 0, s>>>(counts, w.usum, M, ld, has_random, alpha, wr, f_empty_full, w.scal);
   GS_LAUNCHED();
-  k_build<<<gnnshap::grid_for(M * M, 256, 16384), 256, 0, s>>>(w.G, w.usum, M, has_random, alpha, wr, w.scal);
+  k_build<<<static_cast<unsigned>(M), 256, 0, s>>>(w.G, w.usum, M, ld, has_random, alpha, wr, w.scal);
   GS_LAUNCHED();
-  k_rhs_finish<<<1, 1024, 0, s>>>(w.part, nch, M, w.rhs, w.scal);
+  const int64_t nbm = gnnshap::ceil_div(M, 256);
+  k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch, M, w.dv, w.bsum);
   GS_LAUNCHED();
-  const int64_t nblk = gnnshap::ceil_div(M, kNB);
-  for (int64_t jb = 0; jb < nblk; ++jb) {
+  k_rhs_center<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.dv, w.bsum, nbm, M, w.rhs);
+  GS_LAUNCHED();
+  for (int64_t o = 0; o < M; o += kPB) {
     {
       GS_TIMED("k_potrf", s);
-      k_potrf<<<1, 64, 0, s>>>(w.G, M, jb, info, w.Ld);
+      k_potrf<<<1, 256, kPotrfLds, s>>>(w.G, ld, M, o, info, w.Winv);
     }
     GS_LAUNCHED();
-    const int64_t rest = nblk - jb - 1;
-    if (rest > 0) {
-      const int64_t rows = M - (jb + 1) * kNB;
-      {
-        GS_TIMED("k_trsm", s);
-        k_trsm<<<static_cast<unsigned>(gnnshap::ceil_div(rows, 256)), 256, 0, s>>>(w.G, M, jb, w.Ld);
-      }
-      GS_LAUNCHED();
-      {
-        GS_TIMED("k_syrk", s);
-        k_syrk<<<dim3(static_cast<unsigned>(rest), static_cast<unsigned>(rest)), 256, 0, s>>>(w.G, M, jb);
-      }
-      GS_LAUNCHED();
+    const int64_t r0 = o + kPB;
+    if (r0 >= M) break;
+    const int64_t rows = M - r0;
+    const int64_t tr = gnnshap::ceil_div(rows, kGT);
+    float* panel = w.G + r0 * ld + o;
+    {
+      GS_TIMED("k_trsm", s);   // panel <- panel L_jj^-T = panel Winv^T
+      k_gemm_nt<false><<<static_cast<unsigned>(tr), 256, 0, s>>>(panel, ld, w.Winv, kPB, panel, ld, rows, kPB, kPB,
+                                                                  1.f, 0.f, 1);
     }
+    GS_LAUNCHED();
+    {
+      GS_TIMED("k_syrk", s);   // trailing lower triangle -= panel panel^T
+      k_gemm_nt<true><<<static_cast<unsigned>(tr * (tr + 1) / 2), 256, 0, s>>>(panel, ld, panel, ld, w.G + r0 * ld + r0,
+                                                                                ld, rows, rows, kPB, -1.f, 1.f, 0);
+    }
+    GS_LAUNCHED();
   }
   // L x = rhs, L^T psi = x (psi into rhs), phi = Delta/M + psi
   for (int64_t s0 = 0; s0 < M; s0 += kSeg) {
     const int64_t s1 = std::min(M, s0 + kSeg);
     {
       GS_TIMED("k_trsv", s);
-      k_trsv_fwd<<<1, 1024, 0, s>>>(w.G, M, s0, s1, w.rhs, w.x);
+      k_trsv_fwd<<<1, 1024, kTrsvLds, s>>>(w.G, ld, s0, s1, w.rhs, w.x);
     }
     GS_LAUNCHED();
     if (s1 < M) {
-      k_gemv_fwd<<<static_cast<unsigned>(gnnshap::ceil_div((M - s1) * 64, 256)), 256, 0, s>>>(w.G, M, s0, s1, w.x,
+      k_gemv_fwd<<<static_cast<unsigned>(gnnshap::ceil_div((M - s1) * 64, 256)), 256, 0, s>>>(w.G, ld, M, s0, s1, w.x,
                                                                                              w.rhs);
       GS_LAUNCHED();
     }
@@ -952,11 +1242,11 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     const int64_t s1 = std::min(M, s0 + kSeg);
     {
       GS_TIMED("k_trsv", s);
-      k_trsv_bwd<<<1, 1024, 0, s>>>(w.G, M, s0, s1, w.x, w.rhs);
+      k_trsv_bwd<<<1, 1024, kTrsvLds, s>>>(w.G, ld, s0, s1, w.x, w.rhs);
     }
     GS_LAUNCHED();
     if (s0 > 0) {
-      k_gemv_bwd<<<static_cast<unsigned>(gnnshap::ceil_div(s0, 256)), 256, 0, s>>>(w.G, M, s0, s1, w.rhs, w.x);
+      k_gemv_bwd<<<static_cast<unsigned>(gnnshap::ceil_div(s0, 64)), 256, 0, s>>>(w.G, ld, s0, s1, w.rhs, w.x);
       GS_LAUNCHED();
     }
   }
