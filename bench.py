@@ -2,9 +2,12 @@
 
 One step = Alg. 1 for every target of the Cora-shaped workload (2,708 nodes,
 10,556 directed edges, 2-layer GCN 16 hidden / 7 classes, 100 targets with
-20..400 players, 10,000 coalitions each): extract the computational graph,
-plan, sample, evaluate every coalition, solve the least squares.  Inputs
-(graph, features, weights) are resident in HBM before the timed region.
+20..400 players, 10,000 coalitions each): extract the computational graphs,
+plan, sample, evaluate every coalition, solve the least squares.  By default
+the whole batch of targets goes through one launch per step
+(gnnshap_extract_batch + gnnshap_explain_batch); --mode streams runs the
+single-target calls on several streams instead.  Inputs (graph, features,
+weights) are resident in HBM before the timed region.
 
 Prints one JSON line: coalition evaluations per second over the whole job,
 explain latency per target (host wall time from extraction to phi on the
@@ -29,6 +32,8 @@ def parse():
     ap.add_argument("--config", default="cora")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--mode", choices=["batch", "streams"], default="batch",
+                    help="batch: one launch per step for all targets; streams: per-target calls on several streams")
     ap.add_argument("--streams", type=int, default=3)
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -64,59 +69,63 @@ def cpu_baseline(cfg, seconds):
 HBM_PEAK_GBS = 8000.0
 VALU_FP32_TFLOPS = 78.6
 VALU_INT_TOPS = 39.3
-SMALL_SOLVE_LDS = 163840      # LDS of one workgroup on gfx950: the one-workgroup solve's limit
-
-
-def _small_solve(M):
-    return M * 16 + (M * (M + 1) // 2) * 4 <= SMALL_SOLVE_LDS
 
 
 def work_model(kernel, results, dims):
     """Algorithmic work of the timed kernel over one step: (amount, unit, bound, peak).
 
-    k_solve_small  M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
+    k_solve_small / k_solve_mid / k_solve_one_batch (one-workgroup solves)
+                   M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
     k_eval_l2      (k/2) M h useful MACs per target (complement pairs cover every
                    player-feature product once) + the layer-2 dot products
     k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
                    per 64 rows and pair
     k_sample       k x ceil(M/64) x 8 bytes of masks + 4 k bytes of weights written
     k_rhs_part     (k/2) x ceil(M/64) x 8 bytes of masks + 4 k bytes of y read
+    (a *_batch kernel does the same work for every target of the batch)
     """
+    from paper_2401_04829_amd import _lib
     h = dims[1]
+    base = kernel[:-len("_batch")] if kernel.endswith("_batch") else kernel
     tot = 0.0
     for r in results:
         M, k = r.plan.num_players, r.plan.num_rows
         wpr = r.plan.words_per_row
         kr = k // 2 - r.plan.random_begin
-        if kernel == "k_solve_small":
-            if _small_solve(M):
+        if base in ("k_solve_small", "k_solve_mid", "k_solve_one"):
+            path = _lib.gnnshap_solve_info(r.plan)
+            if (base == "k_solve_small" and path == 1) or (base == "k_solve_mid" and path == 2) or \
+                    (base == "k_solve_one" and path in (1, 2)):
                 tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
-        elif kernel == "k_eval_l2":
+        elif base == "k_eval_l2":
             n1 = r.sub.sg.hop_ptr[2]
             tot += 2.0 * ((k / 2.0) * M * h + k * n1 * h)
-        elif kernel == "k_gram":
+        elif base == "k_gram":
             tot += (kr / 64.0) * M * (M + 1) / 2.0
-        elif kernel == "k_sample":
+        elif base == "k_sample":
             tot += k * wpr * 8.0 + 4.0 * k
-        elif kernel == "k_rhs_part":
+        elif base == "k_rhs_part":
             tot += (k / 2.0) * wpr * 8.0 + 4.0 * k
-    if kernel in ("k_sample", "k_rhs_part"):
+    if base in ("k_sample", "k_rhs_part"):
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
-    if kernel == "k_gram":
+    if base == "k_gram":
         return tot, "Tops/s", "alu", VALU_INT_TOPS
     return tot, "TFLOP/s", "alu", VALU_FP32_TFLOPS
 
 
-CANDIDATES = ["k_solve_small", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"]
+CANDIDATES = {
+    "batch": ["k_solve_one_batch", "k_eval_l2_batch", "k_rhs_part_batch", "k_gram_batch", "k_sample_batch"],
+    "streams": ["k_solve_small", "k_solve_mid", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
+}
 
 
-def roofline(step, lib, dims):
+def roofline(step, lib, dims, mode):
     """Times each candidate kernel with HIP events over one step, picks the
     one with the largest total and relates its algorithmic work to its
     average launch duration."""
     import torch
     best = None
-    for name in CANDIDATES:
+    for name in CANDIDATES[mode]:
         lib.gnnshap_timing_begin(name)
         _, res = step()
         torch.cuda.synchronize()
@@ -171,7 +180,10 @@ def main():
 
     def step():
         ex.prepare()                 # X W_1 once per step, shared by every target
-        res = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=args.streams)
+        if args.mode == "batch":
+            res = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+        else:
+            res = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=args.streams)
         return sum(r.plan.num_rows for r in res), res
 
     if args.copy_probe:
@@ -220,14 +232,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.config}: {len(targets)} targets, {cfg['p']} coalitions each, "
                                f"{cfg['indptr'].size - 1} nodes, {cfg['indices'].size} edges, "
-                               f"GCN {cfg['dims']}, {cfg['hops']}-hop"},
+                               f"GCN {cfg['dims']}, {cfg['hops']}-hop",
+                   "mode": args.mode},
         "latency_ms": {"median": statistics.median(lat), "p90": p90, "targets": len(lat)},
         "roofline": None,
         "cpu_baseline": None,
     }
     if not args.no_roofline:
         from paper_2401_04829_amd import _lib
-        out["roofline"] = roofline(step, _lib, cfg["dims"])
+        out["roofline"] = roofline(step, _lib, cfg["dims"], args.mode)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out))

@@ -240,8 +240,63 @@ int gnnshap_solve_wls(const gnnshap_sample_plan* plan,
                       int32_t* info, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* 5. Many targets per launch sequence (Alg. 1 for each of n targets).      */
+/*                                                                          */
+/* The explanations of different targets are independent (Alg. 1 runs per  */
+/* target node); these calls run each step for a whole batch of targets in  */
+/* one launch, so that targets with small computational graphs fill the     */
+/* GPU together.  Every output equals, bit for bit, what the single-target  */
+/* calls above give for the same arguments.                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace for gnnshap_extract_batch on a graph of
+ * num_nodes nodes and n targets. */
+int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, size_t* bytes);
+
+/* gnnshap_extract_subgraph for targets[0 .. n) ([host] int64) into sgs[0 .. n)
+ * ([host] array; each entry has its own num_hops, capacities and [dev]
+ * output arrays, as for the single call).  One workgroup per target, one
+ * host synchronisation for the batch; `ws` zero-filled before first use and
+ * left zero-filled.  Sizes are filled in for every target; if any target
+ * does not fit its capacities, returns GNNSHAP_ECAPACITY (the targets that
+ * fit are complete).  EUNSUPPORTED: graphs of more than 2^18 nodes (use the
+ * single-target call there).  EINVAL as for the single call. */
+int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
+                          gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream);
+
+/* Bytes of device workspace for gnnshap_explain_batch. */
+int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                    int64_t n, const gnnshap_gcn* m, size_t* bytes);
+
+/* Sampling, predictions and least squares of n targets.  sgs[t] ([host]) is
+ * target t's extracted subgraph and plans[t] ([host]) its plan (from
+ * gnnshap_plan_samples, num_players = sgs[t].num_edges); `classes` [host] is
+ * the concatenation of the n class tables in target order (copied on
+ * `stream`; keep it unchanged until then).  Outputs ([dev]) are packed in
+ * target order:
+ *   masks    rows of target t start at word sum_{s<t} k_s * words_per_row_s;
+ *   weights, y   start at sum_{s<t} k_s;
+ *   phi      starts at sum_{s<t} M_s;
+ *   f_empty_full[2t .. 2t+1], class_out[t] (may be NULL), info[t].
+ * X, target_class and the model as for gnnshap_eval_coalitions.  Two-layer
+ * models with X W_1 given and one-workgroup systems run batched; other
+ * targets go through the single-target kernels in the same sequence.
+ * EUNSUPPORTED: more than 65535 targets or M > 131072. */
+int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                          const gnnshap_class* classes, int64_t n, const gnnshap_gcn* m,
+                          const float* X, int32_t target_class, uint64_t* masks, float* weights,
+                          float* y, float* f_empty_full, int32_t* class_out, float* phi,
+                          int32_t* info, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics: HIP-event timing of one kernel.                             */
 /* ------------------------------------------------------------------------ */
+
+/* Which solver the plan's system takes: *path = 1 if one workgroup
+ * assembles, factors and solves it in LDS (its lower triangle fits one CU's
+ * LDS), 2 if one workgroup factors it in global memory (M <= 448), 0 if it
+ * takes the multi-block Cholesky.  Needs the device (queries LDS limits). */
+int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path);
 
 /* Arms timing for the kernels whose name starts with `kernel_name` (e.g.
  * "k_solve_small", "k_eval_l2"): every later launch of such a kernel, from

@@ -64,6 +64,15 @@ _SIGNATURES = {
     "gnnshap_solve_workspace": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(ctypes.c_size_t)]),
     "gnnshap_solve_wls": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(gnnshap_class), c_vp, c_vp, c_vp, c_vp,
                                          c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_extract_batch_workspace": (ctypes.c_int, [c_i64, c_i64, _P(ctypes.c_size_t)]),
+    "gnnshap_extract_batch": (ctypes.c_int, [_P(gnnshap_graph), _P(c_i64), c_i64, _P(gnnshap_subgraph), c_vp,
+                                             ctypes.c_size_t, c_vp]),
+    "gnnshap_explain_batch_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), c_i64,
+                                                       _P(gnnshap_gcn), _P(ctypes.c_size_t)]),
+    "gnnshap_explain_batch": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), _P(gnnshap_class),
+                                             c_i64, _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                             c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_solve_info": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(c_i32)]),
     "gnnshap_timing_begin": (ctypes.c_int, [ctypes.c_char_p]),
     "gnnshap_timing_end": (ctypes.c_int, [_P(ctypes.c_double), _P(c_i64)]),
 }
@@ -180,3 +189,38 @@ def gnnshap_timing_end():
 def gnnshap_solve_wls(plan, classes, masks_ptr, y_ptr, fef_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):
     check(load().gnnshap_solve_wls(ctypes.byref(plan), classes, masks_ptr, y_ptr, fef_ptr, phi_ptr, info_ptr,
                                    ws_ptr, ws_bytes, stream), "solve_wls")
+
+
+def gnnshap_extract_batch_workspace(num_nodes, n):
+    b = ctypes.c_size_t()
+    check(load().gnnshap_extract_batch_workspace(num_nodes, n, ctypes.byref(b)), "extract_batch_workspace")
+    return b.value
+
+
+def gnnshap_extract_batch(graph, targets, sgs, ws_ptr, ws_bytes, stream):
+    """targets: ctypes int64 array; sgs: ctypes array of gnnshap_subgraph.  Returns OK or ECAPACITY."""
+    st = load().gnnshap_extract_batch(ctypes.byref(graph), targets, len(sgs), sgs, ws_ptr, ws_bytes, stream)
+    if st not in (OK, ECAPACITY):
+        check(st, "extract_batch")
+    return st
+
+
+def gnnshap_explain_batch_workspace(sgs, plans, model):
+    b = ctypes.c_size_t()
+    check(load().gnnshap_explain_batch_workspace(sgs, plans, len(sgs), ctypes.byref(model), ctypes.byref(b)),
+          "explain_batch_workspace")
+    return b.value
+
+
+def gnnshap_explain_batch(sgs, plans, classes, model, X_ptr, target_class, masks_ptr, weights_ptr, y_ptr, fef_ptr,
+                          cls_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):
+    check(load().gnnshap_explain_batch(sgs, plans, classes, len(sgs), ctypes.byref(model), X_ptr, target_class,
+                                       masks_ptr, weights_ptr, y_ptr, fef_ptr, cls_ptr, phi_ptr, info_ptr, ws_ptr,
+                                       ws_bytes, stream), "explain_batch")
+
+
+def gnnshap_solve_info(plan):
+    """Solver path of the plan's system: 1 one workgroup in LDS, 2 one workgroup in global memory, 0 multi-block."""
+    v = c_i32()
+    check(load().gnnshap_solve_info(ctypes.byref(plan), ctypes.byref(v)), "solve_info")
+    return v.value

@@ -1,0 +1,83 @@
+// Internal interface of the multi-target path: per-target job records that
+// batched kernels read with blockIdx.y / blockIdx.z = target, and the
+// launchers each stage exports to the batch driver.
+#pragma once
+
+#include "common.h"
+
+namespace gnnshap {
+
+// ---- sampling ---------------------------------------------------------------------------
+struct SampleJob {
+  const gnnshap_class* cls;  // device copy of the class table
+  int64_t ncls, half, M, wpr;
+  uint32_t seed_lo, seed_hi, st_lo, st_hi;
+  uint64_t* masks;
+  float* weights;
+};
+// Samples every job's rows: grid (row blocks, n).
+int launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t max_half, int64_t max_wpr, hipStream_t s);
+
+// ---- evaluation (two-layer GCN, one pass per target) -------------------------------------
+struct EvalJob {
+  const int32_t* node_gid;
+  const int32_t* dst_ptr;
+  const int32_t* edge_src;
+  int64_t n_nodes, n_dst, n1, M, wpr, k;
+  const uint64_t* masks;
+  float* y;
+  float* fef;
+  int32_t* cls_out;
+  // workspace
+  int32_t* ctl;
+  uint64_t* sp_masks;
+  int32_t* sp_rows;
+  float* sp_y;
+  int32_t* live_rows;
+  uint8_t* live_flag;
+  float* Zc1;
+};
+struct EvalModel {
+  const float* XW1;
+  const float* b1;
+  const float* W2;
+  const float* b2;
+  int h, C;
+  int32_t target_class;
+};
+// Whether one target can go through the batched evaluation, and the bytes of
+// its workspace slice.
+bool eval_batchable(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k);
+size_t eval_slice_bytes(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k);
+// Carves job.ctl .. job.Zc1 from a slice.
+void eval_carve_slice(void* base, const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, EvalJob* job);
+int launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& md, int64_t max_nodes, int64_t max_ndst,
+                      int64_t max_n1, int64_t max_wpr, int64_t max_k, hipStream_t s);
+
+// ---- least squares (one-workgroup systems) -----------------------------------------------
+struct SolveJob {
+  const uint64_t* masks;
+  const float* y;
+  const float* fef;
+  float* phi;
+  int32_t* info;
+  const gnnshap_class* cls;  // device copy
+  int64_t ncls, M, wpr, half, rb0, kr, nrb, ld, nch, rpc;
+  double alpha, wr;
+  uint64_t* T;
+  int32_t* counts;
+  double* dz;
+  double* part;
+  int64_t* usum;
+  double* dv;
+  float* Wd;
+  int32_t mid;               // 1: the global-memory one-workgroup path, 0: the LDS-resident one
+};
+// Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
+bool solve_batchable(const gnnshap_sample_plan* plan);
+size_t solve_slice_bytes(const gnnshap_sample_plan* plan);
+int solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice, SolveJob* job);
+int launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
+                       int64_t max_nrb, int64_t max_nch, hipStream_t s);
+
+}  // namespace gnnshap

@@ -1,0 +1,219 @@
+// Many targets per launch sequence: sampling, evaluation and the least squares
+// of n explanations (Alg. 1 steps 2-5 of the GNNShap paper for each target),
+// one launch per step for the whole batch, so small targets fill the GPU
+// together instead of one after another.  Targets whose evaluation or system
+// does not fit the batched kernels go through the single-target calls inside
+// the same sequence; every value is the one the single-target calls give.
+#include <algorithm>
+#include <vector>
+
+#include "batch.h"
+#include "common.h"
+
+namespace {
+
+struct Layout {
+  int64_t n = 0, classes = 0;
+  std::vector<int64_t> mask_off, row_off, player_off, class_off;
+  std::vector<size_t> eval_bytes, solve_bytes;
+};
+
+int make_layout(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, int64_t n, const gnnshap_gcn* m,
+                Layout* L) {
+  if (!sgs || !plans || !m || n < 1) return gnnshap::fail(GNNSHAP_EINVAL, "null argument or n < 1");
+  if (n > 65535) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  L->n = n;
+  L->mask_off.resize(n + 1);
+  L->row_off.resize(n + 1);
+  L->player_off.resize(n + 1);
+  L->class_off.resize(n + 1);
+  L->eval_bytes.resize(n);
+  L->solve_bytes.resize(n);
+  L->mask_off[0] = L->row_off[0] = L->player_off[0] = L->class_off[0] = 0;
+  for (int64_t t = 0; t < n; ++t) {
+    const gnnshap_sample_plan& p = plans[t];
+    if (p.num_players != sgs[t].num_edges)
+      return gnnshap::fail(GNNSHAP_EINVAL, "plan %lld is not for subgraph %lld's players", (long long)t, (long long)t);
+    size_t eb = 0, sb = 0;
+    if (int st = gnnshap_eval_workspace(&sgs[t], m, p.num_rows, &eb)) return st;
+    if (int st = gnnshap_solve_workspace(&p, &sb)) return st;
+    L->eval_bytes[t] = eb;
+    L->solve_bytes[t] = sb;
+    L->mask_off[t + 1] = L->mask_off[t] + p.num_rows * p.words_per_row;
+    L->row_off[t + 1] = L->row_off[t] + p.num_rows;
+    L->player_off[t + 1] = L->player_off[t] + p.num_players;
+    L->class_off[t + 1] = L->class_off[t] + p.num_classes;
+  }
+  L->classes = L->class_off[n];
+  return GNNSHAP_OK;
+}
+
+struct BatchWs {
+  gnnshap_class* classes;
+  gnnshap::SampleJob* sample;
+  gnnshap::EvalJob* eval;
+  gnnshap::SolveJob* solve;
+  std::vector<char*> eval_slice, solve_slice;
+};
+
+BatchWs carve(gnnshap::Carver& c, const Layout& L) {
+  BatchWs b;
+  b.classes = c.take<gnnshap_class>(L.classes);
+  b.sample = c.take<gnnshap::SampleJob>(L.n);
+  b.eval = c.take<gnnshap::EvalJob>(L.n);
+  b.solve = c.take<gnnshap::SolveJob>(L.n);
+  b.eval_slice.resize(L.n);
+  b.solve_slice.resize(L.n);
+  for (int64_t t = 0; t < L.n; ++t) b.eval_slice[t] = c.take<char>(L.eval_bytes[t]);
+  for (int64_t t = 0; t < L.n; ++t) b.solve_slice[t] = c.take<char>(L.solve_bytes[t]);
+  return b;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                               int64_t n, const gnnshap_gcn* model, size_t* bytes) {
+  gnnshap::clear_error();
+  if (!bytes) return gnnshap::fail(GNNSHAP_EINVAL, "bytes is NULL");
+  Layout L;
+  if (int st = make_layout(sgs, plans, n, model, &L)) return st;
+  gnnshap::Carver c(nullptr);
+  carve(c, L);
+  *bytes = c.bytes();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                     const gnnshap_class* classes, int64_t n, const gnnshap_gcn* model,
+                                     const float* X, int32_t target_class, uint64_t* masks, float* weights,
+                                     float* y, float* f_empty_full, int32_t* class_out, float* phi, int32_t* info,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  Layout L;
+  if (int st = make_layout(sgs, plans, n, model, &L)) return st;
+  if (!classes || !masks || !weights || !y || !f_empty_full || !phi || !info || !ws)
+    return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  gnnshap::Carver need(nullptr);
+  carve(need, L);
+  if (ws_bytes < need.bytes()) return gnnshap::fail(GNNSHAP_ECAPACITY, "batch workspace needs %zu bytes", need.bytes());
+  gnnshap::Carver cv(ws);
+  const BatchWs b = carve(cv, L);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int64_t t = 0; t < n; ++t) {
+    if (plans[t].num_players > 131072)
+      return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "sampler supports up to 131072 players");
+    int64_t row = 0;
+    const gnnshap_class* ct = classes + L.class_off[t];
+    for (int64_t i = 0; i < plans[t].num_classes; ++i) {
+      if (ct[i].row_begin != row || ct[i].row_count < 1 || ct[i].size < 1 ||
+          2 * static_cast<int64_t>(ct[i].size) > plans[t].num_players)
+        return gnnshap::fail(GNNSHAP_EINVAL, "class table of target %lld inconsistent", (long long)t);
+      row += ct[i].row_count;
+    }
+    if (row != plans[t].num_rows / 2) return gnnshap::fail(GNNSHAP_EINVAL, "class table of target %lld short", (long long)t);
+  }
+  GS_HIP(hipMemcpyAsync(b.classes, classes, L.classes * sizeof(gnnshap_class), hipMemcpyHostToDevice, s));
+
+  // 1. sampling
+  std::vector<gnnshap::SampleJob> sj(n);
+  int64_t max_half = 0, max_wpr = 0, max_k = 0, max_M = 0;
+  for (int64_t t = 0; t < n; ++t) {
+    const gnnshap_sample_plan& p = plans[t];
+    sj[t] = gnnshap::SampleJob{b.classes + L.class_off[t], p.num_classes, p.num_rows / 2, p.num_players,
+                               p.words_per_row, static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32),
+                               static_cast<uint32_t>(p.stream_id), static_cast<uint32_t>(p.stream_id >> 32),
+                               masks + L.mask_off[t], weights + L.row_off[t]};
+    max_half = std::max(max_half, p.num_rows / 2);
+    max_wpr = std::max(max_wpr, p.words_per_row);
+    max_k = std::max(max_k, p.num_rows);
+    max_M = std::max(max_M, p.num_players);
+  }
+  GS_HIP(hipMemcpyAsync(b.sample, sj.data(), n * sizeof(gnnshap::SampleJob), hipMemcpyHostToDevice, s));
+  if (int st = gnnshap::launch_sample_batch(b.sample, n, max_half, max_wpr, s)) return st;
+
+  // 2. coalition values
+  bool eval_all = model->num_layers == 2 && model->XW1;
+  for (int64_t t = 0; t < n && eval_all; ++t) eval_all = gnnshap::eval_batchable(&sgs[t], model, plans[t].num_rows);
+  int st_eval = GNNSHAP_EUNSUPPORTED;
+  if (eval_all) {
+    std::vector<gnnshap::EvalJob> ej(n);
+    int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0;
+    for (int64_t t = 0; t < n; ++t) {
+      const gnnshap_subgraph& g = sgs[t];
+      gnnshap::EvalJob& J = ej[t];
+      J = gnnshap::EvalJob{};
+      J.node_gid = g.node_gid;
+      J.dst_ptr = g.dst_ptr;
+      J.edge_src = g.edge_src;
+      J.n_nodes = g.num_nodes;
+      J.n_dst = g.num_dst;
+      J.n1 = g.hop_ptr[2];
+      J.M = g.num_edges;
+      J.wpr = plans[t].words_per_row;
+      J.k = plans[t].num_rows;
+      J.masks = masks + L.mask_off[t];
+      J.y = y + L.row_off[t];
+      J.fef = f_empty_full + 2 * t;
+      J.cls_out = class_out ? class_out + t : nullptr;
+      gnnshap::eval_carve_slice(b.eval_slice[t], &g, model, J.k, &J);
+      max_nodes = std::max(max_nodes, J.n_nodes);
+      max_ndst = std::max(max_ndst, J.n_dst);
+      max_n1 = std::max(max_n1, J.n1);
+    }
+    GS_HIP(hipMemcpyAsync(b.eval, ej.data(), n * sizeof(gnnshap::EvalJob), hipMemcpyHostToDevice, s));
+    const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
+                                model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
+    st_eval = gnnshap::launch_eval_batch(b.eval, n, md, max_nodes, max_ndst, max_n1, max_wpr, max_k, s);
+    if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
+    gnnshap::clear_error();
+  }
+  if (st_eval != GNNSHAP_OK) {
+    for (int64_t t = 0; t < n; ++t) {
+      const gnnshap_sample_plan& p = plans[t];
+      if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
+                                           p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
+                                           class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t], s))
+        return st;
+    }
+  }
+
+  // 3. least squares: one-workgroup systems batched, the rest one by one
+  std::vector<gnnshap::SolveJob> vj;
+  std::vector<int64_t> rest;
+  int64_t bM = 0, bw = 0, bh = 0, bnrb = 0, bnch = 0;
+  for (int64_t t = 0; t < n; ++t) {
+    const gnnshap_sample_plan& p = plans[t];
+    if (!gnnshap::solve_batchable(&p)) {
+      rest.push_back(t);
+      continue;
+    }
+    gnnshap::SolveJob J{};
+    if (int st = gnnshap::solve_fill_job(&p, classes + L.class_off[t], b.solve_slice[t], &J)) return st;
+    J.masks = masks + L.mask_off[t];
+    J.y = y + L.row_off[t];
+    J.fef = f_empty_full + 2 * t;
+    J.phi = phi + L.player_off[t];
+    J.info = info + t;
+    J.cls = b.classes + L.class_off[t];
+    bM = std::max(bM, J.M);
+    bw = std::max(bw, J.wpr);
+    bh = std::max(bh, J.half);
+    bnrb = std::max(bnrb, J.nrb);
+    bnch = std::max(bnch, J.nch);
+    vj.push_back(J);
+  }
+  if (!vj.empty()) {
+    GS_HIP(hipMemcpyAsync(b.solve, vj.data(), vj.size() * sizeof(gnnshap::SolveJob), hipMemcpyHostToDevice, s));
+    if (int st = gnnshap::launch_solve_batch(b.solve, static_cast<int64_t>(vj.size()), bM, bw, bh, bnrb, bnch, s))
+      return st;
+  }
+  for (int64_t t : rest) {
+    if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
+                                   f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
+                                   L.solve_bytes[t], s))
+      return st;
+  }
+  return GNNSHAP_OK;
+  GS_TRY_END
+}

@@ -18,6 +18,7 @@
 // Coalitions without an in-edge of v are not evaluated (Sec. 3.4.1): their
 // value is f(empty), which is exact.  f(empty) and f(E_c) come from two extra
 // rows (no players / all players) run through the same kernels first.
+#include "batch.h"
 #include "common.h"
 
 namespace {
@@ -412,13 +413,13 @@ __global__ void __launch_bounds__(256) k_final(
 //            H^1[b, x] . W_2[:, c] for the explained class (or every class);
 //   layer 2  y = d_v^-1/2 (sum_{(u->v) in S} d_u^-1/2 t[u] + d_v^-1/2 t[v]) + b_2.
 template <int FPT>
-__global__ void __launch_bounds__(256) k_eval_l2(
+__device__ __forceinline__ void eval_l2_body(
     const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t row_off,
     int64_t cap, const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr,
     const int32_t* __restrict__ edge_src, int64_t n_dst, int64_t n1, const float* __restrict__ Zc,
     const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
     const int32_t* __restrict__ ctl, bool all_classes, int tbr, float* __restrict__ y_rows,
-    float* __restrict__ y_all) {
+    float* __restrict__ y_all, int64_t block) {
   constexpr int FS = 8 * FPT;
   extern __shared__ __align__(16) float sm[];
   const int ncls = all_classes ? C : 1;
@@ -427,7 +428,7 @@ __global__ void __launch_bounds__(256) k_eval_l2(
   float* zs = tt + tbr * n1 * ncls;                   // 64 x FS
   int32_t* ss = reinterpret_cast<int32_t*>(zs + kChunkE * FS);
   const int64_t nr = rows_in_pass(dyn_count, row_off, cap);
-  const int64_t b_base = static_cast<int64_t>(blockIdx.x) * tbr;
+  const int64_t b_base = block * tbr;
   if (b_base >= nr) return;
   const int tid = threadIdx.x;
   const int tb = tid >> 3, fg = tid & 7;
@@ -538,8 +539,20 @@ __global__ void __launch_bounds__(256) k_eval_l2(
   }
 }
 
-__global__ void k_pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
-                             int32_t* class_out, float* f_empty_full) {
+template <int FPT>
+__global__ void __launch_bounds__(256) k_eval_l2(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t row_off,
+    int64_t cap, const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr,
+    const int32_t* __restrict__ edge_src, int64_t n_dst, int64_t n1, const float* __restrict__ Zc,
+    const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
+    const int32_t* __restrict__ ctl, bool all_classes, int tbr, float* __restrict__ y_rows,
+    float* __restrict__ y_all) {
+  eval_l2_body<FPT>(masks, wpr, rows, row_off, cap, dyn_count, dst_ptr, edge_src, n_dst, n1, Zc, b1, W2, b2, h, C,
+                    ctl, all_classes, tbr, y_rows, y_all, blockIdx.x);
+}
+
+__device__ __forceinline__ void pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
+                                           int32_t* class_out, float* f_empty_full) {
   int c = requested;
   if (c < 0) {
     c = 0;
@@ -552,10 +565,15 @@ __global__ void k_pick_class(const float* __restrict__ sp_y, int C, int requeste
   f_empty_full[1] = sp_y[C + c];
 }
 
+__global__ void k_pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
+                             int32_t* class_out, float* f_empty_full) {
+  pick_class(sp_y, C, requested, ctl, class_out, f_empty_full);
+}
+
 // A coalition is evaluated only if it holds an in-edge of v (players [0, indeg v)).
-__global__ void __launch_bounds__(256) k_live(const uint64_t* __restrict__ masks, int64_t wpr,
-                                              int64_t k, const int32_t* __restrict__ dst_ptr,
-                                              int32_t* ctl, int32_t* live_rows, uint8_t* live_flag) {
+__device__ __forceinline__ void live_rows_of(const uint64_t* __restrict__ masks, int64_t wpr, int64_t k,
+                                             const int32_t* __restrict__ dst_ptr, int32_t* ctl,
+                                             int32_t* live_rows, uint8_t* live_flag) {
   const int lane = threadIdx.x & 63;
   const int64_t indeg = dst_ptr[1];
   const int64_t nwords = (indeg + 63) >> 6;
@@ -584,6 +602,12 @@ __global__ void __launch_bounds__(256) k_live(const uint64_t* __restrict__ masks
       if (live) live_rows[base + __popcll(bal & ((1ull << lane) - 1ull))] = static_cast<int32_t>(b);
     }
   }
+}
+
+__global__ void __launch_bounds__(256) k_live(const uint64_t* __restrict__ masks, int64_t wpr,
+                                              int64_t k, const int32_t* __restrict__ dst_ptr,
+                                              int32_t* ctl, int32_t* live_rows, uint8_t* live_flag) {
+  live_rows_of(masks, wpr, k, dst_ptr, ctl, live_rows, live_flag);
 }
 
 __global__ void k_fill_pruned(const uint8_t* __restrict__ live_flag, int64_t k,
@@ -718,6 +742,62 @@ int run_pass(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn* m, co
   return GNNSHAP_OK;
 }
 
+// ---- multi-target path: one job per blockIdx.y -------------------------------------------
+
+__global__ void k_init_batch(const gnnshap::EvalJob* __restrict__ jobs) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t < 8) J.ctl[t] = 0;
+  if (t < 2) J.sp_rows[t] = static_cast<int32_t>(t);
+  for (int64_t w = t; w < J.wpr; w += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    J.sp_masks[w] = 0;
+    const int64_t lo = w * 64;
+    const int64_t nb = J.M - lo >= 64 ? 64 : J.M - lo;
+    J.sp_masks[J.wpr + w] = nb >= 64 ? ~uint64_t(0) : ((uint64_t(1) << nb) - 1);
+  }
+}
+
+__global__ void k_gather_batch(const gnnshap::EvalJob* __restrict__ jobs, const float* __restrict__ XW1, int h) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  const int64_t total = J.n_nodes * h;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total;
+       t += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t u = t / h, f = t % h;
+    J.Zc1[t] = XW1[static_cast<int64_t>(J.node_gid[u]) * h + f];
+  }
+}
+
+// special: the two rows with no / all players, every class; else the live rows.
+template <int FPT>
+__global__ void __launch_bounds__(256) k_eval_l2_batch(const gnnshap::EvalJob* __restrict__ jobs,
+                                                       gnnshap::EvalModel md, bool special, int tbr) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  if (special)
+    eval_l2_body<FPT>(J.sp_masks, J.wpr, J.sp_rows, 0, 2, nullptr, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1,
+                      md.b1, md.W2, md.b2, md.h, md.C, J.ctl, true, tbr, nullptr, J.sp_y, blockIdx.x);
+  else
+    eval_l2_body<FPT>(J.masks, J.wpr, J.live_rows, 0, J.k, J.ctl + 1, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1,
+                      md.b1, md.W2, md.b2, md.h, md.C, J.ctl, false, tbr, J.y, J.sp_y, blockIdx.x);
+}
+
+__global__ void k_pick_class_batch(const gnnshap::EvalJob* __restrict__ jobs, int C, int requested) {
+  const gnnshap::EvalJob J = jobs[blockIdx.x];
+  pick_class(J.sp_y, C, requested, J.ctl, J.cls_out, J.fef);
+}
+
+__global__ void __launch_bounds__(256) k_live_batch(const gnnshap::EvalJob* __restrict__ jobs) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  live_rows_of(J.masks, J.wpr, J.k, J.dst_ptr, J.ctl, J.live_rows, J.live_flag);
+}
+
+__global__ void k_fill_pruned_batch(const gnnshap::EvalJob* __restrict__ jobs) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  const float f0 = J.fef[0];
+  for (int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; b < J.k;
+       b += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    if (!J.live_flag[b]) J.y[b] = f0;
+}
+
 }  // namespace
 
 extern "C" int gnnshap_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k,
@@ -807,4 +887,87 @@ extern "C" int gnnshap_transform_features(const float* X, int64_t n, int32_t d, 
     return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "matrix too large");
   return launch_gemm(static_cast<hipStream_t>(stream), X, d, nullptr, nullptr, W, h, Z, h, 0, n, h, d);
   GS_TRY_END
+}
+
+// ---- multi-target path: host side --------------------------------------------------------
+
+bool gnnshap::eval_batchable(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k) {
+  Shape sh;
+  if (make_shape(sg, m, k, &sh) != GNNSHAP_OK) {
+    clear_error();
+    return false;
+  }
+  return m->XW1 && m->W && m->W[1] && sh.L == 2 && sh.hops >= 2 && sh.tile >= k && k <= INT32_MAX &&
+         fused_l2_ok(sh, 2, true) && fused_l2_ok(sh, k, false);
+}
+
+size_t gnnshap::eval_slice_bytes(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k) {
+  Shape sh;
+  if (make_shape(sg, m, k, &sh) != GNNSHAP_OK) return 0;
+  Carver c(nullptr);
+  carve(c, sh);
+  return c.bytes();
+}
+
+void gnnshap::eval_carve_slice(void* base, const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k,
+                               EvalJob* job) {
+  Shape sh;
+  make_shape(sg, m, k, &sh);
+  Carver c(base);
+  const Ws w = carve(c, sh);
+  job->ctl = w.ctl;
+  job->sp_masks = w.sp_masks;
+  job->sp_rows = w.sp_rows;
+  job->sp_y = w.sp_y;
+  job->live_rows = w.live_rows;
+  job->live_flag = w.live_flag;
+  job->Zc1 = w.Zc[1];
+}
+
+int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& md, int64_t max_nodes,
+                               int64_t max_ndst, int64_t max_n1, int64_t max_wpr, int64_t max_k, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  Shape sh;                          // the largest shapes of the batch, for LDS sizing
+  sh.n_dst = max_ndst;
+  sh.nd[1] = max_n1;
+  const int fpt = feature_split(md.h);
+  const int tb_main = static_cast<int>(max_k < kTB ? max_k : kTB);
+  const size_t lds_sp = fused_lds_bytes(sh, 2, md.C, 8 * fpt);
+  const size_t lds_main = fused_lds_bytes(sh, tb_main, 1, 8 * fpt);
+  if (lds_sp > 65536 || lds_main > 65536)
+    return fail(GNNSHAP_EUNSUPPORTED, "batched evaluation needs %zu bytes of LDS", std::max(lds_sp, lds_main));
+  const unsigned nn = static_cast<unsigned>(n);
+  k_init_batch<<<dim3(grid_for(max_wpr, 256, 64), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  k_gather_batch<<<dim3(grid_for(max_nodes * md.h, 256, 2048), nn), 256, 0, s>>>(jobs, md.XW1, md.h);
+  GS_LAUNCHED();
+#define GS_L2B(F, GRID, LDS, SPECIAL, TBR) k_eval_l2_batch<F><<<GRID, 256, LDS, s>>>(jobs, md, SPECIAL, TBR)
+#define GS_L2B_ALL(GRID, LDS, SPECIAL, TBR)            \
+  switch (fpt) {                                       \
+    case 1: GS_L2B(1, GRID, LDS, SPECIAL, TBR); break; \
+    case 2: GS_L2B(2, GRID, LDS, SPECIAL, TBR); break; \
+    case 4: GS_L2B(4, GRID, LDS, SPECIAL, TBR); break; \
+    case 8: GS_L2B(8, GRID, LDS, SPECIAL, TBR); break; \
+    default: GS_L2B(16, GRID, LDS, SPECIAL, TBR); break; \
+  }
+  {
+    GS_TIMED("k_eval_l2_batch", s);
+    GS_L2B_ALL(dim3(1, nn), lds_sp, true, 2);
+  }
+  GS_LAUNCHED();
+  k_pick_class_batch<<<nn, 1, 0, s>>>(jobs, md.C, md.target_class);
+  GS_LAUNCHED();
+  k_live_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  {
+    GS_TIMED("k_eval_l2_batch", s);
+    GS_L2B_ALL(dim3(static_cast<unsigned>(ceil_div(max_k, tb_main)), nn), lds_main, false, tb_main);
+  }
+  GS_LAUNCHED();
+#undef GS_L2B_ALL
+#undef GS_L2B
+  k_fill_pruned_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }

@@ -7,6 +7,8 @@
 // global-id order (which yields the (dist, id) order without a sort), a scan
 // of the destinations' in-degrees, then the player arrays.  The host waits
 // once, to learn the sizes.
+#include <vector>
+
 #include "common.h"
 
 namespace {
@@ -253,11 +255,11 @@ constexpr int64_t kOneBlockNodes = int64_t(1) << 18;
 // caller's capacities, and the reset of the workspace.  counters[0..hops]
 // receive the level sizes, counters[kLevels] = M, counters[kLevels + 1] = 1 if
 // the arrays were written.
-__global__ void __launch_bounds__(1024) k_extract_one(const int64_t* __restrict__ indptr,
-                                                      const int32_t* __restrict__ indices, int64_t n,
-                                                      int64_t v, int hops, Ws w, int64_t cap_nodes,
-                                                      int64_t cap_edges, int32_t* node_gid, int32_t* dst_ptr,
-                                                      int32_t* edge_src, int32_t* edge_dst, int64_t* edge_gid) {
+__device__ __forceinline__ void extract_one_body(const int64_t* __restrict__ indptr,
+                                                 const int32_t* __restrict__ indices, int64_t n, int64_t v,
+                                                 int hops, const Ws& w, int64_t cap_nodes, int64_t cap_edges,
+                                                 int32_t* node_gid, int32_t* dst_ptr, int32_t* edge_src,
+                                                 int32_t* edge_dst, int64_t* edge_gid, int64_t* result) {
   __shared__ int64_t lvl[kLevels + 2];     // queue offsets of the levels
   __shared__ unsigned int qcount;
   __shared__ int64_t buf[1024];
@@ -357,9 +359,9 @@ __global__ void __launch_bounds__(1024) k_extract_one(const int64_t* __restrict_
     }
   }
   if (tid == 0) {
-    for (int l = 0; l <= hops; ++l) w.counters[l] = lvl[l + 1] - lvl[l];
-    w.counters[kLevels] = m;
-    w.counters[kLevels + 1] = ok;
+    for (int l = 0; l <= hops; ++l) result[l] = lvl[l + 1] - lvl[l];
+    result[kLevels] = m;
+    result[kLevels + 1] = ok;
   }
   __syncthreads();
   // back to the zero state (the counters are cleared after the host copy)
@@ -373,8 +375,66 @@ __global__ void __launch_bounds__(1024) k_extract_one(const int64_t* __restrict_
   for (int64_t i = tid; i <= n_dst; i += 1024) w.dstptr[i] = 0;
 }
 
+__global__ void __launch_bounds__(1024) k_extract_one(const int64_t* __restrict__ indptr,
+                                                      const int32_t* __restrict__ indices, int64_t n,
+                                                      int64_t v, int hops, Ws w, int64_t cap_nodes,
+                                                      int64_t cap_edges, int32_t* node_gid, int32_t* dst_ptr,
+                                                      int32_t* edge_src, int32_t* edge_dst, int64_t* edge_gid) {
+  extract_one_body(indptr, indices, n, v, hops, w, cap_nodes, cap_edges, node_gid, dst_ptr, edge_src, edge_dst,
+                   edge_gid, w.counters);
+}
+
 __global__ void k_zero_counters(int64_t* counters) {
   if (threadIdx.x < kCounters) counters[threadIdx.x] = 0;
+}
+
+// ---- multi-target path --------------------------------------------------------------------
+
+struct ExtractJob {
+  int64_t v;
+  int hops;
+  Ws w;                    // this target's slice (zero between calls)
+  int64_t cap_nodes, cap_edges;
+  int32_t* node_gid;
+  int32_t* dst_ptr;
+  int32_t* edge_src;
+  int32_t* edge_dst;
+  int64_t* edge_gid;
+};
+
+// One workgroup per target; result rows of kCounters int64.
+__global__ void __launch_bounds__(1024) k_extract_batch(const int64_t* __restrict__ indptr,
+                                                        const int32_t* __restrict__ indices, int64_t n,
+                                                        const ExtractJob* __restrict__ jobs, int64_t* results) {
+  const ExtractJob J = jobs[blockIdx.x];
+  extract_one_body(indptr, indices, n, J.v, J.hops, J.w, J.cap_nodes, J.cap_edges, J.node_gid, J.dst_ptr,
+                   J.edge_src, J.edge_dst, J.edge_gid, results + static_cast<int64_t>(blockIdx.x) * kCounters);
+}
+
+__global__ void k_zero_results(int64_t* results, int64_t count) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    results[i] = 0;
+}
+
+// Batch workspace (all zero between calls, whatever the batch size): the job
+// table, the result rows, then one slice per target.
+struct BatchWs {
+  ExtractJob* jobs;
+  int64_t* results;
+  char* slices;
+  size_t slice_bytes;
+};
+
+BatchWs carve_batch(gnnshap::Carver& c, int64_t num_nodes, int64_t n) {
+  BatchWs b;
+  gnnshap::Carver one(nullptr);
+  carve(one, num_nodes);
+  b.slice_bytes = one.bytes();
+  b.jobs = c.take<ExtractJob>(n);
+  b.results = c.take<int64_t>(n * kCounters);
+  b.slices = c.take<char>(static_cast<size_t>(n) * b.slice_bytes);
+  return b;
 }
 
 }  // namespace
@@ -500,5 +560,85 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
                                                                                          nblk * kLevels);
   GS_LAUNCHED();
   return status;
+  GS_TRY_END
+}
+
+extern "C" int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, size_t* bytes) {
+  gnnshap::clear_error();
+  if (!bytes || num_nodes < 1 || n < 1) return gnnshap::fail(GNNSHAP_EINVAL, "bad arguments");
+  gnnshap::Carver c(nullptr);
+  carve_batch(c, num_nodes, n);
+  *bytes = c.bytes();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
+                                     gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (!g || !targets || !sgs || !ws) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  if (!g->indptr || !g->indices) return gnnshap::fail(GNNSHAP_EINVAL, "null graph arrays");
+  const int64_t nn = g->num_nodes;
+  if (nn < 1 || nn > INT32_MAX) return gnnshap::fail(GNNSHAP_EINVAL, "num_nodes out of range");
+  if (n < 1 || n > INT32_MAX) return gnnshap::fail(GNNSHAP_EINVAL, "n out of range");
+  if (nn > kOneBlockNodes)
+    return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "batched extraction supports graphs of up to %lld nodes",
+                         (long long)kOneBlockNodes);
+  gnnshap::Carver need(nullptr);
+  carve_batch(need, nn, n);
+  if (ws_bytes < need.bytes())
+    return gnnshap::fail(GNNSHAP_ECAPACITY, "batch extract workspace needs %zu bytes", need.bytes());
+  gnnshap::Carver c(ws);
+  const BatchWs b = carve_batch(c, nn, n);
+  std::vector<ExtractJob> jobs(static_cast<size_t>(n));
+  for (int64_t t = 0; t < n; ++t) {
+    const gnnshap_subgraph* sg = &sgs[t];
+    if (targets[t] < 0 || targets[t] >= nn) return gnnshap::fail(GNNSHAP_EINVAL, "target %lld out of range", (long long)t);
+    if (sg->num_hops < 1 || sg->num_hops > GNNSHAP_MAX_HOPS)
+      return gnnshap::fail(GNNSHAP_EINVAL, "num_hops out of range in subgraph %lld", (long long)t);
+    if ((sg->cap_nodes > 0 && (!sg->node_gid || !sg->dst_ptr)) ||
+        (sg->cap_edges > 0 && (!sg->edge_src || !sg->edge_dst || !sg->edge_gid)))
+      return gnnshap::fail(GNNSHAP_EINVAL, "null output arrays in subgraph %lld", (long long)t);
+    gnnshap::Carver sc(b.slices + static_cast<size_t>(t) * b.slice_bytes);
+    jobs[t] = ExtractJob{targets[t], sg->num_hops, carve(sc, nn), sg->cap_nodes, sg->cap_edges, sg->node_gid,
+                         sg->dst_ptr, sg->edge_src, sg->edge_dst, sg->edge_gid};
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  GS_HIP(hipMemcpyAsync(b.jobs, jobs.data(), jobs.size() * sizeof(ExtractJob), hipMemcpyHostToDevice, s));
+  {
+    GS_TIMED("k_extract_batch", s);
+    k_extract_batch<<<static_cast<unsigned>(n), 1024, 0, s>>>(g->indptr, g->indices, nn, b.jobs, b.results);
+  }
+  GS_LAUNCHED();
+  std::vector<int64_t> h(static_cast<size_t>(n) * kCounters);
+  GS_HIP(hipMemcpyAsync(h.data(), b.results, h.size() * sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  // back to all-zero: result rows and the job table (the slices reset themselves)
+  k_zero_results<<<gnnshap::grid_for(n * kCounters, 256, 64), 256, 0, s>>>(b.results, n * kCounters);
+  GS_LAUNCHED();
+  static_assert(sizeof(ExtractJob) % sizeof(int64_t) == 0, "job records are whole int64 words");
+  const int64_t job_words = n * static_cast<int64_t>(sizeof(ExtractJob) / sizeof(int64_t));
+  k_zero_results<<<gnnshap::grid_for(job_words, 256, 64), 256, 0, s>>>(reinterpret_cast<int64_t*>(b.jobs), job_words);
+  GS_LAUNCHED();
+  GS_HIP(hipStreamSynchronize(s));
+  bool all_ok = true;
+  for (int64_t t = 0; t < n; ++t) {
+    gnnshap_subgraph* sg = &sgs[t];
+    const int64_t* r = h.data() + t * kCounters;
+    const int levels = sg->num_hops + 1;
+    int64_t nodes = 0;
+    sg->hop_ptr[0] = 0;
+    for (int l = 0; l < levels; ++l) {
+      nodes += r[l];
+      sg->hop_ptr[l + 1] = nodes;
+    }
+    for (int l = levels + 1; l < GNNSHAP_MAX_HOPS + 2; ++l) sg->hop_ptr[l] = nodes;
+    sg->num_nodes = nodes;
+    sg->num_dst = sg->hop_ptr[sg->num_hops];
+    sg->num_edges = r[kLevels];
+    if (r[kLevels] > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "more than 2^31 players");
+    all_ok = all_ok && r[kLevels + 1] != 0;
+  }
+  if (!all_ok) return gnnshap::fail(GNNSHAP_ECAPACITY, "some subgraphs exceed their capacities");
+  return GNNSHAP_OK;
   GS_TRY_END
 }

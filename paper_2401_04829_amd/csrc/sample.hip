@@ -7,6 +7,7 @@
 // takes one step, lanes whose draw cannot interact with an earlier step of
 // the same chunk decide at once, the others are replayed in step order, so
 // the result is exactly the sequential algorithm's.
+#include "batch.h"
 #include "common.h"
 
 namespace {
@@ -57,11 +58,13 @@ __device__ __forceinline__ uint64_t binom(int64_t n, int64_t r) {
 
 __device__ __forceinline__ void set_bit(uint32_t* bs, int64_t j) { bs[j >> 5] |= 1u << (j & 31); }
 
-__global__ void __launch_bounds__(64) k_sample(const gnnshap_class* __restrict__ cls, int64_t ncls,
-                                               int64_t half, int64_t M, int64_t wpr, uint32_t seed_lo,
-                                               uint32_t seed_hi, uint32_t st_lo, uint32_t st_hi,
-                                               uint64_t* __restrict__ masks,
-                                               float* __restrict__ weights) {
+// Rows first, first + stride, ... < half of one job; one wavefront.
+__device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t first, int64_t stride) {
+  const gnnshap_class* __restrict__ cls = J.cls;
+  const int64_t ncls = J.ncls, half = J.half, M = J.M, wpr = J.wpr;
+  const uint32_t seed_lo = J.seed_lo, seed_hi = J.seed_hi, st_lo = J.st_lo, st_hi = J.st_hi;
+  uint64_t* __restrict__ masks = J.masks;
+  float* __restrict__ weights = J.weights;
   extern __shared__ uint32_t lds[];
   const int64_t nw = 2 * wpr;           // 32-bit words per bitset
   uint32_t* S = lds;                    // the row being built
@@ -72,7 +75,7 @@ __global__ void __launch_bounds__(64) k_sample(const gnnshap_class* __restrict__
     D1[w] = 0;
     D2[w] = 0;
   }
-  for (int64_t i = blockIdx.x; i < half; i += gridDim.x) {
+  for (int64_t i = first; i < half; i += stride) {
     int64_t lo = 0, hi = ncls - 1;      // last class starting at or before row i
     while (lo < hi) {
       const int64_t mid = (lo + hi + 1) >> 1;
@@ -168,6 +171,15 @@ __global__ void __launch_bounds__(64) k_sample(const gnnshap_class* __restrict__
   }
 }
 
+__global__ void __launch_bounds__(64) k_sample(gnnshap::SampleJob J) { sample_rows(J, blockIdx.x, gridDim.x); }
+
+// One job per blockIdx.y.
+__global__ void __launch_bounds__(64) k_sample_batch(const gnnshap::SampleJob* __restrict__ jobs) {
+  const gnnshap::SampleJob J = jobs[blockIdx.y];
+  if (blockIdx.x >= J.half) return;
+  sample_rows(J, blockIdx.x, gridDim.x);
+}
+
 int check_plan(const gnnshap_sample_plan* plan) {
   if (!plan) return gnnshap::fail(GNNSHAP_EINVAL, "plan is NULL");
   if (plan->num_players < 2 || plan->num_rows < 2 || (plan->num_rows % 2) ||
@@ -223,12 +235,25 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
   const unsigned grid = static_cast<unsigned>(half < 65536 ? half : 65536);
   {
     GS_TIMED("k_sample", s);
-    k_sample<<<grid, 64, lds, s>>>(w.classes, plan->num_classes, half, M, wpr,
-                                   static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
-                                   static_cast<uint32_t>(plan->stream_id),
-                                   static_cast<uint32_t>(plan->stream_id >> 32), masks, weights);
+    const gnnshap::SampleJob job{w.classes, plan->num_classes, half, M, wpr,
+                                 static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
+                                 static_cast<uint32_t>(plan->stream_id),
+                                 static_cast<uint32_t>(plan->stream_id >> 32), masks, weights};
+    k_sample<<<grid, 64, lds, s>>>(job);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END
+}
+
+int gnnshap::launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t max_half, int64_t max_wpr,
+                                 hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  const size_t lds = static_cast<size_t>(3 * 2 * max_wpr) * sizeof(uint32_t);
+  const dim3 grid(static_cast<unsigned>(max_half < 65536 ? max_half : 65536), static_cast<unsigned>(n));
+  GS_TIMED("k_sample_batch", s);
+  k_sample_batch<<<grid, 64, lds, s>>>(jobs);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }

@@ -22,8 +22,10 @@
 // 256-row segments whose triangle sits in LDS, with multi-block GEMVs carrying
 // each segment to the rows outside it.  The right-hand side is accumulated in
 // fp64.
+#include <algorithm>
 #include <cmath>
 
+#include "batch.h"
 #include "common.h"
 
 namespace {
@@ -33,6 +35,7 @@ constexpr int kTB = 64;        // diagonal block of the triangular solves (one w
 constexpr int kSB = 32;        // panel width, one-workgroup path
 constexpr int64_t kSeg = 256;  // segment of the triangular solves (its triangle in LDS)
 constexpr int kMaxChunks = 256;
+constexpr int kMidMax = 448;   // largest system of the global-memory one-workgroup path
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -50,6 +53,7 @@ struct Ws {
   float* rhs;        // M
   float* x;          // M
   float* Winv;       // kPB x kPB inverse of the current diagonal factor
+  float* Wd;         // one-workgroup mid-size path: ceil(M/64) inverse diagonal factors (64 x 64)
 };
 
 // Row stride of G: a multiple of 64 floats keeps every row 256-byte aligned.
@@ -83,6 +87,7 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   w.rhs = c.take<float>(M);
   w.x = c.take<float>(M);
   w.Winv = c.take<float>(kPB * kPB);
+  w.Wd = c.take<float>(M <= kMidMax ? gnnshap::ceil_div(M, 64) * 64 * 64 : 1);
   return w;
 }
 
@@ -131,12 +136,10 @@ __device__ __forceinline__ void chol_regs(float (&a)[NB], int64_t o, int32_t* in
 }
 
 // T[rb, j]: transpose 64 rows x 64 players with ballots.  One wave per (rb, word).
-__global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ masks, int64_t wpr,
-                                                  int64_t row0, int64_t nrows, int64_t M,
-                                                  uint64_t* __restrict__ T) {
+__device__ __forceinline__ void transpose_body(const uint64_t* __restrict__ masks, int64_t wpr, int64_t row0,
+                                               int64_t nrows, int64_t M, uint64_t* __restrict__ T, int64_t rb,
+                                               int64_t w) {
   const int lane = threadIdx.x;
-  const int64_t rb = blockIdx.x;
-  const int64_t w = blockIdx.y;
   const int64_t r = rb * 64 + lane;
   const uint64_t word = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
   uint64_t mine = 0;
@@ -149,11 +152,15 @@ __global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ m
   if (j < M) T[rb * M + j] = mine;
 }
 
+__global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ masks, int64_t wpr, int64_t row0,
+                                                  int64_t nrows, int64_t M, uint64_t* __restrict__ T) {
+  transpose_body(masks, wpr, row0, nrows, M, T, blockIdx.x, blockIdx.y);
+}
+
 // Counts C[i, j] = sum_rb popcount(T[rb, i] & T[rb, j]) for 64x64 tiles with J >= I,
 // stored in both halves (row stride ld).
-__global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
-                                              int32_t* __restrict__ C) {
-  const int64_t I = blockIdx.y, J = blockIdx.x;
+__device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
+                                          int32_t* __restrict__ C, int64_t I, int64_t J) {
   if (J < I) return;
   __shared__ uint64_t Ti[16][64];
   __shared__ uint64_t Tj[16][64];
@@ -198,6 +205,11 @@ __global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, in
       C[j * ld + i] = acc[q][r];
     }
   }
+}
+
+__global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
+                                              int32_t* __restrict__ C) {
+  gram_body(T, nrb, M, ld, C, blockIdx.y, blockIdx.x);
 }
 
 // usum[i] = sum_j C[i, j]; one wave per row.
@@ -269,10 +281,9 @@ __global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restri
 
 // dz_b = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|) for b < half; a
 // representative row has its class's size, its complement M minus that.
-__global__ void __launch_bounds__(256) k_dz(const float* __restrict__ y, int64_t half, int64_t M,
-                                            const gnnshap_class* __restrict__ cls, int64_t ncls,
-                                            const float* __restrict__ fef, double* __restrict__ dz) {
-  const int64_t b = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+__device__ __forceinline__ void dz_body(const float* __restrict__ y, int64_t half, int64_t M,
+                                        const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                        const float* __restrict__ fef, double* __restrict__ dz, int64_t b) {
   if (b >= half) return;
   const double Md = static_cast<double>(M);
   const double f0 = static_cast<double>(fef[0]);
@@ -289,17 +300,23 @@ __global__ void __launch_bounds__(256) k_dz(const float* __restrict__ y, int64_t
   dz[b] = z1 - z2;
 }
 
+__global__ void __launch_bounds__(256) k_dz(const float* __restrict__ y, int64_t half, int64_t M,
+                                            const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                            const float* __restrict__ fef, double* __restrict__ dz) {
+  dz_body(y, half, M, cls, ncls, fef, dz, static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x);
+}
+
 // Partial right-hand sides: part[ch, j] = sum_{b in chunk ch} dz_b m_bj.  A
 // wavefront owns one 64-player word column and the rows of one chunk: each
 // row's word and dz_b are wave-uniform (scalar loads) and every lane tests
 // its own bit.
-__global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
-                                                  int64_t M, const double* __restrict__ dz, int64_t rows_per_chunk,
-                                                  double* __restrict__ part) {
+__device__ __forceinline__ void rhs_part_body(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
+                                              int64_t M, const double* __restrict__ dz, int64_t rows_per_chunk,
+                                              double* __restrict__ part, int64_t bx, int64_t chunk) {
   const int lane = threadIdx.x & 63;
-  const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t w = bx * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (w >= wpr) return;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * rows_per_chunk;
+  const int64_t r0 = chunk * rows_per_chunk;
   const int64_t r1 = r0 + rows_per_chunk < half ? r0 + rows_per_chunk : half;
   const uint64_t* col = masks + w;
   double acc = 0.0;
@@ -317,7 +334,13 @@ __global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ m
   }
   for (; b < r1; ++b) acc += ((col[b * wpr] >> lane) & 1) ? dz[b] : 0.0;
   const int64_t j = w * 64 + lane;
-  if (j < M) part[static_cast<int64_t>(blockIdx.y) * M + j] = acc;
+  if (j < M) part[chunk * M + j] = acc;
+}
+
+__global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
+                                                  int64_t M, const double* __restrict__ dz, int64_t rows_per_chunk,
+                                                  double* __restrict__ part) {
+  rhs_part_body(masks, wpr, half, M, dz, rows_per_chunk, part, blockIdx.x, blockIdx.y);
 }
 
 // dv[j] = sum over chunks of part[., j] (fixed order); bsum[block] = sum of its dv.
@@ -363,11 +386,10 @@ size_t small_lds_bytes(int64_t M) {
          static_cast<size_t>((M * (M + 1)) / 2) * sizeof(float);
 }
 
-__global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__ C, int64_t ldc, int64_t M,
-                                                     bool has_random,
-                                                     double alpha, double wr, const float* __restrict__ fef,
-                                                     const double* __restrict__ part, int64_t nch,
-                                                     int32_t* info, float* __restrict__ phi) {
+__device__ __forceinline__ void solve_small_body(const int32_t* __restrict__ C, int64_t ldc, int64_t M,
+                                                 bool has_random, double alpha, double wr,
+                                                 const float* __restrict__ fef, const double* __restrict__ part,
+                                                 int64_t nch, int32_t* info, float* __restrict__ phi) {
   extern __shared__ __align__(16) unsigned char smem[];
   double* dv = reinterpret_cast<double*>(smem);      // M: row sums, then the raw right-hand side
   float* rhs = reinterpret_cast<float*>(dv + M);     // M
@@ -621,6 +643,13 @@ __global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__
   for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rhs[i]));
 }
 
+__global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__ C, int64_t ldc, int64_t M,
+                                                     bool has_random, double alpha, double wr,
+                                                     const float* __restrict__ fef, const double* __restrict__ part,
+                                                     int64_t nch, int32_t* info, float* __restrict__ phi) {
+  solve_small_body(C, ldc, M, has_random, alpha, wr, fef, part, nch, info, phi);
+}
+
 __global__ void k_zero_info(int32_t* info) { *info = 0; }
 
 // ---- multi-block path: diagonal blocks --------------------------------------------------
@@ -814,6 +843,221 @@ __global__ void __launch_bounds__(256) k_potrf(float* G, int64_t ld, int64_t M, 
     else v = c < 64 ? S2[(r - 64) * kHP + c] : S4[(r - 64) * kHP + c - 64];
     Winv[t] = v;
   }
+}
+
+// ---- one-workgroup path for mid-size systems ---------------------------------------------
+//
+// M <= kMidMax: the system stays in global memory (L2-resident at these
+// sizes) and one workgroup factors it in 64-wide panels: the wavefront
+// Cholesky-and-inverse of the diagonal block, the panel as an MFMA product
+// with that inverse (kept in LDS), the trailing update as 32x32 MFMA tiles
+// spread over the four wavefronts.  The forward substitution rides along
+// (z_p = W_p r_p, then r_I -= L_Ip z_p from the panel in LDS); the backward
+// one reads L and the stored inverses once more.  The counts are turned into
+// G~ entries when the first panel touches them.
+
+constexpr int kMidBlk = kMidMax / 64;
+constexpr size_t kMidLds = (static_cast<size_t>(1 + kMidBlk) * kHB + 64 + kMidMax + 4 * 64) * sizeof(float) +
+                           static_cast<size_t>(kMidMax) * sizeof(double);
+
+// G: the counts (int32, row stride ld, both halves) on entry, the factor on
+// exit; usum: their row sums; dvg: the summed right-hand side before
+// centring; Wd: room for the ceil(M/64) inverse diagonal factors.
+__device__ __forceinline__ void solve_mid_body(float* G, int64_t ld, int64_t M, bool has_random, double alpha,
+                                               double wr, const int64_t* __restrict__ usum,
+                                               const double* __restrict__ dvg, const float* __restrict__ fef,
+                                               float* __restrict__ Wd, int32_t* info, float* __restrict__ phi) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* D0 = reinterpret_cast<float*>(smem);  // diagonal block -> L_pp
+  float* D1 = D0 + kHB;                        // W_pp = L_pp^-1
+  float* P = D1 + kHB;                         // blocks below the diagonal block -> L_Ip
+  float* col = P + (kMidBlk - 1) * kHB;        // 64: column broadcasts of the wavefront Cholesky
+  float* rv = col + 64;                        // kMidMax: r, then z, then psi
+  float* red4 = rv + kMidMax;                  // 4 x 64
+  double* ud = reinterpret_cast<double*>(red4 + 4 * 64);  // kMidMax: usum / M
+  __shared__ double red[3][4];
+  __shared__ double sc[4];                     // gamma, mean of dv, Delta, -
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int h = lane >> 5, rl = lane & 31;
+  const double Md = static_cast<double>(M), inv_m = 1.0 / Md;
+  const int32_t* C = reinterpret_cast<const int32_t*>(G);
+  const int64_t nblk = (M + 63) / 64;
+  if (tid == 0) *info = 0;
+
+  // 1. trace and sigma of the counts, mean of the right-hand side
+  double tr = 0.0, sg = 0.0, sv = 0.0;
+  for (int64_t i = tid; i < M; i += 256) {
+    if (has_random) {
+      tr += static_cast<double>(C[i * ld + i]);
+      sg += static_cast<double>(usum[i]);
+      ud[i] = static_cast<double>(usum[i]) * inv_m;
+    }
+    sv += dvg[i];
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    tr += __shfl_xor(tr, off);
+    sg += __shfl_xor(sg, off);
+    sv += __shfl_xor(sv, off);
+  }
+  if (lane == 0) {
+    red[0][wave] = tr;
+    red[1][wave] = sg;
+    red[2][wave] = sv;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const double trace = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    const double sigma = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    const double tr_pgp = alpha * (Md - 1.0) + 2.0 * wr * (trace - sigma / Md);
+    sc[0] = tr_pgp / (Md - 1.0);
+    sc[1] = ((red[2][0] + red[2][1]) + (red[2][2] + red[2][3])) / Md;
+    sc[2] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
+    sc[3] = sigma;
+  }
+  __syncthreads();
+  const double gamma = sc[0], sigma = sc[3];
+  for (int64_t i = tid; i < nblk * 64; i += 256) rv[i] = i < M ? static_cast<float>(dvg[i] - sc[1]) : 0.f;
+  const double base = -alpha * inv_m + gamma * inv_m + (has_random ? 2.0 * wr * sigma * inv_m * inv_m : 0.0);
+  const double wr2 = 2.0 * wr;
+  // G~_ij from the count c_ij (first touch only)
+  auto gt = [&](int64_t i, int64_t j, int32_t cij) -> float {
+    double v = base + (i == j ? alpha : 0.0);
+    if (has_random) v += wr2 * (static_cast<double>(cij) - ud[i] - ud[j]);
+    return static_cast<float>(v);
+  };
+  // 64x64 block at (r0, c0) into LDS (pitch kHP): zeros outside the lower
+  // part of G (identity on the diagonal past M when `diag`)
+  auto load_block = [&](float* dst, int64_t r0, int64_t c0, bool diag, bool first) {
+    float v[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int t = tid + q * 256;
+      const int64_t gi = r0 + (t >> 6), gj = c0 + (t & 63);
+      const bool ok = gi < M && gj < M && (!diag || gj <= gi);
+      v[q] = ok ? G[gi * ld + gj] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int t = tid + q * 256;
+      const int r = t >> 6, c = t & 63;
+      const int64_t gi = r0 + r, gj = c0 + c;
+      float x = v[q];
+      if (first && gi < M && gj < M && (!diag || gj <= gi)) x = gt(gi, gj, __float_as_int(x));
+      if (diag && r == c && gi >= M) x = 1.f;
+      dst[r * kHP + c] = x;
+    }
+  };
+  __syncthreads();
+
+  // 2. factorisation with the forward substitution
+  for (int64_t p = 0; p < nblk; ++p) {
+    const int64_t o = p * 64;
+    const int nI = static_cast<int>(nblk - p - 1);
+    const bool first = p == 0;
+    load_block(D0, o, o, true, first);
+    for (int I = 0; I < nI; ++I) load_block(P + I * kHB, o + 64 * (I + 1), o, false, first);
+    __syncthreads();
+    if (wave == 0) {
+      chol_inv64(D0, D1, col, o, info);
+      // z_p = W_pp r_p
+      float z = 0.f;
+#pragma unroll 8
+      for (int c = 0; c < 64; ++c) z += D1[lane * kHP + c] * rv[o + c];
+      __builtin_amdgcn_wave_barrier();
+      rv[o + lane] = z;
+    }
+    __syncthreads();
+    for (int t = tid; t < 64 * 64; t += 256) {
+      const int r = t >> 6, c = t & 63;
+      const int64_t gi = o + r, gj = o + c;
+      if (gi < M && gj <= gi) G[gi * ld + gj] = D0[r * kHP + c];
+      Wd[p * 4096 + t] = D1[r * kHP + c];
+    }
+    for (int I = 0; I < nI; ++I) mm64<true>(P + I * kHB, D1, P + I * kHB, 1.f, 0.f);   // L_Ip = A_Ip W^T
+    // store L_Ip; r_I -= L_Ip z_p
+    for (int R = tid; R < nI * 64; R += 256) {
+      const float* pr = P + (R >> 6) * kHB + (R & 63) * kHP;
+      float s = 0.f;
+#pragma unroll 8
+      for (int c = 0; c < 64; ++c) s += pr[c] * rv[o + c];
+      rv[o + 64 + R] -= s;
+    }
+    for (int I = 0; I < nI; ++I)
+      for (int t = tid; t < 64 * 64; t += 256) {
+        const int r = t >> 6, c = t & 63;
+        const int64_t gi = o + 64 * (I + 1) + r;
+        if (gi < M) G[gi * ld + o + c] = P[I * kHB + r * kHP + c];
+      }
+    // trailing tiles A_IJ -= L_Ip L_Jp^T: (pair, 32x32 quadrant) tasks over the wavefronts;
+    // the strictly upper quadrant of a diagonal tile is skipped
+    const int tasks = 4 * (nI * (nI + 1) / 2);
+    for (int task = wave; task < tasks; task += 4) {
+      const int pair = task >> 2, q = task & 3;
+      int I = 0;
+      while ((I + 1) * (I + 2) / 2 <= pair) ++I;
+      const int J = pair - I * (I + 1) / 2;
+      const int qr = q >> 1, qc = q & 1;
+      if (I == J && qr < qc) continue;
+      const int64_t gi0 = o + 64 * (I + 1) + 32 * qr, gj = o + 64 * (J + 1) + 32 * qc + rl;
+      f32x16 acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t gi = gi0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const bool ok = gi < M && gj < M;
+        float x = ok ? G[gi * ld + gj] : 0.f;
+        if (first && ok) x = gt(gi, gj, __float_as_int(x));
+        acc[r] = x;
+      }
+      const float* xa = P + I * kHB + (32 * qr + rl) * kHP + h * 32;
+      const float* xb = P + J * kHB + (32 * qc + rl) * kHP + h * 32;
+#pragma unroll
+      for (int s4 = 0; s4 < 32; s4 += 4) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(xa + s4);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(xb + s4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(-a[e], b[e], acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t gi = gi0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (gi < M && gj < M) G[gi * ld + gj] = acc[r];
+      }
+    }
+    __syncthreads();
+  }
+
+  // 3. backward substitution: psi_p = W_pp^T (z_p - sum_I L_Ip^T psi_I)
+  for (int64_t p = nblk - 1; p >= 0; --p) {
+    const int64_t o = p * 64;
+    const int c = tid & 63, g = tid >> 6;
+    const bool real = o + c < M;      // columns past M (row padding of G) are never read
+    float acc = 0.f;
+    if (real) {
+#pragma unroll 8
+      for (int64_t row = o + 64 + g; row < M; row += 4) acc += G[row * ld + o + c] * rv[row];
+    }
+    red4[g * 64 + c] = acc;
+    __syncthreads();
+    if (tid < 64)
+      red4[tid] = o + tid < M ? rv[o + tid] - ((red4[tid] + red4[64 + tid]) + (red4[128 + tid] + red4[192 + tid])) : 0.f;
+    __syncthreads();
+    if (tid < 64) {
+      float ps = 0.f;
+#pragma unroll 8
+      for (int cc = tid; cc < 64; ++cc) ps += Wd[p * 4096 + cc * 64 + tid] * red4[cc];
+      rv[o + tid] = ps;
+    }
+    __syncthreads();
+  }
+  const double delta = sc[2];
+  for (int64_t i = tid; i < M; i += 256) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rv[i]));
+}
+
+__global__ void __launch_bounds__(256) k_solve_mid(float* G, int64_t ld, int64_t M, bool has_random, double alpha,
+                                                   double wr, const int64_t* __restrict__ usum,
+                                                   const double* __restrict__ dvg, const float* __restrict__ fef,
+                                                   float* __restrict__ Wd, int32_t* info, float* __restrict__ phi) {
+  solve_mid_body(G, ld, M, has_random, alpha, wr, usum, dvg, fef, Wd, info, phi);
 }
 
 // ---- multi-block path: MFMA GEMM ---------------------------------------------------------
@@ -1084,18 +1328,90 @@ double binom_d(int64_t n, int64_t r) {
   return v;
 }
 
+// ---- multi-target path (one-workgroup systems): one job per blockIdx.y / .z --------------
+
+__global__ void __launch_bounds__(64) k_transpose_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.z];
+  if (J.kr <= 0 || blockIdx.x >= J.nrb || blockIdx.y >= J.wpr) return;
+  transpose_body(J.masks, J.wpr, J.rb0, J.kr, J.M, J.T, blockIdx.x, blockIdx.y);
+}
+
+__global__ void __launch_bounds__(256) k_gram_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.z];
+  const int64_t nb = (J.M + 63) / 64;
+  if (J.kr <= 0 || blockIdx.x >= nb || blockIdx.y >= nb) return;
+  gram_body(J.T, J.nrb, J.M, J.ld, J.counts, blockIdx.y, blockIdx.x);
+}
+
+__global__ void __launch_bounds__(256) k_dz_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.y];
+  dz_body(J.y, J.half, J.M, J.cls, J.ncls, J.fef, J.dz, static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x);
+}
+
+__global__ void __launch_bounds__(256) k_rhs_part_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.z];
+  if (blockIdx.y >= J.nch) return;
+  rhs_part_body(J.masks, J.wpr, J.half, J.M, J.dz, J.rpc, J.part, blockIdx.x, blockIdx.y);
+}
+
+// Row sums of the counts and the summed right-hand side, for the mid-size jobs.
+__global__ void __launch_bounds__(256) k_rowsum_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.y];
+  if (!J.mid || J.kr <= 0) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  if (i >= J.M) return;
+  long long s = 0;
+  for (int64_t j = lane; j < J.M; j += 64) s += J.counts[i * J.ld + j];
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane == 0) J.usum[i] = s;
+}
+
+__global__ void __launch_bounds__(256) k_rhs_sum_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.y];
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (!J.mid || j >= J.M) return;
+  double v = 0.0;
+  for (int64_t c = 0; c < J.nch; ++c) v += J.part[c * J.M + j];
+  J.dv[j] = v;
+}
+
+// One workgroup per job: the LDS-resident path for small systems, the
+// global-memory path for mid-size ones.
+__global__ void __launch_bounds__(256) k_solve_one_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.x];
+  if (J.mid)
+    solve_mid_body(reinterpret_cast<float*>(J.counts), J.ld, J.M, J.kr > 0, J.alpha, J.wr, J.usum, J.dv, J.fef, J.Wd,
+                   J.info, J.phi);
+  else
+    solve_small_body(J.counts, J.ld, J.M, J.kr > 0, J.alpha, J.wr, J.fef, J.part, J.nch, J.info, J.phi);
+}
+
 // Whether `kernel` may be launched with `bytes` of dynamic LDS on the current
-// device; above the 64 KiB default, its limit is raised once to the device
-// maximum.
+// device (its static LDS counts against the same limit); above the 64 KiB
+// default, its dynamic limit is raised once to all the device allows.
 bool allow_lds(const void* kernel, size_t bytes, bool& raised) {
-  if (bytes <= 65536) return true;
-  const int cap = gnnshap::max_lds_bytes();
-  if (bytes > static_cast<size_t>(cap)) return false;
+  hipFuncAttributes a{};
+  if (hipFuncGetAttributes(&a, kernel) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  const size_t cap = static_cast<size_t>(gnnshap::max_lds_bytes());
+  const size_t fixed = a.sharedSizeBytes;
+  if (bytes + fixed > cap) return false;
+  if (bytes + fixed <= 65536) return true;
   if (!raised) {
-    raised = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, cap) == hipSuccess;
+    raised = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 static_cast<int>(cap - fixed)) == hipSuccess;
     (void)hipGetLastError();
   }
   return raised;
+}
+
+// The LDS-resident one-workgroup path: its packed triangle plus a margin for
+// the static LDS of the kernels that run it.
+bool small_fits(int64_t M) {
+  return small_lds_bytes(M) + 16384 <= static_cast<size_t>(gnnshap::max_lds_bytes());
 }
 
 }  // namespace
@@ -1170,11 +1486,28 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
 
   const size_t small_bytes = small_lds_bytes(M);
   static bool small_lds = false;
-  if (allow_lds(reinterpret_cast<const void*>(&k_solve_small), small_bytes, small_lds)) {
+  if (small_fits(M) && allow_lds(reinterpret_cast<const void*>(&k_solve_small), small_bytes, small_lds)) {
     {
       GS_TIMED("k_solve_small", s);
       k_solve_small<<<1, 256, small_bytes, s>>>(counts, ld, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
                                                 phi);
+    }
+    GS_LAUNCHED();
+    return GNNSHAP_OK;
+  }
+  static bool mid_lds = false;
+  if (M <= kMidMax && allow_lds(reinterpret_cast<const void*>(&k_solve_mid), kMidLds, mid_lds)) {
+    if (has_random) {
+      k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, ld, w.usum);
+      GS_LAUNCHED();
+    }
+    const int64_t nbm = gnnshap::ceil_div(M, 256);
+    k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch, M, w.dv, w.bsum);
+    GS_LAUNCHED();
+    {
+      GS_TIMED("k_solve_mid", s);
+      k_solve_mid<<<1, 256, kMidLds, s>>>(w.G, ld, M, has_random, alpha, wr, w.usum, w.dv, f_empty_full, w.Wd, info,
+                                          phi);
     }
     GS_LAUNCHED();
     return GNNSHAP_OK;
@@ -1254,4 +1587,107 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END
+}
+
+// ---- multi-target path: host side --------------------------------------------------------
+
+bool gnnshap::solve_batchable(const gnnshap_sample_plan* plan) {
+  if (check_plan(plan, nullptr) != GNNSHAP_OK) {
+    clear_error();
+    return false;
+  }
+  return plan->num_players <= kMidMax || small_fits(plan->num_players);
+}
+
+size_t gnnshap::solve_slice_bytes(const gnnshap_sample_plan* plan) {
+  Carver c(nullptr);
+  carve(c, plan);
+  return c.bytes();
+}
+
+int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice,
+                            SolveJob* job) {
+  if (int st = check_plan(plan, classes)) return st;
+  Carver c(slice);
+  const Ws w = carve(c, plan);
+  const int64_t M = plan->num_players;
+  job->ncls = plan->num_classes;
+  job->M = M;
+  job->wpr = plan->words_per_row;
+  job->half = plan->num_rows / 2;
+  job->rb0 = plan->random_begin;
+  job->kr = job->half - job->rb0;
+  job->nrb = ceil_div(job->kr, 64);
+  job->ld = ld_of(M);
+  job->nch = n_chunks(job->half, job->wpr);
+  job->rpc = ceil_div(job->half, job->nch);
+  job->wr = job->kr > 0 ? plan->random_weight : 0.0;
+  double alpha = 0.0;
+  for (int64_t i = 0; i < plan->num_classes; ++i) {
+    if (!classes[i].full) continue;
+    const int64_t cs = classes[i].size;
+    const double kappa = 2 * cs < M ? 2.0 : 1.0;
+    alpha += classes[i].weight * kappa * binom_d(M - 2, cs - 1);
+  }
+  job->alpha = alpha;
+  job->T = w.T;
+  job->counts = reinterpret_cast<int32_t*>(w.G);
+  job->dz = w.dz;
+  job->part = w.part;
+  job->usum = w.usum;
+  job->dv = w.dv;
+  job->Wd = w.Wd;
+  job->mid = small_fits(M) ? 0 : 1;
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
+                                int64_t max_nrb, int64_t max_nch, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  const size_t lds = std::max(kMidLds, small_fits(max_M) ? small_lds_bytes(max_M) : small_lds_bytes(1));
+  static bool raised = false;
+  if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
+    return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
+  const unsigned nn = static_cast<unsigned>(n);
+  if (max_nrb > 0) {
+    {
+      GS_TIMED("k_transpose_batch", s);
+      k_transpose_batch<<<dim3(static_cast<unsigned>(max_nrb), static_cast<unsigned>(max_wpr), nn), 64, 0, s>>>(jobs);
+    }
+    GS_LAUNCHED();
+    const unsigned nb = static_cast<unsigned>(ceil_div(max_M, 64));
+    {
+      GS_TIMED("k_gram_batch", s);
+      k_gram_batch<<<dim3(nb, nb, nn), 256, 0, s>>>(jobs);
+    }
+    GS_LAUNCHED();
+    k_rowsum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M * 64, 256)), nn), 256, 0, s>>>(jobs);
+    GS_LAUNCHED();
+  }
+  k_dz_batch<<<dim3(static_cast<unsigned>(ceil_div(max_half, 256)), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  {
+    GS_TIMED("k_rhs_part_batch", s);
+    k_rhs_part_batch<<<dim3(static_cast<unsigned>(ceil_div(max_wpr, 4)), static_cast<unsigned>(max_nch), nn), 256, 0,
+                       s>>>(jobs);
+  }
+  GS_LAUNCHED();
+  k_rhs_sum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M, 256)), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  {
+    GS_TIMED("k_solve_one_batch", s);
+    k_solve_one_batch<<<nn, 256, lds, s>>>(jobs);
+  }
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+extern "C" int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path) {
+  gnnshap::clear_error();
+  if (!path) return gnnshap::fail(GNNSHAP_EINVAL, "path is NULL");
+  if (int st = check_plan(plan, nullptr)) return st;
+  const int64_t M = plan->num_players;
+  *path = small_fits(M) ? 1 : (M <= kMidMax ? 2 : 0);
+  return GNNSHAP_OK;
 }

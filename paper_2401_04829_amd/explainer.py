@@ -90,7 +90,10 @@ class Explainer:
         self.ws_sample = _Buffer(dev)
         self.ws_eval = _Buffer(dev)
         self.ws_solve = _Buffer(dev)
+        self.ws_batch = _Buffer(dev)
         self._pipe = None
+        self._bx = None                          # batched extraction: (n, zero-filled workspace)
+        self._plans = {}                         # (M, p) -> (plan, classes): the plan does not depend on seed
 
     def prepare(self):
         """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
@@ -209,3 +212,112 @@ class Explainer:
         L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws), ws.numel(), s)
         return Explanation(target=target, sub=sub, plan=plan, classes=classes, masks=masks, weights=weights, y=y,
                            f_empty_full=fef, cls=cls, phi=phi, info=info)
+
+    # -- many targets per launch sequence ------------------------------------------------------
+
+    def _plan(self, M, num_samples, seed, stream_id):
+        key = (int(M), int(num_samples))
+        hit = self._plans.get(key)
+        if hit is None:
+            hit = L.gnnshap_plan_samples(int(M), int(num_samples), 0, 0)
+            self._plans[key] = hit
+        plan, classes = hit
+        out = L.gnnshap_sample_plan()
+        ctypes.pointer(out)[0] = plan
+        out.seed = int(seed)
+        out.stream_id = int(stream_id)
+        return out, classes
+
+    def extract_batch(self, targets):
+        """gnnshap_extract_batch: the computational graphs of all targets with one
+        host synchronisation; capacities grow and the batch is redone on
+        ECAPACITY.  Returns a list of Subgraph views into packed buffers."""
+        dev = self.device
+        n = len(targets)
+        if self._bx is None or self._bx[0] < n:
+            nbytes = L.gnnshap_extract_batch_workspace(self.indptr.numel() - 1, n)
+            self._bx = (n, torch.zeros(nbytes, dtype=torch.uint8, device=dev))
+        ws = self._bx[1]
+        tg = (ctypes.c_int64 * n)(*[int(v) for v in targets])
+        while True:
+            cn, ce = self._cap
+            node_gid = torch.empty((n, cn), dtype=torch.int32, device=dev)
+            dst_ptr = torch.empty((n, cn + 1), dtype=torch.int32, device=dev)
+            edge_src = torch.empty((n, ce), dtype=torch.int32, device=dev)
+            edge_dst = torch.empty((n, ce), dtype=torch.int32, device=dev)
+            edge_gid = torch.empty((n, ce), dtype=torch.int64, device=dev)
+            sgs = (L.gnnshap_subgraph * n)()
+            pn, pd, ps, pe, pg = (node_gid.data_ptr(), dst_ptr.data_ptr(), edge_src.data_ptr(), edge_dst.data_ptr(),
+                                  edge_gid.data_ptr())
+            for t in range(n):
+                sg = sgs[t]
+                sg.num_hops, sg.cap_nodes, sg.cap_edges = self.hops, cn, ce
+                sg.node_gid, sg.dst_ptr = pn + 4 * cn * t, pd + 4 * (cn + 1) * t
+                sg.edge_src, sg.edge_dst, sg.edge_gid = ps + 4 * ce * t, pe + 4 * ce * t, pg + 8 * ce * t
+            st = L.gnnshap_extract_batch(self.graph, tg, sgs, _vp(ws), ws.numel(), self.stream())
+            if st == L.OK:
+                break
+            self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
+                         max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
+        subs = []
+        for t in range(n):
+            sg = sgs[t]
+            m, nn, nd = sg.num_edges, sg.num_nodes, sg.num_dst
+            subs.append(Subgraph(sg=sg, node_gid=node_gid[t, :nn], dst_ptr=dst_ptr[t, :nd + 1],
+                                 edge_src=edge_src[t, :m], edge_dst=edge_dst[t, :m], edge_gid=edge_gid[t, :m]))
+        return subs, sgs
+
+    def explain_batch(self, targets, num_samples, seed, target_class=-1):
+        """Alg. 1 for every target, one launch per step for the whole batch
+        (gnnshap_extract_batch, then gnnshap_explain_batch); each target's
+        Philox stream is its node id.  Results equal explain()'s bit for bit.
+        Returns one Explanation per target (views into packed tensors, valid
+        once the current stream has run)."""
+        if self.XW1 is None:
+            self.prepare()
+        dev = self.device
+        subs, sgs = self.extract_batch(targets)
+        n = len(targets)
+        plans = (L.gnnshap_sample_plan * n)()
+        tables = []
+        for t, v in enumerate(targets):
+            M = sgs[t].num_edges
+            if M < 2:
+                raise ValueError(f"target {v} has {M} players; at least 2 are needed")
+            plans[t], cl = self._plan(M, num_samples, seed, v)
+            tables.append(cl)
+        ncls = sum(len(c) for c in tables)
+        classes = (L.gnnshap_class * ncls)()
+        o = 0
+        for cl in tables:
+            ctypes.memmove(ctypes.byref(classes, o * ctypes.sizeof(L.gnnshap_class)), cl, ctypes.sizeof(cl))
+            o += len(cl)
+        ks = [plans[t].num_rows for t in range(n)]
+        wprs = [plans[t].words_per_row for t in range(n)]
+        Ms = [plans[t].num_players for t in range(n)]
+        words = sum(k * w for k, w in zip(ks, wprs))
+        rows, players = sum(ks), sum(Ms)
+        masks = torch.empty(words, dtype=torch.int64, device=dev)
+        weights = torch.empty(rows, dtype=torch.float32, device=dev)
+        y = torch.empty(rows, dtype=torch.float32, device=dev)
+        fef = torch.empty(2 * n, dtype=torch.float32, device=dev)
+        cls = torch.empty(n, dtype=torch.int32, device=dev)
+        phi = torch.empty(players, dtype=torch.float32, device=dev)
+        info = torch.empty(n, dtype=torch.int32, device=dev)
+        ws = self.ws_batch.get(L.gnnshap_explain_batch_workspace(sgs, plans, self.model))
+        L.gnnshap_explain_batch(sgs, plans, classes, self.model, _vp(self.X), int(target_class), _vp(masks),
+                                _vp(weights), _vp(y), _vp(fef), _vp(cls), _vp(phi), _vp(info), _vp(ws), ws.numel(),
+                                self.stream())
+        out = []
+        mo = ro = po = co = 0
+        for t, v in enumerate(targets):
+            k, w, M, nc = ks[t], wprs[t], Ms[t], len(tables[t])
+            out.append(Explanation(target=v, sub=subs[t], plan=plans[t], classes=tables[t],
+                                   masks=masks[mo:mo + k * w].view(k, w), weights=weights[ro:ro + k],
+                                   y=y[ro:ro + k], f_empty_full=fef[2 * t:2 * t + 2], cls=cls[t:t + 1],
+                                   phi=phi[po:po + M], info=info[t:t + 1]))
+            mo += k * w
+            ro += k
+            po += M
+            co += nc
+        return out

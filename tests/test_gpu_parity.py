@@ -339,9 +339,12 @@ def test_solve_exhaustive_equals_exact_shapley(dev, M):
     _phi_close(phi.cpu().numpy().astype(np.float64), exact, rel=1e-4)
 
 
-@pytest.mark.parametrize("M,p", [(20, 10000), (60, 2000), (400, 10000), (1000, 6668), (4000, 25000)])
+@pytest.mark.parametrize("M,p", [(20, 10000), (60, 2000), (262, 4000), (263, 4000), (400, 10000), (448, 6000),
+                                 (449, 6000), (1000, 6668), (4000, 25000)])
 def test_solve_recovers_additive_game(dev, M, p):
-    """y = f0 + m.a has phi = a exactly for any determined sample set."""
+    """y = f0 + m.a has phi = a exactly for any determined sample set (sizes on
+    both sides of the LDS one-workgroup, global one-workgroup and multi-block
+    limits)."""
     from paper_2401_04829_amd import _lib as L
     from paper_2401_04829_amd.explainer import _vp
     _say("additive", M, p)
@@ -451,3 +454,83 @@ def test_full_size_workload(dev, name, picks):
         _phi_close(_solve_phi(res, y_add, 0.25, 0.25 + a.sum()), a)
         del res, y_add
         torch.cuda.empty_cache()
+
+
+# -- 6. many targets per launch sequence ----------------------------------------------------
+
+def _same_sub(a, b):
+    assert a.sg.num_nodes == b.sg.num_nodes and a.sg.num_edges == b.sg.num_edges and a.sg.num_dst == b.sg.num_dst
+    assert a.hop_ptr == b.hop_ptr
+    for name in ("node_gid", "dst_ptr", "edge_src", "edge_dst", "edge_gid"):
+        assert torch.equal(getattr(a, name), getattr(b, name)), name
+
+
+def test_extract_batch_matches_single(dev):
+    """gnnshap_extract_batch gives the single-target arrays, grows on
+    ECAPACITY, and leaves its workspace zero-filled for any batch size."""
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    ex._cap = [8, 16]                                  # force the capacity retry
+    targets = cfg["targets"]
+    subs, _ = ex.extract_batch(targets)
+    torch.cuda.synchronize()
+    for v, sb in zip(targets, subs):
+        _say("extract batch", v)
+        _check_subgraph(sb, subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"]))
+    assert int(ex._bx[1].count_nonzero()) == 0
+    subs2, _ = ex.extract_batch(targets[:7])           # smaller batch on the same workspace
+    torch.cuda.synchronize()
+    for v, sb in zip(targets[:7], subs2):
+        _same_sub(sb, ex.extract(v))
+    assert int(ex._bx[1].count_nonzero()) == 0
+
+
+@pytest.mark.parametrize("name,count", [("tiny", None), ("cora", None), ("pubmed", 6)])
+def test_explain_batch_matches_single(dev, name, count):
+    """gnnshap_explain_batch equals the single-target calls bit for bit: masks,
+    weights, values, f(empty)/f(E_c), class, phi and info (Cora-shaped targets
+    above the one-workgroup solve size and the three-layer PubMed-shaped model
+    take the single-target kernels inside the batch)."""
+    cfg = W.make_config(name)
+    ex = explainer_for(cfg)
+    targets = cfg["targets"] if count is None else cfg["targets"][:count]
+    many = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+    torch.cuda.synchronize()
+    for v, r in zip(targets, many):
+        _say("explain batch", name, v, r.plan.num_players)
+        one = ex.explain(v, cfg["p"], cfg["seed"])
+        torch.cuda.synchronize()
+        _same_sub(r.sub, one.sub)
+        for field in ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info"):
+            assert torch.equal(getattr(r, field), getattr(one, field)), field
+        assert int(r.info.item()) == 0
+
+
+def test_explain_batch_against_oracle(dev):
+    """Batched results against the oracle on the Cora-shaped workload: sampled
+    rows' masks bit-exact, values within the y bar, phi within the phi bar."""
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    targets = cfg["targets"][:12]
+    many = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(4)
+    for v, r in zip(targets, many):
+        _say("batch oracle", v)
+        ref_sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
+        M = ref_sub["num_edges"]
+        game = _oracle_game(cfg, ref_sub, None)
+        full_logits = game.logits(np.ones(M, bool))
+        cls = gcn.predicted_class(full_logits)
+        game.cls = cls
+        f0, f1 = game(np.zeros(M, bool)), float(full_logits[cls])
+        assert int(r.cls.item()) == cls
+        pl = sampler.plan(M, cfg["p"])
+        m, w = sampler.sample(pl, cfg["seed"], v)
+        np.testing.assert_array_equal(masks_np(r.masks), sampler.pack(m))
+        rows = np.unique(rng.integers(0, pl["k"], 32))
+        y_ref = game.values(m[rows])
+        err = np.abs(r.y.cpu().numpy()[rows].astype(np.float64) - y_ref)
+        assert (err <= y_tolerance(y_ref, f0, f1)).all()
+        phi_ref = wls.kernel_shap(m, w, game.values(m), f0, f1)
+        _phi_close(r.phi.cpu().numpy().astype(np.float64), phi_ref)

@@ -95,3 +95,15 @@ def test_workspace_queries_and_argument_checks():
     assert lib.gnnshap_extract_subgraph(ctypes.byref(g), 0, ctypes.byref(sub), 1, 10 ** 6, None) == L.EINVAL
     sub.num_hops = 2
     assert lib.gnnshap_extract_subgraph(ctypes.byref(g), 0, ctypes.byref(sub), 1, 16, None) == L.ECAPACITY
+
+
+def test_batch_entry_points_reject_bad_arguments():
+    lib = L.load()
+    n = ctypes.c_size_t()
+    assert lib.gnnshap_extract_batch_workspace(100, 0, ctypes.byref(n)) == L.EINVAL
+    assert lib.gnnshap_extract_batch_workspace(0, 4, ctypes.byref(n)) == L.EINVAL
+    assert lib.gnnshap_extract_batch_workspace(100, 4, ctypes.byref(n)) == L.OK and n.value > 0
+    assert lib.gnnshap_extract_batch(None, None, 1, None, None, 0, None) == L.EINVAL
+    assert lib.gnnshap_explain_batch_workspace(None, None, 1, None, ctypes.byref(n)) == L.EINVAL
+    assert lib.gnnshap_explain_batch(None, None, None, 0, None, None, -1, None, None, None, None, None, None, None,
+                                     None, 0, None) == L.EINVAL
