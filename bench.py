@@ -182,8 +182,8 @@ def main():
         ex.prepare()                 # X W_1 once per step, shared by every target
         if args.mode == "batch":
             res = ex.explain_batch(targets, cfg["p"], cfg["seed"])
-        else:
-            res = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=args.streams)
+            return res.total_rows, res
+        res = ex.explain_many(targets, cfg["p"], cfg["seed"], n_streams=args.streams)
         return sum(r.plan.num_rows for r in res), res
 
     if args.copy_probe:

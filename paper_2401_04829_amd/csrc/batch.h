@@ -36,6 +36,7 @@ struct EvalJob {
   int32_t* live_rows;
   uint8_t* live_flag;
   float* Zc1;
+  int32_t rows_ok;     // the main pass takes the one-thread-per-coalition kernel
 };
 struct EvalModel {
   const float* XW1;
@@ -51,8 +52,11 @@ bool eval_batchable(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k)
 size_t eval_slice_bytes(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k);
 // Carves job.ctl .. job.Zc1 from a slice.
 void eval_carve_slice(void* base, const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, EvalJob* job);
+// LDS of a target's one-thread-per-coalition main pass, 0 if it does not take it.
+size_t eval_rows_lds(const gnnshap_subgraph* sg, const gnnshap_gcn* m);
 int launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& md, int64_t max_nodes, int64_t max_ndst,
-                      int64_t max_n1, int64_t max_wpr, int64_t max_k, hipStream_t s);
+                      int64_t max_n1, int64_t max_wpr, int64_t max_k, int64_t rows_jobs, size_t rows_lds,
+                      hipStream_t s);
 
 // ---- least squares (one-workgroup systems) -----------------------------------------------
 struct SolveJob {

@@ -138,7 +138,8 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
   int st_eval = GNNSHAP_EUNSUPPORTED;
   if (eval_all) {
     std::vector<gnnshap::EvalJob> ej(n);
-    int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0;
+    int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0, rows_jobs = 0;
+    size_t rows_lds = 0;
     for (int64_t t = 0; t < n; ++t) {
       const gnnshap_subgraph& g = sgs[t];
       gnnshap::EvalJob& J = ej[t];
@@ -157,6 +158,10 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       J.fef = f_empty_full + 2 * t;
       J.cls_out = class_out ? class_out + t : nullptr;
       gnnshap::eval_carve_slice(b.eval_slice[t], &g, model, J.k, &J);
+      const size_t rl = gnnshap::eval_rows_lds(&g, model);
+      J.rows_ok = rl > 0 ? 1 : 0;
+      rows_jobs += J.rows_ok;
+      rows_lds = std::max(rows_lds, rl);
       max_nodes = std::max(max_nodes, J.n_nodes);
       max_ndst = std::max(max_ndst, J.n_dst);
       max_n1 = std::max(max_n1, J.n1);
@@ -164,7 +169,8 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     GS_HIP(hipMemcpyAsync(b.eval, ej.data(), n * sizeof(gnnshap::EvalJob), hipMemcpyHostToDevice, s));
     const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
                                 model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
-    st_eval = gnnshap::launch_eval_batch(b.eval, n, md, max_nodes, max_ndst, max_n1, max_wpr, max_k, s);
+    st_eval = gnnshap::launch_eval_batch(b.eval, n, md, max_nodes, max_ndst, max_n1, max_wpr, max_k, rows_jobs,
+                                         rows_lds, s);
     if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
     gnnshap::clear_error();
   }

@@ -539,6 +539,137 @@ __device__ __forceinline__ void eval_l2_body(
   }
 }
 
+// Main pass of the two-layer evaluation with one thread per coalition, for
+// narrow hidden layers (h <= H): a block of kRowsPerBlock coalitions stages
+// what they all read (each player's source and Z^1 row, Z^1 of H_1, the
+// destinations' player ranges) in LDS once; per coalition the degrees, layer
+// 1 at every node of H_1 folded into the explained logit, and layer 2 at the
+// target then run from registers and LDS without further barriers.
+constexpr int kRowsPerBlock = 128;
+
+size_t rows_lds_bytes(int64_t n_dst, int64_t n1, int64_t M, int H) {
+  return sizeof(float) * static_cast<size_t>(M * H + n1 * H + kRowsPerBlock * (n_dst + n1)) +
+         sizeof(int32_t) * static_cast<size_t>(M + n_dst + 1);
+}
+
+template <int H>
+__device__ __forceinline__ void eval_rows_body(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
+    const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src,
+    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zc, const float* __restrict__ b1,
+    const float* __restrict__ W2, const float* __restrict__ b2, int h, int C, const int32_t* __restrict__ ctl,
+    float* __restrict__ y_rows, int64_t block) {
+  constexpr int R = kRowsPerBlock;
+  extern __shared__ __align__(16) float sm[];
+  float* zall = sm;                                            // M x H
+  float* zself = zall + M * H;                                 // n1 x H
+  float* dinv = zself + n1 * H;                                // n_dst x R
+  float* tt = dinv + n_dst * R;                                // n1 x R
+  int32_t* sall = reinterpret_cast<int32_t*>(tt + n1 * R);     // M
+  int32_t* dptr = sall + M;                                    // n_dst + 1
+  const int64_t nr = rows_in_pass(dyn_count, 0, cap);
+  const int64_t b0 = block * R;
+  if (b0 >= nr) return;
+  const int tid = threadIdx.x;
+  const int64_t b = b0 + tid;
+  const bool valid = b < nr;
+  const int c0 = ctl[0];
+#pragma unroll 4
+  for (int64_t e = tid; e < M; e += R) sall[e] = edge_src[e];
+  for (int64_t x = tid; x <= n_dst; x += R) dptr[x] = dst_ptr[x];
+#pragma unroll 4
+  for (int64_t t = tid; t < n1 * H; t += R) {
+    const int64_t x = t / H, f = t % H;
+    zself[t] = f < h ? Zc[x * h + f] : 0.f;
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int64_t t = tid; t < M * H; t += R) {
+    const int64_t e = t / H, f = t % H;
+    zall[t] = f < h ? Zc[static_cast<int64_t>(sall[e]) * h + f] : 0.f;
+  }
+  const int64_t row = valid ? static_cast<int64_t>(rows[b]) : 0;
+  const uint64_t* mrow = masks + row * wpr;
+  // degrees of every destination under this coalition
+  for (int64_t x = 0; x < n_dst; ++x) {
+    const int64_t e0 = dptr[x], e1 = dptr[x + 1];
+    int cnt = 0;
+    for (int64_t w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+      uint64_t word = mrow[w];
+      const int64_t lo = w * 64;
+      if (e0 > lo) word &= ~uint64_t(0) << (e0 - lo);
+      if (e1 < lo + 64) word &= (uint64_t(1) << (e1 - lo)) - 1;
+      cnt += __popcll(word);
+    }
+    dinv[x * R + tid] = rsqrtf(1.0f + static_cast<float>(cnt));
+  }
+  float w2v[H], b1v[H];
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    w2v[i] = i < h ? W2[static_cast<int64_t>(i) * C + c0] : 0.f;
+    b1v[i] = (b1 && i < h) ? b1[i] : 0.f;
+  }
+  __syncthreads();
+  // layer 1 at every node of H_1, folded into the explained logit
+  for (int64_t x = 0; x < n1; ++x) {
+    const int64_t e0 = dptr[x], e1 = dptr[x + 1];
+    float acc[H];
+#pragma unroll
+    for (int i = 0; i < H; ++i) acc[i] = 0.f;
+    for (int64_t w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+      uint64_t bits = mrow[w];
+      const int64_t lo = w * 64;
+      if (e0 > lo) bits &= ~uint64_t(0) << (e0 - lo);
+      if (e1 < lo + 64) bits &= (uint64_t(1) << (e1 - lo)) - 1;
+      while (bits) {
+        const int64_t e = lo + __ffsll(static_cast<long long>(bits)) - 1;
+        bits &= bits - 1;
+        const int32_t u = sall[e];
+        const float coef = u < n_dst ? dinv[u * R + tid] : 1.0f;
+        const float* z = zall + e * H;
+#pragma unroll
+        for (int i = 0; i < H; i += 4) {
+          const float4 zz = *reinterpret_cast<const float4*>(z + i);
+          acc[i] += coef * zz.x;
+          acc[i + 1] += coef * zz.y;
+          acc[i + 2] += coef * zz.z;
+          acc[i + 3] += coef * zz.w;
+        }
+      }
+    }
+    const float dx = dinv[x * R + tid];
+    float p = 0.f;
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+      const float hv = i < h ? fmaxf(dx * (acc[i] + dx * zself[x * H + i]) + b1v[i], 0.f) : 0.f;
+      p += hv * w2v[i];
+    }
+    tt[x * R + tid] = p;
+  }
+  // layer 2 at the target
+  const int64_t indeg = dptr[1];
+  const float dv = dinv[tid];
+  float acc = 0.f;
+  for (int64_t e = 0; e < indeg; ++e) {
+    if (!((mrow[e >> 6] >> (e & 63)) & 1)) continue;
+    const int32_t u = sall[e];
+    acc += dinv[u * R + tid] * tt[u * R + tid];
+  }
+  acc += dv * tt[tid];
+  if (valid) y_rows[row] = dv * acc + (b2 ? b2[c0] : 0.f);
+}
+
+template <int H>
+__global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
+    const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src,
+    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zc, const float* __restrict__ b1,
+    const float* __restrict__ W2, const float* __restrict__ b2, int h, int C, const int32_t* __restrict__ ctl,
+    float* __restrict__ y_rows) {
+  eval_rows_body<H>(masks, wpr, rows, cap, dyn_count, dst_ptr, edge_src, n_dst, n1, M, Zc, b1, W2, b2, h, C, ctl,
+                    y_rows, blockIdx.x);
+}
+
 template <int FPT>
 __global__ void __launch_bounds__(256) k_eval_l2(
     const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t row_off,
@@ -618,6 +749,52 @@ __global__ void k_fill_pruned(const uint8_t* __restrict__ live_flag, int64_t k,
     if (!live_flag[b]) y[b] = f0;
 }
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Z[r, :] = X[r, :] W for 16 rows per workgroup, h = 16 NT columns, fp32
+// MFMA 16x16x4.  The four wavefronts split K into quarters and each lane
+// group of 16 lanes takes a quarter of its wavefront's range, so every MFMA
+// sums four k; the four partial 16 x h tiles are added in LDS in a fixed
+// order (no atomics: the result does not depend on scheduling).
+template <int NT>
+__global__ void __launch_bounds__(256) k_transform(const float* __restrict__ X, int64_t n, int d,
+                                                   const float* __restrict__ W, int h, float* __restrict__ Z) {
+  __shared__ float part[4][16][16 * NT + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 16;
+  const int64_t row = r0 + c;
+  const int kq = (d + 3) / 4;
+  const int kb = wave * kq;
+  const int ke = kb + kq < d ? kb + kq : d;
+  const int kg = (kq + 3) / 4;
+  const int k0 = kb + g * kg;
+  f32x4_t acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const float* xr = X + (row < n ? row : 0) * static_cast<int64_t>(d);
+#pragma unroll 4
+  for (int s = 0; s < kg; ++s) {
+    const int k = k0 + s;
+    const bool kin = k < ke && k < k0 + kg;
+    const float a = (kin && row < n) ? xr[k] : 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float b = kin ? W[static_cast<int64_t>(k) * h + t * 16 + c] : 0.f;
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[t], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) part[wave][4 * g + r][t * 16 + c] = acc[t][r];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 16 * h; idx += 256) {
+    const int i = idx / h, j = idx % h;
+    if (r0 + i < n) Z[(r0 + i) * h + j] = (part[0][i][j] + part[1][i][j]) + (part[2][i][j] + part[3][i][j]);
+  }
+}
+
 int launch_gemm(hipStream_t s, const float* A, int64_t lda, const int32_t* arow, const float* abias,
                 const float* B, int64_t ldb, float* C, int64_t ldc, int64_t m0, int64_t rows, int64_t N,
                 int64_t K, const int32_t* dyn = nullptr, int64_t dyn_off = 0, int64_t dyn_cap = 0,
@@ -695,12 +872,26 @@ int launch_fused_l2(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn
                                    sh.n_dst, sh.nd[1], w.Zc[1], b1, m->W[1], b2, h, C, w.ctl, all_classes, \
                                    tbr, y_rows, w.sp_y)
   GS_TIMED("k_eval_l2", s);
-  switch (fpt) {
-    case 1: GS_L2(1); break;
-    case 2: GS_L2(2); break;
-    case 4: GS_L2(4); break;
-    case 8: GS_L2(8); break;
-    default: GS_L2(16); break;
+  const int H = h <= 16 ? 16 : 32;
+  const size_t lds_rows = rows_lds_bytes(sh.n_dst, sh.nd[1], sg->num_edges, H);
+  if (!all_classes && row_off == 0 && h <= 32 && lds_rows <= 65536) {
+    const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(cap, kRowsPerBlock));
+    if (H == 16)
+      k_eval_rows<16><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src,
+                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], b1, m->W[1],
+                                                          b2, h, C, w.ctl, y_rows);
+    else
+      k_eval_rows<32><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src,
+                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], b1, m->W[1],
+                                                          b2, h, C, w.ctl, y_rows);
+  } else {
+    switch (fpt) {
+      case 1: GS_L2(1); break;
+      case 2: GS_L2(2); break;
+      case 4: GS_L2(4); break;
+      case 8: GS_L2(8); break;
+      default: GS_L2(16); break;
+    }
   }
 #undef GS_L2
   GS_LAUNCHED();
@@ -775,9 +966,19 @@ __global__ void __launch_bounds__(256) k_eval_l2_batch(const gnnshap::EvalJob* _
   if (special)
     eval_l2_body<FPT>(J.sp_masks, J.wpr, J.sp_rows, 0, 2, nullptr, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1,
                       md.b1, md.W2, md.b2, md.h, md.C, J.ctl, true, tbr, nullptr, J.sp_y, blockIdx.x);
-  else
+  else if (!J.rows_ok)
     eval_l2_body<FPT>(J.masks, J.wpr, J.live_rows, 0, J.k, J.ctl + 1, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1,
                       md.b1, md.W2, md.b2, md.h, md.C, J.ctl, false, tbr, J.y, J.sp_y, blockIdx.x);
+}
+
+// Main pass of the jobs that take the one-thread-per-coalition kernel.
+template <int H>
+__global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows_batch(const gnnshap::EvalJob* __restrict__ jobs,
+                                                                   gnnshap::EvalModel md) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  if (!J.rows_ok) return;
+  eval_rows_body<H>(J.masks, J.wpr, J.live_rows, J.k, J.ctl + 1, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.M, J.Zc1,
+                    md.b1, md.W2, md.b2, md.h, md.C, J.ctl, J.y, blockIdx.x);
 }
 
 __global__ void k_pick_class_batch(const gnnshap::EvalJob* __restrict__ jobs, int C, int requested) {
@@ -883,9 +1084,26 @@ extern "C" int gnnshap_transform_features(const float* X, int64_t n, int32_t d, 
   gnnshap::clear_error();
   if (!X || !W || !Z) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
   if (n < 1 || d < 1 || h < 1) return gnnshap::fail(GNNSHAP_EINVAL, "bad sizes");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (h % 16 == 0 && h <= 128 && gnnshap::ceil_div(n, 16) <= INT32_MAX) {
+    const unsigned g = static_cast<unsigned>(gnnshap::ceil_div(n, 16));
+    GS_TIMED("k_transform", s);
+    switch (h / 16) {
+      case 1: k_transform<1><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 2: k_transform<2><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 3: k_transform<3><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 4: k_transform<4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 5: k_transform<5><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 6: k_transform<6><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 7: k_transform<7><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      default: k_transform<8><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+    }
+    GS_LAUNCHED();
+    return GNNSHAP_OK;
+  }
   if (gnnshap::ceil_div(n, 64) > INT32_MAX || gnnshap::ceil_div(h, 64) > 65535)
     return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "matrix too large");
-  return launch_gemm(static_cast<hipStream_t>(stream), X, d, nullptr, nullptr, W, h, Z, h, 0, n, h, d);
+  return launch_gemm(s, X, d, nullptr, nullptr, W, h, Z, h, 0, n, h, d);
   GS_TRY_END
 }
 
@@ -925,7 +1143,8 @@ void gnnshap::eval_carve_slice(void* base, const gnnshap_subgraph* sg, const gnn
 }
 
 int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& md, int64_t max_nodes,
-                               int64_t max_ndst, int64_t max_n1, int64_t max_wpr, int64_t max_k, hipStream_t s) {
+                               int64_t max_ndst, int64_t max_n1, int64_t max_wpr, int64_t max_k, int64_t rows_jobs,
+                               size_t rows_lds, hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   Shape sh;                          // the largest shapes of the batch, for LDS sizing
@@ -960,9 +1179,16 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
   GS_LAUNCHED();
   k_live_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
-  {
+  if (rows_jobs < n) {
     GS_TIMED("k_eval_l2_batch", s);
     GS_L2B_ALL(dim3(static_cast<unsigned>(ceil_div(max_k, tb_main)), nn), lds_main, false, tb_main);
+  }
+  GS_LAUNCHED();
+  if (rows_jobs > 0) {
+    GS_TIMED("k_eval_rows_batch", s);
+    const dim3 g(static_cast<unsigned>(ceil_div(max_k, kRowsPerBlock)), nn);
+    if (md.h <= 16) k_eval_rows_batch<16><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md);
+    else k_eval_rows_batch<32><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md);
   }
   GS_LAUNCHED();
 #undef GS_L2B_ALL
@@ -970,4 +1196,12 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
   k_fill_pruned_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
   return GNNSHAP_OK;
+}
+
+// Whether a target's main pass takes the one-thread-per-coalition kernel, and its LDS.
+size_t gnnshap::eval_rows_lds(const gnnshap_subgraph* sg, const gnnshap_gcn* m) {
+  const int h = m->dims[1];
+  if (m->num_layers != 2 || h > 32) return 0;
+  const size_t b = rows_lds_bytes(sg->num_dst, sg->hop_ptr[2], sg->num_edges, h <= 16 ? 16 : 32);
+  return b <= 65536 ? b : 0;
 }

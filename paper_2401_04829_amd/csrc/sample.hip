@@ -58,8 +58,12 @@ __device__ __forceinline__ uint64_t binom(int64_t n, int64_t r) {
 
 __device__ __forceinline__ void set_bit(uint32_t* bs, int64_t j) { bs[j >> 5] |= 1u << (j & 31); }
 
-// Rows first, first + stride, ... < half of one job; one wavefront.
-__device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t first, int64_t stride) {
+constexpr int64_t kMaxComb = 64;   // enumerated subsets stepped incrementally up to this size
+
+// Rows [r_begin, min(r_end, half)) of one job; one wavefront.  The class of
+// the first row is found by binary search, later rows advance through the
+// class table (rows are grouped by class).
+__device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t r_begin, int64_t r_end) {
   const gnnshap_class* __restrict__ cls = J.cls;
   const int64_t ncls = J.ncls, half = J.half, M = J.M, wpr = J.wpr;
   const uint32_t seed_lo = J.seed_lo, seed_hi = J.seed_hi, st_lo = J.st_lo, st_hi = J.st_hi;
@@ -75,36 +79,60 @@ __device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t
     D1[w] = 0;
     D2[w] = 0;
   }
-  for (int64_t i = first; i < half; i += stride) {
-    int64_t lo = 0, hi = ncls - 1;      // last class starting at or before row i
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (cls[mid].row_begin <= i) lo = mid; else hi = mid - 1;
+  if (r_end > half) r_end = half;
+  int64_t lo = 0, hi = ncls - 1;        // last class starting at or before row r_begin
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (cls[mid].row_begin <= r_begin) lo = mid; else hi = mid - 1;
+  }
+  gnnshap_class cur = cls[lo];
+  int64_t next_begin = lo + 1 < ncls ? cls[lo + 1].row_begin : half;
+  // lane 0's last enumerated subset (positions in LDS), to step to the next rank
+  __shared__ int32_t comb[kMaxComb];
+  int64_t comb_cls = -1, comb_rank = -2;
+  for (int64_t i = r_begin; i < r_end; ++i) {
+    while (i >= next_begin) {
+      ++lo;
+      cur = cls[lo];
+      next_begin = lo + 1 < ncls ? cls[lo + 1].row_begin : half;
     }
-    const int64_t c = cls[lo].size;
-    const int full = cls[lo].full;
-    const int64_t rank = i - cls[lo].row_begin;
-    const float wt = static_cast<float>(cls[lo].weight);
+    const int64_t c = cur.size;
+    const int full = cur.full;
+    const int64_t rank = i - cur.row_begin;
+    const float wt = static_cast<float>(cur.weight);
     for (int64_t w = lane; w < nw; w += 64) S[w] = 0;
     __syncthreads();
     if (full) {
       if (lane == 0) {
-        // rank-th c-subset in lexicographic order: for each position, skip
-        // whole blocks of subsets with one binary search (hockey-stick sums).
-        uint64_t q = static_cast<uint64_t>(rank);
-        int64_t x = 0;
-        for (int64_t jj = 1; jj <= c; ++jj) {
-          const int64_t r = c - jj;
-          const uint64_t top = binom(M - x, r + 1);
-          int64_t a = x, b = M - r - 1;
-          while (a < b) {
-            const int64_t mid = (a + b + 1) >> 1;
-            if (top - binom(M - mid, r + 1) <= q) a = mid; else b = mid - 1;
+        if (c <= kMaxComb && comb_cls == lo && comb_rank + 1 == rank) {
+          // the next c-subset in lexicographic order: bump the last position
+          // that can move, restart the positions after it
+          int64_t p = c - 1;
+          while (comb[p] == M - c + p) --p;
+          ++comb[p];
+          for (int64_t q = p + 1; q < c; ++q) comb[q] = comb[q - 1] + 1;
+          for (int64_t q = 0; q < c; ++q) set_bit(S, comb[q]);
+        } else {
+          // rank-th c-subset in lexicographic order: for each position, skip
+          // whole blocks of subsets with one binary search (hockey-stick sums).
+          uint64_t q = static_cast<uint64_t>(rank);
+          int64_t x = 0;
+          for (int64_t jj = 1; jj <= c; ++jj) {
+            const int64_t r = c - jj;
+            const uint64_t top = binom(M - x, r + 1);
+            int64_t a = x, b = M - r - 1;
+            while (a < b) {
+              const int64_t mid = (a + b + 1) >> 1;
+              if (top - binom(M - mid, r + 1) <= q) a = mid; else b = mid - 1;
+            }
+            q -= top - binom(M - a, r + 1);
+            set_bit(S, a);
+            if (c <= kMaxComb) comb[jj - 1] = static_cast<int32_t>(a);
+            x = a + 1;
           }
-          q -= top - binom(M - a, r + 1);
-          set_bit(S, a);
-          x = a + 1;
         }
+        comb_cls = c <= kMaxComb ? lo : -1;
+        comb_rank = rank;
       }
     } else {
       for (int64_t base = 0; base < c; base += 64) {
@@ -171,13 +199,26 @@ __device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t
   }
 }
 
-__global__ void __launch_bounds__(64) k_sample(gnnshap::SampleJob J) { sample_rows(J, blockIdx.x, gridDim.x); }
+// Consecutive representative rows per wavefront: enough workgroups to fill
+// the GPU several times over, at most kRowsPerBlock rows each.
+constexpr int64_t kRowsPerBlock = 16;
+
+int64_t rows_per_block(int64_t half) {
+  int64_t r = half / 4096;
+  return r < 1 ? 1 : (r > kRowsPerBlock ? kRowsPerBlock : r);
+}
+
+__global__ void __launch_bounds__(64) k_sample(gnnshap::SampleJob J, int64_t rpb) {
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rpb;
+  sample_rows(J, r0, r0 + rpb);
+}
 
 // One job per blockIdx.y.
-__global__ void __launch_bounds__(64) k_sample_batch(const gnnshap::SampleJob* __restrict__ jobs) {
+__global__ void __launch_bounds__(64) k_sample_batch(const gnnshap::SampleJob* __restrict__ jobs, int64_t rpb) {
   const gnnshap::SampleJob J = jobs[blockIdx.y];
-  if (blockIdx.x >= J.half) return;
-  sample_rows(J, blockIdx.x, gridDim.x);
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rpb;
+  if (r0 >= J.half) return;
+  sample_rows(J, r0, r0 + rpb);
 }
 
 int check_plan(const gnnshap_sample_plan* plan) {
@@ -232,14 +273,17 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
                         hipMemcpyHostToDevice, s));
   const int64_t wpr = plan->words_per_row;
   const size_t lds = static_cast<size_t>(3 * 2 * wpr) * sizeof(uint32_t);
-  const unsigned grid = static_cast<unsigned>(half < 65536 ? half : 65536);
+  const int64_t rpb = rows_per_block(half);
+  const int64_t nblk = gnnshap::ceil_div(half, rpb);
+  if (nblk > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "too many rows");
+  const unsigned grid = static_cast<unsigned>(nblk);
   {
     GS_TIMED("k_sample", s);
     const gnnshap::SampleJob job{w.classes, plan->num_classes, half, M, wpr,
                                  static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
                                  static_cast<uint32_t>(plan->stream_id),
                                  static_cast<uint32_t>(plan->stream_id >> 32), masks, weights};
-    k_sample<<<grid, 64, lds, s>>>(job);
+    k_sample<<<grid, 64, lds, s>>>(job, rpb);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
@@ -251,9 +295,14 @@ int gnnshap::launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t max_h
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   const size_t lds = static_cast<size_t>(3 * 2 * max_wpr) * sizeof(uint32_t);
-  const dim3 grid(static_cast<unsigned>(max_half < 65536 ? max_half : 65536), static_cast<unsigned>(n));
+  // at least 4096 workgroups over the batch
+  int64_t rpb = max_half * n / 4096;
+  rpb = rpb < 1 ? 1 : (rpb > kRowsPerBlock ? kRowsPerBlock : rpb);
+  const int64_t nblk = ceil_div(max_half, rpb);
+  if (nblk > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "too many rows");
+  const dim3 grid(static_cast<unsigned>(nblk), static_cast<unsigned>(n));
   GS_TIMED("k_sample_batch", s);
-  k_sample_batch<<<grid, 64, lds, s>>>(jobs);
+  k_sample_batch<<<grid, 64, lds, s>>>(jobs, rpb);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }

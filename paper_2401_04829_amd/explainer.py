@@ -231,7 +231,7 @@ class Explainer:
     def extract_batch(self, targets):
         """gnnshap_extract_batch: the computational graphs of all targets with one
         host synchronisation; capacities grow and the batch is redone on
-        ECAPACITY.  Returns a list of Subgraph views into packed buffers."""
+        ECAPACITY.  Returns (BatchSubgraphs, ctypes array of gnnshap_subgraph)."""
         dev = self.device
         n = len(targets)
         if self._bx is None or self._bx[0] < n:
@@ -241,14 +241,10 @@ class Explainer:
         tg = (ctypes.c_int64 * n)(*[int(v) for v in targets])
         while True:
             cn, ce = self._cap
-            node_gid = torch.empty((n, cn), dtype=torch.int32, device=dev)
-            dst_ptr = torch.empty((n, cn + 1), dtype=torch.int32, device=dev)
-            edge_src = torch.empty((n, ce), dtype=torch.int32, device=dev)
-            edge_dst = torch.empty((n, ce), dtype=torch.int32, device=dev)
-            edge_gid = torch.empty((n, ce), dtype=torch.int64, device=dev)
+            bufs = BatchSubgraphs(n, cn, ce, dev)
             sgs = (L.gnnshap_subgraph * n)()
-            pn, pd, ps, pe, pg = (node_gid.data_ptr(), dst_ptr.data_ptr(), edge_src.data_ptr(), edge_dst.data_ptr(),
-                                  edge_gid.data_ptr())
+            pn, pd, ps, pe, pg = (bufs.node_gid.data_ptr(), bufs.dst_ptr.data_ptr(), bufs.edge_src.data_ptr(),
+                                  bufs.edge_dst.data_ptr(), bufs.edge_gid.data_ptr())
             for t in range(n):
                 sg = sgs[t]
                 sg.num_hops, sg.cap_nodes, sg.cap_edges = self.hops, cn, ce
@@ -259,20 +255,15 @@ class Explainer:
                 break
             self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
                          max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
-        subs = []
-        for t in range(n):
-            sg = sgs[t]
-            m, nn, nd = sg.num_edges, sg.num_nodes, sg.num_dst
-            subs.append(Subgraph(sg=sg, node_gid=node_gid[t, :nn], dst_ptr=dst_ptr[t, :nd + 1],
-                                 edge_src=edge_src[t, :m], edge_dst=edge_dst[t, :m], edge_gid=edge_gid[t, :m]))
-        return subs, sgs
+        bufs.sgs = sgs
+        return bufs, sgs
 
     def explain_batch(self, targets, num_samples, seed, target_class=-1):
         """Alg. 1 for every target, one launch per step for the whole batch
         (gnnshap_extract_batch, then gnnshap_explain_batch); each target's
         Philox stream is its node id.  Results equal explain()'s bit for bit.
-        Returns one Explanation per target (views into packed tensors, valid
-        once the current stream has run)."""
+        Returns a BatchExplanations (packed tensors, valid once the current
+        stream has run; indexing gives per-target Explanation views)."""
         if self.XW1 is None:
             self.prepare()
         dev = self.device
@@ -289,35 +280,72 @@ class Explainer:
         ncls = sum(len(c) for c in tables)
         classes = (L.gnnshap_class * ncls)()
         o = 0
+        csz = ctypes.sizeof(L.gnnshap_class)
         for cl in tables:
-            ctypes.memmove(ctypes.byref(classes, o * ctypes.sizeof(L.gnnshap_class)), cl, ctypes.sizeof(cl))
+            ctypes.memmove(ctypes.byref(classes, o * csz), cl, ctypes.sizeof(cl))
             o += len(cl)
-        ks = [plans[t].num_rows for t in range(n)]
-        wprs = [plans[t].words_per_row for t in range(n)]
-        Ms = [plans[t].num_players for t in range(n)]
-        words = sum(k * w for k, w in zip(ks, wprs))
-        rows, players = sum(ks), sum(Ms)
-        masks = torch.empty(words, dtype=torch.int64, device=dev)
-        weights = torch.empty(rows, dtype=torch.float32, device=dev)
-        y = torch.empty(rows, dtype=torch.float32, device=dev)
-        fef = torch.empty(2 * n, dtype=torch.float32, device=dev)
-        cls = torch.empty(n, dtype=torch.int32, device=dev)
-        phi = torch.empty(players, dtype=torch.float32, device=dev)
-        info = torch.empty(n, dtype=torch.int32, device=dev)
+        out = BatchExplanations(targets, subs, plans, tables, dev)
         ws = self.ws_batch.get(L.gnnshap_explain_batch_workspace(sgs, plans, self.model))
-        L.gnnshap_explain_batch(sgs, plans, classes, self.model, _vp(self.X), int(target_class), _vp(masks),
-                                _vp(weights), _vp(y), _vp(fef), _vp(cls), _vp(phi), _vp(info), _vp(ws), ws.numel(),
-                                self.stream())
-        out = []
-        mo = ro = po = co = 0
-        for t, v in enumerate(targets):
-            k, w, M, nc = ks[t], wprs[t], Ms[t], len(tables[t])
-            out.append(Explanation(target=v, sub=subs[t], plan=plans[t], classes=tables[t],
-                                   masks=masks[mo:mo + k * w].view(k, w), weights=weights[ro:ro + k],
-                                   y=y[ro:ro + k], f_empty_full=fef[2 * t:2 * t + 2], cls=cls[t:t + 1],
-                                   phi=phi[po:po + M], info=info[t:t + 1]))
-            mo += k * w
-            ro += k
-            po += M
-            co += nc
+        L.gnnshap_explain_batch(sgs, plans, classes, self.model, _vp(self.X), int(target_class), _vp(out.masks),
+                                _vp(out.weights), _vp(out.y), _vp(out.fef), _vp(out.cls), _vp(out.phi),
+                                _vp(out.info), _vp(ws), ws.numel(), self.stream())
         return out
+
+
+class BatchSubgraphs:
+    """Packed subgraph buffers of a batch: target t owns row t of each array."""
+
+    def __init__(self, n, cap_nodes, cap_edges, dev):
+        self.node_gid = torch.empty((n, cap_nodes), dtype=torch.int32, device=dev)
+        self.dst_ptr = torch.empty((n, cap_nodes + 1), dtype=torch.int32, device=dev)
+        self.edge_src = torch.empty((n, cap_edges), dtype=torch.int32, device=dev)
+        self.edge_dst = torch.empty((n, cap_edges), dtype=torch.int32, device=dev)
+        self.edge_gid = torch.empty((n, cap_edges), dtype=torch.int64, device=dev)
+        self.sgs = None
+
+    def __getitem__(self, t):
+        sg = self.sgs[t]
+        m, nn, nd = sg.num_edges, sg.num_nodes, sg.num_dst
+        return Subgraph(sg=sg, node_gid=self.node_gid[t, :nn], dst_ptr=self.dst_ptr[t, :nd + 1],
+                        edge_src=self.edge_src[t, :m], edge_dst=self.edge_dst[t, :m], edge_gid=self.edge_gid[t, :m])
+
+
+class BatchExplanations:
+    """Outputs of gnnshap_explain_batch, packed in target order; entry t is
+    materialised as an Explanation (tensor views) on access."""
+
+    def __init__(self, targets, subs, plans, tables, dev):
+        n = len(targets)
+        self.targets, self.subs, self.plans, self.tables = list(targets), subs, plans, tables
+        self.k = [plans[t].num_rows for t in range(n)]
+        self.wpr = [plans[t].words_per_row for t in range(n)]
+        self.M = [plans[t].num_players for t in range(n)]
+        self.total_rows = sum(self.k)
+        self.mask_off, self.row_off, self.player_off = [0], [0], [0]
+        for t in range(n):
+            self.mask_off.append(self.mask_off[-1] + self.k[t] * self.wpr[t])
+            self.row_off.append(self.row_off[-1] + self.k[t])
+            self.player_off.append(self.player_off[-1] + self.M[t])
+        self.masks = torch.empty(self.mask_off[-1], dtype=torch.int64, device=dev)
+        self.weights = torch.empty(self.total_rows, dtype=torch.float32, device=dev)
+        self.y = torch.empty(self.total_rows, dtype=torch.float32, device=dev)
+        self.fef = torch.empty(2 * n, dtype=torch.float32, device=dev)
+        self.cls = torch.empty(n, dtype=torch.int32, device=dev)
+        self.phi = torch.empty(self.player_off[-1], dtype=torch.float32, device=dev)
+        self.info = torch.empty(n, dtype=torch.int32, device=dev)
+
+    def __len__(self):
+        return len(self.targets)
+
+    def __getitem__(self, t):
+        if t < 0:
+            t += len(self)
+        mo, ro, po = self.mask_off[t], self.row_off[t], self.player_off[t]
+        k, w, M = self.k[t], self.wpr[t], self.M[t]
+        return Explanation(target=self.targets[t], sub=self.subs[t], plan=self.plans[t], classes=self.tables[t],
+                           masks=self.masks[mo:mo + k * w].view(k, w), weights=self.weights[ro:ro + k],
+                           y=self.y[ro:ro + k], f_empty_full=self.fef[2 * t:2 * t + 2], cls=self.cls[t:t + 1],
+                           phi=self.phi[po:po + M], info=self.info[t:t + 1])
+
+    def __iter__(self):
+        return (self[t] for t in range(len(self)))
