@@ -74,7 +74,7 @@ VALU_INT_TOPS = 39.3
 def work_model(kernel, results, dims):
     """Algorithmic work of the timed kernel over one step: (amount, unit, bound, peak).
 
-    k_solve_small / k_solve_mid / k_solve_one_batch (one-workgroup solves)
+    k_solve_mid / k_solve_one_batch (one-workgroup solves)
                    M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
     k_eval_l2      (k/2) M h useful MACs per target (complement pairs cover every
                    player-feature product once) + the layer-2 dot products
@@ -92,10 +92,8 @@ def work_model(kernel, results, dims):
         M, k = r.plan.num_players, r.plan.num_rows
         wpr = r.plan.words_per_row
         kr = k // 2 - r.plan.random_begin
-        if base in ("k_solve_small", "k_solve_mid", "k_solve_one"):
-            path = _lib.gnnshap_solve_info(r.plan)
-            if (base == "k_solve_small" and path == 1) or (base == "k_solve_mid" and path == 2) or \
-                    (base == "k_solve_one" and path in (1, 2)):
+        if base in ("k_solve_mid", "k_solve_one"):
+            if _lib.gnnshap_solve_info(r.plan) == 1:
                 tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
         elif base == "k_eval_l2":
             n1 = r.sub.sg.hop_ptr[2]
@@ -115,7 +113,7 @@ def work_model(kernel, results, dims):
 
 CANDIDATES = {
     "batch": ["k_solve_one_batch", "k_eval_l2_batch", "k_rhs_part_batch", "k_gram_batch", "k_sample_batch"],
-    "streams": ["k_solve_small", "k_solve_mid", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
+    "streams": ["k_solve_mid", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
 }
 
 

@@ -292,10 +292,8 @@ int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan
 /* Diagnostics: HIP-event timing of one kernel.                             */
 /* ------------------------------------------------------------------------ */
 
-/* Which solver the plan's system takes: *path = 1 if one workgroup
- * assembles, factors and solves it in LDS (its lower triangle fits one CU's
- * LDS), 2 if one workgroup factors it in global memory (M <= 448), 0 if it
- * takes the multi-block Cholesky.  Needs the device (queries LDS limits). */
+/* Which solver the plan's system takes: *path = 1 if one workgroup factors
+ * and solves it (M <= 448), 0 if it takes the multi-block Cholesky. */
 int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path);
 
 /* Arms timing for the kernels whose name starts with `kernel_name` (e.g.

@@ -220,7 +220,7 @@ def gnnshap_explain_batch(sgs, plans, classes, model, X_ptr, target_class, masks
 
 
 def gnnshap_solve_info(plan):
-    """Solver path of the plan's system: 1 one workgroup in LDS, 2 one workgroup in global memory, 0 multi-block."""
+    """Solver path of the plan's system: 1 one workgroup, 0 multi-block."""
     v = c_i32()
     check(load().gnnshap_solve_info(ctypes.byref(plan), ctypes.byref(v)), "solve_info")
     return v.value

@@ -74,8 +74,8 @@ struct SolveJob {
   double* part;
   int64_t* usum;
   double* dv;
+  double* scal;
   float* Wd;
-  int32_t mid;               // 1: the global-memory one-workgroup path, 0: the LDS-resident one
 };
 // Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
 bool solve_batchable(const gnnshap_sample_plan* plan);

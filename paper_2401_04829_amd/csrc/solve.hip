@@ -14,9 +14,9 @@
 //   * the random rows share one weight w_r, so their part is 2 w_r P C_R P
 //     with C_R the integer co-occurrence counts of the random representative
 //     rows, computed exactly by popcounts on a bit-transposed copy.
-// Systems whose lower triangle fits in LDS are assembled, factored and solved
-// by one workgroup.  Larger ones use a blocked right-looking Cholesky over the
-// whole GPU with 128-wide panels: one workgroup factors the diagonal block and
+// Systems of up to 448 players are factored and solved by one workgroup
+// (several targets' systems side by side in a batch).  Larger ones use a
+// blocked right-looking Cholesky over the whole GPU with 128-wide panels: one workgroup factors the diagonal block and
 // inverts its factor, then the panel solve (a product with that inverse) and
 // the trailing update run as fp32 MFMA GEMMs.  The triangular solves go by
 // 256-row segments whose triangle sits in LDS, with multi-block GEMVs carrying
@@ -32,7 +32,6 @@ namespace {
 
 constexpr int kPB = 128;       // panel width, multi-block Cholesky
 constexpr int kTB = 64;        // diagonal block of the triangular solves (one wavefront)
-constexpr int kSB = 32;        // panel width, one-workgroup path
 constexpr int64_t kSeg = 256;  // segment of the triangular solves (its triangle in LDS)
 constexpr int kMaxChunks = 256;
 constexpr int kMidMax = 448;   // largest system of the global-memory one-workgroup path
@@ -99,40 +98,6 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
   return v;
-}
-
-// a[lane] without a dynamic register index: unrolled selects.
-template <int NB>
-__device__ __forceinline__ float lane_entry(const float (&a)[NB]) {
-  const int lane = threadIdx.x & 63;
-  float d = 1.f;
-#pragma unroll
-  for (int c = 0; c < NB; ++c) d = c == lane ? a[c] : d;
-  return d;
-}
-
-// Cholesky of an NB x NB lower block held by one wavefront, row `lane` in
-// a[] (rows and columns past the real block are the identity).  Column k:
-// broadcast the pivot, scale the column, rank-1 update of the later
-// columns.  Entries above each lane's diagonal are left undefined.  The
-// first non-positive pivot (1-based, offset o) goes to *info and is replaced
-// by 1.
-template <int NB>
-__device__ __forceinline__ void chol_regs(float (&a)[NB], int64_t o, int32_t* info) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 0; k < NB; ++k) {
-    float piv = bcast(a[k], k);
-    if (!(piv > 0.f)) {
-      if (lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + k + 1));
-      piv = 1.f;
-    }
-    // lane k holds the pivot itself: piv / sqrt(piv) = sqrt(piv), so one
-    // scaling serves the diagonal and the column below it
-    a[k] *= 1.0f / sqrtf(piv);
-#pragma unroll
-    for (int j = k + 1; j < NB; ++j) a[j] -= a[k] * bcast(a[k], j);
-  }
 }
 
 // T[rb, j]: transpose 64 rows x 64 players with ballots.  One wave per (rb, word).
@@ -225,9 +190,9 @@ __global__ void __launch_bounds__(256) k_rowsum(const int32_t* __restrict__ C, i
 }
 
 // scal: trace and sigma of the counts (exact), gamma, Delta, f0.  One block.
-__global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, const int64_t* __restrict__ usum,
-                                                 int64_t M, int64_t ld, bool has_random, double alpha, double wr,
-                                                 const float* __restrict__ fef, double* scal) {
+__device__ __forceinline__ void scalars_body(const int32_t* __restrict__ C, const int64_t* __restrict__ usum,
+                                             int64_t M, int64_t ld, bool has_random, double alpha, double wr,
+                                             const float* __restrict__ fef, double* scal) {
   __shared__ long long st[256], ss[256];
   const int tid = threadIdx.x;
   long long tr = 0, sg = 0;
@@ -259,16 +224,21 @@ __global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, 
   }
 }
 
-// In place: counts (int32) -> G~ (fp32) on the lower triangle (the factorisation reads nothing else).
-__global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restrict__ usum, int64_t M, int64_t ld,
-                                               bool has_random, double alpha, double wr,
-                                               const double* __restrict__ scal) {
+__global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, const int64_t* __restrict__ usum,
+                                                 int64_t M, int64_t ld, bool has_random, double alpha, double wr,
+                                                 const float* __restrict__ fef, double* scal) {
+  scalars_body(C, usum, M, ld, has_random, alpha, wr, fef, scal);
+}
+
+// Row i of the lower triangle: counts (int32) -> G~ (fp32) in place.
+__device__ __forceinline__ void build_row(float* G, const int64_t* __restrict__ usum, int64_t M, int64_t ld,
+                                          bool has_random, double alpha, double wr, const double* __restrict__ scal,
+                                          int64_t i) {
   const double Md = static_cast<double>(M);
   const double inv_m = 1.0 / Md;
   const double sigma = scal[1], gamma = scal[2];
   const double base = -alpha * inv_m + gamma * inv_m + (has_random ? 2.0 * wr * sigma * inv_m * inv_m : 0.0);
   const double wr2 = 2.0 * wr;
-  const int64_t i = blockIdx.x;          // one block per row
   for (int64_t j = threadIdx.x; j <= i; j += blockDim.x) {
     double v = base + (i == j ? alpha : 0.0);
     if (has_random) {
@@ -277,6 +247,13 @@ __global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restri
     }
     G[i * ld + j] = static_cast<float>(v);
   }
+}
+
+// In place: counts (int32) -> G~ (fp32) on the lower triangle (the factorisation reads nothing else).
+__global__ void __launch_bounds__(256) k_build(float* G, const int64_t* __restrict__ usum, int64_t M, int64_t ld,
+                                               bool has_random, double alpha, double wr,
+                                               const double* __restrict__ scal) {
+  build_row(G, usum, M, ld, has_random, alpha, wr, scal, blockIdx.x);   // one block per row
 }
 
 // dz_b = z_b - z_{b+half}, z_b = w_b (y_b - f0 - Delta/M |S_b|) for b < half; a
@@ -377,279 +354,6 @@ __global__ void __launch_bounds__(256) k_rhs_center(const double* __restrict__ d
   if (j < M) rhs[j] = static_cast<float>(dv[j] - mean);
 }
 
-// One-workgroup path: the lower triangle of G~ packed in LDS (row i at
-// i(i+1)/2).
-__device__ __forceinline__ int64_t tri(int64_t i, int64_t j) { return ((i * (i + 1)) >> 1) + j; }
-
-size_t small_lds_bytes(int64_t M) {
-  return static_cast<size_t>(M) * (sizeof(double) + 2 * sizeof(float)) +
-         static_cast<size_t>((M * (M + 1)) / 2) * sizeof(float);
-}
-
-__device__ __forceinline__ void solve_small_body(const int32_t* __restrict__ C, int64_t ldc, int64_t M,
-                                                 bool has_random, double alpha, double wr,
-                                                 const float* __restrict__ fef, const double* __restrict__ part,
-                                                 int64_t nch, int32_t* info, float* __restrict__ phi) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  double* dv = reinterpret_cast<double*>(smem);      // M: row sums, then the raw right-hand side
-  float* rhs = reinterpret_cast<float*>(dv + M);     // M
-  float* xv = rhs + M;                               // M
-  float* A = xv + M;                                 // packed lower triangle
-  __shared__ float Blk[kSB][kSB + 1];                // staging of the current diagonal block
-  __shared__ float Ld[kSB][kSB + 1];                 // padded diagonal factor of the current block
-  __shared__ float rd[kSB];                          // its reciprocal pivots
-  __shared__ double red[2][4];
-  __shared__ double sc[4];
-  const int tid = threadIdx.x;
-  const int nt = blockDim.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const double Md = static_cast<double>(M);
-  if (tid == 0) *info = 0;
-
-  // 1. counts -> LDS (lower part; exact as floats below 2^24), row sums, trace
-  double trl = 0.0, sgl = 0.0;
-  if (has_random) {
-    for (int64_t i = wave; i < M; i += nt / 64) {
-      long long sum = 0;
-      for (int64_t j0 = 0; j0 < M; j0 += 512) {
-        int32_t v[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int64_t j = j0 + q * 64 + lane;
-          v[q] = C[i * ldc + (j < M ? j : 0)];
-          v[q] = j < M ? v[q] : 0;
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int64_t j = j0 + q * 64 + lane;
-          sum += v[q];
-          if (j <= i) A[tri(i, j)] = static_cast<float>(v[q]);
-          trl += j == i ? static_cast<double>(v[q]) : 0.0;
-        }
-      }
-      for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
-      if (lane == 0) dv[i] = static_cast<double>(sum);
-      sgl += lane == 0 ? static_cast<double>(sum) : 0.0;
-    }
-  }
-  for (int off = 32; off > 0; off >>= 1) {
-    trl += __shfl_xor(trl, off);
-    sgl += __shfl_xor(sgl, off);
-  }
-  if (lane == 0) {
-    red[0][wave] = trl;
-    red[1][wave] = sgl;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    double tr = 0.0, sg = 0.0;
-    for (int w = 0; w < nt / 64; ++w) {
-      tr += red[0][w];
-      sg += red[1][w];
-    }
-    const double tr_pgp = alpha * (Md - 1.0) + 2.0 * wr * (tr - sg / Md);
-    sc[0] = sg;
-    sc[1] = tr_pgp / (Md - 1.0);
-    sc[2] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
-  }
-  __syncthreads();
-  const double sigma = sc[0], gamma = sc[1], delta = sc[2];
-
-  // 2. G~ = alpha P + 2 wr P C P + gamma 11^T/M, lower triangle in place
-  for (int64_t i = 0, base = 0; i < M; base += i + 1, ++i) {
-    for (int64_t j = tid; j <= i; j += nt) {
-      double v = alpha * ((i == j ? 1.0 : 0.0) - 1.0 / Md) + gamma / Md;
-      if (has_random) v += 2.0 * wr * (static_cast<double>(A[base + j]) - (dv[i] + dv[j]) / Md + sigma / (Md * Md));
-      A[base + j] = static_cast<float>(v);
-    }
-  }
-  __syncthreads();
-
-  // 3. right-hand side P r from the partial sums (8 loads in flight per thread)
-  double sl = 0.0;
-  for (int64_t j = tid; j < M; j += nt) {
-    double v = 0.0;
-    for (int64_t c0 = 0; c0 < nch; c0 += 8) {
-      double t[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) t[q] = part[(c0 + q < nch ? c0 + q : 0) * M + j];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v += c0 + q < nch ? t[q] : 0.0;
-    }
-    dv[j] = v;
-    sl += v;
-  }
-  for (int off = 32; off > 0; off >>= 1) sl += __shfl_xor(sl, off);
-  if (lane == 0) red[0][wave] = sl;
-  __syncthreads();
-  if (tid == 0) {
-    double t = 0.0;
-    for (int w = 0; w < nt / 64; ++w) t += red[0][w];
-    sc[3] = t / Md;
-  }
-  __syncthreads();
-  for (int64_t j = tid; j < M; j += nt) rhs[j] = static_cast<float>(dv[j] - sc[3]);
-  __syncthreads();
-
-  // 4. Cholesky, 32-wide blocks
-  for (int64_t o = 0; o < M; o += kSB) {
-    const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
-    for (int t = tid; t < kSB * kSB; t += nt) {      // padded block: identity past nbe
-      const int r = t / kSB, c = t % kSB;
-      Blk[r][c] = (r < nbe && c <= r) ? A[tri(o + r, o + c)] : (r == c ? 1.f : 0.f);
-    }
-    __syncthreads();
-    if (wave == 0) {
-      float a[kSB];
-#pragma unroll
-      for (int c = 0; c < kSB; ++c) a[c] = Blk[lane & (kSB - 1)][c];
-      chol_regs<kSB>(a, o, info);
-      if (lane < kSB) {
-#pragma unroll
-        for (int c = 0; c < kSB; ++c) Blk[lane][c] = a[c];
-      }
-    }
-    __syncthreads();
-    for (int t = tid; t < kSB * kSB; t += nt) {
-      const int r = t / kSB, c = t % kSB;
-      const float v = c <= r ? Blk[r][c] : 0.f;
-      Ld[r][c] = v;
-      if (c == r) rd[r] = 1.0f / v;
-      if (r < nbe && c <= r) A[tri(o + r, o + c)] = v;
-    }
-    __syncthreads();
-    // rows below exist only when the diagonal block is full (nbe == kSB)
-    const int64_t r0 = o + nbe;
-    const int64_t T = M - r0;
-    for (int64_t i = r0 + tid; i < M; i += nt) {
-      float x[kSB];
-      const int64_t bi = tri(i, o);
-#pragma unroll
-      for (int c = 0; c < kSB; ++c) x[c] = A[bi + c];
-#pragma unroll
-      for (int c = 0; c < kSB; ++c) {
-        x[c] *= rd[c];
-#pragma unroll
-        for (int q = c + 1; q < kSB; ++q) x[q] -= x[c] * Ld[q][c];
-        __builtin_amdgcn_sched_barrier(0);   // column by column: keeps register pressure low
-      }
-#pragma unroll
-      for (int c = 0; c < kSB; ++c)
-        A[bi + c] = x[c];
-    }
-    __syncthreads();
-    const int64_t T4 = (T + 3) / 4;
-    for (int64_t t = tid; t < T4 * T4; t += nt) {
-      const int64_t I = t / T4, J = t % T4;
-      if (J > I) continue;
-      float acc[4][4] = {};
-      int64_t pi[4], pj[4];
-      bool oi[4], oj[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t ri = r0 + 4 * I + q, rj = r0 + 4 * J + q;
-        oi[q] = ri < M;
-        oj[q] = rj < M;
-        pi[q] = oi[q] ? tri(ri, o) : 0;
-        pj[q] = oj[q] ? tri(rj, o) : 0;
-      }
-      for (int c = 0; c < nbe; ++c) {
-        float pa[4], pb[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          pa[q] = oi[q] ? A[pi[q] + c] : 0.f;
-          pb[q] = oj[q] ? A[pj[q] + c] : 0.f;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[q][r] += pa[q] * pb[r];
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t i = r0 + 4 * I + q;
-        if (i >= M) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t j = r0 + 4 * J + r;
-          if (j <= i) A[tri(i, j)] -= acc[q][r];
-        }
-      }
-    }
-    __syncthreads();
-  }
-
-  // 5. forward substitution L x = rhs (one wavefront per diagonal block)
-  for (int64_t o = 0; o < M; o += kSB) {
-    const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
-    // strictly lower part of the diagonal block and its reciprocal pivots
-    for (int t = tid; t < kSB * kSB; t += nt) {
-      const int r = t / kSB, c = t % kSB;
-      Blk[r][c] = (r < nbe && c < r) ? A[tri(o + r, o + c)] : 0.f;
-      if (c == r) rd[r] = r < nbe ? 1.0f / A[tri(o + r, o + r)] : 1.f;
-    }
-    __syncthreads();
-    if (wave == 0) {
-      // b_k is final once the columns before k are applied: x_k = b_k / L_kk
-      const int rl = lane & (kSB - 1);
-      float b = lane < nbe ? rhs[o + lane] : 0.f;
-      float lr[kSB];
-#pragma unroll
-      for (int c = 0; c < kSB; ++c) lr[c] = Blk[rl][c];
-#pragma unroll
-      for (int k = 0; k < kSB; ++k) b -= lr[k] * (bcast(b, k) * rd[k]);
-      if (lane < nbe) xv[o + lane] = b * rd[rl];
-    }
-    __syncthreads();
-    for (int64_t i = o + nbe + tid; i < M; i += nt) {
-      float acc = 0.f;
-      const int64_t bi = tri(i, o);
-      for (int c = 0; c < nbe; ++c) acc += A[bi + c] * xv[o + c];
-      rhs[i] -= acc;
-    }
-    __syncthreads();
-  }
-
-  // 6. backward substitution L^T z = x (z overwrites rhs)
-  for (int64_t o = ((M - 1) / kSB) * kSB; o >= 0; o -= kSB) {
-    const int nbe = static_cast<int>(M - o < kSB ? M - o : kSB);
-    // Blk[r][k] = L[o+k][o+r] for k > r (the strictly upper part of L_jj^T)
-    for (int t = tid; t < kSB * kSB; t += nt) {
-      const int r = t / kSB, k = t % kSB;
-      Blk[r][k] = (k < nbe && r < k) ? A[tri(o + k, o + r)] : 0.f;
-      if (k == r) rd[r] = r < nbe ? 1.0f / A[tri(o + r, o + r)] : 1.f;
-    }
-    __syncthreads();
-    if (wave == 0) {
-      const int rl = lane & (kSB - 1);
-      float b = lane < nbe ? xv[o + lane] : 0.f;
-      float lc[kSB];
-#pragma unroll
-      for (int k = 0; k < kSB; ++k) lc[k] = Blk[rl][k];
-#pragma unroll
-      for (int k = kSB - 1; k >= 0; --k) b -= lc[k] * (bcast(b, k) * rd[k]);
-      if (lane < nbe) rhs[o + lane] = b * rd[rl];
-    }
-    __syncthreads();
-    for (int64_t i = tid; i < o; i += nt) {
-      float acc = 0.f;
-      for (int c = 0; c < nbe; ++c) acc += A[tri(o + c, i)] * rhs[o + c];
-      xv[i] -= acc;
-    }
-    __syncthreads();
-  }
-
-  // 7. phi = Delta/M + psi
-  for (int64_t i = tid; i < M; i += nt) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rhs[i]));
-}
-
-__global__ void __launch_bounds__(256) k_solve_small(const int32_t* __restrict__ C, int64_t ldc, int64_t M,
-                                                     bool has_random, double alpha, double wr,
-                                                     const float* __restrict__ fef, const double* __restrict__ part,
-                                                     int64_t nch, int32_t* info, float* __restrict__ phi) {
-  solve_small_body(C, ldc, M, has_random, alpha, wr, fef, part, nch, info, phi);
-}
-
 __global__ void k_zero_info(int32_t* info) { *info = 0; }
 
 // ---- multi-block path: diagonal blocks --------------------------------------------------
@@ -671,22 +375,19 @@ __device__ __forceinline__ void chol_wave(float (&a)[64], float* col, int64_t o,
   for (int k = 0; k < 64; ++k) {
     col[lane] = a[k];
     __builtin_amdgcn_wave_barrier();
-    float cv[64];
-#pragma unroll
-    for (int j4 = k & ~3; j4 < 64; j4 += 4) {
-      const f32x4 q = *reinterpret_cast<const f32x4*>(col + j4);
-      cv[j4] = q[0];
-      cv[j4 + 1] = q[1];
-      cv[j4 + 2] = q[2];
-      cv[j4 + 3] = q[3];
-    }
-    const bool ok = cv[k] > 0.f;
+    const float piv = col[k];
+    const bool ok = piv > 0.f;
     bad = (bad == 0 && !ok) ? k + 1 : bad;
-    const float rs = 1.0f / sqrtf(ok ? cv[k] : 1.f);
+    const float rs = 1.0f / sqrtf(ok ? piv : 1.f);
     a[k] *= rs;                    // L[lane][k] (lane k: sqrt of the pivot)
     const float t = a[k] * rs;     // L[lane][k] / L[k][k]: L[j][k] = col[j] rs
 #pragma unroll
-    for (int j = k + 1; j < 64; ++j) a[j] -= t * cv[j];
+    for (int j4 = (k + 1) & ~3; j4 < 64; j4 += 4) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(col + j4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j4 + e > k) a[j4 + e] -= t * q[e];
+    }
     __builtin_amdgcn_wave_barrier();
   }
   if (bad != 0 && lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + bad));
@@ -702,50 +403,176 @@ __device__ __forceinline__ void inv_wave(const float* Lt, float (&w)[64]) {
 #pragma unroll
   for (int p = 0; p < 64; ++p) {
     const float* row = Lt + p * kHP;
-    float rv[64];
-#pragma unroll
-    for (int j4 = p & ~3; j4 < 64; j4 += 4) {
-      const f32x4 q = *reinterpret_cast<const f32x4*>(row + j4);
-      rv[j4] = q[0];
-      rv[j4 + 1] = q[1];
-      rv[j4 + 2] = q[2];
-      rv[j4 + 3] = q[3];
-    }
-    w[p] *= 1.0f / rv[p];
+    w[p] *= 1.0f / row[p];
     const float u = w[p];
 #pragma unroll
-    for (int i = p + 1; i < 64; ++i) w[i] -= rv[i] * u;
+    for (int j4 = (p + 1) & ~3; j4 < 64; j4 += 4) {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(row + j4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j4 + e > p) w[j4 + e] -= q[e] * u;
+    }
+  }
+}
+
+// ---- one wavefront: Cholesky factor and its inverse of a 64x64 block -------------------
+//
+// Recursive 2x2 blocking on LDS blocks (pitch kHP), all in one wavefront:
+//   L11 = chol(A11), W11 = L11^-1     (recursively)
+//   L21 = A21 W11^T, A22 -= L21 L21^T, L22 = chol(A22), W22 = L22^-1,
+//   W21 = -W22 (L21 W11),
+// down to 8x8 blocks, which every lane factors and inverts in its own
+// registers (no communication); the products are fp32 MFMA (32x32) or VALU.
+// S <- L (zeros above the diagonal), Wb <- L^-1 (zeros above the diagonal).
+// The first non-positive pivot (1-based, offset o) goes to *info and is
+// replaced by 1.
+
+__device__ __forceinline__ void chol_inv8(float* S, float* Wb, int64_t o, int32_t* info) {
+  const int lane = threadIdx.x & 63;
+  float a[8][8], rd[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
+    for (int c = 0; c <= r; ++c) a[r][c] = S[r * kHP + c];
+  int bad = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float piv = a[k][k];
+#pragma unroll
+    for (int q = 0; q < k; ++q) piv -= a[k][q] * a[k][q];
+    const bool ok = piv > 0.f;
+    bad = (bad == 0 && !ok) ? k + 1 : bad;
+    const float d = sqrtf(ok ? piv : 1.f);
+    rd[k] = 1.0f / d;
+    a[k][k] = d;
+#pragma unroll
+    for (int i = k + 1; i < 8; ++i) {
+      float t = a[i][k];
+#pragma unroll
+      for (int q = 0; q < k; ++q) t -= a[i][q] * a[k][q];
+      a[i][k] = t * rd[k];
+    }
+  }
+  float w[8][8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    w[j][j] = rd[j];
+#pragma unroll
+    for (int i = j + 1; i < 8; ++i) {
+      float t = 0.f;
+#pragma unroll
+      for (int q = j; q < i; ++q) t -= a[i][q] * w[q][j];
+      w[i][j] = t * rd[i];
+    }
+  }
+  // lane l writes element (l / 8, l % 8) of L and of W
+  const int r = lane >> 3, c = lane & 7;
+  float lv = 0.f, wv = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j <= i; ++j) {
+      lv = (r == i && c == j) ? a[i][j] : lv;
+      wv = (r == i && c == j) ? w[i][j] : wv;
+    }
+  __builtin_amdgcn_wave_barrier();
+  S[r * kHP + c] = lv;
+  Wb[r * kHP + c] = wv;
+  __builtin_amdgcn_wave_barrier();
+  if (bad != 0 && lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + bad));
+}
+
+// One wavefront, H x H blocks (H = 8 or 16): D = alpha op(X, Y) + beta D,
+// op = X Y^T (kNT) or X Y.  Every product is read before D is written, so D
+// may alias X or Y.
+template <int H, bool kNT>
+__device__ __forceinline__ void prod_small(float* D, const float* X, const float* Y, float alpha, float beta) {
+  constexpr int Q = H * H / 64;
+  const int lane = threadIdx.x & 63;
+  float out[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int oi = lane + 64 * q, i = oi / H, j = oi % H;
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < H; ++k) sum += X[i * kHP + k] * (kNT ? Y[j * kHP + k] : Y[k * kHP + j]);
+    out[q] = sum;
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int oi = lane + 64 * q, i = oi / H, j = oi % H;
+    float* d = D + i * kHP + j;
+    *d = beta == 0.f ? alpha * out[q] : beta * *d + alpha * out[q];
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
+// One wavefront, 32 x 32 blocks: the same product as 16 fp32 MFMA 32x32x2
+// (lane half h feeds k in [16h, 16h + 16)).
+template <bool kNT>
+__device__ __forceinline__ void prod32(float* D, const float* X, const float* Y, float alpha, float beta) {
+  const int lane = threadIdx.x & 63, h = lane >> 5, rl = lane & 31;
+  f32x16 acc = {};
+  const float* xr = X + rl * kHP + 16 * h;
+#pragma unroll
+  for (int s4 = 0; s4 < 16; s4 += 4) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(xr + s4);
+    f32x4 b;
+    if (kNT) {
+      b = *reinterpret_cast<const f32x4*>(Y + rl * kHP + 16 * h + s4);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) b[e] = Y[(16 * h + s4 + e) * kHP + rl];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc, 0, 0, 0);
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float* d = D + (8 * (r >> 2) + 4 * h + (r & 3)) * kHP + rl;
+    *d = beta == 0.f ? alpha * acc[r] : beta * *d + alpha * acc[r];
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
+template <int H, bool kNT>
+__device__ __forceinline__ void prod_h(float* D, const float* X, const float* Y, float alpha, float beta) {
+  if constexpr (H == 32) prod32<kNT>(D, X, Y, alpha, beta);
+  else prod_small<H, kNT>(D, X, Y, alpha, beta);
+}
+
+template <int N>
+__device__ __forceinline__ void chol_inv_rec(float* S, float* Wb, int64_t o, int32_t* info) {
+  if constexpr (N == 8) {
+    chol_inv8(S, Wb, o, info);
+  } else {
+    constexpr int H = N / 2;
+    const int lane = threadIdx.x & 63;
+    float* S21 = S + H * kHP;
+    float* S22 = S21 + H;
+    float* W21 = Wb + H * kHP;
+    float* W22 = W21 + H;
+    chol_inv_rec<H>(S, Wb, o, info);
+    prod_h<H, true>(S21, S21, Wb, 1.f, 0.f);       // L21 = A21 W11^T
+    prod_h<H, true>(S22, S21, S21, -1.f, 1.f);     // A22 - L21 L21^T
+    chol_inv_rec<H>(S22, W22, o + H, info);
+    prod_h<H, false>(W21, S21, Wb, 1.f, 0.f);      // L21 W11
+    prod_h<H, false>(W21, W22, W21, -1.f, 0.f);    // W21 = -W22 (L21 W11)
+    for (int t = lane; t < H * H; t += 64) {       // the upper right blocks
+      S[(t / H) * kHP + H + t % H] = 0.f;
+      Wb[(t / H) * kHP + H + t % H] = 0.f;
+    }
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
 // One wavefront: S (64x64, pitch kHP) <- L = chol(S) (zeros above the
-// diagonal) and Wb <- L^-1, using Wb for L^T on the way.
+// diagonal) and Wb <- L^-1.  `col` is unused (kept for the callers' layout).
 __device__ __forceinline__ void chol_inv64(float* S, float* Wb, float* col, int64_t o, int32_t* info) {
-  const int lane = threadIdx.x & 63;
-  {
-    float a[64];
-#pragma unroll
-    for (int c4 = 0; c4 < 64; c4 += 4) {
-      const f32x4 q = *reinterpret_cast<const f32x4*>(S + lane * kHP + c4);
-      a[c4] = q[0];
-      a[c4 + 1] = q[1];
-      a[c4 + 2] = q[2];
-      a[c4 + 3] = q[3];
-    }
-    chol_wave(a, col, o, info);
-#pragma unroll
-    for (int c = 0; c < 64; ++c) {
-      const float v = c <= lane ? a[c] : 0.f;
-      S[lane * kHP + c] = v;
-      Wb[c * kHP + lane] = v;
-    }
-  }
-  __builtin_amdgcn_wave_barrier();
-  float w[64];
-  inv_wave(Wb, w);
-  __builtin_amdgcn_wave_barrier();
-#pragma unroll
-  for (int i = 0; i < 64; ++i) Wb[i * kHP + lane] = w[i];
+  (void)col;
+  chol_inv_rec<64>(S, Wb, o, info);
 }
 
 // D = alpha op(X, Y) + beta D on 64x64 LDS blocks, op = X Y^T (kNT) or X Y;
@@ -845,182 +672,218 @@ __global__ void __launch_bounds__(256) k_potrf(float* G, int64_t ld, int64_t M, 
   }
 }
 
-// ---- one-workgroup path for mid-size systems ---------------------------------------------
+// ---- one-workgroup path (systems of up to kMidMax players) --------------------------------
 //
-// M <= kMidMax: the system stays in global memory (L2-resident at these
-// sizes) and one workgroup factors it in 64-wide panels: the wavefront
-// Cholesky-and-inverse of the diagonal block, the panel as an MFMA product
-// with that inverse (kept in LDS), the trailing update as 32x32 MFMA tiles
-// spread over the four wavefronts.  The forward substitution rides along
-// (z_p = W_p r_p, then r_I -= L_Ip z_p from the panel in LDS); the backward
-// one reads L and the stored inverses once more.  The counts are turned into
-// G~ entries when the first panel touches them.
+// G~ is assembled in global memory by multi-block kernels (L2-resident at
+// these sizes) and one workgroup of four wavefronts factors it in 64-wide
+// panels.  Per panel:
+// the panel blocks are loaded at once; L_Ip = A_Ip W_pp^T as MFMA products
+// (W_pp = L_pp^-1, one task per 32-row half); the forward substitution rides
+// along (z_p = W_pp r_p, r_I -= L_Ip z_p); the trailing tiles of the next
+// panel's block column are updated first, then wavefront 0 factors and
+// inverts the next diagonal block (wavefront Cholesky with LDS column
+// broadcasts) while the other three update the rest of the trailing matrix
+// in 32x32 MFMA tiles.  The backward substitution reads L and the stored
+// inverses once more.
 
+constexpr int kMidThreads = 256;
 constexpr int kMidBlk = kMidMax / 64;
-constexpr size_t kMidLds = (static_cast<size_t>(1 + kMidBlk) * kHB + 64 + kMidMax + 4 * 64) * sizeof(float) +
-                           static_cast<size_t>(kMidMax) * sizeof(double);
+constexpr size_t kMidLds = (static_cast<size_t>(1 + kMidBlk) * kHB + 64 + kMidMax + 4 * 64) * sizeof(float);
 
-// G: the counts (int32, row stride ld, both halves) on entry, the factor on
-// exit; usum: their row sums; dvg: the summed right-hand side before
-// centring; Wd: room for the ceil(M/64) inverse diagonal factors.
-__device__ __forceinline__ void solve_mid_body(float* G, int64_t ld, int64_t M, bool has_random, double alpha,
-                                               double wr, const int64_t* __restrict__ usum,
-                                               const double* __restrict__ dvg, const float* __restrict__ fef,
-                                               float* __restrict__ Wd, int32_t* info, float* __restrict__ phi) {
+// G: G~ on its lower triangle (row stride ld) on entry, the factor on exit;
+// dvg: the summed right-hand side before centring; Wd: room for the
+// ceil(M/64) inverse diagonal factors.
+__device__ __forceinline__ void solve_mid_body(float* G, int64_t ld, int64_t M, const double* __restrict__ dvg,
+                                               const float* __restrict__ fef, float* __restrict__ Wd, int32_t* info,
+                                               float* __restrict__ phi) {
+  constexpr int NT = kMidThreads, NW = NT / 64;
   extern __shared__ __align__(16) unsigned char smem[];
-  float* D0 = reinterpret_cast<float*>(smem);  // diagonal block -> L_pp
+  float* D0 = reinterpret_cast<float*>(smem);  // diagonal block -> L_pp (and the look-ahead's)
   float* D1 = D0 + kHB;                        // W_pp = L_pp^-1
   float* P = D1 + kHB;                         // blocks below the diagonal block -> L_Ip
   float* col = P + (kMidBlk - 1) * kHB;        // 64: column broadcasts of the wavefront Cholesky
   float* rv = col + 64;                        // kMidMax: r, then z, then psi
-  float* red4 = rv + kMidMax;                  // 4 x 64
-  double* ud = reinterpret_cast<double*>(red4 + 4 * 64);  // kMidMax: usum / M
-  __shared__ double red[3][4];
-  __shared__ double sc[4];                     // gamma, mean of dv, Delta, -
+  float* red8 = rv + kMidMax;                  // NW x 64
+  __shared__ double red[NW];
+  __shared__ double sc[2];                     // mean of dv, Delta
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, rl = lane & 31;
-  const double Md = static_cast<double>(M), inv_m = 1.0 / Md;
-  const int32_t* C = reinterpret_cast<const int32_t*>(G);
+  const double Md = static_cast<double>(M);
   const int64_t nblk = (M + 63) / 64;
   if (tid == 0) *info = 0;
 
-  // 1. trace and sigma of the counts, mean of the right-hand side
-  double tr = 0.0, sg = 0.0, sv = 0.0;
-  for (int64_t i = tid; i < M; i += 256) {
-    if (has_random) {
-      tr += static_cast<double>(C[i * ld + i]);
-      sg += static_cast<double>(usum[i]);
-      ud[i] = static_cast<double>(usum[i]) * inv_m;
-    }
-    sv += dvg[i];
-  }
-  for (int off = 32; off > 0; off >>= 1) {
-    tr += __shfl_xor(tr, off);
-    sg += __shfl_xor(sg, off);
-    sv += __shfl_xor(sv, off);
-  }
-  if (lane == 0) {
-    red[0][wave] = tr;
-    red[1][wave] = sg;
-    red[2][wave] = sv;
-  }
+  // 1. the centred right-hand side r = P dv
+  double sv = 0.0;
+  for (int64_t i = tid; i < M; i += NT) sv += dvg[i];
+  for (int off = 32; off > 0; off >>= 1) sv += __shfl_xor(sv, off);
+  if (lane == 0) red[wave] = sv;
   __syncthreads();
   if (tid == 0) {
-    const double trace = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
-    const double sigma = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
-    const double tr_pgp = alpha * (Md - 1.0) + 2.0 * wr * (trace - sigma / Md);
-    sc[0] = tr_pgp / (Md - 1.0);
-    sc[1] = ((red[2][0] + red[2][1]) + (red[2][2] + red[2][3])) / Md;
-    sc[2] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
-    sc[3] = sigma;
+    double t = 0.0;
+    for (int w = 0; w < NW; ++w) t += red[w];
+    sc[0] = t / Md;
+    sc[1] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
   }
   __syncthreads();
-  const double gamma = sc[0], sigma = sc[3];
-  for (int64_t i = tid; i < nblk * 64; i += 256) rv[i] = i < M ? static_cast<float>(dvg[i] - sc[1]) : 0.f;
-  const double base = -alpha * inv_m + gamma * inv_m + (has_random ? 2.0 * wr * sigma * inv_m * inv_m : 0.0);
-  const double wr2 = 2.0 * wr;
-  // G~_ij from the count c_ij (first touch only)
-  auto gt = [&](int64_t i, int64_t j, int32_t cij) -> float {
-    double v = base + (i == j ? alpha : 0.0);
-    if (has_random) v += wr2 * (static_cast<double>(cij) - ud[i] - ud[j]);
-    return static_cast<float>(v);
-  };
-  // 64x64 block at (r0, c0) into LDS (pitch kHP): zeros outside the lower
-  // part of G (identity on the diagonal past M when `diag`)
-  auto load_block = [&](float* dst, int64_t r0, int64_t c0, bool diag, bool first) {
-    float v[16];
+  for (int64_t i = tid; i < nblk * 64; i += NT) rv[i] = i < M ? static_cast<float>(dvg[i] - sc[0]) : 0.f;
+  const int ldi = static_cast<int>(ld);       // M <= kMidMax: 32-bit offsets within G
+  // one wavefront: the 64x64 diagonal block at (o, o) into D0 (lower part,
+  // identity past M), then D0 <- L, D1 <- L^-1
+  auto diag_factor = [&](int64_t o) {
+    const float* base = G + o * ld + o;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int t = tid + q * 256;
-      const int64_t gi = r0 + (t >> 6), gj = c0 + (t & 63);
-      const bool ok = gi < M && gj < M && (!diag || gj <= gi);
-      v[q] = ok ? G[gi * ld + gj] : 0.f;
+    for (int h2 = 0; h2 < 64; h2 += 32) {
+      float v[32];
+#pragma unroll
+      for (int q = 0; q < 32; ++q) {
+        const int r = h2 + q;
+        const bool ok = o + r < M && lane <= r;
+        v[q] = ok ? base[r * ldi + lane] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 32; ++q) {
+        const int r = h2 + q;
+        float x = v[q];
+        if (o + r >= M && r == lane) x = 1.f;
+        D0[r * kHP + lane] = x;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    chol_inv64(D0, D1, col, o, info);
+  };
+  // one task: trailing quadrant (qr, qc) of tile (I, J) below panel o: A -= L_Io L_Jo^T
+  auto trailing = [&](int64_t o, int I, int J, int q) {
+    const int qr = q >> 1, qc = q & 1;
+    if (I == J && qr < qc) return;
+    const int64_t gi0 = o + 64 * (I + 1) + 32 * qr, gj = o + 64 * (J + 1) + 32 * qc + rl;
+    float* tile = G + gi0 * ld + (gj - rl);
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rr = 8 * (r >> 2) + 4 * h + (r & 3);
+      const bool ok = gi0 + rr < M && gj < M;
+      acc[r] = ok ? tile[rr * ldi + rl] : 0.f;
+    }
+    const float* xa = P + I * kHB + (32 * qr + rl) * kHP + h * 32;
+    const float* xb = P + J * kHB + (32 * qc + rl) * kHP + h * 32;
+#pragma unroll
+    for (int s4 = 0; s4 < 32; s4 += 4) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(xa + s4);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(xb + s4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(-a[e], b[e], acc, 0, 0, 0);
     }
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int t = tid + q * 256;
-      const int r = t >> 6, c = t & 63;
-      const int64_t gi = r0 + r, gj = c0 + c;
-      float x = v[q];
-      if (first && gi < M && gj < M && (!diag || gj <= gi)) x = gt(gi, gj, __float_as_int(x));
-      if (diag && r == c && gi >= M) x = 1.f;
-      dst[r * kHP + c] = x;
+    for (int r = 0; r < 16; ++r) {
+      const int rr = 8 * (r >> 2) + 4 * h + (r & 3);
+      if (gi0 + rr < M && gj < M) tile[rr * ldi + rl] = acc[r];
     }
   };
   __syncthreads();
 
-  // 2. factorisation with the forward substitution
-  for (int64_t p = 0; p < nblk; ++p) {
+  // 2. factorisation with the forward substitution; "panel -1" only factors
+  // the first diagonal block
+  for (int64_t p = -1; p < nblk; ++p) {
     const int64_t o = p * 64;
     const int nI = static_cast<int>(nblk - p - 1);
-    const bool first = p == 0;
-    load_block(D0, o, o, true, first);
-    for (int I = 0; I < nI; ++I) load_block(P + I * kHB, o + 64 * (I + 1), o, false, first);
-    __syncthreads();
+    if (p >= 0) {
+    // (a) the blocks below the diagonal block, three blocks' loads in flight at a time
+    {
+      constexpr int QB = 4096 / NT;
+      const float* base = G + (o + 64) * ld + o;
+      for (int I0 = 0; I0 < nI; I0 += 3) {
+        float v[3][QB];
+#pragma unroll
+        for (int ii = 0; ii < 3; ++ii)
+#pragma unroll
+          for (int q = 0; q < QB; ++q) {
+            const int t = tid + q * NT;
+            const int r = 64 * (I0 + ii) + (t >> 6);
+            v[ii][q] = (I0 + ii < nI && o + 64 + r < M) ? base[r * ldi + (t & 63)] : 0.f;
+          }
+#pragma unroll
+        for (int ii = 0; ii < 3; ++ii) {
+          if (I0 + ii >= nI) break;
+#pragma unroll
+          for (int q = 0; q < QB; ++q) {
+            const int t = tid + q * NT;
+            P[(I0 + ii) * kHB + (t >> 6) * kHP + (t & 63)] = v[ii][q];
+          }
+        }
+      }
+    }
+    // (b) z_p = W_pp r_p; L_pp and W_pp to global
     if (wave == 0) {
-      chol_inv64(D0, D1, col, o, info);
-      // z_p = W_pp r_p
       float z = 0.f;
 #pragma unroll 8
       for (int c = 0; c < 64; ++c) z += D1[lane * kHP + c] * rv[o + c];
       __builtin_amdgcn_wave_barrier();
       rv[o + lane] = z;
     }
-    __syncthreads();
-    for (int t = tid; t < 64 * 64; t += 256) {
+    for (int t = tid; t < 64 * 64; t += NT) {
       const int r = t >> 6, c = t & 63;
       const int64_t gi = o + r, gj = o + c;
       if (gi < M && gj <= gi) G[gi * ld + gj] = D0[r * kHP + c];
       Wd[p * 4096 + t] = D1[r * kHP + c];
     }
-    for (int I = 0; I < nI; ++I) mm64<true>(P + I * kHB, D1, P + I * kHB, 1.f, 0.f);   // L_Ip = A_Ip W^T
-    // store L_Ip; r_I -= L_Ip z_p
-    for (int R = tid; R < nI * 64; R += 256) {
+    __syncthreads();
+    // (c) L_Ip = A_Ip W_pp^T, one task per 32-row half of a block
+    for (int task = wave; task < 2 * nI; task += NW) {
+      const int I = task >> 1, qr = task & 1;
+      float* blk = P + I * kHB;
+      f32x16 a0 = {}, a1 = {};
+      const float* xr = blk + (32 * qr + rl) * kHP + h * 32;
+#pragma unroll
+      for (int s4 = 0; s4 < 32; s4 += 4) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(xr + s4);
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(D1 + rl * kHP + h * 32 + s4);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(D1 + (32 + rl) * kHP + h * 32 + s4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          a0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b0[e], a0, 0, 0, 0);
+          a1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b1[e], a1, 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float* d = blk + (32 * qr + 8 * (r >> 2) + 4 * h + (r & 3)) * kHP + rl;
+        d[0] = a0[r];
+        d[32] = a1[r];
+      }
+    }
+    __syncthreads();
+    // (d) r_I -= L_Ip z_p; L_Ip to global
+    for (int R = tid; R < nI * 64; R += NT) {
       const float* pr = P + (R >> 6) * kHB + (R & 63) * kHP;
-      float s = 0.f;
+      float sum = 0.f;
 #pragma unroll 8
-      for (int c = 0; c < 64; ++c) s += pr[c] * rv[o + c];
-      rv[o + 64 + R] -= s;
+      for (int c = 0; c < 64; ++c) sum += pr[c] * rv[o + c];
+      rv[o + 64 + R] -= sum;
     }
     for (int I = 0; I < nI; ++I)
-      for (int t = tid; t < 64 * 64; t += 256) {
+      for (int t = tid; t < 64 * 64; t += NT) {
         const int r = t >> 6, c = t & 63;
         const int64_t gi = o + 64 * (I + 1) + r;
         if (gi < M) G[gi * ld + o + c] = P[I * kHB + r * kHP + c];
       }
-    // trailing tiles A_IJ -= L_Ip L_Jp^T: (pair, 32x32 quadrant) tasks over the wavefronts;
-    // the strictly upper quadrant of a diagonal tile is skipped
-    const int tasks = 4 * (nI * (nI + 1) / 2);
-    for (int task = wave; task < tasks; task += 4) {
-      const int pair = task >> 2, q = task & 3;
-      int I = 0;
-      while ((I + 1) * (I + 2) / 2 <= pair) ++I;
-      const int J = pair - I * (I + 1) / 2;
-      const int qr = q >> 1, qc = q & 1;
-      if (I == J && qr < qc) continue;
-      const int64_t gi0 = o + 64 * (I + 1) + 32 * qr, gj = o + 64 * (J + 1) + 32 * qc + rl;
-      f32x16 acc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t gi = gi0 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const bool ok = gi < M && gj < M;
-        float x = ok ? G[gi * ld + gj] : 0.f;
-        if (first && ok) x = gt(gi, gj, __float_as_int(x));
-        acc[r] = x;
-      }
-      const float* xa = P + I * kHB + (32 * qr + rl) * kHP + h * 32;
-      const float* xb = P + J * kHB + (32 * qc + rl) * kHP + h * 32;
-#pragma unroll
-      for (int s4 = 0; s4 < 32; s4 += 4) {
-        const f32x4 a = *reinterpret_cast<const f32x4*>(xa + s4);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(xb + s4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(-a[e], b[e], acc, 0, 0, 0);
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t gi = gi0 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (gi < M && gj < M) G[gi * ld + gj] = acc[r];
+    // (e) the next panel's block column first
+    for (int task = wave; task < 4 * nI; task += NW) trailing(o, task >> 2, 0, task & 3);
+    __syncthreads();
+    }
+    // (f) wavefront 0 factors the next diagonal block; the others update the rest
+    if (nI > 0) {
+      if (wave == 0) {
+        diag_factor(o + 64);
+      } else if (p >= 0) {
+        const int tasks = 4 * (nI * (nI - 1) / 2);
+        for (int task = wave - 1; task < tasks; task += NW - 1) {
+          const int pair = task >> 2;
+          int I1 = 0;
+          while ((I1 + 1) * (I1 + 2) / 2 <= pair) ++I1;
+          const int J1 = pair - I1 * (I1 + 1) / 2;
+          trailing(o, I1 + 1, J1 + 1, task & 3);
+        }
       }
     }
     __syncthreads();
@@ -1034,30 +897,33 @@ __device__ __forceinline__ void solve_mid_body(float* G, int64_t ld, int64_t M, 
     float acc = 0.f;
     if (real) {
 #pragma unroll 8
-      for (int64_t row = o + 64 + g; row < M; row += 4) acc += G[row * ld + o + c] * rv[row];
+      for (int64_t row = o + 64 + g; row < M; row += NW) acc += G[row * ld + o + c] * rv[row];
     }
-    red4[g * 64 + c] = acc;
+    red8[g * 64 + c] = acc;
     __syncthreads();
-    if (tid < 64)
-      red4[tid] = o + tid < M ? rv[o + tid] - ((red4[tid] + red4[64 + tid]) + (red4[128 + tid] + red4[192 + tid])) : 0.f;
+    if (tid < 64) {
+      float sum = 0.f;
+      for (int gg = 0; gg < NW; ++gg) sum += red8[gg * 64 + tid];
+      red8[tid] = o + tid < M ? rv[o + tid] - sum : 0.f;
+    }
     __syncthreads();
     if (tid < 64) {
       float ps = 0.f;
 #pragma unroll 8
-      for (int cc = tid; cc < 64; ++cc) ps += Wd[p * 4096 + cc * 64 + tid] * red4[cc];
+      for (int cc = tid; cc < 64; ++cc) ps += Wd[p * 4096 + cc * 64 + tid] * red8[cc];
       rv[o + tid] = ps;
     }
     __syncthreads();
   }
-  const double delta = sc[2];
-  for (int64_t i = tid; i < M; i += 256) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rv[i]));
+  const double delta = sc[1];
+  for (int64_t i = tid; i < M; i += NT) phi[i] = static_cast<float>(delta / Md + static_cast<double>(rv[i]));
 }
 
-__global__ void __launch_bounds__(256) k_solve_mid(float* G, int64_t ld, int64_t M, bool has_random, double alpha,
-                                                   double wr, const int64_t* __restrict__ usum,
-                                                   const double* __restrict__ dvg, const float* __restrict__ fef,
-                                                   float* __restrict__ Wd, int32_t* info, float* __restrict__ phi) {
-  solve_mid_body(G, ld, M, has_random, alpha, wr, usum, dvg, fef, Wd, info, phi);
+__global__ void __launch_bounds__(kMidThreads) k_solve_mid(float* G, int64_t ld, int64_t M,
+                                                           const double* __restrict__ dvg,
+                                                           const float* __restrict__ fef, float* __restrict__ Wd,
+                                                           int32_t* info, float* __restrict__ phi) {
+  solve_mid_body(G, ld, M, dvg, fef, Wd, info, phi);
 }
 
 // ---- multi-block path: MFMA GEMM ---------------------------------------------------------
@@ -1149,6 +1015,8 @@ __global__ void __launch_bounds__(256) k_gemm_nt(const float* A, int64_t lda, co
 // lower triangle into LDS (packed, row i at i(i+1)/2) and substitutes through
 // it in 64-row blocks (one wavefront per diagonal block); multi-block GEMVs
 // then carry the segment's unknowns to the rows outside it.
+
+__device__ __forceinline__ int64_t tri(int64_t i, int64_t j) { return ((i * (i + 1)) >> 1) + j; }
 
 constexpr size_t kTrsvLds = (kSeg * (kSeg + 1) / 2 + 2 * kSeg) * sizeof(float);
 
@@ -1357,7 +1225,7 @@ __global__ void __launch_bounds__(256) k_rhs_part_batch(const gnnshap::SolveJob*
 // Row sums of the counts and the summed right-hand side, for the mid-size jobs.
 __global__ void __launch_bounds__(256) k_rowsum_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
-  if (!J.mid || J.kr <= 0) return;
+  if (J.kr <= 0) return;
   const int lane = threadIdx.x & 63;
   const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
   if (i >= J.M) return;
@@ -1370,21 +1238,27 @@ __global__ void __launch_bounds__(256) k_rowsum_batch(const gnnshap::SolveJob* _
 __global__ void __launch_bounds__(256) k_rhs_sum_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
   const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (!J.mid || j >= J.M) return;
+  if (j >= J.M) return;
   double v = 0.0;
   for (int64_t c = 0; c < J.nch; ++c) v += J.part[c * J.M + j];
   J.dv[j] = v;
 }
 
-// One workgroup per job: the LDS-resident path for small systems, the
-// global-memory path for mid-size ones.
-__global__ void __launch_bounds__(256) k_solve_one_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+__global__ void __launch_bounds__(256) k_scalars_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.x];
-  if (J.mid)
-    solve_mid_body(reinterpret_cast<float*>(J.counts), J.ld, J.M, J.kr > 0, J.alpha, J.wr, J.usum, J.dv, J.fef, J.Wd,
-                   J.info, J.phi);
-  else
-    solve_small_body(J.counts, J.ld, J.M, J.kr > 0, J.alpha, J.wr, J.fef, J.part, J.nch, J.info, J.phi);
+  scalars_body(J.counts, J.usum, J.M, J.ld, J.kr > 0, J.alpha, J.wr, J.fef, J.scal);
+}
+
+__global__ void __launch_bounds__(256) k_build_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.y];
+  if (blockIdx.x >= J.M) return;
+  build_row(reinterpret_cast<float*>(J.counts), J.usum, J.M, J.ld, J.kr > 0, J.alpha, J.wr, J.scal, blockIdx.x);
+}
+
+// One workgroup per job.
+__global__ void __launch_bounds__(kMidThreads) k_solve_one_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.x];
+  solve_mid_body(reinterpret_cast<float*>(J.counts), J.ld, J.M, J.dv, J.fef, J.Wd, J.info, J.phi);
 }
 
 // Whether `kernel` may be launched with `bytes` of dynamic LDS on the current
@@ -1408,11 +1282,6 @@ bool allow_lds(const void* kernel, size_t bytes, bool& raised) {
   return raised;
 }
 
-// The LDS-resident one-workgroup path: its packed triangle plus a margin for
-// the static LDS of the kernels that run it.
-bool small_fits(int64_t M) {
-  return small_lds_bytes(M) + 16384 <= static_cast<size_t>(gnnshap::max_lds_bytes());
-}
 
 }  // namespace
 
@@ -1484,30 +1353,22 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   }
   GS_LAUNCHED();
 
-  const size_t small_bytes = small_lds_bytes(M);
-  static bool small_lds = false;
-  if (small_fits(M) && allow_lds(reinterpret_cast<const void*>(&k_solve_small), small_bytes, small_lds)) {
-    {
-      GS_TIMED("k_solve_small", s);
-      k_solve_small<<<1, 256, small_bytes, s>>>(counts, ld, M, has_random, alpha, wr, f_empty_full, w.part, nch, info,
-                                                phi);
-    }
-    GS_LAUNCHED();
-    return GNNSHAP_OK;
-  }
   static bool mid_lds = false;
   if (M <= kMidMax && allow_lds(reinterpret_cast<const void*>(&k_solve_mid), kMidLds, mid_lds)) {
     if (has_random) {
       k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, ld, w.usum);
       GS_LAUNCHED();
     }
+    k_scalars<<<1, 256, 0, s>>>(counts, w.usum, M, ld, has_random, alpha, wr, f_empty_full, w.scal);
+    GS_LAUNCHED();
+    k_build<<<static_cast<unsigned>(M), 256, 0, s>>>(w.G, w.usum, M, ld, has_random, alpha, wr, w.scal);
+    GS_LAUNCHED();
     const int64_t nbm = gnnshap::ceil_div(M, 256);
     k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch, M, w.dv, w.bsum);
     GS_LAUNCHED();
     {
       GS_TIMED("k_solve_mid", s);
-      k_solve_mid<<<1, 256, kMidLds, s>>>(w.G, ld, M, has_random, alpha, wr, w.usum, w.dv, f_empty_full, w.Wd, info,
-                                          phi);
+      k_solve_mid<<<1, kMidThreads, kMidLds, s>>>(w.G, ld, M, w.dv, f_empty_full, w.Wd, info, phi);
     }
     GS_LAUNCHED();
     return GNNSHAP_OK;
@@ -1596,7 +1457,7 @@ bool gnnshap::solve_batchable(const gnnshap_sample_plan* plan) {
     clear_error();
     return false;
   }
-  return plan->num_players <= kMidMax || small_fits(plan->num_players);
+  return plan->num_players <= kMidMax;
 }
 
 size_t gnnshap::solve_slice_bytes(const gnnshap_sample_plan* plan) {
@@ -1637,7 +1498,7 @@ int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class
   job->usum = w.usum;
   job->dv = w.dv;
   job->Wd = w.Wd;
-  job->mid = small_fits(M) ? 0 : 1;
+  job->scal = w.scal;
   return GNNSHAP_OK;
 }
 
@@ -1645,7 +1506,7 @@ int gnnshap::launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, 
                                 int64_t max_nrb, int64_t max_nch, hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
-  const size_t lds = std::max(kMidLds, small_fits(max_M) ? small_lds_bytes(max_M) : small_lds_bytes(1));
+  const size_t lds = kMidLds;
   static bool raised = false;
   if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
     return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
@@ -1665,6 +1526,10 @@ int gnnshap::launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, 
     k_rowsum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M * 64, 256)), nn), 256, 0, s>>>(jobs);
     GS_LAUNCHED();
   }
+  k_scalars_batch<<<nn, 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  k_build_batch<<<dim3(static_cast<unsigned>(max_M), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
   k_dz_batch<<<dim3(static_cast<unsigned>(ceil_div(max_half, 256)), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
   {
@@ -1677,7 +1542,7 @@ int gnnshap::launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, 
   GS_LAUNCHED();
   {
     GS_TIMED("k_solve_one_batch", s);
-    k_solve_one_batch<<<nn, 256, lds, s>>>(jobs);
+    k_solve_one_batch<<<nn, kMidThreads, lds, s>>>(jobs);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
@@ -1688,6 +1553,6 @@ extern "C" int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path
   if (!path) return gnnshap::fail(GNNSHAP_EINVAL, "path is NULL");
   if (int st = check_plan(plan, nullptr)) return st;
   const int64_t M = plan->num_players;
-  *path = small_fits(M) ? 1 : (M <= kMidMax ? 2 : 0);
+  *path = M <= kMidMax ? 1 : 0;
   return GNNSHAP_OK;
 }
