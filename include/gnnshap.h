@@ -151,7 +151,8 @@ typedef struct {
   double random_weight;    /* out: weight of every random row (0 if none) */
 } gnnshap_sample_plan;
 
-/* Host-only, pure.  Fills *plan's outputs and classes[0 .. num_classes).
+/* Host-only, pure, thread-safe (plans of recent (M, p) pairs are kept and
+ * reused).  Fills *plan's outputs and classes[0 .. num_classes).
  * If `classes` is NULL or cap_classes < num_classes, returns
  * GNNSHAP_ECAPACITY with the outputs of *plan filled.  EINVAL: M < 2, odd
  * or non-positive p, or more than 2^31 rows. */
@@ -256,13 +257,38 @@ int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, size_t* bytes)
 /* gnnshap_extract_subgraph for targets[0 .. n) ([host] int64) into sgs[0 .. n)
  * ([host] array; each entry has its own num_hops, capacities and [dev]
  * output arrays, as for the single call).  One workgroup per target, one
- * host synchronisation for the batch; `ws` zero-filled before first use and
- * left zero-filled.  Sizes are filled in for every target; if any target
+ * host synchronisation for the batch; `ws` zero-filled before first use,
+ * after which every call leaves it ready for the next batch call (of any
+ * n up to the size it was made for).  Sizes are filled in for every target; if any target
  * does not fit its capacities, returns GNNSHAP_ECAPACITY (the targets that
  * fit are complete).  EUNSUPPORTED: graphs of more than 2^18 nodes (use the
  * single-target call there).  EINVAL as for the single call. */
 int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
                           gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream);
+
+/* Host only: fills sgs[0 .. n) for outputs packed by target, as rows of
+ * [dev] node_gid[n][cap_nodes], dst_ptr[n][cap_nodes + 1],
+ * edge_src[n][cap_edges], edge_dst[n][cap_edges] (int32) and
+ * edge_gid[n][cap_edges] (int64); every entry gets num_hops and the two
+ * capacities, and zero sizes. */
+int gnnshap_subgraph_batch_init(gnnshap_subgraph* sgs, int64_t n, int32_t num_hops, int64_t cap_nodes,
+                                int64_t cap_edges, int32_t* node_gid, int32_t* dst_ptr, int32_t* edge_src,
+                                int32_t* edge_dst, int64_t* edge_gid);
+
+/* Host only, pure: gnnshap_plan_samples for each target of a batch.
+ * plans[t] gets num_players = sgs[t].num_edges, num_samples, seed,
+ * stream_id = stream_ids[t] ([host] int64, e.g. the target's global id)
+ * and the outputs; the n class tables go to classes[] concatenated in
+ * target order, *num_classes records in all.  totals ([host] int64[3], may
+ * be NULL) receives the sizes of gnnshap_explain_batch's packed outputs:
+ * sum_t k_t * words_per_row_t, sum_t k_t and sum_t M_t.  If `classes` is
+ * NULL or cap_classes < *num_classes, returns GNNSHAP_ECAPACITY with plans,
+ * *num_classes and totals filled.  EINVAL as for the single call, naming
+ * the target. */
+int gnnshap_plan_batch(const gnnshap_subgraph* sgs, const int64_t* stream_ids, int64_t n,
+                       int64_t num_samples, uint64_t seed, gnnshap_sample_plan* plans,
+                       gnnshap_class* classes, int64_t cap_classes, int64_t* num_classes,
+                       int64_t* totals);
 
 /* Bytes of device workspace for gnnshap_explain_batch. */
 int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
@@ -297,7 +323,7 @@ int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan
 int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path);
 
 /* Arms timing for the kernels whose name starts with `kernel_name` (e.g.
- * "k_solve_small", "k_eval_l2"): every later launch of such a kernel, from
+ * "k_solve_mid", "k_eval_l2"): every later launch of such a kernel, from
  * any entry point, is bracketed by two HIP events recorded on the launch's
  * own stream.  EINVAL if the name is empty or timing is already armed. */
 int gnnshap_timing_begin(const char* kernel_name);

@@ -67,6 +67,11 @@ _SIGNATURES = {
     "gnnshap_extract_batch_workspace": (ctypes.c_int, [c_i64, c_i64, _P(ctypes.c_size_t)]),
     "gnnshap_extract_batch": (ctypes.c_int, [_P(gnnshap_graph), _P(c_i64), c_i64, _P(gnnshap_subgraph), c_vp,
                                              ctypes.c_size_t, c_vp]),
+    "gnnshap_subgraph_batch_init": (ctypes.c_int, [_P(gnnshap_subgraph), c_i64, c_i32, c_i64, c_i64, c_vp, c_vp,
+                                                    c_vp, c_vp, c_vp]),
+    "gnnshap_plan_batch": (ctypes.c_int, [_P(gnnshap_subgraph), _P(c_i64), c_i64, c_i64, ctypes.c_uint64,
+                                          _P(gnnshap_sample_plan), _P(gnnshap_class), c_i64, _P(c_i64),
+                                          _P(c_i64)]),
     "gnnshap_explain_batch_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), c_i64,
                                                        _P(gnnshap_gcn), _P(ctypes.c_size_t)]),
     "gnnshap_explain_batch": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), _P(gnnshap_class),
@@ -203,6 +208,26 @@ def gnnshap_extract_batch(graph, targets, sgs, ws_ptr, ws_bytes, stream):
     if st not in (OK, ECAPACITY):
         check(st, "extract_batch")
     return st
+
+
+def gnnshap_subgraph_batch_init(sgs, num_hops, cap_nodes, cap_edges, node_gid, dst_ptr, edge_src, edge_dst,
+                                edge_gid):
+    check(load().gnnshap_subgraph_batch_init(sgs, len(sgs), num_hops, cap_nodes, cap_edges, node_gid, dst_ptr,
+                                             edge_src, edge_dst, edge_gid), "subgraph_batch_init")
+
+
+def gnnshap_plan_batch(sgs, stream_ids, num_samples, seed, plans, classes):
+    """Plans of a batch into `plans` and `classes` (ctypes arrays).  Returns
+    (status, num_classes, totals): OK, or ECAPACITY when `classes` is too
+    short (plans and the counts are filled either way)."""
+    ncls = c_i64()
+    tot = (c_i64 * 3)()
+    cap = len(classes) if classes is not None else 0
+    st = load().gnnshap_plan_batch(sgs, stream_ids, len(sgs), num_samples, seed, plans, classes, cap,
+                                   ctypes.byref(ncls), tot)
+    if st not in (OK, ECAPACITY):
+        check(st, "plan_batch")
+    return st, ncls.value, tuple(tot)
 
 
 def gnnshap_explain_batch_workspace(sgs, plans, model):

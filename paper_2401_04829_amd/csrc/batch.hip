@@ -113,10 +113,17 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     }
     if (row != plans[t].num_rows / 2) return gnnshap::fail(GNNSHAP_EINVAL, "class table of target %lld short", (long long)t);
   }
-  GS_HIP(hipMemcpyAsync(b.classes, classes, L.classes * sizeof(gnnshap_class), hipMemcpyHostToDevice, s));
+  // The class tables and the three job tables sit at the front of the
+  // workspace; they are assembled in a host image of that range and copied
+  // in one transfer before the first launch.
+  char* const base = static_cast<char*>(ws);
+  const size_t front = static_cast<size_t>(reinterpret_cast<char*>(b.solve + n) - base);
+  std::vector<char> image(front, 0);
+  auto at = [&](const void* dev_ptr) { return image.data() + (static_cast<const char*>(dev_ptr) - base); };
+  std::copy(classes, classes + L.classes, reinterpret_cast<gnnshap_class*>(at(b.classes)));
 
-  // 1. sampling
-  std::vector<gnnshap::SampleJob> sj(n);
+  // 1. sampling jobs
+  gnnshap::SampleJob* sj = reinterpret_cast<gnnshap::SampleJob*>(at(b.sample));
   int64_t max_half = 0, max_wpr = 0, max_k = 0, max_M = 0;
   for (int64_t t = 0; t < n; ++t) {
     const gnnshap_sample_plan& p = plans[t];
@@ -129,17 +136,14 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     max_k = std::max(max_k, p.num_rows);
     max_M = std::max(max_M, p.num_players);
   }
-  GS_HIP(hipMemcpyAsync(b.sample, sj.data(), n * sizeof(gnnshap::SampleJob), hipMemcpyHostToDevice, s));
-  if (int st = gnnshap::launch_sample_batch(b.sample, n, max_half, max_wpr, s)) return st;
 
-  // 2. coalition values
+  // 2. coalition-value jobs (two-layer models with X W_1 given)
   bool eval_all = model->num_layers == 2 && model->XW1;
   for (int64_t t = 0; t < n && eval_all; ++t) eval_all = gnnshap::eval_batchable(&sgs[t], model, plans[t].num_rows);
-  int st_eval = GNNSHAP_EUNSUPPORTED;
+  int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0, rows_jobs = 0;
+  size_t rows_lds = 0;
   if (eval_all) {
-    std::vector<gnnshap::EvalJob> ej(n);
-    int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0, rows_jobs = 0;
-    size_t rows_lds = 0;
+    gnnshap::EvalJob* ej = reinterpret_cast<gnnshap::EvalJob*>(at(b.eval));
     for (int64_t t = 0; t < n; ++t) {
       const gnnshap_subgraph& g = sgs[t];
       gnnshap::EvalJob& J = ej[t];
@@ -166,26 +170,11 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       max_ndst = std::max(max_ndst, J.n_dst);
       max_n1 = std::max(max_n1, J.n1);
     }
-    GS_HIP(hipMemcpyAsync(b.eval, ej.data(), n * sizeof(gnnshap::EvalJob), hipMemcpyHostToDevice, s));
-    const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
-                                model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
-    st_eval = gnnshap::launch_eval_batch(b.eval, n, md, max_nodes, max_ndst, max_n1, max_wpr, max_k, rows_jobs,
-                                         rows_lds, s);
-    if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
-    gnnshap::clear_error();
-  }
-  if (st_eval != GNNSHAP_OK) {
-    for (int64_t t = 0; t < n; ++t) {
-      const gnnshap_sample_plan& p = plans[t];
-      if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
-                                           p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
-                                           class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t], s))
-        return st;
-    }
   }
 
-  // 3. least squares: one-workgroup systems batched, the rest one by one
-  std::vector<gnnshap::SolveJob> vj;
+  // 3. least-squares jobs: one-workgroup systems batched, the rest one by one
+  gnnshap::SolveJob* vj = reinterpret_cast<gnnshap::SolveJob*>(at(b.solve));
+  int64_t nv = 0;
   std::vector<int64_t> rest;
   int64_t bM = 0, bw = 0, bh = 0, bnrb = 0, bnch = 0;
   for (int64_t t = 0; t < n; ++t) {
@@ -207,13 +196,31 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     bh = std::max(bh, J.half);
     bnrb = std::max(bnrb, J.nrb);
     bnch = std::max(bnch, J.nch);
-    vj.push_back(J);
+    vj[nv++] = J;
   }
-  if (!vj.empty()) {
-    GS_HIP(hipMemcpyAsync(b.solve, vj.data(), vj.size() * sizeof(gnnshap::SolveJob), hipMemcpyHostToDevice, s));
-    if (int st = gnnshap::launch_solve_batch(b.solve, static_cast<int64_t>(vj.size()), bM, bw, bh, bnrb, bnch, s))
-      return st;
+
+  GS_HIP(hipMemcpyAsync(ws, image.data(), front, hipMemcpyHostToDevice, s));
+  if (int st = gnnshap::launch_sample_batch(b.sample, n, max_half, max_wpr, s)) return st;
+  int st_eval = GNNSHAP_EUNSUPPORTED;
+  if (eval_all) {
+    const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
+                                model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
+    st_eval = gnnshap::launch_eval_batch(b.eval, n, md, max_nodes, max_ndst, max_n1, max_wpr, max_k, rows_jobs,
+                                         rows_lds, s);
+    if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
+    gnnshap::clear_error();
   }
+  if (st_eval != GNNSHAP_OK) {
+    for (int64_t t = 0; t < n; ++t) {
+      const gnnshap_sample_plan& p = plans[t];
+      if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
+                                           p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
+                                           class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t], s))
+        return st;
+    }
+  }
+  if (nv > 0)
+    if (int st = gnnshap::launch_solve_batch(b.solve, nv, bM, bw, bh, bnrb, bnch, s)) return st;
   for (int64_t t : rest) {
     if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
                                    f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],

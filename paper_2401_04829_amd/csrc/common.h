@@ -64,6 +64,28 @@ inline int max_lds_bytes() {
   return v;
 }
 
+// Page-locked host staging of at least `bytes` for device-to-host copies of
+// the calling thread (grown on demand, kept until the process ends), so the
+// copy queues behind the kernels instead of blocking the host first.
+// nullptr if the allocation fails.
+inline void* pinned_staging(size_t bytes) {
+  static thread_local void* buf = nullptr;
+  static thread_local size_t cap = 0;
+  if (cap < bytes) {
+    if (buf) (void)hipHostFree(buf);
+    buf = nullptr;
+    cap = 0;
+    const size_t want = bytes < 4096 ? 4096 : bytes;
+    if (hipHostMalloc(&buf, want, hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      buf = nullptr;
+      return nullptr;
+    }
+    cap = want;
+  }
+  return buf;
+}
+
 }  // namespace gnnshap
 
 #define GS_HIP(call)                                                                     \

@@ -411,14 +411,10 @@ __global__ void __launch_bounds__(1024) k_extract_batch(const int64_t* __restric
                    J.edge_src, J.edge_dst, J.edge_gid, results + static_cast<int64_t>(blockIdx.x) * kCounters);
 }
 
-__global__ void k_zero_results(int64_t* results, int64_t count) {
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < count;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    results[i] = 0;
-}
-
-// Batch workspace (all zero between calls, whatever the batch size): the job
-// table, the result rows, then one slice per target.
+// Batch workspace: one slice per target from the front (slice t at a fixed
+// offset, zero between calls), the job table and the result rows (rewritten
+// by every call) at the back.  A workspace sized for n targets serves every
+// smaller batch too, and the two regions of different calls never overlap.
 struct BatchWs {
   ExtractJob* jobs;
   int64_t* results;
@@ -426,14 +422,30 @@ struct BatchWs {
   size_t slice_bytes;
 };
 
-BatchWs carve_batch(gnnshap::Carver& c, int64_t num_nodes, int64_t n) {
-  BatchWs b;
+size_t slice_bytes_of(int64_t num_nodes) {
   gnnshap::Carver one(nullptr);
   carve(one, num_nodes);
-  b.slice_bytes = one.bytes();
-  b.jobs = c.take<ExtractJob>(n);
-  b.results = c.take<int64_t>(n * kCounters);
-  b.slices = c.take<char>(static_cast<size_t>(n) * b.slice_bytes);
+  return one.bytes();
+}
+
+size_t tail_bytes(int64_t n) {
+  gnnshap::Carver t(nullptr);
+  t.take<ExtractJob>(n);
+  t.take<int64_t>(n * kCounters);
+  return t.bytes();
+}
+
+size_t batch_bytes(int64_t num_nodes, int64_t n) {
+  return static_cast<size_t>(n) * slice_bytes_of(num_nodes) + tail_bytes(n);
+}
+
+BatchWs carve_batch(void* ws, size_t ws_bytes, int64_t num_nodes, int64_t n) {
+  BatchWs b;
+  b.slice_bytes = slice_bytes_of(num_nodes);
+  b.slices = static_cast<char*>(ws);
+  gnnshap::Carver t(b.slices + ((ws_bytes - tail_bytes(n)) & ~size_t(255)));
+  b.jobs = t.take<ExtractJob>(n);
+  b.results = t.take<int64_t>(n * kCounters);
   return b;
 }
 
@@ -481,8 +493,9 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
                                        sg->node_gid, sg->dst_ptr, sg->edge_src, sg->edge_dst, sg->edge_gid);
     }
     GS_LAUNCHED();
-    int64_t h[kCounters];
-    GS_HIP(hipMemcpyAsync(h, w.counters, sizeof(h), hipMemcpyDeviceToHost, s));
+    int64_t* h = static_cast<int64_t*>(gnnshap::pinned_staging(kCounters * sizeof(int64_t)));
+    if (!h) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
+    GS_HIP(hipMemcpyAsync(h, w.counters, kCounters * sizeof(int64_t), hipMemcpyDeviceToHost, s));
     k_zero_counters<<<1, 64, 0, s>>>(w.counters);
     GS_LAUNCHED();
     GS_HIP(hipStreamSynchronize(s));
@@ -520,8 +533,9 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
   k_dst_ptr<<<1, 1024, 0, s>>>(g->indptr, w.sorted, w.counters, hops, w.dstptr);
   GS_LAUNCHED();
 
-  int64_t h[kCounters];
-  GS_HIP(hipMemcpyAsync(h, w.counters, sizeof(h), hipMemcpyDeviceToHost, s));
+  int64_t* h = static_cast<int64_t*>(gnnshap::pinned_staging(kCounters * sizeof(int64_t)));
+  if (!h) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
+  GS_HIP(hipMemcpyAsync(h, w.counters, kCounters * sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GS_HIP(hipStreamSynchronize(s));
 
   int64_t nodes = 0;
@@ -566,9 +580,7 @@ extern "C" int gnnshap_extract_subgraph(const gnnshap_graph* g, int64_t target,
 extern "C" int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, size_t* bytes) {
   gnnshap::clear_error();
   if (!bytes || num_nodes < 1 || n < 1) return gnnshap::fail(GNNSHAP_EINVAL, "bad arguments");
-  gnnshap::Carver c(nullptr);
-  carve_batch(c, num_nodes, n);
-  *bytes = c.bytes();
+  *bytes = batch_bytes(num_nodes, n);
   return GNNSHAP_OK;
 }
 
@@ -584,12 +596,9 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
   if (nn > kOneBlockNodes)
     return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "batched extraction supports graphs of up to %lld nodes",
                          (long long)kOneBlockNodes);
-  gnnshap::Carver need(nullptr);
-  carve_batch(need, nn, n);
-  if (ws_bytes < need.bytes())
-    return gnnshap::fail(GNNSHAP_ECAPACITY, "batch extract workspace needs %zu bytes", need.bytes());
-  gnnshap::Carver c(ws);
-  const BatchWs b = carve_batch(c, nn, n);
+  const size_t need = batch_bytes(nn, n);
+  if (ws_bytes < need) return gnnshap::fail(GNNSHAP_ECAPACITY, "batch extract workspace needs %zu bytes", need);
+  const BatchWs b = carve_batch(ws, ws_bytes, nn, n);
   std::vector<ExtractJob> jobs(static_cast<size_t>(n));
   for (int64_t t = 0; t < n; ++t) {
     const gnnshap_subgraph* sg = &sgs[t];
@@ -610,16 +619,15 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
     k_extract_batch<<<static_cast<unsigned>(n), 1024, 0, s>>>(g->indptr, g->indices, nn, b.jobs, b.results);
   }
   GS_LAUNCHED();
-  std::vector<int64_t> h(static_cast<size_t>(n) * kCounters);
-  GS_HIP(hipMemcpyAsync(h.data(), b.results, h.size() * sizeof(int64_t), hipMemcpyDeviceToHost, s));
-  // back to all-zero: result rows and the job table (the slices reset themselves)
-  k_zero_results<<<gnnshap::grid_for(n * kCounters, 256, 64), 256, 0, s>>>(b.results, n * kCounters);
-  GS_LAUNCHED();
-  static_assert(sizeof(ExtractJob) % sizeof(int64_t) == 0, "job records are whole int64 words");
-  const int64_t job_words = n * static_cast<int64_t>(sizeof(ExtractJob) / sizeof(int64_t));
-  k_zero_results<<<gnnshap::grid_for(job_words, 256, 64), 256, 0, s>>>(reinterpret_cast<int64_t*>(b.jobs), job_words);
-  GS_LAUNCHED();
+  // The job table and result rows are rewritten by every call (each
+  // workgroup writes all the counters the host reads below); only the
+  // per-target slices need to start at zero, and they reset themselves.
+  const size_t hbytes = static_cast<size_t>(n) * kCounters * sizeof(int64_t);
+  const int64_t* hp = static_cast<const int64_t*>(gnnshap::pinned_staging(hbytes));
+  if (!hp) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
+  GS_HIP(hipMemcpyAsync(const_cast<int64_t*>(hp), b.results, hbytes, hipMemcpyDeviceToHost, s));
   GS_HIP(hipStreamSynchronize(s));
+  const std::vector<int64_t> h(hp, hp + static_cast<size_t>(n) * kCounters);
   bool all_ok = true;
   for (int64_t t = 0; t < n; ++t) {
     gnnshap_subgraph* sg = &sgs[t];
@@ -641,4 +649,26 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
   if (!all_ok) return gnnshap::fail(GNNSHAP_ECAPACITY, "some subgraphs exceed their capacities");
   return GNNSHAP_OK;
   GS_TRY_END
+}
+
+extern "C" int gnnshap_subgraph_batch_init(gnnshap_subgraph* sgs, int64_t n, int32_t num_hops, int64_t cap_nodes,
+                                           int64_t cap_edges, int32_t* node_gid, int32_t* dst_ptr,
+                                           int32_t* edge_src, int32_t* edge_dst, int64_t* edge_gid) {
+  gnnshap::clear_error();
+  if (!sgs || n < 0 || cap_nodes < 0 || cap_edges < 0) return gnnshap::fail(GNNSHAP_EINVAL, "bad argument");
+  if ((cap_nodes > 0 && (!node_gid || !dst_ptr)) || (cap_edges > 0 && (!edge_src || !edge_dst || !edge_gid)))
+    return gnnshap::fail(GNNSHAP_EINVAL, "null output arrays");
+  for (int64_t t = 0; t < n; ++t) {
+    gnnshap_subgraph& sg = sgs[t];
+    sg = gnnshap_subgraph{};
+    sg.num_hops = num_hops;
+    sg.cap_nodes = cap_nodes;
+    sg.cap_edges = cap_edges;
+    sg.node_gid = node_gid ? node_gid + t * cap_nodes : nullptr;
+    sg.dst_ptr = dst_ptr ? dst_ptr + t * (cap_nodes + 1) : nullptr;
+    sg.edge_src = edge_src ? edge_src + t * cap_edges : nullptr;
+    sg.edge_dst = edge_dst ? edge_dst + t * cap_edges : nullptr;
+    sg.edge_gid = edge_gid ? edge_gid + t * cap_edges : nullptr;
+  }
+  return GNNSHAP_OK;
 }

@@ -94,6 +94,7 @@ class Explainer:
         self._pipe = None
         self._bx = None                          # batched extraction: (n, zero-filled workspace)
         self._plans = {}                         # (M, p) -> (plan, classes): the plan does not depend on seed
+        self._ncls_hint = 1024                   # class-table length explain_batch allocates
 
     def prepare(self):
         """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
@@ -243,19 +244,15 @@ class Explainer:
             cn, ce = self._cap
             bufs = BatchSubgraphs(n, cn, ce, dev)
             sgs = (L.gnnshap_subgraph * n)()
-            pn, pd, ps, pe, pg = (bufs.node_gid.data_ptr(), bufs.dst_ptr.data_ptr(), bufs.edge_src.data_ptr(),
-                                  bufs.edge_dst.data_ptr(), bufs.edge_gid.data_ptr())
-            for t in range(n):
-                sg = sgs[t]
-                sg.num_hops, sg.cap_nodes, sg.cap_edges = self.hops, cn, ce
-                sg.node_gid, sg.dst_ptr = pn + 4 * cn * t, pd + 4 * (cn + 1) * t
-                sg.edge_src, sg.edge_dst, sg.edge_gid = ps + 4 * ce * t, pe + 4 * ce * t, pg + 8 * ce * t
+            L.gnnshap_subgraph_batch_init(sgs, self.hops, cn, ce, _vp(bufs.node_gid), _vp(bufs.dst_ptr),
+                                          _vp(bufs.edge_src), _vp(bufs.edge_dst), _vp(bufs.edge_gid))
             st = L.gnnshap_extract_batch(self.graph, tg, sgs, _vp(ws), ws.numel(), self.stream())
             if st == L.OK:
                 break
             self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
                          max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
         bufs.sgs = sgs
+        bufs.targets = tg
         return bufs, sgs
 
     def explain_batch(self, targets, num_samples, seed, target_class=-1):
@@ -270,25 +267,16 @@ class Explainer:
         subs, sgs = self.extract_batch(targets)
         n = len(targets)
         plans = (L.gnnshap_sample_plan * n)()
-        tables = []
-        for t, v in enumerate(targets):
-            M = sgs[t].num_edges
-            if M < 2:
-                raise ValueError(f"target {v} has {M} players; at least 2 are needed")
-            plans[t], cl = self._plan(M, num_samples, seed, v)
-            tables.append(cl)
-        ncls = sum(len(c) for c in tables)
-        classes = (L.gnnshap_class * ncls)()
-        o = 0
-        csz = ctypes.sizeof(L.gnnshap_class)
-        for cl in tables:
-            ctypes.memmove(ctypes.byref(classes, o * csz), cl, ctypes.sizeof(cl))
-            o += len(cl)
-        out = BatchExplanations(targets, subs, plans, tables, dev)
+        cl = (L.gnnshap_class * self._ncls_hint)()
+        st, ncls, totals = L.gnnshap_plan_batch(sgs, subs.targets, int(num_samples), int(seed), plans, cl)
+        if st == L.ECAPACITY:
+            self._ncls_hint = ncls + ncls // 4
+            cl = (L.gnnshap_class * self._ncls_hint)()
+            st, ncls, totals = L.gnnshap_plan_batch(sgs, subs.targets, int(num_samples), int(seed), plans, cl)
+        out = BatchExplanations(targets, subs, plans, cl, ncls, totals, dev)
         ws = self.ws_batch.get(L.gnnshap_explain_batch_workspace(sgs, plans, self.model))
-        L.gnnshap_explain_batch(sgs, plans, classes, self.model, _vp(self.X), int(target_class), _vp(out.masks),
-                                _vp(out.weights), _vp(out.y), _vp(out.fef), _vp(out.cls), _vp(out.phi),
-                                _vp(out.info), _vp(ws), ws.numel(), self.stream())
+        L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *out.pointers(),
+                                _vp(ws), ws.numel(), self.stream())
         return out
 
 
@@ -311,28 +299,56 @@ class BatchSubgraphs:
 
 
 class BatchExplanations:
-    """Outputs of gnnshap_explain_batch, packed in target order; entry t is
-    materialised as an Explanation (tensor views) on access."""
+    """Outputs of gnnshap_explain_batch, packed in target order in one device
+    allocation; entry t is materialised as an Explanation (tensor views) on
+    access.  `classes` holds the concatenated class tables (the first
+    num_classes records)."""
 
-    def __init__(self, targets, subs, plans, tables, dev):
+    _FIELDS = (("masks", torch.int64, 8), ("weights", torch.float32, 4), ("y", torch.float32, 4),
+               ("fef", torch.float32, 4), ("cls", torch.int32, 4), ("phi", torch.float32, 4),
+               ("info", torch.int32, 4))
+
+    def __init__(self, targets, subs, plans, classes, num_classes, totals, dev):
         n = len(targets)
-        self.targets, self.subs, self.plans, self.tables = list(targets), subs, plans, tables
-        self.k = [plans[t].num_rows for t in range(n)]
-        self.wpr = [plans[t].words_per_row for t in range(n)]
-        self.M = [plans[t].num_players for t in range(n)]
-        self.total_rows = sum(self.k)
-        self.mask_off, self.row_off, self.player_off = [0], [0], [0]
-        for t in range(n):
-            self.mask_off.append(self.mask_off[-1] + self.k[t] * self.wpr[t])
-            self.row_off.append(self.row_off[-1] + self.k[t])
-            self.player_off.append(self.player_off[-1] + self.M[t])
-        self.masks = torch.empty(self.mask_off[-1], dtype=torch.int64, device=dev)
-        self.weights = torch.empty(self.total_rows, dtype=torch.float32, device=dev)
-        self.y = torch.empty(self.total_rows, dtype=torch.float32, device=dev)
-        self.fef = torch.empty(2 * n, dtype=torch.float32, device=dev)
-        self.cls = torch.empty(n, dtype=torch.int32, device=dev)
-        self.phi = torch.empty(self.player_off[-1], dtype=torch.float32, device=dev)
-        self.info = torch.empty(n, dtype=torch.int32, device=dev)
+        self.targets, self.subs, self.plans, self.classes, self.num_classes = targets, subs, plans, classes, num_classes
+        words, rows, players = totals
+        self.total_rows = rows
+        counts = (words, rows, rows, 2 * n, n, players, n)
+        self._span, off = {}, 0
+        for (name, _, size), c in zip(self._FIELDS, counts):
+            self._span[name] = (off, c)
+            off += (c * size + 255) // 256 * 256
+        self.buf = torch.empty(max(off, 256), dtype=torch.uint8, device=dev)
+        self._offs = None
+
+    def pointers(self):
+        """Device addresses of the seven outputs, in gnnshap_explain_batch's order."""
+        base = self.buf.data_ptr()
+        return tuple(ctypes.c_void_p(base + self._span[name][0]) for name, _, _ in self._FIELDS)
+
+    def _view(self, name):
+        off, c = self._span[name]
+        dt, size = next((d, z) for f, d, z in self._FIELDS if f == name)
+        return self.buf[off:off + c * size].view(dt)
+
+    masks = property(lambda self: self._view("masks"))
+    weights = property(lambda self: self._view("weights"))
+    y = property(lambda self: self._view("y"))
+    fef = property(lambda self: self._view("fef"))
+    cls = property(lambda self: self._view("cls"))
+    phi = property(lambda self: self._view("phi"))
+    info = property(lambda self: self._view("info"))
+
+    def _offsets(self):
+        if self._offs is None:
+            mo, ro, po, co = [0], [0], [0], [0]
+            for p in self.plans:
+                mo.append(mo[-1] + p.num_rows * p.words_per_row)
+                ro.append(ro[-1] + p.num_rows)
+                po.append(po[-1] + p.num_players)
+                co.append(co[-1] + p.num_classes)
+            self._offs = (mo, ro, po, co)
+        return self._offs
 
     def __len__(self):
         return len(self.targets)
@@ -340,12 +356,15 @@ class BatchExplanations:
     def __getitem__(self, t):
         if t < 0:
             t += len(self)
-        mo, ro, po = self.mask_off[t], self.row_off[t], self.player_off[t]
-        k, w, M = self.k[t], self.wpr[t], self.M[t]
-        return Explanation(target=self.targets[t], sub=self.subs[t], plan=self.plans[t], classes=self.tables[t],
-                           masks=self.masks[mo:mo + k * w].view(k, w), weights=self.weights[ro:ro + k],
-                           y=self.y[ro:ro + k], f_empty_full=self.fef[2 * t:2 * t + 2], cls=self.cls[t:t + 1],
-                           phi=self.phi[po:po + M], info=self.info[t:t + 1])
+        mo, ro, po, co = (o[t] for o in self._offsets())
+        p = self.plans[t]
+        k, w, M = p.num_rows, p.words_per_row, p.num_players
+        tab = (L.gnnshap_class * p.num_classes)(*self.classes[co:co + p.num_classes])
+        masks, weights, y, fef, cls, phi, info = (self._view(f) for f, _, _ in self._FIELDS)
+        return Explanation(target=self.targets[t], sub=self.subs[t], plan=p, classes=tab,
+                           masks=masks[mo:mo + k * w].view(k, w), weights=weights[ro:ro + k],
+                           y=y[ro:ro + k], f_empty_full=fef[2 * t:2 * t + 2], cls=cls[t:t + 1],
+                           phi=phi[po:po + M], info=info[t:t + 1])
 
     def __iter__(self):
         return (self[t] for t in range(len(self)))

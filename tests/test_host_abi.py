@@ -107,3 +107,51 @@ def test_batch_entry_points_reject_bad_arguments():
     assert lib.gnnshap_explain_batch_workspace(None, None, 1, None, ctypes.byref(n)) == L.EINVAL
     assert lib.gnnshap_explain_batch(None, None, None, 0, None, None, -1, None, None, None, None, None, None, None,
                                      None, 0, None) == L.EINVAL
+
+
+def test_plan_batch_equals_single_plans():
+    Ms = [7, 60, 60, 2, 400, 7, 33, 1000]
+    sgs = (L.gnnshap_subgraph * len(Ms))()
+    for sg, M in zip(sgs, Ms):
+        sg.num_edges = M
+    ids = (ctypes.c_int64 * len(Ms))(*[100 + i for i in range(len(Ms))])
+    plans = (L.gnnshap_sample_plan * len(Ms))()
+    st, ncls, totals = L.gnnshap_plan_batch(sgs, ids, 2000, 77, plans, None)
+    assert st == L.ECAPACITY and ncls > 0
+    short = (L.gnnshap_class * (ncls - 1))()
+    assert L.gnnshap_plan_batch(sgs, ids, 2000, 77, plans, short)[0] == L.ECAPACITY
+    classes = (L.gnnshap_class * ncls)()
+    st, ncls2, totals = L.gnnshap_plan_batch(sgs, ids, 2000, 77, plans, classes)
+    assert st == L.OK and ncls2 == ncls
+    o, words, rows = 0, 0, 0
+    for t, M in enumerate(Ms):
+        plan, cl = L.gnnshap_plan_samples(M, 2000, 77, 100 + t)
+        got = plans[t]
+        for f, _ in L.gnnshap_sample_plan._fields_:
+            assert getattr(got, f) == getattr(plan, f), (t, f)
+        for i in range(plan.num_classes):
+            a, b = classes[o + i], cl[i]
+            assert (a.size, a.full, a.row_begin, a.row_count, a.weight) == \
+                   (b.size, b.full, b.row_begin, b.row_count, b.weight)
+        o += plan.num_classes
+        words += plan.num_rows * plan.words_per_row
+        rows += plan.num_rows
+    assert o == ncls and totals == (words, rows, sum(Ms))
+    sgs[3].num_edges = 1
+    st = L.load().gnnshap_plan_batch(sgs, ids, len(Ms), 2000, 77, plans, classes, ncls, ctypes.byref(ctypes.c_int64()),
+                                     None)
+    assert st == L.EINVAL and "target 3" in L.load().gnnshap_last_error().decode()
+
+
+def test_subgraph_batch_init_strides():
+    sgs = (L.gnnshap_subgraph * 3)()
+    L.gnnshap_subgraph_batch_init(sgs, 2, 10, 20, 1 << 20, 2 << 20, 3 << 20, 4 << 20, 5 << 20)
+    for t, sg in enumerate(sgs):
+        assert (sg.num_hops, sg.cap_nodes, sg.cap_edges, sg.num_edges) == (2, 10, 20, 0)
+        assert sg.node_gid == (1 << 20) + 4 * 10 * t
+        assert sg.dst_ptr == (2 << 20) + 4 * 11 * t
+        assert sg.edge_src == (3 << 20) + 4 * 20 * t
+        assert sg.edge_dst == (4 << 20) + 4 * 20 * t
+        assert sg.edge_gid == (5 << 20) + 8 * 20 * t
+    with pytest.raises(RuntimeError):
+        L.gnnshap_subgraph_batch_init(sgs, 2, 10, 20, None, 2 << 20, 3 << 20, 4 << 20, 5 << 20)
