@@ -14,9 +14,14 @@ struct SampleJob {
   uint32_t seed_lo, seed_hi, st_lo, st_hi;
   uint64_t* masks;
   float* weights;
+  int64_t blk0, rpb;         // first workgroup of the job in the launch, rows per workgroup
 };
-// Samples every job's rows: grid (row blocks, n).
-int launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t max_half, int64_t max_wpr, hipStream_t s);
+// Fills blk0 and rpb of jobs[0 .. n) (rows per workgroup inversely
+// proportional to a row's cost, so that the workgroups of large and small
+// targets take about as long) and returns the number of workgroups.
+int64_t plan_sample_batch(SampleJob* jobs, int64_t n);
+// Samples every job's rows: one workgroup per `rpb` rows of a job.
+int launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t blocks, int64_t max_wpr, hipStream_t s);
 
 // ---- evaluation (two-layer GCN, one pass per target) -------------------------------------
 struct EvalJob {
@@ -81,7 +86,10 @@ struct SolveJob {
 bool solve_batchable(const gnnshap_sample_plan* plan);
 size_t solve_slice_bytes(const gnnshap_sample_plan* plan);
 int solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice, SolveJob* job);
-int launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
-                       int64_t max_nrb, int64_t max_nch, hipStream_t s);
+// The solve of a batch in two launches sequences: G~ and the right-hand side
+// (multi-block kernels), then one workgroup per system.
+int launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
+                         int64_t max_nrb, int64_t max_nch, hipStream_t s);
+int launch_solve_factor(const SolveJob* jobs, int64_t n, hipStream_t s);
 
 }  // namespace gnnshap

@@ -5,12 +5,63 @@
 // does not fit the batched kernels go through the single-target calls inside
 // the same sequence; every value is the one the single-target calls give.
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 #include <vector>
 
 #include "batch.h"
 #include "common.h"
 
+namespace gnnshap {
+
+// Side streams of the current device for the calling thread, each with the
+// two events that fork work onto it and join it back (created on first use,
+// default priority, kept until the process ends).
+constexpr int kSideStreams = 2;
+
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+
+struct DeviceSides {
+  int device = -1;
+  SideStream side[kSideStreams];
+};
+
+SideStream* side_stream(int i) {
+  static thread_local std::vector<DeviceSides> per_device;
+  int dev = 0;
+  if (i < 0 || i >= kSideStreams || hipGetDevice(&dev) != hipSuccess) return nullptr;
+  for (DeviceSides& d : per_device)
+    if (d.device == dev) return &d.side[i];
+  DeviceSides d;
+  d.device = dev;
+  for (SideStream& x : d.side) {
+    if (hipStreamCreateWithFlags(&x.stream, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&x.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+  }
+  per_device.push_back(d);
+  return &per_device.back().side[i];
+}
+
+}  // namespace gnnshap
+
 namespace {
+
+// Panels (64 players each) from which a one-workgroup system joins group 0,
+// given the largest system's panel count; 0 = one group.
+int64_t split_cut(int64_t max_panels) {
+  if (const char* e = getenv("GS_CUT")) {
+    const long long c = atoll(e);
+    return c < 0 ? max_panels + c : c;
+  }
+  return max_panels >= 4 ? max_panels - 2 : 0;
+}
 
 struct Layout {
   int64_t n = 0, classes = 0;
@@ -69,6 +120,29 @@ BatchWs carve(gnnshap::Carver& c, const Layout& L) {
   return b;
 }
 
+// The target order (group 0 first, each group in target order) and the
+// group boundaries: group g = order[bound[g], bound[g+1]).  Group 0 holds the
+// one-workgroup systems of at least split_cut() panels, group 1 the rest.
+void split_groups(const gnnshap_sample_plan* plans, int64_t n, std::vector<int64_t>* order, int64_t bound[3]) {
+  int64_t max_panels = 0;
+  for (int64_t t = 0; t < n; ++t)
+    if (gnnshap::solve_batchable(&plans[t]))
+      max_panels = std::max<int64_t>(max_panels, (plans[t].num_players + 63) / 64);
+  const int64_t cut = split_cut(max_panels);
+  auto group_of = [&](int64_t t) -> int {
+    return cut > 0 && gnnshap::solve_batchable(&plans[t]) && (plans[t].num_players + 63) / 64 >= cut ? 0 : 1;
+  };
+  order->clear();
+  order->reserve(n);
+  bound[0] = 0;
+  for (int g = 0; g < 2; ++g) {
+    for (int64_t t = 0; t < n; ++t)
+      if (group_of(t) == g) order->push_back(t);
+    bound[g + 1] = static_cast<int64_t>(order->size());
+  }
+  if (bound[1] == n) bound[1] = 0;   // everything large: one group
+}
+
 }  // namespace
 
 extern "C" int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
@@ -113,119 +187,179 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     }
     if (row != plans[t].num_rows / 2) return gnnshap::fail(GNNSHAP_EINVAL, "class table of target %lld short", (long long)t);
   }
-  // The class tables and the three job tables sit at the front of the
-  // workspace; they are assembled in a host image of that range and copied
-  // in one transfer before the first launch.
+  // Targets run in two groups when their systems differ much in size: the
+  // largest one-workgroup systems (whose factorisations set the length of the
+  // whole sequence) and their sampling and evaluation on a side stream, the
+  // rest on `stream`, each step launched for both groups before the next, so
+  // that the long factorisations overlap the other group's work.
+  std::vector<int64_t> order;
+  int64_t bound[3];
+  split_groups(plans, n, &order, bound);
+
+  // The class tables and the three job tables (in group order) sit at the
+  // front of the workspace; they are assembled in a host image of that range
+  // and copied in one transfer before the first launch.
   char* const base = static_cast<char*>(ws);
   const size_t front = static_cast<size_t>(reinterpret_cast<char*>(b.solve + n) - base);
   std::vector<char> image(front, 0);
   auto at = [&](const void* dev_ptr) { return image.data() + (static_cast<const char*>(dev_ptr) - base); };
   std::copy(classes, classes + L.classes, reinterpret_cast<gnnshap_class*>(at(b.classes)));
-
-  // 1. sampling jobs
   gnnshap::SampleJob* sj = reinterpret_cast<gnnshap::SampleJob*>(at(b.sample));
-  int64_t max_half = 0, max_wpr = 0, max_k = 0, max_M = 0;
-  for (int64_t t = 0; t < n; ++t) {
-    const gnnshap_sample_plan& p = plans[t];
-    sj[t] = gnnshap::SampleJob{b.classes + L.class_off[t], p.num_classes, p.num_rows / 2, p.num_players,
-                               p.words_per_row, static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32),
-                               static_cast<uint32_t>(p.stream_id), static_cast<uint32_t>(p.stream_id >> 32),
-                               masks + L.mask_off[t], weights + L.row_off[t]};
-    max_half = std::max(max_half, p.num_rows / 2);
-    max_wpr = std::max(max_wpr, p.words_per_row);
-    max_k = std::max(max_k, p.num_rows);
-    max_M = std::max(max_M, p.num_players);
-  }
+  gnnshap::EvalJob* ej = reinterpret_cast<gnnshap::EvalJob*>(at(b.eval));
+  gnnshap::SolveJob* vj = reinterpret_cast<gnnshap::SolveJob*>(at(b.solve));
 
-  // 2. coalition-value jobs (two-layer models with X W_1 given)
-  bool eval_all = model->num_layers == 2 && model->XW1;
-  for (int64_t t = 0; t < n && eval_all; ++t) eval_all = gnnshap::eval_batchable(&sgs[t], model, plans[t].num_rows);
-  int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0, rows_jobs = 0;
-  size_t rows_lds = 0;
-  if (eval_all) {
-    gnnshap::EvalJob* ej = reinterpret_cast<gnnshap::EvalJob*>(at(b.eval));
-    for (int64_t t = 0; t < n; ++t) {
-      const gnnshap_subgraph& g = sgs[t];
-      gnnshap::EvalJob& J = ej[t];
-      J = gnnshap::EvalJob{};
-      J.node_gid = g.node_gid;
-      J.dst_ptr = g.dst_ptr;
-      J.edge_src = g.edge_src;
-      J.n_nodes = g.num_nodes;
-      J.n_dst = g.num_dst;
-      J.n1 = g.hop_ptr[2];
-      J.M = g.num_edges;
-      J.wpr = plans[t].words_per_row;
-      J.k = plans[t].num_rows;
+  struct Group {
+    int64_t begin = 0, end = 0;                      // range of order[]
+    int64_t blocks = 0, max_wpr = 0, max_k = 0;      // sampling
+    bool eval_all = false;                           // batched evaluation
+    int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0, rows_jobs = 0;
+    size_t rows_lds = 0;
+    int64_t solve_begin = 0, solve_count = 0;        // range of the solve job table
+    int64_t bM = 0, bw = 0, bh = 0, bnrb = 0, bnch = 0;
+    std::vector<int64_t> rest;                       // targets solved one by one
+  } grp[2];
+  for (int g = 0; g < 2; ++g) {
+    grp[g].begin = bound[g];
+    grp[g].end = bound[g + 1];
+  }
+  int64_t nv = 0;
+  for (Group& G : grp) {
+    // 1. sampling jobs
+    for (int64_t j = G.begin; j < G.end; ++j) {
+      const int64_t t = order[j];
+      const gnnshap_sample_plan& p = plans[t];
+      sj[j] = gnnshap::SampleJob{b.classes + L.class_off[t], p.num_classes, p.num_rows / 2, p.num_players,
+                                 p.words_per_row, static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32),
+                                 static_cast<uint32_t>(p.stream_id), static_cast<uint32_t>(p.stream_id >> 32),
+                                 masks + L.mask_off[t], weights + L.row_off[t]};
+      G.max_wpr = std::max(G.max_wpr, p.words_per_row);
+      G.max_k = std::max(G.max_k, p.num_rows);
+    }
+    G.blocks = gnnshap::plan_sample_batch(sj + G.begin, G.end - G.begin);
+    // 2. coalition-value jobs (two-layer models with X W_1 given)
+    G.eval_all = model->num_layers == 2 && model->XW1;
+    for (int64_t j = G.begin; j < G.end && G.eval_all; ++j)
+      G.eval_all = gnnshap::eval_batchable(&sgs[order[j]], model, plans[order[j]].num_rows);
+    if (G.eval_all) {
+      for (int64_t j = G.begin; j < G.end; ++j) {
+        const int64_t t = order[j];
+        const gnnshap_subgraph& g = sgs[t];
+        gnnshap::EvalJob& J = ej[j];
+        J = gnnshap::EvalJob{};
+        J.node_gid = g.node_gid;
+        J.dst_ptr = g.dst_ptr;
+        J.edge_src = g.edge_src;
+        J.n_nodes = g.num_nodes;
+        J.n_dst = g.num_dst;
+        J.n1 = g.hop_ptr[2];
+        J.M = g.num_edges;
+        J.wpr = plans[t].words_per_row;
+        J.k = plans[t].num_rows;
+        J.masks = masks + L.mask_off[t];
+        J.y = y + L.row_off[t];
+        J.fef = f_empty_full + 2 * t;
+        J.cls_out = class_out ? class_out + t : nullptr;
+        gnnshap::eval_carve_slice(b.eval_slice[t], &g, model, J.k, &J);
+        const size_t rl = gnnshap::eval_rows_lds(&g, model);
+        J.rows_ok = rl > 0 ? 1 : 0;
+        G.rows_jobs += J.rows_ok;
+        G.rows_lds = std::max(G.rows_lds, rl);
+        G.max_nodes = std::max(G.max_nodes, J.n_nodes);
+        G.max_ndst = std::max(G.max_ndst, J.n_dst);
+        G.max_n1 = std::max(G.max_n1, J.n1);
+      }
+    }
+    // 3. least-squares jobs: one-workgroup systems batched, the rest one by one
+    G.solve_begin = nv;
+    for (int64_t j = G.begin; j < G.end; ++j) {
+      const int64_t t = order[j];
+      const gnnshap_sample_plan& p = plans[t];
+      if (!gnnshap::solve_batchable(&p)) {
+        G.rest.push_back(t);
+        continue;
+      }
+      gnnshap::SolveJob J{};
+      if (int st = gnnshap::solve_fill_job(&p, classes + L.class_off[t], b.solve_slice[t], &J)) return st;
       J.masks = masks + L.mask_off[t];
       J.y = y + L.row_off[t];
       J.fef = f_empty_full + 2 * t;
-      J.cls_out = class_out ? class_out + t : nullptr;
-      gnnshap::eval_carve_slice(b.eval_slice[t], &g, model, J.k, &J);
-      const size_t rl = gnnshap::eval_rows_lds(&g, model);
-      J.rows_ok = rl > 0 ? 1 : 0;
-      rows_jobs += J.rows_ok;
-      rows_lds = std::max(rows_lds, rl);
-      max_nodes = std::max(max_nodes, J.n_nodes);
-      max_ndst = std::max(max_ndst, J.n_dst);
-      max_n1 = std::max(max_n1, J.n1);
+      J.phi = phi + L.player_off[t];
+      J.info = info + t;
+      J.cls = b.classes + L.class_off[t];
+      G.bM = std::max(G.bM, J.M);
+      G.bw = std::max(G.bw, J.wpr);
+      G.bh = std::max(G.bh, J.half);
+      G.bnrb = std::max(G.bnrb, J.nrb);
+      G.bnch = std::max(G.bnch, J.nch);
+      vj[nv++] = J;
     }
-  }
-
-  // 3. least-squares jobs: one-workgroup systems batched, the rest one by one
-  gnnshap::SolveJob* vj = reinterpret_cast<gnnshap::SolveJob*>(at(b.solve));
-  int64_t nv = 0;
-  std::vector<int64_t> rest;
-  int64_t bM = 0, bw = 0, bh = 0, bnrb = 0, bnch = 0;
-  for (int64_t t = 0; t < n; ++t) {
-    const gnnshap_sample_plan& p = plans[t];
-    if (!gnnshap::solve_batchable(&p)) {
-      rest.push_back(t);
-      continue;
-    }
-    gnnshap::SolveJob J{};
-    if (int st = gnnshap::solve_fill_job(&p, classes + L.class_off[t], b.solve_slice[t], &J)) return st;
-    J.masks = masks + L.mask_off[t];
-    J.y = y + L.row_off[t];
-    J.fef = f_empty_full + 2 * t;
-    J.phi = phi + L.player_off[t];
-    J.info = info + t;
-    J.cls = b.classes + L.class_off[t];
-    bM = std::max(bM, J.M);
-    bw = std::max(bw, J.wpr);
-    bh = std::max(bh, J.half);
-    bnrb = std::max(bnrb, J.nrb);
-    bnch = std::max(bnch, J.nch);
-    vj[nv++] = J;
+    G.solve_count = nv - G.solve_begin;
   }
 
   GS_HIP(hipMemcpyAsync(ws, image.data(), front, hipMemcpyHostToDevice, s));
-  if (int st = gnnshap::launch_sample_batch(b.sample, n, max_half, max_wpr, s)) return st;
-  int st_eval = GNNSHAP_EUNSUPPORTED;
-  if (eval_all) {
-    const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
-                                model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
-    st_eval = gnnshap::launch_eval_batch(b.eval, n, md, max_nodes, max_ndst, max_n1, max_wpr, max_k, rows_jobs,
-                                         rows_lds, s);
-    if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
-    gnnshap::clear_error();
+  hipStream_t gs[2] = {s, s};
+  gnnshap::SideStream* side = nullptr;
+  if (grp[0].end > grp[0].begin) {
+    side = gnnshap::side_stream(0);
+    if (!side) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+    GS_HIP(hipEventRecord(side->fork, s));
+    GS_HIP(hipStreamWaitEvent(side->stream, side->fork, 0));
+    gs[0] = side->stream;
   }
-  if (st_eval != GNNSHAP_OK) {
-    for (int64_t t = 0; t < n; ++t) {
-      const gnnshap_sample_plan& p = plans[t];
-      if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
-                                           p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
-                                           class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t], s))
+  // 1. sampling
+  for (int gi = 0; gi < 2; ++gi) {
+    const Group& G = grp[gi];
+    if (G.end > G.begin)
+      if (int st = gnnshap::launch_sample_batch(b.sample + G.begin, G.end - G.begin, G.blocks, G.max_wpr, gs[gi]))
+        return st;
+  }
+  // 2. coalition values
+  for (int gi = 0; gi < 2; ++gi) {
+    const Group& G = grp[gi];
+    if (G.end == G.begin) continue;
+    int st_eval = GNNSHAP_EUNSUPPORTED;
+    if (G.eval_all) {
+      const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
+                                  model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
+      st_eval = gnnshap::launch_eval_batch(b.eval + G.begin, G.end - G.begin, md, G.max_nodes, G.max_ndst, G.max_n1,
+                                           G.max_wpr, G.max_k, G.rows_jobs, G.rows_lds, gs[gi]);
+      if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
+      gnnshap::clear_error();
+    }
+    if (st_eval != GNNSHAP_OK) {
+      for (int64_t j = G.begin; j < G.end; ++j) {
+        const int64_t t = order[j];
+        const gnnshap_sample_plan& p = plans[t];
+        if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
+                                             p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
+                                             class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t],
+                                             gs[gi]))
+          return st;
+      }
+    }
+  }
+  // 3. least squares: G~ and the right-hand sides, then the factorisations
+  for (int gi = 0; gi < 2; ++gi) {
+    const Group& G = grp[gi];
+    if (G.solve_count > 0)
+      if (int st = gnnshap::launch_solve_prepare(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bh, G.bnrb,
+                                                 G.bnch, gs[gi]))
+        return st;
+  }
+  for (int gi = 0; gi < 2; ++gi) {
+    const Group& G = grp[gi];
+    if (G.solve_count > 0)
+      if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, gs[gi])) return st;
+    for (int64_t t : G.rest) {
+      if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
+                                     f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
+                                     L.solve_bytes[t], gs[gi]))
         return st;
     }
   }
-  if (nv > 0)
-    if (int st = gnnshap::launch_solve_batch(b.solve, nv, bM, bw, bh, bnrb, bnch, s)) return st;
-  for (int64_t t : rest) {
-    if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
-                                   f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
-                                   L.solve_bytes[t], s))
-      return st;
+  if (side) {
+    GS_HIP(hipEventRecord(side->join, side->stream));
+    GS_HIP(hipStreamWaitEvent(s, side->join, 0));
   }
   return GNNSHAP_OK;
   GS_TRY_END

@@ -670,6 +670,104 @@ __global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows(
                     y_rows, blockIdx.x);
 }
 
+// The two end coalitions of a two-layer GCN with hops >= 2 (no players and
+// every player), every class, in one workgroup: the full coalition's degrees
+// are the in-degrees of the subgraph; layer 1 runs with one thread per
+// (node of H_1, feature), the class logits per (node, class) and layer 2 per
+// class.  sp_y[c] = f_c(empty), sp_y[C + c] = f_c(E_c).
+constexpr int kEndsThreads = 256;
+
+size_t ends_lds_bytes(int64_t n_dst, int64_t n1, int h, int C) {
+  const int64_t nx = h >= kEndsThreads ? 1 : kEndsThreads / h;
+  return sizeof(float) * static_cast<size_t>(n_dst + n1 * C + nx * h + h + C);
+}
+
+__device__ __forceinline__ void ends_l2_body(const int32_t* __restrict__ dst_ptr,
+                                             const int32_t* __restrict__ edge_src, int64_t n_dst, int64_t n1,
+                                             const float* __restrict__ Zc, const float* __restrict__ b1,
+                                             const float* __restrict__ W2, const float* __restrict__ b2, int h,
+                                             int C, float* __restrict__ sp_y) {
+  extern __shared__ __align__(16) float sm[];
+  const int64_t nx = h >= kEndsThreads ? 1 : kEndsThreads / h;
+  float* dinv = sm;                   // n_dst: full-coalition d^-1/2
+  float* tt = dinv + n_dst;           // n1 x C: H^1[x] . W_2[:, c] under the full coalition
+  float* hv = tt + n1 * C;            // nx x h: H^1 rows of the current node chunk
+  float* he = hv + nx * h;            // h: H^1 row of the target under the empty coalition
+  float* te = he + h;                 // C
+  const int tid = threadIdx.x;
+  for (int64_t x = tid; x < n_dst; x += kEndsThreads)
+    dinv[x] = rsqrtf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
+  const float d0 = rsqrtf(1.0f);      // degree factor of every node when no edge is present
+  for (int f = tid; f < h; f += kEndsThreads)
+    he[f] = fmaxf(d0 * (0.0f + d0 * Zc[f]) + (b1 ? b1[f] : 0.f), 0.f);
+  __syncthreads();
+  for (int64_t x0 = 0; x0 < n1; x0 += nx) {
+    const int64_t nn = n1 - x0 < nx ? n1 - x0 : nx;
+    for (int64_t it = tid; it < nn * h; it += kEndsThreads) {
+      const int64_t x = x0 + it / h;
+      const int f = static_cast<int>(it % h);
+      const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+      float acc = 0.f;
+      // eight players' loads in flight at a time, summed in player order
+      for (int64_t eb = e0; eb < e1; eb += 8) {
+        int32_t u[8];
+        float z[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) u[q] = eb + q < e1 ? edge_src[eb + q] : 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) z[q] = eb + q < e1 ? Zc[static_cast<int64_t>(u[q]) * h + f] : 0.f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (eb + q < e1) acc += (u[q] < n_dst ? dinv[u[q]] : 1.0f) * z[q];
+      }
+      const float dx = dinv[x];
+      hv[it] = fmaxf(dx * (acc + dx * Zc[x * h + f]) + (b1 ? b1[f] : 0.f), 0.f);
+    }
+    __syncthreads();
+    for (int64_t it = tid; it < nn * C; it += kEndsThreads) {
+      const int64_t xi = it / C;
+      const int c = static_cast<int>(it % C);
+      float t = 0.f;
+      for (int f = 0; f < h; ++f) t += hv[xi * h + f] * W2[static_cast<int64_t>(f) * C + c];
+      tt[(x0 + xi) * C + c] = t;
+    }
+    __syncthreads();
+  }
+  for (int c = tid; c < C; c += kEndsThreads) {
+    float t = 0.f;
+    for (int f = 0; f < h; ++f) t += he[f] * W2[static_cast<int64_t>(f) * C + c];
+    te[c] = t;
+  }
+  __syncthreads();
+  const int64_t indeg = dst_ptr[1];
+  const float dv = dinv[0];
+  for (int c = tid; c < C; c += kEndsThreads) {
+    const float bias = b2 ? b2[c] : 0.f;
+    sp_y[c] = d0 * (0.0f + d0 * te[c]) + bias;
+    float acc = 0.f;
+    for (int64_t eb = 0; eb < indeg; eb += 8) {
+      int32_t u[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) u[q] = eb + q < indeg ? edge_src[eb + q] : 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (eb + q < indeg) acc += dinv[u[q]] * tt[static_cast<int64_t>(u[q]) * C + c];
+    }
+    acc += dv * tt[c];
+    sp_y[C + c] = dv * acc + bias;
+  }
+}
+
+__global__ void __launch_bounds__(kEndsThreads) k_eval_ends(const int32_t* __restrict__ dst_ptr,
+                                                             const int32_t* __restrict__ edge_src, int64_t n_dst,
+                                                             int64_t n1, const float* __restrict__ Zc,
+                                                             const float* __restrict__ b1,
+                                                             const float* __restrict__ W2,
+                                                             const float* __restrict__ b2, int h, int C,
+                                                             float* __restrict__ sp_y) {
+  ends_l2_body(dst_ptr, edge_src, n_dst, n1, Zc, b1, W2, b2, h, C, sp_y);
+}
+
 template <int FPT>
 __global__ void __launch_bounds__(256) k_eval_l2(
     const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t row_off,
@@ -857,6 +955,11 @@ bool fused_l2_ok(const Shape& sh, int64_t cap, bool all_classes) {
   return fused_lds_bytes(sh, tbr, all_classes ? sh.dims[2] : 1, fs) <= 65536;
 }
 
+// Whether the end coalitions take k_eval_ends (two-layer models, hops >= 2).
+bool ends_ok(const Shape& sh) {
+  return sh.L == 2 && sh.hops >= 2 && ends_lds_bytes(sh.n_dst, sh.nd[1], sh.dims[1], sh.dims[2]) <= 65536;
+}
+
 int launch_fused_l2(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn* m, const Shape& sh, const Ws& w,
                     const uint64_t* masks, const int32_t* rows, int64_t row_off, int64_t cap, const int32_t* dyn,
                     bool all_classes, float* y_rows) {
@@ -958,15 +1061,19 @@ __global__ void k_gather_batch(const gnnshap::EvalJob* __restrict__ jobs, const 
   }
 }
 
-// special: the two rows with no / all players, every class; else the live rows.
+// The end coalitions of every job.
+__global__ void __launch_bounds__(kEndsThreads) k_eval_ends_batch(const gnnshap::EvalJob* __restrict__ jobs,
+                                                                   gnnshap::EvalModel md) {
+  const gnnshap::EvalJob J = jobs[blockIdx.x];
+  ends_l2_body(J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1, md.b1, md.W2, md.b2, md.h, md.C, J.sp_y);
+}
+
+// Main pass of the jobs that do not take the one-thread-per-coalition kernel.
 template <int FPT>
 __global__ void __launch_bounds__(256) k_eval_l2_batch(const gnnshap::EvalJob* __restrict__ jobs,
-                                                       gnnshap::EvalModel md, bool special, int tbr) {
+                                                       gnnshap::EvalModel md, int tbr) {
   const gnnshap::EvalJob J = jobs[blockIdx.y];
-  if (special)
-    eval_l2_body<FPT>(J.sp_masks, J.wpr, J.sp_rows, 0, 2, nullptr, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1,
-                      md.b1, md.W2, md.b2, md.h, md.C, J.ctl, true, tbr, nullptr, J.sp_y, blockIdx.x);
-  else if (!J.rows_ok)
+  if (!J.rows_ok)
     eval_l2_body<FPT>(J.masks, J.wpr, J.live_rows, 0, J.k, J.ctl + 1, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1,
                       md.b1, md.W2, md.b2, md.h, md.C, J.ctl, false, tbr, J.y, J.sp_y, blockIdx.x);
 }
@@ -1061,7 +1168,14 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
     }
   }
   // f(empty) and f(E_c) for every class, then the explained class.
-  if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
+  if (ends_ok(sh)) {
+    k_eval_ends<<<1, kEndsThreads, ends_lds_bytes(sh.n_dst, sh.nd[1], sh.dims[1], sh.dims[2]), s>>>(
+        sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], m->b ? m->b[0] : nullptr, m->W[1],
+        m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y);
+    GS_LAUNCHED();
+  } else if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) {
+    return st;
+  }
   k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
   GS_LAUNCHED();
   // Prediction pruning, then the live coalitions in passes of sh.tile rows.
@@ -1116,7 +1230,7 @@ bool gnnshap::eval_batchable(const gnnshap_subgraph* sg, const gnnshap_gcn* m, i
     return false;
   }
   return m->XW1 && m->W && m->W[1] && sh.L == 2 && sh.hops >= 2 && sh.tile >= k && k <= INT32_MAX &&
-         fused_l2_ok(sh, 2, true) && fused_l2_ok(sh, k, false);
+         ends_ok(sh) && fused_l2_ok(sh, k, false);
 }
 
 size_t gnnshap::eval_slice_bytes(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k) {
@@ -1152,27 +1266,27 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
   sh.nd[1] = max_n1;
   const int fpt = feature_split(md.h);
   const int tb_main = static_cast<int>(max_k < kTB ? max_k : kTB);
-  const size_t lds_sp = fused_lds_bytes(sh, 2, md.C, 8 * fpt);
+  const size_t lds_ends = ends_lds_bytes(max_ndst, max_n1, md.h, md.C);
   const size_t lds_main = fused_lds_bytes(sh, tb_main, 1, 8 * fpt);
-  if (lds_sp > 65536 || lds_main > 65536)
-    return fail(GNNSHAP_EUNSUPPORTED, "batched evaluation needs %zu bytes of LDS", std::max(lds_sp, lds_main));
+  if (lds_ends > 65536 || lds_main > 65536)
+    return fail(GNNSHAP_EUNSUPPORTED, "batched evaluation needs %zu bytes of LDS", std::max(lds_ends, lds_main));
   const unsigned nn = static_cast<unsigned>(n);
   k_init_batch<<<dim3(grid_for(max_wpr, 256, 64), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
   k_gather_batch<<<dim3(grid_for(max_nodes * md.h, 256, 2048), nn), 256, 0, s>>>(jobs, md.XW1, md.h);
   GS_LAUNCHED();
-#define GS_L2B(F, GRID, LDS, SPECIAL, TBR) k_eval_l2_batch<F><<<GRID, 256, LDS, s>>>(jobs, md, SPECIAL, TBR)
-#define GS_L2B_ALL(GRID, LDS, SPECIAL, TBR)            \
-  switch (fpt) {                                       \
-    case 1: GS_L2B(1, GRID, LDS, SPECIAL, TBR); break; \
-    case 2: GS_L2B(2, GRID, LDS, SPECIAL, TBR); break; \
-    case 4: GS_L2B(4, GRID, LDS, SPECIAL, TBR); break; \
-    case 8: GS_L2B(8, GRID, LDS, SPECIAL, TBR); break; \
-    default: GS_L2B(16, GRID, LDS, SPECIAL, TBR); break; \
+#define GS_L2B(F, GRID, LDS, TBR) k_eval_l2_batch<F><<<GRID, 256, LDS, s>>>(jobs, md, TBR)
+#define GS_L2B_ALL(GRID, LDS, TBR)            \
+  switch (fpt) {                              \
+    case 1: GS_L2B(1, GRID, LDS, TBR); break; \
+    case 2: GS_L2B(2, GRID, LDS, TBR); break; \
+    case 4: GS_L2B(4, GRID, LDS, TBR); break; \
+    case 8: GS_L2B(8, GRID, LDS, TBR); break; \
+    default: GS_L2B(16, GRID, LDS, TBR); break; \
   }
   {
-    GS_TIMED("k_eval_l2_batch", s);
-    GS_L2B_ALL(dim3(1, nn), lds_sp, true, 2);
+    GS_TIMED("k_eval_ends_batch", s);
+    k_eval_ends_batch<<<nn, kEndsThreads, ends_lds_bytes(max_ndst, max_n1, md.h, md.C), s>>>(jobs, md);
   }
   GS_LAUNCHED();
   k_pick_class_batch<<<nn, 1, 0, s>>>(jobs, md.C, md.target_class);
@@ -1181,7 +1295,7 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
   GS_LAUNCHED();
   if (rows_jobs < n) {
     GS_TIMED("k_eval_l2_batch", s);
-    GS_L2B_ALL(dim3(static_cast<unsigned>(ceil_div(max_k, tb_main)), nn), lds_main, false, tb_main);
+    GS_L2B_ALL(dim3(static_cast<unsigned>(ceil_div(max_k, tb_main)), nn), lds_main, tb_main);
   }
   GS_LAUNCHED();
   if (rows_jobs > 0) {

@@ -213,12 +213,24 @@ __global__ void __launch_bounds__(64) k_sample(gnnshap::SampleJob J, int64_t rpb
   sample_rows(J, r0, r0 + rpb);
 }
 
-// One job per blockIdx.y.
-__global__ void __launch_bounds__(64) k_sample_batch(const gnnshap::SampleJob* __restrict__ jobs, int64_t rpb) {
-  const gnnshap::SampleJob J = jobs[blockIdx.y];
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rpb;
-  if (r0 >= J.half) return;
-  sample_rows(J, r0, r0 + rpb);
+// Workgroup b takes rows [(b - blk0) rpb, + rpb) of the job with the largest
+// blk0 <= b, found by a wavefront-wide search of the job table.
+__global__ void __launch_bounds__(64) k_sample_batch(const gnnshap::SampleJob* __restrict__ jobs, int64_t n) {
+  const int64_t b = blockIdx.x;
+  const int lane = threadIdx.x;
+  int64_t lo = 0, hi = n;   // jobs[lo].blk0 <= b < jobs[hi].blk0 (jobs[n].blk0 = infinity)
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + 63) / 64;
+    const int64_t idx = lo + lane * step;
+    const bool ok = idx < hi && jobs[idx].blk0 <= b;
+    const uint64_t m = __ballot(ok);
+    const int64_t last = 63 - __clzll(static_cast<long long>(m));
+    lo += last * step;
+    hi = lo + step < hi ? lo + step : hi;
+  }
+  const gnnshap::SampleJob J = jobs[lo];
+  const int64_t r0 = (b - J.blk0) * J.rpb;
+  sample_rows(J, r0, r0 + J.rpb);
 }
 
 int check_plan(const gnnshap_sample_plan* plan) {
@@ -290,19 +302,31 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
   GS_TRY_END
 }
 
-int gnnshap::launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t max_half, int64_t max_wpr,
-                                 hipStream_t s) {
+int64_t gnnshap::plan_sample_batch(SampleJob* jobs, int64_t n) {
+  // A row costs about (16 + M) units: the draws and bitset work of its class
+  // size (up to M/2) and the words written.  Workgroups get ~1/65536 of the
+  // batch's cost each, between 1 and kBatchRows rows.
+  constexpr int64_t kBatchRows = 32;
+  double total = 0.0;
+  for (int64_t t = 0; t < n; ++t) total += static_cast<double>(jobs[t].half) * (16.0 + jobs[t].M);
+  const double per_block = total / 65536.0;
+  int64_t blk = 0;
+  for (int64_t t = 0; t < n; ++t) {
+    int64_t r = static_cast<int64_t>(per_block / (16.0 + jobs[t].M));
+    r = r < 1 ? 1 : (r > kBatchRows ? kBatchRows : r);
+    jobs[t].rpb = r;
+    jobs[t].blk0 = blk;
+    blk += ceil_div(jobs[t].half, r);
+  }
+  return blk;
+}
+
+int gnnshap::launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t blocks, int64_t max_wpr, hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
-  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  if (blocks > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "too many rows");
   const size_t lds = static_cast<size_t>(3 * 2 * max_wpr) * sizeof(uint32_t);
-  // at least 4096 workgroups over the batch
-  int64_t rpb = max_half * n / 4096;
-  rpb = rpb < 1 ? 1 : (rpb > kRowsPerBlock ? kRowsPerBlock : rpb);
-  const int64_t nblk = ceil_div(max_half, rpb);
-  if (nblk > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "too many rows");
-  const dim3 grid(static_cast<unsigned>(nblk), static_cast<unsigned>(n));
   GS_TIMED("k_sample_batch", s);
-  k_sample_batch<<<grid, 64, lds, s>>>(jobs, rpb);
+  k_sample_batch<<<static_cast<unsigned>(blocks), 64, lds, s>>>(jobs, n);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }

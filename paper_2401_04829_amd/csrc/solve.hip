@@ -1502,14 +1502,10 @@ int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class
   return GNNSHAP_OK;
 }
 
-int gnnshap::launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
-                                int64_t max_nrb, int64_t max_nch, hipStream_t s) {
+int gnnshap::launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
+                                  int64_t max_nrb, int64_t max_nch, hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
-  const size_t lds = kMidLds;
-  static bool raised = false;
-  if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
-    return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
   const unsigned nn = static_cast<unsigned>(n);
   if (max_nrb > 0) {
     {
@@ -1540,9 +1536,19 @@ int gnnshap::launch_solve_batch(const SolveJob* jobs, int64_t n, int64_t max_M, 
   GS_LAUNCHED();
   k_rhs_sum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M, 256)), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_solve_factor(const SolveJob* jobs, int64_t n, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  const size_t lds = kMidLds;
+  static bool raised = false;
+  if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
+    return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
   {
     GS_TIMED("k_solve_one_batch", s);
-    k_solve_one_batch<<<nn, kMidThreads, lds, s>>>(jobs);
+    k_solve_one_batch<<<static_cast<unsigned>(n), kMidThreads, lds, s>>>(jobs);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
