@@ -7,6 +7,8 @@
 // takes one step, lanes whose draw cannot interact with an earlier step of
 // the same chunk decide at once, the others are replayed in step order, so
 // the result is exactly the sequential algorithm's.
+#include <algorithm>
+
 #include "batch.h"
 #include "common.h"
 
@@ -199,6 +201,82 @@ __device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t
   }
 }
 
+// ---- one lane per row (M <= kLaneMaxPlayers) ----------------------------------------------
+//
+// Lane l builds row r0 + l in its own bitset (LDS word w of lane l at
+// lds[64 w + l]): an enumerated row unranks its lexicographic index, a
+// random row runs Floyd's algorithm step by step with the same Philox draws
+// as the wavefront version, so the rows are identical.  Lanes of one class
+// share the control flow.
+constexpr int64_t kLaneMaxPlayers = 512;
+
+size_t lane_lds_bytes(int64_t wpr) { return static_cast<size_t>(64 * 2 * wpr) * sizeof(uint32_t); }
+
+__device__ __forceinline__ void sample_lane_rows(const gnnshap::SampleJob& J, int64_t r0) {
+  const gnnshap_class* __restrict__ cls = J.cls;
+  const int64_t ncls = J.ncls, half = J.half, M = J.M, wpr = J.wpr;
+  extern __shared__ uint32_t lds[];
+  const int lane = threadIdx.x;
+  const int64_t i = r0 + lane;
+  if (i >= half) return;
+  uint32_t* B = lds + lane;              // this lane's bitset, stride 64 words
+  const int64_t nw = 2 * wpr;
+  for (int64_t w = 0; w < nw; ++w) B[w * 64] = 0;
+  int64_t lo = 0, hi = ncls - 1;         // the class of row i
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (cls[mid].row_begin <= i) lo = mid; else hi = mid - 1;
+  }
+  const gnnshap_class cur = cls[lo];
+  const int64_t c = cur.size;
+  const int64_t rank = i - cur.row_begin;
+  if (cur.full) {
+    // rank-th c-subset in lexicographic order, one position at a time
+    uint64_t q = static_cast<uint64_t>(rank);
+    int64_t x = 0;
+    for (int64_t jj = 1; jj <= c; ++jj) {
+      const int64_t r = c - jj;
+      const uint64_t top = binom(M - x, r + 1);
+      int64_t a = x, b = M - r - 1;
+      while (a < b) {
+        const int64_t mid = (a + b + 1) >> 1;
+        if (top - binom(M - mid, r + 1) <= q) a = mid; else b = mid - 1;
+      }
+      q -= top - binom(M - a, r + 1);
+      B[(a >> 5) * 64] |= 1u << (a & 31);
+      x = a + 1;
+    }
+  } else {
+    uint32_t d0 = 0, d1 = 0, d2 = 0, d3 = 0;
+    for (int64_t st = 0; st < c; ++st) {
+      if ((st & 3) == 0) {
+        d0 = static_cast<uint32_t>(st >> 2);
+        d1 = static_cast<uint32_t>(i);
+        d2 = J.st_lo;
+        d3 = J.st_hi;
+        philox4x32_10(d0, d1, d2, d3, J.seed_lo, J.seed_hi);
+      }
+      const int sel = static_cast<int>(st & 3);
+      const uint32_t u = sel == 0 ? d0 : sel == 1 ? d1 : sel == 2 ? d2 : d3;
+      const int64_t j = M - c + st;
+      const int64_t t = static_cast<int64_t>((static_cast<uint64_t>(u) * static_cast<uint64_t>(j + 1)) >> 32);
+      const bool in = (B[(t >> 5) * 64] >> (t & 31)) & 1u;
+      const int64_t ins = in ? j : t;
+      B[(ins >> 5) * 64] |= 1u << (ins & 31);
+    }
+  }
+  const uint64_t tail = (M & 63) ? ((uint64_t(1) << (M & 63)) - 1) : ~uint64_t(0);
+  for (int64_t w = 0; w < wpr; ++w) {
+    const uint64_t word = static_cast<uint64_t>(B[2 * w * 64]) | (static_cast<uint64_t>(B[(2 * w + 1) * 64]) << 32);
+    const uint64_t valid = (w == wpr - 1) ? tail : ~uint64_t(0);
+    J.masks[i * wpr + w] = word;
+    J.masks[(i + half) * wpr + w] = ~word & valid;
+  }
+  const float wt = static_cast<float>(cur.weight);
+  J.weights[i] = wt;
+  J.weights[i + half] = wt;
+}
+
 // Consecutive representative rows per wavefront: enough workgroups to fill
 // the GPU several times over, at most kRowsPerBlock rows each.
 constexpr int64_t kRowsPerBlock = 16;
@@ -211,6 +289,10 @@ int64_t rows_per_block(int64_t half) {
 __global__ void __launch_bounds__(64) k_sample(gnnshap::SampleJob J, int64_t rpb) {
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * rpb;
   sample_rows(J, r0, r0 + rpb);
+}
+
+__global__ void __launch_bounds__(64) k_sample_lane(gnnshap::SampleJob J) {
+  sample_lane_rows(J, static_cast<int64_t>(blockIdx.x) * 64);
 }
 
 // Workgroup b takes rows [(b - blk0) rpb, + rpb) of the job with the largest
@@ -230,7 +312,8 @@ __global__ void __launch_bounds__(64) k_sample_batch(const gnnshap::SampleJob* _
   }
   const gnnshap::SampleJob J = jobs[lo];
   const int64_t r0 = (b - J.blk0) * J.rpb;
-  sample_rows(J, r0, r0 + J.rpb);
+  if (J.M <= kLaneMaxPlayers) sample_lane_rows(J, r0);
+  else sample_rows(J, r0, r0 + J.rpb);
 }
 
 int check_plan(const gnnshap_sample_plan* plan) {
@@ -284,6 +367,18 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
   GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class),
                         hipMemcpyHostToDevice, s));
   const int64_t wpr = plan->words_per_row;
+  if (M <= kLaneMaxPlayers) {
+    const int64_t nblk = gnnshap::ceil_div(half, 64);
+    if (nblk > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "too many rows");
+    GS_TIMED("k_sample", s);
+    const gnnshap::SampleJob job{w.classes, plan->num_classes, half, M, wpr,
+                                 static_cast<uint32_t>(plan->seed), static_cast<uint32_t>(plan->seed >> 32),
+                                 static_cast<uint32_t>(plan->stream_id),
+                                 static_cast<uint32_t>(plan->stream_id >> 32), masks, weights, 0, 64};
+    k_sample_lane<<<static_cast<unsigned>(nblk), 64, lane_lds_bytes(wpr), s>>>(job);
+    GS_LAUNCHED();
+    return GNNSHAP_OK;
+  }
   const size_t lds = static_cast<size_t>(3 * 2 * wpr) * sizeof(uint32_t);
   const int64_t rpb = rows_per_block(half);
   const int64_t nblk = gnnshap::ceil_div(half, rpb);
@@ -307,13 +402,17 @@ int64_t gnnshap::plan_sample_batch(SampleJob* jobs, int64_t n) {
   // size (up to M/2) and the words written.  Workgroups get ~1/65536 of the
   // batch's cost each, between 1 and kBatchRows rows.
   constexpr int64_t kBatchRows = 32;
+  // Jobs of at most kLaneMaxPlayers players take one lane per row, 64 rows
+  // per workgroup.
   double total = 0.0;
-  for (int64_t t = 0; t < n; ++t) total += static_cast<double>(jobs[t].half) * (16.0 + jobs[t].M);
+  for (int64_t t = 0; t < n; ++t)
+    if (jobs[t].M > kLaneMaxPlayers) total += static_cast<double>(jobs[t].half) * (16.0 + jobs[t].M);
   const double per_block = total / 65536.0;
   int64_t blk = 0;
   for (int64_t t = 0; t < n; ++t) {
     int64_t r = static_cast<int64_t>(per_block / (16.0 + jobs[t].M));
     r = r < 1 ? 1 : (r > kBatchRows ? kBatchRows : r);
+    if (jobs[t].M <= kLaneMaxPlayers) r = 64;
     jobs[t].rpb = r;
     jobs[t].blk0 = blk;
     blk += ceil_div(jobs[t].half, r);
@@ -324,7 +423,8 @@ int64_t gnnshap::plan_sample_batch(SampleJob* jobs, int64_t n) {
 int gnnshap::launch_sample_batch(const SampleJob* jobs, int64_t n, int64_t blocks, int64_t max_wpr, hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
   if (blocks > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "too many rows");
-  const size_t lds = static_cast<size_t>(3 * 2 * max_wpr) * sizeof(uint32_t);
+  const size_t lds = std::max(static_cast<size_t>(3 * 2 * max_wpr) * sizeof(uint32_t),
+                              lane_lds_bytes(std::min<int64_t>(max_wpr, kLaneMaxPlayers / 64)));
   GS_TIMED("k_sample_batch", s);
   k_sample_batch<<<static_cast<unsigned>(blocks), 64, lds, s>>>(jobs, n);
   GS_LAUNCHED();
