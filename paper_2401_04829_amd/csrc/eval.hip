@@ -542,14 +542,17 @@ __device__ __forceinline__ void eval_l2_body(
 // Main pass of the two-layer evaluation with one thread per coalition, for
 // narrow hidden layers (h <= H): a block of kRowsPerBlock coalitions stages
 // what they all read (each player's source and Z^1 row, Z^1 of H_1, the
-// destinations' player ranges) in LDS once; per coalition the degrees, layer
-// 1 at every node of H_1 folded into the explained logit, and layer 2 at the
-// target then run from registers and LDS without further barriers.
+// destinations' player ranges) in LDS once; per coalition the in-degrees of
+// the destinations (16-bit counts in LDS), then layer 1 at every node x of
+// H_1 folded into the explained logit and, as x goes, layer 2 at the target:
+// node x >= 1 of H_1 is the source of the target's player x - 1 (local ids
+// sort the in-neighbours by global id, as the players entering the target).
 constexpr int kRowsPerBlock = 128;
 
 size_t rows_lds_bytes(int64_t n_dst, int64_t n1, int64_t M, int H) {
-  return sizeof(float) * static_cast<size_t>(M * H + n1 * H + kRowsPerBlock * (n_dst + n1)) +
-         sizeof(int32_t) * static_cast<size_t>(M + n_dst + 1);
+  return sizeof(float) * static_cast<size_t>(M * H + n1 * H) +
+         sizeof(uint16_t) * static_cast<size_t>(kRowsPerBlock * n_dst) +
+         sizeof(int32_t) * static_cast<size_t>(M + n_dst + 1) + 16;
 }
 
 template <int H>
@@ -563,10 +566,9 @@ __device__ __forceinline__ void eval_rows_body(
   extern __shared__ __align__(16) float sm[];
   float* zall = sm;                                            // M x H
   float* zself = zall + M * H;                                 // n1 x H
-  float* dinv = zself + n1 * H;                                // n_dst x R
-  float* tt = dinv + n_dst * R;                                // n1 x R
-  int32_t* sall = reinterpret_cast<int32_t*>(tt + n1 * R);     // M
+  int32_t* sall = reinterpret_cast<int32_t*>(zself + n1 * H);  // M
   int32_t* dptr = sall + M;                                    // n_dst + 1
+  uint16_t* deg = reinterpret_cast<uint16_t*>(dptr + n_dst + 1);  // n_dst x R
   const int64_t nr = rows_in_pass(dyn_count, 0, cap);
   const int64_t b0 = block * R;
   if (b0 >= nr) return;
@@ -590,7 +592,7 @@ __device__ __forceinline__ void eval_rows_body(
   }
   const int64_t row = valid ? static_cast<int64_t>(rows[b]) : 0;
   const uint64_t* mrow = masks + row * wpr;
-  // degrees of every destination under this coalition
+  // in-degree of every destination under this coalition
   for (int64_t x = 0; x < n_dst; ++x) {
     const int64_t e0 = dptr[x], e1 = dptr[x + 1];
     int cnt = 0;
@@ -601,7 +603,7 @@ __device__ __forceinline__ void eval_rows_body(
       if (e1 < lo + 64) word &= (uint64_t(1) << (e1 - lo)) - 1;
       cnt += __popcll(word);
     }
-    dinv[x * R + tid] = rsqrtf(1.0f + static_cast<float>(cnt));
+    deg[x * R + tid] = static_cast<uint16_t>(cnt);
   }
   float w2v[H], b1v[H];
 #pragma unroll
@@ -610,7 +612,9 @@ __device__ __forceinline__ void eval_rows_body(
     b1v[i] = (b1 && i < h) ? b1[i] : 0.f;
   }
   __syncthreads();
-  // layer 1 at every node of H_1, folded into the explained logit
+  auto dinv = [&](int64_t x) { return rsqrtf(1.0f + static_cast<float>(deg[x * R + tid])); };
+  // layer 1 at every node of H_1, folded into the explained logit; layer 2 alongside
+  float acc2 = 0.f, t0 = 0.f;
   for (int64_t x = 0; x < n1; ++x) {
     const int64_t e0 = dptr[x], e1 = dptr[x + 1];
     float acc[H];
@@ -625,7 +629,7 @@ __device__ __forceinline__ void eval_rows_body(
         const int64_t e = lo + __ffsll(static_cast<long long>(bits)) - 1;
         bits &= bits - 1;
         const int32_t u = sall[e];
-        const float coef = u < n_dst ? dinv[u * R + tid] : 1.0f;
+        const float coef = u < n_dst ? dinv(u) : 1.0f;
         const float* z = zall + e * H;
 #pragma unroll
         for (int i = 0; i < H; i += 4) {
@@ -637,26 +641,23 @@ __device__ __forceinline__ void eval_rows_body(
         }
       }
     }
-    const float dx = dinv[x * R + tid];
+    const float dx = dinv(x);
     float p = 0.f;
 #pragma unroll
     for (int i = 0; i < H; ++i) {
       const float hv = i < h ? fmaxf(dx * (acc[i] + dx * zself[x * H + i]) + b1v[i], 0.f) : 0.f;
       p += hv * w2v[i];
     }
-    tt[x * R + tid] = p;
+    if (x == 0) {
+      t0 = p;
+    } else if ((mrow[(x - 1) >> 6] >> ((x - 1) & 63)) & 1) {
+      acc2 += dx * p;
+    }
   }
   // layer 2 at the target
-  const int64_t indeg = dptr[1];
-  const float dv = dinv[tid];
-  float acc = 0.f;
-  for (int64_t e = 0; e < indeg; ++e) {
-    if (!((mrow[e >> 6] >> (e & 63)) & 1)) continue;
-    const int32_t u = sall[e];
-    acc += dinv[u * R + tid] * tt[u * R + tid];
-  }
-  acc += dv * tt[tid];
-  if (valid) y_rows[row] = dv * acc + (b2 ? b2[c0] : 0.f);
+  const float dv = dinv(0);
+  acc2 += dv * t0;
+  if (valid) y_rows[row] = dv * acc2 + (b2 ? b2[c0] : 0.f);
 }
 
 template <int H>

@@ -442,9 +442,9 @@ __device__ __forceinline__ void chol_inv8(float* S, float* Wb, int64_t o, int32_
     for (int q = 0; q < k; ++q) piv -= a[k][q] * a[k][q];
     const bool ok = piv > 0.f;
     bad = (bad == 0 && !ok) ? k + 1 : bad;
-    const float d = sqrtf(ok ? piv : 1.f);
-    rd[k] = 1.0f / d;
-    a[k][k] = d;
+    const float pv = ok ? piv : 1.f;
+    rd[k] = __builtin_amdgcn_rsqf(pv);     // 1/sqrt, within 1 ulp
+    a[k][k] = pv * rd[k];
 #pragma unroll
     for (int i = k + 1; i < 8; ++i) {
       float t = a[i][k];
@@ -480,6 +480,26 @@ __device__ __forceinline__ void chol_inv8(float* S, float* Wb, int64_t o, int32_
   Wb[r * kHP + c] = wv;
   __builtin_amdgcn_wave_barrier();
   if (bad != 0 && lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + bad));
+}
+
+// One wavefront, 16 x 16 blocks: the same product as four fp32 MFMA 16x16x4.
+template <bool kNT>
+__device__ __forceinline__ void prod16(float* D, const float* X, const float* Y, float alpha, float beta) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, rl = lane & 15;
+  f32x4 acc = {};
+#pragma unroll
+  for (int k0 = 0; k0 < 16; k0 += 4) {
+    const float av = X[rl * kHP + k0 + g];
+    const float bv = kNT ? Y[rl * kHP + k0 + g] : Y[(k0 + g) * kHP + rl];
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float* d = D + (4 * g + r) * kHP + rl;
+    *d = beta == 0.f ? alpha * acc[r] : beta * *d + alpha * acc[r];
+  }
+  __builtin_amdgcn_wave_barrier();
 }
 
 // One wavefront, H x H blocks (H = 8 or 16): D = alpha op(X, Y) + beta D,
@@ -540,6 +560,7 @@ __device__ __forceinline__ void prod32(float* D, const float* X, const float* Y,
 template <int H, bool kNT>
 __device__ __forceinline__ void prod_h(float* D, const float* X, const float* Y, float alpha, float beta) {
   if constexpr (H == 32) prod32<kNT>(D, X, Y, alpha, beta);
+  else if constexpr (H == 16) prod16<kNT>(D, X, Y, alpha, beta);
   else prod_small<H, kNT>(D, X, Y, alpha, beta);
 }
 
