@@ -81,6 +81,8 @@ struct SolveJob {
   double* dv;
   double* scal;
   float* Wd;
+  float* rv;                 // M: right-hand side, then z, then psi (panel path)
+  int32_t panel;             // 1: the panel path, 0: one workgroup
 };
 // Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
 bool solve_batchable(const gnnshap_sample_plan* plan);
@@ -90,6 +92,10 @@ int solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes
 // (multi-block kernels), then one workgroup per system.
 int launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
                          int64_t max_nrb, int64_t max_nch, hipStream_t s);
-int launch_solve_factor(const SolveJob* jobs, int64_t n, hipStream_t s);
+// max_panels: the most 64-player panels of a job above the panel-path size
+// (0 if none); small: whether some job takes the one-workgroup kernel.
+int launch_solve_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, bool small, hipStream_t s);
+// Whether a one-workgroup-size system takes the panel path.
+bool solve_panel_path(const gnnshap_sample_plan* plan);
 
 }  // namespace gnnshap

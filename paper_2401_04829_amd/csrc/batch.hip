@@ -5,8 +5,6 @@
 // does not fit the batched kernels go through the single-target calls inside
 // the same sequence; every value is the one the single-target calls give.
 #include <algorithm>
-#include <cstdio>
-#include <cstdlib>
 #include <vector>
 
 #include "batch.h"
@@ -52,16 +50,6 @@ SideStream* side_stream(int i) {
 }  // namespace gnnshap
 
 namespace {
-
-// Panels (64 players each) from which a one-workgroup system joins group 0,
-// given the largest system's panel count; 0 = one group.
-int64_t split_cut(int64_t max_panels) {
-  if (const char* e = getenv("GS_CUT")) {
-    const long long c = atoll(e);
-    return c < 0 ? max_panels + c : c;
-  }
-  return max_panels >= 4 ? max_panels - 2 : 0;
-}
 
 struct Layout {
   int64_t n = 0, classes = 0;
@@ -122,25 +110,18 @@ BatchWs carve(gnnshap::Carver& c, const Layout& L) {
 
 // The target order (group 0 first, each group in target order) and the
 // group boundaries: group g = order[bound[g], bound[g+1]).  Group 0 holds the
-// one-workgroup systems of at least split_cut() panels, group 1 the rest.
+// systems that take the panel path, group 1 the rest; a batch with only one
+// kind runs as one group.
 void split_groups(const gnnshap_sample_plan* plans, int64_t n, std::vector<int64_t>* order, int64_t bound[3]) {
-  int64_t max_panels = 0;
-  for (int64_t t = 0; t < n; ++t)
-    if (gnnshap::solve_batchable(&plans[t]))
-      max_panels = std::max<int64_t>(max_panels, (plans[t].num_players + 63) / 64);
-  const int64_t cut = split_cut(max_panels);
-  auto group_of = [&](int64_t t) -> int {
-    return cut > 0 && gnnshap::solve_batchable(&plans[t]) && (plans[t].num_players + 63) / 64 >= cut ? 0 : 1;
-  };
   order->clear();
   order->reserve(n);
   bound[0] = 0;
   for (int g = 0; g < 2; ++g) {
     for (int64_t t = 0; t < n; ++t)
-      if (group_of(t) == g) order->push_back(t);
+      if ((gnnshap::solve_panel_path(&plans[t]) ? 0 : 1) == g) order->push_back(t);
     bound[g + 1] = static_cast<int64_t>(order->size());
   }
-  if (bound[1] == n) bound[1] = 0;   // everything large: one group
+  if (bound[1] == n) bound[1] = 0;   // only panel-path systems: one group
 }
 
 }  // namespace
@@ -187,8 +168,8 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     }
     if (row != plans[t].num_rows / 2) return gnnshap::fail(GNNSHAP_EINVAL, "class table of target %lld short", (long long)t);
   }
-  // Targets run in two groups when their systems differ much in size: the
-  // largest one-workgroup systems (whose factorisations set the length of the
+  // Targets run in two groups when both kinds of systems are present: the
+  // largest ones (panel path, whose factorisations set the length of the
   // whole sequence) and their sampling and evaluation on a side stream, the
   // rest on `stream`, each step launched for both groups before the next, so
   // that the long factorisations overlap the other group's work.
@@ -216,6 +197,8 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     size_t rows_lds = 0;
     int64_t solve_begin = 0, solve_count = 0;        // range of the solve job table
     int64_t bM = 0, bw = 0, bh = 0, bnrb = 0, bnch = 0;
+    int64_t max_panels = 0;                          // of the panel-path systems
+    bool small = false;                              // some one-workgroup system
     std::vector<int64_t> rest;                       // targets solved one by one
   } grp[2];
   for (int g = 0; g < 2; ++g) {
@@ -291,6 +274,8 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       G.bh = std::max(G.bh, J.half);
       G.bnrb = std::max(G.bnrb, J.nrb);
       G.bnch = std::max(G.bnch, J.nch);
+      if (gnnshap::solve_panel_path(&p)) G.max_panels = std::max(G.max_panels, gnnshap::ceil_div(J.M, 64));
+      else G.small = true;
       vj[nv++] = J;
     }
     G.solve_count = nv - G.solve_begin;
@@ -349,7 +334,9 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
   for (int gi = 0; gi < 2; ++gi) {
     const Group& G = grp[gi];
     if (G.solve_count > 0)
-      if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, gs[gi])) return st;
+      if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, G.max_panels, G.small,
+                                                gs[gi]))
+        return st;
     for (int64_t t : G.rest) {
       if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
                                      f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],

@@ -35,6 +35,7 @@ constexpr int kTB = 64;        // diagonal block of the triangular solves (one w
 constexpr int64_t kSeg = 256;  // segment of the triangular solves (its triangle in LDS)
 constexpr int kMaxChunks = 256;
 constexpr int kMidMax = 448;   // largest system of the global-memory one-workgroup path
+constexpr int64_t kPanelMin = 256;  // larger systems (up to kMidMax) take the panel path
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -1279,8 +1280,245 @@ __global__ void __launch_bounds__(256) k_build_batch(const gnnshap::SolveJob* __
 // One workgroup per job.
 __global__ void __launch_bounds__(kMidThreads) k_solve_one_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.x];
+  if (J.panel) return;
   solve_mid_body(reinterpret_cast<float*>(J.counts), J.ld, J.M, J.dv, J.fef, J.Wd, J.info, J.phi);
 }
+
+// ---- panel path (kPanelMin < M <= kMidMax): one launch per panel step -----------------------
+//
+// The same blocked factorisation as the one-workgroup path (64-wide panels,
+// diagonal factors inverted, L_Ip = A_Ip W_pp^T, forward substitution
+// alongside), spread over many small workgroups: per panel p, one workgroup
+// per block below the diagonal forms L_Ip and updates r_I; then one
+// workgroup per trailing tile (I, J) subtracts L_Ip L_Jp^T, and the one
+// holding the next diagonal block factors and inverts it right away.  The
+// largest systems of a batch thus finish in ~20 us per panel instead of
+// occupying one compute unit for their whole factorisation.
+
+constexpr size_t kPanelLds = (3 * kHB + 64) * sizeof(float);
+
+// rv <- P dv (the centred right-hand side, fp32), info <- 0.  One workgroup.
+__device__ __forceinline__ void pp_centre(const double* __restrict__ dvg, int64_t M, float* __restrict__ rv,
+                                          int32_t* info) {
+  __shared__ double red[4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (tid == 0) *info = 0;
+  double sv = 0.0;
+  for (int64_t i = tid; i < M; i += 256) sv += dvg[i];
+  for (int off = 32; off > 0; off >>= 1) sv += __shfl_xor(sv, off);
+  if (lane == 0) red[wave] = sv;
+  __syncthreads();
+  const double mean = (red[0] + red[1] + red[2] + red[3]) / static_cast<double>(M);
+  for (int64_t i = tid; i < M; i += 256) rv[i] = static_cast<float>(dvg[i] - mean);
+  __syncthreads();
+}
+
+// Diagonal block p already in D0 (lower part; rows and columns past M zero):
+// D0 <- L_pp, D1 <- W_pp = L_pp^-1, stored to G and Wd[p]; r_p <- z_p = W_pp r_p.
+__device__ __forceinline__ void pp_diag(float* G, int64_t ld, int64_t M, int64_t p, float* D0, float* D1,
+                                        float* __restrict__ Wd, float* rv, int32_t* info, float* vec) {
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const int64_t o = p * 64;
+  if (tid < 64) {
+    if (o + tid >= M) D0[tid * kHP + tid] = 1.f;   // identity past M
+    vec[tid] = o + tid < M ? rv[o + tid] : 0.f;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    chol_inv64(D0, D1, nullptr, o, info);
+    const int lane = tid;
+    float z = 0.f;
+#pragma unroll 8
+    for (int c = 0; c < 64; ++c) z += D1[lane * kHP + c] * vec[c];
+    if (o + lane < M) rv[o + lane] = z;
+  }
+  __syncthreads();
+  for (int t = tid; t < 64 * 64; t += 256) {
+    const int r = t >> 6, c = t & 63;
+    if (o + r < M && c <= r) G[(o + r) * ld + o + c] = D0[r * kHP + c];
+    Wd[p * 4096 + t] = D1[r * kHP + c];
+  }
+}
+
+// Block (bi, bj) (64 x 64 at rows 64 bi, columns 64 bj) of G into S, zero past M;
+// all sixteen loads of a thread are in flight before the LDS stores.
+__device__ __forceinline__ void pp_load(const float* G, int64_t ld, int64_t M, int64_t bi, int64_t bj, float* S,
+                                        bool lower_only) {
+  const int tid = threadIdx.x;
+  float v[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int t = tid + 256 * q, r = t >> 6, c = t & 63;
+    const int64_t gi = 64 * bi + r, gj = 64 * bj + c;
+    const bool ok = gi < M && gj < M && (!lower_only || c <= r);
+    v[q] = ok ? G[gi * ld + gj] : 0.f;
+  }
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int t = tid + 256 * q;
+    S[(t >> 6) * kHP + (t & 63)] = v[q];
+  }
+}
+
+// Start: centring, then the first diagonal block.
+__device__ __forceinline__ void pp_start_body(const gnnshap::SolveJob& J) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* D0 = reinterpret_cast<float*>(smem);
+  float* D1 = D0 + kHB;
+  float* G = reinterpret_cast<float*>(J.counts);
+  pp_centre(J.dv, J.M, J.rv, J.info);
+  pp_load(G, J.ld, J.M, 0, 0, D0, true);
+  pp_diag(G, J.ld, J.M, 0, D0, D1, J.Wd, J.rv, J.info, D1 + kHB);
+}
+
+// Panel p, block I below the diagonal (workgroup x): L_Ip = A_Ip W_pp^T, r_I -= L_Ip z_p.
+__device__ __forceinline__ void pp_column_body(const gnnshap::SolveJob& J, int64_t p, int64_t I) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int64_t M = J.M, nblk = (M + 63) / 64;
+  if (p + 1 + I >= nblk) return;
+  float* P = reinterpret_cast<float*>(smem);
+  float* D1 = P + kHB;
+  float* G = reinterpret_cast<float*>(J.counts);
+  const int tid = threadIdx.x;
+  const int64_t bi = p + 1 + I, o = p * 64;
+  float* zp = D1 + kHB;                          // z_p
+  {
+    float w[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) w[q] = J.Wd[p * 4096 + tid + 256 * q];
+    const float zv = tid < 64 ? J.rv[o + tid] : 0.f;   // o + 64 <= M here
+    pp_load(G, J.ld, M, bi, p, P, false);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int t = tid + 256 * q;
+      D1[(t >> 6) * kHP + (t & 63)] = w[q];
+    }
+    if (tid < 64) zp[tid] = zv;
+  }
+  __syncthreads();
+  mm64<true>(P, D1, P, 1.f, 0.f);
+  for (int t = tid; t < 64 * 64; t += 256) {
+    const int r = t >> 6, c = t & 63;
+    if (64 * bi + r < M) G[(64 * bi + r) * J.ld + o + c] = P[r * kHP + c];
+  }
+  if (tid < 64 && 64 * bi + tid < M) {
+    float sum = 0.f;
+#pragma unroll 8
+    for (int c = 0; c < 64; ++c) sum += P[tid * kHP + c] * zp[c];
+    J.rv[64 * bi + tid] -= sum;
+  }
+}
+
+// Panel p, trailing tile number `tile` (I >= J, row-major over the lower
+// triangle of the blocks below panel p): A_IJ -= L_Ip L_Jp^T; tile (0, 0) is
+// the next diagonal block and is factored at once.
+__device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_t p, int64_t tile) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int64_t M = J.M, nblk = (M + 63) / 64, nI = nblk - p - 1;
+  if (tile >= nI * (nI + 1) / 2) return;
+  int64_t I = 0;
+  while ((I + 1) * (I + 2) / 2 <= tile) ++I;
+  const int64_t Jb = tile - I * (I + 1) / 2;
+  float* A = reinterpret_cast<float*>(smem);
+  float* X = A + kHB;
+  float* Y = X + kHB;
+  float* G = reinterpret_cast<float*>(J.counts);
+  const int tid = threadIdx.x;
+  const int64_t bi = p + 1 + I, bj = p + 1 + Jb;
+  pp_load(G, J.ld, M, bi, bj, A, I == Jb);
+  pp_load(G, J.ld, M, bi, p, X, false);
+  if (I != Jb) pp_load(G, J.ld, M, bj, p, Y, false);
+  __syncthreads();
+  mm64<true>(X, I == Jb ? X : Y, A, -1.f, 1.f);
+  if (I == 0 && Jb == 0) {
+    pp_diag(G, J.ld, M, p + 1, A, X, J.Wd, J.rv, J.info, Y + kHB);
+    return;
+  }
+  for (int t = tid; t < 64 * 64; t += 256) {
+    const int r = t >> 6, c = t & 63;
+    const int64_t gi = 64 * bi + r, gj = 64 * bj + c;
+    if (gi < M && gj < M && (I != Jb || c <= r)) G[gi * J.ld + gj] = A[r * kHP + c];
+  }
+}
+
+// Backward substitution psi_p = W_pp^T (z_p - sum_I L_Ip^T psi_I) and phi =
+// Delta/M + psi; 1024 threads (64 columns x 16 row groups), z and psi in LDS.
+constexpr int kBackThreads = 1024;
+
+__device__ __forceinline__ void pp_back_body(const gnnshap::SolveJob& J) {
+  __shared__ float red[kBackThreads];
+  __shared__ float vec[kMidMax];
+  __shared__ float Wl[64 * 65];                  // W_pp of the current panel
+  const int64_t M = J.M, ld = J.ld, nblk = (M + 63) / 64;
+  const float* G = reinterpret_cast<const float*>(J.counts);
+  const int tid = threadIdx.x, c = tid & 63, g = tid >> 6;
+  constexpr int NG = kBackThreads / 64;
+  for (int64_t i = tid; i < M; i += kBackThreads) vec[i] = J.rv[i];
+  __syncthreads();
+  for (int64_t p = nblk - 1; p >= 0; --p) {
+    const int64_t o = p * 64;
+    float wv[4096 / kBackThreads];
+#pragma unroll
+    for (int q = 0; q < 4096 / kBackThreads; ++q) wv[q] = J.Wd[p * 4096 + tid + kBackThreads * q];
+    float acc = 0.f;
+    if (o + c < M) {
+#pragma unroll 4
+      for (int64_t row = o + 64 + g; row < M; row += NG) acc += G[row * ld + o + c] * vec[row];
+    }
+    red[g * 64 + c] = acc;
+#pragma unroll
+    for (int q = 0; q < 4096 / kBackThreads; ++q) {
+      const int t = tid + kBackThreads * q;
+      Wl[(t >> 6) * 65 + (t & 63)] = wv[q];
+    }
+    __syncthreads();
+    float t = 0.f;
+    if (tid < 64) {
+      float sum = 0.f;
+#pragma unroll
+      for (int gg = 0; gg < NG; ++gg) sum += red[gg * 64 + tid];
+      t = o + tid < M ? vec[o + tid] - sum : 0.f;
+    }
+    __syncthreads();
+    if (tid < 64) red[tid] = t;
+    __syncthreads();
+    if (tid < 64) {
+      float ps = 0.f;
+#pragma unroll 8
+      for (int cc = tid; cc < 64; ++cc) ps += Wl[cc * 65 + tid] * red[cc];
+      if (o + tid < M) vec[o + tid] = ps;
+    }
+    __syncthreads();
+  }
+  const double delta = static_cast<double>(J.fef[1]) - static_cast<double>(J.fef[0]);
+  const double Md = static_cast<double>(M);
+  for (int64_t i = tid; i < M; i += kBackThreads) J.phi[i] = static_cast<float>(delta / Md + static_cast<double>(vec[i]));
+}
+
+__global__ void __launch_bounds__(256) k_pp_start(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.x];
+  if (J.panel) pp_start_body(J);
+}
+__global__ void __launch_bounds__(256) k_pp_column(const gnnshap::SolveJob* __restrict__ jobs, int64_t p) {
+  const gnnshap::SolveJob J = jobs[blockIdx.y];
+  if (J.panel) pp_column_body(J, p, blockIdx.x);
+}
+__global__ void __launch_bounds__(256) k_pp_trail(const gnnshap::SolveJob* __restrict__ jobs, int64_t p) {
+  const gnnshap::SolveJob J = jobs[blockIdx.y];
+  if (J.panel) pp_trail_body(J, p, blockIdx.x);
+}
+__global__ void __launch_bounds__(kBackThreads) k_pp_back(const gnnshap::SolveJob* __restrict__ jobs) {
+  const gnnshap::SolveJob J = jobs[blockIdx.x];
+  if (J.panel) pp_back_body(J);
+}
+__global__ void __launch_bounds__(256) k_pp_start_one(gnnshap::SolveJob J) { pp_start_body(J); }
+__global__ void __launch_bounds__(256) k_pp_column_one(gnnshap::SolveJob J, int64_t p) {
+  pp_column_body(J, p, blockIdx.x);
+}
+__global__ void __launch_bounds__(256) k_pp_trail_one(gnnshap::SolveJob J, int64_t p) {
+  pp_trail_body(J, p, blockIdx.x);
+}
+__global__ void __launch_bounds__(kBackThreads) k_pp_back_one(gnnshap::SolveJob J) { pp_back_body(J); }
 
 // Whether `kernel` may be launched with `bytes` of dynamic LDS on the current
 // device (its static LDS counts against the same limit); above the 64 KiB
@@ -1387,6 +1625,41 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     const int64_t nbm = gnnshap::ceil_div(M, 256);
     k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch, M, w.dv, w.bsum);
     GS_LAUNCHED();
+    if (gnnshap::solve_panel_path(plan)) {
+      gnnshap::SolveJob J{};
+      J.panel = 1;
+      J.counts = counts;
+      J.ld = ld;
+      J.M = M;
+      J.dv = w.dv;
+      J.rv = w.rhs;
+      J.Wd = w.Wd;
+      J.fef = f_empty_full;
+      J.phi = phi;
+      J.info = info;
+      const int64_t nblk = gnnshap::ceil_div(M, 64);
+      {
+        GS_TIMED("k_pp_start", s);
+        k_pp_start_one<<<1, 256, kPanelLds, s>>>(J);
+      }
+      GS_LAUNCHED();
+      for (int64_t p = 0; p + 1 < nblk; ++p) {
+        const int64_t nI = nblk - p - 1;
+        {
+          GS_TIMED("k_pp_column", s);
+          k_pp_column_one<<<static_cast<unsigned>(nI), 256, kPanelLds, s>>>(J, p);
+        }
+        GS_LAUNCHED();
+        {
+          GS_TIMED("k_pp_trail", s);
+          k_pp_trail_one<<<static_cast<unsigned>(nI * (nI + 1) / 2), 256, kPanelLds, s>>>(J, p);
+        }
+        GS_LAUNCHED();
+      }
+      k_pp_back_one<<<1, kBackThreads, 0, s>>>(J);
+      GS_LAUNCHED();
+      return GNNSHAP_OK;
+    }
     {
       GS_TIMED("k_solve_mid", s);
       k_solve_mid<<<1, kMidThreads, kMidLds, s>>>(w.G, ld, M, w.dv, f_empty_full, w.Wd, info, phi);
@@ -1519,8 +1792,14 @@ int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class
   job->usum = w.usum;
   job->dv = w.dv;
   job->Wd = w.Wd;
+  job->rv = w.rhs;
+  job->panel = solve_panel_path(plan) ? 1 : 0;
   job->scal = w.scal;
   return GNNSHAP_OK;
+}
+
+bool gnnshap::solve_panel_path(const gnnshap_sample_plan* plan) {
+  return solve_batchable(plan) && plan->num_players > kPanelMin;
 }
 
 int gnnshap::launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
@@ -1560,16 +1839,39 @@ int gnnshap::launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M
   return GNNSHAP_OK;
 }
 
-int gnnshap::launch_solve_factor(const SolveJob* jobs, int64_t n, hipStream_t s) {
+int gnnshap::launch_solve_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, bool small, hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
-  const size_t lds = kMidLds;
-  static bool raised = false;
-  if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
-    return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
-  {
+  const unsigned nn = static_cast<unsigned>(n);
+  if (max_panels > 0) {
+    {
+      GS_TIMED("k_pp_start", s);
+      k_pp_start<<<nn, 256, kPanelLds, s>>>(jobs);
+    }
+    GS_LAUNCHED();
+    for (int64_t p = 0; p + 1 < max_panels; ++p) {
+      const int64_t nI = max_panels - p - 1;
+      {
+        GS_TIMED("k_pp_column", s);
+        k_pp_column<<<dim3(static_cast<unsigned>(nI), nn), 256, kPanelLds, s>>>(jobs, p);
+      }
+      GS_LAUNCHED();
+      {
+        GS_TIMED("k_pp_trail", s);
+        k_pp_trail<<<dim3(static_cast<unsigned>(nI * (nI + 1) / 2), nn), 256, kPanelLds, s>>>(jobs, p);
+      }
+      GS_LAUNCHED();
+    }
+    k_pp_back<<<nn, kBackThreads, 0, s>>>(jobs);
+    GS_LAUNCHED();
+  }
+  if (small) {
+    const size_t lds = kMidLds;
+    static bool raised = false;
+    if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
+      return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
     GS_TIMED("k_solve_one_batch", s);
-    k_solve_one_batch<<<static_cast<unsigned>(n), kMidThreads, lds, s>>>(jobs);
+    k_solve_one_batch<<<nn, kMidThreads, lds, s>>>(jobs);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
@@ -1580,6 +1882,6 @@ extern "C" int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path
   if (!path) return gnnshap::fail(GNNSHAP_EINVAL, "path is NULL");
   if (int st = check_plan(plan, nullptr)) return st;
   const int64_t M = plan->num_players;
-  *path = M <= kMidMax ? 1 : 0;
+  *path = M > kMidMax ? 0 : (gnnshap::solve_panel_path(plan) ? 2 : 1);
   return GNNSHAP_OK;
 }
