@@ -76,8 +76,9 @@ def work_model(kernel, results, dims):
 
     k_solve_mid / k_solve_one_batch (one-workgroup solves)
                    M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
-    k_eval_l2      (k/2) M h useful MACs per target (complement pairs cover every
-                   player-feature product once) + the layer-2 dot products
+    k_eval_l2, k_eval_rows
+                   (k/2) M h useful MACs per target (complement pairs cover every
+                   player-feature product once) + the layer-1 logit dot products
     k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
                    per 64 rows and pair
     k_sample       k x ceil(M/64) x 8 bytes of masks + 4 k bytes of weights written
@@ -92,18 +93,22 @@ def work_model(kernel, results, dims):
         M, k = r.plan.num_players, r.plan.num_rows
         wpr = r.plan.words_per_row
         kr = k // 2 - r.plan.random_begin
+        path = _lib.gnnshap_solve_info(r.plan)
+        batched = kernel.endswith("_batch")
         if base in ("k_solve_mid", "k_solve_one"):
-            if _lib.gnnshap_solve_info(r.plan) == 1:
+            if path == 1:
                 tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
-        elif base == "k_eval_l2":
+        elif base in ("k_eval_l2", "k_eval_rows"):
             n1 = r.sub.sg.hop_ptr[2]
             tot += 2.0 * ((k / 2.0) * M * h + k * n1 * h)
         elif base == "k_gram":
-            tot += (kr / 64.0) * M * (M + 1) / 2.0
+            if not batched or path in (1, 2):
+                tot += (kr / 64.0) * M * (M + 1) / 2.0
         elif base == "k_sample":
             tot += k * wpr * 8.0 + 4.0 * k
         elif base == "k_rhs_part":
-            tot += (k / 2.0) * wpr * 8.0 + 4.0 * k
+            if not batched or path in (1, 2):
+                tot += (k / 2.0) * wpr * 8.0 + 4.0 * k
     if base in ("k_sample", "k_rhs_part"):
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
     if base == "k_gram":
@@ -112,7 +117,8 @@ def work_model(kernel, results, dims):
 
 
 CANDIDATES = {
-    "batch": ["k_solve_one_batch", "k_eval_l2_batch", "k_rhs_part_batch", "k_gram_batch", "k_sample_batch"],
+    "batch": ["k_eval_rows_batch", "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_part_batch",
+              "k_sample_batch"],
     "streams": ["k_solve_mid", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
 }
 

@@ -204,8 +204,9 @@ int gnnshap_transform_features(const float* X, int64_t n, int32_t d, const float
 int gnnshap_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_gcn* m,
                            int64_t k, size_t* bytes);
 
-/* y[b] = f(S_b) for b < k.  X is the [dev] feature matrix of the whole graph
- * (num_nodes x dims[0]).  target_class >= 0 selects the explained logit;
+/* y[b] = f(S_b) for b < k.  sg is a subgraph as gnnshap_extract_subgraph
+ * lays it out (its node and player order is relied on).  X is the [dev]
+ * feature matrix of the whole graph (num_nodes x dims[0]).  target_class >= 0 selects the explained logit;
  * -1 selects argmax_c f(E_c)[c] (ties to the lowest c), computed on the
  * device and written to *class_out if class_out is not NULL ([dev] int32).
  * f_empty_full[0] = f(empty), f_empty_full[1] = f(E_c) ([dev] 2 floats). */
