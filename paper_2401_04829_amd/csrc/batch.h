@@ -88,10 +88,13 @@ struct SolveJob {
 bool solve_batchable(const gnnshap_sample_plan* plan);
 size_t solve_slice_bytes(const gnnshap_sample_plan* plan);
 int solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice, SolveJob* job);
-// The solve of a batch in two launches sequences: G~ and the right-hand side
-// (multi-block kernels), then one workgroup per system.
-int launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
-                         int64_t max_nrb, int64_t max_nch, hipStream_t s);
+// The solve of a batch in three launch sequences: G~ from the masks alone
+// (it may run while the coalitions are evaluated), the right-hand side from
+// the values, then the factorisations.
+int launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_nrb,
+                        hipStream_t s);
+int launch_solve_rhs(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
+                     int64_t max_nch, hipStream_t s);
 // max_panels: the most 64-player panels of a job above the panel-path size
 // (0 if none); small: whether some job takes the one-workgroup kernel.
 int launch_solve_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, bool small, hipStream_t s);

@@ -15,7 +15,7 @@ namespace gnnshap {
 // Side streams of the current device for the calling thread, each with the
 // two events that fork work onto it and join it back (created on first use,
 // default priority, kept until the process ends).
-constexpr int kSideStreams = 2;
+constexpr int kSideStreams = 3;
 
 struct SideStream {
   hipStream_t stream = nullptr;
@@ -282,21 +282,34 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
   }
 
   GS_HIP(hipMemcpyAsync(ws, image.data(), front, hipMemcpyHostToDevice, s));
+  // Streams: group 0 runs on side stream 0, group 1 on `stream`; each
+  // group's G~ is built on a side stream of its own (2 for group 0, 1 for
+  // group 1) once its masks are sampled, while its coalitions are evaluated.
   hipStream_t gs[2] = {s, s};
-  gnnshap::SideStream* side = nullptr;
+  gnnshap::SideStream* mat[2] = {nullptr, nullptr};
+  gnnshap::SideStream* side0 = nullptr;
   if (grp[0].end > grp[0].begin) {
-    side = gnnshap::side_stream(0);
-    if (!side) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
-    GS_HIP(hipEventRecord(side->fork, s));
-    GS_HIP(hipStreamWaitEvent(side->stream, side->fork, 0));
-    gs[0] = side->stream;
+    side0 = gnnshap::side_stream(0);
+    if (!side0) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+    GS_HIP(hipEventRecord(side0->fork, s));
+    GS_HIP(hipStreamWaitEvent(side0->stream, side0->fork, 0));
+    gs[0] = side0->stream;
   }
-  // 1. sampling
+  for (int gi = 0; gi < 2; ++gi) {
+    if (grp[gi].solve_count == 0) continue;
+    mat[gi] = gnnshap::side_stream(gi == 0 ? 2 : 1);
+    if (!mat[gi]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+  }
+  // 1. sampling; the matrix streams wait for it
   for (int gi = 0; gi < 2; ++gi) {
     const Group& G = grp[gi];
-    if (G.end > G.begin)
-      if (int st = gnnshap::launch_sample_batch(b.sample + G.begin, G.end - G.begin, G.blocks, G.max_wpr, gs[gi]))
-        return st;
+    if (G.end == G.begin) continue;
+    if (int st = gnnshap::launch_sample_batch(b.sample + G.begin, G.end - G.begin, G.blocks, G.max_wpr, gs[gi]))
+      return st;
+    if (mat[gi]) {
+      GS_HIP(hipEventRecord(mat[gi]->fork, gs[gi]));
+      GS_HIP(hipStreamWaitEvent(mat[gi]->stream, mat[gi]->fork, 0));
+    }
   }
   // 2. coalition values
   for (int gi = 0; gi < 2; ++gi) {
@@ -323,20 +336,33 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       }
     }
   }
-  // 3. least squares: G~ and the right-hand sides, then the factorisations
+  // G~ (launched after the evaluations, which are on the longer chains)
+  for (int gi = 0; gi < 2; ++gi) {
+    const Group& G = grp[gi];
+    if (!mat[gi]) continue;
+    if (int st = gnnshap::launch_solve_matrix(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bnrb,
+                                              mat[gi]->stream))
+      return st;
+    GS_HIP(hipEventRecord(mat[gi]->join, mat[gi]->stream));
+  }
+  // 3. least squares: right-hand sides, then (with G~ ready) the factorisations
   for (int gi = 0; gi < 2; ++gi) {
     const Group& G = grp[gi];
     if (G.solve_count > 0)
-      if (int st = gnnshap::launch_solve_prepare(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bh, G.bnrb,
-                                                 G.bnch, gs[gi]))
+      if (int st = gnnshap::launch_solve_rhs(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bh, G.bnch,
+                                             gs[gi]))
         return st;
   }
-  for (int gi = 0; gi < 2; ++gi) {
+  // the one-workgroup group first: its single launch should not queue behind
+  // the host's launches of the panel sequence
+  for (int gi = 1; gi >= 0; --gi) {
     const Group& G = grp[gi];
-    if (G.solve_count > 0)
+    if (G.solve_count > 0) {
+      GS_HIP(hipStreamWaitEvent(gs[gi], mat[gi]->join, 0));
       if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, G.max_panels, G.small,
                                                 gs[gi]))
         return st;
+    }
     for (int64_t t : G.rest) {
       if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
                                      f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
@@ -344,9 +370,9 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
         return st;
     }
   }
-  if (side) {
-    GS_HIP(hipEventRecord(side->join, side->stream));
-    GS_HIP(hipStreamWaitEvent(s, side->join, 0));
+  if (side0) {
+    GS_HIP(hipEventRecord(side0->join, side0->stream));
+    GS_HIP(hipStreamWaitEvent(s, side0->join, 0));
   }
   return GNNSHAP_OK;
   GS_TRY_END

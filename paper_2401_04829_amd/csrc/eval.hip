@@ -539,6 +539,13 @@ __device__ __forceinline__ void eval_l2_body(
   }
 }
 
+// Z^1 row of local node u: Zsrc row zidx[u] (the graph-wide X W_1 and the
+// subgraph's node ids), or row u when zidx is NULL (per-subgraph rows).
+__device__ __forceinline__ const float* zrow(const float* __restrict__ Zsrc, const int32_t* __restrict__ zidx,
+                                             int32_t u, int h) {
+  return Zsrc + static_cast<int64_t>(zidx ? zidx[u] : u) * h;
+}
+
 // Main pass of the two-layer evaluation with one thread per coalition, for
 // narrow hidden layers (h <= H): a block of kRowsPerBlock coalitions stages
 // what they all read (each player's source and Z^1 row, Z^1 of H_1, the
@@ -549,9 +556,13 @@ __device__ __forceinline__ void eval_l2_body(
 // sort the in-neighbours by global id, as the players entering the target).
 constexpr int kRowsPerBlock = 128;
 
+// Row stride of the staged Z^1 rows: four floats of padding spread the
+// coalitions' scattered row reads over the LDS banks.
+constexpr int zstride(int H) { return H + 4; }
+
 size_t rows_lds_bytes(int64_t n_dst, int64_t n1, int64_t M, int H) {
-  return sizeof(float) * static_cast<size_t>(M * H + n1 * H) +
-         sizeof(uint16_t) * static_cast<size_t>(kRowsPerBlock * n_dst) +
+  return sizeof(float) * static_cast<size_t>(M * zstride(H) + n1 * H) +
+         sizeof(uint16_t) * static_cast<size_t>(kRowsPerBlock * (n_dst + 1)) +
          sizeof(int32_t) * static_cast<size_t>(M + n_dst + 1) + 16;
 }
 
@@ -559,16 +570,17 @@ template <int H>
 __device__ __forceinline__ void eval_rows_body(
     const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
     const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src,
-    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zc, const float* __restrict__ b1,
-    const float* __restrict__ W2, const float* __restrict__ b2, int h, int C, const int32_t* __restrict__ ctl,
-    float* __restrict__ y_rows, int64_t block) {
+    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zsrc, const int32_t* __restrict__ zidx,
+    const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
+    const int32_t* __restrict__ ctl, const float* __restrict__ fef, float* __restrict__ y_rows, int64_t block) {
   constexpr int R = kRowsPerBlock;
+  constexpr int ZS = zstride(H);
   extern __shared__ __align__(16) float sm[];
-  float* zall = sm;                                            // M x H
-  float* zself = zall + M * H;                                 // n1 x H
-  int32_t* sall = reinterpret_cast<int32_t*>(zself + n1 * H);  // M
+  float* zall = sm;                                            // M x ZS
+  float* zself = zall + M * ZS;                                // n1 x H
+  int32_t* sall = reinterpret_cast<int32_t*>(zself + n1 * H);  // M: source, or n_dst past the destinations
   int32_t* dptr = sall + M;                                    // n_dst + 1
-  uint16_t* deg = reinterpret_cast<uint16_t*>(dptr + n_dst + 1);  // n_dst x R
+  uint16_t* deg = reinterpret_cast<uint16_t*>(dptr + n_dst + 1);  // (n_dst + 1) x R, row n_dst = 0
   const int64_t nr = rows_in_pass(dyn_count, 0, cap);
   const int64_t b0 = block * R;
   if (b0 >= nr) return;
@@ -576,29 +588,50 @@ __device__ __forceinline__ void eval_rows_body(
   const int64_t b = b0 + tid;
   const bool valid = b < nr;
   const int c0 = ctl[0];
+  const int nd = static_cast<int>(n_dst), Mi = static_cast<int>(M), n1i = static_cast<int>(n1);
+  // a source outside the destinations has no player entering it: degree 1,
+  // coefficient rsqrt(1 + 0), read from the zero row n_dst
 #pragma unroll 4
-  for (int64_t e = tid; e < M; e += R) sall[e] = edge_src[e];
-  for (int64_t x = tid; x <= n_dst; x += R) dptr[x] = dst_ptr[x];
+  for (int e = tid; e < Mi; e += R) {
+    const int32_t u = edge_src[e];
+    sall[e] = u < nd ? u : nd;
+  }
+  for (int x = tid; x <= nd; x += R) dptr[x] = dst_ptr[x];
 #pragma unroll 4
-  for (int64_t t = tid; t < n1 * H; t += R) {
-    const int64_t x = t / H, f = t % H;
-    zself[t] = f < h ? Zc[x * h + f] : 0.f;
+  for (int t = tid; t < n1i * H; t += R) {
+    const int x = t / H, f = t % H;
+    zself[t] = f < h ? zrow(Zsrc, zidx, x, h)[f] : 0.f;
+  }
+  deg[nd * R + tid] = 0;
+#pragma unroll 4
+  for (int t = tid; t < Mi * H; t += R) {
+    const int e = t / H, f = t % H;
+    zall[e * ZS + f] = f < h ? zrow(Zsrc, zidx, edge_src[e], h)[f] : 0.f;
   }
   __syncthreads();
-#pragma unroll 4
-  for (int64_t t = tid; t < M * H; t += R) {
-    const int64_t e = t / H, f = t % H;
-    zall[t] = f < h ? Zc[static_cast<int64_t>(sall[e]) * h + f] : 0.f;
-  }
-  const int64_t row = valid ? static_cast<int64_t>(rows[b]) : 0;
+  const int64_t row = valid ? (rows ? static_cast<int64_t>(rows[b]) : b) : 0;
   const uint64_t* mrow = masks + row * wpr;
-  // in-degree of every destination under this coalition
-  for (int64_t x = 0; x < n_dst; ++x) {
-    const int64_t e0 = dptr[x], e1 = dptr[x + 1];
-    int cnt = 0;
-    for (int64_t w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+  // without a row list every row is taken; one with no player entering the
+  // target is pruned: its value is f(empty) (Sec. 3.4.1)
+  bool live = valid;
+  if (!rows && valid) {
+    const int indeg = dptr[1];
+    bool any = false;
+    for (int w = 0; w * 64 < indeg; ++w) {
       uint64_t word = mrow[w];
-      const int64_t lo = w * 64;
+      if (indeg - w * 64 < 64) word &= (uint64_t(1) << (indeg - w * 64)) - 1;
+      any = any || word != 0;
+    }
+    live = any;
+    if (!live) y_rows[row] = fef[0];
+  }
+  // in-degree of every destination under this coalition
+  for (int x = 0; x < nd && live; ++x) {
+    const int e0 = dptr[x], e1 = dptr[x + 1];
+    int cnt = 0;
+    for (int w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+      uint64_t word = mrow[w];
+      const int lo = w * 64;
       if (e0 > lo) word &= ~uint64_t(0) << (e0 - lo);
       if (e1 < lo + 64) word &= (uint64_t(1) << (e1 - lo)) - 1;
       cnt += __popcll(word);
@@ -612,32 +645,38 @@ __device__ __forceinline__ void eval_rows_body(
     b1v[i] = (b1 && i < h) ? b1[i] : 0.f;
   }
   __syncthreads();
-  auto dinv = [&](int64_t x) { return rsqrtf(1.0f + static_cast<float>(deg[x * R + tid])); };
+  auto dinv = [&](int x) { return rsqrtf(1.0f + static_cast<float>(deg[x * R + tid])); };
   // layer 1 at every node of H_1, folded into the explained logit; layer 2 alongside
+  if (!live) return;
   float acc2 = 0.f, t0 = 0.f;
-  for (int64_t x = 0; x < n1; ++x) {
-    const int64_t e0 = dptr[x], e1 = dptr[x + 1];
+  for (int x = 0; x < n1i; ++x) {
+    const int e0 = dptr[x], e1 = dptr[x + 1];
     float acc[H];
 #pragma unroll
     for (int i = 0; i < H; ++i) acc[i] = 0.f;
-    for (int64_t w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+    for (int w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
       uint64_t bits = mrow[w];
-      const int64_t lo = w * 64;
+      const int lo = w * 64;
       if (e0 > lo) bits &= ~uint64_t(0) << (e0 - lo);
       if (e1 < lo + 64) bits &= (uint64_t(1) << (e1 - lo)) - 1;
-      while (bits) {
-        const int64_t e = lo + __ffsll(static_cast<long long>(bits)) - 1;
-        bits &= bits - 1;
-        const int32_t u = sall[e];
-        const float coef = u < n_dst ? dinv(u) : 1.0f;
-        const float* z = zall + e * H;
+      // the two 32-bit halves of the word, set bits in ascending order
 #pragma unroll
-        for (int i = 0; i < H; i += 4) {
-          const float4 zz = *reinterpret_cast<const float4*>(z + i);
-          acc[i] += coef * zz.x;
-          acc[i + 1] += coef * zz.y;
-          acc[i + 2] += coef * zz.z;
-          acc[i + 3] += coef * zz.w;
+      for (int half = 0; half < 2; ++half) {
+        uint32_t hb = static_cast<uint32_t>(bits >> (32 * half));
+        const int base = lo + 32 * half;
+        while (hb) {
+          const int e = base + __builtin_ctz(hb);
+          hb &= hb - 1;
+          const float coef = dinv(sall[e]);
+          const float* z = zall + e * ZS;
+#pragma unroll
+          for (int i = 0; i < H; i += 4) {
+            const float4 zz = *reinterpret_cast<const float4*>(z + i);
+            acc[i] += coef * zz.x;
+            acc[i + 1] += coef * zz.y;
+            acc[i + 2] += coef * zz.z;
+            acc[i + 3] += coef * zz.w;
+          }
         }
       }
     }
@@ -657,18 +696,32 @@ __device__ __forceinline__ void eval_rows_body(
   // layer 2 at the target
   const float dv = dinv(0);
   acc2 += dv * t0;
-  if (valid) y_rows[row] = dv * acc2 + (b2 ? b2[c0] : 0.f);
+  y_rows[row] = dv * acc2 + (b2 ? b2[c0] : 0.f);
 }
 
 template <int H>
 __global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows(
     const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
     const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src,
-    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zc, const float* __restrict__ b1,
-    const float* __restrict__ W2, const float* __restrict__ b2, int h, int C, const int32_t* __restrict__ ctl,
-    float* __restrict__ y_rows) {
-  eval_rows_body<H>(masks, wpr, rows, cap, dyn_count, dst_ptr, edge_src, n_dst, n1, M, Zc, b1, W2, b2, h, C, ctl,
-                    y_rows, blockIdx.x);
+    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zsrc, const int32_t* __restrict__ zidx,
+    const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
+    const int32_t* __restrict__ ctl, const float* __restrict__ fef, float* __restrict__ y_rows) {
+  eval_rows_body<H>(masks, wpr, rows, cap, dyn_count, dst_ptr, edge_src, n_dst, n1, M, Zsrc, zidx, b1, W2, b2, h, C,
+                    ctl, fef, y_rows, blockIdx.x);
+}
+
+__device__ __forceinline__ void pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
+                                           int32_t* class_out, float* f_empty_full) {
+  int c = requested;
+  if (c < 0) {
+    c = 0;
+    for (int i = 1; i < C; ++i)
+      if (sp_y[C + i] > sp_y[C + c]) c = i;
+  }
+  ctl[0] = c;
+  if (class_out) *class_out = c;
+  f_empty_full[0] = sp_y[c];
+  f_empty_full[1] = sp_y[C + c];
 }
 
 // The two end coalitions of a two-layer GCN with hops >= 2 (no players and
@@ -683,12 +736,36 @@ size_t ends_lds_bytes(int64_t n_dst, int64_t n1, int h, int C) {
   return sizeof(float) * static_cast<size_t>(n_dst + n1 * C + nx * h + h + C);
 }
 
+// With XW1 given, the workgroup first gathers Zc (n_nodes x h) = the rows of
+// XW1 at the subgraph's node ids (for this kernel and the next ones);
+// afterwards thread 0 picks the explained class (requested, or argmax
+// f(E_c)) into ctl[0], class_out and f_empty_full.
 __device__ __forceinline__ void ends_l2_body(const int32_t* __restrict__ dst_ptr,
                                              const int32_t* __restrict__ edge_src, int64_t n_dst, int64_t n1,
-                                             const float* __restrict__ Zc, const float* __restrict__ b1,
+                                             float* Zc, const float* __restrict__ XW1,
+                                             const int32_t* __restrict__ node_gid, int64_t n_nodes,
+                                             const float* __restrict__ b1,
                                              const float* __restrict__ W2, const float* __restrict__ b2, int h,
-                                             int C, float* __restrict__ sp_y) {
+                                             int C, float* __restrict__ sp_y, int requested, int32_t* ctl,
+                                             int32_t* class_out, float* f_empty_full) {
   extern __shared__ __align__(16) float sm[];
+  if (XW1) {
+    const int64_t total = n_nodes * h;
+    for (int64_t t0 = threadIdx.x; t0 < total; t0 += 4 * kEndsThreads) {
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t t = t0 + q * kEndsThreads;
+        v[q] = t < total ? XW1[static_cast<int64_t>(node_gid[t / h]) * h + t % h] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t t = t0 + q * kEndsThreads;
+        if (t < total) Zc[t] = v[q];
+      }
+    }
+    __syncthreads();
+  }
   const int64_t nx = h >= kEndsThreads ? 1 : kEndsThreads / h;
   float* dinv = sm;                   // n_dst: full-coalition d^-1/2
   float* tt = dinv + n_dst;           // n1 x C: H^1[x] . W_2[:, c] under the full coalition
@@ -757,16 +834,21 @@ __device__ __forceinline__ void ends_l2_body(const int32_t* __restrict__ dst_ptr
     acc += dv * tt[c];
     sp_y[C + c] = dv * acc + bias;
   }
+  __syncthreads();
+  if (tid == 0) pick_class(sp_y, C, requested, ctl, class_out, f_empty_full);
 }
 
 __global__ void __launch_bounds__(kEndsThreads) k_eval_ends(const int32_t* __restrict__ dst_ptr,
                                                              const int32_t* __restrict__ edge_src, int64_t n_dst,
-                                                             int64_t n1, const float* __restrict__ Zc,
+                                                             int64_t n1, float* Zc, const float* __restrict__ XW1,
+                                                             const int32_t* __restrict__ node_gid, int64_t n_nodes,
                                                              const float* __restrict__ b1,
                                                              const float* __restrict__ W2,
                                                              const float* __restrict__ b2, int h, int C,
-                                                             float* __restrict__ sp_y) {
-  ends_l2_body(dst_ptr, edge_src, n_dst, n1, Zc, b1, W2, b2, h, C, sp_y);
+                                                             float* __restrict__ sp_y, int requested, int32_t* ctl,
+                                                             int32_t* class_out, float* f_empty_full) {
+  ends_l2_body(dst_ptr, edge_src, n_dst, n1, Zc, XW1, node_gid, n_nodes, b1, W2, b2, h, C, sp_y, requested, ctl,
+               class_out, f_empty_full);
 }
 
 template <int FPT>
@@ -779,20 +861,6 @@ __global__ void __launch_bounds__(256) k_eval_l2(
     float* __restrict__ y_all) {
   eval_l2_body<FPT>(masks, wpr, rows, row_off, cap, dyn_count, dst_ptr, edge_src, n_dst, n1, Zc, b1, W2, b2, h, C,
                     ctl, all_classes, tbr, y_rows, y_all, blockIdx.x);
-}
-
-__device__ __forceinline__ void pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
-                                           int32_t* class_out, float* f_empty_full) {
-  int c = requested;
-  if (c < 0) {
-    c = 0;
-    for (int i = 1; i < C; ++i)
-      if (sp_y[C + i] > sp_y[C + c]) c = i;
-  }
-  ctl[0] = c;
-  if (class_out) *class_out = c;
-  f_empty_full[0] = sp_y[c];
-  f_empty_full[1] = sp_y[C + c];
 }
 
 __global__ void k_pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
@@ -982,12 +1050,12 @@ int launch_fused_l2(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn
     const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(cap, kRowsPerBlock));
     if (H == 16)
       k_eval_rows<16><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src,
-                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], b1, m->W[1],
-                                                          b2, h, C, w.ctl, y_rows);
+                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], nullptr, b1,
+                                                          m->W[1], b2, h, C, w.ctl, nullptr, y_rows);
     else
       k_eval_rows<32><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src,
-                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], b1, m->W[1],
-                                                          b2, h, C, w.ctl, y_rows);
+                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], nullptr, b1,
+                                                          m->W[1], b2, h, C, w.ctl, nullptr, y_rows);
   } else {
     switch (fpt) {
       case 1: GS_L2(1); break;
@@ -1064,9 +1132,10 @@ __global__ void k_gather_batch(const gnnshap::EvalJob* __restrict__ jobs, const 
 
 // The end coalitions of every job.
 __global__ void __launch_bounds__(kEndsThreads) k_eval_ends_batch(const gnnshap::EvalJob* __restrict__ jobs,
-                                                                   gnnshap::EvalModel md) {
+                                                                   gnnshap::EvalModel md, bool gather) {
   const gnnshap::EvalJob J = jobs[blockIdx.x];
-  ends_l2_body(J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1, md.b1, md.W2, md.b2, md.h, md.C, J.sp_y);
+  ends_l2_body(J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1, gather ? md.XW1 : nullptr, J.node_gid, J.n_nodes, md.b1,
+               md.W2, md.b2, md.h, md.C, J.sp_y, md.target_class, J.ctl, J.cls_out, J.fef);
 }
 
 // Main pass of the jobs that do not take the one-thread-per-coalition kernel.
@@ -1079,19 +1148,17 @@ __global__ void __launch_bounds__(256) k_eval_l2_batch(const gnnshap::EvalJob* _
                       md.b1, md.W2, md.b2, md.h, md.C, J.ctl, false, tbr, J.y, J.sp_y, blockIdx.x);
 }
 
-// Main pass of the jobs that take the one-thread-per-coalition kernel.
+// Main pass of the jobs that take the one-thread-per-coalition kernel;
+// all: every row of the job (pruned rows get f(empty) on the way), else the
+// live rows listed by k_live_batch.
 template <int H>
 __global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows_batch(const gnnshap::EvalJob* __restrict__ jobs,
-                                                                   gnnshap::EvalModel md) {
+                                                                   gnnshap::EvalModel md, bool all) {
   const gnnshap::EvalJob J = jobs[blockIdx.y];
   if (!J.rows_ok) return;
-  eval_rows_body<H>(J.masks, J.wpr, J.live_rows, J.k, J.ctl + 1, J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.M, J.Zc1,
-                    md.b1, md.W2, md.b2, md.h, md.C, J.ctl, J.y, blockIdx.x);
-}
-
-__global__ void k_pick_class_batch(const gnnshap::EvalJob* __restrict__ jobs, int C, int requested) {
-  const gnnshap::EvalJob J = jobs[blockIdx.x];
-  pick_class(J.sp_y, C, requested, J.ctl, J.cls_out, J.fef);
+  eval_rows_body<H>(J.masks, J.wpr, all ? nullptr : J.live_rows, J.k, all ? nullptr : J.ctl + 1, J.dst_ptr,
+                    J.edge_src, J.n_dst, J.n1, J.M, J.Zc1, nullptr, md.b1, md.W2, md.b2, md.h, md.C, J.ctl, J.fef,
+                    J.y, blockIdx.x);
 }
 
 __global__ void __launch_bounds__(256) k_live_batch(const gnnshap::EvalJob* __restrict__ jobs) {
@@ -1146,6 +1213,44 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int L = sh.L;
 
+  // Two-layer models whose coalitions all fit the one-thread-per-coalition
+  // kernel in one pass take two launches: the end coalitions (with the
+  // class), then every row (pruned rows get f(empty) on the way), reading
+  // X W_1 through the subgraph's node ids when it is given.
+  const int H = sh.dims[1] <= 16 ? 16 : 32;
+  const size_t lds_rows = rows_lds_bytes(sh.n_dst, sh.nd[1], sg->num_edges, H);
+  const bool direct = ends_ok(sh) && fused_l2_ok(sh, k, false) && sh.dims[1] <= 32 && lds_rows <= 65536 &&
+                      sh.tile >= k && gnnshap::ceil_div(k, kRowsPerBlock) <= INT32_MAX;
+  if (direct) {
+    if (!m->XW1) {
+      if (int st = launch_gemm(s, X, sh.dims[0], sg->node_gid, nullptr, m->W[0], sh.dims[1], w.Zc[1], sh.dims[1], 0,
+                               sh.n_nodes, sh.dims[1], sh.dims[0]))
+        return st;
+    }
+    const float* Zsrc = w.Zc[1];
+    const int32_t* zidx = nullptr;
+    const float* b1 = m->b ? m->b[0] : nullptr;
+    const float* b2 = m->b ? m->b[1] : nullptr;
+    k_eval_ends<<<1, kEndsThreads, ends_lds_bytes(sh.n_dst, sh.nd[1], sh.dims[1], sh.dims[2]), s>>>(
+        sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], m->XW1, sg->node_gid, sh.n_nodes, b1, m->W[1], b2,
+        sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out, f_empty_full);
+    GS_LAUNCHED();
+    const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(k, kRowsPerBlock));
+    GS_TIMED("k_eval_rows", s);
+    if (H == 16)
+      k_eval_rows<16><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, nullptr, k, nullptr, sg->dst_ptr,
+                                                          sg->edge_src, sh.n_dst, sh.nd[1], sg->num_edges, Zsrc, zidx,
+                                                          b1, m->W[1], b2, sh.dims[1], sh.dims[2], w.ctl,
+                                                          f_empty_full, y);
+    else
+      k_eval_rows<32><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, nullptr, k, nullptr, sg->dst_ptr,
+                                                          sg->edge_src, sh.n_dst, sh.nd[1], sg->num_edges, Zsrc, zidx,
+                                                          b1, m->W[1], b2, sh.dims[1], sh.dims[2], w.ctl,
+                                                          f_empty_full, y);
+    GS_LAUNCHED();
+    return GNNSHAP_OK;
+  }
+
   k_init<<<gnnshap::grid_for(sh.wpr, 256, 64), 256, 0, s>>>(w.ctl, w.sp_masks, w.sp_rows, sh.wpr, sg->num_edges);
   GS_LAUNCHED();
   // Constant rows: Z^1 = X[V_c] W_1 (gathered from X W_1 when given), then the boundary chain.
@@ -1171,14 +1276,15 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   // f(empty) and f(E_c) for every class, then the explained class.
   if (ends_ok(sh)) {
     k_eval_ends<<<1, kEndsThreads, ends_lds_bytes(sh.n_dst, sh.nd[1], sh.dims[1], sh.dims[2]), s>>>(
-        sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], m->b ? m->b[0] : nullptr, m->W[1],
-        m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y);
+        sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], nullptr, nullptr, sh.n_nodes,
+        m->b ? m->b[0] : nullptr, m->W[1], m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y, target_class,
+        w.ctl, class_out, f_empty_full);
     GS_LAUNCHED();
-  } else if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) {
-    return st;
+  } else {
+    if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
+    k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
+    GS_LAUNCHED();
   }
-  k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
-  GS_LAUNCHED();
   // Prediction pruning, then the live coalitions in passes of sh.tile rows.
   k_live<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(masks, sh.wpr, k, sg->dst_ptr, w.ctl, w.live_rows,
                                                          w.live_flag);
@@ -1272,44 +1378,45 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
   if (lds_ends > 65536 || lds_main > 65536)
     return fail(GNNSHAP_EUNSUPPORTED, "batched evaluation needs %zu bytes of LDS", std::max(lds_ends, lds_main));
   const unsigned nn = static_cast<unsigned>(n);
-  k_init_batch<<<dim3(grid_for(max_wpr, 256, 64), nn), 256, 0, s>>>(jobs);
-  GS_LAUNCHED();
-  k_gather_batch<<<dim3(grid_for(max_nodes * md.h, 256, 2048), nn), 256, 0, s>>>(jobs, md.XW1, md.h);
-  GS_LAUNCHED();
-#define GS_L2B(F, GRID, LDS, TBR) k_eval_l2_batch<F><<<GRID, 256, LDS, s>>>(jobs, md, TBR)
-#define GS_L2B_ALL(GRID, LDS, TBR)            \
-  switch (fpt) {                              \
-    case 1: GS_L2B(1, GRID, LDS, TBR); break; \
-    case 2: GS_L2B(2, GRID, LDS, TBR); break; \
-    case 4: GS_L2B(4, GRID, LDS, TBR); break; \
-    case 8: GS_L2B(8, GRID, LDS, TBR); break; \
-    default: GS_L2B(16, GRID, LDS, TBR); break; \
+  const bool all = rows_jobs == n;   // every job takes the one-thread-per-coalition kernel: two launches
+  if (!all) {
+    k_init_batch<<<dim3(grid_for(max_wpr, 256, 64), nn), 256, 0, s>>>(jobs);
+    GS_LAUNCHED();
+    k_gather_batch<<<dim3(grid_for(max_nodes * md.h, 256, 2048), nn), 256, 0, s>>>(jobs, md.XW1, md.h);
+    GS_LAUNCHED();
   }
   {
     GS_TIMED("k_eval_ends_batch", s);
-    k_eval_ends_batch<<<nn, kEndsThreads, ends_lds_bytes(max_ndst, max_n1, md.h, md.C), s>>>(jobs, md);
+    k_eval_ends_batch<<<nn, kEndsThreads, lds_ends, s>>>(jobs, md, all);
   }
   GS_LAUNCHED();
-  k_pick_class_batch<<<nn, 1, 0, s>>>(jobs, md.C, md.target_class);
-  GS_LAUNCHED();
-  k_live_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
-  GS_LAUNCHED();
-  if (rows_jobs < n) {
+  if (!all) {
+    k_live_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
+    GS_LAUNCHED();
+#define GS_L2B(F, GRID, LDS, TBR) k_eval_l2_batch<F><<<GRID, 256, LDS, s>>>(jobs, md, TBR)
     GS_TIMED("k_eval_l2_batch", s);
-    GS_L2B_ALL(dim3(static_cast<unsigned>(ceil_div(max_k, tb_main)), nn), lds_main, tb_main);
+    const dim3 g(static_cast<unsigned>(ceil_div(max_k, tb_main)), nn);
+    switch (fpt) {
+      case 1: GS_L2B(1, g, lds_main, tb_main); break;
+      case 2: GS_L2B(2, g, lds_main, tb_main); break;
+      case 4: GS_L2B(4, g, lds_main, tb_main); break;
+      case 8: GS_L2B(8, g, lds_main, tb_main); break;
+      default: GS_L2B(16, g, lds_main, tb_main); break;
+    }
+#undef GS_L2B
+    GS_LAUNCHED();
   }
-  GS_LAUNCHED();
   if (rows_jobs > 0) {
     GS_TIMED("k_eval_rows_batch", s);
     const dim3 g(static_cast<unsigned>(ceil_div(max_k, kRowsPerBlock)), nn);
-    if (md.h <= 16) k_eval_rows_batch<16><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md);
-    else k_eval_rows_batch<32><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md);
+    if (md.h <= 16) k_eval_rows_batch<16><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md, all);
+    else k_eval_rows_batch<32><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md, all);
   }
   GS_LAUNCHED();
-#undef GS_L2B_ALL
-#undef GS_L2B
-  k_fill_pruned_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
-  GS_LAUNCHED();
+  if (!all) {
+    k_fill_pruned_batch<<<dim3(grid_for(max_k, 256, 4096), nn), 256, 0, s>>>(jobs);
+    GS_LAUNCHED();
+  }
   return GNNSHAP_OK;
 }
 

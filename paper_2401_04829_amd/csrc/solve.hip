@@ -173,6 +173,56 @@ __device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_
   }
 }
 
+// The same counts over the row words [w0, w1) only, added to C with integer
+// atomics (exact in any order; C starts at zero).  A diagonal tile adds each
+// of its entries once, an off-diagonal tile adds both halves.
+__device__ __forceinline__ void gram_part_body(const uint64_t* __restrict__ T, int64_t w0, int64_t w1, int64_t M,
+                                               int64_t ld, int32_t* __restrict__ C, int64_t I, int64_t J) {
+  __shared__ uint64_t Ti[16][64];
+  __shared__ uint64_t Tj[16][64];
+  const int tid = threadIdx.x;
+  const int ty = tid / 16, tx = tid % 16;
+  int acc[4][4] = {};
+  for (int64_t k0 = w0; k0 < w1; k0 += 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + q * 256;
+      const int kk = idx / 64, c = idx % 64;
+      const int64_t i = I * 64 + c, j = J * 64 + c;
+      const bool kin = k0 + kk < w1;
+      Ti[kk][c] = (kin && i < M) ? T[(k0 + kk) * M + i] : 0;
+      Tj[kk][c] = (kin && j < M) ? T[(k0 + kk) * M + j] : 0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < 16; ++kk) {
+      uint64_t a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[q] = Ti[kk][ty * 4 + q];
+        b[q] = Tj[kk][tx * 4 + q];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[q][r] += __popcll(a[q] & b[r]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t i = I * 64 + ty * 4 + q;
+    if (i >= M) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t j = J * 64 + tx * 4 + r;
+      if (j >= M || acc[q][r] == 0) continue;
+      atomicAdd(&C[i * ld + j], acc[q][r]);
+      if (I != J) atomicAdd(&C[j * ld + i], acc[q][r]);
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
                                               int32_t* __restrict__ C) {
   gram_body(T, nrb, M, ld, C, blockIdx.y, blockIdx.x);
@@ -220,8 +270,10 @@ __device__ __forceinline__ void scalars_body(const int32_t* __restrict__ C, cons
     scal[0] = trace;
     scal[1] = sigma;
     scal[2] = tr_pgp / (Md - 1.0);
-    scal[3] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
-    scal[4] = static_cast<double>(fef[0]);
+    if (fef) {
+      scal[3] = static_cast<double>(fef[1]) - static_cast<double>(fef[0]);
+      scal[4] = static_cast<double>(fef[0]);
+    }
   }
 }
 
@@ -1220,17 +1272,31 @@ double binom_d(int64_t n, int64_t r) {
 
 // ---- multi-target path (one-workgroup systems): one job per blockIdx.y / .z --------------
 
+// Also clears the count matrix (M rows of ld) for the Gram's atomics: the
+// job's nrb x wpr workgroups each clear an equal share of it.
 __global__ void __launch_bounds__(64) k_transpose_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.z];
   if (J.kr <= 0 || blockIdx.x >= J.nrb || blockIdx.y >= J.wpr) return;
   transpose_body(J.masks, J.wpr, J.rb0, J.kr, J.M, J.T, blockIdx.x, blockIdx.y);
+  const int64_t nblk = J.nrb * J.wpr, blk = static_cast<int64_t>(blockIdx.x) * J.wpr + blockIdx.y;
+  const int64_t total = J.M * J.ld, per = (total + nblk - 1) / nblk;
+  const int64_t e0 = blk * per, e1 = e0 + per < total ? e0 + per : total;
+  for (int64_t e = e0 + threadIdx.x; e < e1; e += 64) J.counts[e] = 0;
 }
+
+// Workgroup (tile, chunk, job): tile = J' (J' + 1) / 2 + I' over the tiles
+// I' <= J' of the job, chunk = kGramChunk row words.
+constexpr int64_t kGramChunk = 32;
 
 __global__ void __launch_bounds__(256) k_gram_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.z];
   const int64_t nb = (J.M + 63) / 64;
-  if (J.kr <= 0 || blockIdx.x >= nb || blockIdx.y >= nb) return;
-  gram_body(J.T, J.nrb, J.M, J.ld, J.counts, blockIdx.y, blockIdx.x);
+  const int64_t tile = blockIdx.x, w0 = static_cast<int64_t>(blockIdx.y) * kGramChunk;
+  if (J.kr <= 0 || tile >= nb * (nb + 1) / 2 || w0 >= J.nrb) return;
+  int64_t Jt = 0;
+  while ((Jt + 1) * (Jt + 2) / 2 <= tile) ++Jt;
+  const int64_t It = tile - Jt * (Jt + 1) / 2;
+  gram_part_body(J.T, w0, w0 + kGramChunk < J.nrb ? w0 + kGramChunk : J.nrb, J.M, J.ld, J.counts, It, Jt);
 }
 
 __global__ void __launch_bounds__(256) k_dz_batch(const gnnshap::SolveJob* __restrict__ jobs) {
@@ -1268,7 +1334,7 @@ __global__ void __launch_bounds__(256) k_rhs_sum_batch(const gnnshap::SolveJob* 
 
 __global__ void __launch_bounds__(256) k_scalars_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.x];
-  scalars_body(J.counts, J.usum, J.M, J.ld, J.kr > 0, J.alpha, J.wr, J.fef, J.scal);
+  scalars_body(J.counts, J.usum, J.M, J.ld, J.kr > 0, J.alpha, J.wr, nullptr, J.scal);   // G~ only
 }
 
 __global__ void __launch_bounds__(256) k_build_batch(const gnnshap::SolveJob* __restrict__ jobs) {
@@ -1802,8 +1868,8 @@ bool gnnshap::solve_panel_path(const gnnshap_sample_plan* plan) {
   return solve_batchable(plan) && plan->num_players > kPanelMin;
 }
 
-int gnnshap::launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
-                                  int64_t max_nrb, int64_t max_nch, hipStream_t s) {
+int gnnshap::launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_nrb,
+                                 hipStream_t s) {
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   const unsigned nn = static_cast<unsigned>(n);
@@ -1813,10 +1879,12 @@ int gnnshap::launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M
       k_transpose_batch<<<dim3(static_cast<unsigned>(max_nrb), static_cast<unsigned>(max_wpr), nn), 64, 0, s>>>(jobs);
     }
     GS_LAUNCHED();
-    const unsigned nb = static_cast<unsigned>(ceil_div(max_M, 64));
+    const int64_t nb = ceil_div(max_M, 64);
     {
       GS_TIMED("k_gram_batch", s);
-      k_gram_batch<<<dim3(nb, nb, nn), 256, 0, s>>>(jobs);
+      k_gram_batch<<<dim3(static_cast<unsigned>(nb * (nb + 1) / 2), static_cast<unsigned>(ceil_div(max_nrb, kGramChunk)),
+                          nn),
+                     256, 0, s>>>(jobs);
     }
     GS_LAUNCHED();
     k_rowsum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M * 64, 256)), nn), 256, 0, s>>>(jobs);
@@ -1826,6 +1894,14 @@ int gnnshap::launch_solve_prepare(const SolveJob* jobs, int64_t n, int64_t max_M
   GS_LAUNCHED();
   k_build_batch<<<dim3(static_cast<unsigned>(max_M), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_solve_rhs(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
+                              int64_t max_nch, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  const unsigned nn = static_cast<unsigned>(n);
   k_dz_batch<<<dim3(static_cast<unsigned>(ceil_div(max_half, 256)), nn), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
   {
