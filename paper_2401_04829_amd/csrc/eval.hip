@@ -645,7 +645,8 @@ __device__ __forceinline__ void eval_rows_body(
     b1v[i] = (b1 && i < h) ? b1[i] : 0.f;
   }
   __syncthreads();
-  auto dinv = [&](int x) { return rsqrtf(1.0f + static_cast<float>(deg[x * R + tid])); };
+  // 1 + deg >= 1: the hardware reciprocal square root needs no denormal scaling
+  auto dinv = [&](int x) { return __builtin_amdgcn_rsqf(1.0f + static_cast<float>(deg[x * R + tid])); };
   // layer 1 at every node of H_1, folded into the explained logit; layer 2 alongside
   if (!live) return;
   float acc2 = 0.f, t0 = 0.f;
@@ -668,7 +669,7 @@ __device__ __forceinline__ void eval_rows_body(
           const int e = base + __builtin_ctz(hb);
           hb &= hb - 1;
           const float coef = dinv(sall[e]);
-          const float* z = zall + e * ZS;
+          const float* z = zall + __umul24(e, ZS);
 #pragma unroll
           for (int i = 0; i < H; i += 4) {
             const float4 zz = *reinterpret_cast<const float4*>(z + i);
