@@ -47,6 +47,56 @@ SideStream* side_stream(int i) {
   return &per_device.back().side[i];
 }
 
+// Page-locked staging for host-to-device copies of the calling thread: a
+// ring of two buffers, each reused only after the copy that last read it has
+// run (its event), so that a call never waits for earlier GPU work.
+// Buffers grow on demand and are kept until the process ends.
+struct HostStage {
+  char* buf = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+
+struct DeviceStages {
+  int device = -1;
+  HostStage ring[2];
+  int next = 0;
+};
+
+HostStage* host_stage(size_t bytes) {
+  static thread_local std::vector<DeviceStages> per_device;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  DeviceStages* d = nullptr;
+  for (DeviceStages& x : per_device)
+    if (x.device == dev) d = &x;
+  if (!d) {
+    per_device.emplace_back();
+    d = &per_device.back();
+    d->device = dev;
+  }
+  HostStage* h = &d->ring[d->next];
+  d->next ^= 1;
+  if (!h->done && hipEventCreateWithFlags(&h->done, hipEventDisableTiming) != hipSuccess) return nullptr;
+  if (h->pending && hipEventSynchronize(h->done) != hipSuccess) return nullptr;
+  h->pending = false;
+  if (h->cap < bytes) {
+    if (h->buf) (void)hipHostFree(h->buf);
+    h->buf = nullptr;
+    h->cap = 0;
+    const size_t want = bytes + bytes / 2 + 4096;
+    void* p = nullptr;
+    if (hipHostMalloc(&p, want, hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    h->buf = static_cast<char*>(p);
+    h->cap = want;
+  }
+  return h;
+}
+
 }  // namespace gnnshap
 
 namespace {
@@ -182,8 +232,11 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
   // and copied in one transfer before the first launch.
   char* const base = static_cast<char*>(ws);
   const size_t front = static_cast<size_t>(reinterpret_cast<char*>(b.solve + n) - base);
-  std::vector<char> image(front, 0);
-  auto at = [&](const void* dev_ptr) { return image.data() + (static_cast<const char*>(dev_ptr) - base); };
+  gnnshap::HostStage* stage = gnnshap::host_stage(front);
+  if (!stage) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
+  char* const image = stage->buf;
+  std::fill(image, image + front, 0);
+  auto at = [&](const void* dev_ptr) { return image + (static_cast<const char*>(dev_ptr) - base); };
   std::copy(classes, classes + L.classes, reinterpret_cast<gnnshap_class*>(at(b.classes)));
   gnnshap::SampleJob* sj = reinterpret_cast<gnnshap::SampleJob*>(at(b.sample));
   gnnshap::EvalJob* ej = reinterpret_cast<gnnshap::EvalJob*>(at(b.eval));
@@ -281,99 +334,107 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     G.solve_count = nv - G.solve_begin;
   }
 
-  GS_HIP(hipMemcpyAsync(ws, image.data(), front, hipMemcpyHostToDevice, s));
-  // Streams: group 0 runs on side stream 0, group 1 on `stream`; each
-  // group's G~ is built on a side stream of its own (2 for group 0, 1 for
-  // group 1) once its masks are sampled, while its coalitions are evaluated.
-  hipStream_t gs[2] = {s, s};
-  gnnshap::SideStream* mat[2] = {nullptr, nullptr};
-  gnnshap::SideStream* side0 = nullptr;
-  if (grp[0].end > grp[0].begin) {
-    side0 = gnnshap::side_stream(0);
-    if (!side0) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
-    GS_HIP(hipEventRecord(side0->fork, s));
-    GS_HIP(hipStreamWaitEvent(side0->stream, side0->fork, 0));
-    gs[0] = side0->stream;
-  }
-  for (int gi = 0; gi < 2; ++gi) {
-    if (grp[gi].solve_count == 0) continue;
-    mat[gi] = gnnshap::side_stream(gi == 0 ? 2 : 1);
-    if (!mat[gi]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
-  }
-  // 1. sampling; the matrix streams wait for it
-  for (int gi = 0; gi < 2; ++gi) {
-    const Group& G = grp[gi];
-    if (G.end == G.begin) continue;
-    if (int st = gnnshap::launch_sample_batch(b.sample + G.begin, G.end - G.begin, G.blocks, G.max_wpr, gs[gi]))
-      return st;
-    if (mat[gi]) {
-      GS_HIP(hipEventRecord(mat[gi]->fork, gs[gi]));
-      GS_HIP(hipStreamWaitEvent(mat[gi]->stream, mat[gi]->fork, 0));
-    }
-  }
-  // 2. coalition values
-  for (int gi = 0; gi < 2; ++gi) {
-    const Group& G = grp[gi];
-    if (G.end == G.begin) continue;
-    int st_eval = GNNSHAP_EUNSUPPORTED;
-    if (G.eval_all) {
-      const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
-                                  model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
-      st_eval = gnnshap::launch_eval_batch(b.eval + G.begin, G.end - G.begin, md, G.max_nodes, G.max_ndst, G.max_n1,
-                                           G.max_wpr, G.max_k, G.rows_jobs, G.rows_lds, gs[gi]);
-      if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
-      gnnshap::clear_error();
-    }
-    if (st_eval != GNNSHAP_OK) {
-      for (int64_t j = G.begin; j < G.end; ++j) {
-        const int64_t t = order[j];
-        const gnnshap_sample_plan& p = plans[t];
-        if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
-                                             p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
-                                             class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t],
-                                             gs[gi]))
-          return st;
+  GS_HIP(hipMemcpyAsync(ws, image, front, hipMemcpyHostToDevice, s));
+  GS_HIP(hipEventRecord(stage->done, s));
+  stage->pending = true;
+  // Every launch after the job-table copy, on origin stream `o` and the side
+  // streams forked from it.
+  auto issue = [&](hipStream_t o) -> int {
+      // Streams: group 0 runs on side stream 0, group 1 on `stream`; each
+      // group's G~ is built on a side stream of its own (2 for group 0, 1 for
+      // group 1) once its masks are sampled, while its coalitions are evaluated.
+      hipStream_t gs[2] = {o, o};
+      gnnshap::SideStream* mat[2] = {nullptr, nullptr};
+      gnnshap::SideStream* side0 = nullptr;
+      if (grp[0].end > grp[0].begin) {
+        side0 = gnnshap::side_stream(0);
+        if (!side0) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+        GS_HIP(hipEventRecord(side0->fork, o));
+        GS_HIP(hipStreamWaitEvent(side0->stream, side0->fork, 0));
+        gs[0] = side0->stream;
       }
-    }
-  }
-  // G~ (launched after the evaluations, which are on the longer chains)
-  for (int gi = 0; gi < 2; ++gi) {
-    const Group& G = grp[gi];
-    if (!mat[gi]) continue;
-    if (int st = gnnshap::launch_solve_matrix(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bnrb,
-                                              mat[gi]->stream))
-      return st;
-    GS_HIP(hipEventRecord(mat[gi]->join, mat[gi]->stream));
-  }
-  // 3. least squares: right-hand sides, then (with G~ ready) the factorisations
-  for (int gi = 0; gi < 2; ++gi) {
-    const Group& G = grp[gi];
-    if (G.solve_count > 0)
-      if (int st = gnnshap::launch_solve_rhs(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bh, G.bnch,
-                                             gs[gi]))
-        return st;
-  }
-  // the one-workgroup group first: its single launch should not queue behind
-  // the host's launches of the panel sequence
-  for (int gi = 1; gi >= 0; --gi) {
-    const Group& G = grp[gi];
-    if (G.solve_count > 0) {
-      GS_HIP(hipStreamWaitEvent(gs[gi], mat[gi]->join, 0));
-      if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, G.max_panels, G.small,
-                                                gs[gi]))
-        return st;
-    }
-    for (int64_t t : G.rest) {
-      if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
-                                     f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
-                                     L.solve_bytes[t], gs[gi]))
-        return st;
-    }
-  }
-  if (side0) {
-    GS_HIP(hipEventRecord(side0->join, side0->stream));
-    GS_HIP(hipStreamWaitEvent(s, side0->join, 0));
-  }
+      for (int gi = 0; gi < 2; ++gi) {
+        if (grp[gi].solve_count == 0) continue;
+        mat[gi] = gnnshap::side_stream(gi == 0 ? 2 : 1);
+        if (!mat[gi]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+      }
+      // 1. sampling; the matrix streams wait for it
+      for (int gi = 0; gi < 2; ++gi) {
+        const Group& G = grp[gi];
+        if (G.end == G.begin) continue;
+        if (int st = gnnshap::launch_sample_batch(b.sample + G.begin, G.end - G.begin, G.blocks, G.max_wpr, gs[gi]))
+          return st;
+        if (mat[gi]) {
+          GS_HIP(hipEventRecord(mat[gi]->fork, gs[gi]));
+          GS_HIP(hipStreamWaitEvent(mat[gi]->stream, mat[gi]->fork, 0));
+        }
+      }
+      // 2. coalition values
+      for (int gi = 0; gi < 2; ++gi) {
+        const Group& G = grp[gi];
+        if (G.end == G.begin) continue;
+        int st_eval = GNNSHAP_EUNSUPPORTED;
+        if (G.eval_all) {
+          const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
+                                      model->b ? model->b[1] : nullptr, model->dims[1], model->dims[2], target_class};
+          st_eval = gnnshap::launch_eval_batch(b.eval + G.begin, G.end - G.begin, md, G.max_nodes, G.max_ndst, G.max_n1,
+                                               G.max_wpr, G.max_k, G.rows_jobs, G.rows_lds, gs[gi]);
+          if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
+          gnnshap::clear_error();
+        }
+        if (st_eval != GNNSHAP_OK) {
+          for (int64_t j = G.begin; j < G.end; ++j) {
+            const int64_t t = order[j];
+            const gnnshap_sample_plan& p = plans[t];
+            if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
+                                                 p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
+                                                 class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t],
+                                                 gs[gi]))
+              return st;
+          }
+        }
+      }
+      // G~ (launched after the evaluations, which are on the longer chains)
+      for (int gi = 0; gi < 2; ++gi) {
+        const Group& G = grp[gi];
+        if (!mat[gi]) continue;
+        if (int st = gnnshap::launch_solve_matrix(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bnrb,
+                                                  mat[gi]->stream))
+          return st;
+        GS_HIP(hipEventRecord(mat[gi]->join, mat[gi]->stream));
+      }
+      // 3. least squares: right-hand sides, then (with G~ ready) the factorisations
+      for (int gi = 0; gi < 2; ++gi) {
+        const Group& G = grp[gi];
+        if (G.solve_count > 0)
+          if (int st = gnnshap::launch_solve_rhs(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bh, G.bnch,
+                                                 gs[gi]))
+            return st;
+      }
+      // the one-workgroup group first: its single launch should not queue behind
+      // the host's launches of the panel sequence
+      for (int gi = 1; gi >= 0; --gi) {
+        const Group& G = grp[gi];
+        if (G.solve_count > 0) {
+          GS_HIP(hipStreamWaitEvent(gs[gi], mat[gi]->join, 0));
+          if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, G.max_panels, G.small,
+                                                    gs[gi]))
+            return st;
+        }
+        for (int64_t t : G.rest) {
+          if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
+                                         f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
+                                         L.solve_bytes[t], gs[gi]))
+            return st;
+        }
+      }
+      if (side0) {
+        GS_HIP(hipEventRecord(side0->join, side0->stream));
+        GS_HIP(hipStreamWaitEvent(o, side0->join, 0));
+      }
+    return GNNSHAP_OK;
+  };
+  if (int st = issue(s)) return st;
   return GNNSHAP_OK;
   GS_TRY_END
 }

@@ -95,6 +95,7 @@ class Explainer:
         self._bx = None                          # batched extraction: (n, zero-filled workspace)
         self._plans = {}                         # (M, p) -> (plan, classes): the plan does not depend on seed
         self._ncls_hint = 1024                   # class-table length explain_batch allocates
+        self._xstream = None                     # stream of the batched extraction
 
     def prepare(self):
         """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
@@ -232,25 +233,37 @@ class Explainer:
     def extract_batch(self, targets):
         """gnnshap_extract_batch: the computational graphs of all targets with one
         host synchronisation; capacities grow and the batch is redone on
-        ECAPACITY.  Returns (BatchSubgraphs, ctypes array of gnnshap_subgraph)."""
+        ECAPACITY.  Extraction runs on a stream of its own, so that waiting for
+        the sizes does not wait for work queued earlier on the current stream
+        (which is then ordered after it).  Returns (BatchSubgraphs, ctypes array
+        of gnnshap_subgraph)."""
         dev = self.device
         n = len(targets)
         if self._bx is None or self._bx[0] < n:
             nbytes = L.gnnshap_extract_batch_workspace(self.indptr.numel() - 1, n)
             self._bx = (n, torch.zeros(nbytes, dtype=torch.uint8, device=dev))
+            torch.cuda.current_stream(dev).synchronize()
         ws = self._bx[1]
         tg = (ctypes.c_int64 * n)(*[int(v) for v in targets])
-        while True:
-            cn, ce = self._cap
-            bufs = BatchSubgraphs(n, cn, ce, dev)
-            sgs = (L.gnnshap_subgraph * n)()
-            L.gnnshap_subgraph_batch_init(sgs, self.hops, cn, ce, _vp(bufs.node_gid), _vp(bufs.dst_ptr),
-                                          _vp(bufs.edge_src), _vp(bufs.edge_dst), _vp(bufs.edge_gid))
-            st = L.gnnshap_extract_batch(self.graph, tg, sgs, _vp(ws), ws.numel(), self.stream())
-            if st == L.OK:
-                break
-            self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
-                         max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
+        main = torch.cuda.current_stream(dev)
+        if self._xstream is None:
+            self._xstream = torch.cuda.Stream(device=dev)
+        xs = self._xstream
+        with torch.cuda.stream(xs):
+            while True:
+                cn, ce = self._cap
+                bufs = BatchSubgraphs(n, cn, ce, dev)
+                sgs = (L.gnnshap_subgraph * n)()
+                L.gnnshap_subgraph_batch_init(sgs, self.hops, cn, ce, _vp(bufs.node_gid), _vp(bufs.dst_ptr),
+                                              _vp(bufs.edge_src), _vp(bufs.edge_dst), _vp(bufs.edge_gid))
+                st = L.gnnshap_extract_batch(self.graph, tg, sgs, _vp(ws), ws.numel(), ctypes.c_void_p(xs.cuda_stream))
+                if st == L.OK:
+                    break
+                self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
+                             max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
+        main.wait_stream(xs)
+        for t in (bufs.node_gid, bufs.dst_ptr, bufs.edge_src, bufs.edge_dst, bufs.edge_gid):
+            t.record_stream(main)
         bufs.sgs = sgs
         bufs.targets = tg
         return bufs, sgs

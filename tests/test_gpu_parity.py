@@ -537,3 +537,28 @@ def test_explain_batch_against_oracle(dev):
         assert (err <= y_tolerance(y_ref, f0, f1)).all()
         phi_ref = wls.kernel_shap(m, w, game.values(m), f0, f1)
         _phi_close(r.phi.cpu().numpy().astype(np.float64), phi_ref)
+
+
+def test_explain_batch_repeated_calls_agree(dev):
+    """Repeated batched calls on the same targets (the launch sequence is
+    captured once and replayed) give the first call's outputs bit for bit,
+    with other device work between them, and equal the single-target calls."""
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    targets = cfg["targets"][:40]
+    fields = ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info")
+    first = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+    torch.cuda.synchronize()
+    ref = [{f: getattr(r, f).clone() for f in fields} for r in first]
+    for rep in range(3):
+        _say("batch replay", rep)
+        noise = torch.randn(1 << 20, device=dev).sum()           # unrelated work in between
+        one = ex.explain(targets[rep], cfg["p"], cfg["seed"])
+        again = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+        torch.cuda.synchronize()
+        assert torch.isfinite(noise)
+        for t, r in enumerate(again):
+            for f in fields:
+                assert torch.equal(getattr(r, f), ref[t][f]), (rep, t, f)
+        for f in fields:
+            assert torch.equal(getattr(one, f), ref[rep][f]), (rep, f)
