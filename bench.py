@@ -69,6 +69,7 @@ def cpu_baseline(cfg, seconds):
 HBM_PEAK_GBS = 8000.0
 VALU_FP32_TFLOPS = 78.6
 VALU_INT_TOPS = 39.3
+MFMA_FP32_TFLOPS = 157.3
 
 
 def work_model(kernel, results, dims):
@@ -76,9 +77,12 @@ def work_model(kernel, results, dims):
 
     k_solve_mid / k_solve_one_batch (one-workgroup solves)
                    M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
-    k_eval_l2, k_eval_rows
+    k_eval_l2, k_eval_rows, k_eval_rows_mx
                    (k/2) M h useful MACs per target (complement pairs cover every
-                   player-feature product once) + the layer-1 logit dot products
+                   player-feature product once) + the layer-1 logit dot products;
+                   k_eval_rows_mx runs the contraction on fp32 MFMA, so its roof is
+                   the fp32 MFMA peak (the dense 0/1 product it issues is twice the
+                   useful count, which is what is reported)
     k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
                    per 64 rows and pair
     k_sample       k x ceil(M/64) x 8 bytes of masks + 4 k bytes of weights written
@@ -98,7 +102,7 @@ def work_model(kernel, results, dims):
         if base in ("k_solve_mid", "k_solve_one"):
             if path == 1:
                 tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
-        elif base in ("k_eval_l2", "k_eval_rows"):
+        elif base in ("k_eval_l2", "k_eval_rows", "k_eval_rows_mx"):
             n1 = r.sub.sg.hop_ptr[2]
             tot += 2.0 * ((k / 2.0) * M * h + k * n1 * h)
         elif base == "k_gram":
@@ -113,13 +117,15 @@ def work_model(kernel, results, dims):
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
     if base == "k_gram":
         return tot, "Tops/s", "alu", VALU_INT_TOPS
+    if base == "k_eval_rows_mx":
+        return tot, "TFLOP/s", "mfma", MFMA_FP32_TFLOPS
     return tot, "TFLOP/s", "alu", VALU_FP32_TFLOPS
 
 
 CANDIDATES = {
-    "batch": ["k_eval_rows_batch", "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_part_batch",
+    "batch": ["k_eval_rows_mx_batch", "k_eval_rows_batch", "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_part_batch",
               "k_sample_batch"],
-    "streams": ["k_solve_mid", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
+    "streams": ["k_solve_mid", "k_eval_rows_mx", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
 }
 
 

@@ -711,6 +711,212 @@ __global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows(
                     ctl, fef, y_rows, blockIdx.x);
 }
 
+// The same pass for h <= 16 on fp32 MFMA.  Layer 1 at node x of H_1 under
+// a coalition c is a contraction over the players entering x:
+//   acc[f][c] = sum_e Z^1[src e][f] * coef[e][c],
+//   coef[e][c] = [e in c] * d_c(src e)^-1/2,
+// so a wavefront evaluates 64 coalitions as four 16 x 16 output tiles
+// (features x coalitions) with v_mfma_f32_16x16x4f32, four players per step:
+// A (16 features x 4 players) is the staged Z^1 rows, shared by the tiles,
+// B (4 players x 16 coalitions) the mask bit ANDed into the bits of
+// d^-1/2, which a first phase computes for every destination and coalition
+// of the workgroup.  Per node, lane (rl, g) then holds features 4g..4g+3 of
+// coalition rl of each tile: bias, ReLU and the explained logit's weights
+// are applied in registers, the four lane groups summed by two butterflies,
+// and layer 2 at the target accumulates as in the one-thread-per-coalition
+// kernel.  Each coalition's value depends on its own column only, so a row
+// gets the same value whichever rows share its workgroup.
+constexpr int kMxRows = 256;             // coalitions per workgroup (4 wavefronts)
+constexpr int kMxDvs = kMxRows + 16;     // row stride of the d^-1/2 table
+
+size_t rows_mx_lds_bytes(int64_t n_dst, int64_t n1, int64_t M) {
+  const int64_t nw = 2 * ((M + 63) / 64);
+  return sizeof(float) * static_cast<size_t>((M + 8) * 16 + n1 * 16 + (n_dst + 1) * kMxDvs + (nw + 2) * kMxRows +
+                                             (M + 8) + (n_dst + 1) + 2 * kMxRows);
+}
+
+typedef float mx4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void eval_rows_mx_body(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
+    const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src,
+    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zsrc, const int32_t* __restrict__ zidx,
+    const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
+    const int32_t* __restrict__ ctl, const float* __restrict__ fef, float* __restrict__ y_rows, int64_t block) {
+  constexpr int R = kMxRows, DVS = kMxDvs;
+  extern __shared__ __align__(16) float sm[];
+  const int Mi = static_cast<int>(M), nd = static_cast<int>(n_dst), n1i = static_cast<int>(n1);
+  const int nw = static_cast<int>(2 * wpr);                            // 32-bit words per mask row
+  float* zall = sm;                                                    // (M + 8) x 16: Z^1 of each player's source
+  float* zself = zall + (Mi + 8) * 16;                                 // n1 x 16: Z^1 of H_1
+  float* dv = zself + n1i * 16;                                        // (n_dst + 1) x DVS: d^-1/2, row n_dst = 1
+  uint32_t* m32 = reinterpret_cast<uint32_t*>(dv + (nd + 1) * DVS);  // (nw + 2) x R: mask words, two zero rows
+  int32_t* sall = reinterpret_cast<int32_t*>(m32 + (nw + 2) * R);     // M + 8: DVS x (source, or n_dst)
+  int32_t* dptr = sall + Mi + 8;                                       // n_dst + 1
+  int32_t* rowid = dptr + nd + 1;                                      // R
+  int32_t* live = rowid + R;                                           // R
+  const int64_t nr = rows_in_pass(dyn_count, 0, cap);
+  const int64_t b0 = block * R;
+  if (b0 >= nr) return;
+  const int tid = threadIdx.x;
+  const int c0 = ctl[0];
+  for (int e = tid; e < Mi + 8; e += R) {
+    const int32_t u = e < Mi ? edge_src[e] : nd;
+    sall[e] = (u < nd ? u : nd) * DVS;
+  }
+  for (int x = tid; x <= nd; x += R) dptr[x] = dst_ptr[x];
+  for (int t = tid; t < n1i * 16; t += R) {
+    const int x = t >> 4, f = t & 15;
+    zself[t] = f < h ? zrow(Zsrc, zidx, x, h)[f] : 0.f;
+  }
+#pragma unroll 4
+  for (int t = tid; t < (Mi + 8) * 16; t += R) {
+    const int e = t >> 4, f = t & 15;
+    zall[t] = (e < Mi && f < h) ? zrow(Zsrc, zidx, edge_src[e], h)[f] : 0.f;
+  }
+  // phase 1, one thread per coalition: its row, mask words (transposed),
+  // d^-1/2 of every destination, and whether any player enters the target
+  const int64_t bi = b0 + tid;
+  const bool valid = bi < nr;
+  const int64_t row = valid ? (rows ? static_cast<int64_t>(rows[bi]) : bi) : 0;
+  rowid[tid] = static_cast<int32_t>(row);
+  {
+    const uint64_t* mrow = masks + row * wpr;
+    for (int j = 0; j < wpr; ++j) {
+      const uint64_t word = valid ? mrow[j] : 0;
+      m32[(2 * j) * R + tid] = static_cast<uint32_t>(word);
+      m32[(2 * j + 1) * R + tid] = static_cast<uint32_t>(word >> 32);
+    }
+    m32[nw * R + tid] = 0;
+    m32[(nw + 1) * R + tid] = 0;
+  }
+  __syncthreads();
+  for (int x = 0; x < nd; ++x) {
+    const int e0 = dptr[x], e1 = dptr[x + 1];
+    int cnt = 0;
+    for (int j = e0 >> 5; e1 > e0 && j <= ((e1 - 1) >> 5); ++j) {
+      uint32_t word = m32[j * R + tid];
+      const int lo = j * 32;
+      if (e0 > lo) word &= ~0u << (e0 - lo);
+      if (e1 < lo + 32) word &= (1u << (e1 - lo)) - 1;
+      cnt += __popc(word);
+    }
+    if (x == 0) live[tid] = cnt > 0;
+    // 1 + deg >= 1: the hardware reciprocal square root needs no denormal scaling
+    dv[x * DVS + tid] = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(cnt));
+  }
+  dv[nd * DVS + tid] = 1.0f;
+  __syncthreads();
+  // phase 2, one wavefront per 64 coalitions
+  const int lane = tid & 63, rl = lane & 15, g = lane >> 4;
+  const int cb = (tid & ~63) + rl;               // coalition of lane (rl, g) in tile t: cb + 16 t
+  float b1v[4], w2v[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int f = 4 * g + r;
+    b1v[r] = (b1 && f < h) ? b1[f] : 0.f;
+    w2v[r] = f < h ? W2[static_cast<int64_t>(f) * C + c0] : 0.f;
+  }
+  float t0v[4], acc2[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) t0v[t] = acc2[t] = 0.f;
+  for (int x = 0; x < n1i; ++x) {
+    const int e0 = __builtin_amdgcn_readfirstlane(dptr[x]);
+    const int e1 = __builtin_amdgcn_readfirstlane(dptr[x + 1]);
+    const int ng = (e1 - e0 + 3) >> 2;           // steps of four players
+    mx4_t D[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) D[t] = mx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int q0 = 0; q0 < ng; q0 += 8) {
+      // lane (rl, g) takes players s, s + 4, ..., s + 28: one 32-bit window per tile
+      const int s = e0 + 4 * q0 + g;
+      const int j = s >> 5, sh = s & 31;
+      uint32_t win[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const uint32_t lo = m32[j * R + cb + 16 * t], hi = m32[(j + 1) * R + cb + 16 * t];
+        win[t] = static_cast<uint32_t>(((static_cast<uint64_t>(hi) << 32) | lo) >> sh);
+      }
+      const int nq = ng - q0 < 8 ? ng - q0 : 8;
+      // the next step's source and Z^1 value are read ahead (the padding
+      // rows keep them in bounds)
+      int e = s;
+      int uo = sall[e];
+      float z = zall[e * 16 + rl];
+      for (int q = 0; q < nq; ++q) {
+        const float a = e < e1 ? z : 0.f;
+        float dvv[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) dvv[t] = dv[uo + cb + 16 * t];
+        e += 4;
+        uo = sall[e];
+        z = zall[e * 16 + rl];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int bit = __builtin_amdgcn_sbfe(static_cast<int>(win[t]), 4 * q, 1);   // 0 or -1
+          const float bv = __int_as_float(__float_as_int(dvv[t]) & bit);
+          D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv, D[t], 0, 0, 0);
+        }
+      }
+    }
+    const float4 zs = *reinterpret_cast<const float4*>(zself + x * 16 + 4 * g);
+    const float zsv[4] = {zs.x, zs.y, zs.z, zs.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int c = cb + 16 * t;
+      const float dx = dv[x * DVS + c];
+      float p = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float hv = fmaxf(fmaf(dx, fmaf(dx, zsv[r], D[t][r]), b1v[r]), 0.f);
+        p = fmaf(hv, w2v[r], p);
+      }
+      p += __shfl_xor(p, 16);
+      p += __shfl_xor(p, 32);
+      if (x == 0) {
+        t0v[t] = p;
+      } else if ((m32[((x - 1) >> 5) * R + c] >> ((x - 1) & 31)) & 1) {
+        acc2[t] += dx * p;
+      }
+    }
+  }
+  // lane (rl, g) writes coalition rl of tile g; layer 2 at the target, or
+  // f(empty) when no player enters the target (Sec. 3.4.1)
+  float t0 = t0v[0], a2 = acc2[0];
+#pragma unroll
+  for (int t = 1; t < 4; ++t) {
+    if (g == t) {
+      t0 = t0v[t];
+      a2 = acc2[t];
+    }
+  }
+  const int c = cb + 16 * g;
+  if (b0 + c < nr) {
+    const float dv0 = dv[c];
+    y_rows[rowid[c]] = (live[c] || !fef) ? dv0 * (a2 + dv0 * t0) + (b2 ? b2[c0] : 0.f) : fef[0];
+  }
+}
+
+__global__ void __launch_bounds__(kMxRows) k_eval_rows_mx(
+    const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
+    const int32_t* dyn_count, const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src,
+    int64_t n_dst, int64_t n1, int64_t M, const float* __restrict__ Zsrc, const int32_t* __restrict__ zidx,
+    const float* __restrict__ b1, const float* __restrict__ W2, const float* __restrict__ b2, int h, int C,
+    const int32_t* __restrict__ ctl, const float* __restrict__ fef, float* __restrict__ y_rows) {
+  eval_rows_mx_body(masks, wpr, rows, cap, dyn_count, dst_ptr, edge_src, n_dst, n1, M, Zsrc, zidx, b1, W2, b2, h, C,
+                    ctl, fef, y_rows, blockIdx.x);
+}
+
+// The per-coalition main pass of a two-layer model (h <= 32): its LDS bytes,
+// 0 when the target's shapes do not fit, and the coalitions per workgroup.
+size_t rows_pass_lds(int64_t n_dst, int64_t n1, int64_t M, int h) {
+  size_t b = 0;
+  if (h <= 16) b = rows_mx_lds_bytes(n_dst, n1, M);
+  else if (h <= 32) b = rows_lds_bytes(n_dst, n1, M, 32);
+  return b <= 65536 ? b : 0;
+}
+int rows_pass_block(int h) { return h <= 16 ? kMxRows : kRowsPerBlock; }
+
 __device__ __forceinline__ void pick_class(const float* __restrict__ sp_y, int C, int requested, int32_t* ctl,
                                            int32_t* class_out, float* f_empty_full) {
   int c = requested;
@@ -1045,14 +1251,13 @@ int launch_fused_l2(hipStream_t s, const gnnshap_subgraph* sg, const gnnshap_gcn
                                    sh.n_dst, sh.nd[1], w.Zc[1], b1, m->W[1], b2, h, C, w.ctl, all_classes, \
                                    tbr, y_rows, w.sp_y)
   GS_TIMED("k_eval_l2", s);
-  const int H = h <= 16 ? 16 : 32;
-  const size_t lds_rows = rows_lds_bytes(sh.n_dst, sh.nd[1], sg->num_edges, H);
-  if (!all_classes && row_off == 0 && h <= 32 && lds_rows <= 65536) {
-    const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(cap, kRowsPerBlock));
-    if (H == 16)
-      k_eval_rows<16><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src,
-                                                          sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], nullptr, b1,
-                                                          m->W[1], b2, h, C, w.ctl, nullptr, y_rows);
+  const size_t lds_rows = rows_pass_lds(sh.n_dst, sh.nd[1], sg->num_edges, h);
+  if (!all_classes && row_off == 0 && lds_rows > 0) {
+    const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(cap, rows_pass_block(h)));
+    if (h <= 16)
+      k_eval_rows_mx<<<gr, kMxRows, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src, sh.n_dst,
+                                                   sh.nd[1], sg->num_edges, w.Zc[1], nullptr, b1, m->W[1], b2, h, C,
+                                                   w.ctl, nullptr, y_rows);
     else
       k_eval_rows<32><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, rows, cap, dyn, sg->dst_ptr, sg->edge_src,
                                                           sh.n_dst, sh.nd[1], sg->num_edges, w.Zc[1], nullptr, b1,
@@ -1152,6 +1357,15 @@ __global__ void __launch_bounds__(256) k_eval_l2_batch(const gnnshap::EvalJob* _
 // Main pass of the jobs that take the one-thread-per-coalition kernel;
 // all: every row of the job (pruned rows get f(empty) on the way), else the
 // live rows listed by k_live_batch.
+__global__ void __launch_bounds__(kMxRows) k_eval_rows_mx_batch(const gnnshap::EvalJob* __restrict__ jobs,
+                                                                gnnshap::EvalModel md, bool all) {
+  const gnnshap::EvalJob J = jobs[blockIdx.y];
+  if (!J.rows_ok) return;
+  eval_rows_mx_body(J.masks, J.wpr, all ? nullptr : J.live_rows, J.k, all ? nullptr : J.ctl + 1, J.dst_ptr,
+                    J.edge_src, J.n_dst, J.n1, J.M, J.Zc1, nullptr, md.b1, md.W2, md.b2, md.h, md.C, J.ctl, J.fef,
+                    J.y, blockIdx.x);
+}
+
 template <int H>
 __global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows_batch(const gnnshap::EvalJob* __restrict__ jobs,
                                                                    gnnshap::EvalModel md, bool all) {
@@ -1218,10 +1432,9 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   // kernel in one pass take two launches: the end coalitions (with the
   // class), then every row (pruned rows get f(empty) on the way), reading
   // X W_1 through the subgraph's node ids when it is given.
-  const int H = sh.dims[1] <= 16 ? 16 : 32;
-  const size_t lds_rows = rows_lds_bytes(sh.n_dst, sh.nd[1], sg->num_edges, H);
-  const bool direct = ends_ok(sh) && fused_l2_ok(sh, k, false) && sh.dims[1] <= 32 && lds_rows <= 65536 &&
-                      sh.tile >= k && gnnshap::ceil_div(k, kRowsPerBlock) <= INT32_MAX;
+  const size_t lds_rows = rows_pass_lds(sh.n_dst, sh.nd[1], sg->num_edges, sh.dims[1]);
+  const bool direct = ends_ok(sh) && fused_l2_ok(sh, k, false) && lds_rows > 0 && sh.tile >= k &&
+                      gnnshap::ceil_div(k, kRowsPerBlock) <= INT32_MAX;
   if (direct) {
     if (!m->XW1) {
       if (int st = launch_gemm(s, X, sh.dims[0], sg->node_gid, nullptr, m->W[0], sh.dims[1], w.Zc[1], sh.dims[1], 0,
@@ -1236,13 +1449,12 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
         sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], m->XW1, sg->node_gid, sh.n_nodes, b1, m->W[1], b2,
         sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out, f_empty_full);
     GS_LAUNCHED();
-    const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(k, kRowsPerBlock));
-    GS_TIMED("k_eval_rows", s);
-    if (H == 16)
-      k_eval_rows<16><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, nullptr, k, nullptr, sg->dst_ptr,
-                                                          sg->edge_src, sh.n_dst, sh.nd[1], sg->num_edges, Zsrc, zidx,
-                                                          b1, m->W[1], b2, sh.dims[1], sh.dims[2], w.ctl,
-                                                          f_empty_full, y);
+    const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(k, rows_pass_block(sh.dims[1])));
+    GS_TIMED(sh.dims[1] <= 16 ? "k_eval_rows_mx" : "k_eval_rows", s);
+    if (sh.dims[1] <= 16)
+      k_eval_rows_mx<<<gr, kMxRows, lds_rows, s>>>(masks, sh.wpr, nullptr, k, nullptr, sg->dst_ptr, sg->edge_src,
+                                                   sh.n_dst, sh.nd[1], sg->num_edges, Zsrc, zidx, b1, m->W[1], b2,
+                                                   sh.dims[1], sh.dims[2], w.ctl, f_empty_full, y);
     else
       k_eval_rows<32><<<gr, kRowsPerBlock, lds_rows, s>>>(masks, sh.wpr, nullptr, k, nullptr, sg->dst_ptr,
                                                           sg->edge_src, sh.n_dst, sh.nd[1], sg->num_edges, Zsrc, zidx,
@@ -1408,9 +1620,9 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
     GS_LAUNCHED();
   }
   if (rows_jobs > 0) {
-    GS_TIMED("k_eval_rows_batch", s);
-    const dim3 g(static_cast<unsigned>(ceil_div(max_k, kRowsPerBlock)), nn);
-    if (md.h <= 16) k_eval_rows_batch<16><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md, all);
+    GS_TIMED(md.h <= 16 ? "k_eval_rows_mx_batch" : "k_eval_rows_batch", s);
+    const dim3 g(static_cast<unsigned>(ceil_div(max_k, rows_pass_block(md.h))), nn);
+    if (md.h <= 16) k_eval_rows_mx_batch<<<g, kMxRows, rows_lds, s>>>(jobs, md, all);
     else k_eval_rows_batch<32><<<g, kRowsPerBlock, rows_lds, s>>>(jobs, md, all);
   }
   GS_LAUNCHED();
@@ -1423,8 +1635,6 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
 
 // Whether a target's main pass takes the one-thread-per-coalition kernel, and its LDS.
 size_t gnnshap::eval_rows_lds(const gnnshap_subgraph* sg, const gnnshap_gcn* m) {
-  const int h = m->dims[1];
-  if (m->num_layers != 2 || h > 32) return 0;
-  const size_t b = rows_lds_bytes(sg->num_dst, sg->hop_ptr[2], sg->num_edges, h <= 16 ? 16 : 32);
-  return b <= 65536 ? b : 0;
+  if (m->num_layers != 2) return 0;
+  return rows_pass_lds(sg->num_dst, sg->hop_ptr[2], sg->num_edges, m->dims[1]);
 }
