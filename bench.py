@@ -86,7 +86,8 @@ def work_model(kernel, results, dims):
     k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
                    per 64 rows and pair
     k_sample       k x ceil(M/64) x 8 bytes of masks + 4 k bytes of weights written
-    k_rhs_part     (k/2) x ceil(M/64) x 8 bytes of masks + 4 k bytes of y read
+    k_rhs_part, k_rhs_tile
+                   (k/2) x ceil(M/64) x 8 bytes of masks + 4 k bytes of y read
     (a *_batch kernel does the same work for every target of the batch)
     """
     from paper_2401_04829_amd import _lib
@@ -110,10 +111,10 @@ def work_model(kernel, results, dims):
                 tot += (kr / 64.0) * M * (M + 1) / 2.0
         elif base == "k_sample":
             tot += k * wpr * 8.0 + 4.0 * k
-        elif base == "k_rhs_part":
+        elif base in ("k_rhs_part", "k_rhs_tile"):
             if not batched or path in (1, 2):
                 tot += (k / 2.0) * wpr * 8.0 + 4.0 * k
-    if base in ("k_sample", "k_rhs_part"):
+    if base in ("k_sample", "k_rhs_part", "k_rhs_tile"):
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
     if base == "k_gram":
         return tot, "Tops/s", "alu", VALU_INT_TOPS
@@ -123,9 +124,9 @@ def work_model(kernel, results, dims):
 
 
 CANDIDATES = {
-    "batch": ["k_eval_rows_mx_batch", "k_eval_rows_batch", "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_part_batch",
+    "batch": ["k_eval_rows_mx_batch", "k_eval_rows_batch", "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_tile_batch",
               "k_sample_batch"],
-    "streams": ["k_solve_mid", "k_eval_rows_mx", "k_eval_l2", "k_rhs_part", "k_gram", "k_sample"],
+    "streams": ["k_solve_mid", "k_eval_rows_mx", "k_eval_l2", "k_rhs_tile", "k_gram", "k_sample"],
 }
 
 

@@ -71,7 +71,7 @@ struct SolveJob {
   float* phi;
   int32_t* info;
   const gnnshap_class* cls;  // device copy
-  int64_t ncls, M, wpr, half, rb0, kr, nrb, ld, nch, rpc;
+  int64_t ncls, M, wpr, half, rb0, kr, nrb, ld, nch;
   double alpha, wr;
   uint64_t* T;
   int32_t* counts;

@@ -721,11 +721,12 @@ __global__ void __launch_bounds__(kRowsPerBlock) k_eval_rows(
 // B (4 players x 16 coalitions) the mask bit ANDed into the bits of
 // d^-1/2, which a first phase computes for every destination and coalition
 // of the workgroup.  Per node, lane (rl, g) then holds features 4g..4g+3 of
-// coalition rl of each tile: bias, ReLU and the explained logit's weights
-// are applied in registers, the four lane groups summed by two butterflies,
-// and layer 2 at the target accumulates as in the one-thread-per-coalition
-// kernel.  Each coalition's value depends on its own column only, so a row
-// gets the same value whichever rows share its workgroup.
+// coalition rl of each tile: self loop, bias and ReLU are applied in
+// registers and the result, weighted by the node's layer-2 coefficient, is
+// accumulated per feature; the explained logit's weights and the sum over
+// the four lane groups (two butterflies) come once, after the last node.
+// Each coalition's value depends on its own column only, so a row gets the
+// same value whichever rows share its workgroup.
 constexpr int kMxRows = 256;             // coalitions per workgroup (4 wavefronts)
 constexpr int kMxDvs = kMxRows + 16;     // row stride of the d^-1/2 table
 
@@ -817,9 +818,11 @@ __device__ __forceinline__ void eval_rows_mx_body(
     b1v[r] = (b1 && f < h) ? b1[f] : 0.f;
     w2v[r] = f < h ? W2[static_cast<int64_t>(f) * C + c0] : 0.f;
   }
-  float t0v[4], acc2[4];
+  float S[4][4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) t0v[t] = acc2[t] = 0.f;
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) S[t][r] = 0.f;
   for (int x = 0; x < n1i; ++x) {
     const int e0 = __builtin_amdgcn_readfirstlane(dptr[x]);
     const int e1 = __builtin_amdgcn_readfirstlane(dptr[x + 1]);
@@ -838,62 +841,81 @@ __device__ __forceinline__ void eval_rows_mx_body(
         win[t] = static_cast<uint32_t>(((static_cast<uint64_t>(hi) << 32) | lo) >> sh);
       }
       const int nq = ng - q0 < 8 ? ng - q0 : 8;
-      // the next step's source and Z^1 value are read ahead (the padding
-      // rows keep them in bounds)
-      int e = s;
-      int uo = sall[e];
-      float z = zall[e * 16 + rl];
-      for (int q = 0; q < nq; ++q) {
-        const float a = e < e1 ? z : 0.f;
-        float dvv[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) dvv[t] = dv[uo + cb + 16 * t];
-        e += 4;
-        uo = sall[e];
-        z = zall[e * 16 + rl];
+      auto step = [&](int q, float a, const float* dvv) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int bit = __builtin_amdgcn_sbfe(static_cast<int>(win[t]), 4 * q, 1);   // 0 or -1
           const float bv = __int_as_float(__float_as_int(dvv[t]) & bit);
           D[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv, D[t], 0, 0, 0);
         }
+      };
+      // two steps at a time: both steps' reads are issued before the first product
+      int q = 0;
+      for (; q + 1 < nq; q += 2) {
+        const int ea = s + 4 * q, eb = ea + 4;
+        const int ua = sall[ea], ub = sall[eb];
+        const float za = zall[ea * 16 + rl], zb = zall[eb * 16 + rl];
+        float da[4], db[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          da[t] = dv[ua + cb + 16 * t];
+          db[t] = dv[ub + cb + 16 * t];
+        }
+        __builtin_amdgcn_sched_barrier(0);   // keep every read ahead of the products
+        step(q, ea < e1 ? za : 0.f, da);
+        step(q + 1, eb < e1 ? zb : 0.f, db);
+      }
+      if (q < nq) {
+        const int ea = s + 4 * q;
+        const int ua = sall[ea];
+        const float za = zall[ea * 16 + rl];
+        float da[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) da[t] = dv[ua + cb + 16 * t];
+        step(q, ea < e1 ? za : 0.f, da);
       }
     }
+    // H^1 at node x and its weight in layer 2 at the target: d_x^-1/2 when
+    // node x is the target itself or the source of a player in the
+    // coalition, else 0.  The explained logit is linear in these terms, so
+    // S accumulates weight * H^1 per feature and the sum over features (the
+    // four lane groups) is taken once at the end.
     const float4 zs = *reinterpret_cast<const float4*>(zself + x * 16 + 4 * g);
     const float zsv[4] = {zs.x, zs.y, zs.z, zs.w};
+    const int xw = x > 0 ? ((x - 1) >> 5) * R : 0, xb = (x - 1) & 31;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int c = cb + 16 * t;
       const float dx = dv[x * DVS + c];
-      float p = 0.f;
+      const float wx = (x == 0 || ((m32[xw + c] >> xb) & 1)) ? dx : 0.f;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float hv = fmaxf(fmaf(dx, fmaf(dx, zsv[r], D[t][r]), b1v[r]), 0.f);
-        p = fmaf(hv, w2v[r], p);
-      }
-      p += __shfl_xor(p, 16);
-      p += __shfl_xor(p, 32);
-      if (x == 0) {
-        t0v[t] = p;
-      } else if ((m32[((x - 1) >> 5) * R + c] >> ((x - 1) & 31)) & 1) {
-        acc2[t] += dx * p;
+        S[t][r] = fmaf(wx, hv, S[t][r]);
       }
     }
   }
-  // lane (rl, g) writes coalition rl of tile g; layer 2 at the target, or
+  // explained logit per coalition: sum over features, then layer 2's outer
+  // d_target^-1/2 and bias; lane (rl, g) writes coalition rl of tile g, or
   // f(empty) when no player enters the target (Sec. 3.4.1)
-  float t0 = t0v[0], a2 = acc2[0];
+  float pt[4];
 #pragma unroll
-  for (int t = 1; t < 4; ++t) {
-    if (g == t) {
-      t0 = t0v[t];
-      a2 = acc2[t];
-    }
+  for (int t = 0; t < 4; ++t) {
+    float p = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p = fmaf(S[t][r], w2v[r], p);
+    p += __shfl_xor(p, 16);
+    p += __shfl_xor(p, 32);
+    pt[t] = p;
   }
+  float p = pt[0];
+#pragma unroll
+  for (int t = 1; t < 4; ++t)
+    if (g == t) p = pt[t];
   const int c = cb + 16 * g;
   if (b0 + c < nr) {
     const float dv0 = dv[c];
-    y_rows[rowid[c]] = (live[c] || !fef) ? dv0 * (a2 + dv0 * t0) + (b2 ? b2[c0] : 0.f) : fef[0];
+    y_rows[rowid[c]] = (live[c] || !fef) ? fmaf(dv0, p, b2 ? b2[c0] : 0.f) : fef[0];
   }
 }
 

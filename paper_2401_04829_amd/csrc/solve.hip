@@ -69,6 +69,13 @@ int64_t n_chunks(int64_t half, int64_t wpr) {
   return c < 1 ? 1 : c;
 }
 
+// Row chunks of the chunked right-hand side (systems of at most kMidMax players).
+constexpr int kTileRows = 256;
+constexpr int kTileWords = (kMidMax + 63) / 64;          // mask words per row at most
+constexpr int kTileClasses = 256;                         // classes of a system of <= kMidMax players
+
+int64_t tile_chunks(int64_t half) { return gnnshap::ceil_div(half, kTileRows); }
+
 Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   Ws w;
   const int64_t M = p->num_players;
@@ -81,7 +88,7 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   w.usum = c.take<int64_t>(M);
   w.scal = c.take<double>(16);
   w.dz = c.take<double>(half);
-  w.part = c.take<double>(n_chunks(half, p->words_per_row) * M);
+  w.part = c.take<double>(std::max(n_chunks(half, p->words_per_row), tile_chunks(half)) * M);
   w.dv = c.take<double>(M);
   w.bsum = c.take<double>(gnnshap::ceil_div(M, 256));
   w.rhs = c.take<float>(M);
@@ -406,6 +413,90 @@ __global__ void __launch_bounds__(256) k_rhs_center(const double* __restrict__ d
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (j < M) rhs[j] = static_cast<float>(dv[j] - mean);
 }
+
+// Right-hand side of one chunk of kTileRows representative rows, for systems
+// of at most kMidMax players: part[chunk, j] = sum_b dz_b m_bj over the
+// chunk, with dz_b as in dz_body.  Thread t forms dz of row chunk * kTileRows
+// + t (the class found in an LDS copy of the class table) and stages the
+// row's mask words; each wavefront then sums (word column, quarter of the
+// chunk) items over their 64 rows in order, and the quarters are added in
+// order.  Every value is fixed by the chunking alone.
+__device__ __forceinline__ void rhs_tile_body(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
+                                              int64_t M, const float* __restrict__ y,
+                                              const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                              const float* __restrict__ fef, double* __restrict__ part,
+                                              int64_t chunk) {
+  __shared__ int64_t c_begin[kTileClasses];
+  __shared__ int32_t c_size[kTileClasses];
+  __shared__ double c_weight[kTileClasses];
+  __shared__ double zd[kTileRows];
+  __shared__ uint32_t mw[kTileRows * 2 * kTileWords];    // row t: its 2 wpr 32-bit words
+  __shared__ double qs[4 * kTileWords * 64];             // (quarter, word column, bit)
+  const int t = threadIdx.x;
+  const int nc = static_cast<int>(ncls), nw = static_cast<int>(2 * wpr);
+  for (int i = t; i < nc; i += kTileRows) {
+    c_begin[i] = cls[i].row_begin;
+    c_size[i] = cls[i].size;
+    c_weight[i] = cls[i].weight;
+  }
+  const int64_t b = chunk * kTileRows + t;
+  const bool in = b < half;
+  for (int w = 0; w < wpr; ++w) {
+    const uint64_t word = in ? masks[b * wpr + w] : 0;
+    mw[t * nw + 2 * w] = static_cast<uint32_t>(word);
+    mw[t * nw + 2 * w + 1] = static_cast<uint32_t>(word >> 32);
+  }
+  const float yb = in ? y[b] : 0.f, yc = in ? y[b + half] : 0.f;
+  __syncthreads();
+  double d = 0.0;
+  if (in) {
+    const double Md = static_cast<double>(M);
+    const double f0 = static_cast<double>(fef[0]);
+    const double delta = static_cast<double>(fef[1]) - f0;
+    int lo = 0, hi = nc - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (c_begin[mid] <= b) lo = mid; else hi = mid - 1;
+    }
+    const double w = c_weight[lo];
+    const int64_t pc = c_size[lo];
+    const double z1 = w * (static_cast<double>(yb) - f0 - delta / Md * static_cast<double>(pc));
+    const double z2 = w * (static_cast<double>(yc) - f0 - delta / Md * static_cast<double>(M - pc));
+    d = z1 - z2;
+  }
+  zd[t] = d;
+  __syncthreads();
+  const int lane = t & 63, wv = t >> 6;
+  const int word = lane >> 5, bit = lane & 31;
+  for (int it = wv; it < 4 * wpr; it += 4) {
+    const int w = it >> 2, qq = it & 3;
+    double acc = 0.0;
+#pragma unroll 8
+    for (int r = qq * 64; r < qq * 64 + 64; ++r) {
+      const uint32_t m = mw[r * nw + 2 * w + word];
+      acc = fma(static_cast<double>((m >> bit) & 1u), zd[r], acc);   // adds zd[r] exactly when the bit is set
+    }
+    qs[(qq * kTileWords + w) * 64 + lane] = acc;
+  }
+  __syncthreads();
+  for (int64_t j = t; j < M; j += kTileRows) {
+    const int w = static_cast<int>(j >> 6), l = static_cast<int>(j & 63);
+    double sum = 0.0;
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) sum += qs[(qq * kTileWords + w) * 64 + l];
+    part[chunk * M + j] = sum;
+  }
+}
+
+__global__ void __launch_bounds__(kTileRows) k_rhs_tile(const uint64_t* __restrict__ masks, int64_t wpr, int64_t half,
+                                                        int64_t M, const float* __restrict__ y,
+                                                        const gnnshap_class* __restrict__ cls, int64_t ncls,
+                                                        const float* __restrict__ fef, double* __restrict__ part) {
+  rhs_tile_body(masks, wpr, half, M, y, cls, ncls, fef, part, blockIdx.x);
+}
+
+// Whether a system's right-hand side takes the chunked kernel above.
+bool rhs_tiled(int64_t M, int64_t ncls) { return M <= kMidMax && ncls <= kTileClasses; }
 
 __global__ void k_zero_info(int32_t* info) { *info = 0; }
 
@@ -1299,15 +1390,10 @@ __global__ void __launch_bounds__(256) k_gram_batch(const gnnshap::SolveJob* __r
   gram_part_body(J.T, w0, w0 + kGramChunk < J.nrb ? w0 + kGramChunk : J.nrb, J.M, J.ld, J.counts, It, Jt);
 }
 
-__global__ void __launch_bounds__(256) k_dz_batch(const gnnshap::SolveJob* __restrict__ jobs) {
+__global__ void __launch_bounds__(kTileRows) k_rhs_tile_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
-  dz_body(J.y, J.half, J.M, J.cls, J.ncls, J.fef, J.dz, static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x);
-}
-
-__global__ void __launch_bounds__(256) k_rhs_part_batch(const gnnshap::SolveJob* __restrict__ jobs) {
-  const gnnshap::SolveJob J = jobs[blockIdx.z];
-  if (blockIdx.y >= J.nch) return;
-  rhs_part_body(J.masks, J.wpr, J.half, J.M, J.dz, J.rpc, J.part, blockIdx.x, blockIdx.y);
+  if (blockIdx.x >= J.nch) return;
+  rhs_tile_body(J.masks, J.wpr, J.half, J.M, J.y, J.cls, J.ncls, J.fef, J.part, blockIdx.x);
 }
 
 // Row sums of the counts and the summed right-hand side, for the mid-size jobs.
@@ -1666,20 +1752,26 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     }
     GS_LAUNCHED();
   }
-  const int64_t nch = n_chunks(half, wpr);
-  const int64_t rpc = gnnshap::ceil_div(half, nch);
-  k_dz<<<static_cast<unsigned>(gnnshap::ceil_div(half, 256)), 256, 0, s>>>(y, half, M, w.classes, plan->num_classes,
-                                                                           f_empty_full, w.dz);
-  GS_LAUNCHED();
-  {
+  static bool mid_lds = false;
+  const bool mid = M <= kMidMax && allow_lds(reinterpret_cast<const void*>(&k_solve_mid), kMidLds, mid_lds);
+  const bool tiled = mid && rhs_tiled(M, plan->num_classes);
+  const int64_t nch = tiled ? tile_chunks(half) : n_chunks(half, wpr);
+  if (tiled) {
+    GS_TIMED("k_rhs_tile", s);
+    k_rhs_tile<<<static_cast<unsigned>(nch), kTileRows, 0, s>>>(masks, wpr, half, M, y, w.classes,
+                                                               plan->num_classes, f_empty_full, w.part);
+  } else {
+    const int64_t rpc = gnnshap::ceil_div(half, nch);
+    k_dz<<<static_cast<unsigned>(gnnshap::ceil_div(half, 256)), 256, 0, s>>>(y, half, M, w.classes,
+                                                                             plan->num_classes, f_empty_full, w.dz);
+    GS_LAUNCHED();
     GS_TIMED("k_rhs_part", s);
     k_rhs_part<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(wpr, 4)), static_cast<unsigned>(nch)), 256, 0, s>>>(
         masks, wpr, half, M, w.dz, rpc, w.part);
   }
   GS_LAUNCHED();
 
-  static bool mid_lds = false;
-  if (M <= kMidMax && allow_lds(reinterpret_cast<const void*>(&k_solve_mid), kMidLds, mid_lds)) {
+  if (mid) {
     if (has_random) {
       k_rowsum<<<static_cast<unsigned>(gnnshap::ceil_div(M * 64, 256)), 256, 0, s>>>(counts, M, ld, w.usum);
       GS_LAUNCHED();
@@ -1817,7 +1909,7 @@ bool gnnshap::solve_batchable(const gnnshap_sample_plan* plan) {
     clear_error();
     return false;
   }
-  return plan->num_players <= kMidMax;
+  return plan->num_players <= kMidMax && rhs_tiled(plan->num_players, plan->num_classes);
 }
 
 size_t gnnshap::solve_slice_bytes(const gnnshap_sample_plan* plan) {
@@ -1840,8 +1932,7 @@ int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class
   job->kr = job->half - job->rb0;
   job->nrb = ceil_div(job->kr, 64);
   job->ld = ld_of(M);
-  job->nch = n_chunks(job->half, job->wpr);
-  job->rpc = ceil_div(job->half, job->nch);
+  job->nch = tile_chunks(job->half);      // batched systems have at most kMidMax players
   job->wr = job->kr > 0 ? plan->random_weight : 0.0;
   double alpha = 0.0;
   for (int64_t i = 0; i < plan->num_classes; ++i) {
@@ -1902,12 +1993,9 @@ int gnnshap::launch_solve_rhs(const SolveJob* jobs, int64_t n, int64_t max_M, in
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   const unsigned nn = static_cast<unsigned>(n);
-  k_dz_batch<<<dim3(static_cast<unsigned>(ceil_div(max_half, 256)), nn), 256, 0, s>>>(jobs);
-  GS_LAUNCHED();
   {
-    GS_TIMED("k_rhs_part_batch", s);
-    k_rhs_part_batch<<<dim3(static_cast<unsigned>(ceil_div(max_wpr, 4)), static_cast<unsigned>(max_nch), nn), 256, 0,
-                       s>>>(jobs);
+    GS_TIMED("k_rhs_tile_batch", s);
+    k_rhs_tile_batch<<<dim3(static_cast<unsigned>(max_nch), nn), kTileRows, 0, s>>>(jobs);
   }
   GS_LAUNCHED();
   k_rhs_sum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M, 256)), nn), 256, 0, s>>>(jobs);
