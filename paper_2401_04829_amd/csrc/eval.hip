@@ -965,22 +965,109 @@ size_t ends_lds_bytes(int64_t n_dst, int64_t n1, int h, int C) {
   return sizeof(float) * static_cast<size_t>(n_dst + n1 * C + nx * h + h + C);
 }
 
+// Extra LDS when the workgroup keeps Z^1 of the subgraph (n_nodes x h), the
+// players' sources (M), the node ids, the destinations' player ranges and
+// W_2 in LDS: global memory is then read once, in two rounds of independent
+// loads, and the per-node loops read LDS only.
+size_t ends_stage_bytes(int64_t n_nodes, int64_t n_dst, int64_t M, int h, int C) {
+  return sizeof(float) * static_cast<size_t>(n_nodes * h + M + n_nodes + n_dst + 1 + static_cast<int64_t>(h) * C);
+}
+
+// LDS of the end-coalition kernel, staged (S) when it fits in 64 KiB.
+size_t ends_launch_lds(int64_t n_dst, int64_t n1, int64_t n_nodes, int64_t M, int h, int C, bool* S) {
+  const size_t base = ends_lds_bytes(n_dst, n1, h, C);
+  const size_t staged = base + ends_stage_bytes(n_nodes, n_dst, M, h, C);
+  *S = staged <= 65536;
+  return *S ? staged : base;
+}
+
 // With XW1 given, the workgroup first gathers Zc (n_nodes x h) = the rows of
 // XW1 at the subgraph's node ids (for this kernel and the next ones);
 // afterwards thread 0 picks the explained class (requested, or argmax
-// f(E_c)) into ctl[0], class_out and f_empty_full.
+// f(E_c)) into ctl[0], class_out and f_empty_full.  The values do not depend
+// on S (only where the operands are read from).
+template <bool S>
 __device__ __forceinline__ void ends_l2_body(const int32_t* __restrict__ dst_ptr,
                                              const int32_t* __restrict__ edge_src, int64_t n_dst, int64_t n1,
-                                             float* Zc, const float* __restrict__ XW1,
+                                             int64_t M, float* Zc, const float* __restrict__ XW1,
                                              const int32_t* __restrict__ node_gid, int64_t n_nodes,
                                              const float* __restrict__ b1,
                                              const float* __restrict__ W2, const float* __restrict__ b2, int h,
                                              int C, float* __restrict__ sp_y, int requested, int32_t* ctl,
                                              int32_t* class_out, float* f_empty_full) {
   extern __shared__ __align__(16) float sm[];
-  if (XW1) {
+  const int tid = threadIdx.x;
+  const float* Zr = Zc;                 // operands as read below: global memory, or their LDS copies
+  const int32_t* er = edge_src;
+  const int32_t* dp = dst_ptr;
+  const float* w2 = W2;
+  float* rest = sm;
+  if constexpr (S) {
+    float* Zl = sm;                                                  // n_nodes x h
+    int32_t* el = reinterpret_cast<int32_t*>(Zl + n_nodes * h);     // M
+    int32_t* gl = el + M;                                            // n_nodes
+    int32_t* dl = gl + n_nodes;                                      // n_dst + 1
+    float* wl = reinterpret_cast<float*>(dl + n_dst + 1);           // h x C
+    for (int64_t e = tid; e < M; e += kEndsThreads) el[e] = edge_src[e];
+    if (XW1)
+      for (int64_t i = tid; i < n_nodes; i += kEndsThreads) gl[i] = node_gid[i];
+    for (int64_t x = tid; x <= n_dst; x += kEndsThreads) dl[x] = dst_ptr[x];
+    for (int64_t i = tid; i < static_cast<int64_t>(h) * C; i += kEndsThreads) wl[i] = W2[i];
+    __syncthreads();
+    const bool vec = (h & 3) == 0 && (reinterpret_cast<uintptr_t>(Zc) & 15) == 0 &&
+                     (!XW1 || (reinterpret_cast<uintptr_t>(XW1) & 15) == 0);
+    if (vec) {
+      // rows of four floats, eight loads in flight per thread
+      const int hq = h >> 2;
+      const int64_t total = n_nodes * hq;
+      for (int64_t t0 = tid; t0 < total; t0 += 8 * kEndsThreads) {
+        float4 v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int64_t t = t0 + q * kEndsThreads;
+          if (t < total) {
+            const int64_t i = t / hq, c4 = t % hq;
+            v[q] = XW1 ? reinterpret_cast<const float4*>(XW1 + static_cast<int64_t>(gl[i]) * h)[c4]
+                       : reinterpret_cast<const float4*>(Zc)[t];
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int64_t t = t0 + q * kEndsThreads;
+          if (t < total) {
+            reinterpret_cast<float4*>(Zl)[t] = v[q];
+            if (XW1) reinterpret_cast<float4*>(Zc)[t] = v[q];
+          }
+        }
+      }
+    } else {
+      const int64_t total = n_nodes * h;
+      for (int64_t t0 = tid; t0 < total; t0 += 8 * kEndsThreads) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int64_t t = t0 + q * kEndsThreads;
+          v[q] = t < total ? (XW1 ? XW1[static_cast<int64_t>(gl[t / h]) * h + t % h] : Zc[t]) : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int64_t t = t0 + q * kEndsThreads;
+          if (t < total) {
+            Zl[t] = v[q];
+            if (XW1) Zc[t] = v[q];
+          }
+        }
+      }
+    }
+    Zr = Zl;
+    er = el;
+    dp = dl;
+    w2 = wl;
+    rest = wl + static_cast<int64_t>(h) * C;
+    __syncthreads();
+  } else if (XW1) {
     const int64_t total = n_nodes * h;
-    for (int64_t t0 = threadIdx.x; t0 < total; t0 += 4 * kEndsThreads) {
+    for (int64_t t0 = tid; t0 < total; t0 += 4 * kEndsThreads) {
       float v[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -996,88 +1083,153 @@ __device__ __forceinline__ void ends_l2_body(const int32_t* __restrict__ dst_ptr
     __syncthreads();
   }
   const int64_t nx = h >= kEndsThreads ? 1 : kEndsThreads / h;
-  float* dinv = sm;                   // n_dst: full-coalition d^-1/2
+  float* dinv = rest;                 // n_dst: full-coalition d^-1/2
   float* tt = dinv + n_dst;           // n1 x C: H^1[x] . W_2[:, c] under the full coalition
   float* hv = tt + n1 * C;            // nx x h: H^1 rows of the current node chunk
   float* he = hv + nx * h;            // h: H^1 row of the target under the empty coalition
   float* te = he + h;                 // C
-  const int tid = threadIdx.x;
   for (int64_t x = tid; x < n_dst; x += kEndsThreads)
-    dinv[x] = rsqrtf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
+    dinv[x] = rsqrtf(1.0f + static_cast<float>(dp[x + 1] - dp[x]));
   const float d0 = rsqrtf(1.0f);      // degree factor of every node when no edge is present
   for (int f = tid; f < h; f += kEndsThreads)
-    he[f] = fmaxf(d0 * (0.0f + d0 * Zc[f]) + (b1 ? b1[f] : 0.f), 0.f);
+    he[f] = fmaxf(d0 * (0.0f + d0 * Zr[f]) + (b1 ? b1[f] : 0.f), 0.f);
   __syncthreads();
-  for (int64_t x0 = 0; x0 < n1; x0 += nx) {
-    const int64_t nn = n1 - x0 < nx ? n1 - x0 : nx;
-    for (int64_t it = tid; it < nn * h; it += kEndsThreads) {
-      const int64_t x = x0 + it / h;
-      const int f = static_cast<int>(it % h);
-      const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
-      float acc = 0.f;
-      // eight players' loads in flight at a time, summed in player order
-      for (int64_t eb = e0; eb < e1; eb += 8) {
-        int32_t u[8];
-        float z[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) u[q] = eb + q < e1 ? edge_src[eb + q] : 0;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) z[q] = eb + q < e1 ? Zc[static_cast<int64_t>(u[q]) * h + f] : 0.f;
-#pragma unroll
-        for (int q = 0; q < 8; ++q)
-          if (eb + q < e1) acc += (u[q] < n_dst ? dinv[u[q]] : 1.0f) * z[q];
-      }
-      const float dx = dinv[x];
-      hv[it] = fmaxf(dx * (acc + dx * Zc[x * h + f]) + (b1 ? b1[f] : 0.f), 0.f);
-    }
-    __syncthreads();
+  const int lane = tid & 63, wv = tid >> 6;
+  // the class logits of the nodes of one chunk, from their H^1 rows in hv
+  auto chunk_logits = [&](int64_t x0, int64_t nn) {
     for (int64_t it = tid; it < nn * C; it += kEndsThreads) {
       const int64_t xi = it / C;
       const int c = static_cast<int>(it % C);
       float t = 0.f;
-      for (int f = 0; f < h; ++f) t += hv[xi * h + f] * W2[static_cast<int64_t>(f) * C + c];
+      for (int f = 0; f < h; ++f) t += hv[xi * h + f] * w2[static_cast<int64_t>(f) * C + c];
       tt[(x0 + xi) * C + c] = t;
     }
-    __syncthreads();
+  };
+  if (h <= 16) {
+    // one wavefront per node of H_1, four nodes at a time: lane (f, slot)
+    // takes feature f of every fourth player from the slot on (four loads in
+    // flight), and two butterflies add the four slots
+    const int f = lane & 15, slot = lane >> 4;
+    for (int64_t x0 = 0; x0 < n1; x0 += 4) {
+      const int64_t nn = n1 - x0 < 4 ? n1 - x0 : 4;
+      const int64_t x = x0 + wv;
+      float acc = 0.f;
+      if (x < n1 && f < h) {
+        const int64_t e0 = dp[x], e1 = dp[x + 1];
+        float a[4] = {0.f, 0.f, 0.f, 0.f};
+        int64_t e = e0 + slot;
+        for (; e + 12 < e1; e += 16) {
+          int32_t u[4];
+          float z[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) u[q] = er[e + 4 * q];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) z[q] = Zr[static_cast<int64_t>(u[q]) * h + f];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) a[q] += (u[q] < n_dst ? dinv[u[q]] : 1.0f) * z[q];
+        }
+        for (; e < e1; e += 4) {
+          const int32_t u = er[e];
+          a[0] += (u < n_dst ? dinv[u] : 1.0f) * Zr[static_cast<int64_t>(u) * h + f];
+        }
+        acc = (a[0] + a[1]) + (a[2] + a[3]);
+      }
+      acc += __shfl_xor(acc, 16);
+      acc += __shfl_xor(acc, 32);
+      if (x < n1 && slot == 0 && f < h) {
+        const float dx = dinv[x];
+        hv[wv * h + f] = fmaxf(dx * (acc + dx * Zr[x * h + f]) + (b1 ? b1[f] : 0.f), 0.f);
+      }
+      __syncthreads();
+      chunk_logits(x0, nn);
+      __syncthreads();
+    }
+  } else {
+    for (int64_t x0 = 0; x0 < n1; x0 += nx) {
+      const int64_t nn = n1 - x0 < nx ? n1 - x0 : nx;
+      for (int64_t it = tid; it < nn * h; it += kEndsThreads) {
+        const int64_t x = x0 + it / h;
+        const int f = static_cast<int>(it % h);
+        const int64_t e0 = dp[x], e1 = dp[x + 1];
+        float acc = 0.f;
+        // eight players' loads in flight at a time, summed in player order
+        for (int64_t eb = e0; eb < e1; eb += 8) {
+          int32_t u[8];
+          float z[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) u[q] = eb + q < e1 ? er[eb + q] : 0;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) z[q] = eb + q < e1 ? Zr[static_cast<int64_t>(u[q]) * h + f] : 0.f;
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (eb + q < e1) acc += (u[q] < n_dst ? dinv[u[q]] : 1.0f) * z[q];
+        }
+        const float dx = dinv[x];
+        hv[it] = fmaxf(dx * (acc + dx * Zr[x * h + f]) + (b1 ? b1[f] : 0.f), 0.f);
+      }
+      __syncthreads();
+      chunk_logits(x0, nn);
+      __syncthreads();
+    }
   }
   for (int c = tid; c < C; c += kEndsThreads) {
     float t = 0.f;
-    for (int f = 0; f < h; ++f) t += he[f] * W2[static_cast<int64_t>(f) * C + c];
+    for (int f = 0; f < h; ++f) t += he[f] * w2[static_cast<int64_t>(f) * C + c];
     te[c] = t;
   }
   __syncthreads();
-  const int64_t indeg = dst_ptr[1];
+  // layer 2 at the target, one wavefront per class: lanes take the target's
+  // players in turn (the source of player x - 1 is node x of H_1), summed by
+  // a butterfly
+  const int64_t indeg = dp[1];
   const float dv = dinv[0];
-  for (int c = tid; c < C; c += kEndsThreads) {
-    const float bias = b2 ? b2[c] : 0.f;
-    sp_y[c] = d0 * (0.0f + d0 * te[c]) + bias;
+  for (int c = wv; c < C; c += kEndsThreads / 64) {
     float acc = 0.f;
-    for (int64_t eb = 0; eb < indeg; eb += 8) {
-      int32_t u[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) u[q] = eb + q < indeg ? edge_src[eb + q] : 0;
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (eb + q < indeg) acc += dinv[u[q]] * tt[static_cast<int64_t>(u[q]) * C + c];
+    for (int64_t e = lane; e < indeg; e += 64) {
+      const int32_t u = er[e];
+      acc += dinv[u] * tt[static_cast<int64_t>(u) * C + c];
     }
-    acc += dv * tt[c];
-    sp_y[C + c] = dv * acc + bias;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    if (lane == 0) {
+      const float bias = b2 ? b2[c] : 0.f;
+      sp_y[c] = d0 * (0.0f + d0 * te[c]) + bias;
+      sp_y[C + c] = dv * (acc + dv * tt[c]) + bias;
+    }
   }
   __syncthreads();
   if (tid == 0) pick_class(sp_y, C, requested, ctl, class_out, f_empty_full);
 }
 
+template <bool S>
 __global__ void __launch_bounds__(kEndsThreads) k_eval_ends(const int32_t* __restrict__ dst_ptr,
                                                              const int32_t* __restrict__ edge_src, int64_t n_dst,
-                                                             int64_t n1, float* Zc, const float* __restrict__ XW1,
+                                                             int64_t n1, int64_t M, float* Zc,
+                                                             const float* __restrict__ XW1,
                                                              const int32_t* __restrict__ node_gid, int64_t n_nodes,
                                                              const float* __restrict__ b1,
                                                              const float* __restrict__ W2,
                                                              const float* __restrict__ b2, int h, int C,
                                                              float* __restrict__ sp_y, int requested, int32_t* ctl,
                                                              int32_t* class_out, float* f_empty_full) {
-  ends_l2_body(dst_ptr, edge_src, n_dst, n1, Zc, XW1, node_gid, n_nodes, b1, W2, b2, h, C, sp_y, requested, ctl,
-               class_out, f_empty_full);
+  ends_l2_body<S>(dst_ptr, edge_src, n_dst, n1, M, Zc, XW1, node_gid, n_nodes, b1, W2, b2, h, C, sp_y, requested,
+                  ctl, class_out, f_empty_full);
+}
+
+// One launch of k_eval_ends for a single subgraph (staged when it fits).
+void launch_ends(hipStream_t s, const gnnshap_subgraph* sg, int64_t n_dst, int64_t n1, int64_t n_nodes, float* Zc,
+                 const float* XW1, const float* b1, const float* W2, const float* b2, int h, int C, float* sp_y,
+                 int requested, int32_t* ctl, int32_t* class_out, float* f_empty_full) {
+  bool S = false;
+  const size_t lds = ends_launch_lds(n_dst, n1, n_nodes, sg->num_edges, h, C, &S);
+  if (S)
+    k_eval_ends<true><<<1, kEndsThreads, lds, s>>>(sg->dst_ptr, sg->edge_src, n_dst, n1, sg->num_edges, Zc, XW1,
+                                                   sg->node_gid, n_nodes, b1, W2, b2, h, C, sp_y, requested, ctl,
+                                                   class_out, f_empty_full);
+  else
+    k_eval_ends<false><<<1, kEndsThreads, lds, s>>>(sg->dst_ptr, sg->edge_src, n_dst, n1, sg->num_edges, Zc, XW1,
+                                                    sg->node_gid, n_nodes, b1, W2, b2, h, C, sp_y, requested, ctl,
+                                                    class_out, f_empty_full);
 }
 
 template <int FPT>
@@ -1359,11 +1511,12 @@ __global__ void k_gather_batch(const gnnshap::EvalJob* __restrict__ jobs, const 
 }
 
 // The end coalitions of every job.
+template <bool S>
 __global__ void __launch_bounds__(kEndsThreads) k_eval_ends_batch(const gnnshap::EvalJob* __restrict__ jobs,
                                                                    gnnshap::EvalModel md, bool gather) {
   const gnnshap::EvalJob J = jobs[blockIdx.x];
-  ends_l2_body(J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.Zc1, gather ? md.XW1 : nullptr, J.node_gid, J.n_nodes, md.b1,
-               md.W2, md.b2, md.h, md.C, J.sp_y, md.target_class, J.ctl, J.cls_out, J.fef);
+  ends_l2_body<S>(J.dst_ptr, J.edge_src, J.n_dst, J.n1, J.M, J.Zc1, gather ? md.XW1 : nullptr, J.node_gid,
+                  J.n_nodes, md.b1, md.W2, md.b2, md.h, md.C, J.sp_y, md.target_class, J.ctl, J.cls_out, J.fef);
 }
 
 // Main pass of the jobs that do not take the one-thread-per-coalition kernel.
@@ -1467,9 +1620,8 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
     const int32_t* zidx = nullptr;
     const float* b1 = m->b ? m->b[0] : nullptr;
     const float* b2 = m->b ? m->b[1] : nullptr;
-    k_eval_ends<<<1, kEndsThreads, ends_lds_bytes(sh.n_dst, sh.nd[1], sh.dims[1], sh.dims[2]), s>>>(
-        sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], m->XW1, sg->node_gid, sh.n_nodes, b1, m->W[1], b2,
-        sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out, f_empty_full);
+    launch_ends(s, sg, sh.n_dst, sh.nd[1], sh.n_nodes, w.Zc[1], m->XW1, b1, m->W[1], b2, sh.dims[1], sh.dims[2],
+                w.sp_y, target_class, w.ctl, class_out, f_empty_full);
     GS_LAUNCHED();
     const unsigned gr = static_cast<unsigned>(gnnshap::ceil_div(k, rows_pass_block(sh.dims[1])));
     GS_TIMED(sh.dims[1] <= 16 ? "k_eval_rows_mx" : "k_eval_rows", s);
@@ -1510,10 +1662,9 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   }
   // f(empty) and f(E_c) for every class, then the explained class.
   if (ends_ok(sh)) {
-    k_eval_ends<<<1, kEndsThreads, ends_lds_bytes(sh.n_dst, sh.nd[1], sh.dims[1], sh.dims[2]), s>>>(
-        sg->dst_ptr, sg->edge_src, sh.n_dst, sh.nd[1], w.Zc[1], nullptr, nullptr, sh.n_nodes,
-        m->b ? m->b[0] : nullptr, m->W[1], m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y, target_class,
-        w.ctl, class_out, f_empty_full);
+    launch_ends(s, sg, sh.n_dst, sh.nd[1], sh.n_nodes, w.Zc[1], nullptr, m->b ? m->b[0] : nullptr, m->W[1],
+                m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out,
+                f_empty_full);
     GS_LAUNCHED();
   } else {
     if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
@@ -1622,7 +1773,10 @@ int gnnshap::launch_eval_batch(const EvalJob* jobs, int64_t n, const EvalModel& 
   }
   {
     GS_TIMED("k_eval_ends_batch", s);
-    k_eval_ends_batch<<<nn, kEndsThreads, lds_ends, s>>>(jobs, md, all);
+    bool S = false;
+    const size_t lds = ends_launch_lds(max_ndst, max_n1, max_nodes, 64 * max_wpr, md.h, md.C, &S);
+    if (S) k_eval_ends_batch<true><<<nn, kEndsThreads, lds, s>>>(jobs, md, all);
+    else k_eval_ends_batch<false><<<nn, kEndsThreads, lds, s>>>(jobs, md, all);
   }
   GS_LAUNCHED();
   if (!all) {
