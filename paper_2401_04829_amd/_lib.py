@@ -239,13 +239,18 @@ def gnnshap_explain_batch_workspace(sgs, plans, model):
 
 def gnnshap_explain_batch(sgs, plans, classes, model, X_ptr, target_class, masks_ptr, weights_ptr, y_ptr, fef_ptr,
                           cls_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):
-    check(load().gnnshap_explain_batch(sgs, plans, classes, len(sgs), ctypes.byref(model), X_ptr, target_class,
-                                       masks_ptr, weights_ptr, y_ptr, fef_ptr, cls_ptr, phi_ptr, info_ptr, ws_ptr,
-                                       ws_bytes, stream), "explain_batch")
+    """Returns OK, or ECAPACITY when the workspace is too small (nothing was
+    queued then); raises on any other status."""
+    st = load().gnnshap_explain_batch(sgs, plans, classes, len(sgs), ctypes.byref(model), X_ptr, target_class,
+                                      masks_ptr, weights_ptr, y_ptr, fef_ptr, cls_ptr, phi_ptr, info_ptr, ws_ptr,
+                                      ws_bytes, stream)
+    if st not in (OK, ECAPACITY):
+        check(st, "explain_batch")
+    return st
 
 
 def gnnshap_solve_info(plan):
-    """Solver path of the plan's system: 1 one workgroup, 0 multi-block."""
+    """Solver path of the plan's system: 1 one workgroup, 2 the panel path, 0 multi-block."""
     v = c_i32()
     check(load().gnnshap_solve_info(ctypes.byref(plan), ctypes.byref(v)), "solve_info")
     return v.value

@@ -14,8 +14,11 @@ namespace gnnshap {
 
 // Side streams of the current device for the calling thread, each with the
 // two events that fork work onto it and join it back (created on first use,
-// default priority, kept until the process ends).
-constexpr int kSideStreams = 3;
+// default priority, kept until the process ends).  Two: with the caller's
+// stream and the extraction stream of a pipelined caller that makes four,
+// the number of hardware queues a process gets by default, so no two of them
+// share a queue.
+constexpr int kSideStreams = 2;
 
 struct SideStream {
   hipStream_t stream = nullptr;
@@ -47,24 +50,13 @@ SideStream* side_stream(int i) {
   return &per_device.back().side[i];
 }
 
-// Page-locked staging for host-to-device copies of the calling thread: a
-// ring of two buffers, each reused only after the copy that last read it has
-// run (its event), so that a call never waits for earlier GPU work.
-// Buffers grow on demand and are kept until the process ends.
-struct HostStage {
-  char* buf = nullptr;
-  size_t cap = 0;
-  hipEvent_t done = nullptr;
-  bool pending = false;
-};
-
 struct DeviceStages {
   int device = -1;
-  HostStage ring[2];
-  int next = 0;
+  HostStage ring[2][2];
+  int next[2] = {0, 0};
 };
 
-HostStage* host_stage(size_t bytes) {
+HostStage* host_stage(size_t bytes, int ring) {
   static thread_local std::vector<DeviceStages> per_device;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return nullptr;
@@ -76,8 +68,9 @@ HostStage* host_stage(size_t bytes) {
     d = &per_device.back();
     d->device = dev;
   }
-  HostStage* h = &d->ring[d->next];
-  d->next ^= 1;
+  if (ring < 0 || ring > 1) return nullptr;
+  HostStage* h = &d->ring[ring][d->next[ring]];
+  d->next[ring] ^= 1;
   if (!h->done && hipEventCreateWithFlags(&h->done, hipEventDisableTiming) != hipSuccess) return nullptr;
   if (h->pending && hipEventSynchronize(h->done) != hipSuccess) return nullptr;
   h->pending = false;
@@ -232,7 +225,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
   // and copied in one transfer before the first launch.
   char* const base = static_cast<char*>(ws);
   const size_t front = static_cast<size_t>(reinterpret_cast<char*>(b.solve + n) - base);
-  gnnshap::HostStage* stage = gnnshap::host_stage(front);
+  gnnshap::HostStage* stage = gnnshap::host_stage(front, 0);
   if (!stage) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
   char* const image = stage->buf;
   std::fill(image, image + front, 0);
@@ -244,7 +237,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
 
   struct Group {
     int64_t begin = 0, end = 0;                      // range of order[]
-    int64_t blocks = 0, max_wpr = 0, max_k = 0;      // sampling
+    int64_t max_wpr = 0, max_k = 0;                  // sampling
     bool eval_all = false;                           // batched evaluation
     int64_t max_nodes = 0, max_ndst = 0, max_n1 = 0, rows_jobs = 0;
     size_t rows_lds = 0;
@@ -271,7 +264,6 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       G.max_wpr = std::max(G.max_wpr, p.words_per_row);
       G.max_k = std::max(G.max_k, p.num_rows);
     }
-    G.blocks = gnnshap::plan_sample_batch(sj + G.begin, G.end - G.begin);
     // 2. coalition-value jobs (two-layer models with X W_1 given)
     G.eval_all = model->num_layers == 2 && model->XW1;
     for (int64_t j = G.begin; j < G.end && G.eval_all; ++j)
@@ -334,42 +326,48 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     G.solve_count = nv - G.solve_begin;
   }
 
+  // one sampling launch for the whole batch
+  const int64_t sample_blocks = gnnshap::plan_sample_batch(sj, n);
+  const int64_t sample_wpr = std::max(grp[0].max_wpr, grp[1].max_wpr);
+  // one G~ pass for every batched system
+  int64_t mM = 0, mw = 0, mnrb = 0;
+  for (const Group& G : grp) {
+    mM = std::max(mM, G.bM);
+    mw = std::max(mw, G.bw);
+    mnrb = std::max(mnrb, G.bnrb);
+  }
+
   GS_HIP(hipMemcpyAsync(ws, image, front, hipMemcpyHostToDevice, s));
   GS_HIP(hipEventRecord(stage->done, s));
   stage->pending = true;
   // Every launch after the job-table copy, on origin stream `o` and the side
   // streams forked from it.
   auto issue = [&](hipStream_t o) -> int {
-      // Streams: group 0 runs on side stream 0, group 1 on `stream`; each
-      // group's G~ is built on a side stream of its own (2 for group 0, 1 for
-      // group 1) once its masks are sampled, while its coalitions are evaluated.
-      hipStream_t gs[2] = {o, o};
-      gnnshap::SideStream* mat[2] = {nullptr, nullptr};
+      // Streams: the masks of every target are sampled on origin stream `o`;
+      // then group 0 (the panel-path systems) is evaluated and solved on side
+      // stream 0, group 1 on `o`, and G~ of every batched system is built on
+      // side stream 1 while the coalitions are evaluated.  Three event pairs:
+      // the fork after sampling (side streams 0 and 1 wait on it), G~ ready
+      // (both factorisations wait on it) and the join of side stream 0.
       gnnshap::SideStream* side0 = nullptr;
+      gnnshap::SideStream* mat = nullptr;
       if (grp[0].end > grp[0].begin) {
         side0 = gnnshap::side_stream(0);
         if (!side0) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
-        GS_HIP(hipEventRecord(side0->fork, o));
-        GS_HIP(hipStreamWaitEvent(side0->stream, side0->fork, 0));
-        gs[0] = side0->stream;
       }
-      for (int gi = 0; gi < 2; ++gi) {
-        if (grp[gi].solve_count == 0) continue;
-        mat[gi] = gnnshap::side_stream(gi == 0 ? 2 : 1);
-        if (!mat[gi]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+      if (nv > 0) {
+        mat = gnnshap::side_stream(1);
+        if (!mat) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
       }
-      // 1. sampling; the matrix streams wait for it
-      for (int gi = 0; gi < 2; ++gi) {
-        const Group& G = grp[gi];
-        if (G.end == G.begin) continue;
-        if (int st = gnnshap::launch_sample_batch(b.sample + G.begin, G.end - G.begin, G.blocks, G.max_wpr, gs[gi]))
-          return st;
-        if (mat[gi]) {
-          GS_HIP(hipEventRecord(mat[gi]->fork, gs[gi]));
-          GS_HIP(hipStreamWaitEvent(mat[gi]->stream, mat[gi]->fork, 0));
-        }
+      hipStream_t gs[2] = {side0 ? side0->stream : o, o};
+      if (int st = gnnshap::launch_sample_batch(b.sample, n, sample_blocks, sample_wpr, o)) return st;
+      if (side0 || mat) {
+        gnnshap::SideStream* f = side0 ? side0 : mat;
+        GS_HIP(hipEventRecord(f->fork, o));
+        if (side0) GS_HIP(hipStreamWaitEvent(side0->stream, f->fork, 0));
+        if (mat) GS_HIP(hipStreamWaitEvent(mat->stream, f->fork, 0));
       }
-      // 2. coalition values
+      // 1. coalition values
       for (int gi = 0; gi < 2; ++gi) {
         const Group& G = grp[gi];
         if (G.end == G.begin) continue;
@@ -394,14 +392,10 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
           }
         }
       }
-      // G~ (launched after the evaluations, which are on the longer chains)
-      for (int gi = 0; gi < 2; ++gi) {
-        const Group& G = grp[gi];
-        if (!mat[gi]) continue;
-        if (int st = gnnshap::launch_solve_matrix(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bnrb,
-                                                  mat[gi]->stream))
-          return st;
-        GS_HIP(hipEventRecord(mat[gi]->join, mat[gi]->stream));
+      // 2. G~ (launched after the evaluations, which are on the longer chains)
+      if (mat) {
+        if (int st = gnnshap::launch_solve_matrix(b.solve, nv, mM, mw, mnrb, mat->stream)) return st;
+        GS_HIP(hipEventRecord(mat->join, mat->stream));
       }
       // 3. least squares: right-hand sides, then (with G~ ready) the factorisations
       for (int gi = 0; gi < 2; ++gi) {
@@ -416,7 +410,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       for (int gi = 1; gi >= 0; --gi) {
         const Group& G = grp[gi];
         if (G.solve_count > 0) {
-          GS_HIP(hipStreamWaitEvent(gs[gi], mat[gi]->join, 0));
+          GS_HIP(hipStreamWaitEvent(gs[gi], mat->join, 0));
           if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, G.max_panels, G.small,
                                                     gs[gi]))
             return st;

@@ -64,6 +64,21 @@ inline int max_lds_bytes() {
   return v;
 }
 
+// Page-locked staging for host-to-device copies of the calling thread: a
+// ring of two buffers, each reused only after the copy that last read it has
+// run (its event), so that a call never waits for earlier GPU work.
+// Buffers grow on demand and are kept until the process ends.
+struct HostStage {
+  char* buf = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+// The next buffer of ring `ring` (0: batched explanation, 1: batched
+// extraction), with at least `bytes`; after queueing the copy that reads it,
+// record `done` on the copy's stream and set `pending`.  nullptr on failure.
+HostStage* host_stage(size_t bytes, int ring);
+
 // Page-locked host staging of at least `bytes` for device-to-host copies of
 // the calling thread (grown on demand, kept until the process ends), so the
 // copy queues behind the kernels instead of blocking the host first.

@@ -599,7 +599,9 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
   const size_t need = batch_bytes(nn, n);
   if (ws_bytes < need) return gnnshap::fail(GNNSHAP_ECAPACITY, "batch extract workspace needs %zu bytes", need);
   const BatchWs b = carve_batch(ws, ws_bytes, nn, n);
-  std::vector<ExtractJob> jobs(static_cast<size_t>(n));
+  gnnshap::HostStage* stage = gnnshap::host_stage(static_cast<size_t>(n) * sizeof(ExtractJob), 1);
+  if (!stage) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
+  ExtractJob* jobs = reinterpret_cast<ExtractJob*>(stage->buf);
   for (int64_t t = 0; t < n; ++t) {
     const gnnshap_subgraph* sg = &sgs[t];
     if (targets[t] < 0 || targets[t] >= nn) return gnnshap::fail(GNNSHAP_EINVAL, "target %lld out of range", (long long)t);
@@ -613,7 +615,9 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
                          sg->dst_ptr, sg->edge_src, sg->edge_dst, sg->edge_gid};
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  GS_HIP(hipMemcpyAsync(b.jobs, jobs.data(), jobs.size() * sizeof(ExtractJob), hipMemcpyHostToDevice, s));
+  GS_HIP(hipMemcpyAsync(b.jobs, jobs, static_cast<size_t>(n) * sizeof(ExtractJob), hipMemcpyHostToDevice, s));
+  GS_HIP(hipEventRecord(stage->done, s));
+  stage->pending = true;
   {
     GS_TIMED("k_extract_batch", s);
     k_extract_batch<<<static_cast<unsigned>(n), 1024, 0, s>>>(g->indptr, g->indices, nn, b.jobs, b.results);

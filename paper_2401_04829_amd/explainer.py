@@ -96,6 +96,7 @@ class Explainer:
         self._plans = {}                         # (M, p) -> (plan, classes): the plan does not depend on seed
         self._ncls_hint = 1024                   # class-table length explain_batch allocates
         self._xstream = None                     # stream of the batched extraction
+        self._tg_cache = None                    # (target tuple, ctypes int64 array) of the last batch
 
     def prepare(self):
         """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
@@ -234,9 +235,9 @@ class Explainer:
         """gnnshap_extract_batch: the computational graphs of all targets with one
         host synchronisation; capacities grow and the batch is redone on
         ECAPACITY.  Extraction runs on a stream of its own, so that waiting for
-        the sizes does not wait for work queued earlier on the current stream
-        (which is then ordered after it).  Returns (BatchSubgraphs, ctypes array
-        of gnnshap_subgraph)."""
+        the sizes does not wait for work queued earlier on the current stream;
+        it is complete when the call returns.  Returns (BatchSubgraphs, ctypes
+        array of gnnshap_subgraph)."""
         dev = self.device
         n = len(targets)
         if self._bx is None or self._bx[0] < n:
@@ -244,7 +245,10 @@ class Explainer:
             self._bx = (n, torch.zeros(nbytes, dtype=torch.uint8, device=dev))
             torch.cuda.current_stream(dev).synchronize()
         ws = self._bx[1]
-        tg = (ctypes.c_int64 * n)(*[int(v) for v in targets])
+        key = tuple(int(v) for v in targets)
+        if self._tg_cache is None or self._tg_cache[0] != key:
+            self._tg_cache = (key, (ctypes.c_int64 * n)(*key))
+        tg = self._tg_cache[1]
         main = torch.cuda.current_stream(dev)
         if self._xstream is None:
             self._xstream = torch.cuda.Stream(device=dev)
@@ -261,9 +265,10 @@ class Explainer:
                     break
                 self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
                              max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
-        main.wait_stream(xs)
-        for t in (bufs.node_gid, bufs.dst_ptr, bufs.edge_src, bufs.edge_dst, bufs.edge_gid):
-            t.record_stream(main)
+        # the call returns with the extraction complete (it reads the sizes
+        # back), so `main` needs no wait; the allocator learns that the
+        # buffers are used on `main`
+        bufs.buffer.record_stream(main)
         bufs.sgs = sgs
         bufs.targets = tg
         return bufs, sgs
@@ -287,21 +292,36 @@ class Explainer:
             cl = (L.gnnshap_class * self._ncls_hint)()
             st, ncls, totals = L.gnnshap_plan_batch(sgs, subs.targets, int(num_samples), int(seed), plans, cl)
         out = BatchExplanations(targets, subs, plans, cl, ncls, totals, dev)
-        ws = self.ws_batch.get(L.gnnshap_explain_batch_workspace(sgs, plans, self.model))
-        L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *out.pointers(),
-                                _vp(ws), ws.numel(), self.stream())
+        # the workspace is sized on demand: the call checks it before queueing anything
+        ptrs = out.pointers()
+        ws = self.ws_batch.t
+        st = L.ECAPACITY
+        if ws is not None:
+            st = L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *ptrs,
+                                         _vp(ws), ws.numel(), self.stream())
+        if st == L.ECAPACITY:
+            ws = self.ws_batch.get(L.gnnshap_explain_batch_workspace(sgs, plans, self.model))
+            st = L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *ptrs,
+                                         _vp(ws), ws.numel(), self.stream())
+            L.check(st, "explain_batch")
         return out
 
 
 class BatchSubgraphs:
-    """Packed subgraph buffers of a batch: target t owns row t of each array."""
+    """Packed subgraph buffers of a batch, views of one device allocation:
+    target t owns row t of each array."""
 
     def __init__(self, n, cap_nodes, cap_edges, dev):
-        self.node_gid = torch.empty((n, cap_nodes), dtype=torch.int32, device=dev)
-        self.dst_ptr = torch.empty((n, cap_nodes + 1), dtype=torch.int32, device=dev)
-        self.edge_src = torch.empty((n, cap_edges), dtype=torch.int32, device=dev)
-        self.edge_dst = torch.empty((n, cap_edges), dtype=torch.int32, device=dev)
-        self.edge_gid = torch.empty((n, cap_edges), dtype=torch.int64, device=dev)
+        shapes = (("node_gid", torch.int32, 4, (n, cap_nodes)), ("dst_ptr", torch.int32, 4, (n, cap_nodes + 1)),
+                  ("edge_src", torch.int32, 4, (n, cap_edges)), ("edge_dst", torch.int32, 4, (n, cap_edges)),
+                  ("edge_gid", torch.int64, 8, (n, cap_edges)))
+        offs, off = [], 0
+        for _, _, es, shp in shapes:
+            offs.append(off)
+            off = (off + shp[0] * shp[1] * es + 255) // 256 * 256
+        self.buffer = torch.empty(max(off, 256), dtype=torch.uint8, device=dev)
+        for (name, dt, es, shp), o in zip(shapes, offs):
+            setattr(self, name, self.buffer[o:o + shp[0] * shp[1] * es].view(dt).view(shp))
         self.sgs = None
 
     def __getitem__(self, t):
