@@ -267,6 +267,22 @@ int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, size_t* bytes)
 int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
                           gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream);
 
+/* gnnshap_extract_batch in two halves, so that a caller can queue the next
+ * batch's extraction before the current batch's explanation and wait for
+ * the sizes later.  _launch validates the arguments and queues the
+ * extraction and the copy of its sizes to page-locked host memory on
+ * `stream` (same arguments and errors as gnnshap_extract_batch, except
+ * that it never reports ECAPACITY for the subgraphs); _finish waits for
+ * those sizes and fills them into sgs[0 .. n) (the same n and sgs array),
+ * returning OK or ECAPACITY as gnnshap_extract_batch does.  The [dev]
+ * outputs are complete when _finish returns.  Each host thread has at most
+ * one launched extraction: _launch returns EINVAL while one is not
+ * finished, _finish EINVAL when none is launched (or n differs).  `ws` and
+ * the output arrays must not be touched between the two calls. */
+int gnnshap_extract_batch_launch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
+                                 gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream);
+int gnnshap_extract_batch_finish(gnnshap_subgraph* sgs, int64_t n);
+
 /* Host only: fills sgs[0 .. n) for outputs packed by target, as rows of
  * [dev] node_gid[n][cap_nodes], dst_ptr[n][cap_nodes + 1],
  * edge_src[n][cap_edges], edge_dst[n][cap_edges] (int32) and

@@ -67,6 +67,9 @@ _SIGNATURES = {
     "gnnshap_extract_batch_workspace": (ctypes.c_int, [c_i64, c_i64, _P(ctypes.c_size_t)]),
     "gnnshap_extract_batch": (ctypes.c_int, [_P(gnnshap_graph), _P(c_i64), c_i64, _P(gnnshap_subgraph), c_vp,
                                              ctypes.c_size_t, c_vp]),
+    "gnnshap_extract_batch_launch": (ctypes.c_int, [_P(gnnshap_graph), _P(c_i64), c_i64, _P(gnnshap_subgraph),
+                                                    c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_extract_batch_finish": (ctypes.c_int, [_P(gnnshap_subgraph), c_i64]),
     "gnnshap_subgraph_batch_init": (ctypes.c_int, [_P(gnnshap_subgraph), c_i64, c_i32, c_i64, c_i64, c_vp, c_vp,
                                                     c_vp, c_vp, c_vp]),
     "gnnshap_plan_batch": (ctypes.c_int, [_P(gnnshap_subgraph), _P(c_i64), c_i64, c_i64, ctypes.c_uint64,
@@ -207,6 +210,21 @@ def gnnshap_extract_batch(graph, targets, sgs, ws_ptr, ws_bytes, stream):
     st = load().gnnshap_extract_batch(ctypes.byref(graph), targets, len(sgs), sgs, ws_ptr, ws_bytes, stream)
     if st not in (OK, ECAPACITY):
         check(st, "extract_batch")
+    return st
+
+
+def gnnshap_extract_batch_launch(graph, targets, sgs, ws_ptr, ws_bytes, stream):
+    """First half of gnnshap_extract_batch: queues the extraction; sizes come
+    with gnnshap_extract_batch_finish."""
+    check(load().gnnshap_extract_batch_launch(ctypes.byref(graph), targets, len(sgs), sgs, ws_ptr, ws_bytes, stream),
+          "extract_batch_launch")
+
+
+def gnnshap_extract_batch_finish(sgs):
+    """Second half: waits for the sizes of the launched extraction.  Returns OK or ECAPACITY."""
+    st = load().gnnshap_extract_batch_finish(sgs, len(sgs))
+    if st not in (OK, ECAPACITY):
+        check(st, "extract_batch_finish")
     return st
 
 

@@ -80,7 +80,8 @@ HostStage* host_stage(size_t bytes, int ring) {
     h->cap = 0;
     const size_t want = bytes + bytes / 2 + 4096;
     void* p = nullptr;
-    if (hipHostMalloc(&p, want, hipHostMallocDefault) != hipSuccess) {
+    // coherent: the GPU reads it uncached, so a reused buffer is never stale
+    if (hipHostMalloc(&p, want, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
       (void)hipGetLastError();
       return nullptr;
     }
@@ -88,6 +89,22 @@ HostStage* host_stage(size_t bytes, int ring) {
     h->cap = want;
   }
   return h;
+}
+
+__global__ void __launch_bounds__(256) k_copy16(const uint4* __restrict__ src, uint4* __restrict__ dst, size_t n) {
+  for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += static_cast<size_t>(gridDim.x) * 256)
+    dst[i] = src[i];
+}
+
+int copy_by_kernel(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  const size_t n = (bytes + 15) / 16;
+  if (n == 0) return GNNSHAP_OK;
+  if ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 15)
+    return fail(GNNSHAP_EINVAL, "copy buffers must be 16-byte aligned");
+  k_copy16<<<grid_for(static_cast<int64_t>(n), 256, 256), 256, 0, s>>>(static_cast<const uint4*>(src),
+                                                                       static_cast<uint4*>(dst), n);
+  GS_HIP(hipGetLastError());
+  return GNNSHAP_OK;
 }
 
 }  // namespace gnnshap
@@ -337,7 +354,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     mnrb = std::max(mnrb, G.bnrb);
   }
 
-  GS_HIP(hipMemcpyAsync(ws, image, front, hipMemcpyHostToDevice, s));
+  if (int st = gnnshap::copy_by_kernel(ws, image, front, s)) return st;
   GS_HIP(hipEventRecord(stage->done, s));
   stage->pending = true;
   // Every launch after the job-table copy, on origin stream `o` and the side

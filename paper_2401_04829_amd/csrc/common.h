@@ -79,6 +79,14 @@ struct HostStage {
 // record `done` on the copy's stream and set `pending`.  nullptr on failure.
 HostStage* host_stage(size_t bytes, int ring);
 
+// Copies `bytes` rounded up to a multiple of 16 (both buffers must hold the
+// rounded size; both 16-byte aligned) from src to dst with a kernel on `s`,
+// for copies between device memory and the page-locked buffers above: the
+// copy is ordered on the stream like any kernel and never goes through the
+// copy engines, whose queue can hold the host back for milliseconds when
+// many copies are outstanding.  Returns a GNNSHAP status.
+int copy_by_kernel(void* dst, const void* src, size_t bytes, hipStream_t s);
+
 // Page-locked host staging of at least `bytes` for device-to-host copies of
 // the calling thread (grown on demand, kept until the process ends), so the
 // copy queues behind the kernels instead of blocking the host first.

@@ -584,8 +584,29 @@ extern "C" int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, siz
   return GNNSHAP_OK;
 }
 
-extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
-                                     gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream) {
+namespace {
+
+// The calling thread's launched batched extraction: its result rows are
+// copied into page-locked memory behind the kernel, and `ready` is recorded
+// after the copy; gnnshap_extract_batch_finish waits for it.
+struct PendingExtract {
+  int device = -1;
+  int64_t* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ready = nullptr;
+  int64_t n = 0;
+  bool pending = false;
+};
+
+PendingExtract& pending_extract() {
+  static thread_local PendingExtract p;
+  return p;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_extract_batch_launch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
+                                            gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream) {
   GS_TRY_BEGIN
   gnnshap::clear_error();
   if (!g || !targets || !sgs || !ws) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
@@ -596,9 +617,29 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
   if (nn > kOneBlockNodes)
     return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "batched extraction supports graphs of up to %lld nodes",
                          (long long)kOneBlockNodes);
+  PendingExtract& pe = pending_extract();
+  if (pe.pending) return gnnshap::fail(GNNSHAP_EINVAL, "a batched extraction of this thread is not finished");
   const size_t need = batch_bytes(nn, n);
   if (ws_bytes < need) return gnnshap::fail(GNNSHAP_ECAPACITY, "batch extract workspace needs %zu bytes", need);
   const BatchWs b = carve_batch(ws, ws_bytes, nn, n);
+  int dev = 0;
+  GS_HIP(hipGetDevice(&dev));
+  if (pe.device != dev) {
+    if (pe.ready) (void)hipEventDestroy(pe.ready);
+    pe.ready = nullptr;
+    pe.device = dev;
+  }
+  if (!pe.ready) GS_HIP(hipEventCreateWithFlags(&pe.ready, hipEventDisableTiming));
+  const size_t hbytes = static_cast<size_t>(n) * kCounters * sizeof(int64_t);
+  if (pe.cap < hbytes) {
+    if (pe.host) (void)hipHostFree(pe.host);
+    pe.host = nullptr;
+    pe.cap = 0;
+    void* hp = nullptr;
+    GS_HIP(hipHostMalloc(&hp, (hbytes + 15) / 16 * 16, hipHostMallocMapped | hipHostMallocCoherent));
+    pe.host = static_cast<int64_t*>(hp);
+    pe.cap = hbytes;
+  }
   gnnshap::HostStage* stage = gnnshap::host_stage(static_cast<size_t>(n) * sizeof(ExtractJob), 1);
   if (!stage) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
   ExtractJob* jobs = reinterpret_cast<ExtractJob*>(stage->buf);
@@ -615,7 +656,7 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
                          sg->dst_ptr, sg->edge_src, sg->edge_dst, sg->edge_gid};
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  GS_HIP(hipMemcpyAsync(b.jobs, jobs, static_cast<size_t>(n) * sizeof(ExtractJob), hipMemcpyHostToDevice, s));
+  if (int st = gnnshap::copy_by_kernel(b.jobs, jobs, static_cast<size_t>(n) * sizeof(ExtractJob), s)) return st;
   GS_HIP(hipEventRecord(stage->done, s));
   stage->pending = true;
   {
@@ -624,18 +665,31 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
   }
   GS_LAUNCHED();
   // The job table and result rows are rewritten by every call (each
-  // workgroup writes all the counters the host reads below); only the
+  // workgroup writes all the counters the host reads back); only the
   // per-target slices need to start at zero, and they reset themselves.
-  const size_t hbytes = static_cast<size_t>(n) * kCounters * sizeof(int64_t);
-  const int64_t* hp = static_cast<const int64_t*>(gnnshap::pinned_staging(hbytes));
-  if (!hp) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
-  GS_HIP(hipMemcpyAsync(const_cast<int64_t*>(hp), b.results, hbytes, hipMemcpyDeviceToHost, s));
-  GS_HIP(hipStreamSynchronize(s));
-  const std::vector<int64_t> h(hp, hp + static_cast<size_t>(n) * kCounters);
+  if (int st = gnnshap::copy_by_kernel(pe.host, b.results, hbytes, s)) return st;
+  GS_HIP(hipEventRecord(pe.ready, s));
+  pe.n = n;
+  pe.pending = true;
+  return GNNSHAP_OK;
+  GS_TRY_END
+}
+
+extern "C" int gnnshap_extract_batch_finish(gnnshap_subgraph* sgs, int64_t n) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  PendingExtract& pe = pending_extract();
+  if (!sgs) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  if (!pe.pending || pe.n != n)
+    return gnnshap::fail(GNNSHAP_EINVAL, "no batched extraction of %lld targets was launched by this thread",
+                         (long long)n);
+  pe.pending = false;
+  GS_HIP(hipEventSynchronize(pe.ready));
+  const int64_t* h = pe.host;
   bool all_ok = true;
   for (int64_t t = 0; t < n; ++t) {
     gnnshap_subgraph* sg = &sgs[t];
-    const int64_t* r = h.data() + t * kCounters;
+    const int64_t* r = h + t * kCounters;
     const int levels = sg->num_hops + 1;
     int64_t nodes = 0;
     sg->hop_ptr[0] = 0;
@@ -653,6 +707,12 @@ extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targ
   if (!all_ok) return gnnshap::fail(GNNSHAP_ECAPACITY, "some subgraphs exceed their capacities");
   return GNNSHAP_OK;
   GS_TRY_END
+}
+
+extern "C" int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_t n,
+                                     gnnshap_subgraph* sgs, void* ws, size_t ws_bytes, void* stream) {
+  if (int st = gnnshap_extract_batch_launch(g, targets, n, sgs, ws, ws_bytes, stream)) return st;
+  return gnnshap_extract_batch_finish(sgs, n);
 }
 
 extern "C" int gnnshap_subgraph_batch_init(gnnshap_subgraph* sgs, int64_t n, int32_t num_hops, int64_t cap_nodes,

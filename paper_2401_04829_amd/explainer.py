@@ -238,6 +238,12 @@ class Explainer:
         the sizes does not wait for work queued earlier on the current stream;
         it is complete when the call returns.  Returns (BatchSubgraphs, ctypes
         array of gnnshap_subgraph)."""
+        return self.extract_batch_finish(self.extract_batch_start(targets))
+
+    def extract_batch_start(self, targets):
+        """First half of extract_batch (gnnshap_extract_batch_launch): queues the
+        extraction on the extraction stream and returns a pending batch for
+        extract_batch_finish.  One batch may be pending at a time."""
         dev = self.device
         n = len(targets)
         if self._bx is None or self._bx[0] < n:
@@ -253,24 +259,32 @@ class Explainer:
         if self._xstream is None:
             self._xstream = torch.cuda.Stream(device=dev)
         xs = self._xstream
+        cn, ce = self._cap
         with torch.cuda.stream(xs):
-            while True:
-                cn, ce = self._cap
-                bufs = BatchSubgraphs(n, cn, ce, dev)
-                sgs = (L.gnnshap_subgraph * n)()
-                L.gnnshap_subgraph_batch_init(sgs, self.hops, cn, ce, _vp(bufs.node_gid), _vp(bufs.dst_ptr),
-                                              _vp(bufs.edge_src), _vp(bufs.edge_dst), _vp(bufs.edge_gid))
-                st = L.gnnshap_extract_batch(self.graph, tg, sgs, _vp(ws), ws.numel(), ctypes.c_void_p(xs.cuda_stream))
-                if st == L.OK:
-                    break
-                self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
-                             max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
-        # the call returns with the extraction complete (it reads the sizes
-        # back), so `main` needs no wait; the allocator learns that the
-        # buffers are used on `main`
+            bufs = BatchSubgraphs(n, cn, ce, dev)
+        sgs = (L.gnnshap_subgraph * n)()
+        L.gnnshap_subgraph_batch_init(sgs, self.hops, cn, ce, _vp(bufs.node_gid), _vp(bufs.dst_ptr),
+                                      _vp(bufs.edge_src), _vp(bufs.edge_dst), _vp(bufs.edge_gid))
+        L.gnnshap_extract_batch_launch(self.graph, tg, sgs, _vp(ws), ws.numel(), ctypes.c_void_p(xs.cuda_stream))
+        # the buffers are used on the current stream once the sizes are back
+        # (the extraction is then complete, so that stream needs no wait)
         bufs.buffer.record_stream(main)
         bufs.sgs = sgs
         bufs.targets = tg
+        bufs.target_ids = key
+        return bufs
+
+    def extract_batch_finish(self, bufs):
+        """Second half (gnnshap_extract_batch_finish): waits for the sizes; on
+        ECAPACITY the capacities grow and the batch is extracted again.
+        Returns (BatchSubgraphs, ctypes array of gnnshap_subgraph)."""
+        sgs = bufs.sgs
+        while L.gnnshap_extract_batch_finish(sgs) != L.OK:
+            cn, ce = self._cap
+            self._cap = [max(max(int(sg.num_nodes * 1.25) + 16 for sg in sgs), cn),
+                         max(max(int(sg.num_edges * 1.25) + 64 for sg in sgs), ce)]
+            bufs = self.extract_batch_start(bufs.target_ids)
+            sgs = bufs.sgs
         return bufs, sgs
 
     def explain_batch(self, targets, num_samples, seed, target_class=-1):
@@ -281,9 +295,38 @@ class Explainer:
         stream has run; indexing gives per-target Explanation views)."""
         if self.XW1 is None:
             self.prepare()
-        dev = self.device
         subs, sgs = self.extract_batch(targets)
-        n = len(targets)
+        return self._explain_extracted(subs, sgs, num_samples, seed, target_class)
+
+    def explain_batches(self, batches, num_samples, seed, target_class=-1, prepare_each=False):
+        """explain_batch over a sequence of target batches, pipelined: the next
+        batch's extraction is queued before the current batch's explanation,
+        so that its sizes are ready when they are needed.  prepare_each: X W_1
+        again before every batch.  Yields one BatchExplanations per batch, in
+        order; each equals explain_batch's for the same batch."""
+        it = iter(batches)
+        first = next(it, None)
+        if first is None:
+            return
+        pend = self.extract_batch_start(first)
+        try:
+            while pend is not None:
+                if prepare_each or self.XW1 is None:
+                    self.prepare()
+                subs, sgs = self.extract_batch_finish(pend)
+                pend = None
+                nxt = next(it, None)
+                pend = self.extract_batch_start(nxt) if nxt is not None else None
+                yield self._explain_extracted(subs, sgs, num_samples, seed, target_class)
+        finally:
+            if pend is not None:          # stopped early: collect the queued extraction
+                L.gnnshap_extract_batch_finish(pend.sgs)
+
+    def _explain_extracted(self, subs, sgs, num_samples, seed, target_class):
+        """Plans and gnnshap_explain_batch for extracted subgraphs."""
+        dev = self.device
+        n = len(sgs)
+        targets = subs.target_ids
         plans = (L.gnnshap_sample_plan * n)()
         cl = (L.gnnshap_class * self._ncls_hint)()
         st, ncls, totals = L.gnnshap_plan_batch(sgs, subs.targets, int(num_samples), int(seed), plans, cl)

@@ -540,9 +540,9 @@ def test_explain_batch_against_oracle(dev):
 
 
 def test_explain_batch_repeated_calls_agree(dev):
-    """Repeated batched calls on the same targets (the launch sequence is
-    captured once and replayed) give the first call's outputs bit for bit,
-    with other device work between them, and equal the single-target calls."""
+    """Repeated batched calls on the same targets give the first call's
+    outputs bit for bit, with other device work between them, and equal the
+    single-target calls."""
     cfg = W.make_config("cora")
     ex = explainer_for(cfg)
     targets = cfg["targets"][:40]
@@ -562,3 +562,39 @@ def test_explain_batch_repeated_calls_agree(dev):
                 assert torch.equal(getattr(r, f), ref[t][f]), (rep, t, f)
         for f in fields:
             assert torch.equal(getattr(one, f), ref[rep][f]), (rep, f)
+
+
+@pytest.mark.gpu
+def test_explain_batches_pipelined_equal_batch_calls(dev):
+    """The pipelined sequence (each batch's extraction queued before the
+    previous batch's explanation) gives every batch exactly what a separate
+    explain_batch call gives; batches of different sizes, one repeated, and a
+    generator stopped early leaves no extraction pending."""
+    cfg = W.make_config("cora")
+    ex = explainer_for(cfg)
+    tg = cfg["targets"]
+    batches = [tg[:30], tg[30:45], tg[:30], tg[45:100]]
+    fields = ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info")
+    refs = []
+    for b in batches:
+        r = ex.explain_batch(b, cfg["p"], cfg["seed"])
+        torch.cuda.synchronize()
+        refs.append([{f: getattr(e, f).clone() for f in fields} for e in r])
+    outs = list(ex.explain_batches(batches, cfg["p"], cfg["seed"], prepare_each=True))
+    torch.cuda.synchronize()
+    assert len(outs) == len(batches)
+    for i, (out, ref) in enumerate(zip(outs, refs)):
+        _say("pipelined batch", i, len(batches[i]))
+        assert len(out) == len(batches[i])
+        for t, e in enumerate(out):
+            assert e.target == batches[i][t]
+            for f in fields:
+                assert torch.equal(getattr(e, f), ref[t][f]), (i, t, f)
+    gen = ex.explain_batches(batches, cfg["p"], cfg["seed"])
+    next(gen)
+    gen.close()                          # the second batch's extraction was queued
+    again = ex.explain_batch(batches[1], cfg["p"], cfg["seed"])
+    torch.cuda.synchronize()
+    for t, e in enumerate(again):
+        for f in fields:
+            assert torch.equal(getattr(e, f), refs[1][t][f]), (t, f)

@@ -104,6 +104,10 @@ def test_batch_entry_points_reject_bad_arguments():
     assert lib.gnnshap_extract_batch_workspace(0, 4, ctypes.byref(n)) == L.EINVAL
     assert lib.gnnshap_extract_batch_workspace(100, 4, ctypes.byref(n)) == L.OK and n.value > 0
     assert lib.gnnshap_extract_batch(None, None, 1, None, None, 0, None) == L.EINVAL
+    assert lib.gnnshap_extract_batch_launch(None, None, 1, None, None, 0, None) == L.EINVAL
+    sgs = (L.gnnshap_subgraph * 2)()
+    assert lib.gnnshap_extract_batch_finish(sgs, 2) == L.EINVAL       # nothing launched by this thread
+    assert lib.gnnshap_extract_batch_finish(None, 2) == L.EINVAL
     assert lib.gnnshap_explain_batch_workspace(None, None, 1, None, ctypes.byref(n)) == L.EINVAL
     assert lib.gnnshap_explain_batch(None, None, None, 0, None, None, -1, None, None, None, None, None, None, None,
                                      None, 0, None) == L.EINVAL
