@@ -71,22 +71,27 @@ HostStage* host_stage(size_t bytes, int ring) {
   if (ring < 0 || ring > 1) return nullptr;
   HostStage* h = &d->ring[ring][d->next[ring]];
   d->next[ring] ^= 1;
-  if (!h->done && hipEventCreateWithFlags(&h->done, hipEventDisableTiming) != hipSuccess) return nullptr;
-  if (h->pending && hipEventSynchronize(h->done) != hipSuccess) return nullptr;
-  h->pending = false;
-  if (h->cap < bytes) {
-    if (h->buf) (void)hipHostFree(h->buf);
-    h->buf = nullptr;
-    h->cap = 0;
-    const size_t want = bytes + bytes / 2 + 4096;
+  // Growing a buffer (page-locked allocation takes milliseconds) grows the
+  // other buffer of the ring too when it is idle, so that the cost falls on
+  // one call.
+  const size_t want = bytes + bytes / 2 + 4096;
+  for (HostStage* x : {h, &d->ring[ring][d->next[ring]]}) {
+    if (!x->done && hipEventCreateWithFlags(&x->done, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (x != h && (x->pending || x->cap >= bytes)) continue;
+    if (x->pending && hipEventSynchronize(x->done) != hipSuccess) return nullptr;
+    x->pending = false;
+    if (x->cap >= bytes) continue;
+    if (x->buf) (void)hipHostFree(x->buf);
+    x->buf = nullptr;
+    x->cap = 0;
     void* p = nullptr;
     // coherent: the GPU reads it uncached, so a reused buffer is never stale
     if (hipHostMalloc(&p, want, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
       (void)hipGetLastError();
       return nullptr;
     }
-    h->buf = static_cast<char*>(p);
-    h->cap = want;
+    x->buf = static_cast<char*>(p);
+    x->cap = want;
   }
   return h;
 }
