@@ -336,8 +336,8 @@ int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan
 /* ------------------------------------------------------------------------ */
 
 /* Which solver the plan's system takes: *path = 1 if one workgroup factors
- * and solves it (M <= 256), 2 if it is factored panel by panel by small
- * workgroups (256 < M <= 448), 0 if it takes the multi-block Cholesky. */
+ * and solves it (M <= 192), 2 if it is factored panel by panel by small
+ * workgroups (192 < M <= 448), 0 if it takes the multi-block Cholesky. */
 int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path);
 
 /* Arms timing for the kernels whose name starts with `kernel_name` (e.g.

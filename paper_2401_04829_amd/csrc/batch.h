@@ -95,9 +95,15 @@ int launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t 
                         hipStream_t s);
 int launch_solve_rhs(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
                      int64_t max_nch, hipStream_t s);
-// max_panels: the most 64-player panels of a job above the panel-path size
-// (0 if none); small: whether some job takes the one-workgroup kernel.
-int launch_solve_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, bool small, hipStream_t s);
+// Panel-path systems (J.panel): the factorisation of G~ (max_panels = the
+// most 64-player panels of a job), which does not read the right-hand side,
+// and the solve (centring, forward and backward substitution).  Other jobs
+// are skipped by both.
+int launch_panel_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, hipStream_t s);
+int launch_panel_solve(const SolveJob* jobs, int64_t n, hipStream_t s);
+// The one-workgroup systems (factorisation and solves in one kernel; panel
+// jobs are skipped).
+int launch_solve_one(const SolveJob* jobs, int64_t n, hipStream_t s);
 // Whether a one-workgroup-size system takes the panel path.
 bool solve_panel_path(const gnnshap_sample_plan* plan);
 

@@ -5,6 +5,13 @@
 // does not fit the batched kernels go through the single-target calls inside
 // the same sequence; every value is the one the single-target calls give.
 #include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <thread>
 #include <vector>
 
 #include "batch.h"
@@ -13,7 +20,7 @@
 namespace gnnshap {
 
 // Side streams of the current device for the calling thread, each with the
-// two events that fork work onto it and join it back (created on first use,
+// events that fork work onto it and join it back, and one more (created on first use,
 // default priority, kept until the process ends).  Two: with the caller's
 // stream and the extraction stream of a pipelined caller that makes four,
 // the number of hardware queues a process gets by default, so no two of them
@@ -22,7 +29,7 @@ constexpr int kSideStreams = 2;
 
 struct SideStream {
   hipStream_t stream = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr, aux = nullptr;
 };
 
 struct DeviceSides {
@@ -41,13 +48,90 @@ SideStream* side_stream(int i) {
   for (SideStream& x : d.side) {
     if (hipStreamCreateWithFlags(&x.stream, hipStreamNonBlocking) != hipSuccess ||
         hipEventCreateWithFlags(&x.fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess) {
+        hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&x.aux, hipEventDisableTiming) != hipSuccess) {
       (void)hipGetLastError();
       return nullptr;
     }
   }
   per_device.push_back(d);
   return &per_device.back().side[i];
+}
+
+// A host thread that issues one target group's launches while the calling
+// thread issues the other's: every launch and event costs a few
+// microseconds of host time, and for a batch of 100 small targets that host
+// time, not the GPU, bounds the step.  One per calling thread, created on
+// first use; between jobs it spins for up to kSpinUs, then sleeps.
+class Issuer {
+ public:
+  static constexpr int kSpinUs = 1000;
+  Issuer() : th_([this] { loop(); }) {}
+  ~Issuer() {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      stop_ = true;
+    }
+    cv_.notify_one();
+    th_.join();
+  }
+  // Runs f on the worker (with `device` current) and returns at once.
+  void post(int device, std::function<int()> f) {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      job_ = std::move(f);
+      device_ = device;
+      state_.store(1, std::memory_order_release);
+    }
+    cv_.notify_one();
+  }
+  // Waits for the posted job; its status, with its error text copied to the
+  // calling thread.
+  int wait() {
+    while (state_.load(std::memory_order_acquire) != 2) std::this_thread::yield();
+    state_.store(0, std::memory_order_relaxed);
+    if (status_ != GNNSHAP_OK) return fail(status_, "%s", msg_);
+    return GNNSHAP_OK;
+  }
+
+ private:
+  void loop() {
+    for (;;) {
+      const auto t0 = std::chrono::steady_clock::now();
+      while (state_.load(std::memory_order_acquire) != 1 &&
+             std::chrono::steady_clock::now() - t0 < std::chrono::microseconds(kSpinUs))
+        std::this_thread::yield();
+      std::function<int()> f;
+      int dev = 0;
+      {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [this] { return stop_ || state_.load(std::memory_order_acquire) == 1; });
+        if (stop_) return;
+        f = std::move(job_);
+        dev = device_;
+      }
+      int st = hipSetDevice(dev) == hipSuccess ? GNNSHAP_OK : fail(GNNSHAP_EHIP, "hipSetDevice failed");
+      if (st == GNNSHAP_OK) st = f();
+      status_ = st;
+      std::strncpy(msg_, st == GNNSHAP_OK ? "" : gnnshap_last_error(), sizeof(msg_) - 1);
+      msg_[sizeof(msg_) - 1] = 0;
+      state_.store(2, std::memory_order_release);
+    }
+  }
+  std::mutex mu_;
+  std::condition_variable cv_;
+  std::function<int()> job_;
+  int device_ = 0;
+  std::atomic<int> state_{0};      // 0 idle, 1 posted, 2 done
+  int status_ = GNNSHAP_OK;
+  char msg_[512] = "";
+  bool stop_ = false;
+  std::thread th_;
+};
+
+Issuer& issuer() {
+  static thread_local Issuer w;
+  return w;
 }
 
 struct DeviceStages {
@@ -370,7 +454,9 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       // stream 0, group 1 on `o`, and G~ of every batched system is built on
       // side stream 1 while the coalitions are evaluated.  Three event pairs:
       // the fork after sampling (side streams 0 and 1 wait on it), G~ ready
-      // (both factorisations wait on it) and the join of side stream 0.
+      // (both factorisations wait on it) and the join of side stream 0.  The
+      // launches of side stream 0 are issued by the worker thread while this
+      // thread issues the others.
       gnnshap::SideStream* side0 = nullptr;
       gnnshap::SideStream* mat = nullptr;
       if (grp[0].end > grp[0].begin) {
@@ -389,10 +475,10 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
         if (side0) GS_HIP(hipStreamWaitEvent(side0->stream, f->fork, 0));
         if (mat) GS_HIP(hipStreamWaitEvent(mat->stream, f->fork, 0));
       }
-      // 1. coalition values
-      for (int gi = 0; gi < 2; ++gi) {
+      // coalition values of group gi
+      auto eval_group = [&](int gi) -> int {
         const Group& G = grp[gi];
-        if (G.end == G.begin) continue;
+        if (G.end == G.begin) return GNNSHAP_OK;
         int st_eval = GNNSHAP_EUNSUPPORTED;
         if (G.eval_all) {
           const gnnshap::EvalModel md{model->XW1, model->b ? model->b[0] : nullptr, model->W[1],
@@ -413,29 +499,28 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
               return st;
           }
         }
-      }
-      // 2. G~ (launched after the evaluations, which are on the longer chains)
-      if (mat) {
-        if (int st = gnnshap::launch_solve_matrix(b.solve, nv, mM, mw, mnrb, mat->stream)) return st;
-        GS_HIP(hipEventRecord(mat->join, mat->stream));
-      }
-      // 3. least squares: right-hand sides, then (with G~ ready) the factorisations
-      for (int gi = 0; gi < 2; ++gi) {
-        const Group& G = grp[gi];
-        if (G.solve_count > 0)
-          if (int st = gnnshap::launch_solve_rhs(b.solve + G.solve_begin, G.solve_count, G.bM, G.bw, G.bh, G.bnch,
-                                                 gs[gi]))
-            return st;
-      }
-      // the one-workgroup group first: its single launch should not queue behind
-      // the host's launches of the panel sequence
-      for (int gi = 1; gi >= 0; --gi) {
+        return GNNSHAP_OK;
+      };
+      // right-hand side, then the factorisations and solves of group gi:
+      // one-workgroup systems (factorisation and solves in one kernel) once G~
+      // is ready; panel-path systems factored on the matrix stream right
+      // behind G~ (the factorisation does not read the right-hand side), then
+      // solved on the group's stream once both are ready
+      auto solve_group = [&](int gi) -> int {
         const Group& G = grp[gi];
         if (G.solve_count > 0) {
-          GS_HIP(hipStreamWaitEvent(gs[gi], mat->join, 0));
-          if (int st = gnnshap::launch_solve_factor(b.solve + G.solve_begin, G.solve_count, G.max_panels, G.small,
-                                                    gs[gi]))
-            return st;
+          const gnnshap::SolveJob* jb = b.solve + G.solve_begin;
+          if (int st = gnnshap::launch_solve_rhs(jb, G.solve_count, G.bM, G.bw, G.bh, G.bnch, gs[gi])) return st;
+          if (G.max_panels > 0) {
+            if (int st = gnnshap::launch_panel_factor(jb, G.solve_count, G.max_panels, mat->stream)) return st;
+            GS_HIP(hipEventRecord(mat->aux, mat->stream));
+            GS_HIP(hipStreamWaitEvent(gs[gi], mat->aux, 0));
+            if (int st = gnnshap::launch_panel_solve(jb, G.solve_count, gs[gi])) return st;
+          }
+          if (G.small) {
+            GS_HIP(hipStreamWaitEvent(gs[gi], mat->join, 0));
+            if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
+          }
         }
         for (int64_t t : G.rest) {
           if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
@@ -443,12 +528,39 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
                                          L.solve_bytes[t], gs[gi]))
             return st;
         }
+        return GNNSHAP_OK;
+      };
+      // G~ first: it depends on the masks only, and queued ahead of the
+      // evaluations it gets the GPU before their many workgroups fill it
+      int st = GNNSHAP_OK;
+      if (mat) {
+        st = gnnshap::launch_solve_matrix(b.solve, nv, mM, mw, mnrb, mat->stream);
+        if (st == GNNSHAP_OK && hipEventRecord(mat->join, mat->stream) != hipSuccess)
+          st = gnnshap::fail(GNNSHAP_EHIP, "hipEventRecord failed");
+        if (st != GNNSHAP_OK) return st;
       }
+      // group 0 on the worker: evaluation, right-hand side, factorisation, join record
+      gnnshap::Issuer* worker = nullptr;
       if (side0) {
-        GS_HIP(hipEventRecord(side0->join, side0->stream));
-        GS_HIP(hipStreamWaitEvent(o, side0->join, 0));
+        int dev = 0;
+        GS_HIP(hipGetDevice(&dev));
+        worker = &gnnshap::issuer();
+        worker->post(dev, [&]() -> int {
+          if (int st = eval_group(0)) return st;
+          if (int st = solve_group(0)) return st;
+          GS_HIP(hipEventRecord(side0->join, side0->stream));
+          return GNNSHAP_OK;
+        });
       }
-    return GNNSHAP_OK;
+      st = eval_group(1);
+      if (st == GNNSHAP_OK) st = solve_group(1);
+      if (worker) {
+        const int wst = worker->wait();
+        if (st == GNNSHAP_OK) st = wst;
+        if (st == GNNSHAP_OK && hipStreamWaitEvent(o, side0->join, 0) != hipSuccess)
+          st = gnnshap::fail(GNNSHAP_EHIP, "hipStreamWaitEvent failed");
+      }
+      return st;
   };
   if (int st = issue(s)) return st;
   return GNNSHAP_OK;

@@ -35,7 +35,7 @@ constexpr int kTB = 64;        // diagonal block of the triangular solves (one w
 constexpr int64_t kSeg = 256;  // segment of the triangular solves (its triangle in LDS)
 constexpr int kMaxChunks = 256;
 constexpr int kMidMax = 448;   // largest system of the global-memory one-workgroup path
-constexpr int64_t kPanelMin = 256;  // larger systems (up to kMidMax) take the panel path
+constexpr int64_t kPanelMin = 192;  // larger systems (up to kMidMax) take the panel path
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -1365,10 +1365,17 @@ double binom_d(int64_t n, int64_t r) {
 
 // Also clears the count matrix (M rows of ld) for the Gram's atomics: the
 // job's nrb x wpr workgroups each clear an equal share of it.
+// Jobs of at most kGramWhole random row words get each count from one
+// workgroup (plain stores); larger ones are split over chunks of kGramChunk
+// words whose partial counts are added with integer atomics into zeroed counts.
+constexpr int64_t kGramChunk = 32;
+constexpr int64_t kGramWhole = 128;
+
 __global__ void __launch_bounds__(64) k_transpose_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.z];
   if (J.kr <= 0 || blockIdx.x >= J.nrb || blockIdx.y >= J.wpr) return;
   transpose_body(J.masks, J.wpr, J.rb0, J.kr, J.M, J.T, blockIdx.x, blockIdx.y);
+  if (J.nrb <= kGramWhole) return;             // every count is stored by one workgroup
   const int64_t nblk = J.nrb * J.wpr, blk = static_cast<int64_t>(blockIdx.x) * J.wpr + blockIdx.y;
   const int64_t total = J.M * J.ld, per = (total + nblk - 1) / nblk;
   const int64_t e0 = blk * per, e1 = e0 + per < total ? e0 + per : total;
@@ -1376,18 +1383,21 @@ __global__ void __launch_bounds__(64) k_transpose_batch(const gnnshap::SolveJob*
 }
 
 // Workgroup (tile, chunk, job): tile = J' (J' + 1) / 2 + I' over the tiles
-// I' <= J' of the job, chunk = kGramChunk row words.
-constexpr int64_t kGramChunk = 32;
-
+// I' <= J' of the job, chunk = kGramChunk row words (chunk 0 only when the
+// job's counts are whole).
 __global__ void __launch_bounds__(256) k_gram_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.z];
   const int64_t nb = (J.M + 63) / 64;
   const int64_t tile = blockIdx.x, w0 = static_cast<int64_t>(blockIdx.y) * kGramChunk;
-  if (J.kr <= 0 || tile >= nb * (nb + 1) / 2 || w0 >= J.nrb) return;
+  const bool whole = J.nrb <= kGramWhole;
+  if (J.kr <= 0 || tile >= nb * (nb + 1) / 2 || w0 >= J.nrb || (whole && blockIdx.y > 0)) return;
   int64_t Jt = 0;
   while ((Jt + 1) * (Jt + 2) / 2 <= tile) ++Jt;
   const int64_t It = tile - Jt * (Jt + 1) / 2;
-  gram_part_body(J.T, w0, w0 + kGramChunk < J.nrb ? w0 + kGramChunk : J.nrb, J.M, J.ld, J.counts, It, Jt);
+  if (whole)
+    gram_body(J.T, J.nrb, J.M, J.ld, J.counts, It, Jt);
+  else
+    gram_part_body(J.T, w0, w0 + kGramChunk < J.nrb ? w0 + kGramChunk : J.nrb, J.M, J.ld, J.counts, It, Jt);
 }
 
 __global__ void __launch_bounds__(kTileRows) k_rhs_tile_batch(const gnnshap::SolveJob* __restrict__ jobs) {
@@ -1439,51 +1449,27 @@ __global__ void __launch_bounds__(kMidThreads) k_solve_one_batch(const gnnshap::
 // ---- panel path (kPanelMin < M <= kMidMax): one launch per panel step -----------------------
 //
 // The same blocked factorisation as the one-workgroup path (64-wide panels,
-// diagonal factors inverted, L_Ip = A_Ip W_pp^T, forward substitution
-// alongside), spread over many small workgroups: per panel p, one workgroup
-// per block below the diagonal forms L_Ip and updates r_I; then one
-// workgroup per trailing tile (I, J) subtracts L_Ip L_Jp^T, and the one
-// holding the next diagonal block factors and inverts it right away.  The
-// largest systems of a batch thus finish in ~20 us per panel instead of
-// occupying one compute unit for their whole factorisation.
+// diagonal factors inverted, L_Ip = A_Ip W_pp^T), spread over many small
+// workgroups: per panel p, one workgroup per block below the diagonal forms
+// L_Ip; then one workgroup per trailing tile (I, J) subtracts L_Ip L_Jp^T,
+// and the one holding the next diagonal block factors and inverts it right
+// away.  The largest systems of a batch thus finish in ~20 us per panel
+// instead of occupying one compute unit for their whole factorisation.  The
+// factorisation reads G~ only, so it can run before the right-hand side
+// exists; one workgroup per system then centres the right-hand side and runs
+// the forward and backward substitutions (k_pp_solve).
 
 constexpr size_t kPanelLds = (3 * kHB + 64) * sizeof(float);
 
-// rv <- P dv (the centred right-hand side, fp32), info <- 0.  One workgroup.
-__device__ __forceinline__ void pp_centre(const double* __restrict__ dvg, int64_t M, float* __restrict__ rv,
-                                          int32_t* info) {
-  __shared__ double red[4];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  if (tid == 0) *info = 0;
-  double sv = 0.0;
-  for (int64_t i = tid; i < M; i += 256) sv += dvg[i];
-  for (int off = 32; off > 0; off >>= 1) sv += __shfl_xor(sv, off);
-  if (lane == 0) red[wave] = sv;
-  __syncthreads();
-  const double mean = (red[0] + red[1] + red[2] + red[3]) / static_cast<double>(M);
-  for (int64_t i = tid; i < M; i += 256) rv[i] = static_cast<float>(dvg[i] - mean);
-  __syncthreads();
-}
-
 // Diagonal block p already in D0 (lower part; rows and columns past M zero):
-// D0 <- L_pp, D1 <- W_pp = L_pp^-1, stored to G and Wd[p]; r_p <- z_p = W_pp r_p.
+// D0 <- L_pp, D1 <- W_pp = L_pp^-1, stored to G and Wd[p].
 __device__ __forceinline__ void pp_diag(float* G, int64_t ld, int64_t M, int64_t p, float* D0, float* D1,
-                                        float* __restrict__ Wd, float* rv, int32_t* info, float* vec) {
+                                        float* __restrict__ Wd, int32_t* info) {
   const int tid = threadIdx.x, wave = tid >> 6;
   const int64_t o = p * 64;
-  if (tid < 64) {
-    if (o + tid >= M) D0[tid * kHP + tid] = 1.f;   // identity past M
-    vec[tid] = o + tid < M ? rv[o + tid] : 0.f;
-  }
+  if (tid < 64 && o + tid >= M) D0[tid * kHP + tid] = 1.f;   // identity past M
   __syncthreads();
-  if (wave == 0) {
-    chol_inv64(D0, D1, nullptr, o, info);
-    const int lane = tid;
-    float z = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < 64; ++c) z += D1[lane * kHP + c] * vec[c];
-    if (o + lane < M) rv[o + lane] = z;
-  }
+  if (wave == 0) chol_inv64(D0, D1, nullptr, o, info);
   __syncthreads();
   for (int t = tid; t < 64 * 64; t += 256) {
     const int r = t >> 6, c = t & 63;
@@ -1512,18 +1498,18 @@ __device__ __forceinline__ void pp_load(const float* G, int64_t ld, int64_t M, i
   }
 }
 
-// Start: centring, then the first diagonal block.
+// Start: info <- 0, then the first diagonal block.
 __device__ __forceinline__ void pp_start_body(const gnnshap::SolveJob& J) {
   extern __shared__ __align__(16) unsigned char smem[];
   float* D0 = reinterpret_cast<float*>(smem);
   float* D1 = D0 + kHB;
   float* G = reinterpret_cast<float*>(J.counts);
-  pp_centre(J.dv, J.M, J.rv, J.info);
+  if (threadIdx.x == 0) *J.info = 0;
   pp_load(G, J.ld, J.M, 0, 0, D0, true);
-  pp_diag(G, J.ld, J.M, 0, D0, D1, J.Wd, J.rv, J.info, D1 + kHB);
+  pp_diag(G, J.ld, J.M, 0, D0, D1, J.Wd, J.info);
 }
 
-// Panel p, block I below the diagonal (workgroup x): L_Ip = A_Ip W_pp^T, r_I -= L_Ip z_p.
+// Panel p, block I below the diagonal (workgroup x): L_Ip = A_Ip W_pp^T.
 __device__ __forceinline__ void pp_column_body(const gnnshap::SolveJob& J, int64_t p, int64_t I) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int64_t M = J.M, nblk = (M + 63) / 64;
@@ -1533,31 +1519,22 @@ __device__ __forceinline__ void pp_column_body(const gnnshap::SolveJob& J, int64
   float* G = reinterpret_cast<float*>(J.counts);
   const int tid = threadIdx.x;
   const int64_t bi = p + 1 + I, o = p * 64;
-  float* zp = D1 + kHB;                          // z_p
   {
     float w[16];
 #pragma unroll
     for (int q = 0; q < 16; ++q) w[q] = J.Wd[p * 4096 + tid + 256 * q];
-    const float zv = tid < 64 ? J.rv[o + tid] : 0.f;   // o + 64 <= M here
     pp_load(G, J.ld, M, bi, p, P, false);
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int t = tid + 256 * q;
       D1[(t >> 6) * kHP + (t & 63)] = w[q];
     }
-    if (tid < 64) zp[tid] = zv;
   }
   __syncthreads();
   mm64<true>(P, D1, P, 1.f, 0.f);
   for (int t = tid; t < 64 * 64; t += 256) {
     const int r = t >> 6, c = t & 63;
     if (64 * bi + r < M) G[(64 * bi + r) * J.ld + o + c] = P[r * kHP + c];
-  }
-  if (tid < 64 && 64 * bi + tid < M) {
-    float sum = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < 64; ++c) sum += P[tid * kHP + c] * zp[c];
-    J.rv[64 * bi + tid] -= sum;
   }
 }
 
@@ -1583,7 +1560,7 @@ __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_
   __syncthreads();
   mm64<true>(X, I == Jb ? X : Y, A, -1.f, 1.f);
   if (I == 0 && Jb == 0) {
-    pp_diag(G, J.ld, M, p + 1, A, X, J.Wd, J.rv, J.info, Y + kHB);
+    pp_diag(G, J.ld, M, p + 1, A, X, J.Wd, J.info);
     return;
   }
   for (int t = tid; t < 64 * 64; t += 256) {
@@ -1593,20 +1570,67 @@ __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_
   }
 }
 
-// Backward substitution psi_p = W_pp^T (z_p - sum_I L_Ip^T psi_I) and phi =
-// Delta/M + psi; 1024 threads (64 columns x 16 row groups), z and psi in LDS.
+// One workgroup per system, after the factorisation and the right-hand
+// side: r = P dv (centred, fp32), forward substitution z_p = W_pp (r_p -
+// sum_{J<p} L_pJ z_J) panel by panel (left-looking: 16 threads per row read
+// the row's L blocks), backward substitution psi_p = W_pp^T (z_p - sum_{I>p}
+// L_Ip^T psi_I), phi = Delta/M + psi.  1024 threads, vectors in LDS.
 constexpr int kBackThreads = 1024;
 
-__device__ __forceinline__ void pp_back_body(const gnnshap::SolveJob& J) {
+__device__ __forceinline__ void pp_solve_body(const gnnshap::SolveJob& J) {
   __shared__ float red[kBackThreads];
   __shared__ float vec[kMidMax];
   __shared__ float Wl[64 * 65];                  // W_pp of the current panel
+  __shared__ double dred[kBackThreads / 64];
   const int64_t M = J.M, ld = J.ld, nblk = (M + 63) / 64;
   const float* G = reinterpret_cast<const float*>(J.counts);
   const int tid = threadIdx.x, c = tid & 63, g = tid >> 6;
   constexpr int NG = kBackThreads / 64;
-  for (int64_t i = tid; i < M; i += kBackThreads) vec[i] = J.rv[i];
-  __syncthreads();
+  // centring: the mean of dv summed in a fixed order
+  {
+    double sv = 0.0;
+    for (int64_t i = tid; i < M; i += kBackThreads) sv += J.dv[i];
+    for (int off = 32; off > 0; off >>= 1) sv += __shfl_xor(sv, off);
+    if (c == 0) dred[g] = sv;
+    __syncthreads();
+    double tot = 0.0;
+#pragma unroll
+    for (int gg = 0; gg < NG; ++gg) tot += dred[gg];
+    const double mean = tot / static_cast<double>(M);
+    for (int64_t i = tid; i < M; i += kBackThreads) vec[i] = static_cast<float>(J.dv[i] - mean);
+    __syncthreads();
+  }
+  // forward: thread (r = tid / 16, q = tid % 16) of row o + r; rows r >= 64 idle
+  {
+    const int r = tid >> 4, q = tid & 15;
+    for (int64_t p = 0; p < nblk; ++p) {
+      const int64_t o = p * 64;
+      float acc = 0.f;
+      if (r < 64 && o + r < M) {
+        const float* Lr = G + (o + r) * ld;
+#pragma unroll 4
+        for (int64_t col = q; col < o; col += 16) acc += Lr[col] * vec[col];
+      }
+      float wv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) wv[e] = r < 64 ? J.Wd[p * 4096 + r * 64 + q + 16 * e] : 0.f;
+#pragma unroll
+      for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 16);
+      if (r < 64 && q == 0) red[r] = o + r < M ? vec[o + r] - acc : 0.f;   // r_p - sum_J L_pJ z_J
+      __syncthreads();
+      float z = 0.f;
+      if (r < 64) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) z += wv[e] * red[q + 16 * e];
+      }
+#pragma unroll
+      for (int off = 8; off > 0; off >>= 1) z += __shfl_xor(z, off, 16);
+      __syncthreads();
+      if (r < 64 && q == 0 && o + r < M) vec[o + r] = z;
+      __syncthreads();
+    }
+  }
+  // backward
   for (int64_t p = nblk - 1; p >= 0; --p) {
     const int64_t o = p * 64;
     float wv[4096 / kBackThreads];
@@ -1659,9 +1683,9 @@ __global__ void __launch_bounds__(256) k_pp_trail(const gnnshap::SolveJob* __res
   const gnnshap::SolveJob J = jobs[blockIdx.y];
   if (J.panel) pp_trail_body(J, p, blockIdx.x);
 }
-__global__ void __launch_bounds__(kBackThreads) k_pp_back(const gnnshap::SolveJob* __restrict__ jobs) {
+__global__ void __launch_bounds__(kBackThreads) k_pp_solve(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.x];
-  if (J.panel) pp_back_body(J);
+  if (J.panel) pp_solve_body(J);
 }
 __global__ void __launch_bounds__(256) k_pp_start_one(gnnshap::SolveJob J) { pp_start_body(J); }
 __global__ void __launch_bounds__(256) k_pp_column_one(gnnshap::SolveJob J, int64_t p) {
@@ -1670,7 +1694,7 @@ __global__ void __launch_bounds__(256) k_pp_column_one(gnnshap::SolveJob J, int6
 __global__ void __launch_bounds__(256) k_pp_trail_one(gnnshap::SolveJob J, int64_t p) {
   pp_trail_body(J, p, blockIdx.x);
 }
-__global__ void __launch_bounds__(kBackThreads) k_pp_back_one(gnnshap::SolveJob J) { pp_back_body(J); }
+__global__ void __launch_bounds__(kBackThreads) k_pp_solve_one(gnnshap::SolveJob J) { pp_solve_body(J); }
 
 // Whether `kernel` may be launched with `bytes` of dynamic LDS on the current
 // device (its static LDS counts against the same limit); above the 64 KiB
@@ -1814,7 +1838,10 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
         }
         GS_LAUNCHED();
       }
-      k_pp_back_one<<<1, kBackThreads, 0, s>>>(J);
+      {
+        GS_TIMED("k_pp_solve", s);
+        k_pp_solve_one<<<1, kBackThreads, 0, s>>>(J);
+      }
       GS_LAUNCHED();
       return GNNSHAP_OK;
     }
@@ -2003,40 +2030,49 @@ int gnnshap::launch_solve_rhs(const SolveJob* jobs, int64_t n, int64_t max_M, in
   return GNNSHAP_OK;
 }
 
-int gnnshap::launch_solve_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, bool small, hipStream_t s) {
-  if (n < 1) return GNNSHAP_OK;
+int gnnshap::launch_panel_factor(const SolveJob* jobs, int64_t n, int64_t max_panels, hipStream_t s) {
+  if (n < 1 || max_panels < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   const unsigned nn = static_cast<unsigned>(n);
-  if (max_panels > 0) {
+  {
+    GS_TIMED("k_pp_start", s);
+    k_pp_start<<<nn, 256, kPanelLds, s>>>(jobs);
+  }
+  GS_LAUNCHED();
+  for (int64_t p = 0; p + 1 < max_panels; ++p) {
+    const int64_t nI = max_panels - p - 1;
     {
-      GS_TIMED("k_pp_start", s);
-      k_pp_start<<<nn, 256, kPanelLds, s>>>(jobs);
+      GS_TIMED("k_pp_column", s);
+      k_pp_column<<<dim3(static_cast<unsigned>(nI), nn), 256, kPanelLds, s>>>(jobs, p);
     }
     GS_LAUNCHED();
-    for (int64_t p = 0; p + 1 < max_panels; ++p) {
-      const int64_t nI = max_panels - p - 1;
-      {
-        GS_TIMED("k_pp_column", s);
-        k_pp_column<<<dim3(static_cast<unsigned>(nI), nn), 256, kPanelLds, s>>>(jobs, p);
-      }
-      GS_LAUNCHED();
-      {
-        GS_TIMED("k_pp_trail", s);
-        k_pp_trail<<<dim3(static_cast<unsigned>(nI * (nI + 1) / 2), nn), 256, kPanelLds, s>>>(jobs, p);
-      }
-      GS_LAUNCHED();
+    {
+      GS_TIMED("k_pp_trail", s);
+      k_pp_trail<<<dim3(static_cast<unsigned>(nI * (nI + 1) / 2), nn), 256, kPanelLds, s>>>(jobs, p);
     }
-    k_pp_back<<<nn, kBackThreads, 0, s>>>(jobs);
     GS_LAUNCHED();
   }
-  if (small) {
-    const size_t lds = kMidLds;
-    static bool raised = false;
-    if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
-      return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
-    GS_TIMED("k_solve_one_batch", s);
-    k_solve_one_batch<<<nn, kMidThreads, lds, s>>>(jobs);
-  }
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_panel_solve(const SolveJob* jobs, int64_t n, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  GS_TIMED("k_pp_solve", s);
+  k_pp_solve<<<static_cast<unsigned>(n), kBackThreads, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_solve_one(const SolveJob* jobs, int64_t n, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  const size_t lds = kMidLds;
+  static bool raised = false;
+  if (!allow_lds(reinterpret_cast<const void*>(&k_solve_one_batch), lds, raised))
+    return fail(GNNSHAP_EUNSUPPORTED, "batched solve needs %zu bytes of LDS", lds);
+  GS_TIMED("k_solve_one_batch", s);
+  k_solve_one_batch<<<static_cast<unsigned>(n), kMidThreads, lds, s>>>(jobs);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }
