@@ -623,7 +623,7 @@ __device__ __forceinline__ void chol_inv8(float* S, float* Wb, int64_t o, int32_
   S[r * kHP + c] = lv;
   Wb[r * kHP + c] = wv;
   __builtin_amdgcn_wave_barrier();
-  if (bad != 0 && lane == 0) atomicCAS(info, 0, static_cast<int32_t>(o + bad));
+  if (bad != 0 && lane == 0 && info) atomicCAS(info, 0, static_cast<int32_t>(o + bad));
 }
 
 // One wavefront, 16 x 16 blocks: the same product as four fp32 MFMA 16x16x4.
@@ -1450,32 +1450,41 @@ __global__ void __launch_bounds__(kMidThreads) k_solve_one_batch(const gnnshap::
 //
 // The same blocked factorisation as the one-workgroup path (64-wide panels,
 // diagonal factors inverted, L_Ip = A_Ip W_pp^T), spread over many small
-// workgroups: per panel p, one workgroup per block below the diagonal forms
-// L_Ip; then one workgroup per trailing tile (I, J) subtracts L_Ip L_Jp^T,
-// and the one holding the next diagonal block factors and inverts it right
-// away.  The largest systems of a batch thus finish in ~20 us per panel
-// instead of occupying one compute unit for their whole factorisation.  The
+// workgroups, one launch per panel: one workgroup per trailing tile (I, J)
+// subtracts L_Ip L_Jp^T; the one holding the next diagonal block factors and
+// inverts it, and each one in the next panel's column updates that diagonal
+// block too, factors it again (the same operands and code, so the same
+// bits) and forms its L_I,p+1 = A_I,p+1 W^T at once, so the next panel's
+// blocks are ready when the launch ends.  The largest systems of a batch thus
+// finish in ~20 us per panel instead of occupying one compute unit for their
+// whole factorisation.  The
 // factorisation reads G~ only, so it can run before the right-hand side
 // exists; one workgroup per system then centres the right-hand side and runs
 // the forward and backward substitutions (k_pp_solve).
 
 constexpr size_t kPanelLds = (3 * kHB + 64) * sizeof(float);
 
+// In LDS: D (lower part valid) <- chol, W <- its inverse, for diagonal block
+// p of a system of M players (rows past M become the identity); `info`
+// receives a non-positive pivot (NULL: not reported).  Four wavefronts.
+__device__ __forceinline__ void pp_factor_diag(float* D, float* W, int64_t M, int64_t p, int32_t* info) {
+  const int tid = threadIdx.x;
+  if (tid < 64 && p * 64 + tid >= M) D[tid * kHP + tid] = 1.f;
+  __syncthreads();
+  if ((tid >> 6) == 0) chol_inv64(D, W, nullptr, p * 64, info);
+  __syncthreads();
+}
+
 // Diagonal block p already in D0 (lower part; rows and columns past M zero):
-// D0 <- L_pp, D1 <- W_pp = L_pp^-1, stored to G and Wd[p].
+// D0 <- L_pp, D1 <- W_pp = L_pp^-1, W_pp stored to Wd[p].  L_pp itself is
+// not stored: the substitutions use W_pp, and G's diagonal block keeps the
+// value the next panel's column workgroups read while this one runs.
 __device__ __forceinline__ void pp_diag(float* G, int64_t ld, int64_t M, int64_t p, float* D0, float* D1,
                                         float* __restrict__ Wd, int32_t* info) {
-  const int tid = threadIdx.x, wave = tid >> 6;
-  const int64_t o = p * 64;
-  if (tid < 64 && o + tid >= M) D0[tid * kHP + tid] = 1.f;   // identity past M
-  __syncthreads();
-  if (wave == 0) chol_inv64(D0, D1, nullptr, o, info);
-  __syncthreads();
-  for (int t = tid; t < 64 * 64; t += 256) {
-    const int r = t >> 6, c = t & 63;
-    if (o + r < M && c <= r) G[(o + r) * ld + o + c] = D0[r * kHP + c];
-    Wd[p * 4096 + t] = D1[r * kHP + c];
-  }
+  (void)G;
+  (void)ld;
+  pp_factor_diag(D0, D1, M, p, info);
+  for (int t = threadIdx.x; t < 64 * 64; t += 256) Wd[p * 4096 + t] = D1[(t >> 6) * kHP + (t & 63)];
 }
 
 // Block (bi, bj) (64 x 64 at rows 64 bi, columns 64 bj) of G into S, zero past M;
@@ -1498,49 +1507,45 @@ __device__ __forceinline__ void pp_load(const float* G, int64_t ld, int64_t M, i
   }
 }
 
-// Start: info <- 0, then the first diagonal block.
-__device__ __forceinline__ void pp_start_body(const gnnshap::SolveJob& J) {
+// Block bi of column p: A (in LDS, = A_{bi,p} updated by the earlier panels)
+// <- L_{bi,p} = A W_pp^T, stored to G.
+__device__ __forceinline__ void pp_form_column(float* G, int64_t ld, int64_t M, int64_t bi, int64_t p, float* A,
+                                               const float* W) {
+  mm64<true>(A, W, A, 1.f, 0.f);
+  for (int t = threadIdx.x; t < 64 * 64; t += 256) {
+    const int r = t >> 6, c = t & 63;
+    if (64 * bi + r < M) G[(64 * bi + r) * ld + p * 64 + c] = A[r * kHP + c];
+  }
+}
+
+// Start, workgroup I of the first column: I = 0 factors diagonal block 0
+// (info <- 0 first; L_00 and W_00 stored); I > 0 factors it too (not
+// reported) and forms L_I0.
+__device__ __forceinline__ void pp_start_body(const gnnshap::SolveJob& J, int64_t I) {
   extern __shared__ __align__(16) unsigned char smem[];
   float* D0 = reinterpret_cast<float*>(smem);
   float* D1 = D0 + kHB;
+  float* A = D1 + kHB;
   float* G = reinterpret_cast<float*>(J.counts);
-  if (threadIdx.x == 0) *J.info = 0;
-  pp_load(G, J.ld, J.M, 0, 0, D0, true);
-  pp_diag(G, J.ld, J.M, 0, D0, D1, J.Wd, J.info);
-}
-
-// Panel p, block I below the diagonal (workgroup x): L_Ip = A_Ip W_pp^T.
-__device__ __forceinline__ void pp_column_body(const gnnshap::SolveJob& J, int64_t p, int64_t I) {
-  extern __shared__ __align__(16) unsigned char smem[];
   const int64_t M = J.M, nblk = (M + 63) / 64;
-  if (p + 1 + I >= nblk) return;
-  float* P = reinterpret_cast<float*>(smem);
-  float* D1 = P + kHB;
-  float* G = reinterpret_cast<float*>(J.counts);
-  const int tid = threadIdx.x;
-  const int64_t bi = p + 1 + I, o = p * 64;
-  {
-    float w[16];
-#pragma unroll
-    for (int q = 0; q < 16; ++q) w[q] = J.Wd[p * 4096 + tid + 256 * q];
-    pp_load(G, J.ld, M, bi, p, P, false);
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int t = tid + 256 * q;
-      D1[(t >> 6) * kHP + (t & 63)] = w[q];
-    }
+  if (I >= nblk) return;
+  if (I == 0) {
+    if (threadIdx.x == 0) *J.info = 0;
+    pp_load(G, J.ld, M, 0, 0, D0, true);
+    pp_diag(G, J.ld, M, 0, D0, D1, J.Wd, J.info);
+    return;
   }
-  __syncthreads();
-  mm64<true>(P, D1, P, 1.f, 0.f);
-  for (int t = tid; t < 64 * 64; t += 256) {
-    const int r = t >> 6, c = t & 63;
-    if (64 * bi + r < M) G[(64 * bi + r) * J.ld + o + c] = P[r * kHP + c];
-  }
+  pp_load(G, J.ld, M, 0, 0, D0, true);
+  pp_load(G, J.ld, M, I, 0, A, false);
+  pp_factor_diag(D0, D1, M, 0, nullptr);
+  pp_form_column(G, J.ld, M, I, 0, A, D1);
 }
 
 // Panel p, trailing tile number `tile` (I >= J, row-major over the lower
-// triangle of the blocks below panel p): A_IJ -= L_Ip L_Jp^T; tile (0, 0) is
-// the next diagonal block and is factored at once.
+// triangle of the blocks below panel p): A_IJ -= L_Ip L_Jp^T.  Tile (0, 0)
+// is the next diagonal block and is factored at once (stored, reported);
+// tiles (I, 0) update the next diagonal block as well, factor it and form
+// L_{I, p+1}.
 __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_t p, int64_t tile) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int64_t M = J.M, nblk = (M + 63) / 64, nI = nblk - p - 1;
@@ -1561,6 +1566,15 @@ __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_
   mm64<true>(X, I == Jb ? X : Y, A, -1.f, 1.f);
   if (I == 0 && Jb == 0) {
     pp_diag(G, J.ld, M, p + 1, A, X, J.Wd, J.info);
+    return;
+  }
+  if (Jb == 0) {
+    // the next diagonal block: X <- A_{bj,bj} - L_{bj,p} L_{bj,p}^T, factored
+    pp_load(G, J.ld, M, bj, bj, X, true);
+    __syncthreads();
+    mm64<true>(Y, Y, X, -1.f, 1.f);
+    pp_factor_diag(X, Y, M, bj, nullptr);
+    pp_form_column(G, J.ld, M, bi, bj, A, Y);
     return;
   }
   for (int t = tid; t < 64 * 64; t += 256) {
@@ -1672,12 +1686,8 @@ __device__ __forceinline__ void pp_solve_body(const gnnshap::SolveJob& J) {
 }
 
 __global__ void __launch_bounds__(256) k_pp_start(const gnnshap::SolveJob* __restrict__ jobs) {
-  const gnnshap::SolveJob J = jobs[blockIdx.x];
-  if (J.panel) pp_start_body(J);
-}
-__global__ void __launch_bounds__(256) k_pp_column(const gnnshap::SolveJob* __restrict__ jobs, int64_t p) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
-  if (J.panel) pp_column_body(J, p, blockIdx.x);
+  if (J.panel) pp_start_body(J, blockIdx.x);
 }
 __global__ void __launch_bounds__(256) k_pp_trail(const gnnshap::SolveJob* __restrict__ jobs, int64_t p) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
@@ -1687,10 +1697,7 @@ __global__ void __launch_bounds__(kBackThreads) k_pp_solve(const gnnshap::SolveJ
   const gnnshap::SolveJob J = jobs[blockIdx.x];
   if (J.panel) pp_solve_body(J);
 }
-__global__ void __launch_bounds__(256) k_pp_start_one(gnnshap::SolveJob J) { pp_start_body(J); }
-__global__ void __launch_bounds__(256) k_pp_column_one(gnnshap::SolveJob J, int64_t p) {
-  pp_column_body(J, p, blockIdx.x);
-}
+__global__ void __launch_bounds__(256) k_pp_start_one(gnnshap::SolveJob J) { pp_start_body(J, blockIdx.x); }
 __global__ void __launch_bounds__(256) k_pp_trail_one(gnnshap::SolveJob J, int64_t p) {
   pp_trail_body(J, p, blockIdx.x);
 }
@@ -1822,16 +1829,11 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
       const int64_t nblk = gnnshap::ceil_div(M, 64);
       {
         GS_TIMED("k_pp_start", s);
-        k_pp_start_one<<<1, 256, kPanelLds, s>>>(J);
+        k_pp_start_one<<<static_cast<unsigned>(nblk), 256, kPanelLds, s>>>(J);
       }
       GS_LAUNCHED();
       for (int64_t p = 0; p + 1 < nblk; ++p) {
         const int64_t nI = nblk - p - 1;
-        {
-          GS_TIMED("k_pp_column", s);
-          k_pp_column_one<<<static_cast<unsigned>(nI), 256, kPanelLds, s>>>(J, p);
-        }
-        GS_LAUNCHED();
         {
           GS_TIMED("k_pp_trail", s);
           k_pp_trail_one<<<static_cast<unsigned>(nI * (nI + 1) / 2), 256, kPanelLds, s>>>(J, p);
@@ -2036,16 +2038,11 @@ int gnnshap::launch_panel_factor(const SolveJob* jobs, int64_t n, int64_t max_pa
   const unsigned nn = static_cast<unsigned>(n);
   {
     GS_TIMED("k_pp_start", s);
-    k_pp_start<<<nn, 256, kPanelLds, s>>>(jobs);
+    k_pp_start<<<dim3(static_cast<unsigned>(max_panels), nn), 256, kPanelLds, s>>>(jobs);
   }
   GS_LAUNCHED();
   for (int64_t p = 0; p + 1 < max_panels; ++p) {
     const int64_t nI = max_panels - p - 1;
-    {
-      GS_TIMED("k_pp_column", s);
-      k_pp_column<<<dim3(static_cast<unsigned>(nI), nn), 256, kPanelLds, s>>>(jobs, p);
-    }
-    GS_LAUNCHED();
     {
       GS_TIMED("k_pp_trail", s);
       k_pp_trail<<<dim3(static_cast<unsigned>(nI * (nI + 1) / 2), nn), 256, kPanelLds, s>>>(jobs, p);
