@@ -83,16 +83,21 @@ struct SolveJob {
   float* Wd;
   float* rv;                 // M: right-hand side, then z, then psi (panel path)
   int32_t panel;             // 1: the panel path, 0: one workgroup
+  int32_t counts_in;         // 1: G~ is built from the counts as the panel path first reads each block
 };
 // Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
 bool solve_batchable(const gnnshap_sample_plan* plan);
 size_t solve_slice_bytes(const gnnshap_sample_plan* plan);
 int solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice, SolveJob* job);
-// The solve of a batch in three launch sequences: G~ from the masks alone
-// (it may run while the coalitions are evaluated), the right-hand side from
-// the values, then the factorisations.
+// The solve of a batch in launch sequences: the integer counts, their row
+// sums and the scalars of G~ from the masks alone (they may run while the
+// coalitions are evaluated), the right-hand side from the values, then G~
+// and the factorisations.
 int launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_nrb,
                         hipStream_t s);
+// G~ in place of the counts for the jobs that do not build it as they read it
+// (after launch_solve_matrix).
+int launch_solve_build(const SolveJob* jobs, int64_t n, int64_t max_M, hipStream_t s);
 int launch_solve_rhs(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_half,
                      int64_t max_nch, hipStream_t s);
 // Panel-path systems (J.panel): the factorisation of G~ (max_panels = the

@@ -502,10 +502,11 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
         return GNNSHAP_OK;
       };
       // right-hand side, then the factorisations and solves of group gi:
-      // one-workgroup systems (factorisation and solves in one kernel) once G~
-      // is ready; panel-path systems factored on the matrix stream right
-      // behind G~ (the factorisation does not read the right-hand side), then
-      // solved on the group's stream once both are ready
+      // one-workgroup systems (G~ built in place, then factorisation and
+      // solves in one kernel) once the counts are ready; panel-path systems
+      // factored on the matrix stream right behind the counts (building G~ as
+      // each block is first read; the factorisation does not read the
+      // right-hand side), then solved on the group's stream once both are ready
       auto solve_group = [&](int gi) -> int {
         const Group& G = grp[gi];
         if (G.solve_count > 0) {
@@ -519,6 +520,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
           }
           if (G.small) {
             GS_HIP(hipStreamWaitEvent(gs[gi], mat->join, 0));
+            if (int st = gnnshap::launch_solve_build(jb, G.solve_count, G.bM, gs[gi])) return st;
             if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
           }
         }

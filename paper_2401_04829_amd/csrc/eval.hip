@@ -1321,16 +1321,22 @@ __global__ void __launch_bounds__(256) k_transform(const float* __restrict__ X, 
 #pragma unroll
   for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const float* xr = X + (row < n ? row : 0) * static_cast<int64_t>(d);
-#pragma unroll 4
-  for (int s = 0; s < kg; ++s) {
-    const int k = k0 + s;
-    const bool kin = k < ke && k < k0 + kg;
-    const float a = (kin && row < n) ? xr[k] : 0.f;
+  const int k1 = ke < k0 + kg ? ke : k0 + kg;     // this lane group's k range [k0, k1)
+  // sixteen steps at a time: every load of a batch is issued before its products
+  for (int s0 = 0; s0 < kg; s0 += 16) {
+    float a[16], b[16][NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const float b = kin ? W[static_cast<int64_t>(k) * h + t * 16 + c] : 0.f;
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[t], 0, 0, 0);
+    for (int i = 0; i < 16; ++i) {
+      const int k = k0 + s0 + i;
+      const bool kin = k < k1;
+      a[i] = (kin && row < n) ? xr[k] : 0.f;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) b[i][t] = kin ? W[static_cast<int64_t>(k) * h + t * 16 + c] : 0.f;
     }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[i][t], acc[t], 0, 0, 0);
   }
 #pragma unroll
   for (int t = 0; t < NT; ++t)

@@ -132,8 +132,43 @@ __global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ m
 
 // Counts C[i, j] = sum_rb popcount(T[rb, i] & T[rb, j]) for 64x64 tiles with J >= I,
 // stored in both halves (row stride ld).
+// Row sums of a 64 x 64 count tile (I, J) held 4 x 4 per thread (thread
+// (ty, tx) = (tid / 16, tid % 16) holds rows 4 ty.. and columns 4 tx..),
+// added to usum with integer atomics (exact in any order): rows of I get the
+// tile's row sums; for an off-diagonal tile the rows of J get its column
+// sums (the mirrored tile).  Every thread of the workgroup calls it.
+__device__ __forceinline__ void tile_row_sums(const int (&acc)[4][4], int64_t M, int64_t I, int64_t J,
+                                              int64_t* __restrict__ usum) {
+  __shared__ int colsum[64];
+  const int tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
+  if (tid < 64) colsum[tid] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    int rs = acc[q][0] + acc[q][1] + acc[q][2] + acc[q][3];
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 16);
+    const int64_t i = I * 64 + ty * 4 + q;
+    if (tx == 0 && i < M && rs != 0) atomicAdd(reinterpret_cast<unsigned long long*>(&usum[i]),
+                                                static_cast<unsigned long long>(rs));
+  }
+  if (I != J) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int cs = acc[0][r] + acc[1][r] + acc[2][r] + acc[3][r];
+      if (cs != 0) atomicAdd(&colsum[tx * 4 + r], cs);
+    }
+    __syncthreads();
+    const int64_t j = J * 64 + tid;
+    if (tid < 64 && j < M && colsum[tid] != 0)
+      atomicAdd(reinterpret_cast<unsigned long long*>(&usum[j]), static_cast<unsigned long long>(colsum[tid]));
+  }
+}
+
+// usum: NULL, or row sums to add the tile's sums to (tile_row_sums).
 __device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
-                                          int32_t* __restrict__ C, int64_t I, int64_t J) {
+                                          int32_t* __restrict__ C, int64_t I, int64_t J,
+                                          int64_t* __restrict__ usum = nullptr) {
   if (J < I) return;
   __shared__ uint64_t Ti[16][64];
   __shared__ uint64_t Tj[16][64];
@@ -178,13 +213,15 @@ __device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_
       C[j * ld + i] = acc[q][r];
     }
   }
+  if (usum) tile_row_sums(acc, M, I, J, usum);
 }
 
 // The same counts over the row words [w0, w1) only, added to C with integer
 // atomics (exact in any order; C starts at zero).  A diagonal tile adds each
 // of its entries once, an off-diagonal tile adds both halves.
 __device__ __forceinline__ void gram_part_body(const uint64_t* __restrict__ T, int64_t w0, int64_t w1, int64_t M,
-                                               int64_t ld, int32_t* __restrict__ C, int64_t I, int64_t J) {
+                                               int64_t ld, int32_t* __restrict__ C, int64_t I, int64_t J,
+                                               int64_t* __restrict__ usum) {
   __shared__ uint64_t Ti[16][64];
   __shared__ uint64_t Tj[16][64];
   const int tid = threadIdx.x;
@@ -228,6 +265,7 @@ __device__ __forceinline__ void gram_part_body(const uint64_t* __restrict__ T, i
       if (I != J) atomicAdd(&C[j * ld + i], acc[q][r]);
     }
   }
+  tile_row_sums(acc, M, I, J, usum);
 }
 
 __global__ void __launch_bounds__(256) k_gram(const uint64_t* __restrict__ T, int64_t nrb, int64_t M, int64_t ld,
@@ -291,21 +329,41 @@ __global__ void __launch_bounds__(256) k_scalars(const int32_t* __restrict__ C, 
 }
 
 // Row i of the lower triangle: counts (int32) -> G~ (fp32) in place.
+// Entry (i, j) of G~ from the integer counts: base + alpha [i = j]
+// + 2 wr (c_ij - (u_i + u_j)/M), in fp64, rounded once to fp32.  `Gb`
+// holds the per-system constants (the build kernel and the panel path's
+// loads use the same expression, so G~ has the same bits either way).
+struct GtBuild {
+  double base, alpha, wr2, inv_m;
+  bool has_random;
+};
+
+__device__ __forceinline__ GtBuild gt_build(int64_t M, bool has_random, double alpha, double wr,
+                                            const double* __restrict__ scal) {
+  const double inv_m = 1.0 / static_cast<double>(M);
+  const double sigma = scal[1], gamma = scal[2];
+  GtBuild b;
+  b.base = -alpha * inv_m + gamma * inv_m + (has_random ? 2.0 * wr * sigma * inv_m * inv_m : 0.0);
+  b.alpha = alpha;
+  b.wr2 = 2.0 * wr;
+  b.inv_m = inv_m;
+  b.has_random = has_random;
+  return b;
+}
+
+__device__ __forceinline__ float gt_entry(const GtBuild& b, int32_t cij, int64_t ui, int64_t uj, bool diag) {
+  double v = b.base + (diag ? b.alpha : 0.0);
+  if (b.has_random) v += b.wr2 * (static_cast<double>(cij) - static_cast<double>(ui + uj) * b.inv_m);
+  return static_cast<float>(v);
+}
+
 __device__ __forceinline__ void build_row(float* G, const int64_t* __restrict__ usum, int64_t M, int64_t ld,
                                           bool has_random, double alpha, double wr, const double* __restrict__ scal,
                                           int64_t i) {
-  const double Md = static_cast<double>(M);
-  const double inv_m = 1.0 / Md;
-  const double sigma = scal[1], gamma = scal[2];
-  const double base = -alpha * inv_m + gamma * inv_m + (has_random ? 2.0 * wr * sigma * inv_m * inv_m : 0.0);
-  const double wr2 = 2.0 * wr;
+  const GtBuild b = gt_build(M, has_random, alpha, wr, scal);
   for (int64_t j = threadIdx.x; j <= i; j += blockDim.x) {
-    double v = base + (i == j ? alpha : 0.0);
-    if (has_random) {
-      const double cij = static_cast<double>(reinterpret_cast<const int32_t*>(G)[i * ld + j]);
-      v += wr2 * (cij - static_cast<double>(usum[i] + usum[j]) * inv_m);
-    }
-    G[i * ld + j] = static_cast<float>(v);
+    const int32_t cij = has_random ? reinterpret_cast<const int32_t*>(G)[i * ld + j] : 0;
+    G[i * ld + j] = gt_entry(b, cij, has_random ? usum[i] : 0, has_random ? usum[j] : 0, i == j);
   }
 }
 
@@ -1375,6 +1433,8 @@ __global__ void __launch_bounds__(64) k_transpose_batch(const gnnshap::SolveJob*
   const gnnshap::SolveJob J = jobs[blockIdx.z];
   if (J.kr <= 0 || blockIdx.x >= J.nrb || blockIdx.y >= J.wpr) return;
   transpose_body(J.masks, J.wpr, J.rb0, J.kr, J.M, J.T, blockIdx.x, blockIdx.y);
+  if (blockIdx.x == 0 && blockIdx.y == 0)       // the Gram adds its row sums into usum
+    for (int64_t i = threadIdx.x; i < J.M; i += 64) J.usum[i] = 0;
   if (J.nrb <= kGramWhole) return;             // every count is stored by one workgroup
   const int64_t nblk = J.nrb * J.wpr, blk = static_cast<int64_t>(blockIdx.x) * J.wpr + blockIdx.y;
   const int64_t total = J.M * J.ld, per = (total + nblk - 1) / nblk;
@@ -1395,28 +1455,15 @@ __global__ void __launch_bounds__(256) k_gram_batch(const gnnshap::SolveJob* __r
   while ((Jt + 1) * (Jt + 2) / 2 <= tile) ++Jt;
   const int64_t It = tile - Jt * (Jt + 1) / 2;
   if (whole)
-    gram_body(J.T, J.nrb, J.M, J.ld, J.counts, It, Jt);
+    gram_body(J.T, J.nrb, J.M, J.ld, J.counts, It, Jt, J.usum);
   else
-    gram_part_body(J.T, w0, w0 + kGramChunk < J.nrb ? w0 + kGramChunk : J.nrb, J.M, J.ld, J.counts, It, Jt);
+    gram_part_body(J.T, w0, w0 + kGramChunk < J.nrb ? w0 + kGramChunk : J.nrb, J.M, J.ld, J.counts, It, Jt, J.usum);
 }
 
 __global__ void __launch_bounds__(kTileRows) k_rhs_tile_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
   if (blockIdx.x >= J.nch) return;
   rhs_tile_body(J.masks, J.wpr, J.half, J.M, J.y, J.cls, J.ncls, J.fef, J.part, blockIdx.x);
-}
-
-// Row sums of the counts and the summed right-hand side, for the mid-size jobs.
-__global__ void __launch_bounds__(256) k_rowsum_batch(const gnnshap::SolveJob* __restrict__ jobs) {
-  const gnnshap::SolveJob J = jobs[blockIdx.y];
-  if (J.kr <= 0) return;
-  const int lane = threadIdx.x & 63;
-  const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
-  if (i >= J.M) return;
-  long long s = 0;
-  for (int64_t j = lane; j < J.M; j += 64) s += J.counts[i * J.ld + j];
-  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
-  if (lane == 0) J.usum[i] = s;
 }
 
 __global__ void __launch_bounds__(256) k_rhs_sum_batch(const gnnshap::SolveJob* __restrict__ jobs) {
@@ -1435,7 +1482,7 @@ __global__ void __launch_bounds__(256) k_scalars_batch(const gnnshap::SolveJob* 
 
 __global__ void __launch_bounds__(256) k_build_batch(const gnnshap::SolveJob* __restrict__ jobs) {
   const gnnshap::SolveJob J = jobs[blockIdx.y];
-  if (blockIdx.x >= J.M) return;
+  if (blockIdx.x >= J.M || J.counts_in) return;
   build_row(reinterpret_cast<float*>(J.counts), J.usum, J.M, J.ld, J.kr > 0, J.alpha, J.wr, J.scal, blockIdx.x);
 }
 
@@ -1518,6 +1565,45 @@ __device__ __forceinline__ void pp_form_column(float* G, int64_t ld, int64_t M, 
   }
 }
 
+// pp_load for a block that still holds the integer counts (the panel path's
+// first touch of each block when G~ was not built in place): each entry is
+// built on the way (gt_entry).
+__device__ __forceinline__ void pp_load_counts(const gnnshap::SolveJob& J, int64_t bi, int64_t bj, float* S,
+                                               bool lower_only) {
+  const int tid = threadIdx.x;
+  const int64_t M = J.M;
+  const GtBuild b = gt_build(M, J.kr > 0, J.alpha, J.wr, J.scal);
+  const int32_t* C = J.counts;
+  int32_t cv[16];
+  int64_t ui[16], uj[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int t = tid + 256 * q, r = t >> 6, c = t & 63;
+    const int64_t gi = 64 * bi + r, gj = 64 * bj + c;
+    const bool ok = gi < M && gj < M && (!lower_only || c <= r);
+    cv[q] = (ok && b.has_random) ? C[gi * J.ld + gj] : 0;
+    ui[q] = (ok && b.has_random) ? J.usum[gi] : 0;
+    uj[q] = (ok && b.has_random) ? J.usum[gj] : 0;
+  }
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int t = tid + 256 * q, r = t >> 6, c = t & 63;
+    const int64_t gi = 64 * bi + r, gj = 64 * bj + c;
+    const bool ok = gi < M && gj < M && (!lower_only || c <= r);
+    S[r * kHP + c] = ok ? gt_entry(b, cv[q], ui[q], uj[q], gi == gj) : 0.f;
+  }
+}
+
+// A block of G~ as the panel path reads it: from the counts on a block's first
+// touch when the system was not built in place, else as stored.
+__device__ __forceinline__ void pp_load_g(const gnnshap::SolveJob& J, int64_t bi, int64_t bj, float* S,
+                                          bool lower_only, bool first_touch) {
+  if (first_touch && J.counts_in)
+    pp_load_counts(J, bi, bj, S, lower_only);
+  else
+    pp_load(reinterpret_cast<const float*>(J.counts), J.ld, J.M, bi, bj, S, lower_only);
+}
+
 // Start, workgroup I of the first column: I = 0 factors diagonal block 0
 // (info <- 0 first; L_00 and W_00 stored); I > 0 factors it too (not
 // reported) and forms L_I0.
@@ -1531,12 +1617,12 @@ __device__ __forceinline__ void pp_start_body(const gnnshap::SolveJob& J, int64_
   if (I >= nblk) return;
   if (I == 0) {
     if (threadIdx.x == 0) *J.info = 0;
-    pp_load(G, J.ld, M, 0, 0, D0, true);
+    pp_load_g(J, 0, 0, D0, true, true);
     pp_diag(G, J.ld, M, 0, D0, D1, J.Wd, J.info);
     return;
   }
-  pp_load(G, J.ld, M, 0, 0, D0, true);
-  pp_load(G, J.ld, M, I, 0, A, false);
+  pp_load_g(J, 0, 0, D0, true, true);
+  pp_load_g(J, I, 0, A, false, true);
   pp_factor_diag(D0, D1, M, 0, nullptr);
   pp_form_column(G, J.ld, M, I, 0, A, D1);
 }
@@ -1559,7 +1645,7 @@ __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_
   float* G = reinterpret_cast<float*>(J.counts);
   const int tid = threadIdx.x;
   const int64_t bi = p + 1 + I, bj = p + 1 + Jb;
-  pp_load(G, J.ld, M, bi, bj, A, I == Jb);
+  pp_load_g(J, bi, bj, A, I == Jb, p == 0);
   pp_load(G, J.ld, M, bi, p, X, false);
   if (I != Jb) pp_load(G, J.ld, M, bj, p, Y, false);
   __syncthreads();
@@ -1570,7 +1656,7 @@ __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_
   }
   if (Jb == 0) {
     // the next diagonal block: X <- A_{bj,bj} - L_{bj,p} L_{bj,p}^T, factored
-    pp_load(G, J.ld, M, bj, bj, X, true);
+    pp_load_g(J, bj, bj, X, true, p == 0);
     __syncthreads();
     mm64<true>(Y, Y, X, -1.f, 1.f);
     pp_factor_diag(X, Y, M, bj, nullptr);
@@ -1980,6 +2066,7 @@ int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class
   job->Wd = w.Wd;
   job->rv = w.rhs;
   job->panel = solve_panel_path(plan) ? 1 : 0;
+  job->counts_in = job->panel;          // panel systems build G~ as their blocks are first read
   job->scal = w.scal;
   return GNNSHAP_OK;
 }
@@ -2007,12 +2094,16 @@ int gnnshap::launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M,
                      256, 0, s>>>(jobs);
     }
     GS_LAUNCHED();
-    k_rowsum_batch<<<dim3(static_cast<unsigned>(ceil_div(max_M * 64, 256)), nn), 256, 0, s>>>(jobs);
-    GS_LAUNCHED();
   }
   k_scalars_batch<<<nn, 256, 0, s>>>(jobs);
   GS_LAUNCHED();
-  k_build_batch<<<dim3(static_cast<unsigned>(max_M), nn), 256, 0, s>>>(jobs);
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_solve_build(const SolveJob* jobs, int64_t n, int64_t max_M, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
+  k_build_batch<<<dim3(static_cast<unsigned>(max_M), static_cast<unsigned>(n)), 256, 0, s>>>(jobs);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }
