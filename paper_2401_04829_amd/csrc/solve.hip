@@ -175,17 +175,29 @@ __device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_
   const int tid = threadIdx.x;
   const int ty = tid / 16, tx = tid % 16;
   int acc[4][4] = {};
-  for (int64_t k0 = 0; k0 < nrb; k0 += 16) {
+  // the next stage's words are fetched while the current stage is counted
+  uint64_t ni[4], nj[4];
+  auto fetch = [&](int64_t k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int idx = tid + q * 256;
       const int kk = idx / 64, c = idx % 64;
       const int64_t i = I * 64 + c, j = J * 64 + c;
       const bool kin = k0 + kk < nrb;
-      Ti[kk][c] = (kin && i < M) ? T[(k0 + kk) * M + i] : 0;
-      Tj[kk][c] = (kin && j < M) ? T[(k0 + kk) * M + j] : 0;
+      ni[q] = (kin && i < M) ? T[(k0 + kk) * M + i] : 0;
+      nj[q] = (kin && j < M) ? T[(k0 + kk) * M + j] : 0;
+    }
+  };
+  fetch(0);
+  for (int64_t k0 = 0; k0 < nrb; k0 += 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + q * 256;
+      Ti[idx / 64][idx % 64] = ni[q];
+      Tj[idx / 64][idx % 64] = nj[q];
     }
     __syncthreads();
+    if (k0 + 16 < nrb) fetch(k0 + 16);
 #pragma unroll 4
     for (int kk = 0; kk < 16; ++kk) {
       uint64_t a[4], b[4];
@@ -227,17 +239,28 @@ __device__ __forceinline__ void gram_part_body(const uint64_t* __restrict__ T, i
   const int tid = threadIdx.x;
   const int ty = tid / 16, tx = tid % 16;
   int acc[4][4] = {};
-  for (int64_t k0 = w0; k0 < w1; k0 += 16) {
+  uint64_t ni[4], nj[4];
+  auto fetch = [&](int64_t k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int idx = tid + q * 256;
       const int kk = idx / 64, c = idx % 64;
       const int64_t i = I * 64 + c, j = J * 64 + c;
       const bool kin = k0 + kk < w1;
-      Ti[kk][c] = (kin && i < M) ? T[(k0 + kk) * M + i] : 0;
-      Tj[kk][c] = (kin && j < M) ? T[(k0 + kk) * M + j] : 0;
+      ni[q] = (kin && i < M) ? T[(k0 + kk) * M + i] : 0;
+      nj[q] = (kin && j < M) ? T[(k0 + kk) * M + j] : 0;
+    }
+  };
+  fetch(w0);
+  for (int64_t k0 = w0; k0 < w1; k0 += 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + q * 256;
+      Ti[idx / 64][idx % 64] = ni[q];
+      Tj[idx / 64][idx % 64] = nj[q];
     }
     __syncthreads();
+    if (k0 + 16 < w1) fetch(k0 + 16);
 #pragma unroll 4
     for (int kk = 0; kk < 16; ++kk) {
       uint64_t a[4], b[4];
