@@ -133,21 +133,22 @@ CANDIDATES = {
 }
 
 
-def roofline(step, lib, dims, mode):
-    """Times each candidate kernel with HIP events over one step, picks the
-    one with the largest total and relates its algorithmic work to its
-    average launch duration."""
+def roofline(run, lib, dims, mode, steps=10):
+    """Times each candidate kernel with HIP events over `steps` steps run as in
+    the timed region, picks the one with the largest total and relates its
+    algorithmic work to its average launch duration."""
     import torch
     best = None
     for name in CANDIDATES[mode]:
         lib.gnnshap_timing_begin(name)
-        _, res = step()
+        res = run(steps)
         torch.cuda.synchronize()
         ms, n = lib.gnnshap_timing_end()
         if n and (best is None or ms > best[1]):
             best = (name, ms, n, res)
     name, ms, n, res = best
     amount, unit, bound, peak = work_model(name, res, dims)
+    amount *= steps
     avg_s = ms / 1e3 / n
     per_launch = amount / n
     scale = 1e9 if unit == "GB/s" else 1e12
@@ -211,18 +212,23 @@ def main():
 
     def run(steps):
         """`steps` steps; in batch mode pipelined, each batch's extraction queued
-        before the previous batch's explanation.  Returns the coalitions done."""
+        before the previous batch's explanation.  Returns (coalitions done, the
+        last step's results)."""
+        total, last = 0, None
         if args.mode == "batch":
-            total = 0
             for res in ex.explain_batches(itertools.repeat(targets, steps), cfg["p"], cfg["seed"], prepare_each=True):
                 total += res.total_rows
-            return total
-        return sum(step()[0] for _ in range(steps))
+                last = res
+            return total, last
+        for _ in range(steps):
+            k, last = step()
+            total += k
+        return total, last
 
     run(args.warmup)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    total_k = run(args.steps)
+    total_k, _ = run(args.steps)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_per_step = 1e3 * dt / args.steps
@@ -260,7 +266,7 @@ def main():
     }
     if not args.no_roofline:
         from paper_2401_04829_amd import _lib
-        out["roofline"] = roofline(step, _lib, cfg["dims"], args.mode)
+        out["roofline"] = roofline(lambda n: run(n)[1], _lib, cfg["dims"], args.mode)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out))
