@@ -235,7 +235,15 @@ int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes);
  * (all [dev]).  `classes` as for gnnshap_sample_coalitions.  *info ([dev]
  * int32) receives 0, or j > 0 if the j-th pivot (1-based) of the Cholesky
  * factorisation was not positive (phi is then not meaningful; this happens
- * when the sampled rows do not determine phi). */
+ * when the sampled rows do not determine phi).
+ * Systems of more than gnnshap_set_iterative_threshold() players (default
+ * 5000) are not factored: conjugate gradients run on the projected normal
+ * equations, applying the masks and their transpose straight from the bits
+ * (Sec. 3.5 fits large systems iteratively), until the residual falls to
+ * 1e-8 of its initial norm; *info is then 0, or M + 1 if that did not happen
+ * within 4000 iterations or the iteration broke down.  That path waits on
+ * `stream` for its stopping test (the call returns once the iteration has
+ * stopped; the write of phi is still queued). */
 int gnnshap_solve_wls(const gnnshap_sample_plan* plan,
                       const gnnshap_class* classes, const uint64_t* masks,
                       const float* y, const float* f_empty_full, float* phi,
@@ -337,8 +345,16 @@ int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan
 
 /* Which solver the plan's system takes: *path = 1 if one workgroup factors
  * and solves it (M <= 192), 2 if it is factored panel by panel by small
- * workgroups (192 < M <= 448), 0 if it takes the multi-block Cholesky. */
+ * workgroups (192 < M <= 448), 0 if it takes the multi-block Cholesky, 3 if
+ * it is solved iteratively (M above the iterative threshold). */
 int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path);
+
+/* Sets the process-wide number of players above which systems are solved
+ * iteratively (Sec. 3.5 switches at 5000, the default) instead of being
+ * factored; also for gnnshap_explain_batch, where such targets take the
+ * single-target solver.  Set it before querying workspace sizes: the
+ * iterative path needs a different workspace.  EINVAL if below 1. */
+int gnnshap_set_iterative_threshold(int64_t num_players);
 
 /* Arms timing for the kernels whose name starts with `kernel_name` (e.g.
  * "k_solve_mid", "k_eval_l2"): every later launch of such a kernel, from

@@ -81,6 +81,7 @@ _SIGNATURES = {
                                              c_i64, _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                              c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_solve_info": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(c_i32)]),
+    "gnnshap_set_iterative_threshold": (ctypes.c_int, [c_i64]),
     "gnnshap_timing_begin": (ctypes.c_int, [ctypes.c_char_p]),
     "gnnshap_timing_end": (ctypes.c_int, [_P(ctypes.c_double), _P(c_i64)]),
 }
@@ -268,7 +269,12 @@ def gnnshap_explain_batch(sgs, plans, classes, model, X_ptr, target_class, masks
 
 
 def gnnshap_solve_info(plan):
-    """Solver path of the plan's system: 1 one workgroup, 2 the panel path, 0 multi-block."""
+    """Solver path of the plan's system: 1 one workgroup, 2 the panel path, 0 multi-block, 3 iterative."""
     v = c_i32()
     check(load().gnnshap_solve_info(ctypes.byref(plan), ctypes.byref(v)), "solve_info")
     return v.value
+
+
+def gnnshap_set_iterative_threshold(num_players):
+    """Players above which systems are solved iteratively (process-wide; default 5000)."""
+    check(load().gnnshap_set_iterative_threshold(int(num_players)), "set_iterative_threshold")

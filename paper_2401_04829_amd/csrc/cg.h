@@ -1,0 +1,76 @@
+// Matrix-free solver of the projected Kernel-SHAP normal equations (Sec. 3.5:
+// large systems are fitted iteratively instead of being factored).
+#pragma once
+
+#include "common.h"
+
+namespace gnnshap {
+
+// Device state of one iterative solve.
+struct CgState {
+  double rr0;      // squared norm of the initial residual
+  int32_t done;    // set by the iteration that stops
+  int32_t iters;   // iterations run
+  int32_t status;  // 0 converged, 1 iteration limit, 2 lost positive curvature
+  int32_t pad;
+};
+
+// Buffers of the iterative solver, carved from the solve workspace.
+struct CgWs {
+  double* x;       // M: psi
+  double* r;       // words_per_row * 64: residual, zero beyond M
+  double* p;       // M: search direction
+  double* s;       // M: A p
+  double* upart;   // npc x kr: partial products R r per player chunk
+  double* u;       // nrb * 64: R r, zero beyond kr
+  double* qpart;   // nrc x M: partial products R^T u per row chunk
+  double* uu;      // nbu x 2: partial |u|^2 and |m|.u
+  double* rr;      // 3 x nbc: partial r.r of iterations t mod 3
+  double* hist;    // 2: step lengths of even and odd iterations
+  int32_t* sz;     // kr: sizes of the random representative rows
+  uint64_t* blocked;  // nrb x words_per_row x 64: the random rows in row blocks
+  CgState* st;
+};
+
+// Launch shape of the iterative solver for M players and kr random
+// representative rows (words_per_row mask words per row).
+struct CgShape {
+  int64_t M, wpr, kr, nrb;
+  int64_t npc, pwords;  // product R r: player chunks of pwords words
+  int64_t nrc, rbc;     // product R^T u: row chunks of rbc row blocks
+  int64_t nbu, nbc;     // workgroups of the row and player passes
+};
+CgShape cg_shape(int64_t M, int64_t wpr, int64_t kr);
+CgWs cg_carve(Carver& c, const CgShape& sh);
+
+// The problem handed over by the solve entry point: the bit-transposed random
+// rows T (nrb x M), the same rows in row blocks (word w of the 64 rows of
+// block rb contiguous, rows beyond kr zero),
+// the summed right-hand side dv (M, before centring) with its per-block sums
+// bsum (nb of them), the class table (device) and the enumerated part alpha.
+struct CgProblem {
+  const uint64_t* T;
+  const uint64_t* blocked;
+  const double* dv;
+  const double* bsum;
+  int64_t nb;
+  const gnnshap_class* classes;
+  int64_t ncls;
+  int64_t rb0;          // first random representative row
+  double alpha;         // enumerated classes: their projected Gram is alpha P
+  double wr;            // weight of every random row
+  const float* fef;     // f(empty), f(full)
+  float* phi;
+  int32_t* info;
+};
+
+// Conjugate gradients on 1-perp; returns once the iteration has stopped
+// (the host waits on the stream for the stopping test) and phi/info are
+// queued on `s`.  *iters_out (may be null) receives the iterations run.
+int cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out);
+
+// Largest number of players solved by factorisation; larger systems are
+// solved iteratively.  Process-wide, default 5000 (Sec. 3.5).
+int64_t iterative_threshold();
+
+}  // namespace gnnshap

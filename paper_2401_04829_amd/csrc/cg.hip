@@ -1,0 +1,529 @@
+// Matrix-free conjugate gradients for the projected Kernel-SHAP normal
+// equations (Sec. 3.5 of the GNNShap paper: above 5000 players the regression
+// is fitted iteratively rather than by a direct solve).
+//
+// Unknown psi in 1-perp, phi = Delta/M + psi.  With R the random
+// representative rows (each stands for itself and its complement) and P the
+// centring projector, the operator on 1-perp is
+//     A v = alpha v + 2 w_r P R^T (R v),
+// alpha collecting the enumerated classes (their projected Gram is a multiple
+// of P).  No Gram matrix is formed: every iteration applies R and R^T to the
+// residual straight from the packed bits.
+//
+// The recurrences are those of Chronopoulos and Gear's conjugate gradients
+// (SIAM J. Sci. Stat. Comput. 1989), which apply A to the residual r and
+// carry s = A p along: with w = A r, gamma = r.r and delta = r.w,
+//     beta = gamma / gamma_prev, a = gamma / (delta - beta gamma / a_prev),
+//     p = r + beta p, s = w + beta s, x += a p, r -= a s.
+// Every vector a pass reads was finished by an earlier kernel.  Each
+// workgroup turns its slice of that vector into nibble tables in LDS (sums of
+// the vector over every subset of 4 consecutive entries); each lane then
+// loads its own mask word with ordinary vector loads and adds one table entry
+// per 4 bits (a bit extract, an address and an fp64 add per nibble, instead
+// of a multiply-add per bit).  delta needs no extra reduction:
+// r.A r = alpha |r|^2 + 2 w_r |R r|^2 for r in 1-perp.
+//
+// Per iteration t:
+//   pass A   stopping test on gamma_t; partial products R r over player chunks
+//            (lane = row, the rows' words in row blocks);
+//   rows     u = R r summed over the chunks, partial |u|^2 and |m|.u;
+//   pass B   partial products R^T u over row chunks (lane = player, words of
+//            the bit-transposed rows);
+//   update   w = alpha r + 2 w_r (R^T u - mean), the scalars, the vector steps
+//            and the partial sums of the new gamma.
+// Vectors and every sum are fp64; partial sums are reduced in a fixed order,
+// so repeated solves give the same bits.  The iteration stops when
+// |r| <= kTol |r_0| or after kMaxIt iterations; the host queues iterations in
+// chunks and checks a flag the device writes to mapped host memory, so at
+// most one chunk runs idle.
+#include <algorithm>
+#include <atomic>
+
+#include "cg.h"
+
+namespace {
+
+constexpr double kTol = 1e-8;
+constexpr int64_t kMaxIt = 4000;
+constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
+constexpr int kWaves = 8;            // waves per workgroup of both passes
+constexpr int64_t kTabWords = 31;    // nibble tables per workgroup: 31 words (62 KiB of LDS)
+
+struct Args {
+  const int32_t* sz;
+  int64_t M, wpr, kr, nrb, npc, pwords, nrc, rbc, nbu, nbc;
+  double alpha, wr2, tol2;
+  int64_t maxit;
+  int32_t has_random;
+  double* x;
+  double* r;       // wpr * 64 (zero beyond M)
+  double* p;
+  double* s;
+  double* upart;
+  double* u;       // nrb * 64 (zero beyond kr)
+  double* qpart;
+  double* uu;
+  double* rr;      // 3 x nbc
+  double* hist;    // step length of even and odd iterations
+  gnnshap::CgState* st;
+  int32_t* host_flag;  // mapped host memory: [0] done, [1] iterations
+};
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Sum of a block's values v over its threads (blockDim.x a multiple of 64,
+// at most 1024); the result is returned to every thread.
+__device__ __forceinline__ double block_sum_d(double v, double* red) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum_d(v);
+  __syncthreads();
+  if (lane == 0) red[wv] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int i = 0; i < nw; ++i) s += red[i];
+  return s;
+}
+
+// Sum of n values by one whole wave in a fixed order: lane l adds entries
+// l, l + 64, ..., then a fixed butterfly; every wave gets the same bits.
+__device__ __forceinline__ double wave_fixed_sum(const double* __restrict__ a, int64_t n, int64_t stride = 1) {
+  double s = 0.0;
+  for (int64_t i = threadIdx.x & 63; i < n; i += 64) s += a[i * stride];
+  return wave_sum_d(s);
+}
+
+// Nibble tables: for 64 consecutive entries v[0..63] of a vector, table k
+// (k = 0..15) holds at index n the sum of v[4k + i] over the set bits i of n,
+// so that the sum of v over the set bits of a 64-bit word is the sum of 16
+// table reads.  One table is 16 fp64 entries, 128 bytes: its entries fall in
+// distinct LDS banks, so 64 lanes reading one table never conflict.
+__device__ __forceinline__ void build_nibble_table(const double* __restrict__ v4, double* tab) {
+  const double v0 = v4[0], v1 = v4[1], v2 = v4[2], v3 = v4[3];
+  const double v01 = v0 + v1;
+  double e[8] = {0.0, v0, v1, v01, v2, v0 + v2, v1 + v2, v01 + v2};
+#pragma unroll
+  for (int n = 0; n < 8; ++n) {
+    tab[n] = e[n];
+    tab[8 + n] = e[n] + v3;
+  }
+}
+
+// acc[0..3] += sum over the set bits b of word of v[b], from the word's 16
+// nibble tables at tab (256 entries).
+__device__ __forceinline__ void nibble_dot(uint64_t word, const double* tab, double (&acc)[4]) {
+  const uint32_t lo = static_cast<uint32_t>(word), hi = static_cast<uint32_t>(word >> 32);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k & 3] += tab[k * 16 + ((lo >> (4 * k)) & 15)];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k & 3] += tab[(8 + k) * 16 + ((hi >> (4 * k)) & 15)];
+}
+
+// r = dv - mean(dv) (zero beyond M), x = p = s = 0, partial gamma_0; u zero
+// beyond kr; sizes of the random rows.  Grid: nbc workgroups of 256.
+__global__ void __launch_bounds__(256) k_cg_init(Args a, const double* __restrict__ dv,
+                                                 const double* __restrict__ bsum, int64_t nb,
+                                                 const gnnshap_class* __restrict__ cls, int64_t ncls, int64_t rb0,
+                                                 int32_t* sz) {
+  __shared__ double red[4];
+  __shared__ double mean;
+  if (threadIdx.x == 0) {
+    double sm = 0.0;
+    for (int64_t i = 0; i < nb; ++i) sm += bsum[i];
+    mean = sm / static_cast<double>(a.M);
+  }
+  __syncthreads();
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  double r2 = 0.0;
+  if (j < a.wpr * 64) {
+    const double rj = j < a.M ? dv[j] - mean : 0.0;
+    a.r[j] = rj;
+    r2 = rj * rj;
+    if (j < a.M) {
+      a.x[j] = 0.0;
+      a.p[j] = 0.0;
+      a.s[j] = 0.0;
+    }
+  }
+  const double sb = block_sum_d(r2, red);
+  if (threadIdx.x == 0) a.rr[blockIdx.x] = sb;   // gamma_0: slot 0
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    a.st->done = 0;
+    a.st->iters = 0;
+    a.st->status = 0;
+  }
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int64_t b = a.kr + j; b < a.nrb * 64; b += stride) a.u[b] = 0.0;
+  // row sizes: class of row rb0 + b by binary search over row_begin
+  for (int64_t b = j; b < a.kr; b += stride) {
+    const int64_t row = rb0 + b;
+    int64_t lo = 0, hi = ncls - 1;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (cls[mid].row_begin <= row) lo = mid; else hi = mid - 1;
+    }
+    sz[b] = cls[lo].size;
+  }
+}
+
+// Stopping test of iteration t, taken identically by every wave of pass A
+// from the partial sums of gamma_t; `writer` records the stop.
+__device__ __forceinline__ bool cg_stop(const Args& a, int64_t t, bool writer) {
+  const double g = wave_fixed_sum(a.rr + (t % 3) * a.nbc, a.nbc);
+  const double g0 = t == 0 ? g : a.st->rr0;
+  const bool bad = !(g == g) || g > 1e300;
+  const bool conv = !bad && g <= a.tol2 * g0;
+  if (conv || bad || t >= a.maxit) {
+    if (writer) {
+      a.st->done = 1;
+      a.st->iters = static_cast<int32_t>(t);
+      a.st->status = conv ? 0 : (bad ? 2 : 1);
+      __hip_atomic_store(a.host_flag + 1, static_cast<int32_t>(t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(a.host_flag, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    return true;
+  }
+  if (t == 0 && writer) a.st->rr0 = g;
+  return false;
+}
+
+// Pass A: upart[pc, b] = sum over the words of player chunk pc of the bits of
+// row b times r.  The workgroup builds the chunk's nibble tables of r in LDS
+// (r is padded with zeros to whole words); then one wave per 64 rows
+// (lane = row) reads the row-blocked words, 512 contiguous bytes per word,
+// and sums table entries.
+__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_t* __restrict__ blocked,
+                                                          const double* __restrict__ r,
+                                                          double* __restrict__ upart, int64_t t) {
+  extern __shared__ double tab[];   // pwords * 256
+  if (a.st->done) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t rb = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool writer = blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0;
+  if (cg_stop(a, t, writer)) return;   // the same outcome in every wave
+  const int64_t pc = blockIdx.y;
+  const int64_t w0 = pc * a.pwords;
+  const int64_t w1 = w0 + a.pwords < a.wpr ? w0 + a.pwords : a.wpr;
+  const int64_t nw = w1 - w0;
+  for (int64_t q = threadIdx.x; q < nw * 16; q += kWaves * 64) build_nibble_table(r + w0 * 64 + q * 4, tab + q * 16);
+  __syncthreads();
+  if (rb >= a.nrb) return;
+  const uint64_t* src = blocked + (rb * a.wpr + w0) * 64 + lane;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  uint64_t next = src[0];
+  for (int64_t w = 0; w < nw; ++w) {
+    const uint64_t word = next;
+    if (w + 1 < nw) next = src[(w + 1) * 64];
+    nibble_dot(word, tab + w * 256, acc);
+  }
+  const int64_t row = rb * 64 + lane;
+  if (row < a.kr) upart[pc * a.kr + row] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
+// u = R r (sum over the player chunks in order), with partial |u|^2 and |m|.u.
+__global__ void __launch_bounds__(256) k_cg_rows(Args a) {
+  __shared__ double red[4];
+  if (a.st->done) return;
+  const int64_t b = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  double uu = 0.0, su = 0.0;
+  if (b < a.kr) {
+    double v = 0.0;
+    for (int64_t c = 0; c < a.npc; ++c) v += a.upart[c * a.kr + b];
+    a.u[b] = v;
+    uu = v * v;
+    su = static_cast<double>(a.sz[b]) * v;
+  }
+  const double s1 = block_sum_d(uu, red);
+  const double s2 = block_sum_d(su, red);
+  if (threadIdx.x == 0) {
+    a.uu[2 * blockIdx.x] = s1;
+    a.uu[2 * blockIdx.x + 1] = s2;
+  }
+}
+
+// Pass B: qpart[c, j] = sum over the row blocks of chunk c of the bits of
+// player j times u.  The workgroup builds the chunk's nibble tables of u in
+// LDS (u is padded with zeros to whole row blocks); then one wave per 64
+// players (lane = player) reads the bit-transposed words T[rb, j] and sums
+// table entries.
+__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_t* __restrict__ T,
+                                                          const double* __restrict__ u,
+                                                          double* __restrict__ qpart) {
+  extern __shared__ double tab[];   // rbc * 256
+  if (a.st->done) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t c = blockIdx.y;
+  const int64_t b0 = c * a.rbc;
+  const int64_t b1 = b0 + a.rbc < a.nrb ? b0 + a.rbc : a.nrb;
+  const int64_t nb = b1 - b0;
+  for (int64_t q = threadIdx.x; q < nb * 16; q += kWaves * 64) build_nibble_table(u + b0 * 64 + q * 4, tab + q * 16);
+  __syncthreads();
+  if (g >= a.wpr) return;
+  const int64_t j = g * 64 + lane;
+  const bool valid = j < a.M;
+  const uint64_t* col = T + (valid ? j : 0);
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  uint64_t next = valid ? col[b0 * a.M] : 0;
+  for (int64_t rb = 0; rb < nb; ++rb) {
+    const uint64_t word = next;
+    if (rb + 1 < nb) next = valid ? col[(b0 + rb + 1) * a.M] : 0;
+    nibble_dot(word, tab + rb * 256, acc);
+  }
+  if (valid) qpart[c * a.M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
+// Update of iteration t (see the recurrences above); partial gamma_{t+1}.
+__global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
+  __shared__ double red[4];
+  __shared__ double coef[3];
+  if (a.st->done) return;
+  if (threadIdx.x < 64) {
+    const double g = wave_fixed_sum(a.rr + (t % 3) * a.nbc, a.nbc);
+    const double uu = a.has_random ? wave_fixed_sum(a.uu, a.nbu, 2) : 0.0;
+    const double su = a.has_random ? wave_fixed_sum(a.uu + 1, a.nbu, 2) : 0.0;
+    const double delta = a.alpha * g + a.wr2 * uu;
+    double beta = 0.0, den = delta;
+    if (t > 0) {
+      const double gp = wave_fixed_sum(a.rr + ((t + 2) % 3) * a.nbc, a.nbc);
+      beta = g / gp;
+      den = delta - beta * g / a.hist[(t + 1) & 1];
+    }
+    const double step = g / den;
+    if (threadIdx.x == 0) {
+      const bool ok = den > 0.0 && step == step && step < 1e300 && beta == beta;
+      coef[0] = ok ? step : -1.0;
+      coef[1] = beta;
+      coef[2] = su / static_cast<double>(a.M);
+      if (ok && blockIdx.x == 0) a.hist[t & 1] = step;
+    }
+  }
+  __syncthreads();
+  const double step = coef[0], beta = coef[1], mq = coef[2];
+  if (step < 0.0) {   // identical in every workgroup
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      a.st->done = 1;
+      a.st->iters = static_cast<int32_t>(t);
+      a.st->status = 2;
+      __hip_atomic_store(a.host_flag + 1, static_cast<int32_t>(t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(a.host_flag, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    return;
+  }
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  double r2 = 0.0;
+  if (j < a.M) {
+    double q = 0.0;
+    if (a.has_random)
+      for (int64_t c = 0; c < a.nrc; ++c) q += a.qpart[c * a.M + j];
+    const double rj = a.r[j];
+    const double wj = a.alpha * rj + a.wr2 * (q - mq);
+    const double pj = rj + beta * a.p[j];
+    const double sj = wj + beta * a.s[j];
+    a.p[j] = pj;
+    a.s[j] = sj;
+    a.x[j] += step * pj;
+    const double rn = rj - step * sj;
+    a.r[j] = rn;
+    r2 = rn * rn;
+  }
+  const double sb = block_sum_d(r2, red);
+  if (threadIdx.x == 0) a.rr[((t + 1) % 3) * a.nbc + blockIdx.x] = sb;
+}
+
+// phi = Delta/M + x - mean(x) (the projection made exact), info from the state.
+__global__ void __launch_bounds__(1024) k_cg_finish(const double* __restrict__ x, int64_t M,
+                                                    const gnnshap::CgState* __restrict__ st,
+                                                    const float* __restrict__ fef, float* __restrict__ phi,
+                                                    int32_t* info) {
+  __shared__ double red[16];
+  double sm = 0.0;
+  for (int64_t j = threadIdx.x; j < M; j += 1024) sm += x[j];
+  const double mean = block_sum_d(sm, red) / static_cast<double>(M);
+  const double base = (static_cast<double>(fef[1]) - static_cast<double>(fef[0])) / static_cast<double>(M);
+  for (int64_t j = threadIdx.x; j < M; j += 1024) phi[j] = static_cast<float>(base + (x[j] - mean));
+  if (threadIdx.x == 0) *info = st->status == 0 ? 0 : static_cast<int32_t>(M + 1);
+}
+
+// Mapped page-locked stopping flag of the calling thread and its device address.
+struct HostFlag {
+  int32_t* host = nullptr;
+  int32_t* dev = nullptr;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+};
+
+HostFlag* host_flag() {
+  static thread_local HostFlag f;
+  if (!f.host) {
+    void* h = nullptr;
+    if (hipHostMalloc(&h, 256, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, h, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipHostFree(h);
+      return nullptr;
+    }
+    for (int i = 0; i < 2; ++i)
+      if (hipEventCreateWithFlags(&f.ev[i], hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+      }
+    f.host = static_cast<int32_t*>(h);
+    f.dev = static_cast<int32_t*>(d);
+  }
+  return &f;
+}
+
+std::atomic<int64_t> g_threshold{5000};
+
+}  // namespace
+
+int64_t gnnshap::iterative_threshold() { return g_threshold.load(std::memory_order_relaxed); }
+
+extern "C" int gnnshap_set_iterative_threshold(int64_t num_players) {
+  gnnshap::clear_error();
+  if (num_players < 1) return gnnshap::fail(GNNSHAP_EINVAL, "threshold must be at least 1");
+  g_threshold.store(num_players, std::memory_order_relaxed);
+  return GNNSHAP_OK;
+}
+
+gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr) {
+  CgShape s{};
+  s.M = M;
+  s.wpr = wpr;
+  s.kr = kr;
+  s.nrb = ceil_div(kr, 64);
+  const int64_t nrb = s.nrb > 0 ? s.nrb : 1;
+  // pass A: about 4096 waves (row blocks x player chunks of whole words), at
+  // most kTabWords words of tables per workgroup
+  const int64_t npc = std::max<int64_t>(ceil_div(wpr, kTabWords), std::min(ceil_div(4096, nrb), wpr));
+  s.pwords = ceil_div(wpr, npc);
+  s.npc = ceil_div(wpr, s.pwords);
+  // pass B: about 4096 waves (player words x chunks of whole row blocks), at
+  // most kTabWords row blocks of tables per workgroup
+  const int64_t nrc = std::max<int64_t>(ceil_div(nrb, kTabWords), std::min(ceil_div(4096, wpr), nrb));
+  s.rbc = ceil_div(nrb, nrc);
+  s.nrc = ceil_div(nrb, s.rbc);
+  s.nbu = ceil_div(kr > 0 ? kr : 1, 256);
+  s.nbc = ceil_div(wpr * 64, 256);
+  return s;
+}
+
+gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
+  CgWs w;
+  const int64_t kr = sh.kr > 0 ? sh.kr : 1;
+  w.x = c.take<double>(sh.M);
+  w.r = c.take<double>(sh.wpr * 64);
+  w.p = c.take<double>(sh.M);
+  w.s = c.take<double>(sh.M);
+  w.upart = c.take<double>(sh.npc * kr);
+  w.u = c.take<double>((sh.nrb > 0 ? sh.nrb : 1) * 64);
+  w.qpart = c.take<double>(sh.nrc * sh.M);
+  w.uu = c.take<double>(2 * sh.nbu);
+  w.rr = c.take<double>(3 * sh.nbc);
+  w.hist = c.take<double>(2);
+  w.sz = c.take<int32_t>(kr);
+  w.blocked = c.take<uint64_t>((sh.nrb > 0 ? sh.nrb : 1) * sh.wpr * 64);
+  w.st = c.take<CgState>(1);
+  return w;
+}
+
+int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out) {
+  HostFlag* hf = host_flag();
+  if (!hf) return fail(GNNSHAP_EHIP, "could not allocate the solver's host flag");
+  Args a{};
+  a.sz = w.sz;
+  a.M = sh.M;
+  a.wpr = sh.wpr;
+  a.kr = sh.kr;
+  a.nrb = sh.nrb;
+  a.npc = sh.npc;
+  a.pwords = sh.pwords;
+  a.nrc = sh.nrc;
+  a.rbc = sh.rbc;
+  a.nbu = sh.nbu;
+  a.nbc = sh.nbc;
+  a.alpha = pr.alpha;
+  a.wr2 = sh.kr > 0 ? 2.0 * pr.wr : 0.0;
+  a.tol2 = kTol * kTol;
+  a.maxit = kMaxIt;
+  a.has_random = sh.kr > 0 ? 1 : 0;
+  a.x = w.x;
+  a.r = w.r;
+  a.p = w.p;
+  a.s = w.s;
+  a.upart = w.upart;
+  a.u = w.u;
+  a.qpart = w.qpart;
+  a.uu = w.uu;
+  a.rr = w.rr;
+  a.hist = w.hist;
+  a.st = w.st;
+  a.host_flag = hf->dev;
+  // no kernel of an earlier solve of this thread writes the flag any more:
+  // each solve returns only after its stopping iteration has run
+  __atomic_store_n(hf->host, 0, __ATOMIC_RELEASE);
+  __atomic_store_n(hf->host + 1, -1, __ATOMIC_RELEASE);
+  {
+    GS_TIMED("k_cg_init", s);
+    k_cg_init<<<static_cast<unsigned>(sh.nbc), 256, 0, s>>>(a, pr.dv, pr.bsum, pr.nb, pr.classes, pr.ncls, pr.rb0,
+                                                            w.sz);
+  }
+  GS_LAUNCHED();
+  const bool random = sh.kr > 0;
+  const dim3 ga(static_cast<unsigned>(ceil_div(std::max<int64_t>(sh.nrb, 1), kWaves)),
+                static_cast<unsigned>(sh.npc));
+  const dim3 gb(static_cast<unsigned>(ceil_div(sh.wpr, kWaves)), static_cast<unsigned>(sh.nrc));
+  // Iterations 0 .. kMaxIt - 1 in full; pass A alone of iteration kMaxIt
+  // (it always stops).  The host waits for chunk c - 1 after queueing chunk c.
+  int64_t t = 0, chunk = 0;
+  bool stopped = false;
+  while (t <= kMaxIt && !stopped) {
+    const int64_t t_end = std::min(t + kChunk, kMaxIt + 1);
+    for (; t < t_end; ++t) {
+      {
+        GS_TIMED("k_cg_pass_a", s);
+        k_cg_pass_a<<<ga, kWaves * 64, sh.pwords * 256 * sizeof(double), s>>>(a, pr.blocked, w.r, w.upart, t);
+      }
+      GS_LAUNCHED();
+      if (t == kMaxIt) continue;
+      if (random) {
+        {
+          GS_TIMED("k_cg_rows", s);
+          k_cg_rows<<<static_cast<unsigned>(sh.nbu), 256, 0, s>>>(a);
+        }
+        GS_LAUNCHED();
+        {
+          GS_TIMED("k_cg_pass_b", s);
+          k_cg_pass_b<<<gb, kWaves * 64, sh.rbc * 256 * sizeof(double), s>>>(a, pr.T, w.u, w.qpart);
+        }
+        GS_LAUNCHED();
+      }
+      {
+        GS_TIMED("k_cg_update", s);
+        k_cg_update<<<static_cast<unsigned>(sh.nbc), 256, 0, s>>>(a, t);
+      }
+      GS_LAUNCHED();
+    }
+    GS_HIP(hipEventRecord(hf->ev[chunk & 1], s));
+    if (chunk > 0) {
+      GS_HIP(hipEventSynchronize(hf->ev[(chunk - 1) & 1]));
+      stopped = __atomic_load_n(hf->host, __ATOMIC_ACQUIRE) != 0;
+    }
+    ++chunk;
+  }
+  if (!stopped) GS_HIP(hipEventSynchronize(hf->ev[(chunk - 1) & 1]));
+  if (iters_out) *iters_out = __atomic_load_n(hf->host + 1, __ATOMIC_ACQUIRE);
+  {
+    GS_TIMED("k_cg_finish", s);
+    k_cg_finish<<<1, 1024, 0, s>>>(w.x, sh.M, w.st, pr.fef, pr.phi, pr.info);
+  }
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}

@@ -26,6 +26,7 @@
 #include <cmath>
 
 #include "batch.h"
+#include "cg.h"
 #include "common.h"
 
 namespace {
@@ -54,7 +55,15 @@ struct Ws {
   float* x;          // M
   float* Winv;       // kPB x kPB inverse of the current diagonal factor
   float* Wd;         // one-workgroup mid-size path: ceil(M/64) inverse diagonal factors (64 x 64)
+  gnnshap::CgWs cg;  // iterative path only (no G, Winv, Wd)
 };
+
+// Systems above the process-wide threshold are solved iteratively (Sec. 3.5).
+bool iterative(const gnnshap_sample_plan* p) { return p->num_players > gnnshap::iterative_threshold(); }
+
+gnnshap::CgShape cg_shape_of(const gnnshap_sample_plan* p) {
+  return gnnshap::cg_shape(p->num_players, p->words_per_row, p->num_rows / 2 - p->random_begin);
+}
 
 // Row stride of G: a multiple of 64 floats keeps every row 256-byte aligned.
 int64_t ld_of(int64_t M) { return gnnshap::ceil_div(M, 64) * 64; }
@@ -84,6 +93,19 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
   const int64_t nrb = gnnshap::ceil_div(kr, 64);
   w.classes = c.take<gnnshap_class>(p->num_classes > 0 ? p->num_classes : 1);
   w.T = c.take<uint64_t>((nrb > 0 ? nrb : 1) * M);
+  if (iterative(p)) {
+    w.G = nullptr;
+    w.usum = nullptr;
+    w.scal = nullptr;
+    w.dz = c.take<double>(half);
+    w.part = c.take<double>(n_chunks(half, p->words_per_row) * M);
+    w.dv = c.take<double>(M);
+    w.bsum = c.take<double>(gnnshap::ceil_div(M, 256));
+    w.rhs = w.x = w.Winv = w.Wd = nullptr;
+    w.cg = gnnshap::cg_carve(c, cg_shape_of(p));
+    return w;
+  }
+  w.cg = gnnshap::CgWs{};
   w.G = c.take<float>(M * ld_of(M));
   w.usum = c.take<int64_t>(M);
   w.scal = c.take<double>(16);
@@ -128,6 +150,18 @@ __device__ __forceinline__ void transpose_body(const uint64_t* __restrict__ mask
 __global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ masks, int64_t wpr, int64_t row0,
                                                   int64_t nrows, int64_t M, uint64_t* __restrict__ T) {
   transpose_body(masks, wpr, row0, nrows, M, T, blockIdx.x, blockIdx.y);
+}
+
+// T as above, and the same words in row blocks: B[(rb * wpr + w) * 64 + b] =
+// word w of row rb * 64 + b (zero beyond nrows), so that a wave reading word
+// w of 64 consecutive rows reads 512 contiguous bytes.
+__global__ void __launch_bounds__(64) k_transpose_blocked(const uint64_t* __restrict__ masks, int64_t wpr,
+                                                          int64_t row0, int64_t nrows, int64_t M,
+                                                          uint64_t* __restrict__ T, uint64_t* __restrict__ B) {
+  const int64_t rb = blockIdx.x, w = blockIdx.y;
+  const int64_t r = rb * 64 + threadIdx.x;
+  B[(rb * wpr + w) * 64 + threadIdx.x] = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
+  transpose_body(masks, wpr, row0, nrows, M, T, rb, w);
 }
 
 // Counts C[i, j] = sum_rb popcount(T[rb, i] & T[rb, j]) for 64x64 tiles with J >= I,
@@ -1877,6 +1911,45 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     alpha += classes[i].weight * kappa * binom_d(M - 2, c - 1);
   }
   GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class), hipMemcpyHostToDevice, s));
+  if (iterative(plan)) {
+    // R as bit-transposed rows (the product R p), the right-hand side, then
+    // conjugate gradients straight from the bits
+    if (has_random) {
+      GS_TIMED("k_transpose", s);
+      k_transpose_blocked<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(kr, 64)), static_cast<unsigned>(wpr)), 64, 0,
+                            s>>>(masks, wpr, rb0, kr, M, w.T, w.cg.blocked);
+    }
+    GS_LAUNCHED();
+    const int64_t nch = n_chunks(half, wpr);
+    const int64_t rpc = gnnshap::ceil_div(half, nch);
+    k_dz<<<static_cast<unsigned>(gnnshap::ceil_div(half, 256)), 256, 0, s>>>(y, half, M, w.classes, plan->num_classes,
+                                                                             f_empty_full, w.dz);
+    GS_LAUNCHED();
+    {
+      GS_TIMED("k_rhs_part", s);
+      k_rhs_part<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(wpr, 4)), static_cast<unsigned>(nch)), 256, 0, s>>>(
+          masks, wpr, half, M, w.dz, rpc, w.part);
+    }
+    GS_LAUNCHED();
+    const int64_t nbm = gnnshap::ceil_div(M, 256);
+    k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch, M, w.dv, w.bsum);
+    GS_LAUNCHED();
+    gnnshap::CgProblem pr{};
+    pr.T = w.T;
+    pr.blocked = w.cg.blocked;
+    pr.dv = w.dv;
+    pr.bsum = w.bsum;
+    pr.nb = nbm;
+    pr.classes = w.classes;
+    pr.ncls = plan->num_classes;
+    pr.rb0 = rb0;
+    pr.alpha = alpha;
+    pr.wr = wr;
+    pr.fef = f_empty_full;
+    pr.phi = phi;
+    pr.info = info;
+    return gnnshap::cg_solve(pr, cg_shape_of(plan), w.cg, s, nullptr);
+  }
   int32_t* counts = reinterpret_cast<int32_t*>(w.G);
   if (has_random) {
     const int64_t nrb = gnnshap::ceil_div(kr, 64);
@@ -2047,7 +2120,7 @@ bool gnnshap::solve_batchable(const gnnshap_sample_plan* plan) {
     clear_error();
     return false;
   }
-  return plan->num_players <= kMidMax && rhs_tiled(plan->num_players, plan->num_classes);
+  return plan->num_players <= kMidMax && rhs_tiled(plan->num_players, plan->num_classes) && !iterative(plan);
 }
 
 size_t gnnshap::solve_slice_bytes(const gnnshap_sample_plan* plan) {
@@ -2193,6 +2266,6 @@ extern "C" int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path
   if (!path) return gnnshap::fail(GNNSHAP_EINVAL, "path is NULL");
   if (int st = check_plan(plan, nullptr)) return st;
   const int64_t M = plan->num_players;
-  *path = M > kMidMax ? 0 : (gnnshap::solve_panel_path(plan) ? 2 : 1);
+  *path = iterative(plan) ? 3 : M > kMidMax ? 0 : (gnnshap::solve_panel_path(plan) ? 2 : 1);
   return GNNSHAP_OK;
 }

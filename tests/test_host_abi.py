@@ -159,3 +159,26 @@ def test_subgraph_batch_init_strides():
         assert sg.edge_gid == (5 << 20) + 8 * 20 * t
     with pytest.raises(RuntimeError):
         L.gnnshap_subgraph_batch_init(sgs, 2, 10, 20, None, 2 << 20, 3 << 20, 4 << 20, 5 << 20)
+
+
+def test_iterative_threshold_selects_path_and_workspace():
+    """Above the iterative threshold (default 5000 players, Sec. 3.5) the
+    solve reports path 3 and needs no M x M matrix in its workspace."""
+    lib = L.load()
+    assert lib.gnnshap_set_iterative_threshold(0) == L.EINVAL
+    try:
+        plan, _ = L.gnnshap_plan_samples(6000, 50000, 1, 2)
+        assert L.gnnshap_solve_info(plan) == 3
+        small, _ = L.gnnshap_plan_samples(4000, 25000, 1, 2)
+        assert L.gnnshap_solve_info(small) == 0
+        direct = L.gnnshap_solve_workspace(small)
+        L.gnnshap_set_iterative_threshold(3999)
+        assert L.gnnshap_solve_info(small) == 3
+        assert L.gnnshap_solve_workspace(small) < min(direct, 4000 * 4000 * 4) // 3
+        mid, _ = L.gnnshap_plan_samples(300, 4000, 1, 2)
+        assert L.gnnshap_solve_info(mid) == 2
+        L.gnnshap_set_iterative_threshold(299)
+        assert L.gnnshap_solve_info(mid) == 3
+    finally:
+        L.gnnshap_set_iterative_threshold(5000)
+    assert L.gnnshap_solve_info(mid) == 2
