@@ -47,7 +47,7 @@ constexpr double kTol = 1e-8;
 constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
 constexpr int kWaves = 8;            // waves per workgroup of both passes
-constexpr int64_t kTabWords = 31;    // nibble tables per workgroup: 31 words (62 KiB of LDS)
+constexpr int64_t kTabWords = 16;    // nibble tables per workgroup: 16 words (32 KiB of LDS)
 
 struct Args {
   const int32_t* sz;
@@ -203,12 +203,14 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
   const int lane = threadIdx.x & 63;
   const int64_t rb = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const bool writer = blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0;
-  if (cg_stop(a, t, writer)) return;   // the same outcome in every wave
   const int64_t pc = blockIdx.y;
   const int64_t w0 = pc * a.pwords;
   const int64_t w1 = w0 + a.pwords < a.wpr ? w0 + a.pwords : a.wpr;
   const int64_t nw = w1 - w0;
+  // the tables do not depend on the stopping test: built first, so that the
+  // test's reads overlap them
   for (int64_t q = threadIdx.x; q < nw * 16; q += kWaves * 64) build_nibble_table(r + w0 * 64 + q * 4, tab + q * 16);
+  if (cg_stop(a, t, writer)) return;   // the same outcome in every wave
   __syncthreads();
   if (rb >= a.nrb) return;
   const uint64_t* src = blocked + (rb * a.wpr + w0) * 64 + lane;
@@ -281,6 +283,16 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
   __shared__ double red[4];
   __shared__ double coef[3];
   if (a.st->done) return;
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  // this thread's vector entries first: their loads overlap the scalar sums
+  double q = 0.0, rj = 0.0, pj = 0.0, sj = 0.0;
+  if (j < a.M) {
+    if (a.has_random)
+      for (int64_t c = 0; c < a.nrc; ++c) q += a.qpart[c * a.M + j];
+    rj = a.r[j];
+    pj = a.p[j];
+    sj = a.s[j];
+  }
   if (threadIdx.x < 64) {
     const double g = wave_fixed_sum(a.rr + (t % 3) * a.nbc, a.nbc);
     const double uu = a.has_random ? wave_fixed_sum(a.uu, a.nbu, 2) : 0.0;
@@ -313,20 +325,15 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
     }
     return;
   }
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   double r2 = 0.0;
   if (j < a.M) {
-    double q = 0.0;
-    if (a.has_random)
-      for (int64_t c = 0; c < a.nrc; ++c) q += a.qpart[c * a.M + j];
-    const double rj = a.r[j];
     const double wj = a.alpha * rj + a.wr2 * (q - mq);
-    const double pj = rj + beta * a.p[j];
-    const double sj = wj + beta * a.s[j];
-    a.p[j] = pj;
-    a.s[j] = sj;
-    a.x[j] += step * pj;
-    const double rn = rj - step * sj;
+    const double pn = rj + beta * pj;
+    const double sn = wj + beta * sj;
+    a.p[j] = pn;
+    a.s[j] = sn;
+    a.x[j] += step * pn;
+    const double rn = rj - step * sn;
     a.r[j] = rn;
     r2 = rn * rn;
   }
