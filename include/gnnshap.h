@@ -340,6 +340,41 @@ int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan
                           int32_t* info, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* 6. Fidelity of an explanation (eq. 7-8, Sec. 4.3; protocol of Sec. 4.6). */
+/*                                                                          */
+/* Importance of a player is |phi| (Sec. 2.3), larger first, equal values   */
+/* by lower player index.  G_S = all players but the floor(s M) least       */
+/* important (sparsity s); G_{C\S} = all but the min(k, M) most important.  */
+/* f is the explained output (the class logit, as for the coalitions).     */
+/* ------------------------------------------------------------------------ */
+
+/* The two coalitions: masks[0 .. wpr) = G_S, masks[wpr .. 2 wpr) = G_{C\S}
+ * (wpr = ceil(M/64) words each, the mask layout of section 2) for phi [dev]
+ * float[M]; masks [dev].  EINVAL: M < 1, sparsity outside [0, 1],
+ * top_k < 0. */
+int gnnshap_fidelity_masks(const float* phi, int64_t M, double sparsity, int64_t top_k, uint64_t* masks,
+                           void* stream);
+
+/* Bytes of device workspace for gnnshap_fidelity on subgraph sg. */
+int gnnshap_fidelity_workspace(const gnnshap_subgraph* sg, const gnnshap_gcn* m, size_t* bytes);
+
+/* One target's fidelity terms: out[0] = |f(G_C) - f(G_S)| (its term of
+ * eq. 7), out[1] = |f(G_C) - f(G_{C\S})| (eq. 8), out[2] = f(G_C) ([dev]
+ * 3 floats).  phi ([dev] float[M], M = sg->num_edges) are the explanation's
+ * values; NaN values order unspecified.  G_S and G_{C\S} are written as two
+ * coalitions and evaluated by gnnshap_eval_coalitions (target_class as
+ * there: -1 = the predicted class on G_C).  EINVAL: sparsity outside
+ * [0, 1], top_k < 0, a subgraph without players; ECAPACITY: workspace. */
+int gnnshap_fidelity(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X, int32_t target_class,
+                     const float* phi, double sparsity, int64_t top_k, float* out, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/* eq. 7 and eq. 8 over n targets: avg[0] = mean of terms[t * stride],
+ * avg[1] = mean of terms[t * stride + 1] (all [dev]; fp64 sums in a fixed
+ * order).  EINVAL: n < 1 or stride < 2. */
+int gnnshap_fidelity_average(const float* terms, int64_t n, int64_t stride, float* avg, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics: HIP-event timing of one kernel.                             */
 /* ------------------------------------------------------------------------ */
 

@@ -82,6 +82,11 @@ _SIGNATURES = {
                                              c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_solve_info": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(c_i32)]),
     "gnnshap_set_iterative_threshold": (ctypes.c_int, [c_i64]),
+    "gnnshap_fidelity_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), _P(ctypes.c_size_t)]),
+    "gnnshap_fidelity": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_dbl, c_i64,
+                                        c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_fidelity_average": (ctypes.c_int, [c_vp, c_i64, c_i64, c_vp, c_vp]),
+    "gnnshap_fidelity_masks": (ctypes.c_int, [c_vp, c_i64, c_dbl, c_i64, c_vp, c_vp]),
     "gnnshap_timing_begin": (ctypes.c_int, [ctypes.c_char_p]),
     "gnnshap_timing_end": (ctypes.c_int, [_P(ctypes.c_double), _P(c_i64)]),
 }
@@ -273,6 +278,27 @@ def gnnshap_solve_info(plan):
     v = c_i32()
     check(load().gnnshap_solve_info(ctypes.byref(plan), ctypes.byref(v)), "solve_info")
     return v.value
+
+
+def gnnshap_fidelity_workspace(sg, model):
+    n = ctypes.c_size_t()
+    check(load().gnnshap_fidelity_workspace(ctypes.byref(sg), ctypes.byref(model), ctypes.byref(n)),
+          "fidelity_workspace")
+    return n.value
+
+
+def gnnshap_fidelity(sg, model, X_ptr, target_class, phi_ptr, sparsity, top_k, out_ptr, ws_ptr, ws_bytes, stream):
+    check(load().gnnshap_fidelity(ctypes.byref(sg), ctypes.byref(model), X_ptr, int(target_class), phi_ptr,
+                                  float(sparsity), int(top_k), out_ptr, ws_ptr, ws_bytes, stream), "fidelity")
+
+
+def gnnshap_fidelity_masks(phi_ptr, M, sparsity, top_k, masks_ptr, stream):
+    check(load().gnnshap_fidelity_masks(phi_ptr, int(M), float(sparsity), int(top_k), masks_ptr, stream),
+          "fidelity_masks")
+
+
+def gnnshap_fidelity_average(terms_ptr, n, stride, avg_ptr, stream):
+    check(load().gnnshap_fidelity_average(terms_ptr, int(n), int(stride), avg_ptr, stream), "fidelity_average")
 
 
 def gnnshap_set_iterative_threshold(num_players):

@@ -91,6 +91,7 @@ class Explainer:
         self.ws_eval = _Buffer(dev)
         self.ws_solve = _Buffer(dev)
         self.ws_batch = _Buffer(dev)
+        self.ws_fid = _Buffer(dev)
         self._pipe = None
         self._bx = None                          # batched extraction: (n, zero-filled workspace)
         self._plans = {}                         # (M, p) -> (plan, classes): the plan does not depend on seed
@@ -286,6 +287,29 @@ class Explainer:
             bufs = self.extract_batch_start(bufs.target_ids)
             sgs = bufs.sgs
         return bufs, sgs
+
+    def fidelity(self, explanations, sparsity=0.3, top_k=10, target_class=-1):
+        """Fidelity- and Fidelity+ (eq. 7-8) of explanations whose subgraph
+        arrays are still valid (explain()'s until the next extract(), a
+        BatchExplanations' until the next batch): per target
+        gnnshap_fidelity with the explanation's phi (G_S drops the
+        floor(sparsity M) least important players by |phi|, G_C minus S the
+        top_k most important; Sec. 4.6 uses 0.3 and 10), then
+        gnnshap_fidelity_average.  Returns (terms, avg): float32 [n, 3] rows
+        (Fidelity- term, Fidelity+ term, f(G_C)) and [2] (eq. 7, eq. 8), on
+        the device, valid once the current stream has run."""
+        items = list(explanations)
+        n = len(items)
+        terms = torch.empty((n, 3), dtype=torch.float32, device=self.device)
+        avg = torch.empty(2, dtype=torch.float32, device=self.device)
+        s = self.stream()
+        for t, e in enumerate(items):
+            nbytes = L.gnnshap_fidelity_workspace(e.sub.sg, self.model)
+            ws = self.ws_fid.get(nbytes)
+            L.gnnshap_fidelity(e.sub.sg, self.model, _vp(self.X), target_class, _vp(e.phi), sparsity, top_k,
+                               _vp(terms[t]), _vp(ws), ws.numel(), s)
+        L.gnnshap_fidelity_average(_vp(terms), n, 3, _vp(avg), s)
+        return terms, avg
 
     def explain_batch(self, targets, num_samples, seed, target_class=-1):
         """Alg. 1 for every target, one launch per step for the whole batch

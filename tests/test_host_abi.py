@@ -182,3 +182,20 @@ def test_iterative_threshold_selects_path_and_workspace():
     finally:
         L.gnnshap_set_iterative_threshold(5000)
     assert L.gnnshap_solve_info(mid) == 2
+
+
+def test_fidelity_entry_points_reject_bad_arguments():
+    """Argument checks of the fidelity calls (eq. 7-8) happen before any launch."""
+    lib = L.load()
+    fake = ctypes.c_void_p(256)
+    assert lib.gnnshap_fidelity_masks(None, 10, 0.3, 10, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_masks(fake, 0, 0.3, 10, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_masks(fake, 10, 1.5, 10, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_masks(fake, 10, float("nan"), 10, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_masks(fake, 10, 0.3, -1, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_average(fake, 0, 3, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_average(fake, 4, 1, fake, None) == L.EINVAL
+    assert lib.gnnshap_fidelity_average(None, 4, 3, fake, None) == L.EINVAL
+    sg = L.gnnshap_subgraph(num_hops=2)
+    n = ctypes.c_size_t()
+    assert lib.gnnshap_fidelity_workspace(ctypes.byref(sg), None, ctypes.byref(n)) == L.EINVAL
