@@ -15,5 +15,5 @@ so that degree does not correlate with id.
 from .graphs import (chung_lu_pairs, dcsbm_pairs, in_csr_from_pairs,  # noqa: F401
                      in_csr_from_directed, random_digraph)
 from .params import (binary_features, tfidf_features, gaussian_features,  # noqa: F401
-                     glorot_gcn)
+                     glorot_gcn, glorot_gat)
 from .configs import CONFIGS, make_config, player_count  # noqa: F401

@@ -39,3 +39,28 @@ def glorot_gcn(dims, seed, bias="zero"):
         else:
             bs.append(rng.uniform(-0.1, 0.1, size=dims[l + 1]).astype(np.float32))
     return Ws, bs
+
+
+def glorot_gat(d, heads, head_dim, classes, seed, bias="zero"):
+    """Random-init parameters of a two-layer GAT: layer 1 `heads` heads of
+    width `head_dim` (outputs concatenated), layer 2 one head of width
+    `classes`.  Weights and attention vectors Glorot-uniform, biases zero or
+    U(-0.1, 0.1).  Returned as a dict of fp32 arrays: W1 [d, heads*head_dim],
+    att_src1 / att_dst1 [heads, head_dim], b1 [heads*head_dim],
+    W2 [heads*head_dim, classes], att_src2 / att_dst2 [classes], b2 [classes]."""
+    rng = _rng(seed)
+    hf = heads * head_dim
+
+    def glorot(shape, fan_in, fan_out):
+        a = np.sqrt(6.0 / (fan_in + fan_out))
+        return rng.uniform(-a, a, size=shape).astype(np.float32)
+
+    def b(n):
+        if bias == "zero":
+            return np.zeros(n, dtype=np.float32)
+        return rng.uniform(-0.1, 0.1, size=n).astype(np.float32)
+
+    return dict(W1=glorot((d, hf), d, hf), att_src1=glorot((heads, head_dim), head_dim, 1),
+                att_dst1=glorot((heads, head_dim), head_dim, 1), b1=b(hf),
+                W2=glorot((hf, classes), hf, classes), att_src2=glorot((classes,), classes, 1),
+                att_dst2=glorot((classes,), classes, 1), b2=b(classes))
