@@ -375,6 +375,47 @@ int gnnshap_fidelity(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const flo
 int gnnshap_fidelity_average(const float* terms, int64_t n, int64_t stride, float* avg, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* 7. Coalition values of a two-layer GAT (App. E).                         */
+/*                                                                          */
+/* A coalition keeps its edges and every self loop.  Layer 1: `heads`       */
+/* attention heads of width head_dim (Velickovic et al. 2018: z = X W_1,    */
+/* e_h(u -> x) = LeakyReLU(a_src,h . z_h[u] + a_dst,h . z_h[x]), softmax    */
+/* over the edges into x present in the coalition and the self loop,        */
+/* out_h[x] = sum alpha z_h[u]), heads concatenated, plus b_1, then ELU.    */
+/* Layer 2: one head of width num_classes on the layer-1 outputs, plus b_2. */
+/* The softmax is renormalised under each coalition: only present edges     */
+/* compete.  y = the layer-2 output at the target for the explained class.  */
+/* The subgraph must have num_hops = 2 (players = edges into H_1).          */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t heads;                 /* layer-1 heads, heads * head_dim <= 256 */
+  int32_t head_dim;
+  int32_t num_classes;           /* C, layer-2 width */
+  int32_t reserved;
+  const float* XW1;              /* [dev] num_nodes x heads*head_dim: X W_1 for every node
+                                    (gnnshap_transform_features); required */
+  const float* att_src1;         /* [dev] heads x head_dim */
+  const float* att_dst1;         /* [dev] heads x head_dim */
+  const float* b1;               /* [dev] heads*head_dim */
+  const float* W2;               /* [dev] heads*head_dim x C */
+  const float* att_src2;         /* [dev] C */
+  const float* att_dst2;         /* [dev] C */
+  const float* b2;               /* [dev] C */
+  double negative_slope;         /* LeakyReLU slope of the attention logits, in [0, 1) (0.2) */
+} gnnshap_gat;
+
+/* Bytes of device workspace for evaluating k coalitions of sg with model m. */
+int gnnshap_gat_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_gat* m, int64_t k, size_t* bytes);
+
+/* y[b] = f(S_b) for b < k under the GAT (outputs, classes and pruning as for
+ * gnnshap_eval_coalitions: a coalition without an in-edge of the target has
+ * the value f(empty)).  EINVAL: num_hops != 2, bad sizes or model arrays,
+ * target_class out of range; ECAPACITY: workspace. */
+int gnnshap_gat_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gat* m, int32_t target_class,
+                                const uint64_t* masks, int64_t k, int64_t words_per_row, float* y,
+                                float* f_empty_full, int32_t* class_out, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics: HIP-event timing of one kernel.                             */
 /* ------------------------------------------------------------------------ */
 

@@ -37,16 +37,17 @@ def elu(x):
     return np.where(x > 0, x, np.expm1(np.minimum(x, 0.0)))
 
 
-def layer_dense(H, present, sub, W, a_src, a_dst, b, slope=0.2):
+def layer_dense(H, present, sub, W, a_src, a_dst, b, slope=0.2, Z=None):
     """One GAT layer with dense attention matrices: A[w, u] = 1 for present
-    edges u -> w and for u = w; the softmax runs over each row's ones."""
+    edges u -> w and for u = w; the softmax runs over each row's ones.  Z,
+    if given, is H W (a constant of the target for the first layer)."""
     n = H.shape[0]
     a_src = _as64(a_src).reshape(-1, _as64(a_src).shape[-1])
     heads, F = a_src.shape
     a_dst = _as64(a_dst).reshape(heads, F)
     A = np.eye(n, dtype=bool)
     A[sub["edge_dst"][present], sub["edge_src"][present]] = True
-    Z = (H @ _as64(W)).reshape(n, heads, F)
+    Z = (H @ _as64(W) if Z is None else Z).reshape(n, heads, F)
     out = np.zeros((n, heads, F))
     for h in range(heads):
         s = Z[:, h, :] @ a_src[h]
@@ -59,7 +60,7 @@ def layer_dense(H, present, sub, W, a_src, a_dst, b, slope=0.2):
     return out.reshape(n, heads * F) + _as64(b)[None, :]
 
 
-def layer_edges(H, present, sub, W, a_src, a_dst, b, slope=0.2):
+def layer_edges(H, present, sub, W, a_src, a_dst, b, slope=0.2, Z=None):
     """The same layer over an edge list (present edges and self loops),
     normalised per destination."""
     n = H.shape[0]
@@ -68,17 +69,17 @@ def layer_edges(H, present, sub, W, a_src, a_dst, b, slope=0.2):
     a_dst = _as64(a_dst).reshape(heads, F)
     src = np.concatenate([sub["edge_src"][present], np.arange(n)])
     dst = np.concatenate([sub["edge_dst"][present], np.arange(n)])
-    Z = (H @ _as64(W)).reshape(n, heads, F)
+    Z = (H @ _as64(W) if Z is None else Z).reshape(n, heads, F)
     s = np.einsum("nhf,hf->nh", Z, a_src)
     d = np.einsum("nhf,hf->nh", Z, a_dst)
     e = leaky(s[src] + d[dst], slope)                       # edges x heads
+    mx = np.full((n, heads), -np.inf)
+    np.maximum.at(mx, dst, e)
+    p = np.exp(e - mx[dst])
+    den = np.zeros((n, heads))
+    np.add.at(den, dst, p)
     out = np.zeros((n, heads, F))
-    for w in range(n):
-        sel = np.nonzero(dst == w)[0]
-        ew = e[sel]
-        p = np.exp(ew - ew.max(axis=0, keepdims=True))
-        p /= p.sum(axis=0, keepdims=True)
-        out[w] = np.einsum("eh,ehf->hf", p, Z[src[sel]])
+    np.add.at(out, dst, (p / den[dst])[:, :, None] * Z[src])
     return out.reshape(n, heads * F) + _as64(b)[None, :]
 
 
@@ -89,6 +90,7 @@ class GatGame:
         self.sub = sub
         self.p = {k: _as64(v) for k, v in params.items()}
         self.H0 = _as64(X)[sub["node_gid"]]
+        self.Z1 = self.H0 @ self.p["W1"]          # X W_1 rows: the same for every coalition
         self.cls = cls
         self.layer = layer_dense if dense else layer_edges
         self.slope = slope
@@ -97,7 +99,7 @@ class GatGame:
         present = np.asarray(mask, dtype=bool)
         p = self.p
         H1 = elu(self.layer(self.H0, present, self.sub, p["W1"], p["att_src1"], p["att_dst1"], p["b1"],
-                            self.slope))
+                            self.slope, Z=self.Z1))
         H2 = self.layer(H1, present, self.sub, p["W2"], p["att_src2"][None, :], p["att_dst2"][None, :], p["b2"],
                         self.slope)
         return H2[0]

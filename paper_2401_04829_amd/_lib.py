@@ -44,6 +44,12 @@ class gnnshap_gcn(ctypes.Structure):
                 ("W", ctypes.POINTER(c_vp)), ("b", ctypes.POINTER(c_vp)), ("XW1", c_vp)]
 
 
+class gnnshap_gat(ctypes.Structure):
+    _fields_ = [("heads", c_i32), ("head_dim", c_i32), ("num_classes", c_i32), ("reserved", c_i32),
+                ("XW1", c_vp), ("att_src1", c_vp), ("att_dst1", c_vp), ("b1", c_vp), ("W2", c_vp),
+                ("att_src2", c_vp), ("att_dst2", c_vp), ("b2", c_vp), ("negative_slope", c_dbl)]
+
+
 _P = ctypes.POINTER
 _SIGNATURES = {
     "gnnshap_status_str": (ctypes.c_char_p, [ctypes.c_int]),
@@ -87,6 +93,10 @@ _SIGNATURES = {
                                         c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_fidelity_average": (ctypes.c_int, [c_vp, c_i64, c_i64, c_vp, c_vp]),
     "gnnshap_fidelity_masks": (ctypes.c_int, [c_vp, c_i64, c_dbl, c_i64, c_vp, c_vp]),
+    "gnnshap_gat_eval_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gat), c_i64,
+                                                  _P(ctypes.c_size_t)]),
+    "gnnshap_gat_eval_coalitions": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gat), c_i32, c_vp, c_i64, c_i64,
+                                                   c_vp, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_timing_begin": (ctypes.c_int, [ctypes.c_char_p]),
     "gnnshap_timing_end": (ctypes.c_int, [_P(ctypes.c_double), _P(c_i64)]),
 }
@@ -290,6 +300,20 @@ def gnnshap_fidelity_workspace(sg, model):
 def gnnshap_fidelity(sg, model, X_ptr, target_class, phi_ptr, sparsity, top_k, out_ptr, ws_ptr, ws_bytes, stream):
     check(load().gnnshap_fidelity(ctypes.byref(sg), ctypes.byref(model), X_ptr, int(target_class), phi_ptr,
                                   float(sparsity), int(top_k), out_ptr, ws_ptr, ws_bytes, stream), "fidelity")
+
+
+def gnnshap_gat_eval_workspace(sg, model, k):
+    n = ctypes.c_size_t()
+    check(load().gnnshap_gat_eval_workspace(ctypes.byref(sg), ctypes.byref(model), int(k), ctypes.byref(n)),
+          "gat_eval_workspace")
+    return n.value
+
+
+def gnnshap_gat_eval_coalitions(sg, model, target_class, masks_ptr, k, wpr, y_ptr, fef_ptr, cls_ptr, ws_ptr,
+                                ws_bytes, stream):
+    check(load().gnnshap_gat_eval_coalitions(ctypes.byref(sg), ctypes.byref(model), int(target_class), masks_ptr,
+                                             int(k), int(wpr), y_ptr, fef_ptr, cls_ptr, ws_ptr, ws_bytes, stream),
+          "gat_eval_coalitions")
 
 
 def gnnshap_fidelity_masks(phi_ptr, M, sparsity, top_k, masks_ptr, stream):

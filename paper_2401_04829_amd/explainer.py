@@ -207,15 +207,19 @@ class Explainer:
         y = torch.empty(k, dtype=torch.float32, device=dev)
         fef = torch.empty(2, dtype=torch.float32, device=dev)
         cls = torch.empty(1, dtype=torch.int32, device=dev)
-        ws = ws_eval.get(L.gnnshap_eval_workspace(sub.sg, self.model, k))
-        L.gnnshap_eval_coalitions(sub.sg, self.model, _vp(self.X), int(target_class), _vp(masks), k, wpr, _vp(y),
-                                  _vp(fef), _vp(cls), _vp(ws), ws.numel(), s)
+        self._evaluate(sub, target_class, masks, k, wpr, y, fef, cls, ws_eval, s)
         phi = torch.empty(M, dtype=torch.float32, device=dev)
         info = torch.empty(1, dtype=torch.int32, device=dev)
         ws = ws_solve.get(L.gnnshap_solve_workspace(plan))
         L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(ws), ws.numel(), s)
         return Explanation(target=target, sub=sub, plan=plan, classes=classes, masks=masks, weights=weights, y=y,
                            f_empty_full=fef, cls=cls, phi=phi, info=info)
+
+    def _evaluate(self, sub, target_class, masks, k, wpr, y, fef, cls, ws_eval, s):
+        """gnnshap_eval_coalitions on the current stream."""
+        ws = ws_eval.get(L.gnnshap_eval_workspace(sub.sg, self.model, k))
+        L.gnnshap_eval_coalitions(sub.sg, self.model, _vp(self.X), int(target_class), _vp(masks), k, wpr, _vp(y),
+                                  _vp(fef), _vp(cls), _vp(ws), ws.numel(), s)
 
     # -- many targets per launch sequence ------------------------------------------------------
 
@@ -468,3 +472,43 @@ class BatchExplanations:
 
     def __iter__(self):
         return (self[t] for t in range(len(self)))
+
+
+class GatExplainer(Explainer):
+    """Alg. 1 for a two-layer GAT (App. E): the same extraction (2 hops),
+    plan, sampler and least squares as Explainer, with the coalition values
+    of gnnshap_gat_eval_coalitions.  `params` as workloads.glorot_gat makes
+    them (W1, att_src1, att_dst1, b1, W2, att_src2, att_dst2, b2).  Single
+    targets only (explain, explain_many)."""
+
+    def __init__(self, indptr, indices, X, params, device="cuda", negative_slope=0.2):
+        heads, head_dim = (int(v) for v in params["att_src1"].shape)
+        classes = int(params["W2"].shape[1])
+        super().__init__(indptr, indices, X, [params["W1"], params["W2"]], [params["b1"], params["b2"]], 2, device)
+        self.gat_params = {k: torch.as_tensor(v, dtype=torch.float32).to(self.device).contiguous()
+                           for k, v in params.items()}
+        p = self.gat_params
+        self.gat = L.gnnshap_gat(heads=heads, head_dim=head_dim, num_classes=classes, XW1=None,
+                                 att_src1=p["att_src1"].data_ptr(), att_dst1=p["att_dst1"].data_ptr(),
+                                 b1=p["b1"].data_ptr(), W2=p["W2"].data_ptr(), att_src2=p["att_src2"].data_ptr(),
+                                 att_dst2=p["att_dst2"].data_ptr(), b2=p["b2"].data_ptr(),
+                                 negative_slope=float(negative_slope))
+
+    def prepare(self):
+        super().prepare()
+        self.gat.XW1 = self.XW1.data_ptr()
+
+    def _evaluate(self, sub, target_class, masks, k, wpr, y, fef, cls, ws_eval, s):
+        """gnnshap_gat_eval_coalitions on the current stream."""
+        ws = ws_eval.get(L.gnnshap_gat_eval_workspace(sub.sg, self.gat, k))
+        L.gnnshap_gat_eval_coalitions(sub.sg, self.gat, int(target_class), _vp(masks), k, wpr, _vp(y), _vp(fef),
+                                      _vp(cls), _vp(ws), ws.numel(), s)
+
+    def explain_batch(self, *args, **kwargs):
+        raise NotImplementedError("the batched entry points evaluate GCNs; explain GAT targets one at a time")
+
+    def explain_batches(self, *args, **kwargs):
+        raise NotImplementedError("the batched entry points evaluate GCNs; explain GAT targets one at a time")
+
+    def fidelity(self, *args, **kwargs):
+        raise NotImplementedError("gnnshap_fidelity evaluates GCNs")

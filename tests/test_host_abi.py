@@ -199,3 +199,26 @@ def test_fidelity_entry_points_reject_bad_arguments():
     sg = L.gnnshap_subgraph(num_hops=2)
     n = ctypes.c_size_t()
     assert lib.gnnshap_fidelity_workspace(ctypes.byref(sg), None, ctypes.byref(n)) == L.EINVAL
+
+
+def test_gat_entry_points_reject_bad_arguments():
+    """The GAT calls (App. E) check the subgraph depth and the model shape
+    before any launch."""
+    lib = L.load()
+    fake = 256
+    m = L.gnnshap_gat(heads=8, head_dim=16, num_classes=7, XW1=fake, att_src1=fake, att_dst1=fake, b1=fake, W2=fake,
+                      att_src2=fake, att_dst2=fake, b2=fake, negative_slope=0.2)
+    sg = L.gnnshap_subgraph(num_hops=2, num_nodes=10, num_edges=12, num_dst=4)
+    n = ctypes.c_size_t()
+    assert lib.gnnshap_gat_eval_workspace(ctypes.byref(sg), ctypes.byref(m), 100, ctypes.byref(n)) == L.OK
+    assert n.value > 0
+    sg3 = L.gnnshap_subgraph(num_hops=3, num_nodes=10, num_edges=12, num_dst=4)
+    assert lib.gnnshap_gat_eval_workspace(ctypes.byref(sg3), ctypes.byref(m), 100, ctypes.byref(n)) == L.EINVAL
+    for bad in (dict(heads=0), dict(head_dim=33, heads=8), dict(num_classes=0), dict(negative_slope=1.0),
+                dict(XW1=None)):
+        mb = L.gnnshap_gat(heads=8, head_dim=16, num_classes=7, XW1=fake, att_src1=fake, att_dst1=fake, b1=fake,
+                           W2=fake, att_src2=fake, att_dst2=fake, b2=fake, negative_slope=0.2)
+        for k, v in bad.items():
+            setattr(mb, k, v)
+        assert lib.gnnshap_gat_eval_workspace(ctypes.byref(sg), ctypes.byref(mb), 100, ctypes.byref(n)) == L.EINVAL, bad
+    assert lib.gnnshap_gat_eval_workspace(ctypes.byref(sg), ctypes.byref(m), 0, ctypes.byref(n)) == L.EINVAL
