@@ -1300,19 +1300,21 @@ __global__ void k_fill_pruned(const uint8_t* __restrict__ live_flag, int64_t k,
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Z[r, :] = X[r, :] W for 16 rows per workgroup, h = 16 NT columns, fp32
-// MFMA 16x16x4.  The four wavefronts split K into quarters and each lane
+// MFMA 16x16x4.  The KW wavefronts split K into KW parts and each lane
 // group of 16 lanes takes a quarter of its wavefront's range, so every MFMA
-// sums four k; the four partial 16 x h tiles are added in LDS in a fixed
-// order (no atomics: the result does not depend on scheduling).
-template <int NT>
-__global__ void __launch_bounds__(256) k_transform(const float* __restrict__ X, int64_t n, int d,
-                                                   const float* __restrict__ W, int h, float* __restrict__ Z) {
-  __shared__ float part[4][16][16 * NT + 1];
+// sums four k; the KW partial 16 x h tiles are added in LDS in a fixed order
+// (no atomics: the result does not depend on scheduling).  Narrow outputs
+// use 16 wavefronts: a 16-row tile then has four times as many loads in
+// flight (the kernel is bound by their latency, not by the MFMAs).
+template <int NT, int KW>
+__global__ void __launch_bounds__(KW * 64) k_transform(const float* __restrict__ X, int64_t n, int d,
+                                                       const float* __restrict__ W, int h, float* __restrict__ Z) {
+  __shared__ float part[KW][16][16 * NT + 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 16;
   const int64_t row = r0 + c;
-  const int kq = (d + 3) / 4;
+  const int kq = (d + KW - 1) / KW;
   const int kb = wave * kq;
   const int ke = kb + kq < d ? kb + kq : d;
   const int kg = (kq + 3) / 4;
@@ -1343,9 +1345,14 @@ __global__ void __launch_bounds__(256) k_transform(const float* __restrict__ X, 
 #pragma unroll
     for (int r = 0; r < 4; ++r) part[wave][4 * g + r][t * 16 + c] = acc[t][r];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < 16 * h; idx += 256) {
+  for (int idx = threadIdx.x; idx < 16 * h; idx += KW * 64) {
     const int i = idx / h, j = idx % h;
-    if (r0 + i < n) Z[(r0 + i) * h + j] = (part[0][i][j] + part[1][i][j]) + (part[2][i][j] + part[3][i][j]);
+    if (r0 + i < n) {
+      float v = 0.f;
+#pragma unroll
+      for (int q = 0; q < KW; q += 4) v += (part[q][i][j] + part[q + 1][i][j]) + (part[q + 2][i][j] + part[q + 3][i][j]);
+      Z[(r0 + i) * h + j] = v;
+    }
   }
 }
 
@@ -1702,14 +1709,14 @@ extern "C" int gnnshap_transform_features(const float* X, int64_t n, int32_t d, 
     const unsigned g = static_cast<unsigned>(gnnshap::ceil_div(n, 16));
     GS_TIMED("k_transform", s);
     switch (h / 16) {
-      case 1: k_transform<1><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      case 2: k_transform<2><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      case 3: k_transform<3><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      case 4: k_transform<4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      case 5: k_transform<5><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      case 6: k_transform<6><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      case 7: k_transform<7><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
-      default: k_transform<8><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 1: k_transform<1, 16><<<g, 1024, 0, s>>>(X, n, d, W, h, Z); break;
+      case 2: k_transform<2, 16><<<g, 1024, 0, s>>>(X, n, d, W, h, Z); break;
+      case 3: k_transform<3, 4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 4: k_transform<4, 4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 5: k_transform<5, 4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 6: k_transform<6, 4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      case 7: k_transform<7, 4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
+      default: k_transform<8, 4><<<g, 256, 0, s>>>(X, n, d, W, h, Z); break;
     }
     GS_LAUNCHED();
     return GNNSHAP_OK;
