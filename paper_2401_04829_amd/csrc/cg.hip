@@ -293,25 +293,32 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
     pj = a.p[j];
     sj = a.s[j];
   }
-  if (threadIdx.x < 64) {
-    const double g = wave_fixed_sum(a.rr + (t % 3) * a.nbc, a.nbc);
-    const double uu = a.has_random ? wave_fixed_sum(a.uu, a.nbu, 2) : 0.0;
-    const double su = a.has_random ? wave_fixed_sum(a.uu + 1, a.nbu, 2) : 0.0;
+  // the four scalar sums, one per wavefront, side by side
+  __shared__ double sums[4];
+  {
+    const int wv = threadIdx.x >> 6;
+    double v = 0.0;
+    if (wv == 0) v = wave_fixed_sum(a.rr + (t % 3) * a.nbc, a.nbc);
+    else if (wv == 1) v = a.has_random ? wave_fixed_sum(a.uu, a.nbu, 2) : 0.0;
+    else if (wv == 2) v = a.has_random ? wave_fixed_sum(a.uu + 1, a.nbu, 2) : 0.0;
+    else v = t > 0 ? wave_fixed_sum(a.rr + ((t + 2) % 3) * a.nbc, a.nbc) : 1.0;
+    if ((threadIdx.x & 63) == 0) sums[wv] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double g = sums[0], uu = sums[1], su = sums[2], gp = sums[3];
     const double delta = a.alpha * g + a.wr2 * uu;
     double beta = 0.0, den = delta;
     if (t > 0) {
-      const double gp = wave_fixed_sum(a.rr + ((t + 2) % 3) * a.nbc, a.nbc);
       beta = g / gp;
       den = delta - beta * g / a.hist[(t + 1) & 1];
     }
     const double step = g / den;
-    if (threadIdx.x == 0) {
-      const bool ok = den > 0.0 && step == step && step < 1e300 && beta == beta;
-      coef[0] = ok ? step : -1.0;
-      coef[1] = beta;
-      coef[2] = su / static_cast<double>(a.M);
-      if (ok && blockIdx.x == 0) a.hist[t & 1] = step;
-    }
+    const bool ok = den > 0.0 && step == step && step < 1e300 && beta == beta;
+    coef[0] = ok ? step : -1.0;
+    coef[1] = beta;
+    coef[2] = su / static_cast<double>(a.M);
+    if (ok && blockIdx.x == 0) a.hist[t & 1] = step;
   }
   __syncthreads();
   const double step = coef[0], beta = coef[1], mq = coef[2];
