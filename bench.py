@@ -41,7 +41,83 @@ def parse():
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="bytes of a plain device copy run before the steps (counter calibration)")
+    ap.add_argument("--solver-sweep", action="store_true",
+                    help="instead of the step: least-squares solve times, factorisation vs iterative")
+    ap.add_argument("--gat", action="store_true",
+                    help="instead of the step: explain times of the GAT variant and the GCN, one target at a time")
     return ap.parse_args()
+
+
+def solver_sweep():
+    """Solve times of gnnshap_solve_wls on sampled plans of 6,000-30,000
+    players, through the factorisation and through the iterative path
+    (Sec. 3.5), on noisy values; one JSON line per case."""
+    import torch
+    from paper_2401_04829_amd import _lib as L
+    from paper_2401_04829_amd.explainer import _vp
+    dev = torch.device("cuda:0")
+    s = torch.cuda.current_stream().cuda_stream
+    for M, p in [(6000, 50000), (12000, 50000), (20000, 50000), (30000, 100000)]:
+        plan, classes = L.gnnshap_plan_samples(M, p, 3, 4)
+        k, wpr = plan.num_rows, plan.words_per_row
+        masks = torch.empty((k, wpr), dtype=torch.int64, device=dev)
+        weights = torch.empty(k, dtype=torch.float32, device=dev)
+        ws = torch.empty(max(L.gnnshap_sample_workspace(plan), 256), dtype=torch.uint8, device=dev)
+        L.gnnshap_sample_coalitions(plan, classes, _vp(masks), _vp(weights), _vp(ws), ws.numel(), s)
+        g = torch.Generator(device=dev)
+        g.manual_seed(M)
+        y = torch.randn(k, generator=g, device=dev)
+        fef = torch.tensor([0.1, 0.7], dtype=torch.float32, device=dev)
+        res = {}
+        for path, thr in (("factorised", M + 1), ("iterative", M - 1)):
+            L.gnnshap_set_iterative_threshold(thr)
+            phi = torch.empty(M, dtype=torch.float32, device=dev)
+            info = torch.empty(1, dtype=torch.int32, device=dev)
+            wsol = torch.empty(L.gnnshap_solve_workspace(plan), dtype=torch.uint8, device=dev)
+            times = []
+            for _ in range(3):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                L.gnnshap_solve_wls(plan, classes, _vp(masks), _vp(y), _vp(fef), _vp(phi), _vp(info), _vp(wsol),
+                                    wsol.numel(), s)
+                torch.cuda.synchronize()
+                times.append(1e3 * (time.perf_counter() - t0))
+            res[path] = (min(times), int(info.item()), phi.double())
+            del wsol
+        L.gnnshap_set_iterative_threshold(5000)
+        a, b = res["factorised"][2], res["iterative"][2]
+        print(json.dumps({"solver_sweep": {"players": M, "coalitions": p, "random_rows": k // 2 - plan.random_begin,
+                                           "factorised_ms": res["factorised"][0], "iterative_ms": res["iterative"][0],
+                                           "info": [res["factorised"][1], res["iterative"][1]],
+                                           "max_dphi_over_max_phi": float((a - b).abs().max() / a.abs().max())}}))
+        del masks, weights, ws, y
+        torch.cuda.empty_cache()
+
+
+def gat_times():
+    """Explain times of 100 cora-shaped targets x 10,000 coalitions, one
+    target at a time, for the two-layer GAT of App. E (8 heads of 16,
+    random-init) and for the GCN of the same workload."""
+    import torch
+    import workloads as W
+    from paper_2401_04829_amd.explainer import Explainer, GatExplainer
+    cfg = W.make_config("cora")
+    P = W.glorot_gat(cfg["X"].shape[1], 8, 16, len(cfg["weights"][-1][0]), 41)
+    for name, ex in (("gat", GatExplainer(cfg["indptr"], cfg["indices"], cfg["X"], P)),
+                     ("gcn", Explainer(cfg["indptr"], cfg["indices"], cfg["X"], cfg["weights"], cfg["biases"],
+                                       cfg["hops"]))):
+        best = None
+        for _ in range(2):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for v in cfg["targets"]:
+                ex.explain(v, cfg["p"], cfg["seed"])
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            best = dt if best is None else min(best, dt)
+        print(json.dumps({"explain_one_at_a_time": {"model": name, "targets": len(cfg["targets"]),
+                                                    "coalitions": cfg["p"], "ms_total": 1e3 * best,
+                                                    "ms_per_target": 1e3 * best / len(cfg["targets"])}}))
 
 
 def cpu_baseline(cfg, seconds):
@@ -188,6 +264,12 @@ def main():
     from paper_2401_04829_amd.explainer import Explainer
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.solver_sweep or args.gat:
+        if args.solver_sweep:
+            solver_sweep()
+        if args.gat:
+            gat_times()
+        return
     dev = torch.device("cuda:0")
     cfg = W.make_config(args.config)
     ex = Explainer(cfg["indptr"], cfg["indices"], cfg["X"], cfg["weights"], cfg["biases"], cfg["hops"], device=dev)
