@@ -362,7 +362,8 @@ __global__ void __launch_bounds__(1024) k_cg_finish(const double* __restrict__ x
   if (threadIdx.x == 0) *info = st->status == 0 ? 0 : static_cast<int32_t>(M + 1);
 }
 
-// Mapped page-locked stopping flag of the calling thread and its device address.
+// Mapped page-locked stopping flag of the calling thread, its device address
+// and the two events of the chunked wait (kept until the process ends).
 struct HostFlag {
   int32_t* host = nullptr;
   int32_t* dev = nullptr;

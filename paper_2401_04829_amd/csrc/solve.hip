@@ -15,7 +15,8 @@
 //     with C_R the integer co-occurrence counts of the random representative
 //     rows, computed exactly by popcounts on a bit-transposed copy.
 // Systems of up to 448 players are factored and solved by one workgroup
-// (several targets' systems side by side in a batch).  Larger ones use a
+// (several targets' systems side by side in a batch).  Larger ones, up to
+// the iterative threshold (above it the system is not formed: cg.hip), use a
 // blocked right-looking Cholesky over the whole GPU with 128-wide panels: one workgroup factors the diagonal block and
 // inverts its factor, then the panel solve (a product with that inverse) and
 // the trailing update run as fp32 MFMA GEMMs.  The triangular solves go by
