@@ -241,10 +241,10 @@ int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes);
  * equations, applying the masks and their transpose straight from the bits
  * (Sec. 3.5 fits large systems iteratively), until the residual falls to
  * 1e-8 of its initial norm; *info is then 0, or M + 1 if that did not happen
- * within 4000 iterations or the iteration broke down.  Unlike the
- * factorisation, it does not detect systems the sampled rows leave
- * undetermined (fewer random rows than players): there the residual can
- * still fall and phi is one of many minimisers.  That path waits on
+ * within 4000 iterations, the iteration broke down, or the plan has no
+ * enumerated class and fewer than M - 1 random rows (then the rows cannot
+ * determine phi).  Other rank deficiencies are not detected on that path:
+ * the residual can still fall and phi is then one of many minimisers.  That path waits on
  * `stream` for its stopping test (the call returns once the iteration has
  * stopped; the write of phi is still queued). */
 int gnnshap_solve_wls(const gnnshap_sample_plan* plan,

@@ -352,14 +352,14 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
 __global__ void __launch_bounds__(1024) k_cg_finish(const double* __restrict__ x, int64_t M,
                                                     const gnnshap::CgState* __restrict__ st,
                                                     const float* __restrict__ fef, float* __restrict__ phi,
-                                                    int32_t* info) {
+                                                    int32_t* info, int32_t undetermined) {
   __shared__ double red[16];
   double sm = 0.0;
   for (int64_t j = threadIdx.x; j < M; j += 1024) sm += x[j];
   const double mean = block_sum_d(sm, red) / static_cast<double>(M);
   const double base = (static_cast<double>(fef[1]) - static_cast<double>(fef[0])) / static_cast<double>(M);
   for (int64_t j = threadIdx.x; j < M; j += 1024) phi[j] = static_cast<float>(base + (x[j] - mean));
-  if (threadIdx.x == 0) *info = st->status == 0 ? 0 : static_cast<int32_t>(M + 1);
+  if (threadIdx.x == 0) *info = (st->status == 0 && !undetermined) ? 0 : static_cast<int32_t>(M + 1);
 }
 
 // Mapped page-locked stopping flag of the calling thread, its device address
@@ -537,7 +537,10 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
   if (iters_out) *iters_out = __atomic_load_n(hf->host + 1, __ATOMIC_ACQUIRE);
   {
     GS_TIMED("k_cg_finish", s);
-    k_cg_finish<<<1, 1024, 0, s>>>(w.x, sh.M, w.st, pr.fef, pr.phi, pr.info);
+    // without enumerated classes, fewer than M - 1 random rows cannot
+    // determine psi (1-perp has M - 1 dimensions): reported like a failed pivot
+    const int32_t undetermined = (pr.alpha == 0.0 && sh.kr < sh.M - 1) ? 1 : 0;
+    k_cg_finish<<<1, 1024, 0, s>>>(w.x, sh.M, w.st, pr.fef, pr.phi, pr.info, undetermined);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;

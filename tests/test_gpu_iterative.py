@@ -161,3 +161,21 @@ def test_iterative_through_explain_batch(dev, iterative_above):
                                   r.y.cpu().numpy().astype(np.float64), fef[0], fef[1])
         _phi_close(r.phi.cpu().numpy().astype(np.float64), phi_ref)
     assert saw_iterative
+
+
+def test_iterative_reports_undetermined_plan(dev, iterative_above):
+    """Fewer random rows than M - 1 and no enumerated class: the rows cannot
+    determine phi; the iterative path reports info = M + 1, as the
+    factorisation reports a failed pivot."""
+    M, p = 300, 200
+    plan, classes, masks, _ = sample_on_gpu(M, p, 31, 32)
+    kr = plan.num_rows // 2 - plan.random_begin
+    assert plan.random_begin == 0 and kr < M - 1
+    y = torch.randn(plan.num_rows, device=dev)
+    fef = torch.tensor([0.0, 1.0], dtype=torch.float32, device=dev)
+    iterative_above(M - 1)
+    _, info_it = _solve(dev, plan, classes, masks, y, fef)
+    assert info_it == M + 1
+    iterative_above(M + 1)
+    _, info_direct = _solve(dev, plan, classes, masks, y, fef)
+    assert info_direct > 0
