@@ -84,6 +84,7 @@ struct SolveJob {
   float* rv;                 // M: right-hand side, then z, then psi (panel path)
   int32_t panel;             // 1: the panel path, 0: one workgroup
   int32_t counts_in;         // 1: G~ is built from the counts as the panel path first reads each block
+  int64_t tr0;               // first transpose item (64 rows x 64 players) of the job in the batch
 };
 // Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
 bool solve_batchable(const gnnshap_sample_plan* plan);
@@ -94,7 +95,7 @@ int solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes
 // coalitions are evaluated), the right-hand side from the values, then G~
 // and the factorisations.
 int launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_nrb,
-                        hipStream_t s);
+                        int64_t n_items, hipStream_t s);
 // G~ in place of the counts for the jobs that do not build it as they read it
 // (after launch_solve_matrix).
 int launch_solve_build(const SolveJob* jobs, int64_t n, int64_t max_M, hipStream_t s);

@@ -358,6 +358,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
     grp[g].end = bound[g + 1];
   }
   int64_t nv = 0;
+  int64_t tr_items = 0;   // transpose items (64 rows x 64 players) of the batched systems
   for (Group& G : grp) {
     // 1. sampling jobs
     for (int64_t j = G.begin; j < G.end; ++j) {
@@ -420,6 +421,8 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       J.phi = phi + L.player_off[t];
       J.info = info + t;
       J.cls = b.classes + L.class_off[t];
+      J.tr0 = tr_items;
+      if (J.kr > 0) tr_items += J.nrb * J.wpr;
       G.bM = std::max(G.bM, J.M);
       G.bw = std::max(G.bw, J.wpr);
       G.bh = std::max(G.bh, J.half);
@@ -536,7 +539,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       // evaluations it gets the GPU before their many workgroups fill it
       int st = GNNSHAP_OK;
       if (mat) {
-        st = gnnshap::launch_solve_matrix(b.solve, nv, mM, mw, mnrb, mat->stream);
+        st = gnnshap::launch_solve_matrix(b.solve, nv, mM, mw, mnrb, tr_items, mat->stream);
         if (st == GNNSHAP_OK && hipEventRecord(mat->join, mat->stream) != hipSuccess)
           st = gnnshap::fail(GNNSHAP_EHIP, "hipEventRecord failed");
         if (st != GNNSHAP_OK) return st;

@@ -131,21 +131,31 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// T[rb, j]: transpose 64 rows x 64 players with ballots.  One wave per (rb, word).
+// One stage of the 64 x 64 bit-matrix transpose across a wavefront: lanes l
+// and l ^ S exchange S x S bit blocks (m selects the low S bits of every
+// 2S-bit group).
+template <int S>
+__device__ __forceinline__ uint64_t transpose_stage(uint64_t x, int lane, uint64_t m) {
+  const uint64_t p = __shfl_xor(static_cast<unsigned long long>(x), S);
+  return (lane & S) ? (((p >> S) & m) | (x & ~m)) : ((x & m) | ((p & m) << S));
+}
+
+// T[rb, j]: transpose 64 rows x 64 players, lane = row in, lane = player out,
+// in six exchange stages (blocks of 32, 16, ..., 1 bits).  One wave per (rb, word).
 __device__ __forceinline__ void transpose_body(const uint64_t* __restrict__ masks, int64_t wpr, int64_t row0,
                                                int64_t nrows, int64_t M, uint64_t* __restrict__ T, int64_t rb,
                                                int64_t w) {
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int64_t r = rb * 64 + lane;
-  const uint64_t word = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
-  uint64_t mine = 0;
-#pragma unroll 8
-  for (int p = 0; p < 64; ++p) {
-    const uint64_t bal = __ballot((word >> p) & 1);
-    if (lane == p) mine = bal;
-  }
+  uint64_t x = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
+  x = transpose_stage<32>(x, lane, 0x00000000FFFFFFFFull);
+  x = transpose_stage<16>(x, lane, 0x0000FFFF0000FFFFull);
+  x = transpose_stage<8>(x, lane, 0x00FF00FF00FF00FFull);
+  x = transpose_stage<4>(x, lane, 0x0F0F0F0F0F0F0F0Full);
+  x = transpose_stage<2>(x, lane, 0x3333333333333333ull);
+  x = transpose_stage<1>(x, lane, 0x5555555555555555ull);
   const int64_t j = w * 64 + lane;
-  if (j < M) T[rb * M + j] = mine;
+  if (j < M) T[rb * M + j] = x;
 }
 
 __global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ masks, int64_t wpr, int64_t row0,
@@ -1487,17 +1497,36 @@ double binom_d(int64_t n, int64_t r) {
 constexpr int64_t kGramChunk = 32;
 constexpr int64_t kGramWhole = 128;
 
-__global__ void __launch_bounds__(64) k_transpose_batch(const gnnshap::SolveJob* __restrict__ jobs) {
-  const gnnshap::SolveJob J = jobs[blockIdx.z];
-  if (J.kr <= 0 || blockIdx.x >= J.nrb || blockIdx.y >= J.wpr) return;
-  transpose_body(J.masks, J.wpr, J.rb0, J.kr, J.M, J.T, blockIdx.x, blockIdx.y);
-  if (blockIdx.x == 0 && blockIdx.y == 0)       // the Gram adds its row sums into usum
-    for (int64_t i = threadIdx.x; i < J.M; i += 64) J.usum[i] = 0;
+// One wavefront per transpose item of the batch (four per workgroup): item g
+// belongs to the job with the largest tr0 <= g (a wavefront-wide search of
+// the job table), as (row block, word) = divmod(g - tr0, wpr).
+constexpr int kTrWaves = 4;
+__global__ void __launch_bounds__(kTrWaves * 64) k_transpose_batch(const gnnshap::SolveJob* __restrict__ jobs,
+                                                                   int64_t n, int64_t n_items) {
+  const int lane = threadIdx.x & 63;
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kTrWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (g >= n_items) return;
+  int64_t lo = 0, hi = n;   // jobs[lo].tr0 <= g < jobs[hi].tr0 (jobs[n].tr0 = infinity)
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + 63) / 64;
+    const int64_t idx = lo + lane * step;
+    const bool ok = idx < hi && jobs[idx].tr0 <= g;
+    const uint64_t m = __ballot(ok);
+    const int64_t last = 63 - __clzll(static_cast<long long>(m));
+    lo += last * step;
+    hi = lo + step < hi ? lo + step : hi;
+  }
+  const gnnshap::SolveJob& J = jobs[lo];
+  const int64_t item = g - J.tr0;
+  const int64_t rb = item / J.wpr, w = item % J.wpr;
+  transpose_body(J.masks, J.wpr, J.rb0, J.kr, J.M, J.T, rb, w);
+  if (item == 0)       // the Gram adds its row sums into usum
+    for (int64_t i = lane; i < J.M; i += 64) J.usum[i] = 0;
   if (J.nrb <= kGramWhole) return;             // every count is stored by one workgroup
-  const int64_t nblk = J.nrb * J.wpr, blk = static_cast<int64_t>(blockIdx.x) * J.wpr + blockIdx.y;
+  const int64_t nblk = J.nrb * J.wpr;
   const int64_t total = J.M * J.ld, per = (total + nblk - 1) / nblk;
-  const int64_t e0 = blk * per, e1 = e0 + per < total ? e0 + per : total;
-  for (int64_t e = e0 + threadIdx.x; e < e1; e += 64) J.counts[e] = 0;
+  const int64_t e0 = item * per, e1 = e0 + per < total ? e0 + per : total;
+  for (int64_t e = e0 + lane; e < e1; e += 64) J.counts[e] = 0;
 }
 
 // Workgroup (tile, chunk, job): tile = J' (J' + 1) / 2 + I' over the tiles
@@ -2173,14 +2202,16 @@ bool gnnshap::solve_panel_path(const gnnshap_sample_plan* plan) {
 }
 
 int gnnshap::launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_nrb,
-                                 hipStream_t s) {
+                                 int64_t n_items, hipStream_t s) {
+  (void)max_wpr;
   if (n < 1) return GNNSHAP_OK;
   if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   const unsigned nn = static_cast<unsigned>(n);
-  if (max_nrb > 0) {
+  if (max_nrb > 0 && n_items > 0) {
+    if (ceil_div(n_items, kTrWaves) > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "transpose grid too large");
     {
       GS_TIMED("k_transpose_batch", s);
-      k_transpose_batch<<<dim3(static_cast<unsigned>(max_nrb), static_cast<unsigned>(max_wpr), nn), 64, 0, s>>>(jobs);
+      k_transpose_batch<<<static_cast<unsigned>(ceil_div(n_items, kTrWaves)), kTrWaves * 64, 0, s>>>(jobs, n, n_items);
     }
     GS_LAUNCHED();
     const int64_t nb = ceil_div(max_M, 64);
