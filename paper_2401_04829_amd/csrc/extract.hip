@@ -656,18 +656,18 @@ extern "C" int gnnshap_extract_batch_launch(const gnnshap_graph* g, const int64_
                          sg->dst_ptr, sg->edge_src, sg->edge_dst, sg->edge_gid};
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (int st = gnnshap::copy_by_kernel(b.jobs, jobs, static_cast<size_t>(n) * sizeof(ExtractJob), s)) return st;
-  GS_HIP(hipEventRecord(stage->done, s));
-  stage->pending = true;
+  // The kernel reads the job table straight from the coherent page-locked
+  // staging buffer (each wavefront reads its workgroup's job once) and writes
+  // the result rows straight into page-locked memory: no copy launches.
+  // Every workgroup writes all the counters the host reads back; only the
+  // per-target slices need to start at zero, and they reset themselves.
   {
     GS_TIMED("k_extract_batch", s);
-    k_extract_batch<<<static_cast<unsigned>(n), 1024, 0, s>>>(g->indptr, g->indices, nn, b.jobs, b.results);
+    k_extract_batch<<<static_cast<unsigned>(n), 1024, 0, s>>>(g->indptr, g->indices, nn, jobs, pe.host);
   }
   GS_LAUNCHED();
-  // The job table and result rows are rewritten by every call (each
-  // workgroup writes all the counters the host reads back); only the
-  // per-target slices need to start at zero, and they reset themselves.
-  if (int st = gnnshap::copy_by_kernel(pe.host, b.results, hbytes, s)) return st;
+  GS_HIP(hipEventRecord(stage->done, s));
+  stage->pending = true;
   GS_HIP(hipEventRecord(pe.ready, s));
   pe.n = n;
   pe.pending = true;
