@@ -271,7 +271,9 @@ def main():
             gat_times()
         return
     dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
     cfg = W.make_config(args.config)
+    print(f"workload {args.config}: inputs generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
     ex = Explainer(cfg["indptr"], cfg["indices"], cfg["X"], cfg["weights"], cfg["biases"], cfg["hops"], device=dev)
     targets = cfg["targets"]
 

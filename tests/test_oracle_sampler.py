@@ -152,3 +152,34 @@ def test_plan_rejects_bad_arguments():
         sampler.plan(10, 11)
     with pytest.raises(ValueError):
         sampler.plan(10, 0)
+
+
+@pytest.mark.parametrize("M,p", [(10, 1022), (11, 600), (12, 600), (20, 10000), (63, 2000), (64, 2000),
+                                 (65, 2000), (128, 1000), (129, 1000), (200, 4000)])
+def test_sample_rows_equals_rows_of_sample(M, p):
+    """sample_rows builds each requested row on its own (unranked subset,
+    Floyd subset or complement of its representative); the parity tests of
+    large targets use it as the reference for masks and weights.  Every row
+    it builds must equal the same row of the whole matrix from sample(),
+    which the tests above pin against eq. 3-6 and Alg. 2-3: enumerated
+    classes (the middle class of even M included), random classes, the
+    boundary between them, complement rows and rows whose players cross
+    uint64 word boundaries."""
+    seed, stream = 0x5EED0007 + M, 1000 + M
+    pl = sampler.plan(M, p)
+    masks, w = sampler.sample(pl, seed, stream)
+    k, half, rb = pl["k"], pl["half"], pl["random_begin"]
+    rng = np.random.Generator(np.random.PCG64(M * 7919 + p))
+    edges = {0, max(rb - 1, 0), rb, half - 1, half, min(half + rb, k - 1), k - 1}
+    rows = np.unique(np.concatenate([np.fromiter((r for r in edges if 0 <= r < k), dtype=np.int64),
+                                     rng.integers(0, k, size=min(k, 64))]))
+    got, gw = sampler.sample_rows(pl, rows, seed, stream)
+    np.testing.assert_array_equal(got, masks[rows])
+    np.testing.assert_array_equal(gw, w[rows])
+    # the packed form of the selected rows is the packed form of the matrix rows
+    np.testing.assert_array_equal(sampler.pack(got), sampler.pack(masks)[rows])
+    kinds = {bool(cl["full"]) for cl in pl["classes"]}
+    if M in (10, 12, 20):
+        assert True in kinds              # enumerated classes are covered
+    if M >= 11:
+        assert False in kinds             # random classes are covered
