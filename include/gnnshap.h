@@ -217,6 +217,21 @@ int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m,
                             float* f_empty_full, int32_t* class_out,
                             void* ws, size_t ws_bytes, void* stream);
 
+/* gnnshap_eval_coalitions for masks in the sampler's layout (Alg. 2 pairs
+ * each sampled coalition with its complement, App. C.1): k is even and row
+ * b + k/2 is the complement of row b within the M player bits for every
+ * b < k/2, as gnnshap_sample_coalitions writes them (the call relies on it
+ * and does not check it).  Same arguments, workspace and errors as
+ * gnnshap_eval_coalitions (EINVAL also for odd k).  Two-layer models with a
+ * wide hidden layer then contract only the first half of the rows: the
+ * complement's masked sum is the sum over all players minus the row's. */
+int gnnshap_eval_sampled_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m,
+                                    const float* X, int32_t target_class,
+                                    const uint64_t* masks, int64_t k,
+                                    int64_t words_per_row, float* y,
+                                    float* f_empty_full, int32_t* class_out,
+                                    void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* 4. Constrained Kernel-SHAP least squares (eq. 2-3, Alg. 1, Sec. 3.5).    */
 /*                                                                          */

@@ -66,6 +66,9 @@ _SIGNATURES = {
                                               _P(ctypes.c_size_t)]),
     "gnnshap_eval_coalitions": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp,
                                                c_i64, c_i64, c_vp, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_eval_sampled_coalitions": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp,
+                                                       c_i64, c_i64, c_vp, c_vp, c_vp, c_vp, ctypes.c_size_t,
+                                                       c_vp]),
     "gnnshap_transform_features": (ctypes.c_int, [c_vp, c_i64, c_i32, c_vp, c_i32, c_vp, c_vp]),
     "gnnshap_solve_workspace": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(ctypes.c_size_t)]),
     "gnnshap_solve_wls": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(gnnshap_class), c_vp, c_vp, c_vp, c_vp,
@@ -187,6 +190,13 @@ def gnnshap_eval_coalitions(sg, model, X_ptr, target_class, masks_ptr, k, wpr, y
                             ws_bytes, stream):
     check(load().gnnshap_eval_coalitions(ctypes.byref(sg), ctypes.byref(model), X_ptr, target_class, masks_ptr, k,
                                          wpr, y_ptr, fef_ptr, cls_ptr, ws_ptr, ws_bytes, stream), "eval_coalitions")
+
+
+def gnnshap_eval_sampled_coalitions(sg, model, X_ptr, target_class, masks_ptr, k, wpr, y_ptr, fef_ptr, cls_ptr,
+                                    ws_ptr, ws_bytes, stream):
+    check(load().gnnshap_eval_sampled_coalitions(ctypes.byref(sg), ctypes.byref(model), X_ptr, target_class,
+                                                 masks_ptr, k, wpr, y_ptr, fef_ptr, cls_ptr, ws_ptr, ws_bytes,
+                                                 stream), "eval_sampled_coalitions")
 
 
 def gnnshap_transform_features(X_ptr, n, d, W_ptr, h, Z_ptr, stream):

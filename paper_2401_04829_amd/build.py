@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libgnnshap.so")
 
-HIP_SOURCES = ["extract.hip", "sample.hip", "eval.hip", "solve.hip", "cg.hip", "fidelity.hip", "gat.hip", "batch.hip", "timing.hip"]
+HIP_SOURCES = ["extract.hip", "sample.hip", "eval.hip", "eval_wide.hip", "solve.hip", "cg.hip", "fidelity.hip", "gat.hip", "batch.hip", "timing.hip"]
 HOST_SOURCES = ["plan.cpp", "status.cpp"]
 ARCH = "gfx950"
 

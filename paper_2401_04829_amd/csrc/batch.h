@@ -51,6 +51,11 @@ struct EvalModel {
   int h, C;
   int32_t target_class;
 };
+// gnnshap_eval_coalitions for masks in the sampler's layout (pairs = rows b
+// and b + k/2 are complements; some paths then contract half of the rows).
+int eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X, int32_t target_class,
+                         const uint64_t* masks, int64_t k, int64_t words_per_row, float* y, float* f_empty_full,
+                         int32_t* class_out, void* ws, size_t ws_bytes, void* stream, bool pairs);
 // Whether one target can go through the batched evaluation, and the bytes of
 // its workspace slice.
 bool eval_batchable(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k);

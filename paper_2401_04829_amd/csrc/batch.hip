@@ -495,10 +495,10 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
           for (int64_t j = G.begin; j < G.end; ++j) {
             const int64_t t = order[j];
             const gnnshap_sample_plan& p = plans[t];
-            if (int st = gnnshap_eval_coalitions(&sgs[t], model, X, target_class, masks + L.mask_off[t], p.num_rows,
-                                                 p.words_per_row, y + L.row_off[t], f_empty_full + 2 * t,
-                                                 class_out ? class_out + t : nullptr, b.eval_slice[t], L.eval_bytes[t],
-                                                 gs[gi]))
+            if (int st = gnnshap::eval_coalitions_impl(&sgs[t], model, X, target_class, masks + L.mask_off[t],
+                                                       p.num_rows, p.words_per_row, y + L.row_off[t],
+                                                       f_empty_full + 2 * t, class_out ? class_out + t : nullptr,
+                                                       b.eval_slice[t], L.eval_bytes[t], gs[gi], true))
               return st;
           }
         }

@@ -20,6 +20,7 @@
 // rows (no players / all players) run through the same kernels first.
 #include "batch.h"
 #include "common.h"
+#include "wide.h"
 
 namespace {
 
@@ -35,6 +36,8 @@ struct Shape {
   bool bnd[GNNSHAP_MAX_LAYERS + 1] = {};    // H^j is needed at the boundary rows
   int64_t tile = 0;                          // coalitions per pass
   int64_t k = 0, wpr = 0;
+  bool wide = false;                         // two layers, two hops, wide hidden layer: eval_wide.hip
+  gnnshap::WideShape ws;
 };
 
 struct Ws {
@@ -49,6 +52,7 @@ struct Ws {
   float* dinv;                        // tile x n_dst
   float* Hb[GNNSHAP_MAX_LAYERS + 1];  // tile x nd[j] x dims[j]
   float* Zb[GNNSHAP_MAX_LAYERS + 1];  // tile x nd[j-1] x dims[j]
+  gnnshap::WideWs wide;               // the wide path's arrays (Shape::wide)
 };
 
 int64_t per_row_bytes(const Shape& s) {
@@ -76,6 +80,7 @@ Ws carve(gnnshap::Carver& c, const Shape& s) {
   w.dinv = c.take<float>(s.tile * s.n_dst);
   for (int j = 1; j < s.L; ++j) w.Hb[j] = c.take<float>(s.tile * s.nd[j] * s.dims[j]);
   for (int j = 2; j < s.L; ++j) w.Zb[j] = c.take<float>(s.tile * s.nd[j - 1] * s.dims[j]);
+  if (s.wide) w.wide = gnnshap::wide_carve(c, s.ws);
   return w;
 }
 
@@ -112,6 +117,13 @@ int make_shape(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, Shap
   else if (t >= kTB) t -= t % kTB;
   if (t < 2) t = 2;
   s.tile = t;
+  // The wide path evaluates every row in one launch sequence of its own; the
+  // per-pass arrays above then serve the two end coalitions only.
+  s.wide = gnnshap::wide_applies(s.L, s.hops, s.dims[1]) && s.n_dst == sg->hop_ptr[2];
+  if (s.wide) {
+    s.tile = 2;
+    s.ws = gnnshap::wide_shape(sg->num_edges, s.n_nodes, s.n_dst, k, s.dims[1], s.dims[s.L]);
+  }
   *out = s;
   return GNNSHAP_OK;
 }
@@ -1591,10 +1603,12 @@ extern "C" int gnnshap_eval_workspace(const gnnshap_subgraph* sg, const gnnshap_
   return GNNSHAP_OK;
 }
 
-extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X,
-                                       int32_t target_class, const uint64_t* masks, int64_t k,
-                                       int64_t words_per_row, float* y, float* f_empty_full,
-                                       int32_t* class_out, void* ws, size_t ws_bytes, void* stream) {
+// gnnshap_eval_coalitions; pairs: rows b and b + k/2 are complements (the
+// sampler's layout), which the wide path uses to contract half of the rows.
+int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X,
+                                  int32_t target_class, const uint64_t* masks, int64_t k, int64_t words_per_row,
+                                  float* y, float* f_empty_full, int32_t* class_out, void* ws, size_t ws_bytes,
+                                  void* stream, bool pairs) {
   GS_TRY_BEGIN
   gnnshap::clear_error();
   if (k < 1) return gnnshap::fail(GNNSHAP_EINVAL, "k must be >= 1");
@@ -1684,6 +1698,9 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
     k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
     GS_LAUNCHED();
   }
+  if (sh.wide)
+    return gnnshap::launch_wide(sh.ws, w.wide, sg, masks, sh.wpr, w.Zc[1], m->b ? m->b[0] : nullptr, m->W[1],
+                                m->b ? m->b[1] : nullptr, w.ctl, f_empty_full, pairs, y, s);
   // Prediction pruning, then the live coalitions in passes of sh.tile rows.
   k_live<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(masks, sh.wpr, k, sg->dst_ptr, w.ctl, w.live_rows,
                                                          w.live_flag);
@@ -1696,6 +1713,23 @@ extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap
   GS_LAUNCHED();
   return GNNSHAP_OK;
   GS_TRY_END
+}
+
+extern "C" int gnnshap_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X,
+                                       int32_t target_class, const uint64_t* masks, int64_t k,
+                                       int64_t words_per_row, float* y, float* f_empty_full,
+                                       int32_t* class_out, void* ws, size_t ws_bytes, void* stream) {
+  return gnnshap::eval_coalitions_impl(sg, m, X, target_class, masks, k, words_per_row, y, f_empty_full, class_out,
+                                       ws, ws_bytes, stream, false);
+}
+
+extern "C" int gnnshap_eval_sampled_coalitions(const gnnshap_subgraph* sg, const gnnshap_gcn* m, const float* X,
+                                               int32_t target_class, const uint64_t* masks, int64_t k,
+                                               int64_t words_per_row, float* y, float* f_empty_full,
+                                               int32_t* class_out, void* ws, size_t ws_bytes, void* stream) {
+  if (k % 2) return gnnshap::fail(GNNSHAP_EINVAL, "sampled coalitions come in complement pairs: k must be even");
+  return gnnshap::eval_coalitions_impl(sg, m, X, target_class, masks, k, words_per_row, y, f_empty_full, class_out,
+                                       ws, ws_bytes, stream, true);
 }
 
 extern "C" int gnnshap_transform_features(const float* X, int64_t n, int32_t d, const float* W, int32_t h, float* Z,

@@ -1,0 +1,465 @@
+// Coalition values of a two-layer GCN with a wide hidden layer, on fp32 MFMA
+// (Sec. 3.4 of the GNNShap paper; the GCN of Sec. 4.2).
+//
+// With two hops, H_1 = {v} and v's in-neighbours are the only nodes that
+// players enter.  Under coalition c, layer 1 at x in H_1 is
+//   H^1_c[x] = relu( d_c(x)^-1/2 ( sum_{e -> x, e in c} d_c(src e)^-1/2 Z[src e] + d_c(x)^-1/2 Z[x] ) + b_1 ),
+// Z = X W_1, d = 1 + in-degree under c; y_c = H^2_c[v, class] is
+//   d_c(v)^-1/2 ( sum_{e -> v, e in c} d_c(src e)^-1/2 t_c[src e] + d_c(v)^-1/2 t_c[v] ) + b_2,
+// t_c[x] = H^1_c[x] . W_2[:, class].
+// A source outside H_1 has no players entering it, so its degree is 1 under
+// every coalition: for those players the sum is a 0/1 contraction
+//   D_c[f] = sum_e [e in c] Z[src e][f],
+// a (features x players) x (players x coalitions) product with the mask bits
+// as the right operand, run here on v_mfma_f32_16x16x4f32.  The few players
+// whose source lies in H_1 (the in-edges of v, the edge v -> x, edges between
+// in-neighbours) carry a coalition-dependent d^-1/2 and are added in the
+// epilogue.  For the sampler's complement pairs (row b + k/2 = NOT row b),
+// D of the complement is S - D_c with S the sum over all those players, so
+// only the first half of the rows is contracted.
+//
+// Kernels, per target:
+//   k_wide_prep  one workgroup: operand-unit offsets of each node and the
+//                list of players whose source is in H_1
+//   k_wide_zop   the A operands: for 16 players (one unit) and 16 features
+//                (one tile), lane (r, g) of a wavefront holds Z[src][f] for
+//                feature 16 tile + r and players 4 s + g, s = 0..3, as one
+//                float4 (zero for padding and for the players above)
+//   k_wide_sum   S (pairs only): per node and feature, fixed summation order
+//   k_wide_deg   in-degree of every node of H_1 under every contracted row
+//   k_wide_l1    one workgroup per (node, 256 coalitions, 128 features):
+//                four wavefronts of 64 coalitions, 4 x 8 16x16 output tiles
+//                each; then the epilogue to t_c[x] (and the complement's)
+//   k_wide_out   y per row from t, the degrees and the mask bits of v's in-edges
+#include "wide.h"
+
+namespace {
+
+typedef float mx4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;                      // wavefronts per workgroup
+constexpr int kWaveRows = 64;                  // coalitions per wavefront (four tiles of 16)
+constexpr int kBlockRows = kWaves * kWaveRows;
+constexpr int kTiles = 8;                      // 16-feature tiles per workgroup
+constexpr int kUnit = 16;                      // players per operand unit (four MFMA steps of four)
+
+__global__ void __launch_bounds__(1024) k_wide_prep(const int32_t* __restrict__ dst_ptr,
+                                                    const int32_t* __restrict__ edge_src, int64_t n1,
+                                                    int32_t* __restrict__ seg, int32_t* __restrict__ spec_ptr,
+                                                    int32_t* __restrict__ spec_e) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nwaves = blockDim.x >> 6;
+  // counts: one wavefront per node
+  for (int64_t x = wave; x < n1; x += nwaves) {
+    const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+    int cnt = 0;
+    for (int b = e0; b < e1; b += 64) {
+      const int e = b + lane;
+      const bool sp = e < e1 && edge_src[e] < n1;
+      cnt += __popcll(__ballot(sp));
+    }
+    if (lane == 0) {
+      spec_ptr[x + 1] = cnt;
+      seg[x + 1] = (e1 - e0 + kUnit - 1) / kUnit;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    seg[0] = 0;
+    spec_ptr[0] = 0;
+    for (int64_t x = 0; x < n1; ++x) {
+      seg[x + 1] += seg[x];
+      spec_ptr[x + 1] += spec_ptr[x];
+    }
+  }
+  __syncthreads();
+  // lists in player order
+  for (int64_t x = wave; x < n1; x += nwaves) {
+    const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+    int out = spec_ptr[x];
+    for (int b = e0; b < e1; b += 64) {
+      const int e = b + lane;
+      const bool sp = e < e1 && edge_src[e] < n1;
+      const uint64_t m = __ballot(sp);
+      if (sp) spec_e[out + __popcll(m & ((uint64_t(1) << lane) - 1))] = e;
+      out += __popcll(m);
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) k_wide_zop(const int32_t* __restrict__ dst_ptr,
+                                                  const int32_t* __restrict__ edge_src, int64_t n1,
+                                                  const int32_t* __restrict__ seg, const float* __restrict__ Zc, int h,
+                                                  int ntot, int64_t units_cap, float4* __restrict__ Zop) {
+  const int64_t units = seg[n1];
+  const int64_t total = units * ntot * 64;
+  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    const int lane = static_cast<int>(idx & 63);
+    const int64_t rest = idx >> 6;
+    const int ft = static_cast<int>(rest % ntot);
+    const int64_t U = rest / ntot;
+    if (U >= units_cap) break;
+    int64_t lo = 0, hi = n1;                    // node x with seg[x] <= U < seg[x + 1]
+    while (hi - lo > 1) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (seg[mid] <= U) lo = mid;
+      else hi = mid;
+    }
+    const int64_t x = lo;
+    const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+    const int base = e0 + static_cast<int>(U - seg[x]) * kUnit;
+    const int f = 16 * ft + (lane & 15), g = lane >> 4;
+    float v[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int e = base + 4 * s + g;
+      const int32_t u = e < e1 ? edge_src[e] : 0;
+      v[s] = (e < e1 && u >= n1) ? Zc[static_cast<int64_t>(u) * h + f] : 0.f;
+    }
+    Zop[idx] = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
+// S[x][f] = sum of Z[src e][f] over the players e -> x whose source is not in
+// H_1: thread (j, r) of the workgroup sums the players j, j + 16, ... for
+// feature 16 tile + r, then the 16 partial sums are added in a fixed tree.
+__global__ void __launch_bounds__(256) k_wide_sum(const int32_t* __restrict__ dst_ptr,
+                                                  const int32_t* __restrict__ edge_src, int64_t n1,
+                                                  const float* __restrict__ Zc, int h, int ntot,
+                                                  float* __restrict__ S) {
+  __shared__ float part[16][17];
+  const int64_t x = blockIdx.x / ntot;
+  const int ft = static_cast<int>(blockIdx.x % ntot);
+  const int r = threadIdx.x & 15, j = threadIdx.x >> 4;
+  const int f = 16 * ft + r;
+  const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+  float acc = 0.f;
+  for (int e = e0 + j; e < e1; e += 16) {
+    const int32_t u = edge_src[e];
+    if (u >= n1) acc += Zc[static_cast<int64_t>(u) * h + f];
+  }
+  part[j][r] = acc;
+  __syncthreads();
+  for (int w = 8; w >= 1; w >>= 1) {
+    if (j < w) part[j][r] += part[j + w][r];
+    __syncthreads();
+  }
+  if (j == 0) S[x * h + f] = part[0][r];
+}
+
+// deg[b][x] = number of row b's players entering x, b < nrows, x < n1.
+__global__ void __launch_bounds__(256) k_wide_deg(const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows,
+                                                  const int32_t* __restrict__ dst_ptr, int64_t n1,
+                                                  int32_t* __restrict__ deg) {
+  const int64_t total = nrows * n1;
+  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t b = idx / n1, x = idx % n1;
+    const uint64_t* mr = masks + b * wpr;
+    const int64_t e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+    int cnt = 0;
+    for (int64_t w = e0 >> 6; e1 > e0 && w <= ((e1 - 1) >> 6); ++w) {
+      uint64_t word = mr[w];
+      const int64_t lo = w * 64;
+      if (e0 > lo) word &= ~uint64_t(0) << (e0 - lo);
+      if (e1 < lo + 64) word &= (uint64_t(1) << (e1 - lo)) - 1;
+      cnt += __popcll(word);
+    }
+    deg[idx] = cnt;
+  }
+}
+
+// Layer 1 at node x = blockIdx.x / cblocks for 256 coalitions (block
+// blockIdx.x % cblocks) and features 128 blockIdx.y .. + 127.  Wavefront w
+// holds rows c0 .. c0 + 63, c0 = 256 block + 64 w, as four 16-row tiles;
+// lane (r, g) = (lane % 16, lane / 16) holds, per tile ct and feature tile
+// ft, features 16 ft + 4 g .. + 3 of row c0 + 16 ct + r.  Writes
+// t[fb][row][x] for the row and, with pairs, for row + khalf.
+template <bool PAIRS>
+__global__ void __launch_bounds__(kBlockRows) k_wide_l1(
+    const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows, int64_t khalf, int64_t cblocks,
+    const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src, int64_t n1,
+    const int32_t* __restrict__ seg, const float4* __restrict__ Zop, int ntot, int h, const float* __restrict__ Zc,
+    const float* __restrict__ S, const int32_t* __restrict__ spec_ptr, const int32_t* __restrict__ spec_e,
+    const int32_t* __restrict__ deg, const float* __restrict__ b1, const float* __restrict__ W2, int C,
+    const int32_t* __restrict__ ctl, float* __restrict__ t, int64_t k) {
+  const int64_t x = blockIdx.x / cblocks;
+  const int64_t cb = blockIdx.x % cblocks;
+  const int fb = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rl = lane & 15, g = lane >> 4;
+  const int64_t c0 = cb * kBlockRows + wave * kWaveRows;
+  if (c0 >= nrows) return;                       // no barrier in this kernel
+  const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+  const int u0 = seg[x], nu = seg[x + 1] - u0;
+  const int ft0 = fb * kTiles;
+  const int nt = ntot - ft0 < kTiles ? ntot - ft0 : kTiles;
+
+  int64_t row[4];
+  bool valid[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    row[ct] = c0 + 16 * ct + rl;
+    valid[ct] = row[ct] < nrows;
+  }
+  mx4_t D[4][kTiles];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int ft = 0; ft < kTiles; ++ft) D[ct][ft] = mx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int64_t ustride = static_cast<int64_t>(ntot) * 64;
+  const float4* zp = Zop + static_cast<int64_t>(u0) * ustride + ft0 * 64 + lane;
+  float4 a[kTiles], an[kTiles];
+#pragma unroll
+  for (int ft = 0; ft < kTiles; ++ft)
+    a[ft] = (ft < nt && nu > 0) ? zp[ft * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
+  uint64_t win[4] = {0, 0, 0, 0};
+  for (int q = 0; q < nu; ++q) {
+    if ((q & 3) == 0) {                          // the mask bits of the next 64 players
+      const int64_t pb = e0 + static_cast<int64_t>(kUnit) * q;
+      const int64_t wa = pb >> 6;
+      const int sh = static_cast<int>(pb & 63);
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        uint64_t w = 0;
+        if (valid[ct]) {
+          const uint64_t* mr = masks + row[ct] * wpr;
+          const uint64_t lo = mr[wa];
+          const uint64_t hi = (sh && wa + 1 < wpr) ? mr[wa + 1] : 0;
+          w = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+        }
+        win[ct] = w;
+      }
+    }
+    // next unit's operands while this unit is multiplied
+    const bool more = q + 1 < nu;
+#pragma unroll
+    for (int ft = 0; ft < kTiles; ++ft)
+      an[ft] = (ft < nt && more) ? zp[(q + 1) * ustride + ft * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
+    uint32_t part[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) part[ct] = static_cast<uint32_t>(win[ct] >> (16 * (q & 3)));
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        const float bv = ((part[ct] >> (4 * s + g)) & 1u) ? 1.0f : 0.0f;
+#pragma unroll
+        for (int ft = 0; ft < kTiles; ++ft) {
+          if (ft < nt) {
+            const float av = s == 0 ? a[ft].x : s == 1 ? a[ft].y : s == 2 ? a[ft].z : a[ft].w;
+            D[ct][ft] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, D[ct][ft], 0, 0, 0);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int ft = 0; ft < kTiles; ++ft) a[ft] = an[ft];
+  }
+
+  // epilogue: the players whose source is in H_1, self loop, bias, ReLU and
+  // the explained class's column of W_2, per row (and its complement)
+  const int cls = ctl[0];
+  const int nx = e1 - e0;
+  const int sp0 = spec_ptr[x], sp1 = spec_ptr[x + 1];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    const int64_t rr = valid[ct] ? row[ct] : 0;
+    const int32_t* dg = deg + rr * n1;
+    const uint64_t* mr = masks + rr * wpr;
+    const int dgx = dg[x];
+    const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dgx));
+    const float dxp = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(nx - dgx));
+    float tc = 0.f, tcp = 0.f;
+#pragma unroll
+    for (int ft = 0; ft < kTiles; ++ft) {
+      if (ft >= nt) continue;
+      const int f = 16 * (ft0 + ft) + 4 * g;
+      float av[4] = {D[ct][ft][0], D[ct][ft][1], D[ct][ft][2], D[ct][ft][3]};
+      float ap[4] = {0.f, 0.f, 0.f, 0.f};
+      if (PAIRS) {
+        const float4 s4 = *reinterpret_cast<const float4*>(S + x * h + f);
+        ap[0] = s4.x - av[0];
+        ap[1] = s4.y - av[1];
+        ap[2] = s4.z - av[2];
+        ap[3] = s4.w - av[3];
+      }
+      for (int sp = sp0; sp < sp1; ++sp) {
+        const int e = spec_e[sp];
+        const int32_t u = edge_src[e];
+        const bool bit = (mr[e >> 6] >> (e & 63)) & 1;
+        const int du = dg[u];
+        const float4 zu = *reinterpret_cast<const float4*>(Zc + static_cast<int64_t>(u) * h + f);
+        if (bit) {
+          const float cu = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(du));
+          av[0] = fmaf(cu, zu.x, av[0]);
+          av[1] = fmaf(cu, zu.y, av[1]);
+          av[2] = fmaf(cu, zu.z, av[2]);
+          av[3] = fmaf(cu, zu.w, av[3]);
+        } else if (PAIRS) {
+          const int nuu = dst_ptr[u + 1] - dst_ptr[u];
+          const float cu = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(nuu - du));
+          ap[0] = fmaf(cu, zu.x, ap[0]);
+          ap[1] = fmaf(cu, zu.y, ap[1]);
+          ap[2] = fmaf(cu, zu.z, ap[2]);
+          ap[3] = fmaf(cu, zu.w, ap[3]);
+        }
+      }
+      const float4 zx = *reinterpret_cast<const float4*>(Zc + x * h + f);
+      const float zxv[4] = {zx.x, zx.y, zx.z, zx.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float bb = b1 ? b1[f + i] : 0.f;
+        const float ww = W2[static_cast<int64_t>(f + i) * C + cls];
+        tc = fmaf(fmaxf(fmaf(dx, fmaf(dx, zxv[i], av[i]), bb), 0.f), ww, tc);
+        if (PAIRS) tcp = fmaf(fmaxf(fmaf(dxp, fmaf(dxp, zxv[i], ap[i]), bb), 0.f), ww, tcp);
+      }
+    }
+    tc += __shfl_xor(tc, 16);
+    tc += __shfl_xor(tc, 32);
+    if (PAIRS) {
+      tcp += __shfl_xor(tcp, 16);
+      tcp += __shfl_xor(tcp, 32);
+    }
+    if (valid[ct] && g == 0) {
+      t[(static_cast<int64_t>(fb) * k + row[ct]) * n1 + x] = tc;
+      if (PAIRS) t[(static_cast<int64_t>(fb) * k + row[ct] + khalf) * n1 + x] = tcp;
+    }
+  }
+}
+
+// y of row b (b < nrows) and, with pairs, of its complement b + khalf.
+// Node x >= 1 of H_1 is the source of the target's player x - 1 (the
+// extraction orders both by global id).
+template <bool PAIRS>
+__global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows,
+                                                  int64_t khalf, const int32_t* __restrict__ dst_ptr, int64_t n1,
+                                                  const int32_t* __restrict__ deg, const float* __restrict__ t,
+                                                  int nfb, int64_t k, const float* __restrict__ b2,
+                                                  const int32_t* __restrict__ ctl, const float* __restrict__ fef,
+                                                  float* __restrict__ y) {
+  const int64_t b = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (b >= nrows) return;
+  const int cls = ctl[0];
+  const float bias = b2 ? b2[cls] : 0.f;
+  const uint64_t* mr = masks + b * wpr;
+  const int32_t* dg = deg + b * n1;
+  auto tval = [&](int64_t r, int64_t x) {
+    float s = 0.f;
+    for (int fb = 0; fb < nfb; ++fb) s += t[(static_cast<int64_t>(fb) * k + r) * n1 + x];
+    return s;
+  };
+  {
+    const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dg[0]));
+    float acc = dv * tval(b, 0);
+    bool live = false;
+    for (int64_t x = 1; x < n1; ++x) {
+      const int64_t p = x - 1;
+      if ((mr[p >> 6] >> (p & 63)) & 1) {
+        live = true;
+        acc = fmaf(__builtin_amdgcn_rsqf(1.0f + static_cast<float>(dg[x])), tval(b, x), acc);
+      }
+    }
+    y[b] = live ? fmaf(dv, acc, bias) : fef[0];
+  }
+  if (PAIRS) {
+    const int64_t bc = b + khalf;
+    const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>((dst_ptr[1] - dst_ptr[0]) - dg[0]));
+    float acc = dv * tval(bc, 0);
+    bool live = false;
+    for (int64_t x = 1; x < n1; ++x) {
+      const int64_t p = x - 1;
+      if (!((mr[p >> 6] >> (p & 63)) & 1)) {
+        live = true;
+        const int nxx = dst_ptr[x + 1] - dst_ptr[x];
+        acc = fmaf(__builtin_amdgcn_rsqf(1.0f + static_cast<float>(nxx - dg[x])), tval(bc, x), acc);
+      }
+    }
+    y[bc] = live ? fmaf(dv, acc, bias) : fef[0];
+  }
+}
+
+}  // namespace
+
+namespace gnnshap {
+
+bool wide_applies(int num_layers, int num_hops, int h) {
+  return num_layers == 2 && num_hops == 2 && h > 32 && h % 16 == 0 && h <= 4096;
+}
+
+WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t k, int h, int C) {
+  WideShape s;
+  s.M = M;
+  s.n_nodes = n_nodes;
+  s.n1 = n1;
+  s.k = k;
+  s.h = h;
+  s.C = C;
+  s.ntot = h / 16;
+  s.nfb = static_cast<int>(ceil_div(s.ntot, kTiles));
+  s.units_cap = ceil_div(M, kUnit) + n1;
+  return s;
+}
+
+WideWs wide_carve(Carver& c, const WideShape& s) {
+  WideWs w{};
+  w.seg = c.take<int32_t>(s.n1 + 1);
+  w.spec_ptr = c.take<int32_t>(s.n1 + 1);
+  w.spec_e = c.take<int32_t>(s.M);
+  w.Zop = c.take<float4>(s.units_cap * s.ntot * 64);
+  w.S = c.take<float>(s.n1 * s.h);
+  w.deg = c.take<int32_t>(s.k * s.n1);
+  w.t = c.take<float>(static_cast<int64_t>(s.nfb) * s.k * s.n1);
+  return w;
+}
+
+int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr,
+                const float* Zc, const float* b1, const float* W2, const float* b2, const int32_t* ctl,
+                const float* fef, bool pairs, float* y, hipStream_t st) {
+  if (pairs && (s.k & 1)) return fail(GNNSHAP_EINVAL, "complement pairs need an even number of rows");
+  const int64_t nrows = pairs ? s.k / 2 : s.k;
+  const int64_t khalf = pairs ? s.k / 2 : 0;
+  const int64_t cblocks = ceil_div(nrows, kBlockRows);
+  if (s.n1 * cblocks > INT32_MAX || s.nfb > 65535) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
+  if (s.n1 > INT32_MAX / 2 || s.M > INT32_MAX / 2) return fail(GNNSHAP_EUNSUPPORTED, "subgraph too large");
+  k_wide_prep<<<1, 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, w.seg, w.spec_ptr, w.spec_e);
+  GS_LAUNCHED();
+  k_wide_zop<<<grid_for(s.units_cap * s.ntot * 64, 256, 16384), 256, 0, st>>>(
+      sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc, s.h, s.ntot, s.units_cap, w.Zop);
+  GS_LAUNCHED();
+  if (pairs) {
+    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot), 256, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h,
+                                                                     s.ntot, w.S);
+    GS_LAUNCHED();
+  }
+  k_wide_deg<<<grid_for(nrows * s.n1, 256, 16384), 256, 0, st>>>(masks, wpr, nrows, sg->dst_ptr, s.n1, w.deg);
+  GS_LAUNCHED();
+  {
+    const dim3 grid(static_cast<unsigned>(s.n1 * cblocks), static_cast<unsigned>(s.nfb));
+    GS_TIMED("k_wide_l1", st);
+    if (pairs)
+      k_wide_l1<true><<<grid, kBlockRows, 0, st>>>(masks, wpr, nrows, khalf, cblocks, sg->dst_ptr, sg->edge_src,
+                                                   s.n1, w.seg, w.Zop, s.ntot, s.h, Zc, w.S, w.spec_ptr, w.spec_e,
+                                                   w.deg, b1, W2, s.C, ctl, w.t, s.k);
+    else
+      k_wide_l1<false><<<grid, kBlockRows, 0, st>>>(masks, wpr, nrows, khalf, cblocks, sg->dst_ptr, sg->edge_src,
+                                                    s.n1, w.seg, w.Zop, s.ntot, s.h, Zc, w.S, w.spec_ptr, w.spec_e,
+                                                    w.deg, b1, W2, s.C, ctl, w.t, s.k);
+  }
+  GS_LAUNCHED();
+  {
+    const unsigned g = static_cast<unsigned>(ceil_div(nrows, 256));
+    GS_TIMED("k_wide_out", st);
+    if (pairs)
+      k_wide_out<true><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, s.nfb, s.k, b2,
+                                          ctl, fef, y);
+    else
+      k_wide_out<false><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, s.nfb, s.k, b2,
+                                           ctl, fef, y);
+  }
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+}  // namespace gnnshap

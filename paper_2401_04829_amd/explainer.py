@@ -216,10 +216,11 @@ class Explainer:
                            f_empty_full=fef, cls=cls, phi=phi, info=info)
 
     def _evaluate(self, sub, target_class, masks, k, wpr, y, fef, cls, ws_eval, s):
-        """gnnshap_eval_coalitions on the current stream."""
+        """gnnshap_eval_sampled_coalitions (the masks come from the sampler) on
+        the current stream."""
         ws = ws_eval.get(L.gnnshap_eval_workspace(sub.sg, self.model, k))
-        L.gnnshap_eval_coalitions(sub.sg, self.model, _vp(self.X), int(target_class), _vp(masks), k, wpr, _vp(y),
-                                  _vp(fef), _vp(cls), _vp(ws), ws.numel(), s)
+        L.gnnshap_eval_sampled_coalitions(sub.sg, self.model, _vp(self.X), int(target_class), _vp(masks), k, wpr,
+                                          _vp(y), _vp(fef), _vp(cls), _vp(ws), ws.numel(), s)
 
     # -- many targets per launch sequence ------------------------------------------------------
 
