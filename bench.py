@@ -1,15 +1,17 @@
 """Benchmark of the GNNShap hot path on one MI355X.
 
-One step = Alg. 1 for every target of the Cora-shaped workload (2,708 nodes,
-10,556 directed edges, 2-layer GCN 16 hidden / 7 classes, 100 targets with
-20..400 players, 10,000 coalitions each): X W_1, extract the computational
-graphs, plan, sample, evaluate every coalition, solve the least squares.  By
-default the whole batch of targets goes through one launch per step
-(gnnshap_extract_batch_launch/_finish + gnnshap_explain_batch), the steps
-pipelined: each step's extraction is queued before the previous step's
-explanation.  --mode streams runs the single-target calls on several
-streams instead.  Inputs (graph, features, weights) are resident in HBM
-before the timed region.
+One step = Alg. 1 for every target of the Reddit-shaped workload by default
+(232,965 nodes, 114.6M directed edges, 602-dim features, 2-layer GCN 128
+hidden / 41 classes, 20 targets with 2-hop computational graphs of
+10,000-30,000 players, 100,000 coalitions each): X W_1, extract the
+computational graphs, plan, sample, evaluate every coalition, solve the least
+squares.  The whole batch of targets goes through one launch sequence per
+step (gnnshap_extract_batch_launch/_finish + gnnshap_explain_batch), the
+steps pipelined: each step's extraction is queued before the previous step's
+explanation.  --config names another workload (tiny, cora, pubmed, arxiv);
+--mode streams runs the single-target calls on several streams instead.
+Inputs (graph, features, weights) are resident in HBM before the timed
+region.
 
 Prints one JSON line: coalition evaluations per second over the whole job,
 explain latency per target (host wall time from extraction to phi on the
@@ -30,15 +32,17 @@ sys.path.insert(0, ROOT)
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="cora")
+    ap.add_argument("--config", default="reddit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="wall seconds of oracle work per worker process for cpu_baseline")
     ap.add_argument("--mode", choices=["batch", "streams"], default="batch",
                     help="batch: one launch per step for all targets; streams: per-target calls on several streams")
     ap.add_argument("--streams", type=int, default=3)
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--roofline-steps", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="bytes of a plain device copy run before the steps (counter calibration)")
     ap.add_argument("--solver-sweep", action="store_true",
@@ -120,26 +124,69 @@ def gat_times():
                                                     "ms_per_target": 1e3 * best / len(cfg["targets"])}}))
 
 
-def cpu_baseline(cfg, seconds):
-    """The oracle as it stands, on a bounded sample: whole targets of the same
-    workload, one after another, until `seconds` of CPU work have passed."""
+_CPU_CFG = None
+
+
+def _oracle_worker(job):
+    """One worker of the CPU baseline: the oracle on one target's sampled
+    rows (extraction, the GCN game, the plan, then per row its Floyd or
+    unranked coalition and the fp64 GCN forward) until `seconds` have passed."""
     from threadpoolctl import threadpool_limits
-    from oracle import explain as oracle_explain
-    done_k = 0
+    import numpy as np
+    from oracle import gcn, sampler, subgraph
+    t_index, seconds = job
+    cfg = _CPU_CFG
+    v = cfg["targets"][t_index % len(cfg["targets"])]
     t0 = time.perf_counter()
-    n = 0
+    done = 0
     with threadpool_limits(limits=1):
-        for v in cfg["targets"]:
-            r = oracle_explain.explain(cfg["indptr"], cfg["indices"], cfg["X"], cfg["weights"], cfg["biases"],
-                                       v, cfg["hops"], cfg["p"], cfg["seed"])
-            done_k += r["plan"]["k"]
-            n += 1
-            if time.perf_counter() - t0 >= seconds:
-                break
-    dt = time.perf_counter() - t0
-    return {"value": done_k / dt, "unit": "coalition evals/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} whole targets of the {cfg['name']} workload ({done_k} coalitions, "
-                      f"extract+sample+fp64 GCN per coalition+lstsq) in {dt:.1f} s, 1 thread"}
+        sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
+        M = sub["num_edges"]
+        game = gcn.Game(sub, cfg["X"], cfg["weights"], cfg["biases"])
+        game.cls = gcn.predicted_class(game.logits(np.ones(M, bool)))
+        pl = sampler.plan(M, cfg["p"])
+        rng = np.random.default_rng(1000 + t_index)
+        while time.perf_counter() - t0 < seconds:
+            rows = rng.integers(0, pl["k"], 4)
+            m, _ = sampler.sample_rows(pl, rows, cfg["seed"], v)
+            game.values(m)
+            done += len(rows)
+    return done, time.perf_counter() - t0, M
+
+
+def cpu_baseline(cfg, seconds):
+    """The oracle as it stands on a bounded sample of the same workload, run
+    on the host's cores before the GPU is touched: one process per core
+    (fork, BLAS limited to one thread each), each on one target's sampled
+    rows for `seconds`.  Rate = coalitions evaluated / wall time."""
+    import multiprocessing as mp
+    import platform
+    import numpy as np
+    global _CPU_CFG
+    _CPU_CFG = cfg
+    cores = len(os.sched_getaffinity(0))
+    cores = max(1, min(cores, int(os.environ.get("OMP_NUM_THREADS", cores) or cores), 16))
+    model = platform.processor()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(cores) as pool:
+        res = pool.map(_oracle_worker, [(i, seconds) for i in range(cores)])
+    wall = time.perf_counter() - t0
+    rows = sum(r[0] for r in res)
+    return {"value": rows / wall, "unit": "coalition evals/s", "cores": cores, "kind": "oracle",
+            "sample": f"{rows} coalitions of the {cfg['name']} workload's targets (one target per process, "
+                      f"{cores} processes x ~{seconds:.0f} s, {wall:.1f} s wall): per target the oracle's extraction, "
+                      f"GCN game and plan, per coalition its row of the sampler (Floyd / unranking, sample_rows) "
+                      f"and the fp64 GCN forward; the oracle's least squares is not in the sample (it needs every "
+                      f"row of a target: minutes per target at the reddit-shaped sizes)",
+            "cpu_model": model, "numpy": np.__version__}
 
 
 # Peaks (MI355X): HBM3E 8 TB/s; fp32 VALU without packed-fp32 instructions
@@ -151,17 +198,19 @@ VALU_INT_TOPS = 39.3
 MFMA_FP32_TFLOPS = 157.3
 
 
-def work_model(kernel, results, dims):
-    """Algorithmic work of the timed kernel over one step: (amount, unit, bound, peak).
+def work_model(kernel, results, dims, solves):
+    """Algorithmic work of the timed kernel over the timed steps: (amount, unit, bound, peak).
 
+    k_wide_l1      two-layer GCN, wide hidden layer: (k/2) M h useful MACs per target
+                   (complement pairs cover every player-feature product once) + k n1 h
+                   for the class logit, 2 flop each; fp32 MFMA
+    k_eval_rows_mx, k_eval_rows, k_eval_l2
+                   the same count; k_eval_rows_mx on fp32 MFMA, the others on VALU
+    k_cg_pass_a    per iteration of an iterative solve: the random rows' mask words
+                   (kr x ceil(M/64) x 8 bytes) + the vector r (8 M) + the product (8 kr)
+    k_cg_pass_b    the same words (bit-transposed) + u (8 kr) + the product (8 M)
     k_solve_mid / k_solve_one_batch (one-workgroup solves)
                    M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
-    k_eval_l2, k_eval_rows, k_eval_rows_mx
-                   (k/2) M h useful MACs per target (complement pairs cover every
-                   player-feature product once) + the layer-1 logit dot products;
-                   k_eval_rows_mx runs the contraction on fp32 MFMA, so its roof is
-                   the fp32 MFMA peak (the dense 0/1 product it issues is twice the
-                   useful count, which is what is reported)
     k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
                    per 64 rows and pair
     k_sample       k x ceil(M/64) x 8 bytes of masks + 4 k bytes of weights written
@@ -172,6 +221,11 @@ def work_model(kernel, results, dims):
     from paper_2401_04829_amd import _lib
     h = dims[1]
     base = kernel[:-len("_batch")] if kernel.endswith("_batch") else kernel
+    if base in ("k_cg_pass_a", "k_cg_pass_b"):
+        tot = 0.0
+        for M, wpr, kr, iters in solves:
+            tot += iters * (kr * wpr * 8.0 + 8.0 * M + 8.0 * kr)
+        return tot, "GB/s", "hbm", HBM_PEAK_GBS
     tot = 0.0
     for r in results:
         M, k = r.plan.num_players, r.plan.num_rows
@@ -182,7 +236,7 @@ def work_model(kernel, results, dims):
         if base in ("k_solve_mid", "k_solve_one"):
             if path == 1:
                 tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
-        elif base in ("k_eval_l2", "k_eval_rows", "k_eval_rows_mx"):
+        elif base in ("k_eval_l2", "k_eval_rows", "k_eval_rows_mx", "k_wide_l1"):
             n1 = r.sub.sg.hop_ptr[2]
             tot += 2.0 * ((k / 2.0) * M * h + k * n1 * h)
         elif base == "k_gram":
@@ -197,19 +251,20 @@ def work_model(kernel, results, dims):
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
     if base == "k_gram":
         return tot, "Tops/s", "alu", VALU_INT_TOPS
-    if base == "k_eval_rows_mx":
+    if base in ("k_eval_rows_mx", "k_wide_l1"):
         return tot, "TFLOP/s", "mfma", MFMA_FP32_TFLOPS
     return tot, "TFLOP/s", "alu", VALU_FP32_TFLOPS
 
 
 CANDIDATES = {
-    "batch": ["k_eval_rows_mx_batch", "k_eval_rows_batch", "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_tile_batch",
-              "k_sample_batch"],
-    "streams": ["k_solve_mid", "k_eval_rows_mx", "k_eval_l2", "k_rhs_tile", "k_gram", "k_sample"],
+    "batch": ["k_cg_pass_a", "k_cg_pass_b", "k_wide_l1", "k_eval_rows_mx_batch", "k_eval_rows_batch",
+              "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_tile_batch", "k_sample"],
+    "streams": ["k_cg_pass_a", "k_cg_pass_b", "k_wide_l1", "k_solve_mid", "k_eval_rows_mx", "k_eval_l2",
+                "k_rhs_tile", "k_gram", "k_sample"],
 }
 
 
-def roofline(run, lib, dims, mode, steps=10):
+def roofline(run, lib, dims, mode, steps):
     """Times each candidate kernel with HIP events over `steps` steps run as in
     the timed region, picks the one with the largest total and relates its
     algorithmic work to its average launch duration."""
@@ -220,18 +275,21 @@ def roofline(run, lib, dims, mode, steps=10):
         res = run(steps)
         torch.cuda.synchronize()
         ms, n = lib.gnnshap_timing_end()
+        solves = lib.gnnshap_timing_solves()
         if n and (best is None or ms > best[1]):
-            best = (name, ms, n, res)
-    name, ms, n, res = best
-    amount, unit, bound, peak = work_model(name, res, dims)
-    amount *= steps
+            best = (name, ms, n, res, solves)
+    name, ms, n, res, solves = best
+    amount, unit, bound, peak = work_model(name, res, dims, solves)
+    if not name.startswith("k_cg_"):
+        amount *= steps                          # per-step model, `steps` steps timed
     avg_s = ms / 1e3 / n
     per_launch = amount / n
     scale = 1e9 if unit == "GB/s" else 1e12
     achieved = per_launch / avg_s / scale
     return {"kernel": name, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
             "frac": achieved / peak, "traffic": measured_traffic(name), "launches": n,
-            "avg_launch_us": 1e3 * ms / n, "work_per_launch": per_launch}
+            "avg_launch_us": 1e3 * ms / n, "work_per_launch": per_launch,
+            "iterative_solves": len(solves) if name.startswith("k_cg_") else None}
 
 
 def measured_traffic(kernel):
@@ -259,21 +317,29 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it",
                           "n_gpus": args.gpus}))
         sys.exit(2)
-    import torch
     import workloads as W
-    from paper_2401_04829_amd.explainer import Explainer
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.solver_sweep or args.gat:
+        import torch
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
         if args.solver_sweep:
             solver_sweep()
         if args.gat:
             gat_times()
         return
-    dev = torch.device("cuda:0")
     t_gen = time.perf_counter()
     cfg = W.make_config(args.config)
     print(f"workload {args.config}: inputs generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
+    # the CPU baseline forks its worker processes before anything touches the GPU
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, args.cpu_seconds)
+        print(f"cpu baseline: {cpu['value']:.1f} coalitions/s on {cpu['cores']} cores", file=sys.stderr, flush=True)
+
+    import torch
+    from paper_2401_04829_amd.explainer import Explainer
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
     ex = Explainer(cfg["indptr"], cfg["indices"], cfg["X"], cfg["weights"], cfg["biases"], cfg["hops"], device=dev)
     targets = cfg["targets"]
 
@@ -311,13 +377,20 @@ def main():
 
     run(args.warmup)
     torch.cuda.synchronize()
+    print(f"warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
-    total_k, _ = run(args.steps)
+    total_k, last = run(args.steps)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_per_step = 1e3 * dt / args.steps
+    print(f"timed: {args.steps} steps, {ms_per_step:.1f} ms per step", file=sys.stderr, flush=True)
+    # every system of the last timed step was solved
+    infos = ([int(x) for x in last.info.cpu().tolist()] if args.mode == "batch"
+             else [int(r.info.item()) for r in last])
+    assert all(i == 0 for i in infos), f"solver info {infos}"
 
-    # explain latency per target: extraction to phi on the host
+    # explain latency per target: extraction to phi on the host, after one warm-up target
+    ex.explain(targets[0], cfg["p"], cfg["seed"]).phi.cpu()
     lat = []
     for v in targets:
         t1 = time.perf_counter()
@@ -326,6 +399,7 @@ def main():
         lat.append(1e3 * (time.perf_counter() - t1))
     lat_sorted = sorted(lat)
     p90 = lat_sorted[min(len(lat) - 1, int(round(0.9 * (len(lat) - 1))))]
+    print("latency pass done", file=sys.stderr, flush=True)
 
     out = {
         "metric": "masked coalition evals/sec + explain latency per target node (1 GPU)",
@@ -346,13 +420,11 @@ def main():
                    "mode": args.mode},
         "latency_ms": {"median": statistics.median(lat), "p90": p90, "targets": len(lat)},
         "roofline": None,
-        "cpu_baseline": None,
+        "cpu_baseline": cpu,
     }
     if not args.no_roofline:
         from paper_2401_04829_amd import _lib
-        out["roofline"] = roofline(lambda n: run(n)[1], _lib, cfg["dims"], args.mode)
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
+        out["roofline"] = roofline(lambda n: run(n)[1], _lib, cfg["dims"], args.mode, args.roofline_steps)
     print(json.dumps(out))
 
 

@@ -102,6 +102,7 @@ _SIGNATURES = {
                                                    c_vp, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_timing_begin": (ctypes.c_int, [ctypes.c_char_p]),
     "gnnshap_timing_end": (ctypes.c_int, [_P(ctypes.c_double), _P(c_i64)]),
+    "gnnshap_timing_solves": (ctypes.c_int, [_P(c_i64), c_i64, _P(c_i64)]),
 }
 
 _lib = None
@@ -218,6 +219,19 @@ def gnnshap_timing_end():
     ms, n = ctypes.c_double(), c_i64()
     check(load().gnnshap_timing_end(ctypes.byref(ms), ctypes.byref(n)), "timing_end")
     return ms.value, n.value
+
+
+def gnnshap_timing_solves():
+    """The iterative solves since gnnshap_timing_begin: a list of
+    (players, words per row, random rows, iterations)."""
+    n = c_i64()
+    lib = load()
+    st = lib.gnnshap_timing_solves(None, 0, ctypes.byref(n))
+    if st not in (OK, ECAPACITY):
+        check(st, "timing_solves")
+    buf = (c_i64 * max(4 * n.value, 1))()
+    check(lib.gnnshap_timing_solves(buf, n.value, ctypes.byref(n)), "timing_solves")
+    return [tuple(buf[4 * i:4 * i + 4]) for i in range(n.value)]
 
 
 def gnnshap_solve_wls(plan, classes, masks_ptr, y_ptr, fef_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):

@@ -534,7 +534,9 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
     ++chunk;
   }
   if (!stopped) GS_HIP(hipEventSynchronize(hf->ev[(chunk - 1) & 1]));
-  if (iters_out) *iters_out = __atomic_load_n(hf->host + 1, __ATOMIC_ACQUIRE);
+  const int64_t iters = __atomic_load_n(hf->host + 1, __ATOMIC_ACQUIRE);
+  if (iters_out) *iters_out = iters;
+  timing_note_solve(sh.M, sh.wpr, sh.kr, iters);
   {
     GS_TIMED("k_cg_finish", s);
     // without enumerated classes, fewer than M - 1 random rows cannot

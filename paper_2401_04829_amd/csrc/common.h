@@ -55,6 +55,10 @@ class KernelTimer {
   hipEvent_t stop_ = nullptr;
 };
 
+// Records an iterative solve (players, words per row, random rows,
+// iterations run) for gnnshap_timing_solves while timing is armed.
+void timing_note_solve(int64_t M, int64_t wpr, int64_t kr, int64_t iters);
+
 // Largest dynamic LDS allocation one workgroup may request on the current device.
 inline int max_lds_bytes() {
   int dev = 0;

@@ -1,4 +1,5 @@
 // HIP-event timing of one named kernel (diagnostics for measurements).
+#include <algorithm>
 #include <atomic>
 #include <cstring>
 #include <mutex>
@@ -13,7 +14,15 @@ std::atomic<bool> g_on{false};
 std::mutex g_mu;
 std::string g_name;
 std::vector<std::pair<hipEvent_t, hipEvent_t>> g_recs;
+std::vector<int64_t> g_solves;   // 4 per iterative solve while armed
 }  // namespace
+
+void timing_note_solve(int64_t M, int64_t wpr, int64_t kr, int64_t iters) {
+  if (!g_on.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_on.load()) return;
+  g_solves.insert(g_solves.end(), {M, wpr, kr, iters});
+}
 
 KernelTimer::KernelTimer(const char* name, hipStream_t s) : stream_(s) {
   if (!g_on.load(std::memory_order_relaxed)) return;
@@ -45,6 +54,7 @@ extern "C" int gnnshap_timing_begin(const char* kernel_name) {
   if (gnnshap::g_on.load()) return gnnshap::fail(GNNSHAP_EINVAL, "timing already armed");
   gnnshap::g_name = kernel_name;
   gnnshap::g_recs.clear();
+  gnnshap::g_solves.clear();
   gnnshap::g_on.store(true);
   return GNNSHAP_OK;
 }
@@ -71,4 +81,15 @@ extern "C" int gnnshap_timing_end(double* total_ms, int64_t* launches) {
   if (total_ms) *total_ms = total;
   if (launches) *launches = static_cast<int64_t>(recs.size());
   return status;
+}
+
+extern "C" int gnnshap_timing_solves(int64_t* records, int64_t cap, int64_t* count) {
+  gnnshap::clear_error();
+  if (!count || cap < 0 || (cap > 0 && !records)) return gnnshap::fail(GNNSHAP_EINVAL, "bad arguments");
+  std::lock_guard<std::mutex> lk(gnnshap::g_mu);
+  const int64_t n = static_cast<int64_t>(gnnshap::g_solves.size() / 4);
+  *count = n;
+  if (cap < n) return gnnshap::fail(GNNSHAP_ECAPACITY, "%lld solve records", static_cast<long long>(n));
+  std::copy(gnnshap::g_solves.begin(), gnnshap::g_solves.end(), records);
+  return GNNSHAP_OK;
 }
