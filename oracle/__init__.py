@@ -14,9 +14,13 @@ Every function follows a passage of the GNNShap paper (Akkas & Azad, arXiv
                  c-subsets (Sec. 3.3.2, Alg. 3), complement pairing (App. C.1).
 * ``subgraph`` - the pruned computational graph (Sec. 3.2, App. A).
 * ``gcn``      - the coalition game f(S): a GCN run on the computational graph
-                 with only the coalition's edges present (Sec. 2.2, 3.4, 4.2).
+                 with only the coalition's edges present (Sec. 2.2, 3.4, 4.2);
+                 ``values_many`` evaluates the same formula over a batch of
+                 coalitions for the large workloads.
 * ``wls``      - the constrained Kernel-SHAP weighted least squares
-                 (eq. 2-3, Alg. 1 step 5, Sec. 3.5).
+                 (eq. 2-3, Alg. 1 step 5, Sec. 3.5); ``kernel_shap_normal``
+                 solves the same problem through its normal equations when
+                 the rows are too many for the SVD.
 * ``shapley``  - exact Shapley values by eq. 1 (brute force, small games).
 * ``explain``  - Alg. 1 end to end for one target node.
 

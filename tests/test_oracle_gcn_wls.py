@@ -180,3 +180,100 @@ def test_symmetry_and_dummy_axioms():
     assert abs(ex2[dummy]) < 1e-12
     phi2 = wls.kernel_shap(masks, w, np.array([g2(m) for m in masks]), vals2[0], vals2[-1])
     assert abs(phi2[dummy]) < 1e-10
+
+
+# -- the batched game and the normal-equation solve, pinned against the forms above -------
+
+@pytest.mark.parametrize("L,hops", [(1, 1), (1, 2), (2, 1), (2, 2), (2, 3), (3, 2), (3, 3), (4, 3)])
+def test_values_many_equals_per_coalition_game(L, hops):
+    """gcn.values_many (the layer formula over a batch of coalitions, rows
+    without entering players computed once) gives Game.values (one sparse
+    normalised adjacency per coalition, pinned above against the dense
+    textbook form and closed forms) to 1e-12, with tiny batches so that the
+    chunking is exercised, on random coalitions including the empty and full
+    ones."""
+    dims = [5, 7, 6, 4, 3][:L] + [3]
+    for seed in range(3):
+        indptr, indices = W.random_digraph(45, 140, seed=seed + 10 * L + hops, symmetric=True)
+        X = W.gaussian_features(45, dims[0], seed + 1)
+        Ws, bs = W.glorot_gcn(dims, seed + 2, bias="random")
+        for v in range(0, 45, 4):
+            sub = subgraph.extract(indptr, indices, v, hops)
+            M = sub["num_edges"]
+            if M < 1:
+                continue
+            game = gcn.Game(sub, X, Ws, bs, cls=v % dims[-1])
+            rng = np.random.default_rng(v + seed)
+            masks = rng.random((23, M)) < rng.random((23, 1))
+            masks[0] = False
+            masks[1] = True
+            want = game.values(masks)
+            got = gcn.values_many(game, masks, chunk_bytes=3000)
+            np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12 * max(1.0, np.abs(want).max()))
+
+
+def test_values_many_hub_target_many_players():
+    """A target whose in-neighbours have hundreds of players each, with edges
+    between in-neighbours (sources whose degree varies with the coalition)."""
+    rng = np.random.default_rng(4)
+    n, src, dst = 3000, [], []
+    for x in range(1, 9):
+        src.append(x)
+        dst.append(0)
+        s = rng.choice(np.arange(9, n), size=int(rng.integers(100, 400)), replace=False)
+        src += s.tolist()
+        dst += [x] * s.size
+    src += [1, 2, 3]
+    dst += [2, 3, 5]
+    indptr, indices = W.in_csr_from_pairs(n, np.array(src), np.array(dst))
+    X = W.gaussian_features(n, 12, 5)
+    Ws, bs = W.glorot_gcn([12, 32, 7], 6, bias="random")
+    sub = subgraph.extract(indptr, indices, 0, 2)
+    M = sub["num_edges"]
+    game = gcn.Game(sub, X, Ws, bs, cls=3)
+    pl = sampler.plan(M, 300)
+    masks, _ = sampler.sample(pl, seed=9, stream=0)
+    np.testing.assert_allclose(gcn.values_many(game, masks), game.values(masks), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("M,p", [(5, 30), (9, 200), (40, 600), (150, 2000), (300, 3000)])
+def test_normal_equation_solve_equals_lstsq(M, p):
+    """wls.kernel_shap_normal (Cholesky of the normal equations) gives the
+    lstsq (SVD) solution of kernel_shap to 1e-9 of max|phi| on sampled rows
+    of random games, and keeps efficiency exact."""
+    rng = np.random.default_rng(M)
+    pl = sampler.plan(M, p)
+    masks, w = sampler.sample(pl, seed=4, stream=M)
+    inter = rng.normal(size=(M, M)) / M
+    y = masks @ rng.normal(size=M) + 0.3 * np.einsum("bi,ij,bj->b", masks, inter, masks) + 0.1
+    f0, f1 = 0.1, float(y.max())
+    a = wls.kernel_shap(masks, w, y, f0, f1)
+    b = wls.kernel_shap_normal(masks, w, y, f0, f1, chunk=97)
+    np.testing.assert_allclose(b, a, rtol=0, atol=1e-9 * np.abs(a).max())
+    assert abs(b.sum() - (f1 - f0)) < 1e-10
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_normal_equation_solve_exhaustive_equals_exact_shapley(seed):
+    """Over every coalition the normal-equation solve reproduces eq. 1."""
+    indptr, indices, X, Ws, bs, v, sub = _small_problem(seed)
+    M = sub["num_edges"]
+    game = gcn.Game(sub, X, Ws, bs)
+    game.cls = gcn.predicted_class(game.logits(np.ones(M, bool)))
+    vals = shapley.all_values(game, M)
+    exact = shapley.exact_shapley(vals, M)
+    pl = sampler.plan(M, 2 ** M - 2)
+    masks, w = sampler.sample(pl, seed=1, stream=v)
+    phi = wls.kernel_shap_normal(masks, w, gcn.values_many(game, masks), vals[0], vals[-1])
+    np.testing.assert_allclose(phi, exact, rtol=0, atol=1e-9 * max(1.0, np.abs(exact).max()))
+
+
+def test_normal_equation_solve_recovers_additive_game():
+    rng = np.random.default_rng(6)
+    M = 120
+    a = rng.normal(size=M)
+    f0 = -0.4
+    pl = sampler.plan(M, 4000)
+    masks, w = sampler.sample(pl, seed=2, stream=3)
+    phi = wls.kernel_shap_normal(masks, w, f0 + masks @ a, f0, f0 + a.sum())
+    np.testing.assert_allclose(phi, a, atol=1e-9)
