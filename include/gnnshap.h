@@ -172,6 +172,22 @@ int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
                               uint64_t* masks, float* weights,
                               void* ws, size_t ws_bytes, void* stream);
 
+/* gnnshap_sample_coalitions without a workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  The class table is copied on
+ * `stream` into a fixed array of the library (512 KiB, 16384 records, one
+ * per GPU, held until the process ends) instead of the caller's workspace;
+ * the call allocates nothing.  Every call on a GPU shares that GPU's array:
+ * calls that overlap on one GPU (different streams or host threads) race and
+ * must be ordered by the caller.  Same outputs, bit for bit, and errors as
+ * gnnshap_sample_coalitions; ECAPACITY if the plan has more than 16384 class
+ * records (a plan has at most M/2; 30,000 players and 100,000 samples give
+ * about 13,200); EHIP if the array's device address cannot be obtained. */
+int gnnshap_sample_coalitions_noalloc(const gnnshap_sample_plan* plan,
+                                      const gnnshap_class* classes,
+                                      uint64_t* masks, float* weights,
+                                      void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* 3. Masked GCN predictions (Sec. 3.4, GCN of Sec. 4.2).                   */
 /*                                                                          */

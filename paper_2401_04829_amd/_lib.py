@@ -62,6 +62,8 @@ _SIGNATURES = {
     "gnnshap_sample_workspace": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(ctypes.c_size_t)]),
     "gnnshap_sample_coalitions": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(gnnshap_class), c_vp, c_vp,
                                                  c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_sample_coalitions_noalloc": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(gnnshap_class), c_vp, c_vp,
+                                                         c_vp]),
     "gnnshap_eval_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_i64,
                                               _P(ctypes.c_size_t)]),
     "gnnshap_eval_coalitions": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp,
@@ -179,6 +181,11 @@ def gnnshap_sample_workspace(plan):
 def gnnshap_sample_coalitions(plan, classes, masks_ptr, weights_ptr, ws_ptr, ws_bytes, stream):
     check(load().gnnshap_sample_coalitions(ctypes.byref(plan), classes, masks_ptr, weights_ptr, ws_ptr, ws_bytes,
                                            stream), "sample_coalitions")
+
+
+def gnnshap_sample_coalitions_noalloc(plan, classes, masks_ptr, weights_ptr, stream):
+    check(load().gnnshap_sample_coalitions_noalloc(ctypes.byref(plan), classes, masks_ptr, weights_ptr, stream),
+          "sample_coalitions_noalloc")
 
 
 def gnnshap_eval_workspace(sg, model, k):

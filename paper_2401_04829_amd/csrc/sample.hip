@@ -8,6 +8,7 @@
 // the same chunk decide at once, the others are replayed in step order, so
 // the result is exactly the sequential algorithm's.
 #include <algorithm>
+#include <mutex>
 
 #include "batch.h"
 #include "common.h"
@@ -25,6 +26,36 @@ Ws carve(gnnshap::Carver& c, int64_t ncls) {
   Ws w;
   w.classes = c.take<gnnshap_class>(ncls > 0 ? ncls : 1);
   return w;
+}
+
+// Device copy of the class table for gnnshap_sample_coalitions_noalloc: a
+// fixed array in the library's code object, one per GPU, shared by every call
+// on that GPU.  Host code never passes its name to a kernel or a copy (on the
+// host it only stands for the symbol); it uses the device address that
+// hipGetSymbolAddress returns, looked up once per device.
+constexpr int64_t kScratchClasses = 16384;   // 512 KiB
+__device__ __align__(256) gnnshap_class scratch[kScratchClasses];
+
+constexpr int kMaxDevices = 64;
+
+gnnshap_class* scratch_address() {
+  static std::mutex mu;
+  static gnnshap_class* addr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    addr[dev] = static_cast<gnnshap_class*>(p);
+  }
+  return addr[dev];
 }
 
 // Philox4x32-10 (Salmon et al., SC'11).
@@ -336,22 +367,16 @@ extern "C" int gnnshap_sample_workspace(const gnnshap_sample_plan* plan, size_t*
   return GNNSHAP_OK;
 }
 
-extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
-                                         const gnnshap_class* classes, uint64_t* masks,
-                                         float* weights, void* ws, size_t ws_bytes,
-                                         void* stream) {
-  GS_TRY_BEGIN
-  gnnshap::clear_error();
+namespace {
+
+// Checks the arguments and the class table (consecutive first-half rows).
+int check_sample_args(const gnnshap_sample_plan* plan, const gnnshap_class* classes, const uint64_t* masks,
+                      const float* weights) {
   if (int st = check_plan(plan)) return st;
-  if (!classes || !masks || !weights || !ws) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  if (!classes || !masks || !weights) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
   const int64_t M = plan->num_players;
   if (M > kMaxPlayers)
     return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "sampler supports up to %lld players", (long long)kMaxPlayers);
-  gnnshap::Carver need(nullptr);
-  carve(need, plan->num_classes);
-  if (ws_bytes < need.bytes())
-    return gnnshap::fail(GNNSHAP_ECAPACITY, "sample workspace needs %zu bytes", need.bytes());
-  // The table must describe consecutive first-half rows.
   int64_t row = 0;
   for (int64_t i = 0; i < plan->num_classes; ++i) {
     if (classes[i].row_begin != row || classes[i].row_count < 1 || classes[i].size < 1 ||
@@ -359,11 +384,17 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
       return gnnshap::fail(GNNSHAP_EINVAL, "class table inconsistent at record %lld", (long long)i);
     row += classes[i].row_count;
   }
+  if (row != plan->num_rows / 2) return gnnshap::fail(GNNSHAP_EINVAL, "class table does not cover k/2 rows");
+  return GNNSHAP_OK;
+}
+
+// Copies the class table to dev_classes on the stream and launches the sampler.
+int sample_launch(const gnnshap_sample_plan* plan, const gnnshap_class* classes, uint64_t* masks, float* weights,
+                  gnnshap_class* dev_classes, hipStream_t s) {
+  const int64_t M = plan->num_players;
   const int64_t half = plan->num_rows / 2;
-  if (row != half) return gnnshap::fail(GNNSHAP_EINVAL, "class table does not cover k/2 rows");
-  gnnshap::Carver c(ws);
-  const Ws w = carve(c, plan->num_classes);
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  Ws w;
+  w.classes = dev_classes;
   GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class),
                         hipMemcpyHostToDevice, s));
   const int64_t wpr = plan->words_per_row;
@@ -394,6 +425,39 @@ extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
+}
+
+}  // namespace
+
+extern "C" int gnnshap_sample_coalitions(const gnnshap_sample_plan* plan,
+                                         const gnnshap_class* classes, uint64_t* masks,
+                                         float* weights, void* ws, size_t ws_bytes,
+                                         void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (int st = check_sample_args(plan, classes, masks, weights)) return st;
+  if (!ws) return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
+  gnnshap::Carver need(nullptr);
+  carve(need, plan->num_classes);
+  if (ws_bytes < need.bytes())
+    return gnnshap::fail(GNNSHAP_ECAPACITY, "sample workspace needs %zu bytes", need.bytes());
+  gnnshap::Carver c(ws);
+  const Ws w = carve(c, plan->num_classes);
+  return sample_launch(plan, classes, masks, weights, w.classes, static_cast<hipStream_t>(stream));
+  GS_TRY_END
+}
+
+extern "C" int gnnshap_sample_coalitions_noalloc(const gnnshap_sample_plan* plan, const gnnshap_class* classes,
+                                                 uint64_t* masks, float* weights, void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::clear_error();
+  if (int st = check_sample_args(plan, classes, masks, weights)) return st;
+  if (plan->num_classes > kScratchClasses)
+    return gnnshap::fail(GNNSHAP_ECAPACITY, "the allocation-free sampler holds at most %lld class records (%lld given)",
+                         static_cast<long long>(kScratchClasses), static_cast<long long>(plan->num_classes));
+  gnnshap_class* dev_classes = scratch_address();
+  if (!dev_classes) return gnnshap::fail(GNNSHAP_EHIP, "hipGetSymbolAddress of the sampler's class table failed");
+  return sample_launch(plan, classes, masks, weights, dev_classes, static_cast<hipStream_t>(stream));
   GS_TRY_END
 }
 
