@@ -50,7 +50,9 @@ def _check(ex, indptr, indices, X, P, v, p, seed, rows=None, target_class=-1):
     assert int(res.cls.item()) == cls
     fef = res.f_empty_full.cpu().numpy().astype(np.float64)
     assert np.all(np.abs(fef - [f0, f1]) <= y_tolerance(np.array([f0, f1]), f0, f1))
-    m = sampler.unpack(masks_np(res.masks), M)
+    pl = sampler.plan(M, p)
+    m, w_ref = sampler.sample(pl, seed, v)
+    np.testing.assert_array_equal(masks_np(res.masks), sampler.pack(m))
     k = m.shape[0]
     if rows is None:
         rows = np.arange(k)
@@ -60,7 +62,7 @@ def _check(ex, indptr, indices, X, P, v, p, seed, rows=None, target_class=-1):
     assert (err <= y_tolerance(y_ref, f0, f1)).all(), err.max()
     dead = ~m[:, : int(sub["dst_ptr"][1])].any(axis=1)
     assert np.all(res.y.cpu().numpy()[dead] == res.f_empty_full.cpu().numpy()[0])
-    return res, game, m, (f0, f1)
+    return res, game, m, w_ref, (f0, f1)
 
 
 @pytest.mark.parametrize("heads,F,C", [(8, 16, 7), (1, 5, 3), (3, 20, 4), (4, 64, 2)])
@@ -83,9 +85,9 @@ def test_gat_cora_values_and_phi(dev):
     ex = GatExplainer(cfg["indptr"], cfg["indices"], cfg["X"], P)
     for v in cfg["targets"][:3]:
         _say("gat cora", v)
-        res, game, m, (f0, f1) = _check(ex, cfg["indptr"], cfg["indices"], cfg["X"], P, v, 2000, 7)
+        res, game, m, w, (f0, f1) = _check(ex, cfg["indptr"], cfg["indices"], cfg["X"], P, v, 2000, 7)
         assert int(res.info.item()) == 0
-        phi_ref = wls.kernel_shap(m, res.weights.cpu().numpy().astype(np.float64), game.values(m), f0, f1)
+        phi_ref = wls.kernel_shap(m, w, game.values(m), f0, f1)
         phi = res.phi.cpu().numpy().astype(np.float64)
         assert np.abs(phi - phi_ref).max() <= 1e-3 * np.abs(phi_ref).max()
 
@@ -113,7 +115,8 @@ def test_gat_exhaustive_equals_exact_shapley(dev):
         res = ex.explain(int(v), 2 ** M - 2, 1)
         torch.cuda.synchronize()
         game = G.GatGame(sub, X, P)
-        game.cls = int(res.cls.item())
+        game.cls = int(np.argmax(game.logits(np.ones(M, bool))))
+        assert int(res.cls.item()) == game.cls
         codes = np.arange(1 << M)
         table = np.array([game(((codes[i] >> np.arange(M)) & 1).astype(bool)) for i in range(1 << M)])
         exact = shapley.exact_shapley(table, M)

@@ -326,7 +326,8 @@ def test_solve_exhaustive_equals_exact_shapley(dev, M):
     exact = shapley.exact_shapley(vals, M)
     p = 2 ** M - 2
     plan, classes, masks, _ = sample_on_gpu(M, p, 1, 2)
-    mb = sampler.unpack(masks_np(masks), M)
+    mb, _ = sampler.sample(sampler.plan(M, p), 1, 2)
+    np.testing.assert_array_equal(masks_np(masks), sampler.pack(mb))
     codes = (mb * (1 << np.arange(M))).sum(axis=1)
     y = torch.tensor(vals[codes], dtype=torch.float32, device=dev)
     fef = torch.tensor([vals[0], vals[-1]], dtype=torch.float32, device=dev)
@@ -352,7 +353,9 @@ def test_solve_recovers_additive_game(dev, M, p):
     rng = np.random.default_rng(M)
     a = rng.normal(size=M)
     f0 = 0.25
-    mb = torch.tensor(sampler.unpack(masks_np(masks), M), dtype=torch.float64, device=dev)
+    mo, _ = sampler.sample(sampler.plan(M, p), 5, 6)
+    np.testing.assert_array_equal(masks_np(masks), sampler.pack(mo))
+    mb = torch.tensor(mo, dtype=torch.float64, device=dev)
     y = (f0 + mb @ torch.tensor(a, device=dev)).float()
     fef = torch.tensor([f0, f0 + a.sum()], dtype=torch.float32, device=dev)
     phi = torch.empty(M, dtype=torch.float32, device=dev)
@@ -390,22 +393,23 @@ def _solve_phi(res, y, f0, f1):
 
 
 def _normal_equation_residual(res, phi, f0, chunk=1024):
-    """r = X^T W (y - f0 - X phi) for the sampled rows X and their kernel
-    weights W, and the row sums of |X^T W X|, in fp64 on the device.  The
-    efficiency-constrained least squares optimum has r = lambda * 1."""
+    """r = X^T W (y - f0 - X phi) and b = X^T W (y - f0) for the sampled rows
+    X and their kernel weights W, in fp64 on the device (test-side
+    arithmetic).  The efficiency-constrained least squares optimum has
+    r = lambda * 1."""
     M, k = res.plan.num_players, res.plan.num_rows
     dev = res.masks.device
     ph = torch.tensor(phi, dtype=torch.float64, device=dev)
     r = torch.zeros(M, dtype=torch.float64, device=dev)
-    gsum = torch.zeros(M, dtype=torch.float64, device=dev)
+    b = torch.zeros(M, dtype=torch.float64, device=dev)
     for r0 in range(0, k, chunk):
         r1 = min(k, r0 + chunk)
         X = _unpack_rows(res.masks, M, r0, r1)
         w = res.weights[r0:r1].double()
-        e = res.y[r0:r1].double() - f0 - X @ ph
-        r += X.T @ (w * e)
-        gsum += X.T @ (w * X.sum(dim=1))
-    return r.cpu().numpy(), gsum.cpu().numpy()
+        yc = res.y[r0:r1].double() - f0
+        r += X.T @ (w * (yc - X @ ph))
+        b += X.T @ (w * yc)
+    return r.cpu().numpy(), b.cpu().numpy()
 
 
 def _full_size_targets(cfg, picks):
@@ -420,9 +424,12 @@ def test_full_size_workload(dev, name, picks):
     """At the full sizes of the two large workloads (2-hop graphs of 5k..30k
     players, 50,000 / 100,000 coalitions): extraction bit-exact, sampled
     masks bit-exact, sampled coalition values within the y bar, and phi
-    checked by properties that hold at any size: efficiency, the constrained
-    normal equations of the least squares, and exact recovery of an additive
-    game on the same coalitions."""
+    checked by properties that hold at any size: efficiency, the solved
+    normal equations, and exact recovery of an additive game on the same
+    coalitions.  These properties do not by themselves bound the phi error
+    by the phi bar (that needs the smallest eigenvalue of the system);
+    tests/test_gpu_full_phi.py compares phi element-wise with the oracle's
+    least squares at the smallest target of each large workload."""
     _say("full size", name, "building the workload")
     cfg = W.make_config(name)
     ex = explainer_for(cfg)
@@ -441,11 +448,12 @@ def test_full_size_workload(dev, name, picks):
         fef = res.f_empty_full.cpu().numpy().astype(np.float64)
         delta = fef[1] - fef[0]
         assert abs(phi.sum() - delta) <= 1e-4 * max(1.0, abs(delta)) + 1e-3 * np.abs(phi).max()
-        # first-order optimality: r - mean(r) = -(G d - mean(G d)) for d = phi - phi*,
-        # so the phi bar bounds it by 2 * 1e-3 max|phi| * (largest row sum of G)
-        r, gsum = _normal_equation_residual(res, phi, fef[0])
-        dev_r = np.abs(r - r.mean()).max()
-        assert dev_r <= 2e-3 * np.abs(phi).max() * gsum.max(), (dev_r, np.abs(phi).max(), gsum.max())
+        # the constrained optimum has X^T W (y - f0 - X phi) = lambda 1: the
+        # centred residual of the normal equations must be small against the
+        # centred right-hand side (a solved system, not the phi bar itself)
+        r, b = _normal_equation_residual(res, phi, fef[0])
+        rc, bc = r - r.mean(), b - b.mean()
+        assert np.linalg.norm(rc) <= 1e-3 * np.linalg.norm(bc), (np.linalg.norm(rc), np.linalg.norm(bc))
         # an additive game on the same coalitions has phi = a
         a = np.random.default_rng(M).normal(size=M)
         at = torch.tensor(a, dtype=torch.float64, device=res.masks.device)
