@@ -206,9 +206,15 @@ def work_model(kernel, results, dims, solves):
                    for the class logit, 2 flop each; fp32 MFMA
     k_eval_rows_mx, k_eval_rows, k_eval_l2
                    the same count; k_eval_rows_mx on fp32 MFMA, the others on VALU
-    k_cg_pass_a    per iteration of an iterative solve: the random rows' mask words
-                   (kr x ceil(M/64) x 8 bytes) + the vector r (8 M) + the product (8 kr)
-    k_cg_pass_b    the same words (bit-transposed) + u (8 kr) + the product (8 M)
+    k_cg_pass_a    per iteration of an iterative solve: the mask words of the random
+                   rows kept as bits ((kr - rs) x ceil(M/64) x 8 bytes) + the vector r
+                   (8 M) + the product (8 (kr - rs))
+    k_cg_pass_b    the same words (bit-transposed) + u (8 (kr - rs)) + the product (8 M)
+    k_cg_rows      the player lists of the rs sparse rows (4 nnz bytes), the entries of
+                   r they select (8 nnz) and u (8 kr)
+    k_cg_pass_bs   the player-major lists (4 nnz + 8 (M + 1)), the entries of u they
+                   select (8 nnz) and the product (8 M)
+    k_cg_update    five fp64 vectors of M read (R^T u, r, p, s, x) and four written
     k_solve_mid / k_solve_one_batch (one-workgroup solves)
                    M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
     k_gram         K_R M(M+1)/2 pair counts over the random rows, 1 popcount-AND
@@ -221,10 +227,17 @@ def work_model(kernel, results, dims, solves):
     from paper_2401_04829_amd import _lib
     h = dims[1]
     base = kernel[:-len("_batch")] if kernel.endswith("_batch") else kernel
-    if base in ("k_cg_pass_a", "k_cg_pass_b"):
+    if base.startswith("k_cg_"):
         tot = 0.0
-        for M, wpr, kr, iters in solves:
-            tot += iters * (kr * wpr * 8.0 + 8.0 * M + 8.0 * kr)
+        for M, wpr, kr, iters, rs, nnz in solves:
+            if base in ("k_cg_pass_a", "k_cg_pass_b"):
+                tot += iters * ((kr - rs) * wpr * 8.0 + 8.0 * M + 8.0 * (kr - rs))
+            elif base == "k_cg_rows":
+                tot += iters * (12.0 * nnz + 8.0 * kr)
+            elif base == "k_cg_pass_bs":
+                tot += iters * (12.0 * nnz + 16.0 * M + 8.0)
+            elif base == "k_cg_update":
+                tot += iters * 72.0 * M
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
     tot = 0.0
     for r in results:
@@ -257,9 +270,9 @@ def work_model(kernel, results, dims, solves):
 
 
 CANDIDATES = {
-    "batch": ["k_cg_pass_a", "k_cg_pass_b", "k_wide_l1", "k_eval_rows_mx_batch", "k_eval_rows_batch",
+    "batch": ["k_cg_pass_a", "k_cg_pass_b", "k_cg_rows", "k_cg_pass_bs", "k_cg_update", "k_wide_l1", "k_eval_rows_mx_batch", "k_eval_rows_batch",
               "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_tile_batch", "k_sample"],
-    "streams": ["k_cg_pass_a", "k_cg_pass_b", "k_wide_l1", "k_solve_mid", "k_eval_rows_mx", "k_eval_l2",
+    "streams": ["k_cg_pass_a", "k_cg_pass_b", "k_cg_rows", "k_cg_pass_bs", "k_cg_update", "k_wide_l1", "k_solve_mid", "k_eval_rows_mx", "k_eval_l2",
                 "k_rhs_tile", "k_gram", "k_sample"],
 }
 

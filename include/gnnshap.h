@@ -479,12 +479,13 @@ int gnnshap_timing_begin(const char* kernel_name);
 int gnnshap_timing_end(double* total_ms, int64_t* launches);
 
 /* The iterative solves (Sec. 3.5) run since the last gnnshap_timing_begin,
- * in the order they ran: records[4 i .. 4 i + 3] = players, mask words per
+ * in the order they ran: records[6 i .. 6 i + 5] = players, mask words per
  * row, random representative rows, iterations (the iterations whose products
  * did work; up to seven more queued launches of each kernel find the solve
- * stopped and return at once).  *count receives the number of records;
- * ECAPACITY if cap is smaller.  Diagnostics for measurements, like the
- * timing calls. */
+ * stopped and return at once), random rows kept as player lists (the first
+ * ones, small coalitions), the players in those lists.  *count receives the
+ * number of records; ECAPACITY if cap is smaller (cap counts records).
+ * Diagnostics for measurements, like the timing calls. */
 int gnnshap_timing_solves(int64_t* records, int64_t cap, int64_t* count);
 
 #ifdef __cplusplus

@@ -230,15 +230,15 @@ def gnnshap_timing_end():
 
 def gnnshap_timing_solves():
     """The iterative solves since gnnshap_timing_begin: a list of
-    (players, words per row, random rows, iterations)."""
+    (players, words per row, random rows, iterations, sparse rows, their players)."""
     n = c_i64()
     lib = load()
     st = lib.gnnshap_timing_solves(None, 0, ctypes.byref(n))
     if st not in (OK, ECAPACITY):
         check(st, "timing_solves")
-    buf = (c_i64 * max(4 * n.value, 1))()
+    buf = (c_i64 * max(6 * n.value, 1))()
     check(lib.gnnshap_timing_solves(buf, n.value, ctypes.byref(n)), "timing_solves")
-    return [tuple(buf[4 * i:4 * i + 4]) for i in range(n.value)]
+    return [tuple(buf[6 * i:6 * i + 6]) for i in range(n.value)]
 
 
 def gnnshap_solve_wls(plan, classes, masks_ptr, y_ptr, fef_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):

@@ -30,17 +30,31 @@ struct CgWs {
   int32_t* sz;     // kr: sizes of the random representative rows
   uint64_t* blocked;  // nrb x words_per_row x 64: the random rows in row blocks
   CgState* st;
+  // sparse rows (random rows [0, rs), the smallest coalitions): their players
+  int64_t* csr_ptr;   // rs + 1: players of each sparse row, ascending
+  int32_t* csr_idx;   // nnz
+  int64_t* csc_ptr;   // M + 1: rows of each player, ascending
+  int32_t* csc_row;   // nnz
+  double* qs;         // M: R_s^T u
 };
 
 // Launch shape of the iterative solver for M players and kr random
 // representative rows (words_per_row mask words per row).
 struct CgShape {
   int64_t M, wpr, kr, nrb;
-  int64_t npc, pwords;  // product R r: player chunks of pwords words
-  int64_t nrc, rbc;     // product R^T u: row chunks of rbc row blocks
-  int64_t nbu, nbc;     // workgroups of the row and player passes
+  int64_t rs, nnz;         // sparse rows [0, rs) (whole row blocks), their players
+  int64_t rbd0;            // first row block of the bit products (rs / 64)
+  int64_t npc, pwords;     // product R r: player chunks of pwords words
+  int64_t nrc, rbc;        // product R^T u: row chunks of rbc row blocks
+  int64_t nbu, nbc;        // partial sums of the row passes (pass A's sparse workgroups, then the row
+                           // pass's), workgroups of the player passes
+  int64_t nsa, nsb;        // sparse workgroups of pass A (rows) and pass B (players)
+  int64_t nrcd;            // row chunks of pass B's bit rows (0 without bit rows)
 };
-CgShape cg_shape(int64_t M, int64_t wpr, int64_t kr);
+// The split of the random rows [rb0, rb0 + kr) of a class table into sparse
+// rows (coalition size at most M / kSparseDiv, whole blocks of 64 rows) and
+// bit rows; the shape of the solver for that split.
+CgShape cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t rb0, const gnnshap_class* classes, int64_t ncls);
 CgWs cg_carve(Carver& c, const CgShape& sh);
 
 // The problem handed over by the solve entry point: the bit-transposed random

@@ -23,12 +23,22 @@
 // of a multiply-add per bit).  delta needs no extra reduction:
 // r.A r = alpha |r|^2 + 2 w_r |R r|^2 for r in 1-perp.
 //
+// Rows of small coalitions are mostly zero bits: the random rows whose size
+// is at most M / kSparseDiv (the first ones: the plan orders random classes
+// by ascending size), in whole blocks of 64 rows, are kept as lists of their
+// players instead (sparse rows), built once per solve from the bits, row by
+// row and player by player (both in ascending order).  One wavefront sums a
+// list (lanes stride over it, then a fixed butterfly).
+//
 // Per iteration t:
-//   pass A   stopping test on gamma_t; partial products R r over player chunks
-//            (lane = row, the rows' words in row blocks);
-//   rows     u = R r summed over the chunks, partial |u|^2 and |m|.u;
-//   pass B   partial products R^T u over row chunks (lane = player, words of
-//            the bit-transposed rows);
+//   pass A   stopping test on gamma_t; partial products R r of the bit rows
+//            over player chunks (lane = row, the rows' words in row blocks)
+//            and, in workgroups of their own in the same launch, u = R r of
+//            the sparse rows (a wavefront sums r over a row's players);
+//   rows     u of the bit rows (the sum of their chunks); partial |u|^2, |m|.u;
+//   pass B   partial products R^T u of the bit rows over row chunks (lane =
+//            player, words of the bit-transposed rows) and, in workgroups of
+//            their own, the sparse rows' R_s^T u (a wavefront per player);
 //   update   w = alpha r + 2 w_r (R^T u - mean), the scalars, the vector steps
 //            and the partial sums of the new gamma.
 // Vectors and every sum are fp64; partial sums are reduced in a fixed order,
@@ -38,6 +48,7 @@
 // most one chunk runs idle.
 #include <algorithm>
 #include <atomic>
+#include <vector>
 
 #include "cg.h"
 
@@ -48,10 +59,17 @@ constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
 constexpr int kWaves = 8;            // waves per workgroup of both passes
 constexpr int64_t kTabWords = 16;    // nibble tables per workgroup: 16 words (32 KiB of LDS)
+constexpr int64_t kSparseDiv = 64;   // sparse rows: coalition size at most M / kSparseDiv
 
 struct Args {
   const int32_t* sz;
   int64_t M, wpr, kr, nrb, npc, pwords, nrc, rbc, nbu, nbc;
+  int64_t rs, rbd0, nsa, nsb, nrcd, nxa, nxb;
+  const int64_t* csr_ptr;
+  const int32_t* csr_idx;
+  const int64_t* csc_ptr;
+  const int32_t* csc_row;
+  double* qs;
   double alpha, wr2, tol2;
   int64_t maxit;
   int32_t has_random;
@@ -190,20 +208,66 @@ __device__ __forceinline__ bool cg_stop(const Args& a, int64_t t, bool writer) {
   return false;
 }
 
-// Pass A: upart[pc, b] = sum over the words of player chunk pc of the bits of
-// row b times r.  The workgroup builds the chunk's nibble tables of r in LDS
-// (r is padded with zeros to whole words); then one wave per 64 rows
-// (lane = row) reads the row-blocked words, 512 contiguous bytes per word,
-// and sums table entries.
+// Sum of the entries of v selected by n indices, by one wavefront: lane l
+// takes indices l, l + 64, ... four at a time (their loads issued together),
+// then a fixed butterfly; every lane gets the same bits.
+__device__ __forceinline__ double wave_gather_sum(const int32_t* __restrict__ idx, int64_t n,
+                                                  const double* __restrict__ v) {
+  const int lane = threadIdx.x & 63;
+  double s4[4] = {0.0, 0.0, 0.0, 0.0};
+  int64_t e = lane;
+  for (; e + 192 < n; e += 256) {
+    const int32_t j0 = idx[e], j1 = idx[e + 64], j2 = idx[e + 128], j3 = idx[e + 192];
+    s4[0] += v[j0];
+    s4[1] += v[j1];
+    s4[2] += v[j2];
+    s4[3] += v[j3];
+  }
+  for (int q = 0; e < n; e += 64, ++q) s4[q] += v[idx[e]];
+  return wave_sum_d((s4[0] + s4[1]) + (s4[2] + s4[3]));
+}
+
+// Pass A.  Workgroups (x, y < npc): upart[y, b] = sum over the words of
+// player chunk y of the bits of bit row b times r; the workgroup builds the
+// chunk's nibble tables of r in LDS (r is padded with zeros to whole words),
+// then one wave per 64 rows (lane = row) reads the row-blocked words, 512
+// contiguous bytes per word, and sums table entries.  Workgroups (x, npc),
+// x < nsa: the sparse rows x * kWaves + wave, + nsa * kWaves, ...: u_b = sum
+// of r over the row's players, with the workgroup's partial |u|^2 and |m|.u
+// in uu[2 x], uu[2 x + 1].  Both kinds take the stopping test first.
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_t* __restrict__ blocked,
                                                           const double* __restrict__ r,
                                                           double* __restrict__ upart, int64_t t) {
   extern __shared__ double tab[];   // pwords * 256
-  if (a.st->done) return;
-  const int lane = threadIdx.x & 63;
-  const int64_t rb = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const bool writer = blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0;
+  __shared__ double red[kWaves];
   const int64_t pc = blockIdx.y;
+  // the grid's x extent is the larger of the two kinds': idle workgroups leave at once
+  if (a.st->done || static_cast<int64_t>(blockIdx.x) >= (pc == a.npc ? a.nsa : a.nxa)) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool writer = blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0;
+  if (pc == a.npc) {                  // sparse rows
+    if (cg_stop(a, t, false)) return;
+    const int64_t x = blockIdx.x;
+    double uu = 0.0, su = 0.0;
+    for (int64_t b = x * kWaves + wave; b < a.rs; b += a.nsa * kWaves) {
+      const int64_t e0 = a.csr_ptr[b];
+      const double v = wave_gather_sum(a.csr_idx + e0, a.csr_ptr[b + 1] - e0, r);
+      if (lane == 0) {
+        a.u[b] = v;
+        uu += v * v;
+        su += static_cast<double>(a.sz[b]) * v;
+      }
+    }
+    const double s1 = block_sum_d(uu, red);
+    const double s2 = block_sum_d(su, red);
+    if (threadIdx.x == 0) {
+      a.uu[2 * x] = s1;
+      a.uu[2 * x + 1] = s2;
+    }
+    return;
+  }
+  const int64_t rb = a.rbd0 + static_cast<int64_t>(blockIdx.x) * kWaves + wave;
   const int64_t w0 = pc * a.pwords;
   const int64_t w1 = w0 + a.pwords < a.wpr ? w0 + a.pwords : a.wpr;
   const int64_t nw = w1 - w0;
@@ -225,11 +289,12 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
   if (row < a.kr) upart[pc * a.kr + row] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
-// u = R r (sum over the player chunks in order), with partial |u|^2 and |m|.u.
+// u of the bit rows (the sum of their pass-A chunks, one lane per row) with
+// partial |u|^2 and |m|.u in uu[2 (nsa + x)], uu[2 (nsa + x) + 1].
 __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
   __shared__ double red[4];
   if (a.st->done) return;
-  const int64_t b = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t b = a.rs + static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   double uu = 0.0, su = 0.0;
   if (b < a.kr) {
     double v = 0.0;
@@ -241,25 +306,38 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
   const double s1 = block_sum_d(uu, red);
   const double s2 = block_sum_d(su, red);
   if (threadIdx.x == 0) {
-    a.uu[2 * blockIdx.x] = s1;
-    a.uu[2 * blockIdx.x + 1] = s2;
+    a.uu[2 * (a.nsa + blockIdx.x)] = s1;
+    a.uu[2 * (a.nsa + blockIdx.x) + 1] = s2;
   }
 }
 
-// Pass B: qpart[c, j] = sum over the row blocks of chunk c of the bits of
-// player j times u.  The workgroup builds the chunk's nibble tables of u in
-// LDS (u is padded with zeros to whole row blocks); then one wave per 64
-// players (lane = player) reads the bit-transposed words T[rb, j] and sums
-// table entries.
+// Pass B.  Workgroups (x, c < nrcd): qpart[c, j] = sum over the row blocks of
+// chunk c of the bits of player j times u; the workgroup builds the chunk's
+// nibble tables of u in LDS (u is padded with zeros to whole row blocks),
+// then one wave per 64 players (lane = player) reads the bit-transposed words
+// T[rb, j] and sums table entries.  Workgroups (x, nrcd), x < nsb: the
+// players x * kWaves + wave, + nsb * kWaves, ...: qs[j] = sum of u over the
+// sparse rows holding player j.
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_t* __restrict__ T,
                                                           const double* __restrict__ u,
                                                           double* __restrict__ qpart) {
   extern __shared__ double tab[];   // rbc * 256
-  if (a.st->done) return;
-  const int lane = threadIdx.x & 63;
-  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t c = blockIdx.y;
-  const int64_t b0 = c * a.rbc;
+  // the grid's x extent is the larger of the two kinds': idle workgroups leave at once
+  if (a.st->done || static_cast<int64_t>(blockIdx.x) >= (c == a.nrcd ? a.nsb : a.nxb)) return;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (c == a.nrcd) {                  // sparse rows
+    const int64_t x = blockIdx.x;
+    for (int64_t j = x * kWaves + wave; j < a.M; j += a.nsb * kWaves) {
+      const int64_t e0 = a.csc_ptr[j];
+      const double v = wave_gather_sum(a.csc_row + e0, a.csc_ptr[j + 1] - e0, u);
+      if (lane == 0) a.qs[j] = v;
+    }
+    return;
+  }
+  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  const int64_t b0 = a.rbd0 + c * a.rbc;
   const int64_t b1 = b0 + a.rbc < a.nrb ? b0 + a.rbc : a.nrb;
   const int64_t nb = b1 - b0;
   for (int64_t q = threadIdx.x; q < nb * 16; q += kWaves * 64) build_nibble_table(u + b0 * 64 + q * 4, tab + q * 16);
@@ -278,6 +356,97 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_
   if (valid) qpart[c * a.M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
+// ---- the sparse rows' lists, built once per solve ------------------------------------------
+
+// Exclusive prefix sums of n values by one workgroup of 1024 threads (thread t
+// takes a contiguous run), v[i] -> out[i], total -> out[n].
+template <class T>
+__device__ void block_scan_i64(const T* __restrict__ v, int64_t n, int64_t* __restrict__ out) {
+  __shared__ int64_t part[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (n + 1023) / 1024;
+  const int64_t i0 = t * per, i1 = i0 + per < n ? i0 + per : n;
+  int64_t s = 0;
+  for (int64_t i = i0; i < i1; ++i) s += v[i];
+  part[t] = s;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int64_t x = part[i];
+      part[i] = run;
+      run += x;
+    }
+    out[n] = run;
+  }
+  __syncthreads();
+  int64_t run = part[t];
+  for (int64_t i = i0; i < i1; ++i) {
+    const int64_t x = v[i];
+    out[i] = run;
+    run += x;
+  }
+}
+
+// Row-major lists: csr_ptr = exclusive prefix sums of the sparse rows' sizes.
+__global__ void __launch_bounds__(1024) k_cg_csr_ptr(const int32_t* __restrict__ sz, int64_t rs,
+                                                     int64_t* __restrict__ ptr) {
+  block_scan_i64(sz, rs, ptr);
+}
+
+// Row-major lists: wavefront g reads the words of its 64 rows from the
+// row-blocked copy (lane = row) and writes each set bit's player in order.
+__global__ void __launch_bounds__(64) k_cg_csr_fill(const uint64_t* __restrict__ blocked, int64_t wpr, int64_t rs,
+                                                    const int64_t* __restrict__ ptr, int64_t nnz,
+                                                    int32_t* __restrict__ idx) {
+  const int64_t g = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int64_t b = g * 64 + lane;
+  if (b >= rs) return;
+  int64_t pos = ptr[b];
+  const int64_t end = ptr[b + 1] < nnz ? ptr[b + 1] : nnz;
+  const uint64_t* src = blocked + g * wpr * 64 + lane;
+  for (int64_t w = 0; w < wpr; ++w) {
+    uint64_t word = src[w * 64];
+    while (word && pos < end) {
+      idx[pos++] = static_cast<int32_t>(w * 64 + __builtin_ctzll(word));
+      word &= word - 1;
+    }
+  }
+}
+
+// Player-major lists: cnt[j] = sparse rows holding player j (from the
+// bit-transposed rows T[rb, j], rb < nrb_s).
+__global__ void __launch_bounds__(256) k_cg_csc_count(const uint64_t* __restrict__ T, int64_t M, int64_t nrb_s,
+                                                      int64_t* __restrict__ cnt) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= M) return;
+  int64_t c = 0;
+  for (int64_t rb = 0; rb < nrb_s; ++rb) c += __popcll(T[rb * M + j]);
+  cnt[j] = c;
+}
+
+__global__ void __launch_bounds__(1024) k_cg_csc_scan(const int64_t* __restrict__ cnt, int64_t M,
+                                                      int64_t* __restrict__ ptr) {
+  block_scan_i64(cnt, M, ptr);
+}
+
+__global__ void __launch_bounds__(256) k_cg_csc_fill(const uint64_t* __restrict__ T, int64_t M, int64_t nrb_s,
+                                                     const int64_t* __restrict__ ptr, int64_t nnz,
+                                                     int32_t* __restrict__ rows) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= M) return;
+  int64_t pos = ptr[j];
+  const int64_t end = ptr[j + 1] < nnz ? ptr[j + 1] : nnz;
+  for (int64_t rb = 0; rb < nrb_s; ++rb) {
+    uint64_t word = T[rb * M + j];
+    while (word && pos < end) {
+      rows[pos++] = static_cast<int32_t>(rb * 64 + __builtin_ctzll(word));
+      word &= word - 1;
+    }
+  }
+}
+
 // Update of iteration t (see the recurrences above); partial gamma_{t+1}.
 __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
   __shared__ double red[4];
@@ -287,8 +456,10 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
   // this thread's vector entries first: their loads overlap the scalar sums
   double q = 0.0, rj = 0.0, pj = 0.0, sj = 0.0;
   if (j < a.M) {
-    if (a.has_random)
-      for (int64_t c = 0; c < a.nrc; ++c) q += a.qpart[c * a.M + j];
+    if (a.has_random) {
+      if (a.rs > 0) q = a.qs[j];
+      for (int64_t c = 0; c < a.nrcd; ++c) q += a.qpart[c * a.M + j];
+    }
     rj = a.r[j];
     pj = a.p[j];
     sj = a.s[j];
@@ -408,24 +579,46 @@ extern "C" int gnnshap_set_iterative_threshold(int64_t num_players) {
   return GNNSHAP_OK;
 }
 
-gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr) {
+gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t rb0, const gnnshap_class* classes,
+                                   int64_t ncls) {
   CgShape s{};
   s.M = M;
   s.wpr = wpr;
   s.kr = kr;
   s.nrb = ceil_div(kr, 64);
-  const int64_t nrb = s.nrb > 0 ? s.nrb : 1;
+  // sparse rows: the longest run of random rows from the first whose sizes are
+  // at most M / kSparseDiv, cut to whole 64-row groups
+  if (kr > 0 && classes) {
+    const int64_t tmax = M / kSparseDiv;
+    std::vector<int32_t> sz;
+    sz.reserve(static_cast<size_t>(kr));
+    for (int64_t i = 0; i < ncls && static_cast<int64_t>(sz.size()) < kr; ++i) {
+      if (classes[i].row_begin + classes[i].row_count <= rb0) continue;
+      if (classes[i].size > tmax) break;
+      const int64_t from = std::max<int64_t>(classes[i].row_begin, rb0);
+      for (int64_t r = from; r < classes[i].row_begin + classes[i].row_count; ++r) sz.push_back(classes[i].size);
+    }
+    s.rs = (std::min<int64_t>(static_cast<int64_t>(sz.size()), kr) / 64) * 64;
+    for (int64_t b = 0; b < s.rs; ++b) s.nnz += sz[b];
+  }
+  s.rbd0 = s.rs / 64;
+  const int64_t nrbd = std::max<int64_t>(s.nrb - s.rbd0, 1);
   // pass A: about 4096 waves (row blocks x player chunks of whole words), at
   // most kTabWords words of tables per workgroup
-  const int64_t npc = std::max<int64_t>(ceil_div(wpr, kTabWords), std::min(ceil_div(4096, nrb), wpr));
+  const int64_t npc = std::max<int64_t>(ceil_div(wpr, kTabWords), std::min(ceil_div(4096, nrbd), wpr));
   s.pwords = ceil_div(wpr, npc);
   s.npc = ceil_div(wpr, s.pwords);
   // pass B: about 4096 waves (player words x chunks of whole row blocks), at
   // most kTabWords row blocks of tables per workgroup
-  const int64_t nrc = std::max<int64_t>(ceil_div(nrb, kTabWords), std::min(ceil_div(4096, wpr), nrb));
-  s.rbc = ceil_div(nrb, nrc);
-  s.nrc = ceil_div(nrb, s.rbc);
-  s.nbu = ceil_div(kr > 0 ? kr : 1, 256);
+  const int64_t nrc = std::max<int64_t>(ceil_div(nrbd, kTabWords), std::min(ceil_div(4096, wpr), nrbd));
+  s.rbc = ceil_div(nrbd, nrc);
+  s.nrc = ceil_div(nrbd, s.rbc);
+  // workgroups of the sparse rows in pass A (rows) and pass B (players), at
+  // most 2048 each (each wave loops), and of the bit rows in the row pass
+  s.nsa = s.rs > 0 ? std::min<int64_t>(ceil_div(s.rs, kWaves), 2048) : 0;
+  s.nsb = s.rs > 0 ? std::min<int64_t>(ceil_div(M, kWaves), 2048) : 0;
+  s.nrcd = s.rbd0 < s.nrb ? s.nrc : 0;
+  s.nbu = s.nsa + ceil_div(kr - s.rs > 0 ? kr - s.rs : 1, 256);
   s.nbc = ceil_div(wpr * 64, 256);
   return s;
 }
@@ -446,6 +639,11 @@ gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
   w.sz = c.take<int32_t>(kr);
   w.blocked = c.take<uint64_t>((sh.nrb > 0 ? sh.nrb : 1) * sh.wpr * 64);
   w.st = c.take<CgState>(1);
+  w.csr_ptr = c.take<int64_t>(sh.rs + 1);
+  w.csr_idx = c.take<int32_t>(sh.nnz > 0 ? sh.nnz : 1);
+  w.csc_ptr = c.take<int64_t>(sh.M + 1);
+  w.csc_row = c.take<int32_t>(sh.nnz > 0 ? sh.nnz : 1);
+  w.qs = c.take<double>(sh.M);
   return w;
 }
 
@@ -480,6 +678,18 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
   a.rr = w.rr;
   a.hist = w.hist;
   a.st = w.st;
+  a.rs = sh.rs;
+  a.rbd0 = sh.rbd0;
+  a.nsa = sh.nsa;
+  a.nsb = sh.nsb;
+  a.nrcd = sh.nrcd;
+  a.nxa = ceil_div(std::max<int64_t>(sh.nrb - sh.rbd0, 1), kWaves);
+  a.nxb = ceil_div(sh.wpr, kWaves);
+  a.csr_ptr = w.csr_ptr;
+  a.csr_idx = w.csr_idx;
+  a.csc_ptr = w.csc_ptr;
+  a.csc_row = w.csc_row;
+  a.qs = w.qs;
   a.host_flag = hf->dev;
   // no kernel of an earlier solve of this thread writes the flag any more:
   // each solve returns only after its stopping iteration has run
@@ -491,10 +701,30 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
                                                             w.sz);
   }
   GS_LAUNCHED();
+  if (sh.rs > 0) {
+    // the sparse rows' lists (row sizes from k_cg_init); qs serves as the
+    // count scratch here, it is written before the iterations read it
+    const int64_t nrb_s = sh.rs / 64;
+    GS_TIMED("k_cg_sparse_build", s);
+    k_cg_csr_ptr<<<1, 1024, 0, s>>>(w.sz, sh.rs, w.csr_ptr);
+    GS_LAUNCHED();
+    k_cg_csr_fill<<<static_cast<unsigned>(nrb_s), 64, 0, s>>>(pr.blocked, sh.wpr, sh.rs, w.csr_ptr, sh.nnz,
+                                                             w.csr_idx);
+    GS_LAUNCHED();
+    int64_t* cnt = reinterpret_cast<int64_t*>(w.qs);
+    k_cg_csc_count<<<static_cast<unsigned>(ceil_div(sh.M, 256)), 256, 0, s>>>(pr.T, sh.M, nrb_s, cnt);
+    GS_LAUNCHED();
+    k_cg_csc_scan<<<1, 1024, 0, s>>>(cnt, sh.M, w.csc_ptr);
+    GS_LAUNCHED();
+    k_cg_csc_fill<<<static_cast<unsigned>(ceil_div(sh.M, 256)), 256, 0, s>>>(pr.T, sh.M, nrb_s, w.csc_ptr, sh.nnz,
+                                                                            w.csc_row);
+    GS_LAUNCHED();
+  }
   const bool random = sh.kr > 0;
-  const dim3 ga(static_cast<unsigned>(ceil_div(std::max<int64_t>(sh.nrb, 1), kWaves)),
-                static_cast<unsigned>(sh.npc));
-  const dim3 gb(static_cast<unsigned>(ceil_div(sh.wpr, kWaves)), static_cast<unsigned>(sh.nrc));
+  const int64_t sparse = sh.rs > 0 ? 1 : 0;
+  const dim3 ga(static_cast<unsigned>(std::max(a.nxa, sh.nsa)), static_cast<unsigned>(sh.npc + sparse));
+  const dim3 gb(static_cast<unsigned>(std::max(a.nxb, sh.nsb)), static_cast<unsigned>(sh.nrcd + sparse));
+  const unsigned g_rows = static_cast<unsigned>(sh.nbu - sh.nsa);
   // Iterations 0 .. kMaxIt - 1 in full; pass A alone of iteration kMaxIt
   // (it always stops).  The host waits for chunk c - 1 after queueing chunk c.
   int64_t t = 0, chunk = 0;
@@ -511,7 +741,7 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
       if (random) {
         {
           GS_TIMED("k_cg_rows", s);
-          k_cg_rows<<<static_cast<unsigned>(sh.nbu), 256, 0, s>>>(a);
+          k_cg_rows<<<g_rows, 256, 0, s>>>(a);
         }
         GS_LAUNCHED();
         {
@@ -536,7 +766,7 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
   if (!stopped) GS_HIP(hipEventSynchronize(hf->ev[(chunk - 1) & 1]));
   const int64_t iters = __atomic_load_n(hf->host + 1, __ATOMIC_ACQUIRE);
   if (iters_out) *iters_out = iters;
-  timing_note_solve(sh.M, sh.wpr, sh.kr, iters);
+  timing_note_solve(sh.M, sh.wpr, sh.kr, iters, sh.rs, sh.nnz);
   {
     GS_TIMED("k_cg_finish", s);
     // without enumerated classes, fewer than M - 1 random rows cannot

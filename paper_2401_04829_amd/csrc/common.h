@@ -56,8 +56,9 @@ class KernelTimer {
 };
 
 // Records an iterative solve (players, words per row, random rows,
-// iterations run) for gnnshap_timing_solves while timing is armed.
-void timing_note_solve(int64_t M, int64_t wpr, int64_t kr, int64_t iters);
+// iterations run, sparse rows, their players) for gnnshap_timing_solves
+// while timing is armed.
+void timing_note_solve(int64_t M, int64_t wpr, int64_t kr, int64_t iters, int64_t rs, int64_t nnz);
 
 // Largest dynamic LDS allocation one workgroup may request on the current device.
 inline int max_lds_bytes() {

@@ -62,8 +62,20 @@ struct Ws {
 // Systems above the process-wide threshold are solved iteratively (Sec. 3.5).
 bool iterative(const gnnshap_sample_plan* p) { return p->num_players > gnnshap::iterative_threshold(); }
 
-gnnshap::CgShape cg_shape_of(const gnnshap_sample_plan* p) {
-  return gnnshap::cg_shape(p->num_players, p->words_per_row, p->num_rows / 2 - p->random_begin);
+// The iterative solver's shape for a plan and its class table; without a
+// table (workspace queries), for the table gnnshap_plan_samples gives the plan.
+gnnshap::CgShape cg_shape_of(const gnnshap_sample_plan* p, const gnnshap_class* classes = nullptr) {
+  const int64_t kr = p->num_rows / 2 - p->random_begin;
+  if (classes)
+    return gnnshap::cg_shape(p->num_players, p->words_per_row, kr, p->random_begin, classes, p->num_classes);
+  gnnshap_sample_plan q = *p;
+  std::vector<gnnshap_class> tab(static_cast<size_t>(std::max<int64_t>(p->num_classes, 1)));
+  if (gnnshap_plan_samples(&q, tab.data(), static_cast<int64_t>(tab.size())) != GNNSHAP_OK ||
+      q.num_rows != p->num_rows || q.random_begin != p->random_begin || q.num_classes != p->num_classes) {
+    gnnshap::clear_error();
+    return gnnshap::cg_shape(p->num_players, p->words_per_row, kr, p->random_begin, nullptr, 0);
+  }
+  return gnnshap::cg_shape(p->num_players, p->words_per_row, kr, p->random_begin, tab.data(), q.num_classes);
 }
 
 // Row stride of G: a multiple of 64 floats keeps every row 256-byte aligned.
@@ -86,7 +98,7 @@ constexpr int kTileClasses = 256;                         // classes of a system
 
 int64_t tile_chunks(int64_t half) { return gnnshap::ceil_div(half, kTileRows); }
 
-Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
+Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p, const gnnshap_class* classes = nullptr) {
   Ws w;
   const int64_t M = p->num_players;
   const int64_t half = p->num_rows / 2;
@@ -103,7 +115,7 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p) {
     w.dv = c.take<double>(M);
     w.bsum = c.take<double>(gnnshap::ceil_div(M, 256));
     w.rhs = w.x = w.Winv = w.Wd = nullptr;
-    w.cg = gnnshap::cg_carve(c, cg_shape_of(p));
+    w.cg = gnnshap::cg_carve(c, cg_shape_of(p, classes));
     return w;
   }
   w.cg = gnnshap::CgWs{};
@@ -1919,10 +1931,10 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
   if (int st = check_plan(plan, classes)) return st;
   gnnshap::Carver need(nullptr);
-  carve(need, plan);
+  carve(need, plan, classes);
   if (ws_bytes < need.bytes()) return gnnshap::fail(GNNSHAP_ECAPACITY, "solve workspace needs %zu bytes", need.bytes());
   gnnshap::Carver cv(ws);
-  const Ws w = carve(cv, plan);
+  const Ws w = carve(cv, plan, classes);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t M = plan->num_players;
   const int64_t ld = ld_of(M);
@@ -1978,7 +1990,7 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     pr.fef = f_empty_full;
     pr.phi = phi;
     pr.info = info;
-    return gnnshap::cg_solve(pr, cg_shape_of(plan), w.cg, s, nullptr);
+    return gnnshap::cg_solve(pr, cg_shape_of(plan, classes), w.cg, s, nullptr);
   }
   int32_t* counts = reinterpret_cast<int32_t*>(w.G);
   if (has_random) {

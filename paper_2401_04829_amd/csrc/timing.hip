@@ -14,14 +14,14 @@ std::atomic<bool> g_on{false};
 std::mutex g_mu;
 std::string g_name;
 std::vector<std::pair<hipEvent_t, hipEvent_t>> g_recs;
-std::vector<int64_t> g_solves;   // 4 per iterative solve while armed
+std::vector<int64_t> g_solves;   // 6 per iterative solve while armed
 }  // namespace
 
-void timing_note_solve(int64_t M, int64_t wpr, int64_t kr, int64_t iters) {
+void timing_note_solve(int64_t M, int64_t wpr, int64_t kr, int64_t iters, int64_t rs, int64_t nnz) {
   if (!g_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on.load()) return;
-  g_solves.insert(g_solves.end(), {M, wpr, kr, iters});
+  g_solves.insert(g_solves.end(), {M, wpr, kr, iters, rs, nnz});
 }
 
 KernelTimer::KernelTimer(const char* name, hipStream_t s) : stream_(s) {
@@ -87,7 +87,7 @@ extern "C" int gnnshap_timing_solves(int64_t* records, int64_t cap, int64_t* cou
   gnnshap::clear_error();
   if (!count || cap < 0 || (cap > 0 && !records)) return gnnshap::fail(GNNSHAP_EINVAL, "bad arguments");
   std::lock_guard<std::mutex> lk(gnnshap::g_mu);
-  const int64_t n = static_cast<int64_t>(gnnshap::g_solves.size() / 4);
+  const int64_t n = static_cast<int64_t>(gnnshap::g_solves.size() / 6);
   *count = n;
   if (cap < n) return gnnshap::fail(GNNSHAP_ECAPACITY, "%lld solve records", static_cast<long long>(n));
   std::copy(gnnshap::g_solves.begin(), gnnshap::g_solves.end(), records);
