@@ -227,28 +227,30 @@ __device__ __forceinline__ double wave_gather_sum(const int32_t* __restrict__ id
   return wave_sum_d((s4[0] + s4[1]) + (s4[2] + s4[3]));
 }
 
-// Pass A.  Workgroups (x, y < npc): upart[y, b] = sum over the words of
-// player chunk y of the bits of bit row b times r; the workgroup builds the
-// chunk's nibble tables of r in LDS (r is padded with zeros to whole words),
-// then one wave per 64 rows (lane = row) reads the row-blocked words, 512
-// contiguous bytes per word, and sums table entries.  Workgroups (x, npc),
-// x < nsa: the sparse rows x * kWaves + wave, + nsa * kWaves, ...: u_b = sum
-// of r over the row's players, with the workgroup's partial |u|^2 and |m|.u
-// in uu[2 x], uu[2 x + 1].  Both kinds take the stopping test first.
+// Pass A.  Workgroup y * nxa + x (y < npc): upart[y, b] = sum over the words
+// of player chunk y of the bits of bit row b times r; the workgroup builds
+// the chunk's nibble tables of r in LDS (r is padded with zeros to whole
+// words), then one wave per 64 rows (lane = row) reads the row-blocked
+// words, 512 contiguous bytes per word, and sums table entries.  Workgroup
+// nxa * npc + x (x < nsa): the sparse rows x * kWaves + wave, + nsa * kWaves,
+// ...: u_b = sum of r over the row's players, with the workgroup's partial
+// |u|^2 and |m|.u in uu[2 x], uu[2 x + 1].  Both kinds take the stopping
+// test first.
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_t* __restrict__ blocked,
                                                           const double* __restrict__ r,
                                                           double* __restrict__ upart, int64_t t) {
   extern __shared__ double tab[];   // pwords * 256
   __shared__ double red[kWaves];
-  const int64_t pc = blockIdx.y;
-  // the grid's x extent is the larger of the two kinds': idle workgroups leave at once
-  if (a.st->done || static_cast<int64_t>(blockIdx.x) >= (pc == a.npc ? a.nsa : a.nxa)) return;
+  if (a.st->done) return;
+  // one flat grid: nxa x npc bit-row workgroups, then nsa sparse-row ones
+  const int64_t bid = blockIdx.x;
+  const int64_t pc = bid < a.nxa * a.npc ? bid / a.nxa : a.npc;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const bool writer = blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0;
+  const bool writer = bid == 0 && threadIdx.x == 0;
   if (pc == a.npc) {                  // sparse rows
     if (cg_stop(a, t, false)) return;
-    const int64_t x = blockIdx.x;
+    const int64_t x = bid - a.nxa * a.npc;
     double uu = 0.0, su = 0.0;
     for (int64_t b = x * kWaves + wave; b < a.rs; b += a.nsa * kWaves) {
       const int64_t e0 = a.csr_ptr[b];
@@ -267,7 +269,7 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
     }
     return;
   }
-  const int64_t rb = a.rbd0 + static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  const int64_t rb = a.rbd0 + (bid % a.nxa) * kWaves + wave;
   const int64_t w0 = pc * a.pwords;
   const int64_t w1 = w0 + a.pwords < a.wpr ? w0 + a.pwords : a.wpr;
   const int64_t nw = w1 - w0;
@@ -311,24 +313,25 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
   }
 }
 
-// Pass B.  Workgroups (x, c < nrcd): qpart[c, j] = sum over the row blocks of
-// chunk c of the bits of player j times u; the workgroup builds the chunk's
-// nibble tables of u in LDS (u is padded with zeros to whole row blocks),
-// then one wave per 64 players (lane = player) reads the bit-transposed words
-// T[rb, j] and sums table entries.  Workgroups (x, nrcd), x < nsb: the
-// players x * kWaves + wave, + nsb * kWaves, ...: qs[j] = sum of u over the
-// sparse rows holding player j.
+// Pass B.  Workgroup c * nxb + x (c < nrcd): qpart[c, j] = sum over the row
+// blocks of chunk c of the bits of player j times u; the workgroup builds
+// the chunk's nibble tables of u in LDS (u is padded with zeros to whole row
+// blocks), then one wave per 64 players (lane = player) reads the
+// bit-transposed words T[rb, j] and sums table entries.  Workgroup
+// nxb * nrcd + x (x < nsb): the players x * kWaves + wave, + nsb * kWaves,
+// ...: qs[j] = sum of u over the sparse rows holding player j.
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_t* __restrict__ T,
                                                           const double* __restrict__ u,
                                                           double* __restrict__ qpart) {
   extern __shared__ double tab[];   // rbc * 256
-  const int64_t c = blockIdx.y;
-  // the grid's x extent is the larger of the two kinds': idle workgroups leave at once
-  if (a.st->done || static_cast<int64_t>(blockIdx.x) >= (c == a.nrcd ? a.nsb : a.nxb)) return;
+  if (a.st->done) return;
+  // one flat grid: nxb x nrcd bit-row workgroups, then nsb sparse-row ones
+  const int64_t bid = blockIdx.x;
+  const int64_t c = bid < a.nxb * a.nrcd ? bid / a.nxb : a.nrcd;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (c == a.nrcd) {                  // sparse rows
-    const int64_t x = blockIdx.x;
+    const int64_t x = bid - a.nxb * a.nrcd;
     for (int64_t j = x * kWaves + wave; j < a.M; j += a.nsb * kWaves) {
       const int64_t e0 = a.csc_ptr[j];
       const double v = wave_gather_sum(a.csc_row + e0, a.csc_ptr[j + 1] - e0, u);
@@ -336,7 +339,7 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_
     }
     return;
   }
-  const int64_t g = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  const int64_t g = (bid % a.nxb) * kWaves + wave;
   const int64_t b0 = a.rbd0 + c * a.rbc;
   const int64_t b1 = b0 + a.rbc < a.nrb ? b0 + a.rbc : a.nrb;
   const int64_t nb = b1 - b0;
@@ -721,9 +724,8 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
     GS_LAUNCHED();
   }
   const bool random = sh.kr > 0;
-  const int64_t sparse = sh.rs > 0 ? 1 : 0;
-  const dim3 ga(static_cast<unsigned>(std::max(a.nxa, sh.nsa)), static_cast<unsigned>(sh.npc + sparse));
-  const dim3 gb(static_cast<unsigned>(std::max(a.nxb, sh.nsb)), static_cast<unsigned>(sh.nrcd + sparse));
+  const unsigned ga = static_cast<unsigned>(a.nxa * sh.npc + sh.nsa);
+  const unsigned gb = static_cast<unsigned>(a.nxb * sh.nrcd + sh.nsb);
   const unsigned g_rows = static_cast<unsigned>(sh.nbu - sh.nsa);
   // Iterations 0 .. kMaxIt - 1 in full; pass A alone of iteration kMaxIt
   // (it always stops).  The host waits for chunk c - 1 after queueing chunk c.
