@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "batch.h"
+#include "cg.h"
 #include "common.h"
 
 namespace gnnshap {
@@ -30,6 +31,7 @@ constexpr int kSideStreams = 2;
 struct SideStream {
   hipStream_t stream = nullptr;
   hipEvent_t fork = nullptr, join = nullptr, aux = nullptr;
+  hipEvent_t rest_out = nullptr;   // end of the one-by-one solves queued on this stream
 };
 
 struct DeviceSides {
@@ -49,7 +51,8 @@ SideStream* side_stream(int i) {
     if (hipStreamCreateWithFlags(&x.stream, hipStreamNonBlocking) != hipSuccess ||
         hipEventCreateWithFlags(&x.fork, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&x.aux, hipEventDisableTiming) != hipSuccess) {
+        hipEventCreateWithFlags(&x.aux, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&x.rest_out, hipEventDisableTiming) != hipSuccess) {
       (void)hipGetLastError();
       return nullptr;
     }
@@ -504,6 +507,56 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
         }
         return GNNSHAP_OK;
       };
+      // The systems solved one by one (too large for the batched kernels):
+      // up to three in flight, on `home` and the two side streams (forked
+      // from `home` after everything queued there so far, joined back at the
+      // end), so that one system's iteration overlaps another's; each
+      // iterative solve is stepped chunk by chunk in turn.
+      auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home) -> int {
+        if (rest.empty()) return GNNSHAP_OK;
+        hipStream_t lanes[3] = {home, nullptr, nullptr};
+        gnnshap::SideStream* side[3] = {nullptr, nullptr, nullptr};
+        int nl = 1;
+        if (rest.size() >= 2) {
+          for (int i = 0; i < 2; ++i) {
+            gnnshap::SideStream* ss = gnnshap::side_stream(i);
+            if (!ss) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+            side[nl] = ss;
+            lanes[nl++] = ss->stream;
+          }
+          static thread_local hipEvent_t rest_in = nullptr;
+          if (!rest_in) GS_HIP(hipEventCreateWithFlags(&rest_in, hipEventDisableTiming));
+          GS_HIP(hipEventRecord(rest_in, home));
+          for (int l = 1; l < nl; ++l) GS_HIP(hipStreamWaitEvent(lanes[l], rest_in, 0));
+        }
+        gnnshap::CgRun runs[3];
+        size_t next = 0;
+        for (;;) {
+          for (int l = 0; l < nl; ++l) {
+            while (!runs[l].begun() && next < rest.size()) {
+              const int64_t t = rest[next++];
+              if (int st = gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t],
+                                                    y + L.row_off[t], f_empty_full + 2 * t, phi + L.player_off[t],
+                                                    info + t, b.solve_slice[t], L.solve_bytes[t], lanes[l], &runs[l]))
+                return st;
+            }
+          }
+          bool any = false;
+          for (int l = 0; l < nl; ++l) {
+            if (!runs[l].begun()) continue;
+            any = true;
+            if (int st = runs[l].step()) return st;
+            if (runs[l].done())
+              if (int st = runs[l].finish(nullptr)) return st;
+          }
+          if (!any && next >= rest.size()) break;
+        }
+        for (int l = 1; l < nl; ++l) {
+          GS_HIP(hipEventRecord(side[l]->rest_out, lanes[l]));
+          GS_HIP(hipStreamWaitEvent(home, side[l]->rest_out, 0));
+        }
+        return GNNSHAP_OK;
+      };
       // right-hand side, then the factorisations and solves of group gi:
       // one-workgroup systems (G~ built in place, then factorisation and
       // solves in one kernel) once the counts are ready; panel-path systems
@@ -527,13 +580,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
             if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
           }
         }
-        for (int64_t t : G.rest) {
-          if (int st = gnnshap_solve_wls(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
-                                         f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
-                                         L.solve_bytes[t], gs[gi]))
-            return st;
-        }
-        return GNNSHAP_OK;
+        return solve_rest(G.rest, gs[gi]);
       };
       // G~ first: it depends on the masks only, and queued ahead of the
       // evaluations it gets the GPU before their many workgroups fill it

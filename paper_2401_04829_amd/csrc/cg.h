@@ -2,6 +2,8 @@
 // large systems are fitted iteratively instead of being factored).
 #pragma once
 
+#include <memory>
+
 #include "common.h"
 
 namespace gnnshap {
@@ -25,6 +27,7 @@ struct CgWs {
   double* u;       // nrb * 64: R r, zero beyond kr
   double* qpart;   // nrc x M: partial products R^T u per row chunk
   double* uu;      // nbu x 2: partial |u|^2 and |m|.u
+  double* usp;     // nsa x 2: the same over the sparse rows, per pass-A workgroup
   double* rr;      // 3 x nbc: partial r.r of iterations t mod 3
   double* hist;    // 2: step lengths of even and odd iterations
   int32_t* sz;     // kr: sizes of the random representative rows
@@ -46,8 +49,8 @@ struct CgShape {
   int64_t rbd0;            // first row block of the bit products (rs / 64)
   int64_t npc, pwords;     // product R r: player chunks of pwords words
   int64_t nrc, rbc;        // product R^T u: row chunks of rbc row blocks
-  int64_t nbu, nbc;        // partial sums of the row passes (pass A's sparse workgroups, then the row
-                           // pass's), workgroups of the player passes
+  int64_t nbu, nbc;        // partial sums of the row pass (the sparse rows' total, then one per
+                           // workgroup of bit rows; also its workgroups), workgroups of the player passes
   int64_t nsa, nsb;        // sparse workgroups of pass A (rows) and pass B (players)
   int64_t nrcd;            // row chunks of pass B's bit rows (0 without bit rows)
 };
@@ -76,6 +79,32 @@ struct CgProblem {
   const float* fef;     // f(empty), f(full)
   float* phi;
   int32_t* info;
+};
+
+struct CgArgs;
+
+// One iterative solve driven chunk by chunk, so that a caller can keep
+// several solves in flight, each on its own stream: begin() queues the
+// set-up, every step() queues the next chunk of iterations and waits for the
+// chunk before it (until the iteration has stopped: done()), finish() waits
+// for the stopping iteration, queues phi and info and leaves the object
+// ready for another solve.  At most 8 solves per host thread are in flight
+// at once (each holds a mapped stop flag).
+class CgRun {
+ public:
+  CgRun();
+  ~CgRun();
+  CgRun(const CgRun&) = delete;
+  CgRun& operator=(const CgRun&) = delete;
+  int begin(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s);
+  int step();
+  bool done() const { return stopped_; }
+  bool begun() const { return static_cast<bool>(st_); }
+  int finish(int64_t* iters_out);
+
+ private:
+  std::unique_ptr<CgArgs> st_;
+  bool stopped_ = true;
 };
 
 // Conjugate gradients on 1-perp; returns once the iteration has stopped

@@ -81,6 +81,7 @@ struct Args {
   double* u;       // nrb * 64 (zero beyond kr)
   double* qpart;
   double* uu;
+  double* usp;     // 2 x nsa: pass A's sparse-row partials
   double* rr;      // 3 x nbc
   double* hist;    // step length of even and odd iterations
   gnnshap::CgState* st;
@@ -264,8 +265,8 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
     const double s1 = block_sum_d(uu, red);
     const double s2 = block_sum_d(su, red);
     if (threadIdx.x == 0) {
-      a.uu[2 * x] = s1;
-      a.uu[2 * x + 1] = s2;
+      a.usp[2 * x] = s1;
+      a.usp[2 * x + 1] = s2;
     }
     return;
   }
@@ -292,10 +293,19 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
 }
 
 // u of the bit rows (the sum of their pass-A chunks, one lane per row) with
-// partial |u|^2 and |m|.u in uu[2 (nsa + x)], uu[2 (nsa + x) + 1].
+// partial |u|^2 and |m|.u in uu[2 (1 + x)], uu[2 (1 + x) + 1]; the last
+// workgroup adds pass A's sparse-row partials into uu[0], uu[1] (fixed order).
 __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
   __shared__ double red[4];
   if (a.st->done) return;
+  if (static_cast<int64_t>(blockIdx.x) == a.nbu - 1) {
+    const int wv = threadIdx.x >> 6;
+    if (wv < 2) {
+      const double v = a.nsa > 0 ? wave_fixed_sum(a.usp + wv, a.nsa, 2) : 0.0;
+      if ((threadIdx.x & 63) == 0) a.uu[wv] = v;
+    }
+    return;
+  }
   const int64_t b = a.rs + static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   double uu = 0.0, su = 0.0;
   if (b < a.kr) {
@@ -308,8 +318,8 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
   const double s1 = block_sum_d(uu, red);
   const double s2 = block_sum_d(su, red);
   if (threadIdx.x == 0) {
-    a.uu[2 * (a.nsa + blockIdx.x)] = s1;
-    a.uu[2 * (a.nsa + blockIdx.x) + 1] = s2;
+    a.uu[2 * (1 + blockIdx.x)] = s1;
+    a.uu[2 * (1 + blockIdx.x) + 1] = s2;
   }
 }
 
@@ -536,37 +546,46 @@ __global__ void __launch_bounds__(1024) k_cg_finish(const double* __restrict__ x
   if (threadIdx.x == 0) *info = (st->status == 0 && !undetermined) ? 0 : static_cast<int32_t>(M + 1);
 }
 
-// Mapped page-locked stopping flag of the calling thread, its device address
-// and the two events of the chunked wait (kept until the process ends).
+// Mapped page-locked stopping flags of the calling thread, their device
+// addresses and the two events of each solve's chunked wait: one slot per
+// solve in flight (created on first use, kept until the process ends).
 struct HostFlag {
   int32_t* host = nullptr;
   int32_t* dev = nullptr;
   hipEvent_t ev[2] = {nullptr, nullptr};
+  bool busy = false;
 };
 
-HostFlag* host_flag() {
-  static thread_local HostFlag f;
-  if (!f.host) {
-    void* h = nullptr;
-    if (hipHostMalloc(&h, 256, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
-      (void)hipGetLastError();
-      return nullptr;
-    }
-    void* d = nullptr;
-    if (hipHostGetDevicePointer(&d, h, 0) != hipSuccess) {
-      (void)hipGetLastError();
-      (void)hipHostFree(h);
-      return nullptr;
-    }
-    for (int i = 0; i < 2; ++i)
-      if (hipEventCreateWithFlags(&f.ev[i], hipEventDisableTiming) != hipSuccess) {
+constexpr int kFlagSlots = 8;
+
+HostFlag* acquire_flag() {
+  static thread_local HostFlag pool[kFlagSlots];
+  for (HostFlag& f : pool) {
+    if (f.busy) continue;
+    if (!f.host) {
+      void* h = nullptr;
+      if (hipHostMalloc(&h, 256, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
         (void)hipGetLastError();
         return nullptr;
       }
-    f.host = static_cast<int32_t*>(h);
-    f.dev = static_cast<int32_t*>(d);
+      void* d = nullptr;
+      if (hipHostGetDevicePointer(&d, h, 0) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipHostFree(h);
+        return nullptr;
+      }
+      for (int i = 0; i < 2; ++i)
+        if (hipEventCreateWithFlags(&f.ev[i], hipEventDisableTiming) != hipSuccess) {
+          (void)hipGetLastError();
+          return nullptr;
+        }
+      f.host = static_cast<int32_t*>(h);
+      f.dev = static_cast<int32_t*>(d);
+    }
+    f.busy = true;
+    return &f;
   }
-  return &f;
+  return nullptr;
 }
 
 std::atomic<int64_t> g_threshold{5000};
@@ -621,7 +640,7 @@ gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t r
   s.nsa = s.rs > 0 ? std::min<int64_t>(ceil_div(s.rs, kWaves), 2048) : 0;
   s.nsb = s.rs > 0 ? std::min<int64_t>(ceil_div(M, kWaves), 2048) : 0;
   s.nrcd = s.rbd0 < s.nrb ? s.nrc : 0;
-  s.nbu = s.nsa + ceil_div(kr - s.rs > 0 ? kr - s.rs : 1, 256);
+  s.nbu = 1 + ceil_div(kr - s.rs > 0 ? kr - s.rs : 1, 256);
   s.nbc = ceil_div(wpr * 64, 256);
   return s;
 }
@@ -637,6 +656,7 @@ gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
   w.u = c.take<double>((sh.nrb > 0 ? sh.nrb : 1) * 64);
   w.qpart = c.take<double>(sh.nrc * sh.M);
   w.uu = c.take<double>(2 * sh.nbu);
+  w.usp = c.take<double>(2 * (sh.nsa > 0 ? sh.nsa : 1));
   w.rr = c.take<double>(3 * sh.nbc);
   w.hist = c.take<double>(2);
   w.sz = c.take<int32_t>(kr);
@@ -650,10 +670,35 @@ gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
   return w;
 }
 
-int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out) {
-  HostFlag* hf = host_flag();
-  if (!hf) return fail(GNNSHAP_EHIP, "could not allocate the solver's host flag");
-  Args a{};
+struct gnnshap::CgArgs {
+  Args a;
+  CgShape sh;
+  CgProblem pr;
+  CgWs w;
+  hipStream_t s = nullptr;
+  HostFlag* hf = nullptr;
+  unsigned ga = 0, gb = 0, g_rows = 0;
+  int64_t t = 0, chunk = 0;
+};
+
+gnnshap::CgRun::CgRun() = default;
+gnnshap::CgRun::~CgRun() {
+  if (st_ && st_->hf) st_->hf->busy = false;
+}
+
+int gnnshap::CgRun::begin(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s) {
+  HostFlag* hf = acquire_flag();
+  if (!hf) return fail(GNNSHAP_EHIP, "could not allocate the solver's host flag (or more than %d solves in flight)",
+                       kFlagSlots);
+  st_.reset(new CgArgs());
+  CgArgs& c = *st_;
+  c.hf = hf;
+  c.sh = sh;
+  c.pr = pr;
+  c.w = w;
+  c.s = s;
+  stopped_ = false;
+  Args& a = c.a;
   a.sz = w.sz;
   a.M = sh.M;
   a.wpr = sh.wpr;
@@ -678,6 +723,7 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
   a.u = w.u;
   a.qpart = w.qpart;
   a.uu = w.uu;
+  a.usp = w.usp;
   a.rr = w.rr;
   a.hist = w.hist;
   a.st = w.st;
@@ -694,8 +740,11 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
   a.csc_row = w.csc_row;
   a.qs = w.qs;
   a.host_flag = hf->dev;
-  // no kernel of an earlier solve of this thread writes the flag any more:
-  // each solve returns only after its stopping iteration has run
+  c.ga = static_cast<unsigned>(a.nxa * sh.npc + sh.nsa);
+  c.gb = static_cast<unsigned>(a.nxb * sh.nrcd + sh.nsb);
+  c.g_rows = static_cast<unsigned>(sh.nbu);
+  // no kernel of an earlier solve that used this flag writes it any more:
+  // a solve releases its flag only after its stopping iteration has run
   __atomic_store_n(hf->host, 0, __ATOMIC_RELEASE);
   __atomic_store_n(hf->host + 1, -1, __ATOMIC_RELEASE);
   {
@@ -723,32 +772,38 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
                                                                             w.csc_row);
     GS_LAUNCHED();
   }
+  return GNNSHAP_OK;
+}
+
+// Queues iterations t .. t + kChunk - 1 (pass A alone of iteration kMaxIt,
+// which always stops), records the chunk's event, then waits for the chunk
+// queued before it and reads the stop flag.
+int gnnshap::CgRun::step() {
+  if (!st_ || stopped_) return GNNSHAP_OK;
+  CgArgs& c = *st_;
+  const Args& a = c.a;
+  const CgShape& sh = c.sh;
+  hipStream_t s = c.s;
   const bool random = sh.kr > 0;
-  const unsigned ga = static_cast<unsigned>(a.nxa * sh.npc + sh.nsa);
-  const unsigned gb = static_cast<unsigned>(a.nxb * sh.nrcd + sh.nsb);
-  const unsigned g_rows = static_cast<unsigned>(sh.nbu - sh.nsa);
-  // Iterations 0 .. kMaxIt - 1 in full; pass A alone of iteration kMaxIt
-  // (it always stops).  The host waits for chunk c - 1 after queueing chunk c.
-  int64_t t = 0, chunk = 0;
-  bool stopped = false;
-  while (t <= kMaxIt && !stopped) {
-    const int64_t t_end = std::min(t + kChunk, kMaxIt + 1);
-    for (; t < t_end; ++t) {
+  if (c.t <= kMaxIt) {
+    const int64_t t_end = std::min(c.t + kChunk, kMaxIt + 1);
+    for (; c.t < t_end; ++c.t) {
+      const int64_t t = c.t;
       {
         GS_TIMED("k_cg_pass_a", s);
-        k_cg_pass_a<<<ga, kWaves * 64, sh.pwords * 256 * sizeof(double), s>>>(a, pr.blocked, w.r, w.upart, t);
+        k_cg_pass_a<<<c.ga, kWaves * 64, sh.pwords * 256 * sizeof(double), s>>>(a, c.pr.blocked, c.w.r, c.w.upart, t);
       }
       GS_LAUNCHED();
       if (t == kMaxIt) continue;
       if (random) {
         {
           GS_TIMED("k_cg_rows", s);
-          k_cg_rows<<<g_rows, 256, 0, s>>>(a);
+          k_cg_rows<<<c.g_rows, 256, 0, s>>>(a);
         }
         GS_LAUNCHED();
         {
           GS_TIMED("k_cg_pass_b", s);
-          k_cg_pass_b<<<gb, kWaves * 64, sh.rbc * 256 * sizeof(double), s>>>(a, pr.T, w.u, w.qpart);
+          k_cg_pass_b<<<c.gb, kWaves * 64, sh.rbc * 256 * sizeof(double), s>>>(a, c.pr.T, c.w.u, c.w.qpart);
         }
         GS_LAUNCHED();
       }
@@ -758,24 +813,45 @@ int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hip
       }
       GS_LAUNCHED();
     }
-    GS_HIP(hipEventRecord(hf->ev[chunk & 1], s));
-    if (chunk > 0) {
-      GS_HIP(hipEventSynchronize(hf->ev[(chunk - 1) & 1]));
-      stopped = __atomic_load_n(hf->host, __ATOMIC_ACQUIRE) != 0;
+    GS_HIP(hipEventRecord(c.hf->ev[c.chunk & 1], s));
+    if (c.chunk > 0) {
+      GS_HIP(hipEventSynchronize(c.hf->ev[(c.chunk - 1) & 1]));
+      stopped_ = __atomic_load_n(c.hf->host, __ATOMIC_ACQUIRE) != 0;
     }
-    ++chunk;
+    ++c.chunk;
+  } else {
+    stopped_ = true;     // every iteration is queued; finish() waits for the last chunk
   }
-  if (!stopped) GS_HIP(hipEventSynchronize(hf->ev[(chunk - 1) & 1]));
-  const int64_t iters = __atomic_load_n(hf->host + 1, __ATOMIC_ACQUIRE);
+  return GNNSHAP_OK;
+}
+
+int gnnshap::CgRun::finish(int64_t* iters_out) {
+  if (!st_) return fail(GNNSHAP_EINVAL, "solve not begun");
+  CgArgs& c = *st_;
+  if (c.chunk > 0) GS_HIP(hipEventSynchronize(c.hf->ev[(c.chunk - 1) & 1]));
+  const int64_t iters = __atomic_load_n(c.hf->host + 1, __ATOMIC_ACQUIRE);
   if (iters_out) *iters_out = iters;
+  const CgShape& sh = c.sh;
   timing_note_solve(sh.M, sh.wpr, sh.kr, iters, sh.rs, sh.nnz);
   {
-    GS_TIMED("k_cg_finish", s);
+    GS_TIMED("k_cg_finish", c.s);
     // without enumerated classes, fewer than M - 1 random rows cannot
     // determine psi (1-perp has M - 1 dimensions): reported like a failed pivot
-    const int32_t undetermined = (pr.alpha == 0.0 && sh.kr < sh.M - 1) ? 1 : 0;
-    k_cg_finish<<<1, 1024, 0, s>>>(w.x, sh.M, w.st, pr.fef, pr.phi, pr.info, undetermined);
+    const int32_t undetermined = (c.pr.alpha == 0.0 && sh.kr < sh.M - 1) ? 1 : 0;
+    k_cg_finish<<<1, 1024, 0, c.s>>>(c.w.x, sh.M, c.w.st, c.pr.fef, c.pr.phi, c.pr.info, undetermined);
   }
   GS_LAUNCHED();
+  c.hf->busy = false;
+  c.hf = nullptr;
+  st_.reset();
+  stopped_ = true;
   return GNNSHAP_OK;
+}
+
+int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out) {
+  CgRun run;
+  if (int st = run.begin(pr, sh, w, s)) return st;
+  while (!run.done())
+    if (int st = run.step()) return st;
+  return run.finish(iters_out);
 }

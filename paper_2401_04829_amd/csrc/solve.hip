@@ -1922,9 +1922,12 @@ extern "C" int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* 
   return GNNSHAP_OK;
 }
 
-extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_class* classes,
-                                 const uint64_t* masks, const float* y, const float* f_empty_full, float* phi,
-                                 int32_t* info, void* ws, size_t ws_bytes, void* stream) {
+// gnnshap_solve_wls up to the iteration of an iterative solve, which is left
+// to *run (begun on `stream`); other systems are queued in full and run is
+// left idle.
+int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_class* classes, const uint64_t* masks,
+                             const float* y, const float* f_empty_full, float* phi, int32_t* info, void* ws,
+                             size_t ws_bytes, void* stream, CgRun* run) {
   GS_TRY_BEGIN
   gnnshap::clear_error();
   if (!classes || !masks || !y || !f_empty_full || !phi || !info || !ws)
@@ -1990,7 +1993,7 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
     pr.fef = f_empty_full;
     pr.phi = phi;
     pr.info = info;
-    return gnnshap::cg_solve(pr, cg_shape_of(plan, classes), w.cg, s, nullptr);
+    return run->begin(pr, cg_shape_of(plan, classes), w.cg, s);
   }
   int32_t* counts = reinterpret_cast<int32_t*>(w.G);
   if (has_random) {
@@ -2152,6 +2155,19 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
   k_finish<<<gnnshap::grid_for(M, 256, 1024), 256, 0, s>>>(w.rhs, M, w.scal, phi);
   GS_LAUNCHED();
   return GNNSHAP_OK;
+  GS_TRY_END
+}
+
+extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_class* classes,
+                                 const uint64_t* masks, const float* y, const float* f_empty_full, float* phi,
+                                 int32_t* info, void* ws, size_t ws_bytes, void* stream) {
+  GS_TRY_BEGIN
+  gnnshap::CgRun run;
+  if (int st = gnnshap::solve_wls_start(plan, classes, masks, y, f_empty_full, phi, info, ws, ws_bytes, stream, &run))
+    return st;
+  while (!run.done())
+    if (int st = run.step()) return st;
+  return run.begun() ? run.finish(nullptr) : GNNSHAP_OK;
   GS_TRY_END
 }
 
