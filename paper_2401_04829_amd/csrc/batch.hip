@@ -137,6 +137,21 @@ Issuer& issuer() {
   return w;
 }
 
+// At least n events of the calling thread (created on demand, default flags
+// without timing, kept until the process ends), or nullptr.
+hipEvent_t* event_pool(size_t n) {
+  static thread_local std::vector<hipEvent_t> pool;
+  while (pool.size() < n) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    pool.push_back(e);
+  }
+  return pool.data();
+}
+
 struct DeviceStages {
   int device = -1;
   HostStage ring[2][2];
@@ -481,7 +496,12 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
         if (side0) GS_HIP(hipStreamWaitEvent(side0->stream, f->fork, 0));
         if (mat) GS_HIP(hipStreamWaitEvent(mat->stream, f->fork, 0));
       }
-      // coalition values of group gi
+      // coalition values of group gi; evaluated[t] is an event recorded on the
+      // group's stream once target t's values are there (so that its solve
+      // can start on another stream while later targets are evaluated)
+      hipEvent_t* ev_pool = gnnshap::event_pool(static_cast<size_t>(n));
+      if (!ev_pool) return gnnshap::fail(GNNSHAP_EHIP, "could not create events");
+      std::vector<hipEvent_t> evaluated(static_cast<size_t>(n), nullptr);
       auto eval_group = [&](int gi) -> int {
         const Group& G = grp[gi];
         if (G.end == G.begin) return GNNSHAP_OK;
@@ -493,6 +513,10 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
                                                G.max_wpr, G.max_k, G.rows_jobs, G.rows_lds, gs[gi]);
           if (st_eval != GNNSHAP_OK && st_eval != GNNSHAP_EUNSUPPORTED) return st_eval;
           gnnshap::clear_error();
+          if (st_eval == GNNSHAP_OK) {
+            GS_HIP(hipEventRecord(ev_pool[G.begin], gs[gi]));
+            for (int64_t j = G.begin; j < G.end; ++j) evaluated[order[j]] = ev_pool[G.begin];
+          }
         }
         if (st_eval != GNNSHAP_OK) {
           for (int64_t j = G.begin; j < G.end; ++j) {
@@ -503,15 +527,19 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
                                                        f_empty_full + 2 * t, class_out ? class_out + t : nullptr,
                                                        b.eval_slice[t], L.eval_bytes[t], gs[gi], true))
               return st;
+            GS_HIP(hipEventRecord(ev_pool[j], gs[gi]));
+            evaluated[t] = ev_pool[j];
           }
         }
         return GNNSHAP_OK;
       };
       // The systems solved one by one (too large for the batched kernels):
-      // up to three in flight, on `home` and the two side streams (forked
-      // from `home` after everything queued there so far, joined back at the
-      // end), so that one system's iteration overlaps another's; each
-      // iterative solve is stepped chunk by chunk in turn.
+      // up to three in flight, on `home` and the two side streams (a side
+      // stream waits for its target's values, then everything queued on the
+      // side streams is joined back into `home` at the end), so that one
+      // system's iteration overlaps another's and the evaluation of the
+      // targets after it; each iterative solve is stepped chunk by chunk in
+      // turn.
       auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home) -> int {
         if (rest.empty()) return GNNSHAP_OK;
         hipStream_t lanes[3] = {home, nullptr, nullptr};
@@ -524,10 +552,6 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
             side[nl] = ss;
             lanes[nl++] = ss->stream;
           }
-          static thread_local hipEvent_t rest_in = nullptr;
-          if (!rest_in) GS_HIP(hipEventCreateWithFlags(&rest_in, hipEventDisableTiming));
-          GS_HIP(hipEventRecord(rest_in, home));
-          for (int l = 1; l < nl; ++l) GS_HIP(hipStreamWaitEvent(lanes[l], rest_in, 0));
         }
         gnnshap::CgRun runs[3];
         size_t next = 0;
@@ -535,6 +559,12 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
           for (int l = 0; l < nl; ++l) {
             while (!runs[l].begun() && next < rest.size()) {
               const int64_t t = rest[next++];
+              if (l > 0) {
+                // the target's values (and through them its masks) are ready
+                if (!evaluated[t]) return gnnshap::fail(GNNSHAP_EHIP, "target %lld has no evaluation event",
+                                                        static_cast<long long>(t));
+                GS_HIP(hipStreamWaitEvent(lanes[l], evaluated[t], 0));
+              }
               if (int st = gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t],
                                                     y + L.row_off[t], f_empty_full + 2 * t, phi + L.player_off[t],
                                                     info + t, b.solve_slice[t], L.solve_bytes[t], lanes[l], &runs[l]))
