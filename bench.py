@@ -74,7 +74,7 @@ def solver_sweep():
         fef = torch.tensor([0.1, 0.7], dtype=torch.float32, device=dev)
         res = {}
         for path, thr in (("factorised", M + 1), ("iterative", M - 1)):
-            L.gnnshap_set_iterative_threshold(thr)
+            plan.iterative_threshold = thr
             phi = torch.empty(M, dtype=torch.float32, device=dev)
             info = torch.empty(1, dtype=torch.int32, device=dev)
             wsol = torch.empty(L.gnnshap_solve_workspace(plan), dtype=torch.uint8, device=dev)
@@ -88,7 +88,6 @@ def solver_sweep():
                 times.append(1e3 * (time.perf_counter() - t0))
             res[path] = (min(times), int(info.item()), phi.double())
             del wsol
-        L.gnnshap_set_iterative_threshold(5000)
         a, b = res["factorised"][2], res["iterative"][2]
         print(json.dumps({"solver_sweep": {"players": M, "coalitions": p, "random_rows": k // 2 - plan.random_begin,
                                            "factorised_ms": res["factorised"][0], "iterative_ms": res["iterative"][0],

@@ -15,12 +15,28 @@
  *
  * Conventions shared by every call:
  *   - "[dev]" pointers are device memory of the current HIP device, "[host]"
- *     pointers host memory.  Every buffer is owned by the caller; the library
- *     allocates nothing (scratch space comes from the *_workspace queries,
- *     which report the byte size of a caller-owned device buffer).
+ *     pointers host memory.  Every buffer a call reads or writes is owned by
+ *     the caller, and device scratch space comes from the *_workspace queries
+ *     (the byte size of a caller-owned device buffer).  The library allocates
+ *     no device memory of its own, but it keeps these resources from their
+ *     first use until the process ends (never freed by a call):
+ *       . page-locked host staging buffers, per calling host thread
+ *         (hipHostMalloc), through which the batched calls' job tables reach
+ *         the device and the batched extraction's sizes come back;
+ *       . two side streams with their events per device and calling host
+ *         thread, events marking each evaluated target, and one worker host
+ *         thread per calling thread (gnnshap_explain_batch);
+ *       . mapped page-locked stop flags with two events each, one per
+ *         iterative solve in flight (at most 8 per calling thread);
+ *       . a fixed 512 KiB device array per GPU, in the library's code
+ *         object (gnnshap_sample_coalitions_noalloc);
+ *       . a host cache of recent (M, p) sample plans.
  *   - `stream` is a hipStream_t (NULL = the default stream).  All device work
  *     is enqueued on it and is asynchronous, except where a call says it
- *     blocks.
+ *     blocks: the extraction calls (they return sizes), and
+ *     gnnshap_solve_wls and gnnshap_explain_batch when a system is solved
+ *     iteratively (the host waits on the stream for each chunk's stopping
+ *     test, so the call returns once the iteration has stopped).
  *   - Return value: a gnnshap_status.  No C++ exception crosses the ABI.  On
  *     GNNSHAP_EINVAL or GNNSHAP_ECAPACITY nothing is written except the sizes
  *     a call reports.  gnnshap_last_error() gives a thread-local message about
@@ -149,10 +165,15 @@ typedef struct {
   int64_t random_begin;    /* out: first random representative row */
   double full_fraction;    /* out: total weight of the enumerated rows */
   double random_weight;    /* out: weight of every random row (0 if none) */
+  int64_t iterative_threshold; /* in: systems of more players than this are solved
+                                  iteratively by gnnshap_solve_wls (Sec. 3.5); 0 or
+                                  negative = 5000, the paper's switch.  Kept by
+                                  gnnshap_plan_samples; gnnshap_plan_batch sets 0. */
 } gnnshap_sample_plan;
 
 /* Host-only, pure, thread-safe (plans of recent (M, p) pairs are kept and
- * reused).  Fills *plan's outputs and classes[0 .. num_classes).
+ * reused).  Fills *plan's outputs and classes[0 .. num_classes); the inputs
+ * (num_players, num_samples, seed, stream_id, iterative_threshold) are kept.
  * If `classes` is NULL or cap_classes < num_classes, returns
  * GNNSHAP_ECAPACITY with the outputs of *plan filled.  EINVAL: M < 2, odd
  * or non-positive p, or more than 2^31 rows. */
@@ -267,8 +288,8 @@ int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes);
  * int32) receives 0, or j > 0 if the j-th pivot (1-based) of the Cholesky
  * factorisation was not positive (phi is then not meaningful; this happens
  * when the sampled rows do not determine phi).
- * Systems of more than gnnshap_set_iterative_threshold() players (default
- * 5000) are not factored: conjugate gradients run on the projected normal
+ * Systems of more than plan->iterative_threshold players (default 5000) are
+ * not factored: conjugate gradients run on the projected normal
  * equations, applying the masks and their transpose straight from the bits
  * (Sec. 3.5 fits large systems iteratively), until the residual falls to
  * 1e-8 of its initial norm; *info is then 0, or M + 1 if that did not happen
@@ -312,8 +333,8 @@ int gnnshap_extract_batch(const gnnshap_graph* g, const int64_t* targets, int64_
 /* gnnshap_extract_batch in two halves, so that a caller can queue the next
  * batch's extraction before the current batch's explanation and wait for
  * the sizes later.  _launch validates the arguments and queues the
- * extraction and the copy of its sizes to page-locked host memory on
- * `stream` (same arguments and errors as gnnshap_extract_batch, except
+ * extraction on `stream`, whose kernel writes the sizes straight into
+ * page-locked host memory (same arguments and errors as gnnshap_extract_batch, except
  * that it never reports ECAPACITY for the subgraphs); _finish waits for
  * those sizes and fills them into sgs[0 .. n) (the same n and sgs array),
  * returning OK or ECAPACITY as gnnshap_extract_batch does.  The [dev]
@@ -456,15 +477,10 @@ int gnnshap_gat_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gat* m
 /* Which solver the plan's system takes: *path = 1 if one workgroup factors
  * and solves it (M <= 192), 2 if it is factored panel by panel by small
  * workgroups (192 < M <= 448), 0 if it takes the multi-block Cholesky, 3 if
- * it is solved iteratively (M above the iterative threshold). */
+ * it is solved iteratively (M above plan->iterative_threshold; the
+ * iterative path needs a different workspace, so the workspace query must
+ * see the same threshold as the solve). */
 int gnnshap_solve_info(const gnnshap_sample_plan* plan, int32_t* path);
-
-/* Sets the process-wide number of players above which systems are solved
- * iteratively (Sec. 3.5 switches at 5000, the default) instead of being
- * factored; also for gnnshap_explain_batch, where such targets take the
- * single-target solver.  Set it before querying workspace sizes: the
- * iterative path needs a different workspace.  EINVAL if below 1. */
-int gnnshap_set_iterative_threshold(int64_t num_players);
 
 /* Arms timing for the kernels whose name starts with `kernel_name` (e.g.
  * "k_solve_mid", "k_eval_l2"): every later launch of such a kernel, from

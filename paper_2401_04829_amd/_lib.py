@@ -36,7 +36,8 @@ class gnnshap_class(ctypes.Structure):
 class gnnshap_sample_plan(ctypes.Structure):
     _fields_ = [("num_players", c_i64), ("num_samples", c_i64), ("seed", c_u64), ("stream_id", c_u64),
                 ("num_rows", c_i64), ("words_per_row", c_i64), ("num_classes", c_i64),
-                ("random_begin", c_i64), ("full_fraction", c_dbl), ("random_weight", c_dbl)]
+                ("random_begin", c_i64), ("full_fraction", c_dbl), ("random_weight", c_dbl),
+                ("iterative_threshold", c_i64)]
 
 
 class gnnshap_gcn(ctypes.Structure):
@@ -92,7 +93,6 @@ _SIGNATURES = {
                                              c_i64, _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                              c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_solve_info": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(c_i32)]),
-    "gnnshap_set_iterative_threshold": (ctypes.c_int, [c_i64]),
     "gnnshap_fidelity_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), _P(ctypes.c_size_t)]),
     "gnnshap_fidelity": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_dbl, c_i64,
                                         c_vp, c_vp, ctypes.c_size_t, c_vp]),
@@ -162,8 +162,9 @@ def gnnshap_extract_subgraph(graph, target, sg, ws_ptr, ws_bytes, stream):
     return st
 
 
-def gnnshap_plan_samples(num_players, num_samples, seed, stream_id):
-    plan = gnnshap_sample_plan(num_players=num_players, num_samples=num_samples, seed=seed, stream_id=stream_id)
+def gnnshap_plan_samples(num_players, num_samples, seed, stream_id, iterative_threshold=0):
+    plan = gnnshap_sample_plan(num_players=num_players, num_samples=num_samples, seed=seed, stream_id=stream_id,
+                               iterative_threshold=iterative_threshold)
     st = load().gnnshap_plan_samples(ctypes.byref(plan), None, 0)
     if st != ECAPACITY:
         check(st, "plan_samples")
@@ -354,8 +355,3 @@ def gnnshap_fidelity_masks(phi_ptr, M, sparsity, top_k, masks_ptr, stream):
 
 def gnnshap_fidelity_average(terms_ptr, n, stride, avg_ptr, stream):
     check(load().gnnshap_fidelity_average(terms_ptr, int(n), int(stride), avg_ptr, stream), "fidelity_average")
-
-
-def gnnshap_set_iterative_threshold(num_players):
-    """Players above which systems are solved iteratively (process-wide; default 5000)."""
-    check(load().gnnshap_set_iterative_threshold(int(num_players)), "set_iterative_threshold")

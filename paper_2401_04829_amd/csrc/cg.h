@@ -112,8 +112,11 @@ class CgRun {
 // queued on `s`.  *iters_out (may be null) receives the iterations run.
 int cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out);
 
-// Largest number of players solved by factorisation; larger systems are
-// solved iteratively.  Process-wide, default 5000 (Sec. 3.5).
-int64_t iterative_threshold();
+// Largest number of players a plan's system is solved by factorisation for;
+// larger systems are solved iteratively (Sec. 3.5 switches at 5000, the
+// default when the plan's field is 0 or negative).
+inline int64_t iterative_threshold(const gnnshap_sample_plan* p) {
+  return p->iterative_threshold > 0 ? p->iterative_threshold : 5000;
+}
 
 }  // namespace gnnshap

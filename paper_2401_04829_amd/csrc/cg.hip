@@ -588,18 +588,7 @@ HostFlag* acquire_flag() {
   return nullptr;
 }
 
-std::atomic<int64_t> g_threshold{5000};
-
 }  // namespace
-
-int64_t gnnshap::iterative_threshold() { return g_threshold.load(std::memory_order_relaxed); }
-
-extern "C" int gnnshap_set_iterative_threshold(int64_t num_players) {
-  gnnshap::clear_error();
-  if (num_players < 1) return gnnshap::fail(GNNSHAP_EINVAL, "threshold must be at least 1");
-  g_threshold.store(num_players, std::memory_order_relaxed);
-  return GNNSHAP_OK;
-}
 
 gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t rb0, const gnnshap_class* classes,
                                    int64_t ncls) {

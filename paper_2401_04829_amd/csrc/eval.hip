@@ -1688,6 +1688,15 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
     }
   }
   // f(empty) and f(E_c) for every class, then the explained class.
+  if (sh.wide) {
+    const float* b1 = m->b ? m->b[0] : nullptr;
+    const float* b2 = m->b ? m->b[1] : nullptr;
+    if (int st = gnnshap::launch_wide_ends(sh.ws, w.wide, sg, w.Zc[1], b1, m->W[1], b2, target_class, w.sp_y, w.ctl,
+                                           class_out, f_empty_full, s))
+      return st;
+    return gnnshap::launch_wide(sh.ws, w.wide, sg, masks, sh.wpr, w.Zc[1], b1, m->W[1], b2, w.ctl, f_empty_full,
+                                pairs, y, s);
+  }
   if (ends_ok(sh)) {
     launch_ends(s, sg, sh.n_dst, sh.nd[1], sh.n_nodes, w.Zc[1], nullptr, m->b ? m->b[0] : nullptr, m->W[1],
                 m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out,
@@ -1698,9 +1707,6 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
     k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
     GS_LAUNCHED();
   }
-  if (sh.wide)
-    return gnnshap::launch_wide(sh.ws, w.wide, sg, masks, sh.wpr, w.Zc[1], m->b ? m->b[0] : nullptr, m->W[1],
-                                m->b ? m->b[1] : nullptr, w.ctl, f_empty_full, pairs, y, s);
   // Prediction pruning, then the live coalitions in passes of sh.tile rows.
   k_live<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(masks, sh.wpr, k, sg->dst_ptr, w.ctl, w.live_rows,
                                                          w.live_flag);

@@ -19,6 +19,11 @@
 // only the first half of the rows is contracted.
 //
 // Kernels, per target:
+//   k_wide_ends_l1, k_wide_ends_out
+//                the two end coalitions (no players, every player) for every
+//                class, and the explained class: layer 1 at every node of H_1
+//                by one workgroup per (node, 64 features), layer 2 by one
+//                wavefront per class
 //   k_wide_prep  one workgroup: operand-unit offsets of each node and the
 //                list of players whose source is in H_1
 //   k_wide_zop   the A operands: for 16 players (one unit) and 16 features
@@ -380,6 +385,89 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
   }
 }
 
+// The two end coalitions (no players, every player), layer 1: Hf[x] =
+// H^1 at node x of H_1 under E_c (degrees: the players entering each node),
+// Hf[n1] = H^1 at the target under the empty coalition (its self loop only).
+// Workgroup (x, feature block of 64): wavefront w sums players w, w + 4, ...
+// for its 64 features (lane = feature), the four partial sums are added in
+// a fixed order.
+__global__ void __launch_bounds__(256) k_wide_ends_l1(const int32_t* __restrict__ dst_ptr,
+                                                      const int32_t* __restrict__ edge_src, int64_t n1,
+                                                      const float* __restrict__ Zc, int h,
+                                                      const float* __restrict__ b1, float* __restrict__ Hf) {
+  __shared__ float part[4][64];
+  const int64_t x = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int f = blockIdx.y * 64 + lane;
+  const bool fv = f < h;
+  const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+  float acc = 0.f;
+  for (int e = e0 + wave; e < e1; e += 4) {
+    const int32_t u = edge_src[e];
+    const float du = u < n1 ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[u + 1] - dst_ptr[u])) : 1.0f;
+    if (fv) acc = fmaf(du, Zc[static_cast<int64_t>(u) * h + f], acc);
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0 && fv) {
+    const float a = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+    const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(e1 - e0));
+    const float bb = b1 ? b1[f] : 0.f;
+    const float zx = Zc[x * h + f];
+    Hf[x * h + f] = fmaxf(fmaf(dx, fmaf(dx, zx, a), bb), 0.f);
+    if (x == 0) Hf[n1 * h + f] = fmaxf(zx + bb, 0.f);
+  }
+}
+
+// Layer 2 at the target for every class, then the explained class (the
+// requested one, or argmax f(E_c), ties to the lowest index):
+// sp_y[c] = f_c(empty), sp_y[C + c] = f_c(E_c); ctl[0], class_out and
+// f_empty_full as the other evaluation paths write them.  One workgroup of
+// 1024 threads, one wavefront per class at a time (lane = feature).
+__global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restrict__ dst_ptr, int64_t n1,
+                                                        const float* __restrict__ Hf, int h,
+                                                        const float* __restrict__ W2, const float* __restrict__ b2,
+                                                        int C, int requested, float* __restrict__ sp_y,
+                                                        int32_t* __restrict__ ctl, int32_t* __restrict__ class_out,
+                                                        float* __restrict__ f_empty_full) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[1] - dst_ptr[0]));
+  for (int c = wave; c < C; c += 16) {
+    float full = 0.f, empty = 0.f;
+    for (int64_t x = 0; x < n1; ++x) {
+      float p = 0.f;
+      for (int f = lane; f < h; f += 64) p = fmaf(Hf[x * h + f], W2[static_cast<int64_t>(f) * C + c], p);
+      // node x >= 1 is the source of the target's player x - 1, present in E_c
+      const float wx = x == 0 ? dv : __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
+      full = fmaf(wx, p, full);
+    }
+    for (int f = lane; f < h; f += 64) empty = fmaf(Hf[n1 * h + f], W2[static_cast<int64_t>(f) * C + c], empty);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      full += __shfl_xor(full, off);
+      empty += __shfl_xor(empty, off);
+    }
+    const float bb = b2 ? b2[c] : 0.f;
+    if (lane == 0) {
+      sp_y[c] = empty + bb;
+      sp_y[C + c] = fmaf(dv, full, bb);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int c = requested;
+    if (c < 0) {
+      c = 0;
+      for (int i = 1; i < C; ++i)
+        if (sp_y[C + i] > sp_y[C + c]) c = i;
+    }
+    ctl[0] = c;
+    if (class_out) *class_out = c;
+    f_empty_full[0] = sp_y[c];
+    f_empty_full[1] = sp_y[C + c];
+  }
+}
+
 }  // namespace
 
 namespace gnnshap {
@@ -411,7 +499,24 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
   w.S = c.take<float>(s.n1 * s.h);
   w.deg = c.take<int32_t>(s.k * s.n1);
   w.t = c.take<float>(static_cast<int64_t>(s.nfb) * s.k * s.n1);
+  w.hf = c.take<float>((s.n1 + 1) * s.h);
   return w;
+}
+
+int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const float* Zc, const float* b1,
+                     const float* W2, const float* b2, int32_t target_class, float* sp_y, int32_t* ctl,
+                     int32_t* class_out, float* f_empty_full, hipStream_t st) {
+  if (s.n1 > 65535 * 64) return fail(GNNSHAP_EUNSUPPORTED, "too many nodes in H_1");
+  {
+    GS_TIMED("k_wide_ends", st);
+    k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64))), 256, 0, st>>>(
+        sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h, b1, w.hf);
+    GS_LAUNCHED();
+    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hf, s.h, W2, b2, s.C, target_class, sp_y, ctl, class_out,
+                                         f_empty_full);
+  }
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }
 
 int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr,

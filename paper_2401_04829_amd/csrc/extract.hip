@@ -412,12 +412,10 @@ __global__ void __launch_bounds__(1024) k_extract_batch(const int64_t* __restric
 }
 
 // Batch workspace: one slice per target from the front (slice t at a fixed
-// offset, zero between calls), the job table and the result rows (rewritten
-// by every call) at the back.  A workspace sized for n targets serves every
-// smaller batch too, and the two regions of different calls never overlap.
+// offset, zero between calls), so a workspace sized for n targets serves
+// every smaller batch too.  The job table and the result rows live in
+// page-locked host memory, not here.
 struct BatchWs {
-  ExtractJob* jobs;
-  int64_t* results;
   char* slices;
   size_t slice_bytes;
 };
@@ -428,24 +426,12 @@ size_t slice_bytes_of(int64_t num_nodes) {
   return one.bytes();
 }
 
-size_t tail_bytes(int64_t n) {
-  gnnshap::Carver t(nullptr);
-  t.take<ExtractJob>(n);
-  t.take<int64_t>(n * kCounters);
-  return t.bytes();
-}
+size_t batch_bytes(int64_t num_nodes, int64_t n) { return static_cast<size_t>(n) * slice_bytes_of(num_nodes); }
 
-size_t batch_bytes(int64_t num_nodes, int64_t n) {
-  return static_cast<size_t>(n) * slice_bytes_of(num_nodes) + tail_bytes(n);
-}
-
-BatchWs carve_batch(void* ws, size_t ws_bytes, int64_t num_nodes, int64_t n) {
+BatchWs carve_batch(void* ws, int64_t num_nodes) {
   BatchWs b;
   b.slice_bytes = slice_bytes_of(num_nodes);
   b.slices = static_cast<char*>(ws);
-  gnnshap::Carver t(b.slices + ((ws_bytes - tail_bytes(n)) & ~size_t(255)));
-  b.jobs = t.take<ExtractJob>(n);
-  b.results = t.take<int64_t>(n * kCounters);
   return b;
 }
 
@@ -586,9 +572,9 @@ extern "C" int gnnshap_extract_batch_workspace(int64_t num_nodes, int64_t n, siz
 
 namespace {
 
-// The calling thread's launched batched extraction: its result rows are
-// copied into page-locked memory behind the kernel, and `ready` is recorded
-// after the copy; gnnshap_extract_batch_finish waits for it.
+// The calling thread's launched batched extraction: the kernel writes its
+// result rows straight into page-locked memory (`host`), and `ready` is
+// recorded behind the kernel; gnnshap_extract_batch_finish waits for it.
 struct PendingExtract {
   int device = -1;
   int64_t* host = nullptr;
@@ -621,7 +607,7 @@ extern "C" int gnnshap_extract_batch_launch(const gnnshap_graph* g, const int64_
   if (pe.pending) return gnnshap::fail(GNNSHAP_EINVAL, "a batched extraction of this thread is not finished");
   const size_t need = batch_bytes(nn, n);
   if (ws_bytes < need) return gnnshap::fail(GNNSHAP_ECAPACITY, "batch extract workspace needs %zu bytes", need);
-  const BatchWs b = carve_batch(ws, ws_bytes, nn, n);
+  const BatchWs b = carve_batch(ws, nn);
   int dev = 0;
   GS_HIP(hipGetDevice(&dev));
   if (pe.device != dev) {
@@ -683,8 +669,10 @@ extern "C" int gnnshap_extract_batch_finish(gnnshap_subgraph* sgs, int64_t n) {
   if (!pe.pending || pe.n != n)
     return gnnshap::fail(GNNSHAP_EINVAL, "no batched extraction of %lld targets was launched by this thread",
                          (long long)n);
-  pe.pending = false;
+  // pending is cleared only once the kernel is known to be done, so that no
+  // later launch frees or reuses `host` while the device may still write it
   GS_HIP(hipEventSynchronize(pe.ready));
+  pe.pending = false;
   const int64_t* h = pe.host;
   bool all_ok = true;
   for (int64_t t = 0; t < n; ++t) {

@@ -205,9 +205,11 @@ extern "C" int gnnshap_plan_samples(gnnshap_sample_plan* plan, gnnshap_class* cl
     std::shared_ptr<const Planned> e;
     if (int st = planned(plan->num_players, plan->num_samples, &e)) return st;
     const uint64_t seed = plan->seed, stream_id = plan->stream_id;
+    const int64_t threshold = plan->iterative_threshold;
     *plan = e->plan;
     plan->seed = seed;
     plan->stream_id = stream_id;
+    plan->iterative_threshold = threshold;
     if (!classes || cap_classes < plan->num_classes)
       return gnnshap::fail(GNNSHAP_ECAPACITY, "class table needs %lld records", (long long)plan->num_classes);
     std::copy(e->classes.begin(), e->classes.end(), classes);
@@ -237,6 +239,7 @@ extern "C" int gnnshap_plan_batch(const gnnshap_subgraph* sgs, const int64_t* st
       pt = e->plan;
       pt.seed = seed;
       pt.stream_id = static_cast<uint64_t>(stream_ids[t]);
+      pt.iterative_threshold = 0;
       if (classes && ncls + pt.num_classes <= cap_classes)
         std::copy(e->classes.begin(), e->classes.end(), classes + ncls);
       ncls += pt.num_classes;

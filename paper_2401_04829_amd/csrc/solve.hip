@@ -59,8 +59,8 @@ struct Ws {
   gnnshap::CgWs cg;  // iterative path only (no G, Winv, Wd)
 };
 
-// Systems above the process-wide threshold are solved iteratively (Sec. 3.5).
-bool iterative(const gnnshap_sample_plan* p) { return p->num_players > gnnshap::iterative_threshold(); }
+// Systems above the plan's threshold are solved iteratively (Sec. 3.5).
+bool iterative(const gnnshap_sample_plan* p) { return p->num_players > gnnshap::iterative_threshold(p); }
 
 // The iterative solver's shape for a plan and its class table; without a
 // table (workspace queries), for the table gnnshap_plan_samples gives the plan.

@@ -28,8 +28,16 @@ struct WideWs {
   float* S;           // n1 x h: sum of the operand rows of each node
   int32_t* deg;       // k x n1: in-degree of each node of H_1 under each evaluated row
   float* t;           // nfb x k x n1: each node's layer-1 output times the explained class's W_2 column
+  float* hf;          // (n1 + 1) x h: layer 1 under the end coalitions (E_c at H_1, then empty at the target)
 };
 WideWs wide_carve(Carver& c, const WideShape& s);
+
+// The end coalitions: sp_y[c] = f_c(empty), sp_y[C + c] = f_c(E_c) for every
+// class, then the explained class (target_class, or argmax f(E_c)) into
+// ctl[0], class_out (may be null) and f_empty_full.
+int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const float* Zc, const float* b1,
+                     const float* W2, const float* b2, int32_t target_class, float* sp_y, int32_t* ctl,
+                     int32_t* class_out, float* f_empty_full, hipStream_t st);
 
 // y[b] for rows b < k of `masks` (f(empty) for rows without an in-edge of
 // the target).  Zc: n_nodes x h rows of X W_1 for the subgraph's nodes;

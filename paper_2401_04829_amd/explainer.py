@@ -98,6 +98,7 @@ class Explainer:
         self._ncls_hint = 1024                   # class-table length explain_batch allocates
         self._xstream = None                     # stream of the batched extraction
         self._tg_cache = None                    # (target tuple, ctypes int64 array) of the last batch
+        self.iterative_threshold = 0             # players above which systems are solved iteratively (0: 5000)
 
     def prepare(self):
         """gnnshap_transform_features: X W_1 for every node, shared by all targets."""
@@ -156,7 +157,8 @@ class Explainer:
         if M < 2:
             raise ValueError(f"target {target} has {M} players; at least 2 are needed")
         plan, classes = L.gnnshap_plan_samples(M, int(num_samples), int(seed),
-                                               int(target if stream_id is None else stream_id))
+                                               int(target if stream_id is None else stream_id),
+                                               self.iterative_threshold)
         return self.run(sub, plan, classes, target_class, target)
 
     def explain_many(self, targets, num_samples, seed, target_class=-1, n_streams=3):
@@ -188,7 +190,7 @@ class Explainer:
             M = sub.sg.num_edges
             if M < 2:
                 raise ValueError(f"target {v} has {M} players; at least 2 are needed")
-            plan, classes = L.gnnshap_plan_samples(M, int(num_samples), int(seed), int(v))
+            plan, classes = L.gnnshap_plan_samples(M, int(num_samples), int(seed), int(v), self.iterative_threshold)
             with torch.cuda.stream(lane):
                 out.append(self.run(sub, plan, classes, target_class, v, workspaces=ws))
         for st in lanes:
@@ -363,6 +365,8 @@ class Explainer:
             self._ncls_hint = ncls + ncls // 4
             cl = (L.gnnshap_class * self._ncls_hint)()
             st, ncls, totals = L.gnnshap_plan_batch(sgs, subs.targets, int(num_samples), int(seed), plans, cl)
+        for t in range(n):
+            plans[t].iterative_threshold = self.iterative_threshold
         out = BatchExplanations(targets, subs, plans, cl, ncls, totals, dev)
         # the workspace is sized on demand: the call checks it before queueing anything
         ptrs = out.pointers()

@@ -1,7 +1,7 @@
 """GPU parity of the iterative least-squares solver (Sec. 3.5: large systems
 are fitted iteratively) against the fp64 oracle.
 
-The solver switches on above a process-wide player count (default 5000);
+The solver switches on above the plan's player threshold (default 5000);
 these tests lower it so that systems the oracle solves in seconds take the
 iterative path, with and without enumerated classes, with no random rows at
 all, and through the batched entry point.  Bar: phi within 1e-3 of max|phi|;
@@ -19,19 +19,12 @@ from tests.gpu_util import explainer_for, masks_np, require_gpu, sample_on_gpu
 
 pytestmark = pytest.mark.gpu
 
-DEFAULT_THRESHOLD = 5000
-
 
 @pytest.fixture(scope="module")
 def dev():
     return require_gpu()
 
 
-@pytest.fixture
-def iterative_above():
-    """Sets the iterative threshold for one test and restores the default."""
-    yield L.gnnshap_set_iterative_threshold
-    L.gnnshap_set_iterative_threshold(DEFAULT_THRESHOLD)
 
 
 def _say(*a):
@@ -81,13 +74,13 @@ def _game(M, mb, seed):
 
 
 @pytest.mark.parametrize("M,p", [(10, 1022), (20, 10000), (64, 3000), (300, 4000), (701, 6000), (1500, 8000)])
-def test_iterative_solve_against_oracle(dev, iterative_above, M, p):
+def test_iterative_solve_against_oracle(dev, M, p):
     """Conjugate gradients against the oracle's least squares: every class
     enumerated (no random rows), enumerated and random classes together, and
     random rows only, across one and several mask words and row chunks."""
-    iterative_above(1)
     _say("iterative", M, p)
     plan, classes, masks, weights = sample_on_gpu(M, p, 11, 12)
+    plan.iterative_threshold = 1
     assert L.gnnshap_solve_info(plan) == 3
     mb, w = _oracle_rows(plan, masks, 11, 12)
     v, f0, f1 = _game(M, mb, M)
@@ -124,15 +117,15 @@ def test_factored_solve_with_residual_against_oracle(dev, M, p):
     _phi_close(phi, phi_ref)
 
 
-def test_iterative_exhaustive_equals_exact_shapley(dev, iterative_above):
+def test_iterative_exhaustive_equals_exact_shapley(dev):
     """All coalitions enumerated: the iterative solve gives the exact Shapley
     values of eq. 1 (brute force over 2^M coalitions)."""
-    iterative_above(1)
     M = 9
     rng = np.random.default_rng(3)
     vals = rng.normal(size=1 << M)
     exact = shapley.exact_shapley(vals, M)
     plan, classes, masks, _ = sample_on_gpu(M, 2 ** M - 2, 1, 2)
+    plan.iterative_threshold = 1
     assert L.gnnshap_solve_info(plan) == 3
     mb, _ = _oracle_rows(plan, masks, 1, 2)
     codes = (mb * (1 << np.arange(M))).sum(axis=1)
@@ -144,7 +137,7 @@ def test_iterative_exhaustive_equals_exact_shapley(dev, iterative_above):
 
 
 @pytest.mark.parametrize("M,p", [(600, 4000), (2500, 12000)])
-def test_iterative_matches_factorisation(dev, iterative_above, M, p):
+def test_iterative_matches_factorisation(dev, M, p):
     """The same system through the iterative path and through the Cholesky
     paths agree within the phi bar, and an additive game is recovered."""
     _say("iterative vs direct", M, p)
@@ -153,10 +146,10 @@ def test_iterative_matches_factorisation(dev, iterative_above, M, p):
     a = np.random.default_rng(M).normal(size=M)
     y = (0.25 + mb @ torch.tensor(a, device=dev)).float()
     fef = torch.tensor([0.25, 0.25 + a.sum()], dtype=torch.float32, device=dev)
-    iterative_above(M + 1)
+    plan.iterative_threshold = M + 1
     assert L.gnnshap_solve_info(plan) != 3
     direct, info_d = _solve(dev, plan, classes, masks, y, fef)
-    iterative_above(M - 1)
+    plan.iterative_threshold = M - 1
     assert L.gnnshap_solve_info(plan) == 3
     it, info_i = _solve(dev, plan, classes, masks, y, fef)
     assert info_d == 0 and info_i == 0
@@ -164,7 +157,7 @@ def test_iterative_matches_factorisation(dev, iterative_above, M, p):
     _phi_close(it, direct)
 
 
-def test_iterative_through_explain_batch(dev, iterative_above):
+def test_iterative_through_explain_batch(dev):
     """Cora-shaped targets with the threshold lowered: the batched call sends
     them to the iterative solver and equals the single-target calls bit for
     bit; phi matches the oracle's least squares on the oracle's own masks and
@@ -172,7 +165,7 @@ def test_iterative_through_explain_batch(dev, iterative_above):
     cfg = W.make_config("cora")
     ex = explainer_for(cfg)
     targets = cfg["targets"][:10]
-    iterative_above(40)
+    ex.iterative_threshold = 40
     many = ex.explain_batch(targets, cfg["p"], cfg["seed"])
     torch.cuda.synchronize()
     saw_iterative = False
@@ -197,7 +190,7 @@ def test_iterative_through_explain_batch(dev, iterative_above):
     assert saw_iterative
 
 
-def test_iterative_reports_undetermined_plan(dev, iterative_above):
+def test_iterative_reports_undetermined_plan(dev):
     """Fewer random rows than M - 1 and no enumerated class: the rows cannot
     determine phi; the iterative path reports info = M + 1, as the
     factorisation reports a failed pivot."""
@@ -207,9 +200,9 @@ def test_iterative_reports_undetermined_plan(dev, iterative_above):
     assert plan.random_begin == 0 and kr < M - 1
     y = torch.randn(plan.num_rows, device=dev)
     fef = torch.tensor([0.0, 1.0], dtype=torch.float32, device=dev)
-    iterative_above(M - 1)
+    plan.iterative_threshold = M - 1
     _, info_it = _solve(dev, plan, classes, masks, y, fef)
     assert info_it == M + 1
-    iterative_above(M + 1)
+    plan.iterative_threshold = M + 1
     _, info_direct = _solve(dev, plan, classes, masks, y, fef)
     assert info_direct > 0

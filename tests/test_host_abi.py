@@ -162,25 +162,25 @@ def test_subgraph_batch_init_strides():
 
 
 def test_iterative_threshold_selects_path_and_workspace():
-    """Above the iterative threshold (default 5000 players, Sec. 3.5) the
-    solve reports path 3 and needs no M x M matrix in its workspace."""
-    lib = L.load()
-    assert lib.gnnshap_set_iterative_threshold(0) == L.EINVAL
-    try:
-        plan, _ = L.gnnshap_plan_samples(6000, 50000, 1, 2)
-        assert L.gnnshap_solve_info(plan) == 3
-        small, _ = L.gnnshap_plan_samples(4000, 25000, 1, 2)
-        assert L.gnnshap_solve_info(small) == 0
-        direct = L.gnnshap_solve_workspace(small)
-        L.gnnshap_set_iterative_threshold(3999)
-        assert L.gnnshap_solve_info(small) == 3
-        assert L.gnnshap_solve_workspace(small) < min(direct, 4000 * 4000 * 4) // 2
-        mid, _ = L.gnnshap_plan_samples(300, 4000, 1, 2)
-        assert L.gnnshap_solve_info(mid) == 2
-        L.gnnshap_set_iterative_threshold(299)
-        assert L.gnnshap_solve_info(mid) == 3
-    finally:
-        L.gnnshap_set_iterative_threshold(5000)
+    """Above the plan's iterative threshold (0 = the default 5000 players,
+    Sec. 3.5) the solve reports path 3 and needs no M x M matrix in its
+    workspace; gnnshap_plan_samples keeps the threshold the caller set."""
+    plan, _ = L.gnnshap_plan_samples(6000, 50000, 1, 2)
+    assert plan.iterative_threshold == 0
+    assert L.gnnshap_solve_info(plan) == 3
+    small, _ = L.gnnshap_plan_samples(4000, 25000, 1, 2)
+    assert L.gnnshap_solve_info(small) == 0
+    direct = L.gnnshap_solve_workspace(small)
+    small.iterative_threshold = 3999
+    assert L.gnnshap_solve_info(small) == 3
+    assert L.gnnshap_solve_workspace(small) < min(direct, 4000 * 4000 * 4) // 2
+    again, _ = L.gnnshap_plan_samples(4000, 25000, 1, 2, iterative_threshold=3999)
+    assert again.iterative_threshold == 3999 and L.gnnshap_solve_info(again) == 3
+    mid, _ = L.gnnshap_plan_samples(300, 4000, 1, 2)
+    assert L.gnnshap_solve_info(mid) == 2
+    mid.iterative_threshold = 299
+    assert L.gnnshap_solve_info(mid) == 3
+    mid.iterative_threshold = -5
     assert L.gnnshap_solve_info(mid) == 2
 
 
