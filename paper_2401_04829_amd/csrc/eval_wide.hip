@@ -388,21 +388,21 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
 // The two end coalitions (no players, every player), layer 1: Hf[x] =
 // H^1 at node x of H_1 under E_c (degrees: the players entering each node),
 // Hf[n1] = H^1 at the target under the empty coalition (its self loop only).
-// Workgroup (x, feature block of 64): wavefront w sums players w, w + 4, ...
-// for its 64 features (lane = feature), the four partial sums are added in
-// a fixed order.
-__global__ void __launch_bounds__(256) k_wide_ends_l1(const int32_t* __restrict__ dst_ptr,
-                                                      const int32_t* __restrict__ edge_src, int64_t n1,
-                                                      const float* __restrict__ Zc, int h,
-                                                      const float* __restrict__ b1, float* __restrict__ Hf) {
-  __shared__ float part[4][64];
+// Workgroup (x, feature block of 64): wavefront w sums players w, w + 16,
+// ... for its 64 features (lane = feature), the sixteen partial sums are
+// added in a fixed order.
+__global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict__ dst_ptr,
+                                                       const int32_t* __restrict__ edge_src, int64_t n1,
+                                                       const float* __restrict__ Zc, int h,
+                                                       const float* __restrict__ b1, float* __restrict__ Hf) {
+  __shared__ float part[16][64];
   const int64_t x = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int f = blockIdx.y * 64 + lane;
   const bool fv = f < h;
   const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
   float acc = 0.f;
-  for (int e = e0 + wave; e < e1; e += 4) {
+  for (int e = e0 + wave; e < e1; e += 16) {
     const int32_t u = edge_src[e];
     const float du = u < n1 ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[u + 1] - dst_ptr[u])) : 1.0f;
     if (fv) acc = fmaf(du, Zc[static_cast<int64_t>(u) * h + f], acc);
@@ -410,7 +410,8 @@ __global__ void __launch_bounds__(256) k_wide_ends_l1(const int32_t* __restrict_
   part[wave][lane] = acc;
   __syncthreads();
   if (wave == 0 && fv) {
-    const float a = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+    float a = 0.f;
+    for (int i = 0; i < 16; ++i) a += part[i][lane];
     const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(e1 - e0));
     const float bb = b1 ? b1[f] : 0.f;
     const float zx = Zc[x * h + f];
@@ -509,7 +510,7 @@ int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph
   if (s.n1 > 65535 * 64) return fail(GNNSHAP_EUNSUPPORTED, "too many nodes in H_1");
   {
     GS_TIMED("k_wide_ends", st);
-    k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64))), 256, 0, st>>>(
+    k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64))), 1024, 0, st>>>(
         sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h, b1, w.hf);
     GS_LAUNCHED();
     k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hf, s.h, W2, b2, s.C, target_class, sp_y, ctl, class_out,

@@ -81,10 +81,11 @@ gnnshap::CgShape cg_shape_of(const gnnshap_sample_plan* p, const gnnshap_class* 
 // Row stride of G: a multiple of 64 floats keeps every row 256-byte aligned.
 int64_t ld_of(int64_t M) { return gnnshap::ceil_div(M, 64) * 64; }
 
-// Row chunks of the right-hand side: enough wavefronts (word columns x chunks)
-// to fill the GPU, at least 64 rows per chunk.
+// Row chunks of the right-hand side: enough wavefronts (word columns x chunks,
+// about 32768) that each one's chain of row loads is short, at least 64 rows
+// per chunk.
 int64_t n_chunks(int64_t half, int64_t wpr) {
-  int64_t c = gnnshap::ceil_div(2048, wpr);
+  int64_t c = gnnshap::ceil_div(32768, wpr);
   const int64_t by_rows = gnnshap::ceil_div(half, 64);
   if (c > by_rows) c = by_rows;
   if (c > kMaxChunks) c = kMaxChunks;
