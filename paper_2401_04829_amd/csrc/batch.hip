@@ -538,9 +538,12 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       // stream waits for its target's values, then everything queued on the
       // side streams is joined back into `home` at the end), so that one
       // system's iteration overlaps another's and the evaluation of the
-      // targets after it; each iterative solve is stepped chunk by chunk in
-      // turn.
-      auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home) -> int {
+      // targets after it.  The host polls the solves and steps whichever can
+      // move without waiting, so no solve waits for another's chunk; `home`
+      // holds every evaluation of the group, so it takes a system only once
+      // the last of them (`evals_end`) has completed, while the side streams
+      // start on the first targets as soon as their values are there.
+      auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home, hipEvent_t evals_end) -> int {
         if (rest.empty()) return GNNSHAP_OK;
         hipStream_t lanes[3] = {home, nullptr, nullptr};
         gnnshap::SideStream* side[3] = {nullptr, nullptr, nullptr};
@@ -553,10 +556,17 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
             lanes[nl++] = ss->stream;
           }
         }
+        bool home_free = nl == 1 || !evals_end;
         gnnshap::CgRun runs[3];
         size_t next = 0;
         for (;;) {
+          if (!home_free) {
+            const hipError_t q = hipEventQuery(evals_end);
+            if (q == hipErrorNotReady) (void)hipGetLastError();
+            else home_free = true;
+          }
           for (int l = 0; l < nl; ++l) {
+            if (l == 0 && !home_free) continue;
             while (!runs[l].begun() && next < rest.size()) {
               const int64_t t = rest[next++];
               if (l > 0) {
@@ -571,15 +581,20 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
                 return st;
             }
           }
-          bool any = false;
+          bool any = false, moved = false;
           for (int l = 0; l < nl; ++l) {
             if (!runs[l].begun()) continue;
             any = true;
-            if (int st = runs[l].step()) return st;
-            if (runs[l].done())
+            if (!runs[l].ready()) continue;
+            moved = true;
+            if (runs[l].done()) {
               if (int st = runs[l].finish(nullptr)) return st;
+            } else if (int st = runs[l].step()) {
+              return st;
+            }
           }
           if (!any && next >= rest.size()) break;
+          if (!moved) std::this_thread::sleep_for(std::chrono::microseconds(20));
         }
         for (int l = 1; l < nl; ++l) {
           GS_HIP(hipEventRecord(side[l]->rest_out, lanes[l]));
@@ -610,7 +625,11 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
             if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
           }
         }
-        return solve_rest(G.rest, gs[gi]);
+        // the last evaluation event of the group (recorded on gs[gi])
+        hipEvent_t evals_end = nullptr;
+        for (int64_t j = G.begin; j < G.end; ++j)
+          if (evaluated[order[j]]) evals_end = evaluated[order[j]];
+        return solve_rest(G.rest, gs[gi], evals_end);
       };
       // G~ first: it depends on the masks only, and queued ahead of the
       // evaluations it gets the GPU before their many workgroups fill it

@@ -85,11 +85,14 @@ struct CgArgs;
 
 // One iterative solve driven chunk by chunk, so that a caller can keep
 // several solves in flight, each on its own stream: begin() queues the
-// set-up, every step() queues the next chunk of iterations and waits for the
-// chunk before it (until the iteration has stopped: done()), finish() waits
-// for the stopping iteration, queues phi and info and leaves the object
-// ready for another solve.  At most 8 solves per host thread are in flight
-// at once (each holds a mapped stop flag).
+// set-up; every step() first waits for the chunk before the last one queued
+// and reads the stop flag it left, then (unless the iteration has stopped:
+// done()) queues the next chunk of iterations, so at most two chunks are in
+// flight; finish() waits for the last chunk, queues phi and info and leaves
+// the object ready for another solve.  ready() says whether the next step()
+// or finish() would return without waiting on the device, so one host
+// thread can drive several solves by polling.  At most 8 solves per host
+// thread are in flight at once (each holds a mapped stop flag).
 class CgRun {
  public:
   CgRun();
@@ -100,6 +103,7 @@ class CgRun {
   int step();
   bool done() const { return stopped_; }
   bool begun() const { return static_cast<bool>(st_); }
+  bool ready() const;
   int finish(int64_t* iters_out);
 
  private:

@@ -119,26 +119,63 @@ __device__ __forceinline__ double wave_fixed_sum(const double* __restrict__ a, i
 // (k = 0..15) holds at index n the sum of v[4k + i] over the set bits i of n,
 // so that the sum of v over the set bits of a 64-bit word is the sum of 16
 // table reads.  One table is 16 fp64 entries, 128 bytes: its entries fall in
-// distinct LDS banks, so 64 lanes reading one table never conflict.
-__device__ __forceinline__ void build_nibble_table(const double* __restrict__ v4, double* tab) {
-  const double v0 = v4[0], v1 = v4[1], v2 = v4[2], v3 = v4[3];
-  const double v01 = v0 + v1;
-  double e[8] = {0.0, v0, v1, v01, v2, v0 + v2, v1 + v2, v01 + v2};
-#pragma unroll
-  for (int n = 0; n < 8; ++n) {
-    tab[n] = e[n];
-    tab[8 + n] = e[n] + v3;
+// distinct LDS banks, so 64 lanes reading one table never conflict.  The
+// tables of a workgroup are one static LDS array, word w's 16 tables at
+// byte 2048 w.
+//
+// ntab tables of v (4 entries each) into tab, consecutive threads on
+// consecutive entries, so the writes of a wavefront cover 512 contiguous
+// bytes (no two lanes in one bank).  Entry n of table q is
+// ((v[4q] [n & 1] + v[4q + 1] [n & 2]) + v[4q + 2] [n & 4]) + v[4q + 3] [n & 8],
+// an absent term adding 0.0 (exact).
+__device__ __forceinline__ void build_tables(const double* __restrict__ v, int64_t ntab, double* tab) {
+  for (int64_t e = threadIdx.x; e < ntab * 16; e += blockDim.x) {
+    const double* v4 = v + (e >> 4) * 4;
+    const int n = static_cast<int>(e & 15);
+    const double a0 = (n & 1) ? v4[0] : 0.0;
+    const double a1 = (n & 2) ? v4[1] : 0.0;
+    const double a2 = (n & 4) ? v4[2] : 0.0;
+    const double a3 = (n & 8) ? v4[3] : 0.0;
+    tab[e] = ((a0 + a1) + a2) + a3;
   }
 }
 
 // acc[0..3] += sum over the set bits b of word of v[b], from the word's 16
-// nibble tables at tab (256 entries).
-__device__ __forceinline__ void nibble_dot(uint64_t word, const double* tab, double (&acc)[4]) {
+// tables at byte 2048 W of `tabs` (W a constant, so that the table offsets
+// are immediates of the LDS reads).  Each 32-bit half is masked into two
+// words whose bytes hold 8 x a nibble (the byte offset of the entry in its
+// table): one extract per nibble gives the LDS address.  Table t adds into
+// acc[t & 3], tables in ascending order.
+template <int W>
+__device__ __forceinline__ void nibble_dot(uint64_t word, const char* tabs, double (&acc)[4]) {
+  constexpr uint32_t kM = 0x78787878u;
   const uint32_t lo = static_cast<uint32_t>(word), hi = static_cast<uint32_t>(word >> 32);
+  const uint32_t q[4] = {(lo << 3) & kM, (lo >> 1) & kM, (hi << 3) & kM, (hi >> 1) & kM};
 #pragma unroll
-  for (int k = 0; k < 8; ++k) acc[k & 3] += tab[k * 16 + ((lo >> (4 * k)) & 15)];
+  for (int half = 0; half < 2; ++half)
 #pragma unroll
-  for (int k = 0; k < 8; ++k) acc[k & 3] += tab[(8 + k) * 16 + ((hi >> (4 * k)) & 15)];
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int odd = 0; odd < 2; ++odd) {
+        const int t = 8 * half + 2 * j + odd;
+        const uint32_t off = __builtin_amdgcn_ubfe(q[2 * half + odd], 8 * j, 8);
+        acc[t & 3] += *reinterpret_cast<const double*>(tabs + (W * 2048 + t * 128) + off);
+      }
+}
+
+// acc[0..3] += the products of n <= kTabWords words (word w at src[w * stride])
+// with the tables of consecutive 64-entry groups; the next word's load is
+// issued before the current word's table reads.
+template <int W>
+__device__ __forceinline__ void nibble_dots(const uint64_t* __restrict__ src, int64_t stride, int n, uint64_t next,
+                                            const char* tabs, double (&acc)[4]) {
+  if constexpr (W < kTabWords) {
+    if (W >= n) return;
+    const uint64_t word = next;
+    if (W + 1 < n) next = src[(W + 1) * stride];
+    nibble_dot<W>(word, tabs, acc);
+    nibble_dots<W + 1>(src, stride, n, next, tabs, acc);
+  }
 }
 
 // r = dv - mean(dv) (zero beyond M), x = p = s = 0, partial gamma_0; u zero
@@ -240,8 +277,7 @@ __device__ __forceinline__ double wave_gather_sum(const int32_t* __restrict__ id
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_t* __restrict__ blocked,
                                                           const double* __restrict__ r,
                                                           double* __restrict__ upart, int64_t t) {
-  extern __shared__ double tab[];   // pwords * 256
-  __shared__ double red[kWaves];
+  __shared__ double tab[kTabWords * 256];   // the sparse rows' workgroups: kWaves block sums
   if (a.st->done) return;
   // one flat grid: nxa x npc bit-row workgroups, then nsa sparse-row ones
   const int64_t bid = blockIdx.x;
@@ -262,8 +298,8 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
         su += static_cast<double>(a.sz[b]) * v;
       }
     }
-    const double s1 = block_sum_d(uu, red);
-    const double s2 = block_sum_d(su, red);
+    const double s1 = block_sum_d(uu, tab);
+    const double s2 = block_sum_d(su, tab);
     if (threadIdx.x == 0) {
       a.usp[2 * x] = s1;
       a.usp[2 * x + 1] = s2;
@@ -276,18 +312,13 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
   const int64_t nw = w1 - w0;
   // the tables do not depend on the stopping test: built first, so that the
   // test's reads overlap them
-  for (int64_t q = threadIdx.x; q < nw * 16; q += kWaves * 64) build_nibble_table(r + w0 * 64 + q * 4, tab + q * 16);
+  build_tables(r + w0 * 64, nw * 16, tab);
   if (cg_stop(a, t, writer)) return;   // the same outcome in every wave
   __syncthreads();
   if (rb >= a.nrb) return;
   const uint64_t* src = blocked + (rb * a.wpr + w0) * 64 + lane;
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  uint64_t next = src[0];
-  for (int64_t w = 0; w < nw; ++w) {
-    const uint64_t word = next;
-    if (w + 1 < nw) next = src[(w + 1) * 64];
-    nibble_dot(word, tab + w * 256, acc);
-  }
+  nibble_dots<0>(src, 64, static_cast<int>(nw), src[0], reinterpret_cast<const char*>(tab), acc);
   const int64_t row = rb * 64 + lane;
   if (row < a.kr) upart[pc * a.kr + row] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
@@ -333,7 +364,7 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_t* __restrict__ T,
                                                           const double* __restrict__ u,
                                                           double* __restrict__ qpart) {
-  extern __shared__ double tab[];   // rbc * 256
+  __shared__ double tab[kTabWords * 256];
   if (a.st->done) return;
   // one flat grid: nxb x nrcd bit-row workgroups, then nsb sparse-row ones
   const int64_t bid = blockIdx.x;
@@ -353,19 +384,15 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_
   const int64_t b0 = a.rbd0 + c * a.rbc;
   const int64_t b1 = b0 + a.rbc < a.nrb ? b0 + a.rbc : a.nrb;
   const int64_t nb = b1 - b0;
-  for (int64_t q = threadIdx.x; q < nb * 16; q += kWaves * 64) build_nibble_table(u + b0 * 64 + q * 4, tab + q * 16);
+  build_tables(u + b0 * 64, nb * 16, tab);
   __syncthreads();
   if (g >= a.wpr) return;
   const int64_t j = g * 64 + lane;
   const bool valid = j < a.M;
-  const uint64_t* col = T + (valid ? j : 0);
+  const uint64_t* col = T + b0 * a.M + (valid ? j : 0);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  uint64_t next = valid ? col[b0 * a.M] : 0;
-  for (int64_t rb = 0; rb < nb; ++rb) {
-    const uint64_t word = next;
-    if (rb + 1 < nb) next = valid ? col[(b0 + rb + 1) * a.M] : 0;
-    nibble_dot(word, tab + rb * 256, acc);
-  }
+  // a lane beyond M reads player 0's words and discards its sums
+  nibble_dots<0>(col, a.M, static_cast<int>(nb), col[0], reinterpret_cast<const char*>(tab), acc);
   if (valid) qpart[c * a.M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
@@ -764,9 +791,34 @@ int gnnshap::CgRun::begin(const CgProblem& pr, const CgShape& sh, const CgWs& w,
   return GNNSHAP_OK;
 }
 
-// Queues iterations t .. t + kChunk - 1 (pass A alone of iteration kMaxIt,
-// which always stops), records the chunk's event, then waits for the chunk
-// queued before it and reads the stop flag.
+namespace {
+
+// Whether the work recorded by ev has completed, without waiting; a query
+// that finds it pending leaves no error behind for the next launch check.
+bool event_done(hipEvent_t ev) {
+  const hipError_t e = hipEventQuery(ev);
+  if (e == hipErrorNotReady) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return true;   // complete, or an error that the wait on it reports
+}
+
+}  // namespace
+
+bool gnnshap::CgRun::ready() const {
+  if (!st_) return true;
+  const CgArgs& c = *st_;
+  if (c.chunk == 0) return true;
+  if (stopped_) return event_done(c.hf->ev[(c.chunk - 1) & 1]);   // finish() waits for the last chunk
+  return c.chunk < 2 || event_done(c.hf->ev[c.chunk & 1]);         // step() waits for the one before it
+}
+
+// Waits for the chunk before the last one queued and reads the stop flag;
+// unless the iteration has stopped, queues iterations t .. t + kChunk - 1
+// (pass A alone of iteration kMaxIt, which always stops) and records the
+// chunk's event.  The chunk event ring has two slots: chunk n reuses the
+// event of chunk n - 2, which has completed by then.
 int gnnshap::CgRun::step() {
   if (!st_ || stopped_) return GNNSHAP_OK;
   CgArgs& c = *st_;
@@ -774,43 +826,46 @@ int gnnshap::CgRun::step() {
   const CgShape& sh = c.sh;
   hipStream_t s = c.s;
   const bool random = sh.kr > 0;
-  if (c.t <= kMaxIt) {
-    const int64_t t_end = std::min(c.t + kChunk, kMaxIt + 1);
-    for (; c.t < t_end; ++c.t) {
-      const int64_t t = c.t;
-      {
-        GS_TIMED("k_cg_pass_a", s);
-        k_cg_pass_a<<<c.ga, kWaves * 64, sh.pwords * 256 * sizeof(double), s>>>(a, c.pr.blocked, c.w.r, c.w.upart, t);
-      }
-      GS_LAUNCHED();
-      if (t == kMaxIt) continue;
-      if (random) {
-        {
-          GS_TIMED("k_cg_rows", s);
-          k_cg_rows<<<c.g_rows, 256, 0, s>>>(a);
-        }
-        GS_LAUNCHED();
-        {
-          GS_TIMED("k_cg_pass_b", s);
-          k_cg_pass_b<<<c.gb, kWaves * 64, sh.rbc * 256 * sizeof(double), s>>>(a, c.pr.T, c.w.u, c.w.qpart);
-        }
-        GS_LAUNCHED();
-      }
-      {
-        GS_TIMED("k_cg_update", s);
-        k_cg_update<<<static_cast<unsigned>(sh.nbc), 256, 0, s>>>(a, t);
-      }
-      GS_LAUNCHED();
+  if (c.chunk >= 2) {
+    GS_HIP(hipEventSynchronize(c.hf->ev[c.chunk & 1]));
+    if (__atomic_load_n(c.hf->host, __ATOMIC_ACQUIRE) != 0) {
+      stopped_ = true;
+      return GNNSHAP_OK;
     }
-    GS_HIP(hipEventRecord(c.hf->ev[c.chunk & 1], s));
-    if (c.chunk > 0) {
-      GS_HIP(hipEventSynchronize(c.hf->ev[(c.chunk - 1) & 1]));
-      stopped_ = __atomic_load_n(c.hf->host, __ATOMIC_ACQUIRE) != 0;
-    }
-    ++c.chunk;
-  } else {
-    stopped_ = true;     // every iteration is queued; finish() waits for the last chunk
   }
+  if (c.t > kMaxIt) {
+    stopped_ = true;     // every iteration is queued; finish() waits for the last chunk
+    return GNNSHAP_OK;
+  }
+  const int64_t t_end = std::min(c.t + kChunk, kMaxIt + 1);
+  for (; c.t < t_end; ++c.t) {
+    const int64_t t = c.t;
+    {
+      GS_TIMED("k_cg_pass_a", s);
+      k_cg_pass_a<<<c.ga, kWaves * 64, 0, s>>>(a, c.pr.blocked, c.w.r, c.w.upart, t);
+    }
+    GS_LAUNCHED();
+    if (t == kMaxIt) continue;
+    if (random) {
+      {
+        GS_TIMED("k_cg_rows", s);
+        k_cg_rows<<<c.g_rows, 256, 0, s>>>(a);
+      }
+      GS_LAUNCHED();
+      {
+        GS_TIMED("k_cg_pass_b", s);
+        k_cg_pass_b<<<c.gb, kWaves * 64, 0, s>>>(a, c.pr.T, c.w.u, c.w.qpart);
+      }
+      GS_LAUNCHED();
+    }
+    {
+      GS_TIMED("k_cg_update", s);
+      k_cg_update<<<static_cast<unsigned>(sh.nbc), 256, 0, s>>>(a, t);
+    }
+    GS_LAUNCHED();
+  }
+  GS_HIP(hipEventRecord(c.hf->ev[c.chunk & 1], s));
+  ++c.chunk;
   return GNNSHAP_OK;
 }
 

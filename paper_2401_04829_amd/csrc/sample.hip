@@ -6,7 +6,9 @@
 // Floyd's algorithm on Philox4x32-10 draws, 64 steps at a time: every lane
 // takes one step, lanes whose draw cannot interact with an earlier step of
 // the same chunk decide at once, the others are replayed in step order, so
-// the result is exactly the sequential algorithm's.
+// the result is exactly the sequential algorithm's.  Each Philox call gives
+// the draws of four consecutive steps, so the words of 256 steps are made by
+// one call per lane and staged in LDS.
 #include <algorithm>
 #include <mutex>
 
@@ -122,6 +124,7 @@ __device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t
   int64_t next_begin = lo + 1 < ncls ? cls[lo + 1].row_begin : half;
   // lane 0's last enumerated subset (positions in LDS), to step to the next rank
   __shared__ int32_t comb[kMaxComb];
+  __shared__ uint32_t draws[256];       // Philox words of 256 consecutive Floyd steps
   int64_t comb_cls = -1, comb_rank = -2;
   for (int64_t i = r_begin; i < r_end; ++i) {
     while (i >= next_begin) {
@@ -169,15 +172,26 @@ __device__ __forceinline__ void sample_rows(const gnnshap::SampleJob& J, int64_t
       }
     } else {
       for (int64_t base = 0; base < c; base += 64) {
+        if ((base & 255) == 0) {
+          // the draws of steps base .. base + 255: lane l evaluates counter
+          // base/4 + l, whose four words are the draws of steps base + 4l + 0..3
+          if (base + 4 * lane < c) {
+            uint32_t c0 = static_cast<uint32_t>((base >> 2) + lane), c1 = static_cast<uint32_t>(i), c2 = st_lo,
+                     c3 = st_hi;
+            philox4x32_10(c0, c1, c2, c3, seed_lo, seed_hi);
+            draws[4 * lane] = c0;
+            draws[4 * lane + 1] = c1;
+            draws[4 * lane + 2] = c2;
+            draws[4 * lane + 3] = c3;
+          }
+          __syncthreads();
+        }
         const int64_t s = base + lane;
         const bool act = s < c;
         const int64_t j = M - c + s;
         uint32_t t = 0;
         if (act) {
-          uint32_t c0 = static_cast<uint32_t>(s >> 2), c1 = static_cast<uint32_t>(i), c2 = st_lo, c3 = st_hi;
-          philox4x32_10(c0, c1, c2, c3, seed_lo, seed_hi);
-          const int sel = static_cast<int>(s & 3);
-          const uint32_t u = sel == 0 ? c0 : sel == 1 ? c1 : sel == 2 ? c2 : c3;
+          const uint32_t u = draws[s & 255];
           t = static_cast<uint32_t>((static_cast<uint64_t>(u) * static_cast<uint64_t>(j + 1)) >> 32);
         }
         const int64_t wd = t >> 5;
