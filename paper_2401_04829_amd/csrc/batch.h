@@ -91,13 +91,13 @@ struct SolveJob {
   int32_t counts_in;         // 1: G~ is built from the counts as the panel path first reads each block
   int64_t tr0;               // first transpose item (64 rows x 64 players) of the job in the batch
 };
-class CgRun;
-// gnnshap_solve_wls up to the iteration of an iterative system, which is left
-// to *run (begun on `stream`: the caller steps and finishes it); other systems
-// are queued in full and run is left unbegun.
+class CgGroup;
+// gnnshap_solve_wls up to the iteration of an iterative system, which joins
+// *grp (a group on `stream`, not full: the caller steps it); other systems
+// are queued in full and grp is left as it was.
 int solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_class* classes, const uint64_t* masks,
                     const float* y, const float* f_empty_full, float* phi, int32_t* info, void* ws, size_t ws_bytes,
-                    void* stream, CgRun* run);
+                    void* stream, CgGroup* grp);
 // Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
 bool solve_batchable(const gnnshap_sample_plan* plan);
 size_t solve_slice_bytes(const gnnshap_sample_plan* plan);

@@ -533,72 +533,87 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
         }
         return GNNSHAP_OK;
       };
-      // The systems solved one by one (too large for the batched kernels):
-      // up to three in flight, on `home` and the two side streams (a side
-      // stream waits for its target's values, then everything queued on the
-      // side streams is joined back into `home` at the end), so that one
-      // system's iteration overlaps another's and the evaluation of the
-      // targets after it.  The host polls the solves and steps whichever can
-      // move without waiting, so no solve waits for another's chunk; `home`
-      // holds every evaluation of the group, so it takes a system only once
-      // the last of them (`evals_end`) has completed, while the side streams
-      // start on the first targets as soon as their values are there.
-      auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home, hipEvent_t evals_end) -> int {
+      // The systems solved one by one (too large for the batched kernels).
+      // The iterative ones go to two solver groups, one on each side stream,
+      // each holding up to kPerGroup systems: a group takes a system once its
+      // values are there (a host query of its evaluation event, so a side
+      // stream never waits for a later target) and advances its systems
+      // together; the host steps whichever group can move without waiting.
+      // Two groups let one group's short passes and launch tails overlap the
+      // other's long passes.  The factored ones are queued on `home` behind
+      // every evaluation.  Both side streams are joined back into `home` at
+      // the end.  A single system runs on `home`.
+      auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home) -> int {
         if (rest.empty()) return GNNSHAP_OK;
-        hipStream_t lanes[3] = {home, nullptr, nullptr};
-        gnnshap::SideStream* side[3] = {nullptr, nullptr, nullptr};
-        int nl = 1;
+        constexpr int kPerGroup = 3;
+        gnnshap::SideStream* side[2] = {nullptr, nullptr};
+        gnnshap::CgGroup grp[2];
+        int ng = 1;
+        grp[0].set_stream(home);
         if (rest.size() >= 2) {
           for (int i = 0; i < 2; ++i) {
-            gnnshap::SideStream* ss = gnnshap::side_stream(i);
-            if (!ss) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
-            side[nl] = ss;
-            lanes[nl++] = ss->stream;
+            side[i] = gnnshap::side_stream(i);
+            if (!side[i]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+            grp[i].set_stream(side[i]->stream);
           }
+          ng = 2;
         }
-        bool home_free = nl == 1 || !evals_end;
-        gnnshap::CgRun runs[3];
+        auto evaluated_done = [&](int64_t t) {
+          const hipError_t q = hipEventQuery(evaluated[t]);
+          if (q == hipErrorNotReady) {
+            (void)hipGetLastError();
+            return false;
+          }
+          return true;   // complete, or an error that the stream wait reports
+        };
+        auto start = [&](int64_t t, gnnshap::CgGroup* g) -> int {
+          const hipStream_t st = g->stream();
+          if (st != home) {
+            // the target's values (and through them its masks) are ready
+            if (!evaluated[t]) return gnnshap::fail(GNNSHAP_EHIP, "target %lld has no evaluation event",
+                                                    static_cast<long long>(t));
+            GS_HIP(hipStreamWaitEvent(st, evaluated[t], 0));
+          }
+          return gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t],
+                                          y + L.row_off[t], f_empty_full + 2 * t, phi + L.player_off[t], info + t,
+                                          b.solve_slice[t], L.solve_bytes[t], st, g);
+        };
+        std::vector<int64_t> its;
+        gnnshap::CgGroup on_home;   // stays empty: factored systems are queued in full
+        on_home.set_stream(home);
+        for (int64_t t : rest) {
+          if (plans[t].num_players > gnnshap::iterative_threshold(&plans[t])) its.push_back(t);
+          else if (int st = start(t, &on_home)) return st;
+        }
+        const int cap = ng == 1 ? gnnshap::kCgGroupMax : kPerGroup;
         size_t next = 0;
         for (;;) {
-          if (!home_free) {
-            const hipError_t q = hipEventQuery(evals_end);
-            if (q == hipErrorNotReady) (void)hipGetLastError();
-            else home_free = true;
-          }
-          for (int l = 0; l < nl; ++l) {
-            if (l == 0 && !home_free) continue;
-            while (!runs[l].begun() && next < rest.size()) {
-              const int64_t t = rest[next++];
-              if (l > 0) {
-                // the target's values (and through them its masks) are ready
-                if (!evaluated[t]) return gnnshap::fail(GNNSHAP_EHIP, "target %lld has no evaluation event",
-                                                        static_cast<long long>(t));
-                GS_HIP(hipStreamWaitEvent(lanes[l], evaluated[t], 0));
-              }
-              if (int st = gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t],
-                                                    y + L.row_off[t], f_empty_full + 2 * t, phi + L.player_off[t],
-                                                    info + t, b.solve_slice[t], L.solve_bytes[t], lanes[l], &runs[l]))
-                return st;
-            }
-          }
-          bool any = false, moved = false;
-          for (int l = 0; l < nl; ++l) {
-            if (!runs[l].begun()) continue;
-            any = true;
-            if (!runs[l].ready()) continue;
+          bool moved = false, busy = false;
+          while (next < its.size()) {
+            int gi = -1;
+            for (int i = 0; i < ng; ++i)
+              if (grp[i].size() < cap && (gi < 0 || grp[i].size() < grp[gi].size())) gi = i;
+            if (gi < 0) break;
+            const int64_t t = its[next];
+            if (grp[gi].stream() != home && evaluated[t] && !evaluated_done(t)) break;
+            if (int st = start(t, &grp[gi])) return st;
+            ++next;
             moved = true;
-            if (runs[l].done()) {
-              if (int st = runs[l].finish(nullptr)) return st;
-            } else if (int st = runs[l].step()) {
-              return st;
-            }
           }
-          if (!any && next >= rest.size()) break;
+          for (int i = 0; i < ng; ++i) {
+            if (grp[i].empty()) continue;
+            busy = true;
+            if (!grp[i].ready()) continue;
+            if (int st = grp[i].step()) return st;
+            moved = true;
+          }
+          if (!busy && next >= its.size()) break;
           if (!moved) std::this_thread::sleep_for(std::chrono::microseconds(20));
         }
-        for (int l = 1; l < nl; ++l) {
-          GS_HIP(hipEventRecord(side[l]->rest_out, lanes[l]));
-          GS_HIP(hipStreamWaitEvent(home, side[l]->rest_out, 0));
+        for (int i = 0; i < 2; ++i) {
+          if (!side[i]) continue;
+          GS_HIP(hipEventRecord(side[i]->rest_out, side[i]->stream));
+          GS_HIP(hipStreamWaitEvent(home, side[i]->rest_out, 0));
         }
         return GNNSHAP_OK;
       };
@@ -625,11 +640,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
             if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
           }
         }
-        // the last evaluation event of the group (recorded on gs[gi])
-        hipEvent_t evals_end = nullptr;
-        for (int64_t j = G.begin; j < G.end; ++j)
-          if (evaluated[order[j]]) evals_end = evaluated[order[j]];
-        return solve_rest(G.rest, gs[gi], evals_end);
+        return solve_rest(G.rest, gs[gi]);
       };
       // G~ first: it depends on the masks only, and queued ahead of the
       // evaluations it gets the GPU before their many workgroups fill it

@@ -81,39 +81,48 @@ struct CgProblem {
   int32_t* info;
 };
 
-struct CgArgs;
+// Several iterative solves advanced together on one stream.  Every chunk of
+// iterations is one launch per pass for all members (one flat grid over the
+// members' workgroups), so the members share the GPU inside each launch and
+// the short passes of all members cost one launch latency instead of one
+// each.  add() queues a new member's set-up on the stream (at most
+// kCgGroupMax members at once); step() first waits for the chunk before the
+// last one queued and reads the members' stop flags, queues phi and info of
+// every member that has stopped and releases it, then queues the next chunk
+// of iterations for the members left (each at its own iteration count), so
+// at most two chunks are in flight; ready() says whether step() would return
+// without waiting on the device.  Once empty() every member's phi and info
+// are queued on the stream.  Each member holds a mapped stop flag; at most
+// 16 are held per host thread at once.
+constexpr int kCgGroupMax = 6;
 
-// One iterative solve driven chunk by chunk, so that a caller can keep
-// several solves in flight, each on its own stream: begin() queues the
-// set-up; every step() first waits for the chunk before the last one queued
-// and reads the stop flag it left, then (unless the iteration has stopped:
-// done()) queues the next chunk of iterations, so at most two chunks are in
-// flight; finish() waits for the last chunk, queues phi and info and leaves
-// the object ready for another solve.  ready() says whether the next step()
-// or finish() would return without waiting on the device, so one host
-// thread can drive several solves by polling.  At most 8 solves per host
-// thread are in flight at once (each holds a mapped stop flag).
-class CgRun {
+class CgGroup {
  public:
-  CgRun();
-  ~CgRun();
-  CgRun(const CgRun&) = delete;
-  CgRun& operator=(const CgRun&) = delete;
-  int begin(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s);
-  int step();
-  bool done() const { return stopped_; }
-  bool begun() const { return static_cast<bool>(st_); }
+  CgGroup();
+  ~CgGroup();
+  CgGroup(const CgGroup&) = delete;
+  CgGroup& operator=(const CgGroup&) = delete;
+  void set_stream(hipStream_t s) { s_ = s; }
+  hipStream_t stream() const { return s_; }
+  int add(const CgProblem& pr, const CgShape& sh, const CgWs& w);
+  int size() const;
+  bool empty() const { return size() == 0; }
+  bool full() const { return size() >= kCgGroupMax; }
   bool ready() const;
-  int finish(int64_t* iters_out);
+  int step();
+  // iterations of the member released last (-1 before any)
+  int64_t last_iters() const { return last_iters_; }
 
  private:
-  std::unique_ptr<CgArgs> st_;
-  bool stopped_ = true;
+  struct State;
+  std::unique_ptr<State> st_;
+  hipStream_t s_ = nullptr;
+  int64_t last_iters_ = -1;
 };
 
-// Conjugate gradients on 1-perp; returns once the iteration has stopped
-// (the host waits on the stream for the stopping test) and phi/info are
-// queued on `s`.  *iters_out (may be null) receives the iterations run.
+// Conjugate gradients on 1-perp for one system; returns once its phi and
+// info are queued on `s` (the host waits on the stream for the stopping
+// test).  *iters_out (may be null) receives the iterations run.
 int cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out);
 
 // Largest number of players a plan's system is solved by factorisation for;

@@ -62,6 +62,8 @@ constexpr int64_t kTabWords = 16;    // nibble tables per workgroup: 16 words (3
 constexpr int64_t kSparseDiv = 64;   // sparse rows: coalition size at most M / kSparseDiv
 
 struct Args {
+  const uint64_t* blocked;   // the bit rows in row blocks (pass A)
+  const uint64_t* T;         // the bit rows transposed (pass B)
   const int32_t* sz;
   int64_t M, wpr, kr, nrb, npc, pwords, nrc, rbc, nbu, nbc;
   int64_t rs, rbd0, nsa, nsb, nrcd, nxa, nxb;
@@ -87,6 +89,24 @@ struct Args {
   gnnshap::CgState* st;
   int32_t* host_flag;  // mapped host memory: [0] done, [1] iterations
 };
+
+// The members of one launch of a pass: member m owns workgroups
+// [blk[m], blk[m + 1]) of the flat grid and runs iteration t[m].
+struct GroupArgs {
+  Args a[gnnshap::kCgGroupMax];
+  int64_t t[gnnshap::kCgGroupMax];
+  uint32_t blk[gnnshap::kCgGroupMax + 1];
+  int32_t n;
+};
+
+// The member of this workgroup and the workgroup's index within it.
+__device__ __forceinline__ int member_of(const GroupArgs& g, int64_t& bid) {
+  const uint32_t b = blockIdx.x;
+  int m = 0;
+  while (m + 1 < g.n && b >= g.blk[m + 1]) ++m;
+  bid = static_cast<int64_t>(b - g.blk[m]);
+  return m;
+}
 
 __device__ __forceinline__ double wave_sum_d(double v) {
 #pragma unroll
@@ -274,13 +294,17 @@ __device__ __forceinline__ double wave_gather_sum(const int32_t* __restrict__ id
 // ...: u_b = sum of r over the row's players, with the workgroup's partial
 // |u|^2 and |m|.u in uu[2 x], uu[2 x + 1].  Both kinds take the stopping
 // test first.
-__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_t* __restrict__ blocked,
-                                                          const double* __restrict__ r,
-                                                          double* __restrict__ upart, int64_t t) {
+__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(GroupArgs g) {
   __shared__ double tab[kTabWords * 256];   // the sparse rows' workgroups: kWaves block sums
+  int64_t bid;
+  const int m = member_of(g, bid);
+  const Args& a = g.a[m];
+  const int64_t t = g.t[m];
   if (a.st->done) return;
-  // one flat grid: nxa x npc bit-row workgroups, then nsa sparse-row ones
-  const int64_t bid = blockIdx.x;
+  const uint64_t* __restrict__ blocked = a.blocked;
+  const double* __restrict__ r = a.r;
+  double* __restrict__ upart = a.upart;
+  // one flat grid per member: nxa x npc bit-row workgroups, then nsa sparse-row ones
   const int64_t pc = bid < a.nxa * a.npc ? bid / a.nxa : a.npc;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -326,10 +350,12 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(Args a, const uint64_
 // u of the bit rows (the sum of their pass-A chunks, one lane per row) with
 // partial |u|^2 and |m|.u in uu[2 (1 + x)], uu[2 (1 + x) + 1]; the last
 // workgroup adds pass A's sparse-row partials into uu[0], uu[1] (fixed order).
-__global__ void __launch_bounds__(256) k_cg_rows(Args a) {
+__global__ void __launch_bounds__(256) k_cg_rows(GroupArgs g) {
   __shared__ double red[4];
+  int64_t bid;
+  const Args& a = g.a[member_of(g, bid)];
   if (a.st->done) return;
-  if (static_cast<int64_t>(blockIdx.x) == a.nbu - 1) {
+  if (bid == a.nbu - 1) {
     const int wv = threadIdx.x >> 6;
     if (wv < 2) {
       const double v = a.nsa > 0 ? wave_fixed_sum(a.usp + wv, a.nsa, 2) : 0.0;
@@ -337,7 +363,7 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
     }
     return;
   }
-  const int64_t b = a.rs + static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t b = a.rs + bid * 256 + threadIdx.x;
   double uu = 0.0, su = 0.0;
   if (b < a.kr) {
     double v = 0.0;
@@ -349,8 +375,8 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
   const double s1 = block_sum_d(uu, red);
   const double s2 = block_sum_d(su, red);
   if (threadIdx.x == 0) {
-    a.uu[2 * (1 + blockIdx.x)] = s1;
-    a.uu[2 * (1 + blockIdx.x) + 1] = s2;
+    a.uu[2 * (1 + bid)] = s1;
+    a.uu[2 * (1 + bid) + 1] = s2;
   }
 }
 
@@ -361,13 +387,15 @@ __global__ void __launch_bounds__(256) k_cg_rows(Args a) {
 // bit-transposed words T[rb, j] and sums table entries.  Workgroup
 // nxb * nrcd + x (x < nsb): the players x * kWaves + wave, + nsb * kWaves,
 // ...: qs[j] = sum of u over the sparse rows holding player j.
-__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_t* __restrict__ T,
-                                                          const double* __restrict__ u,
-                                                          double* __restrict__ qpart) {
+__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(GroupArgs g) {
   __shared__ double tab[kTabWords * 256];
+  int64_t bid;
+  const Args& a = g.a[member_of(g, bid)];
   if (a.st->done) return;
-  // one flat grid: nxb x nrcd bit-row workgroups, then nsb sparse-row ones
-  const int64_t bid = blockIdx.x;
+  const uint64_t* __restrict__ T = a.T;
+  const double* __restrict__ u = a.u;
+  double* __restrict__ qpart = a.qpart;
+  // one flat grid per member: nxb x nrcd bit-row workgroups, then nsb sparse-row ones
   const int64_t c = bid < a.nxb * a.nrcd ? bid / a.nxb : a.nrcd;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -380,14 +408,14 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(Args a, const uint64_
     }
     return;
   }
-  const int64_t g = (bid % a.nxb) * kWaves + wave;
+  const int64_t gw = (bid % a.nxb) * kWaves + wave;   // the wavefront's player word
   const int64_t b0 = a.rbd0 + c * a.rbc;
   const int64_t b1 = b0 + a.rbc < a.nrb ? b0 + a.rbc : a.nrb;
   const int64_t nb = b1 - b0;
   build_tables(u + b0 * 64, nb * 16, tab);
   __syncthreads();
-  if (g >= a.wpr) return;
-  const int64_t j = g * 64 + lane;
+  if (gw >= a.wpr) return;
+  const int64_t j = gw * 64 + lane;
   const bool valid = j < a.M;
   const uint64_t* col = T + b0 * a.M + (valid ? j : 0);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
@@ -488,11 +516,15 @@ __global__ void __launch_bounds__(256) k_cg_csc_fill(const uint64_t* __restrict_
 }
 
 // Update of iteration t (see the recurrences above); partial gamma_{t+1}.
-__global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
+__global__ void __launch_bounds__(256) k_cg_update(GroupArgs g) {
   __shared__ double red[4];
   __shared__ double coef[3];
+  int64_t bid;
+  const int m = member_of(g, bid);
+  const Args& a = g.a[m];
+  const int64_t t = g.t[m];
   if (a.st->done) return;
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t j = bid * 256 + threadIdx.x;
   // this thread's vector entries first: their loads overlap the scalar sums
   double q = 0.0, rj = 0.0, pj = 0.0, sj = 0.0;
   if (j < a.M) {
@@ -529,12 +561,12 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
     coef[0] = ok ? step : -1.0;
     coef[1] = beta;
     coef[2] = su / static_cast<double>(a.M);
-    if (ok && blockIdx.x == 0) a.hist[t & 1] = step;
+    if (ok && bid == 0) a.hist[t & 1] = step;
   }
   __syncthreads();
   const double step = coef[0], beta = coef[1], mq = coef[2];
   if (step < 0.0) {   // identical in every workgroup
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (bid == 0 && threadIdx.x == 0) {
       a.st->done = 1;
       a.st->iters = static_cast<int32_t>(t);
       a.st->status = 2;
@@ -556,7 +588,7 @@ __global__ void __launch_bounds__(256) k_cg_update(Args a, int64_t t) {
     r2 = rn * rn;
   }
   const double sb = block_sum_d(r2, red);
-  if (threadIdx.x == 0) a.rr[((t + 1) % 3) * a.nbc + blockIdx.x] = sb;
+  if (threadIdx.x == 0) a.rr[((t + 1) % 3) * a.nbc + bid] = sb;
 }
 
 // phi = Delta/M + x - mean(x) (the projection made exact), info from the state.
@@ -573,17 +605,16 @@ __global__ void __launch_bounds__(1024) k_cg_finish(const double* __restrict__ x
   if (threadIdx.x == 0) *info = (st->status == 0 && !undetermined) ? 0 : static_cast<int32_t>(M + 1);
 }
 
-// Mapped page-locked stopping flags of the calling thread, their device
-// addresses and the two events of each solve's chunked wait: one slot per
-// solve in flight (created on first use, kept until the process ends).
+// Mapped page-locked stopping flags of the calling thread and their device
+// addresses: one slot per solve in flight (created on first use, kept until
+// the process ends).
 struct HostFlag {
   int32_t* host = nullptr;
   int32_t* dev = nullptr;
-  hipEvent_t ev[2] = {nullptr, nullptr};
   bool busy = false;
 };
 
-constexpr int kFlagSlots = 8;
+constexpr int kFlagSlots = 16;
 
 HostFlag* acquire_flag() {
   static thread_local HostFlag pool[kFlagSlots];
@@ -601,11 +632,6 @@ HostFlag* acquire_flag() {
         (void)hipHostFree(h);
         return nullptr;
       }
-      for (int i = 0; i < 2; ++i)
-        if (hipEventCreateWithFlags(&f.ev[i], hipEventDisableTiming) != hipSuccess) {
-          (void)hipGetLastError();
-          return nullptr;
-        }
       f.host = static_cast<int32_t*>(h);
       f.dev = static_cast<int32_t*>(d);
     }
@@ -613,6 +639,41 @@ HostFlag* acquire_flag() {
     return &f;
   }
   return nullptr;
+}
+
+// The two events of a group's chunk ring, per calling thread (created on
+// first use, kept until the process ends).
+struct EventPair {
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  bool busy = false;
+};
+
+constexpr int kPairSlots = 8;
+
+EventPair* acquire_pair() {
+  static thread_local EventPair pool[kPairSlots];
+  for (EventPair& e : pool) {
+    if (e.busy) continue;
+    for (int i = 0; i < 2; ++i)
+      if (!e.ev[i] && hipEventCreateWithFlags(&e.ev[i], hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+      }
+    e.busy = true;
+    return &e;
+  }
+  return nullptr;
+}
+
+// Whether the work recorded by ev has completed, without waiting; a query
+// that finds it pending leaves no error behind for the next launch check.
+bool event_done(hipEvent_t ev) {
+  const hipError_t e = hipEventQuery(ev);
+  if (e == hipErrorNotReady) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return true;   // complete, or an error that the wait on it reports
 }
 
 }  // namespace
@@ -686,35 +747,54 @@ gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
   return w;
 }
 
-struct gnnshap::CgArgs {
+// One member of a group: its arguments, shape, problem and flag, the
+// iteration its next launch runs and its grids.
+struct Member {
   Args a;
-  CgShape sh;
-  CgProblem pr;
-  CgWs w;
-  hipStream_t s = nullptr;
+  gnnshap::CgShape sh;
+  gnnshap::CgProblem pr;
+  gnnshap::CgWs w;
   HostFlag* hf = nullptr;
-  unsigned ga = 0, gb = 0, g_rows = 0;
-  int64_t t = 0, chunk = 0;
+  int64_t t = 0;
+  uint32_t ga = 0, gb = 0, g_rows = 0, g_upd = 0;
 };
 
-gnnshap::CgRun::CgRun() = default;
-gnnshap::CgRun::~CgRun() {
-  if (st_ && st_->hf) st_->hf->busy = false;
+struct gnnshap::CgGroup::State {
+  std::vector<Member> mem;
+  EventPair* ev = nullptr;
+  int64_t chunk = 0;
+};
+
+gnnshap::CgGroup::CgGroup() : st_(new State()) {}
+
+gnnshap::CgGroup::~CgGroup() {
+  for (Member& m : st_->mem)
+    if (m.hf) m.hf->busy = false;
+  if (st_->ev) st_->ev->busy = false;
 }
 
-int gnnshap::CgRun::begin(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s) {
+int gnnshap::CgGroup::size() const { return static_cast<int>(st_->mem.size()); }
+
+int gnnshap::CgGroup::add(const CgProblem& pr, const CgShape& sh, const CgWs& w) {
+  State& S = *st_;
+  if (full()) return fail(GNNSHAP_EINVAL, "solver group already holds %d systems", kCgGroupMax);
+  if (!S.ev) {
+    S.ev = acquire_pair();
+    if (!S.ev) return fail(GNNSHAP_EHIP, "could not create the solver's events (or more than %d groups)", kPairSlots);
+  }
   HostFlag* hf = acquire_flag();
   if (!hf) return fail(GNNSHAP_EHIP, "could not allocate the solver's host flag (or more than %d solves in flight)",
                        kFlagSlots);
-  st_.reset(new CgArgs());
-  CgArgs& c = *st_;
-  c.hf = hf;
-  c.sh = sh;
-  c.pr = pr;
-  c.w = w;
-  c.s = s;
-  stopped_ = false;
-  Args& a = c.a;
+  hipStream_t s = s_;
+  Member m;
+  m.hf = hf;
+  m.sh = sh;
+  m.pr = pr;
+  m.w = w;
+  Args& a = m.a;
+  a = Args{};
+  a.blocked = pr.blocked;
+  a.T = pr.T;
   a.sz = w.sz;
   a.M = sh.M;
   a.wpr = sh.wpr;
@@ -756,11 +836,13 @@ int gnnshap::CgRun::begin(const CgProblem& pr, const CgShape& sh, const CgWs& w,
   a.csc_row = w.csc_row;
   a.qs = w.qs;
   a.host_flag = hf->dev;
-  c.ga = static_cast<unsigned>(a.nxa * sh.npc + sh.nsa);
-  c.gb = static_cast<unsigned>(a.nxb * sh.nrcd + sh.nsb);
-  c.g_rows = static_cast<unsigned>(sh.nbu);
+  m.ga = static_cast<uint32_t>(a.nxa * sh.npc + sh.nsa);
+  m.gb = static_cast<uint32_t>(a.nxb * sh.nrcd + sh.nsb);
+  m.g_rows = static_cast<uint32_t>(sh.nbu);
+  m.g_upd = static_cast<uint32_t>(sh.nbc);
   // no kernel of an earlier solve that used this flag writes it any more:
-  // a solve releases its flag only after its stopping iteration has run
+  // a solve stops writing it at its stopping iteration, which had completed
+  // before the flag was released
   __atomic_store_n(hf->host, 0, __ATOMIC_RELEASE);
   __atomic_store_n(hf->host + 1, -1, __ATOMIC_RELEASE);
   {
@@ -788,114 +870,121 @@ int gnnshap::CgRun::begin(const CgProblem& pr, const CgShape& sh, const CgWs& w,
                                                                             w.csc_row);
     GS_LAUNCHED();
   }
+  S.mem.push_back(m);
   return GNNSHAP_OK;
+}
+
+bool gnnshap::CgGroup::ready() const {
+  const State& S = *st_;
+  return S.chunk < 2 || event_done(S.ev->ev[S.chunk & 1]);   // step() waits for the chunk before last
 }
 
 namespace {
 
-// Whether the work recorded by ev has completed, without waiting; a query
-// that finds it pending leaves no error behind for the next launch check.
-bool event_done(hipEvent_t ev) {
-  const hipError_t e = hipEventQuery(ev);
-  if (e == hipErrorNotReady) {
-    (void)hipGetLastError();
-    return false;
+// Fills g with the members selected by `take` (grid of member m: grid(m)),
+// each at iteration t + dt; returns the total number of workgroups.
+template <class Take, class Grid>
+uint32_t fill_group(GroupArgs& g, const std::vector<Member>& mem, int64_t dt, Take take, Grid grid) {
+  g.n = 0;
+  uint32_t total = 0;
+  for (const Member& m : mem) {
+    if (!take(m, m.t + dt)) continue;
+    g.a[g.n] = m.a;
+    g.t[g.n] = m.t + dt;
+    g.blk[g.n] = total;
+    total += grid(m);
+    ++g.n;
   }
-  return true;   // complete, or an error that the wait on it reports
+  g.blk[g.n] = total;
+  return total;
 }
 
 }  // namespace
 
-bool gnnshap::CgRun::ready() const {
-  if (!st_) return true;
-  const CgArgs& c = *st_;
-  if (c.chunk == 0) return true;
-  if (stopped_) return event_done(c.hf->ev[(c.chunk - 1) & 1]);   // finish() waits for the last chunk
-  return c.chunk < 2 || event_done(c.hf->ev[c.chunk & 1]);         // step() waits for the one before it
-}
-
-// Waits for the chunk before the last one queued and reads the stop flag;
-// unless the iteration has stopped, queues iterations t .. t + kChunk - 1
-// (pass A alone of iteration kMaxIt, which always stops) and records the
-// chunk's event.  The chunk event ring has two slots: chunk n reuses the
-// event of chunk n - 2, which has completed by then.
-int gnnshap::CgRun::step() {
-  if (!st_ || stopped_) return GNNSHAP_OK;
-  CgArgs& c = *st_;
-  const Args& a = c.a;
-  const CgShape& sh = c.sh;
-  hipStream_t s = c.s;
-  const bool random = sh.kr > 0;
-  if (c.chunk >= 2) {
-    GS_HIP(hipEventSynchronize(c.hf->ev[c.chunk & 1]));
-    if (__atomic_load_n(c.hf->host, __ATOMIC_ACQUIRE) != 0) {
-      stopped_ = true;
-      return GNNSHAP_OK;
+// Waits for the chunk before the last one queued; every member whose stop
+// flag is set gets phi and info queued (after the chunks already queued,
+// whose launches it leaves at once) and leaves the group.  Then queues
+// iterations t .. t + kChunk - 1 of every member left (pass A alone of
+// iteration kMaxIt, which always stops; nothing beyond it) and records the
+// chunk's event.  The ring has two events: chunk n reuses the event of chunk
+// n - 2, which has completed by then.
+int gnnshap::CgGroup::step() {
+  State& S = *st_;
+  if (S.mem.empty()) return GNNSHAP_OK;
+  hipStream_t s = s_;
+  if (S.chunk >= 2) {
+    GS_HIP(hipEventSynchronize(S.ev->ev[S.chunk & 1]));
+    for (size_t i = 0; i < S.mem.size();) {
+      Member& m = S.mem[i];
+      if (__atomic_load_n(m.hf->host, __ATOMIC_ACQUIRE) == 0) {
+        ++i;
+        continue;
+      }
+      const int64_t iters = __atomic_load_n(m.hf->host + 1, __ATOMIC_ACQUIRE);
+      last_iters_ = iters;
+      const CgShape& sh = m.sh;
+      timing_note_solve(sh.M, sh.wpr, sh.kr, iters, sh.rs, sh.nnz);
+      {
+        GS_TIMED("k_cg_finish", s);
+        // without enumerated classes, fewer than M - 1 random rows cannot
+        // determine psi (1-perp has M - 1 dimensions): reported like a failed pivot
+        const int32_t undetermined = (m.pr.alpha == 0.0 && sh.kr < sh.M - 1) ? 1 : 0;
+        k_cg_finish<<<1, 1024, 0, s>>>(m.w.x, sh.M, m.w.st, m.pr.fef, m.pr.phi, m.pr.info, undetermined);
+      }
+      GS_LAUNCHED();
+      m.hf->busy = false;
+      S.mem.erase(S.mem.begin() + static_cast<std::ptrdiff_t>(i));
     }
+    if (S.mem.empty()) return GNNSHAP_OK;
   }
-  if (c.t > kMaxIt) {
-    stopped_ = true;     // every iteration is queued; finish() waits for the last chunk
-    return GNNSHAP_OK;
-  }
-  const int64_t t_end = std::min(c.t + kChunk, kMaxIt + 1);
-  for (; c.t < t_end; ++c.t) {
-    const int64_t t = c.t;
+  GroupArgs g;
+  for (int64_t dt = 0; dt < kChunk; ++dt) {
+    uint32_t n = fill_group(g, S.mem, dt, [](const Member&, int64_t t) { return t <= kMaxIt; },
+                            [](const Member& m) { return m.ga; });
+    if (g.n == 0) break;
     {
       GS_TIMED("k_cg_pass_a", s);
-      k_cg_pass_a<<<c.ga, kWaves * 64, 0, s>>>(a, c.pr.blocked, c.w.r, c.w.upart, t);
+      k_cg_pass_a<<<n, kWaves * 64, 0, s>>>(g);
     }
     GS_LAUNCHED();
-    if (t == kMaxIt) continue;
-    if (random) {
+    n = fill_group(g, S.mem, dt, [](const Member& m, int64_t t) { return t < kMaxIt && m.sh.kr > 0; },
+                   [](const Member& m) { return m.g_rows; });
+    if (g.n > 0) {
       {
         GS_TIMED("k_cg_rows", s);
-        k_cg_rows<<<c.g_rows, 256, 0, s>>>(a);
+        k_cg_rows<<<n, 256, 0, s>>>(g);
       }
       GS_LAUNCHED();
+      n = fill_group(g, S.mem, dt, [](const Member& m, int64_t t) { return t < kMaxIt && m.sh.kr > 0; },
+                     [](const Member& m) { return m.gb; });
       {
         GS_TIMED("k_cg_pass_b", s);
-        k_cg_pass_b<<<c.gb, kWaves * 64, 0, s>>>(a, c.pr.T, c.w.u, c.w.qpart);
+        k_cg_pass_b<<<n, kWaves * 64, 0, s>>>(g);
       }
       GS_LAUNCHED();
     }
-    {
-      GS_TIMED("k_cg_update", s);
-      k_cg_update<<<static_cast<unsigned>(sh.nbc), 256, 0, s>>>(a, t);
+    n = fill_group(g, S.mem, dt, [](const Member&, int64_t t) { return t < kMaxIt; },
+                   [](const Member& m) { return m.g_upd; });
+    if (g.n > 0) {
+      {
+        GS_TIMED("k_cg_update", s);
+        k_cg_update<<<n, 256, 0, s>>>(g);
+      }
+      GS_LAUNCHED();
     }
-    GS_LAUNCHED();
   }
-  GS_HIP(hipEventRecord(c.hf->ev[c.chunk & 1], s));
-  ++c.chunk;
-  return GNNSHAP_OK;
-}
-
-int gnnshap::CgRun::finish(int64_t* iters_out) {
-  if (!st_) return fail(GNNSHAP_EINVAL, "solve not begun");
-  CgArgs& c = *st_;
-  if (c.chunk > 0) GS_HIP(hipEventSynchronize(c.hf->ev[(c.chunk - 1) & 1]));
-  const int64_t iters = __atomic_load_n(c.hf->host + 1, __ATOMIC_ACQUIRE);
-  if (iters_out) *iters_out = iters;
-  const CgShape& sh = c.sh;
-  timing_note_solve(sh.M, sh.wpr, sh.kr, iters, sh.rs, sh.nnz);
-  {
-    GS_TIMED("k_cg_finish", c.s);
-    // without enumerated classes, fewer than M - 1 random rows cannot
-    // determine psi (1-perp has M - 1 dimensions): reported like a failed pivot
-    const int32_t undetermined = (c.pr.alpha == 0.0 && sh.kr < sh.M - 1) ? 1 : 0;
-    k_cg_finish<<<1, 1024, 0, c.s>>>(c.w.x, sh.M, c.w.st, c.pr.fef, c.pr.phi, c.pr.info, undetermined);
-  }
-  GS_LAUNCHED();
-  c.hf->busy = false;
-  c.hf = nullptr;
-  st_.reset();
-  stopped_ = true;
+  for (Member& m : S.mem) m.t = std::min(m.t + kChunk, kMaxIt + 1);
+  GS_HIP(hipEventRecord(S.ev->ev[S.chunk & 1], s));
+  ++S.chunk;
   return GNNSHAP_OK;
 }
 
 int gnnshap::cg_solve(const CgProblem& pr, const CgShape& sh, const CgWs& w, hipStream_t s, int64_t* iters_out) {
-  CgRun run;
-  if (int st = run.begin(pr, sh, w, s)) return st;
-  while (!run.done())
-    if (int st = run.step()) return st;
-  return run.finish(iters_out);
+  CgGroup grp;
+  grp.set_stream(s);
+  if (int st = grp.add(pr, sh, w)) return st;
+  while (!grp.empty())
+    if (int st = grp.step()) return st;
+  if (iters_out) *iters_out = grp.last_iters();
+  return GNNSHAP_OK;
 }

@@ -1923,12 +1923,12 @@ extern "C" int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* 
   return GNNSHAP_OK;
 }
 
-// gnnshap_solve_wls up to the iteration of an iterative solve, which is left
-// to *run (begun on `stream`); other systems are queued in full and run is
-// left idle.
+// gnnshap_solve_wls up to the iteration of an iterative solve, whose system
+// joins *grp (its set-up queued on the group's stream, which must be
+// `stream`); other systems are queued in full and grp is left as it was.
 int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_class* classes, const uint64_t* masks,
                              const float* y, const float* f_empty_full, float* phi, int32_t* info, void* ws,
-                             size_t ws_bytes, void* stream, CgRun* run) {
+                             size_t ws_bytes, void* stream, CgGroup* grp) {
   GS_TRY_BEGIN
   gnnshap::clear_error();
   if (!classes || !masks || !y || !f_empty_full || !phi || !info || !ws)
@@ -1994,7 +1994,8 @@ int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_clas
     pr.fef = f_empty_full;
     pr.phi = phi;
     pr.info = info;
-    return run->begin(pr, cg_shape_of(plan, classes), w.cg, s);
+    if (grp->stream() != s) return gnnshap::fail(GNNSHAP_EINVAL, "solver group is on another stream");
+    return grp->add(pr, cg_shape_of(plan, classes), w.cg);
   }
   int32_t* counts = reinterpret_cast<int32_t*>(w.G);
   if (has_random) {
@@ -2163,12 +2164,13 @@ extern "C" int gnnshap_solve_wls(const gnnshap_sample_plan* plan, const gnnshap_
                                  const uint64_t* masks, const float* y, const float* f_empty_full, float* phi,
                                  int32_t* info, void* ws, size_t ws_bytes, void* stream) {
   GS_TRY_BEGIN
-  gnnshap::CgRun run;
-  if (int st = gnnshap::solve_wls_start(plan, classes, masks, y, f_empty_full, phi, info, ws, ws_bytes, stream, &run))
+  gnnshap::CgGroup grp;
+  grp.set_stream(static_cast<hipStream_t>(stream));
+  if (int st = gnnshap::solve_wls_start(plan, classes, masks, y, f_empty_full, phi, info, ws, ws_bytes, stream, &grp))
     return st;
-  while (!run.done())
-    if (int st = run.step()) return st;
-  return run.begun() ? run.finish(nullptr) : GNNSHAP_OK;
+  while (!grp.empty())
+    if (int st = grp.step()) return st;
+  return GNNSHAP_OK;
   GS_TRY_END
 }
 
