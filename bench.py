@@ -42,6 +42,8 @@ def parse():
                     help="batch: one launch per step for all targets; streams: per-target calls on several streams")
     ap.add_argument("--streams", type=int, default=3)
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--no-latency", action="store_true",
+                    help="skip the single-target latency pass (for counter runs)")
     ap.add_argument("--roofline-steps", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="bytes of a plain device copy run before the steps (counter calibration)")
@@ -207,12 +209,14 @@ def work_model(kernel, results, dims, solves):
                    the same count; k_eval_rows_mx on fp32 MFMA, the others on VALU
     k_cg_pass_a    per iteration of an iterative solve: the mask words of the random
                    rows kept as bits ((kr - rs) x ceil(M/64) x 8 bytes) + the vector r
-                   (8 M) + the product (8 (kr - rs))
-    k_cg_pass_b    the same words (bit-transposed) + u (8 (kr - rs)) + the product (8 M)
-    k_cg_rows      the player lists of the rs sparse rows (4 nnz bytes), the entries of
-                   r they select (8 nnz) and u (8 kr)
-    k_cg_pass_bs   the player-major lists (4 nnz + 8 (M + 1)), the entries of u they
-                   select (8 nnz) and the product (8 M)
+                   (8 M) + the product (8 (kr - rs)), and for the rs sparse rows their
+                   player lists (4 nnz + 8 (rs + 1)), the entries of r they select
+                   (8 nnz) and their products (8 rs)
+    k_cg_pass_b    the same words (bit-transposed) + u (8 (kr - rs)) + the product (8 M),
+                   and the player-major lists (4 nnz + 8 (M + 1)), the entries of u
+                   they select (8 nnz) and their products (8 M)
+    k_cg_rows      the pass-A partial products of the bit rows (8 npc (kr - rs), npc
+                   taken as ceil(ceil(M/64) / 16)) and u written (8 (kr - rs))
     k_cg_update    five fp64 vectors of M read (R^T u, r, p, s, x) and four written
     k_solve_mid / k_solve_one_batch (one-workgroup solves)
                    M^3/6 (Cholesky) + 2 M^2 (two triangular solves) MACs, 2 flop each
@@ -229,12 +233,14 @@ def work_model(kernel, results, dims, solves):
     if base.startswith("k_cg_"):
         tot = 0.0
         for M, wpr, kr, iters, rs, nnz in solves:
-            if base in ("k_cg_pass_a", "k_cg_pass_b"):
-                tot += iters * ((kr - rs) * wpr * 8.0 + 8.0 * M + 8.0 * (kr - rs))
+            bits = (kr - rs) * wpr * 8.0 + 8.0 * M + 8.0 * (kr - rs)
+            if base == "k_cg_pass_a":
+                tot += iters * (bits + 12.0 * nnz + 16.0 * rs + 8.0)
+            elif base == "k_cg_pass_b":
+                tot += iters * (bits + 12.0 * nnz + 16.0 * M + 8.0)
             elif base == "k_cg_rows":
-                tot += iters * (12.0 * nnz + 8.0 * kr)
-            elif base == "k_cg_pass_bs":
-                tot += iters * (12.0 * nnz + 16.0 * M + 8.0)
+                npc = -(-wpr // 16)
+                tot += iters * 8.0 * (npc + 1) * (kr - rs)
             elif base == "k_cg_update":
                 tot += iters * 72.0 * M
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
@@ -269,9 +275,9 @@ def work_model(kernel, results, dims, solves):
 
 
 CANDIDATES = {
-    "batch": ["k_cg_pass_a", "k_cg_pass_b", "k_cg_rows", "k_cg_pass_bs", "k_cg_update", "k_wide_l1", "k_eval_rows_mx_batch", "k_eval_rows_batch",
+    "batch": ["k_cg_pass_a", "k_cg_pass_b", "k_cg_rows", "k_cg_update", "k_wide_l1", "k_eval_rows_mx_batch", "k_eval_rows_batch",
               "k_solve_one_batch", "k_eval_l2_batch", "k_gram_batch", "k_rhs_tile_batch", "k_sample"],
-    "streams": ["k_cg_pass_a", "k_cg_pass_b", "k_cg_rows", "k_cg_pass_bs", "k_cg_update", "k_wide_l1", "k_solve_mid", "k_eval_rows_mx", "k_eval_l2",
+    "streams": ["k_cg_pass_a", "k_cg_pass_b", "k_cg_rows", "k_cg_update", "k_wide_l1", "k_solve_mid", "k_eval_rows_mx", "k_eval_l2",
                 "k_rhs_tile", "k_gram", "k_sample"],
 }
 
@@ -402,16 +408,19 @@ def main():
     assert all(i == 0 for i in infos), f"solver info {infos}"
 
     # explain latency per target: extraction to phi on the host, after one warm-up target
-    ex.explain(targets[0], cfg["p"], cfg["seed"]).phi.cpu()
-    lat = []
-    for v in targets:
-        t1 = time.perf_counter()
-        r = ex.explain(v, cfg["p"], cfg["seed"])
-        r.phi.cpu()
-        lat.append(1e3 * (time.perf_counter() - t1))
-    lat_sorted = sorted(lat)
-    p90 = lat_sorted[min(len(lat) - 1, int(round(0.9 * (len(lat) - 1))))]
-    print("latency pass done", file=sys.stderr, flush=True)
+    latency = None
+    if not args.no_latency:
+        ex.explain(targets[0], cfg["p"], cfg["seed"]).phi.cpu()
+        lat = []
+        for v in targets:
+            t1 = time.perf_counter()
+            r = ex.explain(v, cfg["p"], cfg["seed"])
+            r.phi.cpu()
+            lat.append(1e3 * (time.perf_counter() - t1))
+        lat_sorted = sorted(lat)
+        p90 = lat_sorted[min(len(lat) - 1, int(round(0.9 * (len(lat) - 1))))]
+        latency = {"median": statistics.median(lat), "p90": p90, "targets": len(lat)}
+        print("latency pass done", file=sys.stderr, flush=True)
 
     out = {
         "metric": "masked coalition evals/sec + explain latency per target node (1 GPU)",
@@ -430,7 +439,7 @@ def main():
                                f"{cfg['indptr'].size - 1} nodes, {cfg['indices'].size} edges, "
                                f"GCN {cfg['dims']}, {cfg['hops']}-hop",
                    "mode": args.mode},
-        "latency_ms": {"median": statistics.median(lat), "p90": p90, "targets": len(lat)},
+        "latency_ms": latency,
         "roofline": None,
         "cpu_baseline": cpu,
     }

@@ -26,8 +26,9 @@
  *       . two side streams with their events per device and calling host
  *         thread, events marking each evaluated target, and one worker host
  *         thread per calling thread (gnnshap_explain_batch);
- *       . mapped page-locked stop flags with two events each, one per
- *         iterative solve in flight (at most 8 per calling thread);
+ *       . mapped page-locked stop flags, one per iterative solve in flight
+ *         (at most 16 per calling thread), and two events per group of
+ *         iterative solves in flight (at most 8 groups per calling thread);
  *       . a fixed 512 KiB device array per GPU, in the library's code
  *         object (gnnshap_sample_coalitions_noalloc);
  *       . a host cache of recent (M, p) sample plans.
@@ -387,6 +388,13 @@ int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_s
  * X, target_class and the model as for gnnshap_eval_coalitions.  Two-layer
  * models with X W_1 given and one-workgroup systems run batched; other
  * targets go through the single-target kernels in the same sequence.
+ * Systems solved iteratively (more players than their plan's
+ * iterative_threshold) run in two groups of up to three on the library's
+ * side streams, each group advancing its systems together (one launch per
+ * pass of the iteration for the whole group); a system joins a group once
+ * its coalition values are computed.  The call returns once every
+ * iteration has stopped (it polls the groups' events); the last writes of
+ * phi and info are still queued, ordered before later work on `stream`.
  * EUNSUPPORTED: more than 65535 targets or M > 131072. */
 int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
                           const gnnshap_class* classes, int64_t n, const gnnshap_gcn* m,
