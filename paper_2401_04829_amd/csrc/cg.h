@@ -39,6 +39,7 @@ struct CgWs {
   int64_t* csc_ptr;   // M + 1: rows of each player, ascending
   int32_t* csc_row;   // nnz
   double* qs;         // M: R_s^T u
+  int64_t* sitem;     // nsi: pass-A work items over the sparse rows, (first row << 8) | log2(lanes per row)
 };
 
 // Launch shape of the iterative solver for M players and kr random
@@ -52,6 +53,7 @@ struct CgShape {
   int64_t nbu, nbc;        // partial sums of the row pass (the sparse rows' total, then one per
                            // workgroup of bit rows; also its workgroups), workgroups of the player passes
   int64_t nsa, nsb;        // sparse workgroups of pass A (rows) and pass B (players)
+  int64_t nsi;             // pass A's work items over the sparse rows (64 / lanes-per-row rows each)
   int64_t nrcd;            // row chunks of pass B's bit rows (0 without bit rows)
 };
 // The split of the random rows [rb0, rb0 + kr) of a class table into sparse

@@ -27,8 +27,11 @@
 // is at most M / kSparseDiv (the first ones: the plan orders random classes
 // by ascending size), in whole blocks of 64 rows, are kept as lists of their
 // players instead (sparse rows), built once per solve from the bits, row by
-// row and player by player (both in ascending order).  One wavefront sums a
-// list (lanes stride over it, then a fixed butterfly).
+// row and player by player (both in ascending order).  In pass A a group of
+// L lanes sums one row's list (each lane at most about four entries, then a
+// fixed butterfly over the group), L fixed per block of 64 rows from the
+// block's largest row, so a wavefront takes 64 / L rows at once; in pass B
+// one wavefront sums a player's list.
 //
 // Per iteration t:
 //   pass A   stopping test on gamma_t; partial products R r of the bit rows
@@ -66,7 +69,8 @@ struct Args {
   const uint64_t* T;         // the bit rows transposed (pass B)
   const int32_t* sz;
   int64_t M, wpr, kr, nrb, npc, pwords, nrc, rbc, nbu, nbc;
-  int64_t rs, rbd0, nsa, nsb, nrcd, nxa, nxb;
+  int64_t rs, rbd0, nsa, nsb, nrcd, nxa, nxb, nsi;
+  const int64_t* sitem;
   const int64_t* csr_ptr;
   const int32_t* csr_idx;
   const int64_t* csc_ptr;
@@ -245,6 +249,16 @@ __global__ void __launch_bounds__(256) k_cg_init(Args a, const double* __restric
   }
 }
 
+// Lanes per sparse row (as log2) for a block of 64 rows whose largest row
+// has c players: the power of two that gives each lane at most about four
+// entries, at most 64.  Host and device use the same rule.
+__host__ __device__ __forceinline__ int sparse_lanes_log2(int64_t c) {
+  const int64_t need = (c + 3) / 4;
+  int lg = 0;
+  while (lg < 6 && (int64_t(1) << lg) < need) ++lg;
+  return lg;
+}
+
 // Stopping test of iteration t, taken identically by every wave of pass A
 // from the partial sums of gamma_t; `writer` records the stop.
 __device__ __forceinline__ bool cg_stop(const Args& a, int64_t t, bool writer) {
@@ -313,10 +327,27 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(GroupArgs g) {
     if (cg_stop(a, t, false)) return;
     const int64_t x = bid - a.nxa * a.npc;
     double uu = 0.0, su = 0.0;
-    for (int64_t b = x * kWaves + wave; b < a.rs; b += a.nsa * kWaves) {
-      const int64_t e0 = a.csr_ptr[b];
-      const double v = wave_gather_sum(a.csr_idx + e0, a.csr_ptr[b + 1] - e0, r);
-      if (lane == 0) {
+    for (int64_t it = x * kWaves + wave; it < a.nsi; it += a.nsa * kWaves) {
+      const int64_t info = a.sitem[it];
+      const int lg = static_cast<int>(info & 0xff);
+      const int64_t b = (info >> 8) + (lane >> lg);   // this lane group's row
+      const int64_t e0 = a.csr_ptr[b], e1 = a.csr_ptr[b + 1];
+      double v;
+      if (lg == 6) {
+        v = wave_gather_sum(a.csr_idx + e0, e1 - e0, r);
+      } else {
+        // at most four entries per lane (the block's rows have at most 4 L
+        // players), their loads issued together
+        const int L = 1 << lg;
+        const int64_t e = e0 + (lane & (L - 1));
+        const double v0 = e < e1 ? r[a.csr_idx[e]] : 0.0;
+        const double v1 = e + L < e1 ? r[a.csr_idx[e + L]] : 0.0;
+        const double v2 = e + 2 * L < e1 ? r[a.csr_idx[e + 2 * L]] : 0.0;
+        const double v3 = e + 3 * L < e1 ? r[a.csr_idx[e + 3 * L]] : 0.0;
+        v = (v0 + v1) + (v2 + v3);
+        for (int off = L >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off);
+      }
+      if ((lane & ((1 << lg) - 1)) == 0) {
         a.u[b] = v;
         uu += v * v;
         su += static_cast<double>(a.sz[b]) * v;
@@ -458,8 +489,29 @@ __device__ void block_scan_i64(const T* __restrict__ v, int64_t n, int64_t* __re
 
 // Row-major lists: csr_ptr = exclusive prefix sums of the sparse rows' sizes.
 __global__ void __launch_bounds__(1024) k_cg_csr_ptr(const int32_t* __restrict__ sz, int64_t rs,
-                                                     int64_t* __restrict__ ptr) {
+                                                     int64_t* __restrict__ ptr, int64_t* __restrict__ sitem) {
   block_scan_i64(sz, rs, ptr);
+  // pass A's work items: block q (rows 64 q .. 64 q + 63, sizes ascending)
+  // gives 2^lg items of 64 / 2^lg rows each, lg from its largest row
+  // (at most 1024 blocks: thread q owns block q; an inclusive scan of the
+  // item counts in LDS, Hillis-Steele)
+  __shared__ int64_t cnt[2][1024];
+  const int64_t nblk = rs / 64;
+  const int q = threadIdx.x;
+  const int lg = q < nblk ? sparse_lanes_log2(sz[64 * q + 63]) : 0;
+  cnt[0][q] = q < nblk ? (int64_t(1) << lg) : 0;
+  __syncthreads();
+  int cur = 0;
+  for (int off = 1; off < 1024; off <<= 1) {
+    cnt[cur ^ 1][q] = cnt[cur][q] + (q >= off ? cnt[cur][q - off] : 0);
+    cur ^= 1;
+    __syncthreads();
+  }
+  if (q < nblk) {
+    const int64_t first = cnt[cur][q] - (int64_t(1) << lg);
+    const int64_t rows = int64_t(64) >> lg;
+    for (int64_t g = 0; g < (int64_t(1) << lg); ++g) sitem[first + g] = ((int64_t(64) * q + g * rows) << 8) | lg;
+  }
 }
 
 // Row-major lists: wavefront g reads the words of its 64 rows from the
@@ -698,7 +750,9 @@ gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t r
       for (int64_t r = from; r < classes[i].row_begin + classes[i].row_count; ++r) sz.push_back(classes[i].size);
     }
     s.rs = (std::min<int64_t>(static_cast<int64_t>(sz.size()), kr) / 64) * 64;
+    if (s.rs > 64 * 1024) s.rs = 64 * 1024;   // the item table's scan holds 1024 blocks
     for (int64_t b = 0; b < s.rs; ++b) s.nnz += sz[b];
+    for (int64_t q = 0; q < s.rs / 64; ++q) s.nsi += int64_t(1) << sparse_lanes_log2(sz[64 * q + 63]);
   }
   s.rbd0 = s.rs / 64;
   const int64_t nrbd = std::max<int64_t>(s.nrb - s.rbd0, 1);
@@ -714,7 +768,7 @@ gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t r
   s.nrc = ceil_div(nrbd, s.rbc);
   // workgroups of the sparse rows in pass A (rows) and pass B (players), at
   // most 2048 each (each wave loops), and of the bit rows in the row pass
-  s.nsa = s.rs > 0 ? std::min<int64_t>(ceil_div(s.rs, kWaves), 2048) : 0;
+  s.nsa = s.rs > 0 ? std::min<int64_t>(ceil_div(s.nsi, kWaves), 2048) : 0;
   s.nsb = s.rs > 0 ? std::min<int64_t>(ceil_div(M, kWaves), 2048) : 0;
   s.nrcd = s.rbd0 < s.nrb ? s.nrc : 0;
   s.nbu = 1 + ceil_div(kr - s.rs > 0 ? kr - s.rs : 1, 256);
@@ -744,6 +798,7 @@ gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
   w.csc_ptr = c.take<int64_t>(sh.M + 1);
   w.csc_row = c.take<int32_t>(sh.nnz > 0 ? sh.nnz : 1);
   w.qs = c.take<double>(sh.M);
+  w.sitem = c.take<int64_t>(sh.nsi > 0 ? sh.nsi : 1);
   return w;
 }
 
@@ -826,6 +881,8 @@ int gnnshap::CgGroup::add(const CgProblem& pr, const CgShape& sh, const CgWs& w)
   a.rs = sh.rs;
   a.rbd0 = sh.rbd0;
   a.nsa = sh.nsa;
+  a.nsi = sh.nsi;
+  a.sitem = w.sitem;
   a.nsb = sh.nsb;
   a.nrcd = sh.nrcd;
   a.nxa = ceil_div(std::max<int64_t>(sh.nrb - sh.rbd0, 1), kWaves);
@@ -856,7 +913,7 @@ int gnnshap::CgGroup::add(const CgProblem& pr, const CgShape& sh, const CgWs& w)
     // count scratch here, it is written before the iterations read it
     const int64_t nrb_s = sh.rs / 64;
     GS_TIMED("k_cg_sparse_build", s);
-    k_cg_csr_ptr<<<1, 1024, 0, s>>>(w.sz, sh.rs, w.csr_ptr);
+    k_cg_csr_ptr<<<1, 1024, 0, s>>>(w.sz, sh.rs, w.csr_ptr, w.sitem);
     GS_LAUNCHED();
     k_cg_csr_fill<<<static_cast<unsigned>(nrb_s), 64, 0, s>>>(pr.blocked, sh.wpr, sh.rs, w.csr_ptr, sh.nnz,
                                                              w.csr_idx);
