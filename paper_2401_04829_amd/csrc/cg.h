@@ -54,6 +54,7 @@ struct CgShape {
                            // workgroup of bit rows; also its workgroups), workgroups of the player passes
   int64_t nsa, nsb;        // sparse workgroups of pass A (rows) and pass B (players)
   int64_t nsi;             // pass A's work items over the sparse rows (64 / lanes-per-row rows each)
+  int32_t lgb;             // pass B: log2 of the lanes per player list (64 / 2^lgb players per wavefront)
   int64_t nrcd;            // row chunks of pass B's bit rows (0 without bit rows)
 };
 // The split of the random rows [rb0, rb0 + kr) of a class table into sparse

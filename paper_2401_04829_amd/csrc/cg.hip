@@ -31,7 +31,7 @@
 // L lanes sums one row's list (each lane at most about four entries, then a
 // fixed butterfly over the group), L fixed per block of 64 rows from the
 // block's largest row, so a wavefront takes 64 / L rows at once; in pass B
-// one wavefront sums a player's list.
+// groups of lanes sized from the mean list length sum the players' lists.
 //
 // Per iteration t:
 //   pass A   stopping test on gamma_t; partial products R r of the bit rows
@@ -70,6 +70,7 @@ struct Args {
   const int32_t* sz;
   int64_t M, wpr, kr, nrb, npc, pwords, nrc, rbc, nbu, nbc;
   int64_t rs, rbd0, nsa, nsb, nrcd, nxa, nxb, nsi;
+  int32_t lgb;     // pass B: log2 of the lanes summing one player's list
   const int64_t* sitem;
   const int64_t* csr_ptr;
   const int32_t* csr_idx;
@@ -416,8 +417,8 @@ __global__ void __launch_bounds__(256) k_cg_rows(GroupArgs g) {
 // the chunk's nibble tables of u in LDS (u is padded with zeros to whole row
 // blocks), then one wave per 64 players (lane = player) reads the
 // bit-transposed words T[rb, j] and sums table entries.  Workgroup
-// nxb * nrcd + x (x < nsb): the players x * kWaves + wave, + nsb * kWaves,
-// ...: qs[j] = sum of u over the sparse rows holding player j.
+// nxb * nrcd + x (x < nsb): groups of 64 / L players (x * kWaves + wave, +
+// nsb * kWaves, ...): qs[j] = sum of u over the sparse rows holding player j.
 __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(GroupArgs g) {
   __shared__ double tab[kTabWords * 256];
   int64_t bid;
@@ -430,12 +431,30 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(GroupArgs g) {
   const int64_t c = bid < a.nxb * a.nrcd ? bid / a.nxb : a.nrcd;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (c == a.nrcd) {                  // sparse rows
+  if (c == a.nrcd) {                  // sparse rows: 64 / L players per wavefront
     const int64_t x = bid - a.nxb * a.nrcd;
-    for (int64_t j = x * kWaves + wave; j < a.M; j += a.nsb * kWaves) {
-      const int64_t e0 = a.csc_ptr[j];
-      const double v = wave_gather_sum(a.csc_row + e0, a.csc_ptr[j + 1] - e0, u);
-      if (lane == 0) a.qs[j] = v;
+    const int lg = a.lgb, L = 1 << lg;
+    const int64_t nit = (a.M + (64 >> lg) - 1) >> (6 - lg);
+    for (int64_t it = x * kWaves + wave; it < nit; it += a.nsb * kWaves) {
+      const int64_t j = (it << (6 - lg)) + (lane >> lg);
+      double v;
+      if (lg == 6) {
+        const int64_t e0 = a.csc_ptr[j];
+        v = wave_gather_sum(a.csc_row + e0, a.csc_ptr[j + 1] - e0, u);
+      } else {
+        const bool ok = j < a.M;
+        const int64_t e1 = ok ? a.csc_ptr[j + 1] : 0;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        for (int64_t e = (ok ? a.csc_ptr[j] : 0) + (lane & (L - 1)); e < e1; e += 4 * L) {
+          s0 += u[a.csc_row[e]];
+          if (e + L < e1) s1 += u[a.csc_row[e + L]];
+          if (e + 2 * L < e1) s2 += u[a.csc_row[e + 2 * L]];
+          if (e + 3 * L < e1) s3 += u[a.csc_row[e + 3 * L]];
+        }
+        v = (s0 + s1) + (s2 + s3);
+        for (int off = L >> 1; off > 0; off >>= 1) v += __shfl_xor(v, off);
+      }
+      if ((lane & (L - 1)) == 0 && j < a.M) a.qs[j] = v;
     }
     return;
   }
@@ -769,7 +788,9 @@ gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t r
   // workgroups of the sparse rows in pass A (rows) and pass B (players), at
   // most 2048 each (each wave loops), and of the bit rows in the row pass
   s.nsa = s.rs > 0 ? std::min<int64_t>(ceil_div(s.nsi, kWaves), 2048) : 0;
-  s.nsb = s.rs > 0 ? std::min<int64_t>(ceil_div(M, kWaves), 2048) : 0;
+  // pass B: lanes per player list from the mean list length (longer lists loop)
+  s.lgb = sparse_lanes_log2(ceil_div(s.nnz, M));
+  s.nsb = s.rs > 0 ? std::min<int64_t>(ceil_div(ceil_div(M, int64_t(64) >> s.lgb), kWaves), 2048) : 0;
   s.nrcd = s.rbd0 < s.nrb ? s.nrc : 0;
   s.nbu = 1 + ceil_div(kr - s.rs > 0 ? kr - s.rs : 1, 256);
   s.nbc = ceil_div(wpr * 64, 256);
@@ -882,6 +903,7 @@ int gnnshap::CgGroup::add(const CgProblem& pr, const CgShape& sh, const CgWs& w)
   a.rbd0 = sh.rbd0;
   a.nsa = sh.nsa;
   a.nsi = sh.nsi;
+  a.lgb = sh.lgb;
   a.sitem = w.sitem;
   a.nsb = sh.nsb;
   a.nrcd = sh.nrcd;
