@@ -62,7 +62,7 @@ constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
 constexpr int kWaves = 8;            // waves per workgroup of both passes
 constexpr int64_t kTabWords = 16;    // nibble tables per workgroup: 16 words (32 KiB of LDS)
-constexpr int64_t kSparseDiv = 64;   // sparse rows: coalition size at most M / kSparseDiv
+constexpr int64_t kSparseDiv = 128;   // sparse rows: coalition size at most M / kSparseDiv
 
 struct Args {
   const uint64_t* blocked;   // the bit rows in row blocks (pass A)

@@ -182,7 +182,7 @@ __global__ void __launch_bounds__(256) k_wide_deg(const uint64_t* __restrict__ m
 // ft, features 16 ft + 4 g .. + 3 of row c0 + 16 ct + r.  Writes
 // t[fb][row][x] for the row and, with pairs, for row + khalf.
 template <bool PAIRS>
-__global__ void __launch_bounds__(kBlockRows) k_wide_l1(
+__global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
     const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows, int64_t khalf, int64_t cblocks,
     const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src, int64_t n1,
     const int32_t* __restrict__ seg, const float4* __restrict__ Zop, int ntot, int h, const float* __restrict__ Zc,
@@ -219,22 +219,27 @@ __global__ void __launch_bounds__(kBlockRows) k_wide_l1(
 #pragma unroll
   for (int ft = 0; ft < kTiles; ++ft)
     a[ft] = (ft < nt && nu > 0) ? zp[ft * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
-  uint64_t win[4] = {0, 0, 0, 0};
+  // the mask bits of 64 players (units q .. q + 3) of each of the lane's rows;
+  // the window of the next four units is loaded while these are multiplied
+  auto window = [&](int q, int ct) -> uint64_t {
+    if (!valid[ct] || q >= nu) return 0;
+    const int64_t pb = e0 + static_cast<int64_t>(kUnit) * q;
+    const int64_t wa = pb >> 6;
+    const int sh = static_cast<int>(pb & 63);
+    const uint64_t* mr = masks + row[ct] * wpr;
+    const uint64_t lo = mr[wa];
+    const uint64_t hi = (sh && wa + 1 < wpr) ? mr[wa + 1] : 0;
+    return sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+  };
+  uint64_t win[4], wnext[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) wnext[ct] = window(0, ct);
   for (int q = 0; q < nu; ++q) {
-    if ((q & 3) == 0) {                          // the mask bits of the next 64 players
-      const int64_t pb = e0 + static_cast<int64_t>(kUnit) * q;
-      const int64_t wa = pb >> 6;
-      const int sh = static_cast<int>(pb & 63);
+    if ((q & 3) == 0) {
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
-        uint64_t w = 0;
-        if (valid[ct]) {
-          const uint64_t* mr = masks + row[ct] * wpr;
-          const uint64_t lo = mr[wa];
-          const uint64_t hi = (sh && wa + 1 < wpr) ? mr[wa + 1] : 0;
-          w = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
-        }
-        win[ct] = w;
+        win[ct] = wnext[ct];
+        wnext[ct] = window(q + 4, ct);
       }
     }
     // next unit's operands while this unit is multiplied
