@@ -197,14 +197,16 @@ HBM_PEAK_GBS = 8000.0
 VALU_FP32_TFLOPS = 78.6
 VALU_INT_TOPS = 39.3
 MFMA_FP32_TFLOPS = 157.3
+MFMA_BF16_TFLOPS = 2500.0
 
 
 def work_model(kernel, results, dims, solves):
     """Algorithmic work of the timed kernel over the timed steps: (amount, unit, bound, peak).
 
     k_wide_l1      two-layer GCN, wide hidden layer: (k/2) M h useful MACs per target
-                   (complement pairs cover every player-feature product once) + k n1 h
-                   for the class logit, 2 flop each; fp32 MFMA
+                   (complement pairs cover every player-feature product once), 2 flop
+                   each, run as three bf16 products (the fp32 values split exactly into
+                   hi + mid + lo), so 3 x that against the bf16 MFMA peak
     k_eval_rows_mx, k_eval_rows, k_eval_l2
                    the same count; k_eval_rows_mx on fp32 MFMA, the others on VALU
     k_cg_pass_a    per iteration of an iterative solve: the mask words of the random
@@ -254,7 +256,9 @@ def work_model(kernel, results, dims, solves):
         if base in ("k_solve_mid", "k_solve_one"):
             if path == 1:
                 tot += 2.0 * (M ** 3 / 6.0 + 2.0 * M * M)
-        elif base in ("k_eval_l2", "k_eval_rows", "k_eval_rows_mx", "k_wide_l1"):
+        elif base == "k_wide_l1":
+            tot += 3.0 * 2.0 * (k / 2.0) * M * h
+        elif base in ("k_eval_l2", "k_eval_rows", "k_eval_rows_mx"):
             n1 = r.sub.sg.hop_ptr[2]
             tot += 2.0 * ((k / 2.0) * M * h + k * n1 * h)
         elif base == "k_gram":
@@ -269,7 +273,9 @@ def work_model(kernel, results, dims, solves):
         return tot, "GB/s", "hbm", HBM_PEAK_GBS
     if base == "k_gram":
         return tot, "Tops/s", "alu", VALU_INT_TOPS
-    if base in ("k_eval_rows_mx", "k_wide_l1"):
+    if base == "k_wide_l1":
+        return tot, "TFLOP/s", "mfma", MFMA_BF16_TFLOPS
+    if base == "k_eval_rows_mx":
         return tot, "TFLOP/s", "mfma", MFMA_FP32_TFLOPS
     return tot, "TFLOP/s", "alu", VALU_FP32_TFLOPS
 

@@ -11,7 +11,11 @@
 // every coalition: for those players the sum is a 0/1 contraction
 //   D_c[f] = sum_e [e in c] Z[src e][f],
 // a (features x players) x (players x coalitions) product with the mask bits
-// as the right operand, run here on v_mfma_f32_16x16x4f32.  The few players
+// as the right operand.  The mask bits are exact in bf16 and each fp32 value
+// of Z is the exact sum of three bf16 parts (hi + mid + lo, 8 significant
+// bits each), so the product runs on v_mfma_f32_16x16x32_bf16, three per
+// operand tile, with fp32 accumulation: the same sums as an fp32 product at
+// a sixteenth of the MFMA cycles per flop.  The few players
 // whose source lies in H_1 (the in-edges of v, the edge v -> x, edges between
 // in-neighbours) carry a coalition-dependent d^-1/2 and are added in the
 // epilogue.  For the sampler's complement pairs (row b + k/2 = NOT row b),
@@ -26,14 +30,15 @@
 //                wavefront per class
 //   k_wide_prep  one workgroup: operand-unit offsets of each node and the
 //                list of players whose source is in H_1
-//   k_wide_zop   the A operands: for 16 players (one unit) and 16 features
+//   k_wide_zop   the A operands: for 32 players (one unit) and 16 features
 //                (one tile), lane (r, g) of a wavefront holds Z[src][f] for
-//                feature 16 tile + r and players 4 s + g, s = 0..3, as one
-//                float4 (zero for padding and for the players above)
+//                feature 16 tile + r and players 8 g .. 8 g + 7, as three
+//                uint4 of eight bf16 (hi, mid, lo; zero for padding and for
+//                the players above)
 //   k_wide_sum   S (pairs only): per node and feature, fixed summation order
 //   k_wide_deg   in-degree of every node of H_1 under every contracted row
-//   k_wide_l1    one workgroup per (node, 256 coalitions, 128 features):
-//                four wavefronts of 64 coalitions, 4 x 8 16x16 output tiles
+//   k_wide_l1    one workgroup per (node, 256 coalitions, 64 features):
+//                four wavefronts of 64 coalitions, 4 x 4 16x16 output tiles
 //                each; then the epilogue to t_c[x] (and the complement's)
 //   k_wide_out   y per row from t, the degrees and the mask bits of v's in-edges
 #include "wide.h"
@@ -41,12 +46,22 @@
 namespace {
 
 typedef float mx4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8_t __attribute__((ext_vector_type(8)));
 
 constexpr int kWaves = 4;                      // wavefronts per workgroup
 constexpr int kWaveRows = 64;                  // coalitions per wavefront (four tiles of 16)
 constexpr int kBlockRows = kWaves * kWaveRows;
-constexpr int kTiles = 8;                      // 16-feature tiles per workgroup
-constexpr int kUnit = 16;                      // players per operand unit (four MFMA steps of four)
+constexpr int kTiles = 4;                      // 16-feature tiles per workgroup
+constexpr int kUnit = 32;                      // players per operand unit (one bf16 MFMA step)
+constexpr int kParts = 3;                      // bf16 parts of an fp32 operand: hi + mid + lo
+
+// fp32 -> bf16 bits, rounded to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t bf16_bits(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float bf16_value(uint32_t b) { return __uint_as_float(b << 16); }
 
 __global__ void __launch_bounds__(1024) k_wide_prep(const int32_t* __restrict__ dst_ptr,
                                                     const int32_t* __restrict__ edge_src, int64_t n1,
@@ -92,10 +107,16 @@ __global__ void __launch_bounds__(1024) k_wide_prep(const int32_t* __restrict__ 
   }
 }
 
+// The A operands in bf16 parts: for unit U (32 players of one node), feature
+// tile ft and lane (r, g), the eight values Z[src][16 ft + r] of players
+// 8 g .. 8 g + 7 of the unit (zero for padding and for sources in H_1),
+// each split into hi + mid + lo (round to nearest at each step, so the three
+// parts add up to the fp32 value exactly), stored as three uint4 of eight
+// bf16: part p of (U, ft) at Zop[((U ntot + ft) kParts + p) 64 + lane].
 __global__ void __launch_bounds__(256) k_wide_zop(const int32_t* __restrict__ dst_ptr,
                                                   const int32_t* __restrict__ edge_src, int64_t n1,
                                                   const int32_t* __restrict__ seg, const float* __restrict__ Zc, int h,
-                                                  int ntot, int64_t units_cap, float4* __restrict__ Zop) {
+                                                  int ntot, int64_t units_cap, uint4* __restrict__ Zop) {
   const int64_t units = seg[n1];
   const int64_t total = units * ntot * 64;
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
@@ -115,14 +136,29 @@ __global__ void __launch_bounds__(256) k_wide_zop(const int32_t* __restrict__ ds
     const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
     const int base = e0 + static_cast<int>(U - seg[x]) * kUnit;
     const int f = 16 * ft + (lane & 15), g = lane >> 4;
-    float v[4];
+    uint32_t w[kParts][4];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int e = base + 4 * s + g;
-      const int32_t u = e < e1 ? edge_src[e] : 0;
-      v[s] = (e < e1 && u >= n1) ? Zc[static_cast<int64_t>(u) * h + f] : 0.f;
+    for (int t = 0; t < 8; t += 2) {
+      uint32_t pb[kParts][2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int e = base + 8 * g + t + i;
+        const int32_t u = e < e1 ? edge_src[e] : 0;
+        const float v = (e < e1 && u >= n1) ? Zc[static_cast<int64_t>(u) * h + f] : 0.f;
+        const uint32_t b0 = bf16_bits(v);
+        const float r1 = v - bf16_value(b0);
+        const uint32_t b1 = bf16_bits(r1);
+        const uint32_t b2 = bf16_bits(r1 - bf16_value(b1));
+        pb[0][i] = b0;
+        pb[1][i] = b1;
+        pb[2][i] = b2;
+      }
+#pragma unroll
+      for (int p = 0; p < kParts; ++p) w[p][t / 2] = pb[p][0] | (pb[p][1] << 16);
     }
-    Zop[idx] = make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+    for (int p = 0; p < kParts; ++p)
+      Zop[(rest * kParts + p) * 64 + lane] = make_uint4(w[p][0], w[p][1], w[p][2], w[p][3]);
   }
 }
 
@@ -176,7 +212,7 @@ __global__ void __launch_bounds__(256) k_wide_deg(const uint64_t* __restrict__ m
 }
 
 // Layer 1 at node x = blockIdx.x / cblocks for 256 coalitions (block
-// blockIdx.x % cblocks) and features 128 blockIdx.y .. + 127.  Wavefront w
+// blockIdx.x % cblocks) and features 64 blockIdx.y .. + 63.  Wavefront w
 // holds rows c0 .. c0 + 63, c0 = 256 block + 64 w, as four 16-row tiles;
 // lane (r, g) = (lane % 16, lane / 16) holds, per tile ct and feature tile
 // ft, features 16 ft + 4 g .. + 3 of row c0 + 16 ct + r.  Writes
@@ -185,7 +221,7 @@ template <bool PAIRS>
 __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
     const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows, int64_t khalf, int64_t cblocks,
     const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src, int64_t n1,
-    const int32_t* __restrict__ seg, const float4* __restrict__ Zop, int ntot, int h, const float* __restrict__ Zc,
+    const int32_t* __restrict__ seg, const uint4* __restrict__ Zop, int ntot, int h, const float* __restrict__ Zc,
     const float* __restrict__ S, const int32_t* __restrict__ spec_ptr, const int32_t* __restrict__ spec_e,
     const int32_t* __restrict__ deg, const float* __restrict__ b1, const float* __restrict__ W2, int C,
     const int32_t* __restrict__ ctl, float* __restrict__ t, int64_t k) {
@@ -213,14 +249,21 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
 #pragma unroll
     for (int ft = 0; ft < kTiles; ++ft) D[ct][ft] = mx4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int64_t ustride = static_cast<int64_t>(ntot) * 64;
-  const float4* zp = Zop + static_cast<int64_t>(u0) * ustride + ft0 * 64 + lane;
-  float4 a[kTiles], an[kTiles];
+  // A operands of unit q: lane's three parts for each of the kTiles feature
+  // tiles; the next unit's are loaded while this one is multiplied
+  const int64_t ustride = static_cast<int64_t>(ntot) * kParts * 64;
+  const uint4* zp = Zop + static_cast<int64_t>(u0) * ustride + static_cast<int64_t>(ft0) * kParts * 64 + lane;
+  // (every load is of a valid unit and tile: the last unit's successor and
+  // the tiles beyond nt repeat a valid one, whose products are not used)
+  uint4 a[kTiles][kParts], an[kTiles][kParts];
+  if (nu > 0) {
 #pragma unroll
-  for (int ft = 0; ft < kTiles; ++ft)
-    a[ft] = (ft < nt && nu > 0) ? zp[ft * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
-  // the mask bits of 64 players (units q .. q + 3) of each of the lane's rows;
-  // the window of the next four units is loaded while these are multiplied
+    for (int ft = 0; ft < kTiles; ++ft)
+#pragma unroll
+      for (int p = 0; p < kParts; ++p) a[ft][p] = zp[((ft < nt ? ft : nt - 1) * kParts + p) * 64];
+  }
+  // the mask bits of 64 players (units q, q + 1) of each of the lane's rows;
+  // the window of the next two units is loaded while these are multiplied
   auto window = [&](int q, int ct) -> uint64_t {
     if (!valid[ct] || q >= nu) return 0;
     const int64_t pb = e0 + static_cast<int64_t>(kUnit) * q;
@@ -235,37 +278,40 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) wnext[ct] = window(0, ct);
   for (int q = 0; q < nu; ++q) {
-    if ((q & 3) == 0) {
+    if ((q & 1) == 0) {
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
         win[ct] = wnext[ct];
-        wnext[ct] = window(q + 4, ct);
+        wnext[ct] = window(q + 2, ct);
       }
     }
-    // next unit's operands while this unit is multiplied
-    const bool more = q + 1 < nu;
+    const int64_t qn = q + 1 < nu ? q + 1 : q;
 #pragma unroll
     for (int ft = 0; ft < kTiles; ++ft)
-      an[ft] = (ft < nt && more) ? zp[(q + 1) * ustride + ft * 64] : make_float4(0.f, 0.f, 0.f, 0.f);
-    uint32_t part[4];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) part[ct] = static_cast<uint32_t>(win[ct] >> (16 * (q & 3)));
+      for (int p = 0; p < kParts; ++p) an[ft][p] = zp[qn * ustride + ((ft < nt ? ft : nt - 1) * kParts + p) * 64];
+    // B: the lane's eight players 8 g .. 8 g + 7 of the unit for row 16 ct +
+    // rl, as eight bf16 of 0.0 or 1.0 (0x3F80), two per dword
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int ct = 0; ct < 4; ++ct) {
+      const uint32_t byte = static_cast<uint32_t>(win[ct] >> (32 * (q & 1) + 8 * g)) & 0xffu;
+      uint32_t bw[4];
 #pragma unroll
-      for (int ct = 0; ct < 4; ++ct) {
-        const float bv = ((part[ct] >> (4 * s + g)) & 1u) ? 1.0f : 0.0f;
+      for (int t = 0; t < 4; ++t)
+        bw[t] = (((byte >> (2 * t)) & 1u) | (((byte >> (2 * t + 1)) & 1u) << 16)) * 0x3F80u;
+      const bf8_t bv = __builtin_bit_cast(bf8_t, make_uint4(bw[0], bw[1], bw[2], bw[3]));
+      // (tiles beyond nt multiply a repeated valid tile; the epilogue skips them)
 #pragma unroll
-        for (int ft = 0; ft < kTiles; ++ft) {
-          if (ft < nt) {
-            const float av = s == 0 ? a[ft].x : s == 1 ? a[ft].y : s == 2 ? a[ft].z : a[ft].w;
-            D[ct][ft] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, D[ct][ft], 0, 0, 0);
-          }
-        }
-      }
+      for (int ft = 0; ft < kTiles; ++ft)
+#pragma unroll
+        for (int p = 0; p < kParts; ++p)
+          D[ct][ft] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8_t, a[ft][p]), bv, D[ct][ft],
+                                                              0, 0, 0);
     }
 #pragma unroll
-    for (int ft = 0; ft < kTiles; ++ft) a[ft] = an[ft];
+    for (int ft = 0; ft < kTiles; ++ft)
+#pragma unroll
+      for (int p = 0; p < kParts; ++p) a[ft][p] = an[ft][p];
   }
 
   // epilogue: the players whose source is in H_1, self loop, bias, ReLU and
@@ -501,7 +547,7 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
   w.seg = c.take<int32_t>(s.n1 + 1);
   w.spec_ptr = c.take<int32_t>(s.n1 + 1);
   w.spec_e = c.take<int32_t>(s.M);
-  w.Zop = c.take<float4>(s.units_cap * s.ntot * 64);
+  w.Zop = c.take<uint4>(s.units_cap * s.ntot * kParts * 64);
   w.S = c.take<float>(s.n1 * s.h);
   w.deg = c.take<int32_t>(s.k * s.n1);
   w.t = c.take<float>(static_cast<int64_t>(s.nfb) * s.k * s.n1);

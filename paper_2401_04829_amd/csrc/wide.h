@@ -24,7 +24,7 @@ struct WideWs {
   int32_t* seg;       // n1 + 1: first operand unit of each node of H_1
   int32_t* spec_ptr;  // n1 + 1: players of each node whose source is in H_1
   int32_t* spec_e;    // M
-  float4* Zop;        // units_cap x ntot x 64: A operands (see the kernels)
+  uint4* Zop;         // units_cap x ntot x 3 x 64: A operands in bf16 parts (see the kernels)
   float* S;           // n1 x h: sum of the operand rows of each node
   int32_t* deg;       // k x n1: in-degree of each node of H_1 under each evaluated row
   float* t;           // nfb x k x n1: each node's layer-1 output times the explained class's W_2 column
