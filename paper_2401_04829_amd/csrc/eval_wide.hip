@@ -315,16 +315,65 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
   }
 
   // epilogue: the players whose source is in H_1, self loop, bias, ReLU and
-  // the explained class's column of W_2, per row (and its complement)
+  // the explained class's column of W_2, per row (and its complement).  The
+  // player loop runs once for the four row tiles: its source, the source's
+  // size and its feature values are loaded once, each row tile adds them
+  // with its own coefficient (0 for the coalition it is not in).
   const int cls = ctl[0];
   const int nx = e1 - e0;
   const int sp0 = spec_ptr[x], sp1 = spec_ptr[x + 1];
+  const int32_t* dgr[4];
+  const uint64_t* mrr[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
     const int64_t rr = valid[ct] ? row[ct] : 0;
-    const int32_t* dg = deg + rr * n1;
-    const uint64_t* mr = masks + rr * wpr;
-    const int dgx = dg[x];
+    dgr[ct] = deg + rr * n1;
+    mrr[ct] = masks + rr * wpr;
+  }
+  mx4_t P[4][kTiles];   // the complement's sums (pairs)
+#pragma unroll
+  for (int ft = 0; ft < kTiles; ++ft) {
+    const int f = 16 * (ft0 + (ft < nt ? ft : nt - 1)) + 4 * g;
+    const float4 s4 = PAIRS ? *reinterpret_cast<const float4*>(S + x * h + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+      P[ct][ft] = mx4_t{s4.x - D[ct][ft][0], s4.y - D[ct][ft][1], s4.z - D[ct][ft][2], s4.w - D[ct][ft][3]};
+  }
+  for (int sp = sp0; sp < sp1; ++sp) {
+    const int e = spec_e[sp];
+    const int32_t u = edge_src[e];
+    const int nuu = PAIRS ? dst_ptr[u + 1] - dst_ptr[u] : 0;
+    float cw[4], cp[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const bool bit = (mrr[ct][e >> 6] >> (e & 63)) & 1;
+      const int du = dgr[ct][u];
+      cw[ct] = bit ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(du)) : 0.f;
+      cp[ct] = (PAIRS && !bit) ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(nuu - du)) : 0.f;
+    }
+#pragma unroll
+    for (int ft = 0; ft < kTiles; ++ft) {
+      if (ft >= nt) continue;
+      const int f = 16 * (ft0 + ft) + 4 * g;
+      const float4 zu = *reinterpret_cast<const float4*>(Zc + static_cast<int64_t>(u) * h + f);
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        D[ct][ft][0] = fmaf(cw[ct], zu.x, D[ct][ft][0]);
+        D[ct][ft][1] = fmaf(cw[ct], zu.y, D[ct][ft][1]);
+        D[ct][ft][2] = fmaf(cw[ct], zu.z, D[ct][ft][2]);
+        D[ct][ft][3] = fmaf(cw[ct], zu.w, D[ct][ft][3]);
+        if (PAIRS) {
+          P[ct][ft][0] = fmaf(cp[ct], zu.x, P[ct][ft][0]);
+          P[ct][ft][1] = fmaf(cp[ct], zu.y, P[ct][ft][1]);
+          P[ct][ft][2] = fmaf(cp[ct], zu.z, P[ct][ft][2]);
+          P[ct][ft][3] = fmaf(cp[ct], zu.w, P[ct][ft][3]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    const int dgx = dgr[ct][x];
     const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dgx));
     const float dxp = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(nx - dgx));
     float tc = 0.f, tcp = 0.f;
@@ -332,44 +381,14 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
     for (int ft = 0; ft < kTiles; ++ft) {
       if (ft >= nt) continue;
       const int f = 16 * (ft0 + ft) + 4 * g;
-      float av[4] = {D[ct][ft][0], D[ct][ft][1], D[ct][ft][2], D[ct][ft][3]};
-      float ap[4] = {0.f, 0.f, 0.f, 0.f};
-      if (PAIRS) {
-        const float4 s4 = *reinterpret_cast<const float4*>(S + x * h + f);
-        ap[0] = s4.x - av[0];
-        ap[1] = s4.y - av[1];
-        ap[2] = s4.z - av[2];
-        ap[3] = s4.w - av[3];
-      }
-      for (int sp = sp0; sp < sp1; ++sp) {
-        const int e = spec_e[sp];
-        const int32_t u = edge_src[e];
-        const bool bit = (mr[e >> 6] >> (e & 63)) & 1;
-        const int du = dg[u];
-        const float4 zu = *reinterpret_cast<const float4*>(Zc + static_cast<int64_t>(u) * h + f);
-        if (bit) {
-          const float cu = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(du));
-          av[0] = fmaf(cu, zu.x, av[0]);
-          av[1] = fmaf(cu, zu.y, av[1]);
-          av[2] = fmaf(cu, zu.z, av[2]);
-          av[3] = fmaf(cu, zu.w, av[3]);
-        } else if (PAIRS) {
-          const int nuu = dst_ptr[u + 1] - dst_ptr[u];
-          const float cu = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(nuu - du));
-          ap[0] = fmaf(cu, zu.x, ap[0]);
-          ap[1] = fmaf(cu, zu.y, ap[1]);
-          ap[2] = fmaf(cu, zu.z, ap[2]);
-          ap[3] = fmaf(cu, zu.w, ap[3]);
-        }
-      }
       const float4 zx = *reinterpret_cast<const float4*>(Zc + x * h + f);
       const float zxv[4] = {zx.x, zx.y, zx.z, zx.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float bb = b1 ? b1[f + i] : 0.f;
         const float ww = W2[static_cast<int64_t>(f + i) * C + cls];
-        tc = fmaf(fmaxf(fmaf(dx, fmaf(dx, zxv[i], av[i]), bb), 0.f), ww, tc);
-        if (PAIRS) tcp = fmaf(fmaxf(fmaf(dxp, fmaf(dxp, zxv[i], ap[i]), bb), 0.f), ww, tcp);
+        tc = fmaf(fmaxf(fmaf(dx, fmaf(dx, zxv[i], D[ct][ft][i]), bb), 0.f), ww, tc);
+        if (PAIRS) tcp = fmaf(fmaxf(fmaf(dxp, fmaf(dxp, zxv[i], P[ct][ft][i]), bb), 0.f), ww, tcp);
       }
     }
     tc += __shfl_xor(tc, 16);
