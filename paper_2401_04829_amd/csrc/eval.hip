@@ -146,9 +146,12 @@ __global__ void k_init(int32_t* ctl, uint64_t* sp_masks, int32_t* sp_rows, int64
   }
 }
 
-// C[m, :] = op(A[row(m), :]) B for m in [m0, m0 + rows), 64x64 tiles, fp32.
-// row(m) = arow ? arow[m] : m; op(a) = relu(a + abias) if abias else a.  The
-// next 16-wide K slice is fetched into registers while the current one is
+typedef float mx4_t __attribute__((ext_vector_type(4)));
+
+// C[m, :] = op(A[row(m), :]) B for m in [m0, m0 + rows), 64x64 tiles, fp32
+// MFMA (16x16x4) with fp32 accumulation.  row(m) = arow ? arow[m] : m;
+// op(a) = relu(a + abias) if abias else a.  The 16-wide K slices are staged
+// in LDS; the next one is fetched into registers while the current one is
 // multiplied.
 __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64_t lda,
                                               const int32_t* __restrict__ arow,
@@ -158,8 +161,9 @@ __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64
                                               int64_t rows, int64_t N, int64_t K,
                                               const int32_t* dyn_count, int64_t dyn_off,
                                               int64_t dyn_cap, int64_t dyn_mult) {
-  __shared__ float As[16][64 + 4];
-  __shared__ float Bs[16][64];
+  // row stride 80: the 4 x 16 operand reads of a wavefront hit 64 distinct banks
+  __shared__ float As[16][80];
+  __shared__ float Bs[16][80];
   if (dyn_count) {
     const int64_t r = rows_in_pass(dyn_count, dyn_off, dyn_cap) * dyn_mult;
     if (r < rows) rows = r;
@@ -168,7 +172,6 @@ __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64
   if (mb >= m0 + rows) return;
   const int64_t nb = static_cast<int64_t>(blockIdx.y) * 64;
   const int tid = threadIdx.x;
-  const int ty = tid / 16, tx = tid % 16;
   const int kk = tid % 16, kb0 = tid / 64, nn = tid % 64;
   const float* arp[4];
   bool aok[4];
@@ -194,7 +197,14 @@ __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64
       rb[i] = (kr < K && nok) ? B[kr * ldb + nb + nn] : 0.f;
     }
   };
-  float acc[4][4] = {};
+  // wavefront w multiplies rows 16 w .. 16 w + 15 of the tile by its 64
+  // columns on fp32 MFMA (16x16x4): lane (r, g) = (lane % 16, lane / 16)
+  // gives A[16 w + r][k + g] and B[k + g][16 nt + r], and holds D rows
+  // 16 w + 4 g .. + 3 of column 16 nt + r
+  const int wave = tid >> 6, lane = tid & 63, r = lane & 15, g = lane >> 4;
+  mx4_t acc[4];
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) acc[nt] = mx4_t{0.f, 0.f, 0.f, 0.f};
   fetch(0);
   for (int64_t k0 = 0; k0 < K; k0 += 16) {
 #pragma unroll
@@ -205,28 +215,22 @@ __global__ void __launch_bounds__(256) k_gemm(const float* __restrict__ A, int64
     __syncthreads();
     if (k0 + 16 < K) fetch(k0 + 16);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      float a[4], b[4];
+    for (int q = 0; q < 16; q += 4) {
+      const float av = As[q + g][16 * wave + r];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a[i] = As[q][ty * 4 + i];
-        b[i] = Bs[q][tx * 4 + i];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int jn = 0; jn < 4; ++jn) acc[i][jn] += a[i] * b[jn];
+      for (int nt = 0; nt < 4; ++nt)
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, Bs[q + g][16 * nt + r], acc[nt], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int64_t m = mb + ty * 4 + i;
+    const int64_t m = mb + 16 * wave + 4 * g + i;
     if (m >= m0 + rows) continue;
 #pragma unroll
-    for (int jn = 0; jn < 4; ++jn) {
-      const int64_t n = nb + tx * 4 + jn;
-      if (n < N) C[m * ldc + n] = acc[i][jn];
+    for (int nt = 0; nt < 4; ++nt) {
+      const int64_t n = nb + 16 * nt + r;
+      if (n < N) C[m * ldc + n] = acc[nt][i];
     }
   }
 }
@@ -748,7 +752,6 @@ size_t rows_mx_lds_bytes(int64_t n_dst, int64_t n1, int64_t M) {
                                              (M + 8) + (n_dst + 1) + 2 * kMxRows);
 }
 
-typedef float mx4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void eval_rows_mx_body(
     const uint64_t* __restrict__ masks, int64_t wpr, const int32_t* __restrict__ rows, int64_t cap,
