@@ -478,6 +478,21 @@ int gnnshap_gat_eval_coalitions(const gnnshap_subgraph* sg, const gnnshap_gat* m
                                 const uint64_t* masks, int64_t k, int64_t words_per_row, float* y,
                                 float* f_empty_full, int32_t* class_out, void* ws, size_t ws_bytes, void* stream);
 
+/* Bytes of device workspace for gnnshap_gat_explain_batch. */
+int gnnshap_gat_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, int64_t n,
+                                        const gnnshap_gat* m, size_t* bytes);
+
+/* gnnshap_explain_batch for the two-layer GAT (App. E): sampling, the
+ * coalition values of gnnshap_gat_eval_coalitions for every target (one
+ * launch sequence per target, in the batch's order) and the least squares,
+ * with the same arguments, outputs, layout, streams and blocking as
+ * gnnshap_explain_batch (m->XW1 replaces X).  Every output equals, bit for
+ * bit, what the single-target calls give. */
+int gnnshap_gat_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                              const gnnshap_class* classes, int64_t n, const gnnshap_gat* m, int32_t target_class,
+                              uint64_t* masks, float* weights, float* y, float* f_empty_full, int32_t* class_out,
+                              float* phi, int32_t* info, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Diagnostics: HIP-event timing of one kernel.                             */
 /* ------------------------------------------------------------------------ */

@@ -92,6 +92,11 @@ _SIGNATURES = {
     "gnnshap_explain_batch": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), _P(gnnshap_class),
                                              c_i64, _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                              c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
+    "gnnshap_gat_explain_batch_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), c_i64,
+                                                           _P(gnnshap_gat), _P(ctypes.c_size_t)]),
+    "gnnshap_gat_explain_batch": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_sample_plan), _P(gnnshap_class),
+                                                 c_i64, _P(gnnshap_gat), c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                                 c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp]),
     "gnnshap_solve_info": (ctypes.c_int, [_P(gnnshap_sample_plan), _P(c_i32)]),
     "gnnshap_fidelity_workspace": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), _P(ctypes.c_size_t)]),
     "gnnshap_fidelity": (ctypes.c_int, [_P(gnnshap_subgraph), _P(gnnshap_gcn), c_vp, c_i32, c_vp, c_dbl, c_i64,
@@ -312,6 +317,25 @@ def gnnshap_explain_batch(sgs, plans, classes, model, X_ptr, target_class, masks
                                       ws_bytes, stream)
     if st not in (OK, ECAPACITY):
         check(st, "explain_batch")
+    return st
+
+
+def gnnshap_gat_explain_batch_workspace(sgs, plans, model):
+    b = ctypes.c_size_t()
+    check(load().gnnshap_gat_explain_batch_workspace(sgs, plans, len(sgs), ctypes.byref(model), ctypes.byref(b)),
+          "gat_explain_batch_workspace")
+    return b.value
+
+
+def gnnshap_gat_explain_batch(sgs, plans, classes, model, target_class, masks_ptr, weights_ptr, y_ptr, fef_ptr,
+                              cls_ptr, phi_ptr, info_ptr, ws_ptr, ws_bytes, stream):
+    """As gnnshap_explain_batch, for the GAT: OK, or ECAPACITY when the
+    workspace is too small (nothing was queued then); raises otherwise."""
+    st = load().gnnshap_gat_explain_batch(sgs, plans, classes, len(sgs), ctypes.byref(model), target_class,
+                                          masks_ptr, weights_ptr, y_ptr, fef_ptr, cls_ptr, phi_ptr, info_ptr, ws_ptr,
+                                          ws_bytes, stream)
+    if st not in (OK, ECAPACITY):
+        check(st, "gat_explain_batch")
     return st
 
 

@@ -224,9 +224,14 @@ struct Layout {
   std::vector<size_t> eval_bytes, solve_bytes;
 };
 
-int make_layout(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, int64_t n, const gnnshap_gcn* m,
-                Layout* L) {
-  if (!sgs || !plans || !m || n < 1) return gnnshap::fail(GNNSHAP_EINVAL, "null argument or n < 1");
+// The model of a batch: a GCN (gcn) or a two-layer GAT (gat), exactly one set.
+struct Model {
+  const gnnshap_gcn* gcn = nullptr;
+  const gnnshap_gat* gat = nullptr;
+};
+
+int make_layout(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, int64_t n, Model m, Layout* L) {
+  if (!sgs || !plans || !(m.gcn || m.gat) || n < 1) return gnnshap::fail(GNNSHAP_EINVAL, "null argument or n < 1");
   if (n > 65535) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "at most 65535 targets per batch");
   L->n = n;
   L->mask_off.resize(n + 1);
@@ -241,7 +246,9 @@ int make_layout(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, i
     if (p.num_players != sgs[t].num_edges)
       return gnnshap::fail(GNNSHAP_EINVAL, "plan %lld is not for subgraph %lld's players", (long long)t, (long long)t);
     size_t eb = 0, sb = 0;
-    if (int st = gnnshap_eval_workspace(&sgs[t], m, p.num_rows, &eb)) return st;
+    if (int st = m.gcn ? gnnshap_eval_workspace(&sgs[t], m.gcn, p.num_rows, &eb)
+                       : gnnshap_gat_eval_workspace(&sgs[t], m.gat, p.num_rows, &eb))
+      return st;
     if (int st = gnnshap_solve_workspace(&p, &sb)) return st;
     L->eval_bytes[t] = eb;
     L->solve_bytes[t] = sb;
@@ -293,27 +300,29 @@ void split_groups(const gnnshap_sample_plan* plans, int64_t n, std::vector<int64
 
 }  // namespace
 
-extern "C" int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
-                                               int64_t n, const gnnshap_gcn* model, size_t* bytes) {
+namespace {
+
+int batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, int64_t n, Model m,
+                    size_t* bytes) {
   gnnshap::clear_error();
   if (!bytes) return gnnshap::fail(GNNSHAP_EINVAL, "bytes is NULL");
   Layout L;
-  if (int st = make_layout(sgs, plans, n, model, &L)) return st;
+  if (int st = make_layout(sgs, plans, n, m, &L)) return st;
   gnnshap::Carver c(nullptr);
   carve(c, L);
   *bytes = c.bytes();
   return GNNSHAP_OK;
 }
 
-extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
-                                     const gnnshap_class* classes, int64_t n, const gnnshap_gcn* model,
-                                     const float* X, int32_t target_class, uint64_t* masks, float* weights,
-                                     float* y, float* f_empty_full, int32_t* class_out, float* phi, int32_t* info,
-                                     void* ws, size_t ws_bytes, void* stream) {
+int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans, const gnnshap_class* classes,
+                       int64_t n, Model mdl, const float* X, int32_t target_class, uint64_t* masks, float* weights,
+                       float* y, float* f_empty_full, int32_t* class_out, float* phi, int32_t* info, void* ws,
+                       size_t ws_bytes, void* stream) {
   GS_TRY_BEGIN
   gnnshap::clear_error();
   Layout L;
-  if (int st = make_layout(sgs, plans, n, model, &L)) return st;
+  if (int st = make_layout(sgs, plans, n, mdl, &L)) return st;
+  const gnnshap_gcn* model = mdl.gcn;
   if (!classes || !masks || !weights || !y || !f_empty_full || !phi || !info || !ws)
     return gnnshap::fail(GNNSHAP_EINVAL, "null argument");
   gnnshap::Carver need(nullptr);
@@ -390,7 +399,7 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
       G.max_k = std::max(G.max_k, p.num_rows);
     }
     // 2. coalition-value jobs (two-layer models with X W_1 given)
-    G.eval_all = model->num_layers == 2 && model->XW1;
+    G.eval_all = model && model->num_layers == 2 && model->XW1;
     for (int64_t j = G.begin; j < G.end && G.eval_all; ++j)
       G.eval_all = gnnshap::eval_batchable(&sgs[order[j]], model, plans[order[j]].num_rows);
     if (G.eval_all) {
@@ -522,11 +531,18 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
           for (int64_t j = G.begin; j < G.end; ++j) {
             const int64_t t = order[j];
             const gnnshap_sample_plan& p = plans[t];
-            if (int st = gnnshap::eval_coalitions_impl(&sgs[t], model, X, target_class, masks + L.mask_off[t],
-                                                       p.num_rows, p.words_per_row, y + L.row_off[t],
-                                                       f_empty_full + 2 * t, class_out ? class_out + t : nullptr,
-                                                       b.eval_slice[t], L.eval_bytes[t], gs[gi], true))
+            if (model) {
+              if (int st = gnnshap::eval_coalitions_impl(&sgs[t], model, X, target_class, masks + L.mask_off[t],
+                                                         p.num_rows, p.words_per_row, y + L.row_off[t],
+                                                         f_empty_full + 2 * t, class_out ? class_out + t : nullptr,
+                                                         b.eval_slice[t], L.eval_bytes[t], gs[gi], true))
+                return st;
+            } else if (int st = gnnshap_gat_eval_coalitions(&sgs[t], mdl.gat, target_class, masks + L.mask_off[t],
+                                                            p.num_rows, p.words_per_row, y + L.row_off[t],
+                                                            f_empty_full + 2 * t, class_out ? class_out + t : nullptr,
+                                                            b.eval_slice[t], L.eval_bytes[t], gs[gi])) {
               return st;
+            }
             GS_HIP(hipEventRecord(ev_pool[j], gs[gi]));
             evaluated[t] = ev_pool[j];
           }
@@ -677,4 +693,46 @@ extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_
   if (int st = issue(s)) return st;
   return GNNSHAP_OK;
   GS_TRY_END
+}
+
+}  // namespace
+
+extern "C" int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                               int64_t n, const gnnshap_gcn* model, size_t* bytes) {
+  Model m;
+  m.gcn = model;
+  if (!model) return gnnshap::fail(GNNSHAP_EINVAL, "model is NULL");
+  return batch_workspace(sgs, plans, n, m, bytes);
+}
+
+extern "C" int gnnshap_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                     const gnnshap_class* classes, int64_t n, const gnnshap_gcn* model,
+                                     const float* X, int32_t target_class, uint64_t* masks, float* weights,
+                                     float* y, float* f_empty_full, int32_t* class_out, float* phi, int32_t* info,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  Model m;
+  m.gcn = model;
+  if (!model) return gnnshap::fail(GNNSHAP_EINVAL, "model is NULL");
+  return explain_batch_impl(sgs, plans, classes, n, m, X, target_class, masks, weights, y, f_empty_full, class_out,
+                            phi, info, ws, ws_bytes, stream);
+}
+
+extern "C" int gnnshap_gat_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                                   int64_t n, const gnnshap_gat* model, size_t* bytes) {
+  Model m;
+  m.gat = model;
+  if (!model) return gnnshap::fail(GNNSHAP_EINVAL, "model is NULL");
+  return batch_workspace(sgs, plans, n, m, bytes);
+}
+
+extern "C" int gnnshap_gat_explain_batch(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* plans,
+                                         const gnnshap_class* classes, int64_t n, const gnnshap_gat* model,
+                                         int32_t target_class, uint64_t* masks, float* weights, float* y,
+                                         float* f_empty_full, int32_t* class_out, float* phi, int32_t* info,
+                                         void* ws, size_t ws_bytes, void* stream) {
+  Model m;
+  m.gat = model;
+  if (!model) return gnnshap::fail(GNNSHAP_EINVAL, "model is NULL");
+  return explain_batch_impl(sgs, plans, classes, n, m, nullptr, target_class, masks, weights, y, f_empty_full,
+                            class_out, phi, info, ws, ws_bytes, stream);
 }

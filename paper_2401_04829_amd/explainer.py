@@ -373,14 +373,19 @@ class Explainer:
         ws = self.ws_batch.t
         st = L.ECAPACITY
         if ws is not None:
-            st = L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *ptrs,
-                                         _vp(ws), ws.numel(), self.stream())
+            st = self._batch_call(sgs, plans, cl, target_class, ptrs, ws)
         if st == L.ECAPACITY:
-            ws = self.ws_batch.get(L.gnnshap_explain_batch_workspace(sgs, plans, self.model))
-            st = L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *ptrs,
-                                         _vp(ws), ws.numel(), self.stream())
-            L.check(st, "explain_batch")
+            ws = self.ws_batch.get(self._batch_workspace(sgs, plans))
+            L.check(self._batch_call(sgs, plans, cl, target_class, ptrs, ws), "explain_batch")
         return out
+
+    def _batch_workspace(self, sgs, plans):
+        return L.gnnshap_explain_batch_workspace(sgs, plans, self.model)
+
+    def _batch_call(self, sgs, plans, cl, target_class, ptrs, ws):
+        """gnnshap_explain_batch on the current stream (OK or ECAPACITY)."""
+        return L.gnnshap_explain_batch(sgs, plans, cl, self.model, _vp(self.X), int(target_class), *ptrs,
+                                       _vp(ws), ws.numel(), self.stream())
 
 
 class BatchSubgraphs:
@@ -483,8 +488,8 @@ class GatExplainer(Explainer):
     """Alg. 1 for a two-layer GAT (App. E): the same extraction (2 hops),
     plan, sampler and least squares as Explainer, with the coalition values
     of gnnshap_gat_eval_coalitions.  `params` as workloads.glorot_gat makes
-    them (W1, att_src1, att_dst1, b1, W2, att_src2, att_dst2, b2).  Single
-    targets only (explain, explain_many)."""
+    them (W1, att_src1, att_dst1, b1, W2, att_src2, att_dst2, b2).  Batches
+    go through gnnshap_gat_explain_batch (explain_batch, explain_batches)."""
 
     def __init__(self, indptr, indices, X, params, device="cuda", negative_slope=0.2):
         heads, head_dim = (int(v) for v in params["att_src1"].shape)
@@ -509,11 +514,15 @@ class GatExplainer(Explainer):
         L.gnnshap_gat_eval_coalitions(sub.sg, self.gat, int(target_class), _vp(masks), k, wpr, _vp(y), _vp(fef),
                                       _vp(cls), _vp(ws), ws.numel(), s)
 
-    def explain_batch(self, *args, **kwargs):
-        raise NotImplementedError("the batched entry points evaluate GCNs; explain GAT targets one at a time")
+    def _batch_workspace(self, sgs, plans):
+        return L.gnnshap_gat_explain_batch_workspace(sgs, plans, self.gat)
 
-    def explain_batches(self, *args, **kwargs):
-        raise NotImplementedError("the batched entry points evaluate GCNs; explain GAT targets one at a time")
+    def _batch_call(self, sgs, plans, cl, target_class, ptrs, ws):
+        """gnnshap_gat_explain_batch on the current stream (OK or ECAPACITY)."""
+        if not self.gat.XW1:
+            raise RuntimeError("GatExplainer.prepare() must run before explaining (X W_1 of every node)")
+        return L.gnnshap_gat_explain_batch(sgs, plans, cl, self.gat, int(target_class), *ptrs, _vp(ws), ws.numel(),
+                                           self.stream())
 
     def fidelity(self, *args, **kwargs):
         raise NotImplementedError("gnnshap_fidelity evaluates GCNs")

@@ -126,3 +126,39 @@ def test_gat_exhaustive_equals_exact_shapley(dev):
         if done == 2:
             break
     assert done > 0
+
+
+def test_gat_batch_equals_single(dev):
+    """gnnshap_gat_explain_batch (App. E through the batched entry points):
+    for 12 Cora-shaped targets, with targets of a different fixed class as
+    well, every output (masks, weights, coalition values, f(empty), f(E_c),
+    class, phi, info) equals the single-target calls' bit for bit, and the
+    batch's phi of the first target is within the phi bar of the oracle's
+    least squares on the oracle's GAT values."""
+    cfg, P = _cora_gat()
+    ex = GatExplainer(cfg["indptr"], cfg["indices"], cfg["X"], P)
+    targets = [int(v) for v in cfg["targets"][:12]]
+    for target_class in (-1, 2):
+        _say("gat batch", len(targets), "targets, class", target_class)
+        batch = ex.explain_batch(targets, 2000, 7, target_class=target_class)
+        torch.cuda.synchronize()
+        for i, v in enumerate(targets):
+            b = batch[i]
+            s = ex.explain(v, 2000, 7, target_class=target_class)
+            torch.cuda.synchronize()
+            for name in ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info"):
+                assert torch.equal(getattr(b, name), getattr(s, name)), (v, target_class, name)
+    b = ex.explain_batch(targets[:1], 2000, 7)[0]
+    torch.cuda.synchronize()
+    sub = subgraph.extract(cfg["indptr"], cfg["indices"], targets[0], 2)
+    M = sub["num_edges"]
+    game = G.GatGame(sub, cfg["X"], P)
+    game.cls = int(np.argmax(game.logits(np.ones(M, bool))))
+    assert int(b.cls.item()) == game.cls
+    pl = sampler.plan(M, 2000)
+    m, w = sampler.sample(pl, 7, targets[0])
+    np.testing.assert_array_equal(masks_np(b.masks), sampler.pack(m))
+    f0, f1 = game(np.zeros(M, bool)), game(np.ones(M, bool))
+    phi_ref = wls.kernel_shap(m, w, game.values(m), f0, f1)
+    phi = b.phi.cpu().numpy().astype(np.float64)
+    assert np.abs(phi - phi_ref).max() <= 1e-3 * np.abs(phi_ref).max()
