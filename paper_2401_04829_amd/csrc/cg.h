@@ -40,6 +40,7 @@ struct CgWs {
   int32_t* csc_row;   // nnz
   double* qs;         // M: R_s^T u
   int64_t* sitem;     // nsi: pass-A work items over the sparse rows, (first row << 8) | log2(lanes per row)
+  int32_t* segcnt;    // 8 x max(rs, M): per-segment list lengths while the lists are built
 };
 
 // Launch shape of the iterative solver for M players and kr random

@@ -54,14 +54,18 @@
 #include <vector>
 
 #include "cg.h"
+#include "nibble.h"
 
 namespace {
+
+using gnnshap::build_tables;
+using gnnshap::kTabWords;
+using gnnshap::nibble_dots;
 
 constexpr double kTol = 1e-8;
 constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
 constexpr int kWaves = 8;            // waves per workgroup of both passes
-constexpr int64_t kTabWords = 16;    // nibble tables per workgroup: 16 words (32 KiB of LDS)
 constexpr int64_t kSparseDiv = 128;   // sparse rows: coalition size at most M / kSparseDiv
 
 struct Args {
@@ -138,69 +142,6 @@ __device__ __forceinline__ double wave_fixed_sum(const double* __restrict__ a, i
   double s = 0.0;
   for (int64_t i = threadIdx.x & 63; i < n; i += 64) s += a[i * stride];
   return wave_sum_d(s);
-}
-
-// Nibble tables: for 64 consecutive entries v[0..63] of a vector, table k
-// (k = 0..15) holds at index n the sum of v[4k + i] over the set bits i of n,
-// so that the sum of v over the set bits of a 64-bit word is the sum of 16
-// table reads.  One table is 16 fp64 entries, 128 bytes: its entries fall in
-// distinct LDS banks, so 64 lanes reading one table never conflict.  The
-// tables of a workgroup are one static LDS array, word w's 16 tables at
-// byte 2048 w.
-//
-// ntab tables of v (4 entries each) into tab, consecutive threads on
-// consecutive entries, so the writes of a wavefront cover 512 contiguous
-// bytes (no two lanes in one bank).  Entry n of table q is
-// ((v[4q] [n & 1] + v[4q + 1] [n & 2]) + v[4q + 2] [n & 4]) + v[4q + 3] [n & 8],
-// an absent term adding 0.0 (exact).
-__device__ __forceinline__ void build_tables(const double* __restrict__ v, int64_t ntab, double* tab) {
-  for (int64_t e = threadIdx.x; e < ntab * 16; e += blockDim.x) {
-    const double* v4 = v + (e >> 4) * 4;
-    const int n = static_cast<int>(e & 15);
-    const double a0 = (n & 1) ? v4[0] : 0.0;
-    const double a1 = (n & 2) ? v4[1] : 0.0;
-    const double a2 = (n & 4) ? v4[2] : 0.0;
-    const double a3 = (n & 8) ? v4[3] : 0.0;
-    tab[e] = ((a0 + a1) + a2) + a3;
-  }
-}
-
-// acc[0..3] += sum over the set bits b of word of v[b], from the word's 16
-// tables at byte 2048 W of `tabs` (W a constant, so that the table offsets
-// are immediates of the LDS reads).  Each 32-bit half is masked into two
-// words whose bytes hold 8 x a nibble (the byte offset of the entry in its
-// table): one extract per nibble gives the LDS address.  Table t adds into
-// acc[t & 3], tables in ascending order.
-template <int W>
-__device__ __forceinline__ void nibble_dot(uint64_t word, const char* tabs, double (&acc)[4]) {
-  constexpr uint32_t kM = 0x78787878u;
-  const uint32_t lo = static_cast<uint32_t>(word), hi = static_cast<uint32_t>(word >> 32);
-  const uint32_t q[4] = {(lo << 3) & kM, (lo >> 1) & kM, (hi << 3) & kM, (hi >> 1) & kM};
-#pragma unroll
-  for (int half = 0; half < 2; ++half)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int odd = 0; odd < 2; ++odd) {
-        const int t = 8 * half + 2 * j + odd;
-        const uint32_t off = __builtin_amdgcn_ubfe(q[2 * half + odd], 8 * j, 8);
-        acc[t & 3] += *reinterpret_cast<const double*>(tabs + (W * 2048 + t * 128) + off);
-      }
-}
-
-// acc[0..3] += the products of n <= kTabWords words (word w at src[w * stride])
-// with the tables of consecutive 64-entry groups; the next word's load is
-// issued before the current word's table reads.
-template <int W>
-__device__ __forceinline__ void nibble_dots(const uint64_t* __restrict__ src, int64_t stride, int n, uint64_t next,
-                                            const char* tabs, double (&acc)[4]) {
-  if constexpr (W < kTabWords) {
-    if (W >= n) return;
-    const uint64_t word = next;
-    if (W + 1 < n) next = src[(W + 1) * stride];
-    nibble_dot<W>(word, tabs, acc);
-    nibble_dots<W + 1>(src, stride, n, next, tabs, acc);
-  }
 }
 
 // r = dv - mean(dv) (zero beyond M), x = p = s = 0, partial gamma_0; u zero
@@ -533,19 +474,42 @@ __global__ void __launch_bounds__(1024) k_cg_csr_ptr(const int32_t* __restrict__
   }
 }
 
-// Row-major lists: wavefront g reads the words of its 64 rows from the
-// row-blocked copy (lane = row) and writes each set bit's player in order.
-__global__ void __launch_bounds__(64) k_cg_csr_fill(const uint64_t* __restrict__ blocked, int64_t wpr, int64_t rs,
-                                                    const int64_t* __restrict__ ptr, int64_t nnz,
-                                                    int32_t* __restrict__ idx) {
+// The lists are built in kSeg segments at once: of the player words for the
+// row lists, of the row blocks for the player lists.  A count pass gives each
+// (row or player, segment) its number of entries, so the fill pass of a
+// segment starts at the list's start plus the counts of the segments before
+// it; every list comes out in ascending order.
+constexpr int kSeg = 8;
+
+// Row-major lists, counts: wavefront (g, s) reads the words of segment s of its
+// 64 rows from the row-blocked copy (lane = row): cnt[s][b].
+__global__ void __launch_bounds__(64) k_cg_csr_count(const uint64_t* __restrict__ blocked, int64_t wpr, int64_t rs,
+                                                     int32_t* __restrict__ cnt) {
   const int64_t g = blockIdx.x;
-  const int lane = threadIdx.x;
-  const int64_t b = g * 64 + lane;
+  const int sg = blockIdx.y;
+  const int64_t b = g * 64 + threadIdx.x;
+  if (b >= rs) return;
+  const int64_t w0 = wpr * sg / kSeg, w1 = wpr * (sg + 1) / kSeg;
+  const uint64_t* src = blocked + g * wpr * 64 + threadIdx.x;
+  int c = 0;
+  for (int64_t w = w0; w < w1; ++w) c += __popcll(src[w * 64]);
+  cnt[sg * rs + b] = c;
+}
+
+// Row-major lists, fill: the players of segment s of row b in order.
+__global__ void __launch_bounds__(64) k_cg_csr_fill(const uint64_t* __restrict__ blocked, int64_t wpr, int64_t rs,
+                                                    const int64_t* __restrict__ ptr, const int32_t* __restrict__ cnt,
+                                                    int64_t nnz, int32_t* __restrict__ idx) {
+  const int64_t g = blockIdx.x;
+  const int sg = blockIdx.y;
+  const int64_t b = g * 64 + threadIdx.x;
   if (b >= rs) return;
   int64_t pos = ptr[b];
+  for (int q = 0; q < sg; ++q) pos += cnt[q * rs + b];
   const int64_t end = ptr[b + 1] < nnz ? ptr[b + 1] : nnz;
-  const uint64_t* src = blocked + g * wpr * 64 + lane;
-  for (int64_t w = 0; w < wpr; ++w) {
+  const int64_t w0 = wpr * sg / kSeg, w1 = wpr * (sg + 1) / kSeg;
+  const uint64_t* src = blocked + g * wpr * 64 + threadIdx.x;
+  for (int64_t w = w0; w < w1; ++w) {
     uint64_t word = src[w * 64];
     while (word && pos < end) {
       idx[pos++] = static_cast<int32_t>(w * 64 + __builtin_ctzll(word));
@@ -554,30 +518,70 @@ __global__ void __launch_bounds__(64) k_cg_csr_fill(const uint64_t* __restrict__
   }
 }
 
-// Player-major lists: cnt[j] = sparse rows holding player j (from the
-// bit-transposed rows T[rb, j], rb < nrb_s).
+// Player-major lists, counts: cnt[s][j] = the sparse rows of segment s (row
+// blocks nrb_s s / kSeg .. of the bit-transposed rows T[rb, j]) holding j.
 __global__ void __launch_bounds__(256) k_cg_csc_count(const uint64_t* __restrict__ T, int64_t M, int64_t nrb_s,
-                                                      int64_t* __restrict__ cnt) {
+                                                      int32_t* __restrict__ cnt) {
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int sg = blockIdx.y;
   if (j >= M) return;
-  int64_t c = 0;
-  for (int64_t rb = 0; rb < nrb_s; ++rb) c += __popcll(T[rb * M + j]);
-  cnt[j] = c;
+  const int64_t r0 = nrb_s * sg / kSeg, r1 = nrb_s * (sg + 1) / kSeg;
+  int c = 0;
+  for (int64_t rb = r0; rb < r1; ++rb) c += __popcll(T[rb * M + j]);
+  cnt[sg * M + j] = c;
 }
 
-__global__ void __launch_bounds__(1024) k_cg_csc_scan(const int64_t* __restrict__ cnt, int64_t M,
+// ptr[j] = total of player j's segment counts (fixed order), then the
+// exclusive prefix sums over j in place (ptr[M] = the total).
+__global__ void __launch_bounds__(256) k_cg_csc_total(const int32_t* __restrict__ cnt, int64_t M,
                                                       int64_t* __restrict__ ptr) {
-  block_scan_i64(cnt, M, ptr);
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= M) return;
+  int64_t v = 0;
+#pragma unroll
+  for (int q = 0; q < kSeg; ++q) v += cnt[q * M + j];
+  ptr[j] = v;
+}
+
+__global__ void __launch_bounds__(1024) k_cg_csc_scan(int64_t M, int64_t* ptr) {
+  // in place: each thread reads each of its entries before writing it
+  __shared__ int64_t part[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (M + 1023) / 1024;
+  const int64_t i0 = t * per, i1 = i0 + per < M ? i0 + per : M;
+  int64_t s = 0;
+  for (int64_t i = i0; i < i1; ++i) s += ptr[i];
+  part[t] = s;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int64_t x = part[i];
+      part[i] = run;
+      run += x;
+    }
+    ptr[M] = run;
+  }
+  __syncthreads();
+  int64_t run = part[t];
+  for (int64_t i = i0; i < i1; ++i) {
+    const int64_t x = ptr[i];
+    ptr[i] = run;
+    run += x;
+  }
 }
 
 __global__ void __launch_bounds__(256) k_cg_csc_fill(const uint64_t* __restrict__ T, int64_t M, int64_t nrb_s,
-                                                     const int64_t* __restrict__ ptr, int64_t nnz,
-                                                     int32_t* __restrict__ rows) {
+                                                     const int64_t* __restrict__ ptr, const int32_t* __restrict__ cnt,
+                                                     int64_t nnz, int32_t* __restrict__ rows) {
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int sg = blockIdx.y;
   if (j >= M) return;
   int64_t pos = ptr[j];
+  for (int q = 0; q < sg; ++q) pos += cnt[q * M + j];
   const int64_t end = ptr[j + 1] < nnz ? ptr[j + 1] : nnz;
-  for (int64_t rb = 0; rb < nrb_s; ++rb) {
+  const int64_t r0 = nrb_s * sg / kSeg, r1 = nrb_s * (sg + 1) / kSeg;
+  for (int64_t rb = r0; rb < r1; ++rb) {
     uint64_t word = T[rb * M + j];
     while (word && pos < end) {
       rows[pos++] = static_cast<int32_t>(rb * 64 + __builtin_ctzll(word));
@@ -820,6 +824,7 @@ gnnshap::CgWs gnnshap::cg_carve(Carver& c, const CgShape& sh) {
   w.csc_row = c.take<int32_t>(sh.nnz > 0 ? sh.nnz : 1);
   w.qs = c.take<double>(sh.M);
   w.sitem = c.take<int64_t>(sh.nsi > 0 ? sh.nsi : 1);
+  w.segcnt = c.take<int32_t>(kSeg * std::max<int64_t>(std::max<int64_t>(sh.rs, sh.M), 1));
   return w;
 }
 
@@ -934,19 +939,21 @@ int gnnshap::CgGroup::add(const CgProblem& pr, const CgShape& sh, const CgWs& w)
     // the sparse rows' lists (row sizes from k_cg_init); qs serves as the
     // count scratch here, it is written before the iterations read it
     const int64_t nrb_s = sh.rs / 64;
+    const dim3 gr(static_cast<unsigned>(nrb_s), kSeg), gp(static_cast<unsigned>(ceil_div(sh.M, 256)), kSeg);
     GS_TIMED("k_cg_sparse_build", s);
     k_cg_csr_ptr<<<1, 1024, 0, s>>>(w.sz, sh.rs, w.csr_ptr, w.sitem);
     GS_LAUNCHED();
-    k_cg_csr_fill<<<static_cast<unsigned>(nrb_s), 64, 0, s>>>(pr.blocked, sh.wpr, sh.rs, w.csr_ptr, sh.nnz,
-                                                             w.csr_idx);
+    k_cg_csr_count<<<gr, 64, 0, s>>>(pr.blocked, sh.wpr, sh.rs, w.segcnt);
     GS_LAUNCHED();
-    int64_t* cnt = reinterpret_cast<int64_t*>(w.qs);
-    k_cg_csc_count<<<static_cast<unsigned>(ceil_div(sh.M, 256)), 256, 0, s>>>(pr.T, sh.M, nrb_s, cnt);
+    k_cg_csr_fill<<<gr, 64, 0, s>>>(pr.blocked, sh.wpr, sh.rs, w.csr_ptr, w.segcnt, sh.nnz, w.csr_idx);
     GS_LAUNCHED();
-    k_cg_csc_scan<<<1, 1024, 0, s>>>(cnt, sh.M, w.csc_ptr);
+    k_cg_csc_count<<<gp, 256, 0, s>>>(pr.T, sh.M, nrb_s, w.segcnt);
     GS_LAUNCHED();
-    k_cg_csc_fill<<<static_cast<unsigned>(ceil_div(sh.M, 256)), 256, 0, s>>>(pr.T, sh.M, nrb_s, w.csc_ptr, sh.nnz,
-                                                                            w.csc_row);
+    k_cg_csc_total<<<static_cast<unsigned>(ceil_div(sh.M, 256)), 256, 0, s>>>(w.segcnt, sh.M, w.csc_ptr);
+    GS_LAUNCHED();
+    k_cg_csc_scan<<<1, 1024, 0, s>>>(sh.M, w.csc_ptr);
+    GS_LAUNCHED();
+    k_cg_csc_fill<<<gp, 256, 0, s>>>(pr.T, sh.M, nrb_s, w.csc_ptr, w.segcnt, sh.nnz, w.csc_row);
     GS_LAUNCHED();
   }
   S.mem.push_back(m);

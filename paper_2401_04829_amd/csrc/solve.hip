@@ -28,6 +28,7 @@
 
 #include "batch.h"
 #include "cg.h"
+#include "nibble.h"
 #include "common.h"
 
 namespace {
@@ -99,6 +100,17 @@ constexpr int kTileClasses = 256;                         // classes of a system
 
 int64_t tile_chunks(int64_t half) { return gnnshap::ceil_div(half, kTileRows); }
 
+// Iterative path: row chunks of the right-hand side's enumerated rows (from
+// the row-major masks) and of its random rows (kTabWords row blocks of the
+// bit-transposed rows each).
+int64_t rhs_enum_chunks(const gnnshap_sample_plan* p) {
+  return p->random_begin > 0 ? n_chunks(p->random_begin, p->words_per_row) : 0;
+}
+int64_t rhs_rand_chunks(const gnnshap_sample_plan* p) {
+  const int64_t kr = p->num_rows / 2 - p->random_begin;
+  return gnnshap::ceil_div(gnnshap::ceil_div(kr, 64), gnnshap::kTabWords);
+}
+
 Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p, const gnnshap_class* classes = nullptr) {
   Ws w;
   const int64_t M = p->num_players;
@@ -112,7 +124,7 @@ Ws carve(gnnshap::Carver& c, const gnnshap_sample_plan* p, const gnnshap_class* 
     w.usum = nullptr;
     w.scal = nullptr;
     w.dz = c.take<double>(half);
-    w.part = c.take<double>(n_chunks(half, p->words_per_row) * M);
+    w.part = c.take<double>(std::max<int64_t>(rhs_enum_chunks(p) + rhs_rand_chunks(p), 1) * M);
     w.dv = c.take<double>(M);
     w.bsum = c.take<double>(gnnshap::ceil_div(M, 256));
     w.rhs = w.x = w.Winv = w.Wd = nullptr;
@@ -179,12 +191,19 @@ __global__ void __launch_bounds__(64) k_transpose(const uint64_t* __restrict__ m
 // T as above, and the same words in row blocks: B[(rb * wpr + w) * 64 + b] =
 // word w of row rb * 64 + b (zero beyond nrows), so that a wave reading word
 // w of 64 consecutive rows reads 512 contiguous bytes.
-__global__ void __launch_bounds__(64) k_transpose_blocked(const uint64_t* __restrict__ masks, int64_t wpr,
-                                                          int64_t row0, int64_t nrows, int64_t M,
-                                                          uint64_t* __restrict__ T, uint64_t* __restrict__ B) {
-  const int64_t rb = blockIdx.x, w = blockIdx.y;
-  const int64_t r = rb * 64 + threadIdx.x;
-  B[(rb * wpr + w) * 64 + threadIdx.x] = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
+// Workgroup (rb, y): wavefront w' handles word column w = 8 y + w' of row
+// block rb, so the eight wavefronts read neighbouring words of the same 64
+// rows (whole cache lines per workgroup) and write 8 x 512 contiguous bytes
+// of each copy.
+__global__ void __launch_bounds__(512) k_transpose_blocked(const uint64_t* __restrict__ masks, int64_t wpr,
+                                                           int64_t row0, int64_t nrows, int64_t M,
+                                                           uint64_t* __restrict__ T, uint64_t* __restrict__ B) {
+  const int64_t rb = blockIdx.x;
+  const int64_t w = static_cast<int64_t>(blockIdx.y) * 8 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (w >= wpr) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = rb * 64 + lane;
+  B[(rb * wpr + w) * 64 + lane] = r < nrows ? masks[(row0 + r) * wpr + w] : 0;
   transpose_body(masks, wpr, row0, nrows, M, T, rb, w);
 }
 
@@ -520,6 +539,34 @@ __global__ void __launch_bounds__(256) k_rhs_part(const uint64_t* __restrict__ m
 }
 
 // dv[j] = sum over chunks of part[., j] (fixed order); bsum[block] = sum of its dv.
+// The random rows' part of the right-hand side from their bit-transposed
+// copy T (row block rb, player j: bit b = random row 64 rb + b):
+// part[c][j] = sum over the kTabWords row blocks of chunk c of dzr[64 rb + b]
+// over the set bits of T[rb][j], by nibble tables of dzr in LDS (entries from
+// kr on are 0).  Workgroup c nxb + x; wavefront w takes player word 8 x + w,
+// lane = player, so each word load is 512 contiguous bytes.
+__global__ void __launch_bounds__(512) k_rhs_rand(const uint64_t* __restrict__ T, int64_t M, int64_t wpr,
+                                                  int64_t kr, int64_t nrb, const double* __restrict__ dzr,
+                                                  double* __restrict__ part, int64_t nxb) {
+  __shared__ double tab[gnnshap::kTabWords * 256];
+  const int64_t c = blockIdx.x / nxb;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t gw = (static_cast<int64_t>(blockIdx.x) % nxb) * 8 + wave;
+  const int64_t b0 = c * gnnshap::kTabWords;
+  const int64_t b1 = b0 + gnnshap::kTabWords < nrb ? b0 + gnnshap::kTabWords : nrb;
+  const int64_t nb = b1 - b0;
+  gnnshap::build_tables_bounded(dzr + b0 * 64, kr - b0 * 64, nb * 16, tab);
+  __syncthreads();
+  if (gw >= wpr) return;
+  const int64_t j = gw * 64 + lane;
+  const bool valid = j < M;
+  const uint64_t* col = T + b0 * M + (valid ? j : 0);
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  gnnshap::nibble_dots<0>(col, M, static_cast<int>(nb), col[0], reinterpret_cast<const char*>(tab), acc);
+  if (valid) part[c * M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
 __global__ void __launch_bounds__(256) k_rhs_reduce(const double* __restrict__ part, int64_t nch, int64_t M,
                                                     double* __restrict__ dv, double* __restrict__ bsum) {
   __shared__ double red[256];
@@ -1962,23 +2009,35 @@ int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_clas
     // conjugate gradients straight from the bits
     if (has_random) {
       GS_TIMED("k_transpose", s);
-      k_transpose_blocked<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(kr, 64)), static_cast<unsigned>(wpr)), 64, 0,
-                            s>>>(masks, wpr, rb0, kr, M, w.T, w.cg.blocked);
+      k_transpose_blocked<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(kr, 64)),
+                                 static_cast<unsigned>(gnnshap::ceil_div(wpr, 8))),
+                            512, 0, s>>>(masks, wpr, rb0, kr, M, w.T, w.cg.blocked);
     }
     GS_LAUNCHED();
-    const int64_t nch = n_chunks(half, wpr);
-    const int64_t rpc = gnnshap::ceil_div(half, nch);
+    // the right-hand side: the enumerated rows from the row-major masks, the
+    // random rows from their bit-transposed copy, then the chunks in order
+    const int64_t nch_e = rhs_enum_chunks(plan);
+    const int64_t nch_r = has_random ? rhs_rand_chunks(plan) : 0;
     k_dz<<<static_cast<unsigned>(gnnshap::ceil_div(half, 256)), 256, 0, s>>>(y, half, M, w.classes, plan->num_classes,
                                                                              f_empty_full, w.dz);
     GS_LAUNCHED();
-    {
+    if (nch_e > 0) {
       GS_TIMED("k_rhs_part", s);
-      k_rhs_part<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(wpr, 4)), static_cast<unsigned>(nch)), 256, 0, s>>>(
-          masks, wpr, half, M, w.dz, rpc, w.part);
+      const int64_t rpc = gnnshap::ceil_div(rb0, nch_e);
+      k_rhs_part<<<dim3(static_cast<unsigned>(gnnshap::ceil_div(wpr, 4)), static_cast<unsigned>(nch_e)), 256, 0, s>>>(
+          masks, wpr, rb0, M, w.dz, rpc, w.part);
+    }
+    GS_LAUNCHED();
+    if (nch_r > 0) {
+      const int64_t nxb = gnnshap::ceil_div(wpr, 8);
+      if (nxb * nch_r > INT32_MAX) return gnnshap::fail(GNNSHAP_EUNSUPPORTED, "right-hand side grid too large");
+      GS_TIMED("k_rhs_rand", s);
+      k_rhs_rand<<<static_cast<unsigned>(nxb * nch_r), 512, 0, s>>>(w.T, M, wpr, kr, gnnshap::ceil_div(kr, 64),
+                                                                    w.dz + rb0, w.part + nch_e * M, nxb);
     }
     GS_LAUNCHED();
     const int64_t nbm = gnnshap::ceil_div(M, 256);
-    k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch, M, w.dv, w.bsum);
+    k_rhs_reduce<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.part, nch_e + nch_r, M, w.dv, w.bsum);
     GS_LAUNCHED();
     gnnshap::CgProblem pr{};
     pr.T = w.T;
