@@ -65,7 +65,7 @@ using gnnshap::nibble_dots;
 constexpr double kTol = 1e-8;
 constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
-constexpr int kWaves = 8;            // waves per workgroup of both passes
+constexpr int kWaves = 16;           // waves per workgroup of both passes (the tables serve 16 row blocks)
 constexpr int64_t kSparseDiv = 128;   // sparse rows: coalition size at most M / kSparseDiv
 
 struct Args {

@@ -1,5 +1,6 @@
-// Coalition values of a two-layer GCN with a wide hidden layer, on fp32 MFMA
-// (Sec. 3.4 of the GNNShap paper; the GCN of Sec. 4.2).
+// Coalition values of a two-layer GCN with a wide hidden layer, on bf16 MFMA
+// over an exact split of the fp32 operand (Sec. 3.4 of the GNNShap paper;
+// the GCN of Sec. 4.2).
 //
 // With two hops, H_1 = {v} and v's in-neighbours are the only nodes that
 // players enter.  Under coalition c, layer 1 at x in H_1 is
@@ -26,8 +27,9 @@
 //   k_wide_ends_l1, k_wide_ends_out
 //                the two end coalitions (no players, every player) for every
 //                class, and the explained class: layer 1 at every node of H_1
-//                by one workgroup per (node, 64 features), layer 2 by one
-//                wavefront per class
+//                as partial sums by four workgroups per (node, 64 features),
+//                then in one workgroup the sums, layer 1's end and layer 2 by
+//                one wavefront per class
 //   k_wide_prep  one workgroup: operand-unit offsets of each node and the
 //                list of players whose source is in H_1
 //   k_wide_zop   the A operands: for 32 players (one unit) and 16 features
@@ -163,26 +165,31 @@ __global__ void __launch_bounds__(256) k_wide_zop(const int32_t* __restrict__ ds
 }
 
 // S[x][f] = sum of Z[src e][f] over the players e -> x whose source is not in
-// H_1: thread (j, r) of the workgroup sums the players j, j + 16, ... for
-// feature 16 tile + r, then the 16 partial sums are added in a fixed tree.
-__global__ void __launch_bounds__(256) k_wide_sum(const int32_t* __restrict__ dst_ptr,
-                                                  const int32_t* __restrict__ edge_src, int64_t n1,
-                                                  const float* __restrict__ Zc, int h, int ntot,
-                                                  float* __restrict__ S) {
-  __shared__ float part[16][17];
+// H_1: thread (j, r) of the workgroup (1024 threads) sums the players j,
+// j + 64, ... for feature 16 tile + r (four loads in flight), then the 64
+// partial sums are added in a fixed tree.
+__global__ void __launch_bounds__(1024) k_wide_sum(const int32_t* __restrict__ dst_ptr,
+                                                   const int32_t* __restrict__ edge_src, int64_t n1,
+                                                   const float* __restrict__ Zc, int h, int ntot,
+                                                   float* __restrict__ S) {
+  __shared__ float part[64][17];
   const int64_t x = blockIdx.x / ntot;
   const int ft = static_cast<int>(blockIdx.x % ntot);
   const int r = threadIdx.x & 15, j = threadIdx.x >> 4;
   const int f = 16 * ft + r;
   const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
-  float acc = 0.f;
-  for (int e = e0 + j; e < e1; e += 16) {
-    const int32_t u = edge_src[e];
-    if (u >= n1) acc += Zc[static_cast<int64_t>(u) * h + f];
+  float a4[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int e = e0 + j; e < e1; e += 256) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int eq = e + 64 * q;
+      const int32_t u = eq < e1 ? edge_src[eq] : 0;
+      if (eq < e1 && u >= n1) a4[q] += Zc[static_cast<int64_t>(u) * h + f];
+    }
   }
-  part[j][r] = acc;
+  part[j][r] = (a4[0] + a4[1]) + (a4[2] + a4[3]);
   __syncthreads();
-  for (int w = 8; w >= 1; w >>= 1) {
+  for (int w = 32; w >= 1; w >>= 1) {
     if (j < w) part[j][r] += part[j + w][r];
     __syncthreads();
   }
@@ -455,24 +462,26 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
   }
 }
 
-// The two end coalitions (no players, every player), layer 1: Hf[x] =
-// H^1 at node x of H_1 under E_c (degrees: the players entering each node),
-// Hf[n1] = H^1 at the target under the empty coalition (its self loop only).
-// Workgroup (x, feature block of 64): wavefront w sums players w, w + 16,
-// ... for its 64 features (lane = feature), the sixteen partial sums are
-// added in a fixed order.
+// The two end coalitions (no players, every player), layer 1, partial sums:
+// Hp[p][x][f] = sum over part p of the players entering x (the 64 wavefronts
+// of the kEndParts workgroups of (x, feature block) take players w, w + 64,
+// ...) of d(src)^-1/2 Z[src][f] under E_c (degrees: the players entering each
+// node); lane = feature, the sixteen wavefronts' sums added in a fixed order.
+constexpr int kEndParts = 4;
+
 __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict__ dst_ptr,
                                                        const int32_t* __restrict__ edge_src, int64_t n1,
                                                        const float* __restrict__ Zc, int h,
-                                                       const float* __restrict__ b1, float* __restrict__ Hf) {
+                                                       float* __restrict__ Hp) {
   __shared__ float part[16][64];
   const int64_t x = blockIdx.x;
+  const int pp = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int f = blockIdx.y * 64 + lane;
   const bool fv = f < h;
   const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
   float acc = 0.f;
-  for (int e = e0 + wave; e < e1; e += 16) {
+  for (int e = e0 + pp * 16 + wave; e < e1; e += 16 * kEndParts) {
     const int32_t u = edge_src[e];
     const float du = u < n1 ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[u + 1] - dst_ptr[u])) : 1.0f;
     if (fv) acc = fmaf(du, Zc[static_cast<int64_t>(u) * h + f], acc);
@@ -482,11 +491,7 @@ __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict
   if (wave == 0 && fv) {
     float a = 0.f;
     for (int i = 0; i < 16; ++i) a += part[i][lane];
-    const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(e1 - e0));
-    const float bb = b1 ? b1[f] : 0.f;
-    const float zx = Zc[x * h + f];
-    Hf[x * h + f] = fmaxf(fmaf(dx, fmaf(dx, zx, a), bb), 0.f);
-    if (x == 0) Hf[n1 * h + f] = fmaxf(zx + bb, 0.f);
+    Hp[(static_cast<int64_t>(pp) * n1 + x) * h + f] = a;
   }
 }
 
@@ -496,12 +501,28 @@ __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict
 // f_empty_full as the other evaluation paths write them.  One workgroup of
 // 1024 threads, one wavefront per class at a time (lane = feature).
 __global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restrict__ dst_ptr, int64_t n1,
-                                                        const float* __restrict__ Hf, int h,
+                                                        const float* __restrict__ Hp, const float* __restrict__ Zc,
+                                                        const float* __restrict__ b1, int h,
                                                         const float* __restrict__ W2, const float* __restrict__ b2,
                                                         int C, int requested, float* __restrict__ sp_y,
                                                         int32_t* __restrict__ ctl, int32_t* __restrict__ class_out,
-                                                        float* __restrict__ f_empty_full) {
+                                                        float* __restrict__ f_empty_full, float* __restrict__ Hf) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // layer 1 under the end coalitions: Hf[x] at every node of H_1 under E_c
+  // (the parts' sums in order, self loop, bias, ReLU), Hf[n1] at the target
+  // under the empty coalition (its self loop only)
+  for (int64_t i = threadIdx.x; i < n1 * h; i += blockDim.x) {
+    const int64_t x = i / h;
+    const int f = static_cast<int>(i % h);
+    float a = 0.f;
+    for (int q = 0; q < kEndParts; ++q) a += Hp[(static_cast<int64_t>(q) * n1 + x) * h + f];
+    const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
+    const float bb = b1 ? b1[f] : 0.f;
+    const float zx = Zc[x * h + f];
+    Hf[i] = fmaxf(fmaf(dx, fmaf(dx, zx, a), bb), 0.f);
+    if (x == 0) Hf[n1 * h + f] = fmaxf(zx + bb, 0.f);
+  }
+  __syncthreads();
   const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[1] - dst_ptr[0]));
   for (int c = wave; c < C; c += 16) {
     float full = 0.f, empty = 0.f;
@@ -571,6 +592,7 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
   w.deg = c.take<int32_t>(s.k * s.n1);
   w.t = c.take<float>(static_cast<int64_t>(s.nfb) * s.k * s.n1);
   w.hf = c.take<float>((s.n1 + 1) * s.h);
+  w.hp = c.take<float>(kEndParts * s.n1 * s.h);
   return w;
 }
 
@@ -580,11 +602,11 @@ int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph
   if (s.n1 > 65535 * 64) return fail(GNNSHAP_EUNSUPPORTED, "too many nodes in H_1");
   {
     GS_TIMED("k_wide_ends", st);
-    k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64))), 1024, 0, st>>>(
-        sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h, b1, w.hf);
+    k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64)), kEndParts), 1024, 0,
+                     st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h, w.hp);
     GS_LAUNCHED();
-    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hf, s.h, W2, b2, s.C, target_class, sp_y, ctl, class_out,
-                                         f_empty_full);
+    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, Zc, b1, s.h, W2, b2, s.C, target_class, sp_y, ctl,
+                                         class_out, f_empty_full, w.hf);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
@@ -605,8 +627,8 @@ int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg,
       sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc, s.h, s.ntot, s.units_cap, w.Zop);
   GS_LAUNCHED();
   if (pairs) {
-    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot), 256, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h,
-                                                                     s.ntot, w.S);
+    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h,
+                                                                      s.ntot, w.S);
     GS_LAUNCHED();
   }
   k_wide_deg<<<grid_for(nrows * s.n1, 256, 16384), 256, 0, st>>>(masks, wpr, nrows, sg->dst_ptr, s.n1, w.deg);

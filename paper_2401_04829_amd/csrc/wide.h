@@ -29,6 +29,7 @@ struct WideWs {
   int32_t* deg;       // k x n1: in-degree of each node of H_1 under each evaluated row
   float* t;           // nfb x k x n1: each node's layer-1 output times the explained class's W_2 column
   float* hf;          // (n1 + 1) x h: layer 1 under the end coalitions (E_c at H_1, then empty at the target)
+  float* hp;          // 4 x n1 x h: partial sums of the players entering each node under E_c
 };
 WideWs wide_carve(Carver& c, const WideShape& s);
 
