@@ -197,7 +197,7 @@ def cpu_baseline(cfg, seconds):
 
 
 # Peaks (MI355X): HBM3E 8 TB/s; fp32 VALU without packed-fp32 instructions
-# (this build disables them): 256 CUs x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
+# (the library is compiled without them): 256 CUs x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
 # = 78.6 TFLOP/s; 32-bit integer VALU ops at the same issue rate: 39.3 Tops/s.
 HBM_PEAK_GBS = 8000.0
 VALU_FP32_TFLOPS = 78.6
@@ -344,7 +344,7 @@ def measured_traffic(kernel):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it",
+        print(json.dumps({"error": "bench.py runs on one GPU: a share of the targets per GPU is not implemented",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import workloads as W

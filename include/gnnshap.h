@@ -60,7 +60,7 @@ enum gnnshap_status {
   GNNSHAP_ECAPACITY = 2,    /* a caller buffer or workspace is too small; sizes reported */
   GNNSHAP_EHIP = 3,         /* a HIP runtime call failed */
   GNNSHAP_ESINGULAR = 4,    /* reserved: the solver reports pivots through `info` */
-  GNNSHAP_EUNSUPPORTED = 5  /* valid but outside what this build implements */
+  GNNSHAP_EUNSUPPORTED = 5  /* valid but outside what the library implements */
 };
 
 #define GNNSHAP_MAX_HOPS 8

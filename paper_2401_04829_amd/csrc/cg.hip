@@ -59,13 +59,17 @@
 namespace {
 
 using gnnshap::build_tables;
-using gnnshap::kTabWords;
 using gnnshap::nibble_dots;
 
 constexpr double kTol = 1e-8;
 constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
-constexpr int kWaves = 16;           // waves per workgroup of both passes (the tables serve 16 row blocks)
+constexpr int kWaves = 16;           // waves per workgroup of both passes
+constexpr int kTabA = 32;            // pass A: words of r's tables per workgroup (64 KiB of LDS)
+constexpr int kTabB = 32;            // pass B: row blocks of u's tables per workgroup
+constexpr int kPerWaveGroup = 2;     // row blocks (pass A) and player words (pass B) per wavefront
+                                     // in a group of several systems; one for a system alone
+constexpr int64_t kFill = 4096;      // (row block, chunk) pairs of a pass per system, at least
 constexpr int64_t kSparseDiv = 128;   // sparse rows: coalition size at most M / kSparseDiv
 
 struct Args {
@@ -74,6 +78,7 @@ struct Args {
   const int32_t* sz;
   int64_t M, wpr, kr, nrb, npc, pwords, nrc, rbc, nbu, nbc;
   int64_t rs, rbd0, nsa, nsb, nrcd, nxa, nxb, nsi;
+  int32_t pw;                // row blocks / player words per wavefront of the two passes (their grids)
   int32_t lgb;     // pass B: log2 of the lanes summing one player's list
   const int64_t* sitem;
   const int64_t* csr_ptr;
@@ -244,14 +249,16 @@ __device__ __forceinline__ double wave_gather_sum(const int32_t* __restrict__ id
 // Pass A.  Workgroup y * nxa + x (y < npc): upart[y, b] = sum over the words
 // of player chunk y of the bits of bit row b times r; the workgroup builds
 // the chunk's nibble tables of r in LDS (r is padded with zeros to whole
-// words), then one wave per 64 rows (lane = row) reads the row-blocked
-// words, 512 contiguous bytes per word, and sums table entries.  Workgroup
+// words), then each wave takes PW blocks of 64 rows (lane = row),
+// reads their row-blocked words, 512 contiguous bytes per word, and sums
+// table entries.  Workgroup
 // nxa * npc + x (x < nsa): the sparse rows x * kWaves + wave, + nsa * kWaves,
 // ...: u_b = sum of r over the row's players, with the workgroup's partial
 // |u|^2 and |m|.u in uu[2 x], uu[2 x + 1].  Both kinds take the stopping
 // test first.
-__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(GroupArgs g) {
-  __shared__ double tab[kTabWords * 256];   // the sparse rows' workgroups: kWaves block sums
+template <int PW>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(8))) k_cg_pass_a(GroupArgs g) {
+  __shared__ double tab[kTabA * 256];   // the sparse rows' workgroups: kWaves block sums
   int64_t bid;
   const int m = member_of(g, bid);
   const Args& a = g.a[m];
@@ -303,7 +310,8 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(GroupArgs g) {
     }
     return;
   }
-  const int64_t rb = a.rbd0 + (bid % a.nxa) * kWaves + wave;
+  // the wavefront's row blocks: rb, rb + kWaves, ... (PW of them)
+  const int64_t rb = a.rbd0 + (bid % a.nxa) * (kWaves * PW) + wave;
   const int64_t w0 = pc * a.pwords;
   const int64_t w1 = w0 + a.pwords < a.wpr ? w0 + a.pwords : a.wpr;
   const int64_t nw = w1 - w0;
@@ -312,12 +320,16 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_a(GroupArgs g) {
   build_tables(r + w0 * 64, nw * 16, tab);
   if (cg_stop(a, t, writer)) return;   // the same outcome in every wave
   __syncthreads();
-  if (rb >= a.nrb) return;
-  const uint64_t* src = blocked + (rb * a.wpr + w0) * 64 + lane;
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  nibble_dots<0>(src, 64, static_cast<int>(nw), src[0], reinterpret_cast<const char*>(tab), acc);
-  const int64_t row = rb * 64 + lane;
-  if (row < a.kr) upart[pc * a.kr + row] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll 1
+  for (int q = 0; q < PW; ++q) {
+    const int64_t rq = rb + q * kWaves;
+    if (rq >= a.nrb) break;
+    const uint64_t* src = blocked + (rq * a.wpr + w0) * 64 + lane;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    nibble_dots<kTabA>(src, 64, static_cast<int>(nw), src[0], reinterpret_cast<const char*>(tab), acc);
+    const int64_t row = rq * 64 + lane;
+    if (row < a.kr) upart[pc * a.kr + row] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
 }
 
 // u of the bit rows (the sum of their pass-A chunks, one lane per row) with
@@ -356,12 +368,13 @@ __global__ void __launch_bounds__(256) k_cg_rows(GroupArgs g) {
 // Pass B.  Workgroup c * nxb + x (c < nrcd): qpart[c, j] = sum over the row
 // blocks of chunk c of the bits of player j times u; the workgroup builds
 // the chunk's nibble tables of u in LDS (u is padded with zeros to whole row
-// blocks), then one wave per 64 players (lane = player) reads the
-// bit-transposed words T[rb, j] and sums table entries.  Workgroup
+// blocks), then each wave takes PW words of 64 players (lane =
+// player), reads the bit-transposed words T[rb, j] and sums table entries.  Workgroup
 // nxb * nrcd + x (x < nsb): groups of 64 / L players (x * kWaves + wave, +
 // nsb * kWaves, ...): qs[j] = sum of u over the sparse rows holding player j.
-__global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(GroupArgs g) {
-  __shared__ double tab[kTabWords * 256];
+template <int PW>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(8))) k_cg_pass_b(GroupArgs g) {
+  __shared__ double tab[kTabB * 256];
   int64_t bid;
   const Args& a = g.a[member_of(g, bid)];
   if (a.st->done) return;
@@ -399,20 +412,25 @@ __global__ void __launch_bounds__(kWaves * 64) k_cg_pass_b(GroupArgs g) {
     }
     return;
   }
-  const int64_t gw = (bid % a.nxb) * kWaves + wave;   // the wavefront's player word
+  // the wavefront's player words: gw, gw + kWaves, ... (PW of them)
+  const int64_t gw = (bid % a.nxb) * (kWaves * PW) + wave;
   const int64_t b0 = a.rbd0 + c * a.rbc;
   const int64_t b1 = b0 + a.rbc < a.nrb ? b0 + a.rbc : a.nrb;
   const int64_t nb = b1 - b0;
   build_tables(u + b0 * 64, nb * 16, tab);
   __syncthreads();
-  if (gw >= a.wpr) return;
-  const int64_t j = gw * 64 + lane;
-  const bool valid = j < a.M;
-  const uint64_t* col = T + b0 * a.M + (valid ? j : 0);
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  // a lane beyond M reads player 0's words and discards its sums
-  nibble_dots<0>(col, a.M, static_cast<int>(nb), col[0], reinterpret_cast<const char*>(tab), acc);
-  if (valid) qpart[c * a.M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll 1
+  for (int q = 0; q < PW; ++q) {
+    const int64_t gq = gw + q * kWaves;
+    if (gq >= a.wpr) break;
+    const int64_t j = gq * 64 + lane;
+    const bool valid = j < a.M;
+    const uint64_t* col = T + b0 * a.M + (valid ? j : 0);
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    // a lane beyond M reads player 0's words and discards its sums
+    nibble_dots<kTabB>(col, a.M, static_cast<int>(nb), col[0], reinterpret_cast<const char*>(tab), acc);
+    if (valid) qpart[c * a.M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
 }
 
 // ---- the sparse rows' lists, built once per solve ------------------------------------------
@@ -779,14 +797,14 @@ gnnshap::CgShape gnnshap::cg_shape(int64_t M, int64_t wpr, int64_t kr, int64_t r
   }
   s.rbd0 = s.rs / 64;
   const int64_t nrbd = std::max<int64_t>(s.nrb - s.rbd0, 1);
-  // pass A: about 4096 waves (row blocks x player chunks of whole words), at
-  // most kTabWords words of tables per workgroup
-  const int64_t npc = std::max<int64_t>(ceil_div(wpr, kTabWords), std::min(ceil_div(4096, nrbd), wpr));
+  // pass A: at least kFill (row block, player chunk) pairs, chunks of whole
+  // words, at most kTabA words of tables per workgroup
+  const int64_t npc = std::max<int64_t>(ceil_div(wpr, kTabA), std::min(ceil_div(kFill, nrbd), wpr));
   s.pwords = ceil_div(wpr, npc);
   s.npc = ceil_div(wpr, s.pwords);
-  // pass B: about 4096 waves (player words x chunks of whole row blocks), at
-  // most kTabWords row blocks of tables per workgroup
-  const int64_t nrc = std::max<int64_t>(ceil_div(nrbd, kTabWords), std::min(ceil_div(4096, wpr), nrbd));
+  // pass B: at least kFill (player word, row chunk) pairs, chunks of whole
+  // row blocks, at most kTabB row blocks of tables per workgroup
+  const int64_t nrc = std::max<int64_t>(ceil_div(nrbd, kTabB), std::min(ceil_div(kFill, wpr), nrbd));
   s.rbc = ceil_div(nrbd, nrc);
   s.nrc = ceil_div(nrbd, s.rbc);
   // workgroups of the sparse rows in pass A (rows) and pass B (players), at
@@ -839,6 +857,18 @@ struct Member {
   int64_t t = 0;
   uint32_t ga = 0, gb = 0, g_rows = 0, g_upd = 0;
 };
+
+// pw row blocks (pass A) and player words (pass B) per wavefront: the
+// passes' grids follow; the sums, and so the results, do not depend on pw.
+void set_per_wave(Member& m, int pw) {
+  Args& a = m.a;
+  const gnnshap::CgShape& sh = m.sh;
+  a.pw = pw;
+  a.nxa = gnnshap::ceil_div(std::max<int64_t>(sh.nrb - sh.rbd0, 1), kWaves * pw);
+  a.nxb = gnnshap::ceil_div(sh.wpr, kWaves * pw);
+  m.ga = static_cast<uint32_t>(a.nxa * sh.npc + sh.nsa);
+  m.gb = static_cast<uint32_t>(a.nxb * sh.nrcd + sh.nsb);
+}
 
 struct gnnshap::CgGroup::State {
   std::vector<Member> mem;
@@ -912,16 +942,13 @@ int gnnshap::CgGroup::add(const CgProblem& pr, const CgShape& sh, const CgWs& w)
   a.sitem = w.sitem;
   a.nsb = sh.nsb;
   a.nrcd = sh.nrcd;
-  a.nxa = ceil_div(std::max<int64_t>(sh.nrb - sh.rbd0, 1), kWaves);
-  a.nxb = ceil_div(sh.wpr, kWaves);
+  set_per_wave(m, 1);
   a.csr_ptr = w.csr_ptr;
   a.csr_idx = w.csr_idx;
   a.csc_ptr = w.csc_ptr;
   a.csc_row = w.csc_row;
   a.qs = w.qs;
   a.host_flag = hf->dev;
-  m.ga = static_cast<uint32_t>(a.nxa * sh.npc + sh.nsa);
-  m.gb = static_cast<uint32_t>(a.nxb * sh.nrcd + sh.nsb);
   m.g_rows = static_cast<uint32_t>(sh.nbu);
   m.g_upd = static_cast<uint32_t>(sh.nbc);
   // no kernel of an earlier solve that used this flag writes it any more:
@@ -1023,6 +1050,11 @@ int gnnshap::CgGroup::step() {
     }
     if (S.mem.empty()) return GNNSHAP_OK;
   }
+  // a system alone fills the GPU better with one row block (player word)
+  // per wavefront, several systems leave fewer, longer wavefronts
+  const int pw = S.mem.size() >= 2 ? kPerWaveGroup : 1;
+  for (Member& m : S.mem)
+    if (m.a.pw != pw) set_per_wave(m, pw);
   GroupArgs g;
   for (int64_t dt = 0; dt < kChunk; ++dt) {
     uint32_t n = fill_group(g, S.mem, dt, [](const Member&, int64_t t) { return t <= kMaxIt; },
@@ -1030,7 +1062,10 @@ int gnnshap::CgGroup::step() {
     if (g.n == 0) break;
     {
       GS_TIMED("k_cg_pass_a", s);
-      k_cg_pass_a<<<n, kWaves * 64, 0, s>>>(g);
+      if (pw == 1)
+        k_cg_pass_a<1><<<n, kWaves * 64, 0, s>>>(g);
+      else
+        k_cg_pass_a<kPerWaveGroup><<<n, kWaves * 64, 0, s>>>(g);
     }
     GS_LAUNCHED();
     n = fill_group(g, S.mem, dt, [](const Member& m, int64_t t) { return t < kMaxIt && m.sh.kr > 0; },
@@ -1045,7 +1080,10 @@ int gnnshap::CgGroup::step() {
                      [](const Member& m) { return m.gb; });
       {
         GS_TIMED("k_cg_pass_b", s);
-        k_cg_pass_b<<<n, kWaves * 64, 0, s>>>(g);
+        if (pw == 1)
+          k_cg_pass_b<1><<<n, kWaves * 64, 0, s>>>(g);
+        else
+          k_cg_pass_b<kPerWaveGroup><<<n, kWaves * 64, 0, s>>>(g);
       }
       GS_LAUNCHED();
     }

@@ -59,18 +59,18 @@ __device__ __forceinline__ void nibble_dot(uint64_t word, const char* tabs, doub
       }
 }
 
-// acc[0..3] += the products of n <= kTabWords words (word w at src[w * stride])
-// with the tables of consecutive 64-entry groups; the next word's load is
-// issued before the current word's table reads.
-template <int W>
+// acc[0..3] += the products of n <= NW words (word w at src[w * stride]) with
+// the tables of consecutive 64-entry groups; the next word's load is issued
+// before the current word's table reads.
+template <int NW, int W = 0>
 __device__ __forceinline__ void nibble_dots(const uint64_t* __restrict__ src, int64_t stride, int n, uint64_t next,
                                             const char* tabs, double (&acc)[4]) {
-  if constexpr (W < kTabWords) {
+  if constexpr (W < NW) {
     if (W >= n) return;
     const uint64_t word = next;
     if (W + 1 < n) next = src[(W + 1) * stride];
     nibble_dot<W>(word, tabs, acc);
-    nibble_dots<W + 1>(src, stride, n, next, tabs, acc);
+    nibble_dots<NW, W + 1>(src, stride, n, next, tabs, acc);
   }
 }
 

@@ -563,7 +563,7 @@ __global__ void __launch_bounds__(512) k_rhs_rand(const uint64_t* __restrict__ T
   const bool valid = j < M;
   const uint64_t* col = T + b0 * M + (valid ? j : 0);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  gnnshap::nibble_dots<0>(col, M, static_cast<int>(nb), col[0], reinterpret_cast<const char*>(tab), acc);
+  gnnshap::nibble_dots<gnnshap::kTabWords>(col, M, static_cast<int>(nb), col[0], reinterpret_cast<const char*>(tab), acc);
   if (valid) part[c * M + j] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
