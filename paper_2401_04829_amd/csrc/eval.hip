@@ -117,12 +117,12 @@ int make_shape(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, Shap
   else if (t >= kTB) t -= t % kTB;
   if (t < 2) t = 2;
   s.tile = t;
-  // The wide path evaluates every row in one launch sequence of its own; the
+  // The wide path evaluates every row in a launch sequence of its own; the
   // per-pass arrays above then serve the two end coalitions only.
-  s.wide = gnnshap::wide_applies(s.L, s.hops, s.dims[1]) && s.n_dst == sg->hop_ptr[2];
+  s.wide = gnnshap::wide_applies(s.L, s.hops, s.dims) && s.n_dst == sg->hop_ptr[2];
   if (s.wide) {
     s.tile = 2;
-    s.ws = gnnshap::wide_shape(sg->num_edges, s.n_nodes, s.n_dst, k, s.dims[1], s.dims[s.L]);
+    s.ws = gnnshap::wide_shape(sg->num_edges, s.n_nodes, s.n_dst, k, s.dims, s.L);
   }
   *out = s;
   return GNNSHAP_OK;
@@ -1691,7 +1691,7 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
     }
   }
   // f(empty) and f(E_c) for every class, then the explained class.
-  if (sh.wide) {
+  if (sh.wide && L == 2) {
     const float* b1 = m->b ? m->b[0] : nullptr;
     const float* b2 = m->b ? m->b[1] : nullptr;
     if (int st = gnnshap::launch_wide_ends(sh.ws, w.wide, sg, w.Zc[1], b1, m->W[1], b2, target_class, w.sp_y, w.ctl,
@@ -1709,6 +1709,27 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
     if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
     k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
     GS_LAUNCHED();
+  }
+  if (sh.wide) {
+    // three layers: layer 1 and layer 2 at H_1 as contractions, the dense
+    // transform by W_2 between them, in passes over the rows
+    const gnnshap::WideShape& ws = sh.ws;
+    if (int st = gnnshap::launch_wide3_prep(ws, w.wide, sg, masks, sh.wpr, w.Zc[1], w.Zc[2], pairs, s)) return st;
+    const int64_t nrows = pairs ? k / 2 : k;
+    for (int64_t r0 = 0; r0 < nrows; r0 += ws.pass) {
+      const int64_t nloc = std::min(ws.pass, nrows - r0);
+      if (int st = gnnshap::launch_wide3_l1(ws, w.wide, sg, masks, sh.wpr, r0, nloc, w.Zc[1], m->b ? m->b[0] : nullptr,
+                                            pairs, s))
+        return st;
+      if (int st = launch_gemm(s, w.wide.H1, ws.h, nullptr, nullptr, m->W[1], ws.h2, w.wide.Z2, ws.h2, 0,
+                               (pairs ? 2 : 1) * nloc * ws.n1, ws.h2, ws.h))
+        return st;
+      if (int st = gnnshap::launch_wide3_l2(ws, w.wide, sg, masks, sh.wpr, r0, nloc, m->b ? m->b[1] : nullptr,
+                                            m->W[2], w.ctl, pairs, s))
+        return st;
+    }
+    return gnnshap::launch_wide3_out(ws, w.wide, sg, masks, sh.wpr, m->b ? m->b[2] : nullptr, w.ctl, f_empty_full,
+                                     pairs, y, s);
   }
   // Prediction pruning, then the live coalitions in passes of sh.tile rows.
   k_live<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(masks, sh.wpr, k, sg->dst_ptr, w.ctl, w.live_rows,

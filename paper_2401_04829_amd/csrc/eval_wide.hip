@@ -218,37 +218,51 @@ __global__ void __launch_bounds__(256) k_wide_deg(const uint64_t* __restrict__ m
   }
 }
 
-// Layer 1 at node x = blockIdx.x / cblocks for 256 coalitions (block
-// blockIdx.x % cblocks) and features 64 blockIdx.y .. + 63.  Wavefront w
-// holds rows c0 .. c0 + 63, c0 = 256 block + 64 w, as four 16-row tiles;
-// lane (r, g) = (lane % 16, lane / 16) holds, per tile ct and feature tile
-// ft, features 16 ft + 4 g .. + 3 of row c0 + 16 ct + r.  Writes
-// t[fb][row][x] for the row and, with pairs, for row + khalf.
-template <bool PAIRS>
+// What the epilogue of the contraction makes of a layer's sums at x:
+//   kProj   H at x projected on the explained class's column of the next
+//           weight matrix (the last hidden layer): t[fb][row][x]
+//   kFull   H at x itself (layer 1 of a three-layer model): Hout rows
+// and where the players whose source is in H_1 (and x's self loop) take
+// their input row from: Zc (constant, layer 1) or Zrow (the coalition's
+// own rows, layer 2 of a three-layer model: kProjRows).
+enum : int { kProj = 0, kFull = 1, kProjRows = 2 };
+
+// One layer at node x = blockIdx.x / cblocks of H_1 for 256 coalitions
+// (block blockIdx.x % cblocks of the pass's nloc rows r0 .. r0 + nloc - 1)
+// and features 64 blockIdx.y .. + 63.  Wavefront w holds pass rows c0 ..
+// c0 + 63, c0 = 256 block + 64 w, as four 16-row tiles; lane (r, g) = (lane
+// % 16, lane / 16) holds, per tile ct and feature tile ft, features 16 ft +
+// 4 g .. + 3 of pass row c0 + 16 ct + r.  The row's complement (pairs) is
+// row + khalf; per-row arrays of the pass (Hout, Zrow: [pass row][x][f])
+// hold the complement of pass row i at i + nloc.
+template <bool PAIRS, int MODE>
 __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
-    const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows, int64_t khalf, int64_t cblocks,
+    const uint64_t* __restrict__ masks, int64_t wpr, int64_t r0, int64_t nloc, int64_t khalf, int64_t cblocks,
     const int32_t* __restrict__ dst_ptr, const int32_t* __restrict__ edge_src, int64_t n1,
     const int32_t* __restrict__ seg, const uint4* __restrict__ Zop, int ntot, int h, const float* __restrict__ Zc,
     const float* __restrict__ S, const int32_t* __restrict__ spec_ptr, const int32_t* __restrict__ spec_e,
     const int32_t* __restrict__ deg, const float* __restrict__ b1, const float* __restrict__ W2, int C,
-    const int32_t* __restrict__ ctl, float* __restrict__ t, int64_t k) {
+    const int32_t* __restrict__ ctl, float* __restrict__ t, int64_t k, const float* __restrict__ Zrow,
+    float* __restrict__ Hout) {
   const int64_t x = blockIdx.x / cblocks;
   const int64_t cb = blockIdx.x % cblocks;
   const int fb = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rl = lane & 15, g = lane >> 4;
   const int64_t c0 = cb * kBlockRows + wave * kWaveRows;
-  if (c0 >= nrows) return;                       // no barrier in this kernel
+  if (c0 >= nloc) return;                        // no barrier in this kernel
   const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
   const int u0 = seg[x], nu = seg[x + 1] - u0;
   const int ft0 = fb * kTiles;
   const int nt = ntot - ft0 < kTiles ? ntot - ft0 : kTiles;
 
-  int64_t row[4];
+  int64_t row[4], lr[4];   // the mask row and the pass row of each tile (clamped to 0 when invalid)
   bool valid[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
-    row[ct] = c0 + 16 * ct + rl;
-    valid[ct] = row[ct] < nrows;
+    const int64_t i = c0 + 16 * ct + rl;
+    valid[ct] = i < nloc;
+    lr[ct] = valid[ct] ? i : 0;
+    row[ct] = r0 + lr[ct];
   }
   mx4_t D[4][kTiles];
 #pragma unroll
@@ -322,11 +336,12 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
   }
 
   // epilogue: the players whose source is in H_1, self loop, bias, ReLU and
-  // the explained class's column of W_2, per row (and its complement).  The
-  // player loop runs once for the four row tiles: its source, the source's
-  // size and its feature values are loaded once, each row tile adds them
-  // with its own coefficient (0 for the coalition it is not in).
-  const int cls = ctl[0];
+  // (kProj, kProjRows) the explained class's column of the next weight
+  // matrix, per row (and its complement).  The player loop runs once for the
+  // four row tiles: its source, the source's size and (constant input rows)
+  // its feature values are loaded once, each row tile adds them with its own
+  // coefficient (0 for the coalition it is not in).
+  const int cls = MODE == kFull ? 0 : ctl[0];
   const int nx = e1 - e0;
   const int sp0 = spec_ptr[x], sp1 = spec_ptr[x + 1];
   const int32_t* dgr[4];
@@ -362,18 +377,40 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
     for (int ft = 0; ft < kTiles; ++ft) {
       if (ft >= nt) continue;
       const int f = 16 * (ft0 + ft) + 4 * g;
-      const float4 zu = *reinterpret_cast<const float4*>(Zc + static_cast<int64_t>(u) * h + f);
+      if (MODE != kProjRows) {
+        const float4 zu = *reinterpret_cast<const float4*>(Zc + static_cast<int64_t>(u) * h + f);
 #pragma unroll
-      for (int ct = 0; ct < 4; ++ct) {
-        D[ct][ft][0] = fmaf(cw[ct], zu.x, D[ct][ft][0]);
-        D[ct][ft][1] = fmaf(cw[ct], zu.y, D[ct][ft][1]);
-        D[ct][ft][2] = fmaf(cw[ct], zu.z, D[ct][ft][2]);
-        D[ct][ft][3] = fmaf(cw[ct], zu.w, D[ct][ft][3]);
-        if (PAIRS) {
-          P[ct][ft][0] = fmaf(cp[ct], zu.x, P[ct][ft][0]);
-          P[ct][ft][1] = fmaf(cp[ct], zu.y, P[ct][ft][1]);
-          P[ct][ft][2] = fmaf(cp[ct], zu.z, P[ct][ft][2]);
-          P[ct][ft][3] = fmaf(cp[ct], zu.w, P[ct][ft][3]);
+        for (int ct = 0; ct < 4; ++ct) {
+          D[ct][ft][0] = fmaf(cw[ct], zu.x, D[ct][ft][0]);
+          D[ct][ft][1] = fmaf(cw[ct], zu.y, D[ct][ft][1]);
+          D[ct][ft][2] = fmaf(cw[ct], zu.z, D[ct][ft][2]);
+          D[ct][ft][3] = fmaf(cw[ct], zu.w, D[ct][ft][3]);
+          if (PAIRS) {
+            P[ct][ft][0] = fmaf(cp[ct], zu.x, P[ct][ft][0]);
+            P[ct][ft][1] = fmaf(cp[ct], zu.y, P[ct][ft][1]);
+            P[ct][ft][2] = fmaf(cp[ct], zu.z, P[ct][ft][2]);
+            P[ct][ft][3] = fmaf(cp[ct], zu.w, P[ct][ft][3]);
+          }
+        }
+      } else {
+        // the source's row under each coalition (a coalition without the
+        // player skips the load: its coefficient is 0)
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+          if (cw[ct] != 0.f) {
+            const float4 zu = *reinterpret_cast<const float4*>(Zrow + (lr[ct] * n1 + u) * h + f);
+            D[ct][ft][0] = fmaf(cw[ct], zu.x, D[ct][ft][0]);
+            D[ct][ft][1] = fmaf(cw[ct], zu.y, D[ct][ft][1]);
+            D[ct][ft][2] = fmaf(cw[ct], zu.z, D[ct][ft][2]);
+            D[ct][ft][3] = fmaf(cw[ct], zu.w, D[ct][ft][3]);
+          }
+          if (PAIRS && cp[ct] != 0.f) {
+            const float4 zu = *reinterpret_cast<const float4*>(Zrow + ((lr[ct] + nloc) * n1 + u) * h + f);
+            P[ct][ft][0] = fmaf(cp[ct], zu.x, P[ct][ft][0]);
+            P[ct][ft][1] = fmaf(cp[ct], zu.y, P[ct][ft][1]);
+            P[ct][ft][2] = fmaf(cp[ct], zu.z, P[ct][ft][2]);
+            P[ct][ft][3] = fmaf(cp[ct], zu.w, P[ct][ft][3]);
+          }
         }
       }
     }
@@ -383,19 +420,49 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
     const int dgx = dgr[ct][x];
     const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dgx));
     const float dxp = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(nx - dgx));
+    if (MODE == kFull) {
+      // H at x, and at x under the complement, as rows of the pass
+#pragma unroll
+      for (int ft = 0; ft < kTiles; ++ft) {
+        if (ft >= nt) continue;
+        const int f = 16 * (ft0 + ft) + 4 * g;
+        const float4 zx = *reinterpret_cast<const float4*>(Zc + x * h + f);
+        const float zxv[4] = {zx.x, zx.y, zx.z, zx.w};
+        float hv[4], hp[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float bb = b1 ? b1[f + i] : 0.f;
+          hv[i] = fmaxf(fmaf(dx, fmaf(dx, zxv[i], D[ct][ft][i]), bb), 0.f);
+          hp[i] = PAIRS ? fmaxf(fmaf(dxp, fmaf(dxp, zxv[i], P[ct][ft][i]), bb), 0.f) : 0.f;
+        }
+        if (valid[ct]) {
+          *reinterpret_cast<float4*>(Hout + (lr[ct] * n1 + x) * h + f) = make_float4(hv[0], hv[1], hv[2], hv[3]);
+          if (PAIRS)
+            *reinterpret_cast<float4*>(Hout + ((lr[ct] + nloc) * n1 + x) * h + f) =
+                make_float4(hp[0], hp[1], hp[2], hp[3]);
+        }
+      }
+      continue;
+    }
     float tc = 0.f, tcp = 0.f;
 #pragma unroll
     for (int ft = 0; ft < kTiles; ++ft) {
       if (ft >= nt) continue;
       const int f = 16 * (ft0 + ft) + 4 * g;
-      const float4 zx = *reinterpret_cast<const float4*>(Zc + x * h + f);
+      // the self loop's input row: constant, or the coalition's own (and its complement's)
+      const float4 zx = MODE == kProjRows ? *reinterpret_cast<const float4*>(Zrow + (lr[ct] * n1 + x) * h + f)
+                                          : *reinterpret_cast<const float4*>(Zc + x * h + f);
+      const float4 zxc = (MODE == kProjRows && PAIRS)
+                             ? *reinterpret_cast<const float4*>(Zrow + ((lr[ct] + nloc) * n1 + x) * h + f)
+                             : zx;
       const float zxv[4] = {zx.x, zx.y, zx.z, zx.w};
+      const float zxcv[4] = {zxc.x, zxc.y, zxc.z, zxc.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float bb = b1 ? b1[f + i] : 0.f;
         const float ww = W2[static_cast<int64_t>(f + i) * C + cls];
         tc = fmaf(fmaxf(fmaf(dx, fmaf(dx, zxv[i], D[ct][ft][i]), bb), 0.f), ww, tc);
-        if (PAIRS) tcp = fmaf(fmaxf(fmaf(dxp, fmaf(dxp, zxv[i], P[ct][ft][i]), bb), 0.f), ww, tcp);
+        if (PAIRS) tcp = fmaf(fmaxf(fmaf(dxp, fmaf(dxp, zxcv[i], P[ct][ft][i]), bb), 0.f), ww, tcp);
       }
     }
     tc += __shfl_xor(tc, 16);
@@ -564,21 +631,105 @@ __global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restric
 
 namespace gnnshap {
 
-bool wide_applies(int num_layers, int num_hops, int h) {
-  return num_layers == 2 && num_hops == 2 && h > 32 && h % 16 == 0 && h <= 4096;
+namespace {
+
+bool wide_width(int h) { return h > 32 && h % 16 == 0 && h <= 4096; }
+
+// Contracted rows per pass of a three-layer model: H1 and Z2 of a pass's
+// rows and complements fill at most kPassBudget bytes (whole 256-row blocks).
+constexpr int64_t kPassBudget = int64_t(1) << 30;
+
+// Shared set-up: operand units and player lists, layer-1 operands and sums,
+// degrees of the contracted rows.
+int wide_prep(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr,
+              const float* Zc, bool pairs, hipStream_t st) {
+  if (pairs && (s.k & 1)) return fail(GNNSHAP_EINVAL, "complement pairs need an even number of rows");
+  if (s.n1 > INT32_MAX / 2 || s.M > INT32_MAX / 2) return fail(GNNSHAP_EUNSUPPORTED, "subgraph too large");
+  const int64_t nrows = pairs ? s.k / 2 : s.k;
+  k_wide_prep<<<1, 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, w.seg, w.spec_ptr, w.spec_e);
+  GS_LAUNCHED();
+  k_wide_zop<<<grid_for(s.units_cap * s.ntot * 64, 256, 16384), 256, 0, st>>>(
+      sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc, s.h, s.ntot, s.units_cap, w.Zop);
+  GS_LAUNCHED();
+  if (pairs) {
+    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h,
+                                                                      s.ntot, w.S);
+    GS_LAUNCHED();
+  }
+  k_wide_deg<<<grid_for(nrows * s.n1, 256, 16384), 256, 0, st>>>(masks, wpr, nrows, sg->dst_ptr, s.n1, w.deg);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }
 
-WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t k, int h, int C) {
+// One contraction launch over the pass r0 .. r0 + nloc - 1 (see k_wide_l1).
+template <int MODE>
+int wide_layer(const WideShape& s, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr, int64_t r0,
+               int64_t nloc, bool pairs, const uint4* Zop, int ntot, int nfb, int h, const float* Zc, const float* S,
+               const WideWs& w, const float* b, const float* Wp, const int32_t* ctl, const float* Zrow, float* Hout,
+               hipStream_t st) {
+  if (nloc <= 0) return GNNSHAP_OK;
+  const int64_t khalf = pairs ? s.k / 2 : 0;
+  const int64_t cblocks = ceil_div(nloc, kBlockRows);
+  if (s.n1 * cblocks > INT32_MAX || nfb > 65535) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
+  const dim3 grid(static_cast<unsigned>(s.n1 * cblocks), static_cast<unsigned>(nfb));
+  if (pairs)
+    k_wide_l1<true, MODE><<<grid, kBlockRows, 0, st>>>(masks, wpr, r0, nloc, khalf, cblocks, sg->dst_ptr,
+                                                       sg->edge_src, s.n1, w.seg, Zop, ntot, h, Zc, S, w.spec_ptr,
+                                                       w.spec_e, w.deg, b, Wp, s.C, ctl, w.t, s.k, Zrow, Hout);
+  else
+    k_wide_l1<false, MODE><<<grid, kBlockRows, 0, st>>>(masks, wpr, r0, nloc, khalf, cblocks, sg->dst_ptr,
+                                                        sg->edge_src, s.n1, w.seg, Zop, ntot, h, Zc, S, w.spec_ptr,
+                                                        w.spec_e, w.deg, b, Wp, s.C, ctl, w.t, s.k, Zrow, Hout);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int wide_out(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr,
+             int nfb_t, const float* b_last, const int32_t* ctl, const float* fef, bool pairs, float* y,
+             hipStream_t st) {
+  const int64_t nrows = pairs ? s.k / 2 : s.k;
+  const int64_t khalf = pairs ? s.k / 2 : 0;
+  const unsigned g = static_cast<unsigned>(ceil_div(nrows, 256));
+  GS_TIMED("k_wide_out", st);
+  if (pairs)
+    k_wide_out<true><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, nfb_t, s.k, b_last,
+                                        ctl, fef, y);
+  else
+    k_wide_out<false><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, nfb_t, s.k, b_last,
+                                         ctl, fef, y);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+}  // namespace
+
+bool wide_applies(int num_layers, int num_hops, const int32_t* dims) {
+  if (num_hops != 2 || (num_layers != 2 && num_layers != 3)) return false;
+  for (int j = 1; j < num_layers; ++j)
+    if (!wide_width(dims[j])) return false;
+  return true;
+}
+
+WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t k, const int32_t* dims, int num_layers) {
   WideShape s;
   s.M = M;
   s.n_nodes = n_nodes;
   s.n1 = n1;
   s.k = k;
-  s.h = h;
-  s.C = C;
-  s.ntot = h / 16;
+  s.h = dims[1];
+  s.C = dims[num_layers];
+  s.ntot = s.h / 16;
   s.nfb = static_cast<int>(ceil_div(s.ntot, kTiles));
   s.units_cap = ceil_div(M, kUnit) + n1;
+  if (num_layers == 3) {
+    s.h2 = dims[2];
+    s.ntot2 = s.h2 / 16;
+    s.nfb2 = static_cast<int>(ceil_div(s.ntot2, kTiles));
+    const int64_t per_row = 2 * n1 * (static_cast<int64_t>(s.h) + s.h2) * static_cast<int64_t>(sizeof(float));
+    int64_t p = kPassBudget / per_row;
+    p = std::max<int64_t>(kBlockRows, p - p % kBlockRows);
+    s.pass = std::min<int64_t>(p, k);
+  }
   return s;
 }
 
@@ -590,9 +741,16 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
   w.Zop = c.take<uint4>(s.units_cap * s.ntot * kParts * 64);
   w.S = c.take<float>(s.n1 * s.h);
   w.deg = c.take<int32_t>(s.k * s.n1);
-  w.t = c.take<float>(static_cast<int64_t>(s.nfb) * s.k * s.n1);
-  w.hf = c.take<float>((s.n1 + 1) * s.h);
-  w.hp = c.take<float>(kEndParts * s.n1 * s.h);
+  w.t = c.take<float>(static_cast<int64_t>(s.h2 ? s.nfb2 : s.nfb) * s.k * s.n1);
+  if (s.h2 == 0) {
+    w.hf = c.take<float>((s.n1 + 1) * s.h);
+    w.hp = c.take<float>(kEndParts * s.n1 * s.h);
+  } else {
+    w.Zop2 = c.take<uint4>(s.units_cap * s.ntot2 * kParts * 64);
+    w.S2 = c.take<float>(s.n1 * s.h2);
+    w.H1 = c.take<float>(2 * s.pass * s.n1 * s.h);
+    w.Z2 = c.take<float>(2 * s.pass * s.n1 * s.h2);
+  }
   return w;
 }
 
@@ -615,49 +773,55 @@ int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph
 int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr,
                 const float* Zc, const float* b1, const float* W2, const float* b2, const int32_t* ctl,
                 const float* fef, bool pairs, float* y, hipStream_t st) {
-  if (pairs && (s.k & 1)) return fail(GNNSHAP_EINVAL, "complement pairs need an even number of rows");
-  const int64_t nrows = pairs ? s.k / 2 : s.k;
-  const int64_t khalf = pairs ? s.k / 2 : 0;
-  const int64_t cblocks = ceil_div(nrows, kBlockRows);
-  if (s.n1 * cblocks > INT32_MAX || s.nfb > 65535) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
-  if (s.n1 > INT32_MAX / 2 || s.M > INT32_MAX / 2) return fail(GNNSHAP_EUNSUPPORTED, "subgraph too large");
-  k_wide_prep<<<1, 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, w.seg, w.spec_ptr, w.spec_e);
-  GS_LAUNCHED();
-  k_wide_zop<<<grid_for(s.units_cap * s.ntot * 64, 256, 16384), 256, 0, st>>>(
-      sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc, s.h, s.ntot, s.units_cap, w.Zop);
+  if (int r = wide_prep(s, w, sg, masks, wpr, Zc, pairs, st)) return r;
+  {
+    GS_TIMED("k_wide_l1", st);
+    if (int r = wide_layer<kProj>(s, sg, masks, wpr, 0, pairs ? s.k / 2 : s.k, pairs, w.Zop, s.ntot, s.nfb, s.h, Zc,
+                                  w.S, w, b1, W2, ctl, nullptr, nullptr, st))
+      return r;
+  }
+  return wide_out(s, w, sg, masks, wpr, s.nfb, b2, ctl, fef, pairs, y, st);
+}
+
+int launch_wide3_prep(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                      int64_t wpr, const float* Zc1, const float* Zc2, bool pairs, hipStream_t st) {
+  if (s.h2 == 0) return fail(GNNSHAP_EINVAL, "not a three-layer shape");
+  if (int r = wide_prep(s, w, sg, masks, wpr, Zc1, pairs, st)) return r;
+  // layer 2's operands: the input rows of the sources outside H_1 (their
+  // degree is 1 under every coalition, so the rows are constant)
+  k_wide_zop<<<grid_for(s.units_cap * s.ntot2 * 64, 256, 16384), 256, 0, st>>>(
+      sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc2, s.h2, s.ntot2, s.units_cap, w.Zop2);
   GS_LAUNCHED();
   if (pairs) {
-    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h,
-                                                                      s.ntot, w.S);
+    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot2), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc2, s.h2,
+                                                                       s.ntot2, w.S2);
     GS_LAUNCHED();
   }
-  k_wide_deg<<<grid_for(nrows * s.n1, 256, 16384), 256, 0, st>>>(masks, wpr, nrows, sg->dst_ptr, s.n1, w.deg);
-  GS_LAUNCHED();
-  {
-    const dim3 grid(static_cast<unsigned>(s.n1 * cblocks), static_cast<unsigned>(s.nfb));
-    GS_TIMED("k_wide_l1", st);
-    if (pairs)
-      k_wide_l1<true><<<grid, kBlockRows, 0, st>>>(masks, wpr, nrows, khalf, cblocks, sg->dst_ptr, sg->edge_src,
-                                                   s.n1, w.seg, w.Zop, s.ntot, s.h, Zc, w.S, w.spec_ptr, w.spec_e,
-                                                   w.deg, b1, W2, s.C, ctl, w.t, s.k);
-    else
-      k_wide_l1<false><<<grid, kBlockRows, 0, st>>>(masks, wpr, nrows, khalf, cblocks, sg->dst_ptr, sg->edge_src,
-                                                    s.n1, w.seg, w.Zop, s.ntot, s.h, Zc, w.S, w.spec_ptr, w.spec_e,
-                                                    w.deg, b1, W2, s.C, ctl, w.t, s.k);
-  }
-  GS_LAUNCHED();
-  {
-    const unsigned g = static_cast<unsigned>(ceil_div(nrows, 256));
-    GS_TIMED("k_wide_out", st);
-    if (pairs)
-      k_wide_out<true><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, s.nfb, s.k, b2,
-                                          ctl, fef, y);
-    else
-      k_wide_out<false><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, s.nfb, s.k, b2,
-                                           ctl, fef, y);
-  }
-  GS_LAUNCHED();
   return GNNSHAP_OK;
+}
+
+int launch_wide3_l1(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                    int64_t wpr, int64_t r0, int64_t nloc, const float* Zc1, const float* b1, bool pairs,
+                    hipStream_t st) {
+  if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
+  GS_TIMED("k_wide_l1", st);
+  return wide_layer<kFull>(s, sg, masks, wpr, r0, nloc, pairs, w.Zop, s.ntot, s.nfb, s.h, Zc1, w.S, w, b1, nullptr,
+                           nullptr, nullptr, w.H1, st);
+}
+
+int launch_wide3_l2(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                    int64_t wpr, int64_t r0, int64_t nloc, const float* b2, const float* W3, const int32_t* ctl,
+                    bool pairs, hipStream_t st) {
+  if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
+  GS_TIMED("k_wide_l2", st);
+  return wide_layer<kProjRows>(s, sg, masks, wpr, r0, nloc, pairs, w.Zop2, s.ntot2, s.nfb2, s.h2, nullptr, w.S2, w,
+                               b2, W3, ctl, w.Z2, nullptr, st);
+}
+
+int launch_wide3_out(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                     int64_t wpr, const float* b3, const int32_t* ctl, const float* fef, bool pairs, float* y,
+                     hipStream_t st) {
+  return wide_out(s, w, sg, masks, wpr, s.nfb2, b3, ctl, fef, pairs, y, st);
 }
 
 }  // namespace gnnshap

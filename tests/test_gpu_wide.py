@@ -1,15 +1,19 @@
-"""GPU parity of the coalition values of two-layer GCNs with a wide hidden
-layer (the fp32-MFMA contraction of layer 1 at the nodes of H_1), against the
-fp64 oracle game (Sec. 3.4, GCN of Sec. 4.2).
+"""GPU parity of the coalition values of two- and three-layer GCNs with wide
+hidden layers on two hops (the MFMA contraction of each layer at the nodes
+of H_1; for three layers the dense transform by W_2 between them), against
+the fp64 oracle game (Sec. 3.4, GCN of Sec. 4.2).
 
 Bar: |y_gpu - y_ref| <= 1e-4 max(|y_ref|, |f(E_c)|, |f(empty)|); rows
 without an in-edge of the target equal the device's f(empty) exactly.
 Cases: hidden widths of 3 to 17 feature tiles (one, two and three feature
-blocks), in-neighbours with hundreds of players (many 64-player windows at
-unaligned offsets), edges between in-neighbours (players whose source has a
-coalition-dependent degree), random biases, arbitrary masks with an odd row
-count through gnnshap_eval_coalitions, and the sampler's complement pairs
-through the single-target and batched explanations (equal bit for bit).
+blocks), two and three layers (layer-2 widths above, equal to and below
+layer 1's), in-neighbours with hundreds of players (many 64-player windows
+at unaligned offsets), edges between in-neighbours (players whose source
+has a coalition-dependent degree), random biases, arbitrary masks with an
+odd row count through gnnshap_eval_coalitions, and the sampler's complement
+pairs through the single-target and batched explanations (equal bit for
+bit).  Several passes over the rows of a three-layer model are covered at
+full size (the ogbn-arxiv-shaped targets of the parity tests).
 """
 import numpy as np
 import pytest
@@ -80,13 +84,16 @@ def _check_y(y_gpu, masks_bool, game, f0, f1, fef_dev, deg_v):
     assert (y_gpu[pruned] == fef_dev[0]).all()
 
 
-WIDTHS = [(48, 5), (64, 3), (128, 41), (272, 7)]
+# hidden widths and classes: two-layer, then three-layer models
+WIDTHS = [((48,), 5), ((64,), 3), ((128,), 41), ((272,), 7),
+          ((48, 64), 5), ((64, 48), 3), ((256, 256), 40), ((80, 272), 7)]
 
 
-@pytest.mark.parametrize("h,C", WIDTHS)
-def test_wide_arbitrary_masks(dev, h, C):
+@pytest.mark.parametrize("hid,C", WIDTHS)
+def test_wide_arbitrary_masks(dev, hid, C):
     """gnnshap_eval_coalitions on random (not complement-paired) masks, odd k."""
-    cfg = _hub_graph(40 + h, 6, 1500, 800, 24, [24, h, C])
+    h = hid[0] if len(hid) == 1 else hid[0] + 3 * hid[-1]   # a seed per model
+    cfg = _hub_graph(40 + h, 6, 1500, 800, 24, [24, *hid, C])
     ex = explainer_for(cfg)
     ex.prepare()
     v = 0
@@ -107,7 +114,7 @@ def test_wide_arbitrary_masks(dev, h, C):
     fef = torch.empty(2, dtype=torch.float32, device=dev)
     cl = torch.empty(1, dtype=torch.int32, device=dev)
     ws = torch.empty(L.gnnshap_eval_workspace(sub.sg, ex.model, k), dtype=torch.uint8, device=dev)
-    _say("wide arbitrary", h, C, M, k)
+    _say("wide arbitrary", hid, C, M, k)
     L.gnnshap_eval_coalitions(sub.sg, ex.model, _vp(ex.X), -1, _vp(masks), k, wpr, _vp(y), _vp(fef), _vp(cl),
                               _vp(ws), ws.numel(), torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
@@ -118,11 +125,12 @@ def test_wide_arbitrary_masks(dev, h, C):
     _check_y(y.cpu().numpy(), mb, game, f0, f1, fe, sub_ref["dst_ptr"][1])
 
 
-@pytest.mark.parametrize("h,C", WIDTHS)
-def test_wide_sampled_pairs_single_and_batch(dev, h, C):
+@pytest.mark.parametrize("hid,C", WIDTHS)
+def test_wide_sampled_pairs_single_and_batch(dev, hid, C):
     """The sampler's complement pairs: every row through explain() and through
     explain_batch (bit-identical), against the oracle."""
-    cfg = _hub_graph(70 + h, 9, 2500, 1500, 20, [20, h, C])
+    h = hid[0] if len(hid) == 1 else hid[0] + 3 * hid[-1]   # a seed per model
+    cfg = _hub_graph(70 + h, 9, 2500, 1500, 20, [20, *hid, C])
     ex = explainer_for(cfg)
     ex.prepare()
     targets = [0, 1, 3]
@@ -133,7 +141,7 @@ def test_wide_sampled_pairs_single_and_batch(dev, h, C):
         M = sub_ref["num_edges"]
         if M < 2:
             continue
-        _say("wide pairs", h, C, v, M)
+        _say("wide pairs", hid, C, v, M)
         r = ex.explain(v, p, seed)
         torch.cuda.synchronize()
         pl = sampler.plan(M, p)
