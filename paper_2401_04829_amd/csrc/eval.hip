@@ -1700,20 +1700,20 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
     return gnnshap::launch_wide(sh.ws, w.wide, sg, masks, sh.wpr, w.Zc[1], b1, m->W[1], b2, w.ctl, f_empty_full,
                                 pairs, y, s);
   }
-  if (ends_ok(sh)) {
-    launch_ends(s, sg, sh.n_dst, sh.nd[1], sh.n_nodes, w.Zc[1], nullptr, m->b ? m->b[0] : nullptr, m->W[1],
-                m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out,
-                f_empty_full);
-    GS_LAUNCHED();
-  } else {
-    if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
-    k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
-    GS_LAUNCHED();
-  }
   if (sh.wide) {
-    // three layers: layer 1 and layer 2 at H_1 as contractions, the dense
-    // transform by W_2 between them, in passes over the rows
+    // three layers.  The end coalitions: layer 1, its transform by W_2, then
+    // layer 2 and the output layer for every class
     const gnnshap::WideShape& ws = sh.ws;
+    if (int st = gnnshap::launch_wide3_ends_l1(ws, w.wide, sg, w.Zc[1], m->b ? m->b[0] : nullptr, s)) return st;
+    if (int st = launch_gemm(s, w.wide.hf, ws.h, nullptr, nullptr, m->W[1], ws.h2, w.wide.z2e, ws.h2, 0, ws.n1 + 1,
+                             ws.h2, ws.h))
+      return st;
+    if (int st = gnnshap::launch_wide3_ends_l2(ws, w.wide, sg, w.Zc[2], m->b ? m->b[1] : nullptr, m->W[2],
+                                               m->b ? m->b[2] : nullptr, target_class, w.sp_y, w.ctl, class_out,
+                                               f_empty_full, s))
+      return st;
+    // every row: layer 1 and layer 2 at H_1 as contractions, the dense
+    // transform by W_2 between them, in passes over the rows
     if (int st = gnnshap::launch_wide3_prep(ws, w.wide, sg, masks, sh.wpr, w.Zc[1], w.Zc[2], pairs, s)) return st;
     const int64_t nrows = pairs ? k / 2 : k;
     for (int64_t r0 = 0; r0 < nrows; r0 += ws.pass) {
@@ -1730,6 +1730,16 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
     }
     return gnnshap::launch_wide3_out(ws, w.wide, sg, masks, sh.wpr, m->b ? m->b[2] : nullptr, w.ctl, f_empty_full,
                                      pairs, y, s);
+  }
+  if (ends_ok(sh)) {
+    launch_ends(s, sg, sh.n_dst, sh.nd[1], sh.n_nodes, w.Zc[1], nullptr, m->b ? m->b[0] : nullptr, m->W[1],
+                m->b ? m->b[1] : nullptr, sh.dims[1], sh.dims[2], w.sp_y, target_class, w.ctl, class_out,
+                f_empty_full);
+    GS_LAUNCHED();
+  } else {
+    if (int st = run_pass(s, sg, m, sh, w, w.sp_masks, w.sp_rows, 0, 2, nullptr, true, nullptr)) return st;
+    k_pick_class<<<1, 1, 0, s>>>(w.sp_y, sh.dims[L], target_class, w.ctl, class_out, f_empty_full);
+    GS_LAUNCHED();
   }
   // Prediction pruning, then the live coalitions in passes of sh.tile rows.
   k_live<<<gnnshap::grid_for(k, 256, 4096), 256, 0, s>>>(masks, sh.wpr, k, sg->dst_ptr, w.ctl, w.live_rows,

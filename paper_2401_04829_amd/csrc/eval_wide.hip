@@ -529,17 +529,20 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
   }
 }
 
-// The two end coalitions (no players, every player), layer 1, partial sums:
-// Hp[p][x][f] = sum over part p of the players entering x (the 64 wavefronts
-// of the kEndParts workgroups of (x, feature block) take players w, w + 64,
-// ...) of d(src)^-1/2 Z[src][f] under E_c (degrees: the players entering each
-// node); lane = feature, the sixteen wavefronts' sums added in a fixed order.
+// The two end coalitions (no players, every player), one layer, partial
+// sums: Hp[p][x][f] = sum over part p of the players entering x (the 64
+// wavefronts of the kEndParts workgroups of (x, feature block) take players
+// w, w + 64, ...) of d(src)^-1/2 Z(src)[f] under E_c (degrees: the players
+// entering each node); Z(u) = Zin[u] for u in H_1, Zc[u] otherwise (layer 1:
+// both X W_1; layer 2 of a three-layer model: H^1 W_2 under E_c, and the
+// constant rows); lane = feature, the sixteen wavefronts' sums added in a
+// fixed order.
 constexpr int kEndParts = 4;
 
 __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict__ dst_ptr,
                                                        const int32_t* __restrict__ edge_src, int64_t n1,
-                                                       const float* __restrict__ Zc, int h,
-                                                       float* __restrict__ Hp) {
+                                                       const float* __restrict__ Zc, const float* __restrict__ Zin,
+                                                       int h, float* __restrict__ Hp) {
   __shared__ float part[16][64];
   const int64_t x = blockIdx.x;
   const int pp = blockIdx.z;
@@ -551,7 +554,7 @@ __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict
   for (int e = e0 + pp * 16 + wave; e < e1; e += 16 * kEndParts) {
     const int32_t u = edge_src[e];
     const float du = u < n1 ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[u + 1] - dst_ptr[u])) : 1.0f;
-    if (fv) acc = fmaf(du, Zc[static_cast<int64_t>(u) * h + f], acc);
+    if (fv) acc = fmaf(du, (u < n1 ? Zin : Zc)[static_cast<int64_t>(u) * h + f], acc);
   }
   part[wave][lane] = acc;
   __syncthreads();
@@ -562,22 +565,24 @@ __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict
   }
 }
 
-// Layer 2 at the target for every class, then the explained class (the
-// requested one, or argmax f(E_c), ties to the lowest index):
+// The end coalitions' layer at H_1 from the parts' sums: Hf[x] at every
+// node of H_1 under E_c (the sums in order, self loop Zself[x], bias, ReLU),
+// Hf[n1] at the target under the empty coalition (its self loop only:
+// Zempty, the target's input row then).  Then, with C > 0 (the last hidden
+// layer), the output layer at the target for every class and the explained
+// class (the requested one, or argmax f(E_c), ties to the lowest index):
 // sp_y[c] = f_c(empty), sp_y[C + c] = f_c(E_c); ctl[0], class_out and
 // f_empty_full as the other evaluation paths write them.  One workgroup of
 // 1024 threads, one wavefront per class at a time (lane = feature).
 __global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restrict__ dst_ptr, int64_t n1,
-                                                        const float* __restrict__ Hp, const float* __restrict__ Zc,
+                                                        const float* __restrict__ Hp, const float* __restrict__ Zself,
+                                                        const float* __restrict__ Zempty,
                                                         const float* __restrict__ b1, int h,
                                                         const float* __restrict__ W2, const float* __restrict__ b2,
                                                         int C, int requested, float* __restrict__ sp_y,
                                                         int32_t* __restrict__ ctl, int32_t* __restrict__ class_out,
                                                         float* __restrict__ f_empty_full, float* __restrict__ Hf) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  // layer 1 under the end coalitions: Hf[x] at every node of H_1 under E_c
-  // (the parts' sums in order, self loop, bias, ReLU), Hf[n1] at the target
-  // under the empty coalition (its self loop only)
   for (int64_t i = threadIdx.x; i < n1 * h; i += blockDim.x) {
     const int64_t x = i / h;
     const int f = static_cast<int>(i % h);
@@ -585,10 +590,10 @@ __global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restric
     for (int q = 0; q < kEndParts; ++q) a += Hp[(static_cast<int64_t>(q) * n1 + x) * h + f];
     const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
     const float bb = b1 ? b1[f] : 0.f;
-    const float zx = Zc[x * h + f];
-    Hf[i] = fmaxf(fmaf(dx, fmaf(dx, zx, a), bb), 0.f);
-    if (x == 0) Hf[n1 * h + f] = fmaxf(zx + bb, 0.f);
+    Hf[i] = fmaxf(fmaf(dx, fmaf(dx, Zself[x * h + f], a), bb), 0.f);
+    if (x == 0) Hf[n1 * h + f] = fmaxf(Zempty[f] + bb, 0.f);
   }
+  if (C == 0) return;
   __syncthreads();
   const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[1] - dst_ptr[0]));
   for (int c = wave; c < C; c += 16) {
@@ -742,10 +747,11 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
   w.S = c.take<float>(s.n1 * s.h);
   w.deg = c.take<int32_t>(s.k * s.n1);
   w.t = c.take<float>(static_cast<int64_t>(s.h2 ? s.nfb2 : s.nfb) * s.k * s.n1);
-  if (s.h2 == 0) {
-    w.hf = c.take<float>((s.n1 + 1) * s.h);
-    w.hp = c.take<float>(kEndParts * s.n1 * s.h);
-  } else {
+  w.hf = c.take<float>((s.n1 + 1) * s.h);
+  w.hp = c.take<float>(kEndParts * s.n1 * std::max(s.h, s.h2));
+  if (s.h2 > 0) {
+    w.z2e = c.take<float>((s.n1 + 1) * s.h2);
+    w.hf2 = c.take<float>((s.n1 + 1) * s.h2);
     w.Zop2 = c.take<uint4>(s.units_cap * s.ntot2 * kParts * 64);
     w.S2 = c.take<float>(s.n1 * s.h2);
     w.H1 = c.take<float>(2 * s.pass * s.n1 * s.h);
@@ -761,10 +767,10 @@ int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph
   {
     GS_TIMED("k_wide_ends", st);
     k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64)), kEndParts), 1024, 0,
-                     st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h, w.hp);
+                     st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, Zc, s.h, w.hp);
     GS_LAUNCHED();
-    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, Zc, b1, s.h, W2, b2, s.C, target_class, sp_y, ctl,
-                                         class_out, f_empty_full, w.hf);
+    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, Zc, Zc, b1, s.h, W2, b2, s.C, target_class, sp_y,
+                                         ctl, class_out, f_empty_full, w.hf);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
@@ -781,6 +787,34 @@ int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg,
       return r;
   }
   return wide_out(s, w, sg, masks, wpr, s.nfb, b2, ctl, fef, pairs, y, st);
+}
+
+int launch_wide3_ends_l1(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const float* Zc1,
+                         const float* b1, hipStream_t st) {
+  if (s.h2 == 0) return fail(GNNSHAP_EINVAL, "not a three-layer shape");
+  if (s.n1 > 65535 * 64) return fail(GNNSHAP_EUNSUPPORTED, "too many nodes in H_1");
+  GS_TIMED("k_wide_ends", st);
+  k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64)), kEndParts), 1024, 0,
+                   st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc1, Zc1, s.h, w.hp);
+  GS_LAUNCHED();
+  k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, Zc1, Zc1, b1, s.h, nullptr, nullptr, 0, -1, nullptr,
+                                       nullptr, nullptr, nullptr, w.hf);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int launch_wide3_ends_l2(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const float* Zc2,
+                         const float* b2, const float* W3, const float* b3, int32_t target_class, float* sp_y,
+                         int32_t* ctl, int32_t* class_out, float* f_empty_full, hipStream_t st) {
+  if (s.h2 == 0) return fail(GNNSHAP_EINVAL, "not a three-layer shape");
+  GS_TIMED("k_wide_ends", st);
+  k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h2, 64)), kEndParts), 1024, 0,
+                   st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc2, w.z2e, s.h2, w.hp);
+  GS_LAUNCHED();
+  k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, w.z2e, w.z2e + s.n1 * s.h2, b2, s.h2, W3, b3, s.C,
+                                       target_class, sp_y, ctl, class_out, f_empty_full, w.hf2);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }
 
 int launch_wide3_prep(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,

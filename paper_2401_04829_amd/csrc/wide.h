@@ -36,8 +36,10 @@ struct WideWs {
   float* S;           // n1 x h: sum of the layer-1 operand rows of each node
   int32_t* deg;       // k x n1: in-degree of each node of H_1 under each evaluated row
   float* t;           // (nfb or nfb2) x k x n1: each node's last hidden output times the explained class's column
-  float* hf;          // two layers: (n1 + 1) x h: layer 1 under the end coalitions
-  float* hp;          // two layers: 4 x n1 x h: partial sums of the players entering each node under E_c
+  float* hf;          // (n1 + 1) x h: layer 1 under the end coalitions (E_c at H_1, then empty at the target)
+  float* hp;          // 4 x n1 x max(h, h2): partial sums of the players entering each node under E_c
+  float* z2e;         // three layers: (n1 + 1) x h2: hf W_2
+  float* hf2;         // three layers: (n1 + 1) x h2: layer 2 under the end coalitions
   uint4* Zop2;        // three layers: units_cap x ntot2 x 3 x 64: layer-2 A operands
   float* S2;          // three layers: n1 x h2
   float* H1;          // three layers: 2 pass x n1 x h: layer 1 of the pass's rows (complements after them)
@@ -60,6 +62,16 @@ int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph
 int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr,
                 const float* Zc, const float* b1, const float* W2, const float* b2, const int32_t* ctl,
                 const float* fef, bool pairs, float* y, hipStream_t st);
+
+// The end coalitions of a three-layer model: launch_wide3_ends_l1 (layer 1
+// into hf), then the caller's z2e = hf W_2, then launch_wide3_ends_l2 (layer
+// 2, the output layer for every class and the explained class, as
+// launch_wide_ends).
+int launch_wide3_ends_l1(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const float* Zc1,
+                         const float* b1, hipStream_t st);
+int launch_wide3_ends_l2(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const float* Zc2,
+                         const float* b2, const float* W3, const float* b3, int32_t target_class, float* sp_y,
+                         int32_t* ctl, int32_t* class_out, float* f_empty_full, hipStream_t st);
 
 // Three-layer model, in the order the caller queues them:
 //   launch_wide3_prep    operand units, player lists, both layers' A
