@@ -210,7 +210,9 @@ __global__ void __launch_bounds__(512) k_transpose_blocked(const uint64_t* __res
 // Counts C[i, j] = sum_rb popcount(T[rb, i] & T[rb, j]) for 64x64 tiles with J >= I,
 // stored in both halves (row stride ld).
 // Row sums of a 64 x 64 count tile (I, J) held 4 x 4 per thread (thread
-// (ty, tx) = (tid / 16, tid % 16) holds rows 4 ty.. and columns 4 tx..),
+// (ty, tx) = (tid / 16, tid % 16) holds rows ty + 16 q and columns tx + 16 r,
+// q, r < 4, so that a wavefront's LDS reads of the tile's words fall on
+// consecutive words: no bank conflicts),
 // added to usum with integer atomics (exact in any order): rows of I get the
 // tile's row sums; for an off-diagonal tile the rows of J get its column
 // sums (the mirrored tile).  Every thread of the workgroup calls it.
@@ -225,7 +227,7 @@ __device__ __forceinline__ void tile_row_sums(const int (&acc)[4][4], int64_t M,
     int rs = acc[q][0] + acc[q][1] + acc[q][2] + acc[q][3];
 #pragma unroll
     for (int off = 8; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 16);
-    const int64_t i = I * 64 + ty * 4 + q;
+    const int64_t i = I * 64 + ty + 16 * q;
     if (tx == 0 && i < M && rs != 0) atomicAdd(reinterpret_cast<unsigned long long*>(&usum[i]),
                                                 static_cast<unsigned long long>(rs));
   }
@@ -233,7 +235,7 @@ __device__ __forceinline__ void tile_row_sums(const int (&acc)[4][4], int64_t M,
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int cs = acc[0][r] + acc[1][r] + acc[2][r] + acc[3][r];
-      if (cs != 0) atomicAdd(&colsum[tx * 4 + r], cs);
+      if (cs != 0) atomicAdd(&colsum[tx + 16 * r], cs);
     }
     __syncthreads();
     const int64_t j = J * 64 + tid;
@@ -280,8 +282,8 @@ __device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_
       uint64_t a[4], b[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        a[q] = Ti[kk][ty * 4 + q];
-        b[q] = Tj[kk][tx * 4 + q];
+        a[q] = Ti[kk][ty + 16 * q];
+        b[q] = Tj[kk][tx + 16 * q];
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -292,11 +294,11 @@ __device__ __forceinline__ void gram_body(const uint64_t* __restrict__ T, int64_
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int64_t i = I * 64 + ty * 4 + q;
+    const int64_t i = I * 64 + ty + 16 * q;
     if (i >= M) continue;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int64_t j = J * 64 + tx * 4 + r;
+      const int64_t j = J * 64 + tx + 16 * r;
       if (j >= M) continue;
       C[i * ld + j] = acc[q][r];
       C[j * ld + i] = acc[q][r];
@@ -343,8 +345,8 @@ __device__ __forceinline__ void gram_part_body(const uint64_t* __restrict__ T, i
       uint64_t a[4], b[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        a[q] = Ti[kk][ty * 4 + q];
-        b[q] = Tj[kk][tx * 4 + q];
+        a[q] = Ti[kk][ty + 16 * q];
+        b[q] = Tj[kk][tx + 16 * q];
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -355,11 +357,11 @@ __device__ __forceinline__ void gram_part_body(const uint64_t* __restrict__ T, i
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int64_t i = I * 64 + ty * 4 + q;
+    const int64_t i = I * 64 + ty + 16 * q;
     if (i >= M) continue;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int64_t j = J * 64 + tx * 4 + r;
+      const int64_t j = J * 64 + tx + 16 * r;
       if (j >= M || acc[q][r] == 0) continue;
       atomicAdd(&C[i * ld + j], acc[q][r]);
       if (I != J) atomicAdd(&C[j * ld + i], acc[q][r]);
