@@ -556,9 +556,10 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
       // stream never waits for a later target) and advances its systems
       // together; the host steps whichever group can move without waiting.
       // Two groups let one group's short passes and launch tails overlap the
-      // other's long passes.  The factored ones are queued on `home` behind
-      // every evaluation.  Both side streams are joined back into `home` at
-      // the end.  A single system runs on `home`.
+      // other's long passes.  The factored ones are queued in full, in turn on
+      // `home` and the two side streams (their chains of short, mostly
+      // latency-bound launches overlap that way).  Both side streams are
+      // joined back into `home` at the end.  A single system runs on `home`.
       auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home) -> int {
         if (rest.empty()) return GNNSHAP_OK;
         constexpr int kPerGroup = 3;
@@ -597,9 +598,17 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
         std::vector<int64_t> its;
         gnnshap::CgGroup on_home;   // stays empty: factored systems are queued in full
         on_home.set_stream(home);
+        // a factored system only takes its group's stream (no member is added)
+        gnnshap::CgGroup* const carrier[3] = {&on_home, &grp[0], &grp[1]};
+        const int ncar = ng == 2 ? 3 : 1;
+        int turn = 0;
         for (int64_t t : rest) {
-          if (plans[t].num_players > gnnshap::iterative_threshold(&plans[t])) its.push_back(t);
-          else if (int st = start(t, &on_home)) return st;
+          if (plans[t].num_players > gnnshap::iterative_threshold(&plans[t])) {
+            its.push_back(t);
+          } else {
+            if (int st = start(t, carrier[turn])) return st;
+            turn = (turn + 1) % ncar;
+          }
         }
         const int cap = ng == 1 ? gnnshap::kCgGroupMax : kPerGroup;
         size_t next = 0;
