@@ -173,3 +173,29 @@ def test_wide_odd_k_rejected_for_sampled_entry(dev):
     with pytest.raises(L.GnnShapError):
         L.gnnshap_eval_sampled_coalitions(sub.sg, ex.model, _vp(ex.X), -1, _vp(masks), k, wpr, _vp(y), _vp(fef),
                                           None, _vp(ws), ws.numel(), torch.cuda.current_stream().cuda_stream)
+
+
+@pytest.mark.parametrize("hid,C", [((48,), 5), ((64, 48), 3)])
+def test_wide_every_source_in_h1(dev, hid, C):
+    """A star (the target and its leaves, edges both ways): every player's
+    source is in H_1, so no node lies outside it and the contraction has no
+    operand rows; all of layer 1 (and layer 2) comes from the epilogue."""
+    n = 40
+    src = list(range(1, n)) + [0] * (n - 1)
+    dst = [0] * (n - 1) + list(range(1, n))
+    indptr, indices = W.in_csr_from_pairs(n, np.array(src), np.array(dst))
+    X = W.gaussian_features(n, 16, 3)
+    Ws, bs = W.glorot_gcn([16, *hid, C], 4, bias="random")
+    cfg = dict(indptr=indptr, indices=indices, X=X, weights=Ws, biases=bs, hops=2)
+    ex = explainer_for(cfg)
+    ex.prepare()
+    sub_ref, game, cls, f0, f1 = _ref(cfg, 0)
+    assert sub_ref["num_nodes"] == sub_ref["dst_ptr"].shape[0] - 1   # no node outside H_1
+    M = sub_ref["num_edges"]
+    p, seed = 3000, 5
+    _say("wide star", hid, C, M)
+    r = ex.explain(0, p, seed)
+    torch.cuda.synchronize()
+    mb, _ = sampler.sample(sampler.plan(M, p), seed, 0)
+    np.testing.assert_array_equal(masks_np(r.masks), sampler.pack(mb))
+    _check_y(r.y.cpu().numpy(), mb, game, f0, f1, r.f_empty_full.cpu().numpy(), sub_ref["dst_ptr"][1])
