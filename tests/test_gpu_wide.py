@@ -199,3 +199,65 @@ def test_wide_every_source_in_h1(dev, hid, C):
     mb, _ = sampler.sample(sampler.plan(M, p), seed, 0)
     np.testing.assert_array_equal(masks_np(r.masks), sampler.pack(mb))
     _check_y(r.y.cpu().numpy(), mb, game, f0, f1, r.f_empty_full.cpu().numpy(), sub_ref["dst_ptr"][1])
+
+
+def _wide_hub300():
+    """Target 0 with 300 in-neighbours (three in-edges each from outside,
+    some edges between them), 512-wide hidden layers: a row of H1 and Z2 for
+    the 301 nodes of H_1 and its complement takes 2.5 MB, so the three-layer
+    path runs in passes of 256 rows."""
+    rng = np.random.default_rng(7)
+    n, n_nb = 2000, 300
+    src, dst = [], []
+    for x in range(1, n_nb + 1):
+        src.append(x)
+        dst.append(0)
+        s = rng.choice(np.arange(n_nb + 1, n), size=3, replace=False)
+        src += s.tolist()
+        dst += [x] * 3
+    for _ in range(20):
+        a, b = rng.choice(np.arange(1, n_nb + 1), size=2, replace=False)
+        src.append(int(a))
+        dst.append(int(b))
+    indptr, indices = W.in_csr_from_pairs(n, np.array(src), np.array(dst))
+    X = W.gaussian_features(n, 16, 8)
+    Ws, bs = W.glorot_gcn([16, 512, 512, 6], 9, bias="random")
+    return dict(indptr=indptr, indices=indices, X=X, weights=Ws, biases=bs, hops=2)
+
+
+def test_wide_three_layers_several_passes(dev):
+    """Three layers over several passes of rows (the last one ragged), with
+    arbitrary masks (1,001 rows: passes 256, 256, 256, 233) and with the
+    sampler's complement pairs (each pass also writes the complements)."""
+    cfg = _wide_hub300()
+    ex = explainer_for(cfg)
+    ex.prepare()
+    sub_ref, game, cls, f0, f1 = _ref(cfg, 0)
+    M = sub_ref["num_edges"]
+    deg_v = sub_ref["dst_ptr"][1]
+    rng = np.random.default_rng(11)
+    k = 1001
+    mb = rng.random((k, M)) < rng.uniform(0.02, 0.98, size=(k, 1))
+    mb[0] = False
+    mb[1] = True
+    masks = torch.from_numpy(sampler.pack(mb).view(np.int64)).to(dev)
+    sub = ex.extract(0)
+    wpr = (M + 63) // 64
+    y = torch.empty(k, dtype=torch.float32, device=dev)
+    fef = torch.empty(2, dtype=torch.float32, device=dev)
+    cl = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(L.gnnshap_eval_workspace(sub.sg, ex.model, k), dtype=torch.uint8, device=dev)
+    _say("wide three layers, arbitrary masks", M, k)
+    L.gnnshap_eval_coalitions(sub.sg, ex.model, _vp(ex.X), -1, _vp(masks), k, wpr, _vp(y), _vp(fef), _vp(cl),
+                              _vp(ws), ws.numel(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert int(cl.item()) == cls
+    fe = fef.cpu().numpy()
+    _check_y(y.cpu().numpy(), mb, game, f0, f1, fe, deg_v)
+    p, seed = 2000, 17
+    _say("wide three layers, complement pairs", M, p)
+    r = ex.explain(0, p, seed)
+    torch.cuda.synchronize()
+    ms, _ = sampler.sample(sampler.plan(M, p), seed, 0)
+    np.testing.assert_array_equal(masks_np(r.masks), sampler.pack(ms))
+    _check_y(r.y.cpu().numpy(), ms, game, f0, f1, r.f_empty_full.cpu().numpy(), deg_v)
