@@ -641,7 +641,9 @@ namespace {
 bool wide_width(int h) { return h > 32 && h % 16 == 0 && h <= 4096; }
 
 // Contracted rows per pass of a three-layer model: H1 and Z2 of a pass's
-// rows and complements fill at most kPassBudget bytes (whole 256-row blocks).
+// rows and complements fill at most kPassBudget bytes, in whole 256-row
+// blocks, and a pass has at least one block (so with thousands of nodes in
+// H_1 the pass arrays exceed the budget).
 constexpr int64_t kPassBudget = int64_t(1) << 30;
 
 // Shared set-up: operand units and player lists, layer-1 operands and sums,
