@@ -91,13 +91,37 @@ struct SolveJob {
   int32_t counts_in;         // 1: G~ is built from the counts as the panel path first reads each block
   int64_t tr0;               // first transpose item (64 rows x 64 players) of the job in the batch
 };
+// A system of the multi-block Cholesky path (more players than one
+// workgroup takes, up to the iterative threshold) in a batch: the batched
+// factorisation and triangular solves run every such system's steps in one
+// launch each (one system per blockIdx.y).
+struct MbJob {
+  float* G;             // M x M, row stride ld: G~, then its Cholesky factor (lower)
+  float* Winv;          // the inverse of the current 128-wide diagonal block
+  float* rhs;           // M: the centred right-hand side, then L^-T x
+  float* x;             // M
+  const double* scal;   // the system's scalars (Delta at [3])
+  float* phi;           // M
+  int32_t* info;
+  int64_t ld, M;
+};
+
 class CgGroup;
 // gnnshap_solve_wls up to the iteration of an iterative system, which joins
 // *grp (a group on `stream`, not full: the caller steps it); other systems
-// are queued in full and grp is left as it was.
+// are queued in full and grp is left as it was.  set_up_only (systems of the
+// multi-block path): only the steps before the factorisation are queued; the
+// caller runs the rest through launch_solve_mb.
 int solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_class* classes, const uint64_t* masks,
                     const float* y, const float* f_empty_full, float* phi, int32_t* info, void* ws, size_t ws_bytes,
-                    void* stream, CgGroup* grp);
+                    void* stream, CgGroup* grp, bool set_up_only = false);
+// Whether a plan's system takes the multi-block Cholesky path, and its job
+// (G, Winv, rhs, x, scal, ld, M from the workspace slice; the caller sets phi, info).
+bool solve_multiblock(const gnnshap_sample_plan* plan);
+int solve_fill_mb_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice, MbJob* job);
+// The factorisation, both triangular solves and phi of n multi-block systems
+// whose set-up has completed on `s` (max_M: their largest M).
+int launch_solve_mb(const MbJob* jobs, int64_t n, int64_t max_M, hipStream_t s);
 // Whether a plan's system is solved by one workgroup, the bytes of its slice, and the job fields it fixes.
 bool solve_batchable(const gnnshap_sample_plan* plan);
 size_t solve_slice_bytes(const gnnshap_sample_plan* plan);

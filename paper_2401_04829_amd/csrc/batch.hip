@@ -266,6 +266,7 @@ struct BatchWs {
   gnnshap::SampleJob* sample;
   gnnshap::EvalJob* eval;
   gnnshap::SolveJob* solve;
+  gnnshap::MbJob* mb;
   std::vector<char*> eval_slice, solve_slice;
 };
 
@@ -275,6 +276,7 @@ BatchWs carve(gnnshap::Carver& c, const Layout& L) {
   b.sample = c.take<gnnshap::SampleJob>(L.n);
   b.eval = c.take<gnnshap::EvalJob>(L.n);
   b.solve = c.take<gnnshap::SolveJob>(L.n);
+  b.mb = c.take<gnnshap::MbJob>(L.n);
   b.eval_slice.resize(L.n);
   b.solve_slice.resize(L.n);
   for (int64_t t = 0; t < L.n; ++t) b.eval_slice[t] = c.take<char>(L.eval_bytes[t]);
@@ -353,11 +355,11 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
   int64_t bound[3];
   split_groups(plans, n, &order, bound);
 
-  // The class tables and the three job tables (in group order) sit at the
+  // The class tables and the four job tables (in group order) sit at the
   // front of the workspace; they are assembled in a host image of that range
   // and copied in one transfer before the first launch.
   char* const base = static_cast<char*>(ws);
-  const size_t front = static_cast<size_t>(reinterpret_cast<char*>(b.solve + n) - base);
+  const size_t front = static_cast<size_t>(reinterpret_cast<char*>(b.mb + n) - base);
   gnnshap::HostStage* stage = gnnshap::host_stage(front, 0);
   if (!stage) return gnnshap::fail(GNNSHAP_EHIP, "page-locked staging allocation failed");
   char* const image = stage->buf;
@@ -367,6 +369,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
   gnnshap::SampleJob* sj = reinterpret_cast<gnnshap::SampleJob*>(at(b.sample));
   gnnshap::EvalJob* ej = reinterpret_cast<gnnshap::EvalJob*>(at(b.eval));
   gnnshap::SolveJob* vj = reinterpret_cast<gnnshap::SolveJob*>(at(b.solve));
+  gnnshap::MbJob* mj = reinterpret_cast<gnnshap::MbJob*>(at(b.mb));
 
   struct Group {
     int64_t begin = 0, end = 0;                      // range of order[]
@@ -379,12 +382,13 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
     int64_t max_panels = 0;                          // of the panel-path systems
     bool small = false;                              // some one-workgroup system
     std::vector<int64_t> rest;                       // targets solved one by one
+    std::vector<int64_t> mb;                         // of them, multi-block systems: their index in the MbJob table, else -1
   } grp[2];
   for (int g = 0; g < 2; ++g) {
     grp[g].begin = bound[g];
     grp[g].end = bound[g + 1];
   }
-  int64_t nv = 0;
+  int64_t nv = 0, nmb = 0;
   int64_t tr_items = 0;   // transpose items (64 rows x 64 players) of the batched systems
   for (Group& G : grp) {
     // 1. sampling jobs
@@ -438,6 +442,15 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
       const gnnshap_sample_plan& p = plans[t];
       if (!gnnshap::solve_batchable(&p)) {
         G.rest.push_back(t);
+        int64_t m = -1;
+        if (gnnshap::solve_multiblock(&p)) {
+          gnnshap::MbJob& J = mj[nmb];
+          if (int st = gnnshap::solve_fill_mb_job(&p, classes + L.class_off[t], b.solve_slice[t], &J)) return st;
+          J.phi = phi + L.player_off[t];
+          J.info = info + t;
+          m = nmb++;
+        }
+        G.mb.push_back(m);
         continue;
       }
       gnnshap::SolveJob J{};
@@ -556,11 +569,16 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
       // stream never waits for a later target) and advances its systems
       // together; the host steps whichever group can move without waiting.
       // Two groups let one group's short passes and launch tails overlap the
-      // other's long passes.  The factored ones are queued in full, in turn on
-      // `home` and the two side streams (their chains of short, mostly
-      // latency-bound launches overlap that way).  Both side streams are
-      // joined back into `home` at the end.  A single system runs on `home`.
-      auto solve_rest = [&](const std::vector<int64_t>& rest, hipStream_t home) -> int {
+      // other's long passes.  The factored ones go in turn to `home` and the
+      // two side streams (their chains of short, mostly latency-bound launches
+      // overlap that way): a one-workgroup system is queued in full; the
+      // multi-block systems in runs of kMbRun, each run's set-ups on one
+      // stream followed by one batched factorisation and solve of the whole
+      // run (launch_solve_mb: one launch per step for all of them instead of
+      // one per system).  Both side streams are joined back into `home` at
+      // the end.  A single system runs on `home`.
+      auto solve_rest = [&](const Group& Gr, hipStream_t home) -> int {
+        const std::vector<int64_t>& rest = Gr.rest;
         if (rest.empty()) return GNNSHAP_OK;
         constexpr int kPerGroup = 3;
         gnnshap::SideStream* side[2] = {nullptr, nullptr};
@@ -583,7 +601,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
           }
           return true;   // complete, or an error that the stream wait reports
         };
-        auto start = [&](int64_t t, gnnshap::CgGroup* g) -> int {
+        auto start = [&](int64_t t, gnnshap::CgGroup* g, bool set_up_only) -> int {
           const hipStream_t st = g->stream();
           if (st != home) {
             // the target's values (and through them its masks) are ready
@@ -593,7 +611,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
           }
           return gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t],
                                           y + L.row_off[t], f_empty_full + 2 * t, phi + L.player_off[t], info + t,
-                                          b.solve_slice[t], L.solve_bytes[t], st, g);
+                                          b.solve_slice[t], L.solve_bytes[t], st, g, set_up_only);
         };
         std::vector<int64_t> its;
         gnnshap::CgGroup on_home;   // stays empty: factored systems are queued in full
@@ -602,14 +620,32 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
         gnnshap::CgGroup* const carrier[3] = {&on_home, &grp[0], &grp[1]};
         const int ncar = ng == 2 ? 3 : 1;
         int turn = 0;
-        for (int64_t t : rest) {
+        constexpr int64_t kMbRun = 24;
+        int64_t run_begin = -1, run_n = 0, run_M = 0;   // the open run of multi-block systems
+        auto close_run = [&]() -> int {
+          if (run_n == 0) return GNNSHAP_OK;
+          if (int st = gnnshap::launch_solve_mb(b.mb + run_begin, run_n, run_M, carrier[turn]->stream())) return st;
+          run_n = 0;
+          run_M = 0;
+          turn = (turn + 1) % ncar;
+          return GNNSHAP_OK;
+        };
+        for (size_t i = 0; i < rest.size(); ++i) {
+          const int64_t t = rest[i];
           if (plans[t].num_players > gnnshap::iterative_threshold(&plans[t])) {
             its.push_back(t);
+          } else if (Gr.mb[i] >= 0) {
+            if (run_n == 0) run_begin = Gr.mb[i];
+            if (int st = start(t, carrier[turn], true)) return st;
+            run_M = std::max<int64_t>(run_M, plans[t].num_players);
+            if (++run_n == kMbRun)
+              if (int st = close_run()) return st;
           } else {
-            if (int st = start(t, carrier[turn])) return st;
-            turn = (turn + 1) % ncar;
+            if (int st = start(t, carrier[turn], false)) return st;
+            if (run_n == 0) turn = (turn + 1) % ncar;
           }
         }
+        if (int st = close_run()) return st;
         const int cap = ng == 1 ? gnnshap::kCgGroupMax : kPerGroup;
         size_t next = 0;
         for (;;) {
@@ -621,7 +657,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
             if (gi < 0) break;
             const int64_t t = its[next];
             if (grp[gi].stream() != home && evaluated[t] && !evaluated_done(t)) break;
-            if (int st = start(t, &grp[gi])) return st;
+            if (int st = start(t, &grp[gi], false)) return st;
             ++next;
             moved = true;
           }
@@ -665,7 +701,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
             if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
           }
         }
-        return solve_rest(G.rest, gs[gi]);
+        return solve_rest(G, gs[gi]);
       };
       // G~ first: it depends on the masks only, and queued ahead of the
       // evaluations it gets the GPU before their many workgroups fill it

@@ -969,8 +969,8 @@ __device__ __forceinline__ void mm64(const float* X, const float* Y, float* D, f
 //   L11 = chol(A11), W11 = L11^-1, L21 = A21 W11^T, A22 -= L21 L21^T,
 //   L22 = chol(A22), W22 = L22^-1, W21 = -W22 (L21 W11).
 // L goes back to the lower part of G, W = L^-1 (zero above the diagonal) to Winv.
-__global__ void __launch_bounds__(256) k_potrf(float* G, int64_t ld, int64_t M, int64_t o, int32_t* info,
-                                               float* __restrict__ Winv) {
+__device__ __forceinline__ void k_potrf_body(float* G, int64_t ld, int64_t M, int64_t o, int32_t* info,
+                                             float* __restrict__ Winv) {
   extern __shared__ __align__(16) unsigned char smem[];
   float* S0 = reinterpret_cast<float*>(smem);  // A11 -> L11, later L21 W11
   float* S1 = S0 + kHB;                        // W11
@@ -1023,6 +1023,11 @@ __global__ void __launch_bounds__(256) k_potrf(float* G, int64_t ld, int64_t M, 
     else v = c < 64 ? S2[(r - 64) * kHP + c] : S4[(r - 64) * kHP + c - 64];
     Winv[t] = v;
   }
+}
+
+__global__ void __launch_bounds__(256) k_potrf(float* G, int64_t ld, int64_t M, int64_t o, int32_t* info,
+                                               float* __restrict__ Winv) {
+  k_potrf_body(G, ld, M, o, info, Winv);
 }
 
 // ---- one-workgroup path (systems of up to kMidMax players) --------------------------------
@@ -1292,12 +1297,12 @@ constexpr int kGP = kGK + 4;    // LDS row pitch (floats)
 // tiles with J <= I (diagonal tiles written whole).  A may alias C when one
 // tile column covers all of n (the tile reads its rows before writing them).
 template <bool kLower>
-__global__ void __launch_bounds__(256) k_gemm_nt(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
-                                                 int64_t ldc, int64_t m, int64_t n, int64_t K, float alpha,
-                                                 float beta, int64_t tiles_n) {
+__device__ __forceinline__ void k_gemm_nt_body(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
+                                               int64_t ldc, int64_t m, int64_t n, int64_t K, float alpha,
+                                               float beta, int64_t tiles_n, int64_t bx) {
   __shared__ __align__(16) float As[kGT * kGP];
   __shared__ __align__(16) float Bs[kGT * kGP];
-  const int64_t t = blockIdx.x;
+  const int64_t t = bx;
   int64_t I, J;
   if (kLower) {
     I = static_cast<int64_t>((sqrt(8.0 * static_cast<double>(t) + 1.0) - 1.0) * 0.5);
@@ -1362,6 +1367,13 @@ __global__ void __launch_bounds__(256) k_gemm_nt(const float* A, int64_t lda, co
     }
 }
 
+template <bool kLower>
+__global__ void __launch_bounds__(256) k_gemm_nt(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
+                                                 int64_t ldc, int64_t m, int64_t n, int64_t K, float alpha,
+                                                 float beta, int64_t tiles_n) {
+  k_gemm_nt_body<kLower>(A, lda, B, ldb, C, ldc, m, n, K, alpha, beta, tiles_n, blockIdx.x);
+}
+
 // ---- multi-block path: triangular solves ------------------------------------------------
 //
 // Segments [s0, s1) of at most kSeg rows: one workgroup loads the segment's
@@ -1399,8 +1411,8 @@ __device__ __forceinline__ void load_segment(const float* __restrict__ G, int64_
 }
 
 // Forward: x[s0:s1) = L[s0:s1, s0:s1)^-1 rhs[s0:s1) (rhs holds the earlier segments' updates).
-__global__ void __launch_bounds__(1024) k_trsv_fwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
-                                                   const float* __restrict__ rhs, float* __restrict__ x) {
+__device__ __forceinline__ void k_trsv_fwd_body(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                const float* __restrict__ rhs, float* __restrict__ x) {
   extern __shared__ __align__(16) unsigned char smem[];
   float* Ls = reinterpret_cast<float*>(smem);
   float* rd = Ls + kSeg * (kSeg + 1) / 2;
@@ -1436,11 +1448,16 @@ __global__ void __launch_bounds__(1024) k_trsv_fwd(const float* __restrict__ G, 
   for (int64_t t = tid; t < len; t += blockDim.x) x[s0 + t] = v[t];
 }
 
+__global__ void __launch_bounds__(1024) k_trsv_fwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                   const float* __restrict__ rhs, float* __restrict__ x) {
+  k_trsv_fwd_body(G, ld, s0, s1, rhs, x);
+}
+
 // rhs[i] -= L[i, s0:s1) x[s0:s1) for i >= s1; one wavefront per row, four floats per lane.
-__global__ void __launch_bounds__(256) k_gemv_fwd(const float* __restrict__ G, int64_t ld, int64_t M, int64_t s0,
-                                                  int64_t s1, const float* __restrict__ x, float* __restrict__ rhs) {
+__device__ __forceinline__ void k_gemv_fwd_body(const float* __restrict__ G, int64_t ld, int64_t M, int64_t s0,
+                                                int64_t s1, const float* __restrict__ x, float* __restrict__ rhs, int64_t bx) {
   const int lane = threadIdx.x & 63;
-  const int64_t i = s1 + ((static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6);
+  const int64_t i = s1 + ((static_cast<int64_t>(bx) * blockDim.x + threadIdx.x) >> 6);
   if (i >= M) return;
   float acc = 0.f;
   for (int64_t c = s0 + 4 * lane; c < s1; c += 256) {
@@ -1456,9 +1473,14 @@ __global__ void __launch_bounds__(256) k_gemv_fwd(const float* __restrict__ G, i
   if (lane == 0) rhs[i] -= acc;
 }
 
+__global__ void __launch_bounds__(256) k_gemv_fwd(const float* __restrict__ G, int64_t ld, int64_t M, int64_t s0,
+                                                  int64_t s1, const float* __restrict__ x, float* __restrict__ rhs) {
+  k_gemv_fwd_body(G, ld, M, s0, s1, x, rhs, blockIdx.x);
+}
+
 // Backward: z[s0:s1) = L[s0:s1, s0:s1)^-T x[s0:s1) into rhs (x holds the later segments' updates).
-__global__ void __launch_bounds__(1024) k_trsv_bwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
-                                                   const float* __restrict__ x, float* __restrict__ rhs) {
+__device__ __forceinline__ void k_trsv_bwd_body(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                const float* __restrict__ x, float* __restrict__ rhs) {
   extern __shared__ __align__(16) unsigned char smem[];
   float* Ls = reinterpret_cast<float*>(smem);
   float* rd = Ls + kSeg * (kSeg + 1) / 2;
@@ -1494,13 +1516,18 @@ __global__ void __launch_bounds__(1024) k_trsv_bwd(const float* __restrict__ G, 
   for (int64_t t = tid; t < len; t += blockDim.x) rhs[s0 + t] = v[t];
 }
 
+__global__ void __launch_bounds__(1024) k_trsv_bwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                   const float* __restrict__ x, float* __restrict__ rhs) {
+  k_trsv_bwd_body(G, ld, s0, s1, x, rhs);
+}
+
 // x[i] -= sum_{c in [s0, s1)} L[c, i] z[c] for i < s0: 64 rows i per block
 // (coalesced over i), the segment split over four thread groups.
-__global__ void __launch_bounds__(256) k_gemv_bwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
-                                                  const float* __restrict__ z, float* __restrict__ x) {
+__device__ __forceinline__ void k_gemv_bwd_body(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                const float* __restrict__ z, float* __restrict__ x, int64_t bx) {
   __shared__ float red[4][64];
   const int il = threadIdx.x & 63, g = threadIdx.x >> 6;
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 64 + il;
+  const int64_t i = static_cast<int64_t>(bx) * 64 + il;
   float acc = 0.f;
   if (i < s0) {
 #pragma unroll 8
@@ -1511,12 +1538,89 @@ __global__ void __launch_bounds__(256) k_gemv_bwd(const float* __restrict__ G, i
   if (g == 0 && i < s0) x[i] -= (red[0][il] + red[1][il]) + (red[2][il] + red[3][il]);
 }
 
+__global__ void __launch_bounds__(256) k_gemv_bwd(const float* __restrict__ G, int64_t ld, int64_t s0, int64_t s1,
+                                                  const float* __restrict__ z, float* __restrict__ x) {
+  k_gemv_bwd_body(G, ld, s0, s1, z, x, blockIdx.x);
+}
+
+__device__ __forceinline__ void k_finish_body(const float* __restrict__ z, int64_t M, const double* __restrict__ scal,
+                                              float* __restrict__ phi, int64_t bx, int64_t gx) {
+  const double base = scal[3] / static_cast<double>(M);
+  for (int64_t i = static_cast<int64_t>(bx) * blockDim.x + threadIdx.x; i < M;
+       i += static_cast<int64_t>(gx) * blockDim.x)
+    phi[i] = static_cast<float>(base + static_cast<double>(z[i]));
+}
+
 __global__ void k_finish(const float* __restrict__ z, int64_t M, const double* __restrict__ scal,
                          float* __restrict__ phi) {
-  const double base = scal[3] / static_cast<double>(M);
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < M;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    phi[i] = static_cast<float>(base + static_cast<double>(z[i]));
+  k_finish_body(z, M, scal, phi, blockIdx.x, gridDim.x);
+}
+
+// ---- multi-block path, batched: one system per blockIdx.y ---------------------------------
+//
+// Every launch covers the step of the largest system; a system whose M ends
+// before the step returns at once (whole workgroups, before any barrier), so
+// each system sees exactly the launches, grids and arguments it would see
+// alone and its factor and phi are the same bits.
+
+__global__ void __launch_bounds__(256) k_potrf_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t o) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  if (o >= J.M) return;
+  k_potrf_body(J.G, J.ld, J.M, o, J.info, J.Winv);
+}
+
+// panel <- panel W^T (the off-diagonal blocks of the step's 128 columns)
+__global__ void __launch_bounds__(256) k_trsm_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t o) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  const int64_t r0 = o + kPB;
+  if (r0 >= J.M) return;
+  const int64_t rows = J.M - r0;
+  if (static_cast<int64_t>(blockIdx.x) >= (rows + kGT - 1) / kGT) return;
+  float* panel = J.G + r0 * J.ld + o;
+  k_gemm_nt_body<false>(panel, J.ld, J.Winv, kPB, panel, J.ld, rows, kPB, kPB, 1.f, 0.f, 1, blockIdx.x);
+}
+
+// trailing lower triangle -= panel panel^T
+__global__ void __launch_bounds__(256) k_syrk_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t o) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  const int64_t r0 = o + kPB;
+  if (r0 >= J.M) return;
+  const int64_t rows = J.M - r0;
+  const int64_t tr = (rows + kGT - 1) / kGT;
+  if (static_cast<int64_t>(blockIdx.x) >= tr * (tr + 1) / 2) return;
+  const float* panel = J.G + r0 * J.ld + o;
+  k_gemm_nt_body<true>(panel, J.ld, panel, J.ld, J.G + r0 * J.ld + r0, J.ld, rows, rows, kPB, -1.f, 1.f, 0,
+                       blockIdx.x);
+}
+
+__global__ void __launch_bounds__(1024) k_trsv_fwd_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t s0) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  if (s0 >= J.M) return;
+  k_trsv_fwd_body(J.G, J.ld, s0, J.M < s0 + kSeg ? J.M : s0 + kSeg, J.rhs, J.x);
+}
+
+__global__ void __launch_bounds__(256) k_gemv_fwd_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t s0) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  const int64_t s1 = s0 + kSeg;
+  if (s1 >= J.M) return;
+  k_gemv_fwd_body(J.G, J.ld, J.M, s0, s1, J.x, J.rhs, blockIdx.x);
+}
+
+__global__ void __launch_bounds__(1024) k_trsv_bwd_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t s0) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  if (s0 >= J.M) return;
+  k_trsv_bwd_body(J.G, J.ld, s0, J.M < s0 + kSeg ? J.M : s0 + kSeg, J.x, J.rhs);
+}
+
+__global__ void __launch_bounds__(256) k_gemv_bwd_mb(const gnnshap::MbJob* __restrict__ jobs, int64_t s0) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  if (s0 >= J.M) return;
+  k_gemv_bwd_body(J.G, J.ld, s0, J.M < s0 + kSeg ? J.M : s0 + kSeg, J.rhs, J.x, blockIdx.x);
+}
+
+__global__ void k_finish_mb(const gnnshap::MbJob* __restrict__ jobs) {
+  const gnnshap::MbJob J = jobs[blockIdx.y];
+  k_finish_body(J.rhs, J.M, J.scal, J.phi, blockIdx.x, gridDim.x);
 }
 
 int check_plan(const gnnshap_sample_plan* p, const gnnshap_class* classes) {
@@ -1972,12 +2076,23 @@ extern "C" int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* 
   return GNNSHAP_OK;
 }
 
+namespace {
+
+// Whether a factored system of M players is solved by one workgroup (its
+// system in LDS) rather than by the multi-block Cholesky.
+bool takes_mid(int64_t M) {
+  static bool mid_lds = false;
+  return M <= kMidMax && allow_lds(reinterpret_cast<const void*>(&k_solve_mid), kMidLds, mid_lds);
+}
+
+}  // namespace
+
 // gnnshap_solve_wls up to the iteration of an iterative solve, whose system
 // joins *grp (its set-up queued on the group's stream, which must be
 // `stream`); other systems are queued in full and grp is left as it was.
 int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_class* classes, const uint64_t* masks,
                              const float* y, const float* f_empty_full, float* phi, int32_t* info, void* ws,
-                             size_t ws_bytes, void* stream, CgGroup* grp) {
+                             size_t ws_bytes, void* stream, CgGroup* grp, bool set_up_only) {
   GS_TRY_BEGIN
   gnnshap::clear_error();
   if (!classes || !masks || !y || !f_empty_full || !phi || !info || !ws)
@@ -2007,6 +2122,7 @@ int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_clas
   }
   GS_HIP(hipMemcpyAsync(w.classes, classes, plan->num_classes * sizeof(gnnshap_class), hipMemcpyHostToDevice, s));
   if (iterative(plan)) {
+    if (set_up_only) return gnnshap::fail(GNNSHAP_EINVAL, "only a multi-block system is set up alone");
     // R as bit-transposed rows (the product R p), the right-hand side, then
     // conjugate gradients straight from the bits
     if (has_random) {
@@ -2073,8 +2189,8 @@ int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_clas
     }
     GS_LAUNCHED();
   }
-  static bool mid_lds = false;
-  const bool mid = M <= kMidMax && allow_lds(reinterpret_cast<const void*>(&k_solve_mid), kMidLds, mid_lds);
+  const bool mid = takes_mid(M);
+  if (set_up_only && mid) return gnnshap::fail(GNNSHAP_EINVAL, "only a multi-block system is set up alone");
   const bool tiled = mid && rhs_tiled(M, plan->num_classes);
   const int64_t nch = tiled ? tile_chunks(half) : n_chunks(half, wpr);
   if (tiled) {
@@ -2165,6 +2281,7 @@ int gnnshap::solve_wls_start(const gnnshap_sample_plan* plan, const gnnshap_clas
   GS_LAUNCHED();
   k_rhs_center<<<static_cast<unsigned>(nbm), 256, 0, s>>>(w.dv, w.bsum, nbm, M, w.rhs);
   GS_LAUNCHED();
+  if (set_up_only) return GNNSHAP_OK;   // the rest runs batched (launch_solve_mb)
   for (int64_t o = 0; o < M; o += kPB) {
     {
       GS_TIMED("k_potrf", s);
@@ -2291,6 +2408,87 @@ int gnnshap::solve_fill_job(const gnnshap_sample_plan* plan, const gnnshap_class
 
 bool gnnshap::solve_panel_path(const gnnshap_sample_plan* plan) {
   return solve_batchable(plan) && plan->num_players > kPanelMin;
+}
+
+bool gnnshap::solve_multiblock(const gnnshap_sample_plan* plan) {
+  if (check_plan(plan, nullptr) != GNNSHAP_OK) {
+    clear_error();
+    return false;
+  }
+  return !iterative(plan) && !takes_mid(plan->num_players);
+}
+
+int gnnshap::solve_fill_mb_job(const gnnshap_sample_plan* plan, const gnnshap_class* classes, void* slice,
+                               MbJob* job) {
+  if (int st = check_plan(plan, classes)) return st;
+  if (!solve_multiblock(plan)) return fail(GNNSHAP_EINVAL, "system does not take the multi-block path");
+  Carver c(slice);
+  const Ws w = carve(c, plan, classes);
+  job->G = w.G;
+  job->Winv = w.Winv;
+  job->rhs = w.rhs;
+  job->x = w.x;
+  job->scal = w.scal;
+  job->ld = ld_of(plan->num_players);
+  job->M = plan->num_players;
+  return GNNSHAP_OK;
+}
+
+int gnnshap::launch_solve_mb(const MbJob* jobs, int64_t n, int64_t max_M, hipStream_t s) {
+  if (n < 1) return GNNSHAP_OK;
+  if (n > 65535) return fail(GNNSHAP_EUNSUPPORTED, "at most 65535 multi-block systems per launch");
+  static bool potrf_lds = false, fwd_lds = false, bwd_lds = false;
+  if (!allow_lds(reinterpret_cast<const void*>(&k_potrf_mb), kPotrfLds, potrf_lds) ||
+      !allow_lds(reinterpret_cast<const void*>(&k_trsv_fwd_mb), kTrsvLds, fwd_lds) ||
+      !allow_lds(reinterpret_cast<const void*>(&k_trsv_bwd_mb), kTrsvLds, bwd_lds))
+    return fail(GNNSHAP_EHIP, "device cannot give the solver %zu bytes of LDS", kTrsvLds);
+  const unsigned nn = static_cast<unsigned>(n);
+  for (int64_t o = 0; o < max_M; o += kPB) {
+    {
+      GS_TIMED("k_potrf_mb", s);
+      k_potrf_mb<<<dim3(1, nn), 256, kPotrfLds, s>>>(jobs, o);
+    }
+    GS_LAUNCHED();
+    const int64_t r0 = o + kPB;
+    if (r0 >= max_M) break;
+    const int64_t tr = ceil_div(max_M - r0, kGT);
+    {
+      GS_TIMED("k_trsm_mb", s);
+      k_trsm_mb<<<dim3(static_cast<unsigned>(tr), nn), 256, 0, s>>>(jobs, o);
+    }
+    GS_LAUNCHED();
+    {
+      GS_TIMED("k_syrk_mb", s);
+      k_syrk_mb<<<dim3(static_cast<unsigned>(tr * (tr + 1) / 2), nn), 256, 0, s>>>(jobs, o);
+    }
+    GS_LAUNCHED();
+  }
+  for (int64_t s0 = 0; s0 < max_M; s0 += kSeg) {
+    {
+      GS_TIMED("k_trsv_mb", s);
+      k_trsv_fwd_mb<<<dim3(1, nn), 1024, kTrsvLds, s>>>(jobs, s0);
+    }
+    GS_LAUNCHED();
+    const int64_t s1 = std::min(max_M, s0 + kSeg);
+    if (s1 < max_M) {
+      k_gemv_fwd_mb<<<dim3(static_cast<unsigned>(ceil_div((max_M - s1) * 64, 256)), nn), 256, 0, s>>>(jobs, s0);
+      GS_LAUNCHED();
+    }
+  }
+  for (int64_t s0 = ((max_M - 1) / kSeg) * kSeg; s0 >= 0; s0 -= kSeg) {
+    {
+      GS_TIMED("k_trsv_mb", s);
+      k_trsv_bwd_mb<<<dim3(1, nn), 1024, kTrsvLds, s>>>(jobs, s0);
+    }
+    GS_LAUNCHED();
+    if (s0 > 0) {
+      k_gemv_bwd_mb<<<dim3(static_cast<unsigned>(ceil_div(s0, 64)), nn), 256, 0, s>>>(jobs, s0);
+      GS_LAUNCHED();
+    }
+  }
+  k_finish_mb<<<dim3(grid_for(max_M, 256, 1024), nn), 256, 0, s>>>(jobs);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }
 
 int gnnshap::launch_solve_matrix(const SolveJob* jobs, int64_t n, int64_t max_M, int64_t max_wpr, int64_t max_nrb,
