@@ -389,6 +389,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
     grp[g].end = bound[g + 1];
   }
   int64_t nv = 0, nmb = 0;
+  std::vector<int64_t> rest_pos(static_cast<size_t>(n), -1);   // index of a target in its group's rest list
   int64_t tr_items = 0;   // transpose items (64 rows x 64 players) of the batched systems
   for (Group& G : grp) {
     // 1. sampling jobs
@@ -441,6 +442,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
       const int64_t t = order[j];
       const gnnshap_sample_plan& p = plans[t];
       if (!gnnshap::solve_batchable(&p)) {
+        rest_pos[t] = static_cast<int64_t>(G.rest.size());
         G.rest.push_back(t);
         int64_t m = -1;
         if (gnnshap::solve_multiblock(&p)) {
@@ -518,12 +520,150 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
         if (side0) GS_HIP(hipStreamWaitEvent(side0->stream, f->fork, 0));
         if (mat) GS_HIP(hipStreamWaitEvent(mat->stream, f->fork, 0));
       }
-      // coalition values of group gi; evaluated[t] is an event recorded on the
-      // group's stream once target t's values are there (so that its solve
-      // can start on another stream while later targets are evaluated)
       hipEvent_t* ev_pool = gnnshap::event_pool(static_cast<size_t>(n));
       if (!ev_pool) return gnnshap::fail(GNNSHAP_EHIP, "could not create events");
       std::vector<hipEvent_t> evaluated(static_cast<size_t>(n), nullptr);
+      // The systems solved one by one (too large for the batched kernels).
+      // The factored ones are queued as soon as their values are queued (from
+      // eval_group, target by target), in turn on the two side streams, so
+      // that they run beside the evaluation of later targets: a
+      // one-workgroup system in full; the multi-block systems in runs of
+      // kMbRun, each run's set-ups on one stream followed by one batched
+      // factorisation and solve of the whole run (launch_solve_mb: one launch
+      // per step for all of them instead of one per system).  The iterative
+      // ones go to two solver groups, one on each side stream, each holding up
+      // to kPerGroup systems: a group takes a system once its values are there
+      // (a host query of its evaluation event, so a side stream never waits
+      // for a later target) and advances its systems together; the host steps
+      // whichever group can move without waiting.  Two groups let one group's
+      // short passes and launch tails overlap the other's long passes.  Both
+      // side streams are joined back into `home` at the end.  A single system
+      // runs on `home`.
+      struct Rest {
+        hipStream_t home = nullptr;
+        gnnshap::SideStream* side[2] = {nullptr, nullptr};
+        gnnshap::CgGroup cg[2];
+        gnnshap::CgGroup on_home;     // stays empty: factored systems are queued in full
+        int ng = 0;                   // solver groups (0: not opened)
+        int turn = 0;                 // carrier of the next factored system or run
+        int64_t run_begin = -1, run_n = 0, run_M = 0;   // the open run of multi-block systems
+        size_t taken = 0;             // rest[0, taken) queued or listed in its
+        std::vector<int64_t> its;     // iterative systems, in order
+      };
+      Rest rst[2];
+      constexpr int kPerGroup = 3;
+      constexpr int64_t kMbRun = 24;
+      auto rest_open = [&](int gi, hipStream_t home) -> int {
+        Rest& R = rst[gi];
+        const std::vector<int64_t>& rest = grp[gi].rest;
+        R.home = home;
+        R.on_home.set_stream(home);
+        R.ng = 1;
+        R.cg[0].set_stream(home);
+        if (rest.size() >= 2) {
+          for (int i = 0; i < 2; ++i) {
+            R.side[i] = gnnshap::side_stream(i);
+            if (!R.side[i]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
+            R.cg[i].set_stream(R.side[i]->stream);
+          }
+          R.ng = 2;
+        }
+        return GNNSHAP_OK;
+      };
+      auto rest_start = [&](Rest& R, int64_t t, gnnshap::CgGroup* g, bool set_up_only) -> int {
+        const hipStream_t st = g->stream();
+        if (st != R.home) {
+          // the target's values (and through them its masks) are ready
+          if (!evaluated[t]) return gnnshap::fail(GNNSHAP_EHIP, "target %lld has no evaluation event",
+                                                  static_cast<long long>(t));
+          GS_HIP(hipStreamWaitEvent(st, evaluated[t], 0));
+        }
+        return gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t], y + L.row_off[t],
+                                        f_empty_full + 2 * t, phi + L.player_off[t], info + t, b.solve_slice[t],
+                                        L.solve_bytes[t], st, g, set_up_only);
+      };
+      // a factored system only takes its carrier's stream (no member is added)
+      auto carrier = [&](Rest& R) -> gnnshap::CgGroup* { return R.ng == 2 ? &R.cg[R.turn] : &R.on_home; };
+      auto close_run = [&](Rest& R) -> int {
+        if (R.run_n == 0) return GNNSHAP_OK;
+        if (int st = gnnshap::launch_solve_mb(b.mb + R.run_begin, R.run_n, R.run_M, carrier(R)->stream())) return st;
+        R.run_n = 0;
+        R.run_M = 0;
+        R.turn ^= R.ng == 2 ? 1 : 0;
+        return GNNSHAP_OK;
+      };
+      // queue the factored systems of rest[taken, upto) (their values are queued)
+      auto rest_take = [&](int gi, size_t upto) -> int {
+        Rest& R = rst[gi];
+        const Group& Gr = grp[gi];
+        for (; R.taken < upto; ++R.taken) {
+          const size_t i = R.taken;
+          const int64_t t = Gr.rest[i];
+          if (plans[t].num_players > gnnshap::iterative_threshold(&plans[t])) {
+            R.its.push_back(t);
+          } else if (Gr.mb[i] >= 0) {
+            if (R.run_n == 0) R.run_begin = Gr.mb[i];
+            if (int st = rest_start(R, t, carrier(R), true)) return st;
+            R.run_M = std::max<int64_t>(R.run_M, plans[t].num_players);
+            if (++R.run_n == kMbRun)
+              if (int st = close_run(R)) return st;
+          } else {
+            if (int st = rest_start(R, t, carrier(R), false)) return st;
+            if (R.run_n == 0) R.turn ^= R.ng == 2 ? 1 : 0;
+          }
+        }
+        return GNNSHAP_OK;
+      };
+      auto rest_finish = [&](int gi) -> int {
+        Rest& R = rst[gi];
+        if (grp[gi].rest.empty()) return GNNSHAP_OK;
+        if (int st = rest_take(gi, grp[gi].rest.size())) return st;
+        if (int st = close_run(R)) return st;
+        auto evaluated_done = [&](int64_t t) {
+          const hipError_t q = hipEventQuery(evaluated[t]);
+          if (q == hipErrorNotReady) {
+            (void)hipGetLastError();
+            return false;
+          }
+          return true;   // complete, or an error that the stream wait reports
+        };
+        const int ng = R.ng;
+        const int cap = ng == 1 ? gnnshap::kCgGroupMax : kPerGroup;
+        size_t next = 0;
+        for (;;) {
+          bool moved = false, busy = false;
+          while (next < R.its.size()) {
+            int gi2 = -1;
+            for (int i = 0; i < ng; ++i)
+              if (R.cg[i].size() < cap && (gi2 < 0 || R.cg[i].size() < R.cg[gi2].size())) gi2 = i;
+            if (gi2 < 0) break;
+            const int64_t t = R.its[next];
+            if (R.cg[gi2].stream() != R.home && evaluated[t] && !evaluated_done(t)) break;
+            if (int st = rest_start(R, t, &R.cg[gi2], false)) return st;
+            ++next;
+            moved = true;
+          }
+          for (int i = 0; i < ng; ++i) {
+            if (R.cg[i].empty()) continue;
+            busy = true;
+            if (!R.cg[i].ready()) continue;
+            if (int st = R.cg[i].step()) return st;
+            moved = true;
+          }
+          if (!busy && next >= R.its.size()) break;
+          if (!moved) std::this_thread::sleep_for(std::chrono::microseconds(20));
+        }
+        for (int i = 0; i < 2; ++i) {
+          if (!R.side[i]) continue;
+          GS_HIP(hipEventRecord(R.side[i]->rest_out, R.side[i]->stream));
+          GS_HIP(hipStreamWaitEvent(R.home, R.side[i]->rest_out, 0));
+        }
+        return GNNSHAP_OK;
+      };
+      // coalition values of group gi; evaluated[t] is an event recorded on the
+      // group's stream once target t's values are there (so that its solve
+      // can start on another stream while later targets are evaluated, and
+      // is queued right away)
       auto eval_group = [&](int gi) -> int {
         const Group& G = grp[gi];
         if (G.end == G.begin) return GNNSHAP_OK;
@@ -558,123 +698,9 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
             }
             GS_HIP(hipEventRecord(ev_pool[j], gs[gi]));
             evaluated[t] = ev_pool[j];
+            if (rest_pos[t] >= 0)
+              if (int st = rest_take(gi, static_cast<size_t>(rest_pos[t]) + 1)) return st;
           }
-        }
-        return GNNSHAP_OK;
-      };
-      // The systems solved one by one (too large for the batched kernels).
-      // The iterative ones go to two solver groups, one on each side stream,
-      // each holding up to kPerGroup systems: a group takes a system once its
-      // values are there (a host query of its evaluation event, so a side
-      // stream never waits for a later target) and advances its systems
-      // together; the host steps whichever group can move without waiting.
-      // Two groups let one group's short passes and launch tails overlap the
-      // other's long passes.  The factored ones go in turn to `home` and the
-      // two side streams (their chains of short, mostly latency-bound launches
-      // overlap that way): a one-workgroup system is queued in full; the
-      // multi-block systems in runs of kMbRun, each run's set-ups on one
-      // stream followed by one batched factorisation and solve of the whole
-      // run (launch_solve_mb: one launch per step for all of them instead of
-      // one per system).  Both side streams are joined back into `home` at
-      // the end.  A single system runs on `home`.
-      auto solve_rest = [&](const Group& Gr, hipStream_t home) -> int {
-        const std::vector<int64_t>& rest = Gr.rest;
-        if (rest.empty()) return GNNSHAP_OK;
-        constexpr int kPerGroup = 3;
-        gnnshap::SideStream* side[2] = {nullptr, nullptr};
-        gnnshap::CgGroup grp[2];
-        int ng = 1;
-        grp[0].set_stream(home);
-        if (rest.size() >= 2) {
-          for (int i = 0; i < 2; ++i) {
-            side[i] = gnnshap::side_stream(i);
-            if (!side[i]) return gnnshap::fail(GNNSHAP_EHIP, "could not create a side stream");
-            grp[i].set_stream(side[i]->stream);
-          }
-          ng = 2;
-        }
-        auto evaluated_done = [&](int64_t t) {
-          const hipError_t q = hipEventQuery(evaluated[t]);
-          if (q == hipErrorNotReady) {
-            (void)hipGetLastError();
-            return false;
-          }
-          return true;   // complete, or an error that the stream wait reports
-        };
-        auto start = [&](int64_t t, gnnshap::CgGroup* g, bool set_up_only) -> int {
-          const hipStream_t st = g->stream();
-          if (st != home) {
-            // the target's values (and through them its masks) are ready
-            if (!evaluated[t]) return gnnshap::fail(GNNSHAP_EHIP, "target %lld has no evaluation event",
-                                                    static_cast<long long>(t));
-            GS_HIP(hipStreamWaitEvent(st, evaluated[t], 0));
-          }
-          return gnnshap::solve_wls_start(&plans[t], classes + L.class_off[t], masks + L.mask_off[t],
-                                          y + L.row_off[t], f_empty_full + 2 * t, phi + L.player_off[t], info + t,
-                                          b.solve_slice[t], L.solve_bytes[t], st, g, set_up_only);
-        };
-        std::vector<int64_t> its;
-        gnnshap::CgGroup on_home;   // stays empty: factored systems are queued in full
-        on_home.set_stream(home);
-        // a factored system only takes its group's stream (no member is added)
-        gnnshap::CgGroup* const carrier[3] = {&on_home, &grp[0], &grp[1]};
-        const int ncar = ng == 2 ? 3 : 1;
-        int turn = 0;
-        constexpr int64_t kMbRun = 24;
-        int64_t run_begin = -1, run_n = 0, run_M = 0;   // the open run of multi-block systems
-        auto close_run = [&]() -> int {
-          if (run_n == 0) return GNNSHAP_OK;
-          if (int st = gnnshap::launch_solve_mb(b.mb + run_begin, run_n, run_M, carrier[turn]->stream())) return st;
-          run_n = 0;
-          run_M = 0;
-          turn = (turn + 1) % ncar;
-          return GNNSHAP_OK;
-        };
-        for (size_t i = 0; i < rest.size(); ++i) {
-          const int64_t t = rest[i];
-          if (plans[t].num_players > gnnshap::iterative_threshold(&plans[t])) {
-            its.push_back(t);
-          } else if (Gr.mb[i] >= 0) {
-            if (run_n == 0) run_begin = Gr.mb[i];
-            if (int st = start(t, carrier[turn], true)) return st;
-            run_M = std::max<int64_t>(run_M, plans[t].num_players);
-            if (++run_n == kMbRun)
-              if (int st = close_run()) return st;
-          } else {
-            if (int st = start(t, carrier[turn], false)) return st;
-            if (run_n == 0) turn = (turn + 1) % ncar;
-          }
-        }
-        if (int st = close_run()) return st;
-        const int cap = ng == 1 ? gnnshap::kCgGroupMax : kPerGroup;
-        size_t next = 0;
-        for (;;) {
-          bool moved = false, busy = false;
-          while (next < its.size()) {
-            int gi = -1;
-            for (int i = 0; i < ng; ++i)
-              if (grp[i].size() < cap && (gi < 0 || grp[i].size() < grp[gi].size())) gi = i;
-            if (gi < 0) break;
-            const int64_t t = its[next];
-            if (grp[gi].stream() != home && evaluated[t] && !evaluated_done(t)) break;
-            if (int st = start(t, &grp[gi], false)) return st;
-            ++next;
-            moved = true;
-          }
-          for (int i = 0; i < ng; ++i) {
-            if (grp[i].empty()) continue;
-            busy = true;
-            if (!grp[i].ready()) continue;
-            if (int st = grp[i].step()) return st;
-            moved = true;
-          }
-          if (!busy && next >= its.size()) break;
-          if (!moved) std::this_thread::sleep_for(std::chrono::microseconds(20));
-        }
-        for (int i = 0; i < 2; ++i) {
-          if (!side[i]) continue;
-          GS_HIP(hipEventRecord(side[i]->rest_out, side[i]->stream));
-          GS_HIP(hipStreamWaitEvent(home, side[i]->rest_out, 0));
         }
         return GNNSHAP_OK;
       };
@@ -701,7 +727,7 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
             if (int st = gnnshap::launch_solve_one(jb, G.solve_count, gs[gi])) return st;
           }
         }
-        return solve_rest(G, gs[gi]);
+        return rest_finish(gi);
       };
       // G~ first: it depends on the masks only, and queued ahead of the
       // evaluations it gets the GPU before their many workgroups fill it
@@ -719,13 +745,15 @@ int explain_batch_impl(const gnnshap_subgraph* sgs, const gnnshap_sample_plan* p
         GS_HIP(hipGetDevice(&dev));
         worker = &gnnshap::issuer();
         worker->post(dev, [&]() -> int {
+          if (int st = rest_open(0, gs[0])) return st;
           if (int st = eval_group(0)) return st;
           if (int st = solve_group(0)) return st;
           GS_HIP(hipEventRecord(side0->join, side0->stream));
           return GNNSHAP_OK;
         });
       }
-      st = eval_group(1);
+      st = rest_open(1, gs[1]);
+      if (st == GNNSHAP_OK) st = eval_group(1);
       if (st == GNNSHAP_OK) st = solve_group(1);
       if (worker) {
         const int wst = worker->wait();
