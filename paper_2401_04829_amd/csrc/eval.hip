@@ -119,10 +119,10 @@ int make_shape(const gnnshap_subgraph* sg, const gnnshap_gcn* m, int64_t k, Shap
   s.tile = t;
   // The wide path evaluates every row in a launch sequence of its own; the
   // per-pass arrays above then serve the two end coalitions only.
-  s.wide = gnnshap::wide_applies(s.L, s.hops, s.dims) && s.n_dst == sg->hop_ptr[2];
+  s.wide = gnnshap::wide_applies(s.L, s.hops, s.dims);
   if (s.wide) {
     s.tile = 2;
-    s.ws = gnnshap::wide_shape(sg->num_edges, s.n_nodes, s.n_dst, k, s.dims, s.L);
+    s.ws = gnnshap::wide_shape(sg->num_edges, s.n_nodes, s.n_dst, sg->hop_ptr[2], k, s.dims, s.L);
   }
   *out = s;
   return GNNSHAP_OK;
@@ -1721,6 +1721,17 @@ int gnnshap::eval_coalitions_impl(const gnnshap_subgraph* sg, const gnnshap_gcn*
       if (int st = gnnshap::launch_wide3_l1(ws, w.wide, sg, masks, sh.wpr, r0, nloc, w.Zc[1], m->b ? m->b[0] : nullptr,
                                             pairs, s))
         return st;
+      if (ws.agg3) {
+        // three hops: layer 2's sums at the target and its in-neighbours, then W_2 there only
+        if (int st = gnnshap::launch_wide3_agg(ws, w.wide, sg, masks, sh.wpr, r0, nloc, pairs, s)) return st;
+        if (int st = launch_gemm(s, w.wide.A3, ws.h, nullptr, nullptr, m->W[1], ws.h2, w.wide.Z2, ws.h2, 0,
+                                 (pairs ? 2 : 1) * nloc * ws.n2, ws.h2, ws.h))
+          return st;
+        if (int st = gnnshap::launch_wide3_t(ws, w.wide, sg, masks, sh.wpr, r0, nloc, m->b ? m->b[1] : nullptr,
+                                             m->W[2], w.ctl, pairs, s))
+          return st;
+        continue;
+      }
       if (int st = launch_gemm(s, w.wide.H1, ws.h, nullptr, nullptr, m->W[1], ws.h2, w.wide.Z2, ws.h2, 0,
                                (pairs ? 2 : 1) * nloc * ws.n1, ws.h2, ws.h))
         return st;

@@ -115,11 +115,12 @@ __global__ void __launch_bounds__(1024) k_wide_prep(const int32_t* __restrict__ 
 // each split into hi + mid + lo (round to nearest at each step, so the three
 // parts add up to the fp32 value exactly), stored as three uint4 of eight
 // bf16: part p of (U, ft) at Zop[((U ntot + ft) kParts + p) 64 + lane].
+// The units of nodes 0 .. nn - 1 (a prefix of H_1) are built.
 __global__ void __launch_bounds__(256) k_wide_zop(const int32_t* __restrict__ dst_ptr,
-                                                  const int32_t* __restrict__ edge_src, int64_t n1,
+                                                  const int32_t* __restrict__ edge_src, int64_t n1, int64_t nn,
                                                   const int32_t* __restrict__ seg, const float* __restrict__ Zc, int h,
                                                   int ntot, int64_t units_cap, uint4* __restrict__ Zop) {
-  const int64_t units = seg[n1];
+  const int64_t units = seg[nn];
   const int64_t total = units * ntot * 64;
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
        idx += static_cast<int64_t>(gridDim.x) * 256) {
@@ -128,7 +129,7 @@ __global__ void __launch_bounds__(256) k_wide_zop(const int32_t* __restrict__ ds
     const int ft = static_cast<int>(rest % ntot);
     const int64_t U = rest / ntot;
     if (U >= units_cap) break;
-    int64_t lo = 0, hi = n1;                    // node x with seg[x] <= U < seg[x + 1]
+    int64_t lo = 0, hi = nn;                    // node x with seg[x] <= U < seg[x + 1]
     while (hi - lo > 1) {
       const int64_t mid = (lo + hi) >> 1;
       if (seg[mid] <= U) lo = mid;
@@ -479,11 +480,12 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
 }
 
 // y of row b (b < nrows) and, with pairs, of its complement b + khalf.
-// Node x >= 1 of H_1 is the source of the target's player x - 1 (the
-// extraction orders both by global id).
+// Node x of 1 .. n_in - 1 (the first hop) is the source of the target's
+// player x - 1 (the extraction orders both by global id).
 template <bool PAIRS>
 __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ masks, int64_t wpr, int64_t nrows,
                                                   int64_t khalf, const int32_t* __restrict__ dst_ptr, int64_t n1,
+                                                  int64_t n_in,
                                                   const int32_t* __restrict__ deg, const float* __restrict__ t,
                                                   int nfb, int64_t k, const float* __restrict__ b2,
                                                   const int32_t* __restrict__ ctl, const float* __restrict__ fef,
@@ -503,7 +505,7 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
     const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dg[0]));
     float acc = dv * tval(b, 0);
     bool live = false;
-    for (int64_t x = 1; x < n1; ++x) {
+    for (int64_t x = 1; x < n_in; ++x) {
       const int64_t p = x - 1;
       if ((mr[p >> 6] >> (p & 63)) & 1) {
         live = true;
@@ -517,7 +519,7 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
     const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>((dst_ptr[1] - dst_ptr[0]) - dg[0]));
     float acc = dv * tval(bc, 0);
     bool live = false;
-    for (int64_t x = 1; x < n1; ++x) {
+    for (int64_t x = 1; x < n_in; ++x) {
       const int64_t p = x - 1;
       if (!((mr[p >> 6] >> (p & 63)) & 1)) {
         live = true;
@@ -529,6 +531,108 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
   }
 }
 
+// Three layers on three hops, layer 2 at nodes 0 .. n2 - 1 (the target and
+// its in-neighbours), whose in-neighbours all lie in H_1: by linearity of
+// the transform, layer 2's sum at x is A W_2 with
+//   A = d(x)^-1/2 H1[x] + sum_{e -> x, e in c} d(src e)^-1/2 H1[src e],
+// so A is formed first (n2 rows per coalition instead of n1 for the
+// transform).  The pass rows are the rows r0 .. r0 + nloc - 1 and, with
+// pairs, their complements at pass rows nloc .. 2 nloc - 1 (mask bits and
+// degrees complemented).  One workgroup per (node x, 16 pass rows): x's
+// players are staged in LDS (source, players entering the source) 256 at a
+// time; lane (rg, q) of wavefront w takes pass row 16 blk + 4 w + rg and
+// features 4 q .. 4 q + 3 of each 64-feature chunk, four players' loads in
+// flight.  Players in order, so the sums are the same in every call.
+constexpr int kAggRows = 16;
+__global__ void __launch_bounds__(256) k_wide3_agg(const uint64_t* __restrict__ masks, int64_t wpr, int64_t r0,
+                                                   int64_t nloc, bool pairs, const int32_t* __restrict__ dst_ptr,
+                                                   const int32_t* __restrict__ edge_src, int64_t n1, int64_t n2,
+                                                   const int32_t* __restrict__ deg, const float* __restrict__ H1,
+                                                   int h, float* __restrict__ A) {
+  __shared__ int32_t su[256], snu[256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, rg = lane >> 4, q = lane & 15;
+  const int64_t nr = pairs ? 2 * nloc : nloc;
+  const int64_t x = blockIdx.x % n2;
+  const int64_t lr = (blockIdx.x / n2) * kAggRows + 4 * wave + rg;
+  const bool valid = lr < nr;
+  const int64_t lrc = valid ? lr : nr - 1;
+  const bool comp = lrc >= nloc;
+  const int64_t row = r0 + (comp ? lrc - nloc : lrc);   // the contracted row (degrees, mask bits)
+  const uint64_t* mr = masks + row * wpr;
+  const int32_t* dg = deg + row * n1;
+  const float* hr = H1 + lrc * n1 * h;
+  const int dgx = dg[x];
+  const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(comp ? (dst_ptr[x + 1] - dst_ptr[x]) - dgx : dgx));
+  const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+  for (int f0 = 0; f0 < h; f0 += 64) {
+    const int f = f0 + 4 * q;
+    const bool fv = f < h;   // (h is a multiple of 16)
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (fv) {
+      const float4 s4 = *reinterpret_cast<const float4*>(hr + x * h + f);
+      acc = make_float4(dx * s4.x, dx * s4.y, dx * s4.z, dx * s4.w);
+    }
+    for (int eb = e0; eb < e1; eb += 256) {
+      const int n = e1 - eb < 256 ? e1 - eb : 256;
+      __syncthreads();   // the previous chunk's reads are done
+      if (static_cast<int>(threadIdx.x) < n) {
+        const int32_t u = edge_src[eb + threadIdx.x];
+        su[threadIdx.x] = u;
+        snu[threadIdx.x] = u < n1 ? dst_ptr[u + 1] - dst_ptr[u] : 0;
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int j = 0; j < n; ++j) {
+        const int e = eb + j;
+        const int32_t u = su[j];
+        const bool bit = (mr[e >> 6] >> (e & 63)) & 1;
+        // (u >= n1 does not occur in an extracted subgraph: in-neighbours of these nodes lie in H_1)
+        if (bit != comp && u < n1 && fv) {
+          const int du = comp ? snu[j] - dg[u] : dg[u];
+          const float c = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(du));
+          const float4 v = *reinterpret_cast<const float4*>(hr + static_cast<int64_t>(u) * h + f);
+          acc.x = fmaf(c, v.x, acc.x);
+          acc.y = fmaf(c, v.y, acc.y);
+          acc.z = fmaf(c, v.z, acc.z);
+          acc.w = fmaf(c, v.w, acc.w);
+        }
+      }
+    }
+    if (valid && fv) *reinterpret_cast<float4*>(A + (lr * n2 + x) * h + f) = acc;
+  }
+}
+
+// t[row][x] for nodes x < n2 from Z = A W_2 (rows as k_wide3_agg's):
+// H2 = relu(d(x)^-1/2 Z + b_2), t = H2 . W_3[:, class]; one wavefront per
+// (pass row, node), lane = feature, a fixed reduction order.
+__global__ void __launch_bounds__(256) k_wide3_t(const uint64_t* __restrict__ masks, int64_t wpr, int64_t r0,
+                                                 int64_t nloc, bool pairs, int64_t khalf,
+                                                 const int32_t* __restrict__ dst_ptr, int64_t n1, int64_t n2,
+                                                 const int32_t* __restrict__ deg, const float* __restrict__ Z, int h2,
+                                                 const float* __restrict__ b2, const float* __restrict__ W3, int C,
+                                                 const int32_t* __restrict__ ctl, int64_t k, float* __restrict__ t) {
+  const int lane = threadIdx.x & 63;
+  const int64_t item = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nr = pairs ? 2 * nloc : nloc;
+  if (item >= nr * n2) return;
+  const int64_t lr = item / n2, x = item % n2;
+  const bool comp = lr >= nloc;
+  const int64_t row = r0 + (comp ? lr - nloc : lr);
+  const int dgx = deg[row * n1 + x];
+  const int d = comp ? (dst_ptr[x + 1] - dst_ptr[x]) - dgx : dgx;
+  const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(d));
+  const int cls = ctl[0];
+  const float* zr = Z + (lr * n2 + x) * h2;
+  float s = 0.f;
+  for (int f = lane; f < h2; f += 64) {
+    const float hv = fmaxf(fmaf(dx, zr[f], b2 ? b2[f] : 0.f), 0.f);
+    s = fmaf(hv, W3[static_cast<int64_t>(f) * C + cls], s);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane == 0) t[(comp ? row + khalf : row) * n1 + x] = s;
+}
+
 // The two end coalitions (no players, every player), one layer, partial
 // sums: Hp[p][x][f] = sum over part p of the players entering x (the 64
 // wavefronts of the kEndParts workgroups of (x, feature block) take players
@@ -536,11 +640,11 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
 // entering each node); Z(u) = Zin[u] for u in H_1, Zc[u] otherwise (layer 1:
 // both X W_1; layer 2 of a three-layer model: H^1 W_2 under E_c, and the
 // constant rows); lane = feature, the sixteen wavefronts' sums added in a
-// fixed order.
+// fixed order.  Nodes 0 .. nn - 1 (a prefix of H_1, one per blockIdx.x).
 constexpr int kEndParts = 4;
 
 __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict__ dst_ptr,
-                                                       const int32_t* __restrict__ edge_src, int64_t n1,
+                                                       const int32_t* __restrict__ edge_src, int64_t n1, int64_t nn,
                                                        const float* __restrict__ Zc, const float* __restrict__ Zin,
                                                        int h, float* __restrict__ Hp) {
   __shared__ float part[16][64];
@@ -561,21 +665,23 @@ __global__ void __launch_bounds__(1024) k_wide_ends_l1(const int32_t* __restrict
   if (wave == 0 && fv) {
     float a = 0.f;
     for (int i = 0; i < 16; ++i) a += part[i][lane];
-    Hp[(static_cast<int64_t>(pp) * n1 + x) * h + f] = a;
+    Hp[(static_cast<int64_t>(pp) * nn + x) * h + f] = a;
   }
 }
 
-// The end coalitions' layer at H_1 from the parts' sums: Hf[x] at every
-// node of H_1 under E_c (the sums in order, self loop Zself[x], bias, ReLU),
-// Hf[n1] at the target under the empty coalition (its self loop only:
+// The end coalitions' layer at nodes 0 .. nn - 1 of H_1 from the parts' sums:
+// Hf[x] under E_c (the sums in order, self loop Zself[x], bias, ReLU),
+// Hf[nn] at the target under the empty coalition (its self loop only:
 // Zempty, the target's input row then).  Then, with C > 0 (the last hidden
-// layer), the output layer at the target for every class and the explained
+// layer; nodes 1 .. n_in - 1 are the target's in-neighbours, n_in <= nn),
+// the output layer at the target for every class and the explained
 // class (the requested one, or argmax f(E_c), ties to the lowest index):
 // sp_y[c] = f_c(empty), sp_y[C + c] = f_c(E_c); ctl[0], class_out and
 // f_empty_full as the other evaluation paths write them.  One workgroup of
 // 1024 threads, one wavefront per class at a time (lane = feature).
-__global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restrict__ dst_ptr, int64_t n1,
-                                                        const float* __restrict__ Hp, const float* __restrict__ Zself,
+__global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restrict__ dst_ptr, int64_t nn,
+                                                        int64_t n_in, const float* __restrict__ Hp,
+                                                        const float* __restrict__ Zself,
                                                         const float* __restrict__ Zempty,
                                                         const float* __restrict__ b1, int h,
                                                         const float* __restrict__ W2, const float* __restrict__ b2,
@@ -583,29 +689,29 @@ __global__ void __launch_bounds__(1024) k_wide_ends_out(const int32_t* __restric
                                                         int32_t* __restrict__ ctl, int32_t* __restrict__ class_out,
                                                         float* __restrict__ f_empty_full, float* __restrict__ Hf) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int64_t i = threadIdx.x; i < n1 * h; i += blockDim.x) {
+  for (int64_t i = threadIdx.x; i < nn * h; i += blockDim.x) {
     const int64_t x = i / h;
     const int f = static_cast<int>(i % h);
     float a = 0.f;
-    for (int q = 0; q < kEndParts; ++q) a += Hp[(static_cast<int64_t>(q) * n1 + x) * h + f];
+    for (int q = 0; q < kEndParts; ++q) a += Hp[(static_cast<int64_t>(q) * nn + x) * h + f];
     const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
     const float bb = b1 ? b1[f] : 0.f;
     Hf[i] = fmaxf(fmaf(dx, fmaf(dx, Zself[x * h + f], a), bb), 0.f);
-    if (x == 0) Hf[n1 * h + f] = fmaxf(Zempty[f] + bb, 0.f);
+    if (x == 0) Hf[nn * h + f] = fmaxf(Zempty[f] + bb, 0.f);
   }
   if (C == 0) return;
   __syncthreads();
   const float dv = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[1] - dst_ptr[0]));
   for (int c = wave; c < C; c += 16) {
     float full = 0.f, empty = 0.f;
-    for (int64_t x = 0; x < n1; ++x) {
+    for (int64_t x = 0; x < n_in; ++x) {
       float p = 0.f;
       for (int f = lane; f < h; f += 64) p = fmaf(Hf[x * h + f], W2[static_cast<int64_t>(f) * C + c], p);
       // node x >= 1 is the source of the target's player x - 1, present in E_c
       const float wx = x == 0 ? dv : __builtin_amdgcn_rsqf(1.0f + static_cast<float>(dst_ptr[x + 1] - dst_ptr[x]));
       full = fmaf(wx, p, full);
     }
-    for (int f = lane; f < h; f += 64) empty = fmaf(Hf[n1 * h + f], W2[static_cast<int64_t>(f) * C + c], empty);
+    for (int f = lane; f < h; f += 64) empty = fmaf(Hf[nn * h + f], W2[static_cast<int64_t>(f) * C + c], empty);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
       full += __shfl_xor(full, off);
@@ -656,7 +762,7 @@ int wide_prep(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, c
   k_wide_prep<<<1, 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, w.seg, w.spec_ptr, w.spec_e);
   GS_LAUNCHED();
   k_wide_zop<<<grid_for(s.units_cap * s.ntot * 64, 256, 16384), 256, 0, st>>>(
-      sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc, s.h, s.ntot, s.units_cap, w.Zop);
+      sg->dst_ptr, sg->edge_src, s.n1, s.n1, w.seg, Zc, s.h, s.ntot, s.units_cap, w.Zop);
   GS_LAUNCHED();
   if (pairs) {
     k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, s.h,
@@ -668,17 +774,18 @@ int wide_prep(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, c
   return GNNSHAP_OK;
 }
 
-// One contraction launch over the pass r0 .. r0 + nloc - 1 (see k_wide_l1).
+// One contraction launch over the pass r0 .. r0 + nloc - 1 at nodes
+// 0 .. nx - 1 of H_1 (see k_wide_l1).
 template <int MODE>
 int wide_layer(const WideShape& s, const gnnshap_subgraph* sg, const uint64_t* masks, int64_t wpr, int64_t r0,
-               int64_t nloc, bool pairs, const uint4* Zop, int ntot, int nfb, int h, const float* Zc, const float* S,
-               const WideWs& w, const float* b, const float* Wp, const int32_t* ctl, const float* Zrow, float* Hout,
-               hipStream_t st) {
+               int64_t nloc, int64_t nx, bool pairs, const uint4* Zop, int ntot, int nfb, int h, const float* Zc,
+               const float* S, const WideWs& w, const float* b, const float* Wp, const int32_t* ctl,
+               const float* Zrow, float* Hout, hipStream_t st) {
   if (nloc <= 0) return GNNSHAP_OK;
   const int64_t khalf = pairs ? s.k / 2 : 0;
   const int64_t cblocks = ceil_div(nloc, kBlockRows);
-  if (s.n1 * cblocks > INT32_MAX || nfb > 65535) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
-  const dim3 grid(static_cast<unsigned>(s.n1 * cblocks), static_cast<unsigned>(nfb));
+  if (nx * cblocks > INT32_MAX || nfb > 65535) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
+  const dim3 grid(static_cast<unsigned>(nx * cblocks), static_cast<unsigned>(nfb));
   if (pairs)
     k_wide_l1<true, MODE><<<grid, kBlockRows, 0, st>>>(masks, wpr, r0, nloc, khalf, cblocks, sg->dst_ptr,
                                                        sg->edge_src, s.n1, w.seg, Zop, ntot, h, Zc, S, w.spec_ptr,
@@ -699,11 +806,11 @@ int wide_out(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, co
   const unsigned g = static_cast<unsigned>(ceil_div(nrows, 256));
   GS_TIMED("k_wide_out", st);
   if (pairs)
-    k_wide_out<true><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, nfb_t, s.k, b_last,
-                                        ctl, fef, y);
+    k_wide_out<true><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, s.n2, w.deg, w.t, nfb_t, s.k,
+                                        b_last, ctl, fef, y);
   else
-    k_wide_out<false><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, w.deg, w.t, nfb_t, s.k, b_last,
-                                         ctl, fef, y);
+    k_wide_out<false><<<g, 256, 0, st>>>(masks, wpr, nrows, khalf, sg->dst_ptr, s.n1, s.n2, w.deg, w.t, nfb_t, s.k,
+                                         b_last, ctl, fef, y);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }
@@ -711,17 +818,20 @@ int wide_out(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, co
 }  // namespace
 
 bool wide_applies(int num_layers, int num_hops, const int32_t* dims) {
-  if (num_hops != 2 || (num_layers != 2 && num_layers != 3)) return false;
+  const bool shape = (num_hops == 2 && (num_layers == 2 || num_layers == 3)) || (num_hops == 3 && num_layers == 3);
+  if (!shape) return false;
   for (int j = 1; j < num_layers; ++j)
     if (!wide_width(dims[j])) return false;
   return true;
 }
 
-WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t k, const int32_t* dims, int num_layers) {
+WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t n2, int64_t k, const int32_t* dims,
+                     int num_layers) {
   WideShape s;
   s.M = M;
   s.n_nodes = n_nodes;
   s.n1 = n1;
+  s.n2 = n2;
   s.k = k;
   s.h = dims[1];
   s.C = dims[num_layers];
@@ -732,7 +842,9 @@ WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t k, const in
     s.h2 = dims[2];
     s.ntot2 = s.h2 / 16;
     s.nfb2 = static_cast<int>(ceil_div(s.ntot2, kTiles));
-    const int64_t per_row = 2 * n1 * (static_cast<int64_t>(s.h) + s.h2) * static_cast<int64_t>(sizeof(float));
+    s.agg3 = n2 < n1;
+    const int64_t per_row = 2 * (n1 * (static_cast<int64_t>(s.h) + s.h2) + (s.agg3 ? n2 * s.h : 0)) *
+                            static_cast<int64_t>(sizeof(float));
     int64_t p = kPassBudget / per_row;
     p = std::max<int64_t>(kBlockRows, p - p % kBlockRows);
     s.pass = std::min<int64_t>(p, k);
@@ -748,7 +860,7 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
   w.Zop = c.take<uint4>(s.units_cap * s.ntot * kParts * 64);
   w.S = c.take<float>(s.n1 * s.h);
   w.deg = c.take<int32_t>(s.k * s.n1);
-  w.t = c.take<float>(static_cast<int64_t>(s.h2 ? s.nfb2 : s.nfb) * s.k * s.n1);
+  w.t = c.take<float>(static_cast<int64_t>(s.h2 ? (s.agg3 ? 1 : s.nfb2) : s.nfb) * s.k * s.n1);
   w.hf = c.take<float>((s.n1 + 1) * s.h);
   w.hp = c.take<float>(kEndParts * s.n1 * std::max(s.h, s.h2));
   if (s.h2 > 0) {
@@ -758,6 +870,7 @@ WideWs wide_carve(Carver& c, const WideShape& s) {
     w.S2 = c.take<float>(s.n1 * s.h2);
     w.H1 = c.take<float>(2 * s.pass * s.n1 * s.h);
     w.Z2 = c.take<float>(2 * s.pass * s.n1 * s.h2);
+    w.A3 = s.agg3 ? c.take<float>(2 * s.pass * s.n2 * s.h) : nullptr;
   }
   return w;
 }
@@ -769,10 +882,10 @@ int launch_wide_ends(const WideShape& s, const WideWs& w, const gnnshap_subgraph
   {
     GS_TIMED("k_wide_ends", st);
     k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64)), kEndParts), 1024, 0,
-                     st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc, Zc, s.h, w.hp);
+                     st>>>(sg->dst_ptr, sg->edge_src, s.n1, s.n1, Zc, Zc, s.h, w.hp);
     GS_LAUNCHED();
-    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, Zc, Zc, b1, s.h, W2, b2, s.C, target_class, sp_y,
-                                         ctl, class_out, f_empty_full, w.hf);
+    k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, s.n2, w.hp, Zc, Zc, b1, s.h, W2, b2, s.C, target_class,
+                                         sp_y, ctl, class_out, f_empty_full, w.hf);
   }
   GS_LAUNCHED();
   return GNNSHAP_OK;
@@ -784,8 +897,8 @@ int launch_wide(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg,
   if (int r = wide_prep(s, w, sg, masks, wpr, Zc, pairs, st)) return r;
   {
     GS_TIMED("k_wide_l1", st);
-    if (int r = wide_layer<kProj>(s, sg, masks, wpr, 0, pairs ? s.k / 2 : s.k, pairs, w.Zop, s.ntot, s.nfb, s.h, Zc,
-                                  w.S, w, b1, W2, ctl, nullptr, nullptr, st))
+    if (int r = wide_layer<kProj>(s, sg, masks, wpr, 0, pairs ? s.k / 2 : s.k, s.n1, pairs, w.Zop, s.ntot, s.nfb, s.h,
+                                  Zc, w.S, w, b1, W2, ctl, nullptr, nullptr, st))
       return r;
   }
   return wide_out(s, w, sg, masks, wpr, s.nfb, b2, ctl, fef, pairs, y, st);
@@ -797,10 +910,10 @@ int launch_wide3_ends_l1(const WideShape& s, const WideWs& w, const gnnshap_subg
   if (s.n1 > 65535 * 64) return fail(GNNSHAP_EUNSUPPORTED, "too many nodes in H_1");
   GS_TIMED("k_wide_ends", st);
   k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h, 64)), kEndParts), 1024, 0,
-                   st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc1, Zc1, s.h, w.hp);
+                   st>>>(sg->dst_ptr, sg->edge_src, s.n1, s.n1, Zc1, Zc1, s.h, w.hp);
   GS_LAUNCHED();
-  k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, Zc1, Zc1, b1, s.h, nullptr, nullptr, 0, -1, nullptr,
-                                       nullptr, nullptr, nullptr, w.hf);
+  k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, s.n2, w.hp, Zc1, Zc1, b1, s.h, nullptr, nullptr, 0, -1,
+                                       nullptr, nullptr, nullptr, nullptr, w.hf);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }
@@ -810,11 +923,12 @@ int launch_wide3_ends_l2(const WideShape& s, const WideWs& w, const gnnshap_subg
                          int32_t* ctl, int32_t* class_out, float* f_empty_full, hipStream_t st) {
   if (s.h2 == 0) return fail(GNNSHAP_EINVAL, "not a three-layer shape");
   GS_TIMED("k_wide_ends", st);
-  k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n1), static_cast<unsigned>(ceil_div(s.h2, 64)), kEndParts), 1024, 0,
-                   st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc2, w.z2e, s.h2, w.hp);
+  // layer 2 is needed at the target and its in-neighbours only (nodes 0 .. n2 - 1)
+  k_wide_ends_l1<<<dim3(static_cast<unsigned>(s.n2), static_cast<unsigned>(ceil_div(s.h2, 64)), kEndParts), 1024, 0,
+                   st>>>(sg->dst_ptr, sg->edge_src, s.n1, s.n2, Zc2, w.z2e, s.h2, w.hp);
   GS_LAUNCHED();
-  k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n1, w.hp, w.z2e, w.z2e + s.n1 * s.h2, b2, s.h2, W3, b3, s.C,
-                                       target_class, sp_y, ctl, class_out, f_empty_full, w.hf2);
+  k_wide_ends_out<<<1, 1024, 0, st>>>(sg->dst_ptr, s.n2, s.n2, w.hp, w.z2e, w.z2e + s.n1 * s.h2, b2, s.h2, W3, b3,
+                                       s.C, target_class, sp_y, ctl, class_out, f_empty_full, w.hf2);
   GS_LAUNCHED();
   return GNNSHAP_OK;
 }
@@ -823,13 +937,15 @@ int launch_wide3_prep(const WideShape& s, const WideWs& w, const gnnshap_subgrap
                       int64_t wpr, const float* Zc1, const float* Zc2, bool pairs, hipStream_t st) {
   if (s.h2 == 0) return fail(GNNSHAP_EINVAL, "not a three-layer shape");
   if (int r = wide_prep(s, w, sg, masks, wpr, Zc1, pairs, st)) return r;
-  // layer 2's operands: the input rows of the sources outside H_1 (their
-  // degree is 1 under every coalition, so the rows are constant)
+  if (s.agg3) return GNNSHAP_OK;   // layer 2 from A W_2 (no contraction)
+  // layer 2's operands at nodes 0 .. n2 - 1 (where layer 2 is needed): the
+  // input rows of the sources outside H_1 (their degree is 1 under every
+  // coalition, so the rows are constant)
   k_wide_zop<<<grid_for(s.units_cap * s.ntot2 * 64, 256, 16384), 256, 0, st>>>(
-      sg->dst_ptr, sg->edge_src, s.n1, w.seg, Zc2, s.h2, s.ntot2, s.units_cap, w.Zop2);
+      sg->dst_ptr, sg->edge_src, s.n1, s.n2, w.seg, Zc2, s.h2, s.ntot2, s.units_cap, w.Zop2);
   GS_LAUNCHED();
   if (pairs) {
-    k_wide_sum<<<static_cast<unsigned>(s.n1 * s.ntot2), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc2, s.h2,
+    k_wide_sum<<<static_cast<unsigned>(s.n2 * s.ntot2), 1024, 0, st>>>(sg->dst_ptr, sg->edge_src, s.n1, Zc2, s.h2,
                                                                        s.ntot2, w.S2);
     GS_LAUNCHED();
   }
@@ -841,8 +957,8 @@ int launch_wide3_l1(const WideShape& s, const WideWs& w, const gnnshap_subgraph*
                     hipStream_t st) {
   if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
   GS_TIMED("k_wide_l1", st);
-  return wide_layer<kFull>(s, sg, masks, wpr, r0, nloc, pairs, w.Zop, s.ntot, s.nfb, s.h, Zc1, w.S, w, b1, nullptr,
-                           nullptr, nullptr, w.H1, st);
+  return wide_layer<kFull>(s, sg, masks, wpr, r0, nloc, s.n1, pairs, w.Zop, s.ntot, s.nfb, s.h, Zc1, w.S, w, b1,
+                           nullptr, nullptr, nullptr, w.H1, st);
 }
 
 int launch_wide3_l2(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
@@ -850,14 +966,40 @@ int launch_wide3_l2(const WideShape& s, const WideWs& w, const gnnshap_subgraph*
                     bool pairs, hipStream_t st) {
   if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
   GS_TIMED("k_wide_l2", st);
-  return wide_layer<kProjRows>(s, sg, masks, wpr, r0, nloc, pairs, w.Zop2, s.ntot2, s.nfb2, s.h2, nullptr, w.S2, w,
-                               b2, W3, ctl, w.Z2, nullptr, st);
+  return wide_layer<kProjRows>(s, sg, masks, wpr, r0, nloc, s.n2, pairs, w.Zop2, s.ntot2, s.nfb2, s.h2, nullptr,
+                               w.S2, w, b2, W3, ctl, w.Z2, nullptr, st);
+}
+
+int launch_wide3_agg(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                     int64_t wpr, int64_t r0, int64_t nloc, bool pairs, hipStream_t st) {
+  if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
+  if (nloc <= 0) return GNNSHAP_OK;
+  const int64_t blocks = ceil_div((pairs ? 2 : 1) * nloc, kAggRows) * s.n2;
+  if (blocks > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
+  GS_TIMED("k_wide3_agg", st);
+  k_wide3_agg<<<static_cast<unsigned>(blocks), 256, 0, st>>>(
+      masks, wpr, r0, nloc, pairs, sg->dst_ptr, sg->edge_src, s.n1, s.n2, w.deg, w.H1, s.h, w.A3);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
+}
+
+int launch_wide3_t(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                   int64_t wpr, int64_t r0, int64_t nloc, const float* b2, const float* W3, const int32_t* ctl,
+                   bool pairs, hipStream_t st) {
+  if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
+  if (nloc <= 0) return GNNSHAP_OK;
+  const int64_t items = (pairs ? 2 : 1) * nloc * s.n2;
+  k_wide3_t<<<static_cast<unsigned>(ceil_div(items * 64, 256)), 256, 0, st>>>(
+      masks, wpr, r0, nloc, pairs, pairs ? s.k / 2 : 0, sg->dst_ptr, s.n1, s.n2, w.deg, w.Z2, s.h2, b2, W3, s.C, ctl,
+      s.k, w.t);
+  GS_LAUNCHED();
+  return GNNSHAP_OK;
 }
 
 int launch_wide3_out(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
                      int64_t wpr, const float* b3, const int32_t* ctl, const float* fef, bool pairs, float* y,
                      hipStream_t st) {
-  return wide_out(s, w, sg, masks, wpr, s.nfb2, b3, ctl, fef, pairs, y, st);
+  return wide_out(s, w, sg, masks, wpr, s.agg3 ? 1 : s.nfb2, b3, ctl, fef, pairs, y, st);
 }
 
 }  // namespace gnnshap

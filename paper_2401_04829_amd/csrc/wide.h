@@ -13,6 +13,7 @@ namespace gnnshap {
 
 struct WideShape {
   int64_t M = 0, n_nodes = 0, n1 = 0, k = 0;
+  int64_t n2 = 0;          // the target and its in-neighbours (nodes 0 .. n2 - 1; n2 = n1 with two hops)
   int64_t units_cap = 0;   // operand units (32 players each) of the contraction, upper bound
   int h = 0, C = 0;        // layer-1 width; classes
   int ntot = 0;            // 16-feature tiles of layer 1
@@ -20,13 +21,17 @@ struct WideShape {
   int h2 = 0;              // three-layer models: layer-2 width (0: two layers)
   int ntot2 = 0, nfb2 = 0;
   int64_t pass = 0;        // three-layer models: contracted rows per pass
+  bool agg3 = false;       // three hops (n2 < n1): layer 2 from A W_2 (launch_wide3_agg, launch_wide3_t)
 };
 
-// Whether the wide path evaluates a model: two or three layers, two hops
-// (H_1 is then every node with players entering it), hidden widths
-// multiples of 16 above 32.
+// Whether the wide path evaluates a model: two or three layers over two
+// hops, or three layers over three hops, hidden widths multiples of 16
+// above 32.  H_1 (n1 nodes) is the set of nodes that players enter: the
+// target and the first hop with two hops, and also the second hop with
+// three; n2 counts the target and its in-neighbours.
 bool wide_applies(int num_layers, int num_hops, const int32_t* dims);
-WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t k, const int32_t* dims, int num_layers);
+WideShape wide_shape(int64_t M, int64_t n_nodes, int64_t n1, int64_t n2, int64_t k, const int32_t* dims,
+                     int num_layers);
 
 struct WideWs {
   int32_t* seg;       // n1 + 1: first operand unit of each node of H_1
@@ -43,7 +48,8 @@ struct WideWs {
   uint4* Zop2;        // three layers: units_cap x ntot2 x 3 x 64: layer-2 A operands
   float* S2;          // three layers: n1 x h2
   float* H1;          // three layers: 2 pass x n1 x h: layer 1 of the pass's rows (complements after them)
-  float* Z2;          // three layers: 2 pass x n1 x h2: H1 W_2
+  float* Z2;          // three layers: 2 pass x n1 x h2: H1 W_2 (agg3: 2 pass x n2 x h2, A3 W_2)
+  float* A3;          // agg3: 2 pass x n2 x h: layer 2's sums at nodes 0 .. n2 - 1 before W_2
 };
 WideWs wide_carve(Carver& c, const WideShape& s);
 
@@ -90,6 +96,14 @@ int launch_wide3_l1(const WideShape& s, const WideWs& w, const gnnshap_subgraph*
 int launch_wide3_l2(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
                     int64_t wpr, int64_t r0, int64_t nloc, const float* b2, const float* W3, const int32_t* ctl,
                     bool pairs, hipStream_t st);
+// Three hops (s.agg3), in place of the caller's Z2 = H1 W_2 and
+// launch_wide3_l2: launch_wide3_agg (A3), the caller's Z2 = A3 W_2 (2 nloc
+// n2 rows with pairs), launch_wide3_t (t at nodes 0 .. n2 - 1).
+int launch_wide3_agg(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                     int64_t wpr, int64_t r0, int64_t nloc, bool pairs, hipStream_t st);
+int launch_wide3_t(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
+                   int64_t wpr, int64_t r0, int64_t nloc, const float* b2, const float* W3, const int32_t* ctl,
+                   bool pairs, hipStream_t st);
 int launch_wide3_out(const WideShape& s, const WideWs& w, const gnnshap_subgraph* sg, const uint64_t* masks,
                      int64_t wpr, const float* b3, const int32_t* ctl, const float* fef, bool pairs, float* y,
                      hipStream_t st);

@@ -1,7 +1,8 @@
 """GPU parity of the coalition values of two- and three-layer GCNs with wide
-hidden layers on two hops (the MFMA contraction of each layer at the nodes
-of H_1; for three layers the dense transform by W_2 between them), against
-the fp64 oracle game (Sec. 3.4, GCN of Sec. 4.2).
+hidden layers on two hops, and three-layer GCNs on three hops (the MFMA
+contraction of each layer at the nodes that players enter; for three layers
+the dense transform by W_2 between them), against the fp64 oracle game
+(Sec. 3.4, GCN of Sec. 4.2).
 
 Bar: |y_gpu - y_ref| <= 1e-4 max(|y_ref|, |f(E_c)|, |f(empty)|); rows
 without an in-edge of the target equal the device's f(empty) exactly.
@@ -13,7 +14,10 @@ has a coalition-dependent degree), random biases, arbitrary masks with an
 odd row count through gnnshap_eval_coalitions, and the sampler's complement
 pairs through the single-target and batched explanations (equal bit for
 bit).  Several passes over the rows of a three-layer model are covered at
-full size (the ogbn-arxiv-shaped targets of the parity tests).
+full size (the ogbn-arxiv-shaped targets of the parity tests).  Three hops:
+second-hop nodes with many in-edges from the third hop, edges between
+first- and second-hop nodes, layer 2 needed only at the target and its
+in-neighbours.
 """
 import numpy as np
 import pytest
@@ -62,7 +66,7 @@ def _hub_graph(seed, n_nb, n, extra, feat, dims):
 
 
 def _ref(cfg, v, target_class=-1):
-    sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, 2)
+    sub = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])
     M = sub["num_edges"]
     game = gcn.Game(sub, cfg["X"], cfg["weights"], cfg["biases"])
     logits = game.logits(np.ones(M, bool))
@@ -199,6 +203,110 @@ def test_wide_every_source_in_h1(dev, hid, C):
     mb, _ = sampler.sample(sampler.plan(M, p), seed, 0)
     np.testing.assert_array_equal(masks_np(r.masks), sampler.pack(mb))
     _check_y(r.y.cpu().numpy(), mb, game, f0, f1, r.f_empty_full.cpu().numpy(), sub_ref["dst_ptr"][1])
+
+
+def _deep_graph(seed, n_nb, n, extra, feat, dims):
+    """Three hops: node 0 with n_nb in-neighbours (1..n_nb), each with two to
+    six in-neighbours of its own among the next nodes (the second hop), each
+    of those with 20 to 200 in-edges from the rest (the third hop), a few
+    edges between first- and second-hop nodes, and random edges."""
+    rng = np.random.default_rng(seed)
+    src, dst = [], []
+    nxt = n_nb + 1
+    second = []
+    for x in range(1, n_nb + 1):
+        src.append(x)
+        dst.append(0)
+        for _ in range(int(rng.integers(2, 7))):
+            src.append(nxt)
+            dst.append(x)
+            second.append(nxt)
+            nxt += 1
+    for y in second:
+        deg = int(rng.integers(20, 201))
+        s = rng.choice(np.arange(nxt, n), size=deg, replace=False)
+        src.extend(s.tolist())
+        dst.extend([y] * deg)
+    near = np.arange(1, nxt)
+    for _ in range(len(second) // 2):
+        a, b = rng.choice(near, size=2, replace=False)
+        src.append(int(a))
+        dst.append(int(b))
+    src.extend(rng.integers(0, n, extra).tolist())
+    dst.extend(rng.integers(0, n, extra).tolist())
+    indptr, indices = W.in_csr_from_pairs(n, np.array(src), np.array(dst))
+    X = W.gaussian_features(n, feat, seed + 1)
+    Ws, bs = W.glorot_gcn(dims, seed + 2, bias="random")
+    return dict(indptr=indptr, indices=indices, X=X, weights=Ws, biases=bs, hops=3)
+
+
+DEEP = [((64, 64), 3), ((48, 80), 5), ((272, 48), 7)]
+
+
+@pytest.mark.parametrize("hid,C", DEEP)
+def test_wide_three_hops_arbitrary_masks(dev, hid, C):
+    """Three layers on three hops through gnnshap_eval_coalitions: random
+    masks, odd k, every row against the oracle."""
+    cfg = _deep_graph(200 + hid[0] + 3 * hid[1], 6, 6000, 300, 24, [24, *hid, C])
+    ex = explainer_for(cfg)
+    ex.prepare()
+    sub_ref, game, cls, f0, f1 = _ref(cfg, 0)
+    M = sub_ref["num_edges"]
+    hp = sub_ref["hop_ptr"]
+    assert hp[3] > hp[2] + 10 and sub_ref["num_nodes"] > hp[3]    # a real second and third hop
+    rng = np.random.default_rng(hid[0])
+    k = 201
+    mb = rng.random((k, M)) < rng.uniform(0.02, 0.98, size=(k, 1))
+    mb[0] = False
+    mb[1] = True
+    masks = torch.from_numpy(sampler.pack(mb).view(np.int64)).to(dev)
+    sub = ex.extract(0)
+    wpr = (M + 63) // 64
+    y = torch.empty(k, dtype=torch.float32, device=dev)
+    fef = torch.empty(2, dtype=torch.float32, device=dev)
+    cl = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(L.gnnshap_eval_workspace(sub.sg, ex.model, k), dtype=torch.uint8, device=dev)
+    _say("wide three hops, arbitrary masks", hid, C, M, k)
+    L.gnnshap_eval_coalitions(sub.sg, ex.model, _vp(ex.X), -1, _vp(masks), k, wpr, _vp(y), _vp(fef), _vp(cl),
+                              _vp(ws), ws.numel(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert int(cl.item()) == cls
+    fe = fef.cpu().numpy()
+    t0 = y_tolerance(np.array([f0, f1]), f0, f1)
+    assert abs(fe[0] - f0) <= t0[0] and abs(fe[1] - f1) <= t0[1]
+    _check_y(y.cpu().numpy(), mb, game, f0, f1, fe, sub_ref["dst_ptr"][1])
+
+
+@pytest.mark.parametrize("hid,C", DEEP[:2])
+def test_wide_three_hops_pairs_single_and_batch(dev, hid, C):
+    """Three layers on three hops, the sampler's complement pairs: explain()
+    for three targets against the oracle, explain_batch equal bit for bit
+    (5,000 coalitions for 900 to 1,800 players)."""
+    cfg = _deep_graph(300 + hid[0] + 3 * hid[1], 3, 4000, 150, 20, [20, *hid, C])
+    ex = explainer_for(cfg)
+    ex.prepare()
+    p, seed = 5000, 29
+    singles = []
+    for v in (0, 1, 2):
+        sub_ref, game, cls, f0, f1 = _ref(cfg, v)
+        M = sub_ref["num_edges"]
+        if M < 2:
+            continue
+        _say("wide three hops, pairs", hid, C, v, M)
+        r = ex.explain(v, p, seed)
+        torch.cuda.synchronize()
+        mb, _ = sampler.sample(sampler.plan(M, p), seed, v)
+        np.testing.assert_array_equal(masks_np(r.masks), sampler.pack(mb))
+        _check_y(r.y.cpu().numpy(), mb, game, f0, f1, r.f_empty_full.cpu().numpy(), sub_ref["dst_ptr"][1])
+        assert int(r.info.item()) == 0 and bool(torch.isfinite(r.phi).all()), v
+        singles.append((v, r.y.clone(), r.phi.clone(), r.f_empty_full.clone()))
+    res = ex.explain_batch([v for v, *_ in singles], p, seed)
+    torch.cuda.synchronize()
+    for t, (v, y1, phi1, fef1) in enumerate(singles):
+        e = res[t]
+        assert torch.equal(e.y, y1), v
+        assert torch.equal(e.f_empty_full, fef1), v
+        assert torch.equal(e.phi, phi1), v
 
 
 def _wide_hub300():
