@@ -293,7 +293,7 @@ int gnnshap_solve_workspace(const gnnshap_sample_plan* plan, size_t* bytes);
  * not factored: conjugate gradients run on the projected normal
  * equations, applying the masks and their transpose straight from the bits
  * (Sec. 3.5 fits large systems iteratively), until the residual falls to
- * 1e-8 of its initial norm; *info is then 0, or M + 1 if that did not happen
+ * 1e-6 of its initial norm; *info is then 0, or M + 1 if that did not happen
  * within 4000 iterations, the iteration broke down, or the plan has no
  * enumerated class and fewer than M - 1 random rows (then the rows cannot
  * determine phi).  Other rank deficiencies are not detected on that path:

