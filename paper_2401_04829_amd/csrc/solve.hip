@@ -576,7 +576,16 @@ __global__ void __launch_bounds__(256) k_rhs_reduce(const double* __restrict__ p
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + tid;
   double v = 0.0;
   if (j < M) {
-    for (int64_t c = 0; c < nch; ++c) v += part[c * M + j];
+    // the chunks in order; eight loads in flight ahead of their adds
+    int64_t c = 0;
+    for (; c + 8 <= nch; c += 8) {
+      double t[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) t[q] = part[(c + q) * M + j];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v += t[q];
+    }
+    for (; c < nch; ++c) v += part[c * M + j];
     dv[j] = v;
   }
   red[tid] = v;
