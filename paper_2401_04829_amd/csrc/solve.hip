@@ -1897,7 +1897,9 @@ __device__ __forceinline__ void pp_start_body(const gnnshap::SolveJob& J, int64_
 __device__ __forceinline__ void pp_trail_body(const gnnshap::SolveJob& J, int64_t p, int64_t tile) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int64_t M = J.M, nblk = (M + 63) / 64, nI = nblk - p - 1;
-  if (tile >= nI * (nI + 1) / 2) return;
+  // (a batched launch covers the batch's largest system: past this system's
+  // last panel nI <= 0, and nI (nI + 1) / 2 is positive again for nI <= -2)
+  if (nI <= 0 || tile >= nI * (nI + 1) / 2) return;
   int64_t I = 0;
   while ((I + 1) * (I + 2) / 2 <= tile) ++I;
   const int64_t Jb = tile - I * (I + 1) / 2;

@@ -547,6 +547,52 @@ def test_explain_batch_against_oracle(dev):
         _phi_close(r.phi.cpu().numpy().astype(np.float64), phi_ref)
 
 
+def test_explain_batch_stays_inside_its_workspace(dev):
+    """Panel-path systems (193-448 players) of different sizes in one batch:
+    the batched factorisation launches cover the largest system, and a
+    smaller one must ignore the panels past its own.  Targets from the
+    largest to the smallest, so that the smallest system's workspace slice
+    is the last one: every byte past the size the call asks for stays as it
+    was, and the results equal a call in a workspace of exactly that size.
+    (A trailing-update workgroup past a system's last panel once wrote a
+    64 x 64 block past that system's slice.)"""
+    cfg = W.make_config("cora")
+    sizes = []
+    for v in cfg["targets"]:
+        M = subgraph.extract(cfg["indptr"], cfg["indices"], v, cfg["hops"])["num_edges"]
+        if 192 < M <= 448:
+            sizes.append((M, int(v)))
+    sizes.sort(reverse=True)
+    assert (sizes[0][0] + 63) // 64 - (sizes[-1][0] + 63) // 64 >= 2   # two panels more in the largest
+    targets = [v for _, v in sizes]
+    ex = explainer_for(cfg)
+    ref = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+    torch.cuda.synchronize()
+    ref_phi = [ref[t].phi.clone() for t in range(len(targets))]
+    tail = 1 << 20
+    seen = {}
+    orig = type(ex)._batch_call
+
+    def call(self, sgs, plans, cl, target_class, ptrs, ws):
+        need = self._batch_workspace(sgs, plans)
+        big = torch.full((need + tail,), 0xA5, dtype=torch.uint8, device=dev)
+        st = orig(self, sgs, plans, cl, target_class, ptrs, big)
+        torch.cuda.synchronize()
+        seen["untouched"] = bool((big[need:] == 0xA5).all().item())
+        return st
+
+    type(ex)._batch_call = call
+    try:
+        res = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+        torch.cuda.synchronize()
+    finally:
+        type(ex)._batch_call = orig
+    assert seen["untouched"], "the batched call wrote past its workspace"
+    for t in range(len(targets)):
+        assert int(res[t].info.item()) == 0
+        assert torch.equal(res[t].phi, ref_phi[t]), t
+
+
 def test_explain_batch_repeated_calls_agree(dev):
     """Repeated batched calls on the same targets give the first call's
     outputs bit for bit, with other device work between them, and equal the
