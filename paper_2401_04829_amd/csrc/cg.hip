@@ -337,6 +337,23 @@ __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_e
   }
 }
 
+// v0 + x[0] + x[stride] + ... + x[(n - 1) stride], added in that order, with
+// eight loads in flight ahead of their adds.
+__device__ __forceinline__ double chunk_sum(const double* __restrict__ x, int64_t stride, int64_t n,
+                                            double v0 = 0.0) {
+  double v = v0;
+  int64_t c = 0;
+  for (; c + 8 <= n; c += 8) {
+    double t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = x[(c + q) * stride];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v += t[q];
+  }
+  for (; c < n; ++c) v += x[c * stride];
+  return v;
+}
+
 // u of the bit rows (the sum of their pass-A chunks, one lane per row) with
 // partial |u|^2 and |m|.u in uu[2 (1 + x)], uu[2 (1 + x) + 1]; the last
 // workgroup adds pass A's sparse-row partials into uu[0], uu[1] (fixed order).
@@ -356,8 +373,7 @@ __global__ void __launch_bounds__(256) k_cg_rows(GroupArgs g) {
   const int64_t b = a.rs + bid * 256 + threadIdx.x;
   double uu = 0.0, su = 0.0;
   if (b < a.kr) {
-    double v = 0.0;
-    for (int64_t c = 0; c < a.npc; ++c) v += a.upart[c * a.kr + b];
+    const double v = chunk_sum(a.upart + b, a.kr, a.npc);
     a.u[b] = v;
     uu = v * v;
     su = static_cast<double>(a.sz[b]) * v;
@@ -628,7 +644,7 @@ __global__ void __launch_bounds__(256) k_cg_update(GroupArgs g) {
   if (j < a.M) {
     if (a.has_random) {
       if (a.rs > 0) q = a.qs[j];
-      for (int64_t c = 0; c < a.nrcd; ++c) q += a.qpart[c * a.M + j];
+      q = chunk_sum(a.qpart + j, a.M, a.nrcd, q);
     }
     rj = a.r[j];
     pj = a.p[j];
