@@ -593,6 +593,56 @@ def test_explain_batch_stays_inside_its_workspace(dev):
         assert torch.equal(res[t].phi, ref_phi[t]), t
 
 
+@pytest.mark.parametrize("name,n", [("tiny", None), ("cora", 40), ("pubmed", 12)])
+def test_workspaces_need_no_initialisation(dev, name, n):
+    """Every workspace the explainer hands the library (sampling, evaluation,
+    least squares, batch) is filled with 0xFF bytes (NaN in every float, -1
+    in every integer) and followed by a 1 MiB tail of 0xA5: the batched and
+    the single-target calls give the same bits as with ordinary workspaces,
+    so nothing is read before it is written, and no tail byte changes."""
+    from paper_2401_04829_amd import explainer as E
+    tail = 1 << 20
+    given = []
+
+    class Guarded(E._Buffer):
+        def get(self, nbytes):
+            nbytes = max(int(nbytes), 256)
+            t = torch.empty(nbytes + tail, dtype=torch.uint8, device=self.device)
+            t[:nbytes].fill_(0xFF)
+            t[nbytes:].fill_(0xA5)
+            given.append((t, nbytes))
+            self.t = t
+            return t
+
+    def tails_untouched():
+        torch.cuda.synchronize()
+        ok = all(bool((t[k:] == 0xA5).all().item()) for t, k in given)
+        given.clear()
+        return ok
+
+    fields = ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info")
+    cfg = W.make_config(name)
+    targets = list(cfg["targets"])[:n] if n else list(cfg["targets"])
+    ex = explainer_for(cfg)
+    ref = ex.explain_batch(targets, cfg["p"], cfg["seed"])
+    ref1 = [ex.explain(v, cfg["p"], cfg["seed"]) for v in targets[:2]]
+    torch.cuda.synchronize()
+    exg = explainer_for(cfg)
+    for attr in ("ws_sample", "ws_eval", "ws_solve", "ws_batch"):
+        setattr(exg, attr, Guarded(exg.device))
+    _say("guarded workspaces", name, len(targets))
+    res = exg.explain_batch(targets, cfg["p"], cfg["seed"])
+    assert tails_untouched()
+    for t in range(len(targets)):
+        for f in fields:
+            assert torch.equal(getattr(res[t], f), getattr(ref[t], f)), (t, f)
+    for v, r1 in zip(targets[:2], ref1):
+        r = exg.explain(v, cfg["p"], cfg["seed"])
+        assert tails_untouched()
+        for f in fields:
+            assert torch.equal(getattr(r, f), getattr(r1, f)), (v, f)
+
+
 def test_explain_batch_repeated_calls_agree(dev):
     """Repeated batched calls on the same targets give the first call's
     outputs bit for bit, with other device work between them, and equal the
