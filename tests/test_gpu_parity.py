@@ -593,15 +593,13 @@ def test_explain_batch_stays_inside_its_workspace(dev):
         assert torch.equal(res[t].phi, ref_phi[t]), t
 
 
-@pytest.mark.parametrize("name,n", [("tiny", None), ("cora", 40), ("pubmed", 12)])
-def test_workspaces_need_no_initialisation(dev, name, n):
-    """Every workspace the explainer hands the library (sampling, evaluation,
-    least squares, batch) is filled with 0xFF bytes (NaN in every float, -1
-    in every integer) and followed by a 1 MiB tail of 0xA5: the batched and
-    the single-target calls give the same bits as with ordinary workspaces,
-    so nothing is read before it is written, and no tail byte changes."""
+def _guard_workspaces(ex, attrs=("ws_sample", "ws_eval", "ws_solve", "ws_batch", "ws_fid"), tail=1 << 20):
+    """Replace the explainer's workspace buffers by ones whose every request
+    gets a fresh buffer: the bytes asked for filled with 0xFF (NaN in every
+    float, -1 in every integer), then `tail` bytes of 0xA5.  Returns a
+    function that synchronises and tells whether every tail is untouched
+    (and forgets the buffers handed out so far)."""
     from paper_2401_04829_amd import explainer as E
-    tail = 1 << 20
     given = []
 
     class Guarded(E._Buffer):
@@ -614,13 +612,27 @@ def test_workspaces_need_no_initialisation(dev, name, n):
             self.t = t
             return t
 
+    for attr in attrs:
+        setattr(ex, attr, Guarded(ex.device))
+
     def tails_untouched():
         torch.cuda.synchronize()
         ok = all(bool((t[k:] == 0xA5).all().item()) for t, k in given)
         given.clear()
         return ok
+    return tails_untouched
 
-    fields = ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info")
+
+_FIELDS = ("masks", "weights", "y", "f_empty_full", "cls", "phi", "info")
+
+
+@pytest.mark.parametrize("name,n", [("tiny", None), ("cora", 40), ("pubmed", 12)])
+def test_workspaces_need_no_initialisation(dev, name, n):
+    """Every workspace the explainer hands the library (sampling, evaluation,
+    least squares, batch) is filled with 0xFF bytes and followed by a 1 MiB
+    tail of 0xA5: the batched and the single-target calls give the same bits
+    as with ordinary workspaces, so nothing is read before it is written,
+    and no tail byte changes."""
     cfg = W.make_config(name)
     targets = list(cfg["targets"])[:n] if n else list(cfg["targets"])
     ex = explainer_for(cfg)
@@ -628,19 +640,53 @@ def test_workspaces_need_no_initialisation(dev, name, n):
     ref1 = [ex.explain(v, cfg["p"], cfg["seed"]) for v in targets[:2]]
     torch.cuda.synchronize()
     exg = explainer_for(cfg)
-    for attr in ("ws_sample", "ws_eval", "ws_solve", "ws_batch"):
-        setattr(exg, attr, Guarded(exg.device))
+    tails_untouched = _guard_workspaces(exg)
     _say("guarded workspaces", name, len(targets))
     res = exg.explain_batch(targets, cfg["p"], cfg["seed"])
     assert tails_untouched()
     for t in range(len(targets)):
-        for f in fields:
+        for f in _FIELDS:
             assert torch.equal(getattr(res[t], f), getattr(ref[t], f)), (t, f)
     for v, r1 in zip(targets[:2], ref1):
         r = exg.explain(v, cfg["p"], cfg["seed"])
         assert tails_untouched()
-        for f in fields:
+        for f in _FIELDS:
             assert torch.equal(getattr(r, f), getattr(r1, f)), (v, f)
+
+
+def test_gat_and_fidelity_workspaces_need_no_initialisation(dev):
+    """As above for the GAT explainer (batched and single-target calls, 12
+    Cora-shaped targets) and for the fidelity terms of 8 GCN explanations."""
+    from paper_2401_04829_amd.explainer import GatExplainer
+    cfg = W.make_config("cora")
+    P = W.glorot_gat(cfg["X"].shape[1], 8, 16, 7, 41, bias="random")
+    targets = [int(v) for v in cfg["targets"][:12]]
+    ex = GatExplainer(cfg["indptr"], cfg["indices"], cfg["X"], P)
+    ref = ex.explain_batch(targets, 2000, 7)
+    ref1 = ex.explain(targets[0], 2000, 7)
+    torch.cuda.synchronize()
+    exg = GatExplainer(cfg["indptr"], cfg["indices"], cfg["X"], P)
+    tails_untouched = _guard_workspaces(exg)
+    _say("guarded workspaces, gat", len(targets))
+    res = exg.explain_batch(targets, 2000, 7)
+    assert tails_untouched()
+    for t in range(len(targets)):
+        for f in _FIELDS:
+            assert torch.equal(getattr(res[t], f), getattr(ref[t], f)), (t, f)
+    r = exg.explain(targets[0], 2000, 7)
+    assert tails_untouched()
+    for f in _FIELDS:
+        assert torch.equal(getattr(r, f), getattr(ref1, f)), f
+    # fidelity (eq. 7-8) of GCN explanations, ordinary and guarded workspace
+    exf = explainer_for(cfg)
+    exps = list(exf.explain_batch(cfg["targets"][:8], cfg["p"], cfg["seed"]))
+    terms, avg = exf.fidelity(exps, 0.3, 10)
+    torch.cuda.synchronize()
+    terms, avg = terms.clone(), avg.clone()
+    tails_untouched = _guard_workspaces(exf, attrs=("ws_fid",))
+    terms_g, avg_g = exf.fidelity(exps, 0.3, 10)
+    assert tails_untouched()
+    assert torch.equal(terms_g, terms) and torch.equal(avg_g, avg)
 
 
 def test_explain_batch_repeated_calls_agree(dev):
