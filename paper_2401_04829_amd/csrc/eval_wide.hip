@@ -539,10 +539,11 @@ __global__ void __launch_bounds__(256) k_wide_out(const uint64_t* __restrict__ m
 // transform).  The pass rows are the rows r0 .. r0 + nloc - 1 and, with
 // pairs, their complements at pass rows nloc .. 2 nloc - 1 (mask bits and
 // degrees complemented).  One workgroup per (node x, 16 pass rows): x's
-// players are staged in LDS (source, players entering the source) 256 at a
-// time; lane (rg, q) of wavefront w takes pass row 16 blk + 4 w + rg and
-// features 4 q .. 4 q + 3 of each 64-feature chunk, four players' loads in
-// flight.  Players in order, so the sums are the same in every call.
+// players are staged in LDS 256 at a time (source, players entering the
+// source, and the 16 rows' mask bits of them); lane (rg, q) of wavefront w
+// takes pass row 16 blk + 4 w + rg and features 4 q .. 4 q + 3 of each
+// 64-feature chunk, four players' loads in flight.  Players in order, so
+// the sums are the same in every call (an absent player adds 0).
 constexpr int kAggRows = 16;
 __global__ void __launch_bounds__(256) k_wide3_agg(const uint64_t* __restrict__ masks, int64_t wpr, int64_t r0,
                                                    int64_t nloc, bool pairs, const int32_t* __restrict__ dst_ptr,
@@ -550,51 +551,96 @@ __global__ void __launch_bounds__(256) k_wide3_agg(const uint64_t* __restrict__ 
                                                    const int32_t* __restrict__ deg, const float* __restrict__ H1,
                                                    int h, float* __restrict__ A) {
   __shared__ int32_t su[256], snu[256];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, rg = lane >> 4, q = lane & 15;
+  __shared__ uint32_t sbits[kAggRows][8];   // each row's mask bits of the staged players (complemented rows: NOT)
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, rg = lane >> 4, q = lane & 15;
   const int64_t nr = pairs ? 2 * nloc : nloc;
   const int64_t x = blockIdx.x % n2;
-  const int64_t lr = (blockIdx.x / n2) * kAggRows + 4 * wave + rg;
+  const int64_t lr0 = (blockIdx.x / n2) * kAggRows;
+  // pass row lr -> (clamped pass row, complement?, contracted row)
+  auto rowof = [&](int64_t lr, bool& comp, int64_t& row) {
+    const int64_t lrc = lr < nr ? lr : nr - 1;
+    comp = lrc >= nloc;
+    row = r0 + (comp ? lrc - nloc : lrc);
+    return lrc;
+  };
+  const int slot = 4 * wave + rg;
+  const int64_t lr = lr0 + slot;
   const bool valid = lr < nr;
-  const int64_t lrc = valid ? lr : nr - 1;
-  const bool comp = lrc >= nloc;
-  const int64_t row = r0 + (comp ? lrc - nloc : lrc);   // the contracted row (degrees, mask bits)
-  const uint64_t* mr = masks + row * wpr;
+  bool comp;
+  int64_t row;
+  const int64_t lrc = rowof(lr, comp, row);
   const int32_t* dg = deg + row * n1;
   const float* hr = H1 + lrc * n1 * h;
   const int dgx = dg[x];
   const float dx = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(comp ? (dst_ptr[x + 1] - dst_ptr[x]) - dgx : dgx));
   const int e0 = dst_ptr[x], e1 = dst_ptr[x + 1];
+  const int64_t nbits = static_cast<int64_t>(wpr) * 64;   // bits of a mask row
   for (int f0 = 0; f0 < h; f0 += 64) {
     const int f = f0 + 4 * q;
     const bool fv = f < h;   // (h is a multiple of 16)
+    const int fo = fv ? f : 0;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (fv) {
-      const float4 s4 = *reinterpret_cast<const float4*>(hr + x * h + f);
+    {
+      const float4 s4 = *reinterpret_cast<const float4*>(hr + x * h + fo);
       acc = make_float4(dx * s4.x, dx * s4.y, dx * s4.z, dx * s4.w);
     }
     for (int eb = e0; eb < e1; eb += 256) {
       const int n = e1 - eb < 256 ? e1 - eb : 256;
       __syncthreads();   // the previous chunk's reads are done
-      if (static_cast<int>(threadIdx.x) < n) {
-        const int32_t u = edge_src[eb + threadIdx.x];
-        su[threadIdx.x] = u;
-        snu[threadIdx.x] = u < n1 ? dst_ptr[u + 1] - dst_ptr[u] : 0;
+      if (tid < n) {
+        const int32_t u = edge_src[eb + tid];
+        su[tid] = u;
+        snu[tid] = u < n1 ? dst_ptr[u + 1] - dst_ptr[u] : 0;
+      }
+      if (tid < kAggRows * 8) {
+        // bits eb + 32 w .. + 31 of row slot tid / 8 (players past the chunk are never read)
+        const int sl = tid >> 3, w = tid & 7;
+        bool cs;
+        int64_t rs;
+        rowof(lr0 + sl, cs, rs);
+        const int64_t pos = static_cast<int64_t>(eb) + 32 * w;
+        uint32_t bits = 0;
+        if (pos < nbits) {
+          const uint64_t* mrs = masks + rs * wpr;
+          const int64_t wi = pos >> 6;
+          const int sh = static_cast<int>(pos & 63);
+          const uint64_t lo = mrs[wi];
+          const uint64_t hi = (sh > 32 && wi + 1 < wpr) ? mrs[wi + 1] : 0;
+          bits = static_cast<uint32_t>(sh ? (lo >> sh) | (hi << (64 - sh)) : lo);
+        }
+        sbits[sl][w] = cs ? ~bits : bits;
       }
       __syncthreads();
-#pragma unroll 4
-      for (int j = 0; j < n; ++j) {
-        const int e = eb + j;
-        const int32_t u = su[j];
-        const bool bit = (mr[e >> 6] >> (e & 63)) & 1;
-        // (u >= n1 does not occur in an extracted subgraph: in-neighbours of these nodes lie in H_1)
-        if (bit != comp && u < n1 && fv) {
-          const int du = comp ? snu[j] - dg[u] : dg[u];
-          const float c = __builtin_amdgcn_rsqf(1.0f + static_cast<float>(du));
-          const float4 v = *reinterpret_cast<const float4*>(hr + static_cast<int64_t>(u) * h + f);
-          acc.x = fmaf(c, v.x, acc.x);
-          acc.y = fmaf(c, v.y, acc.y);
-          acc.z = fmaf(c, v.z, acc.z);
-          acc.w = fmaf(c, v.w, acc.w);
+      // four players at a time: absent players (coefficient 0) read x's own
+      // row, already in the cache, so the four loads go out together
+      for (int j0 = 0; j0 < n; j0 += 4) {
+        int uq[4];
+        bool pq[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int j = j0 + t;
+          const int jj = j < n ? j : 0;
+          const int32_t u = su[jj];
+          // (u >= n1 does not occur in an extracted subgraph: in-neighbours of these nodes lie in H_1)
+          pq[t] = j < n && ((sbits[slot][jj >> 5] >> (jj & 31)) & 1u) && u < n1;
+          uq[t] = pq[t] ? u : static_cast<int32_t>(x);
+        }
+        int dq[4];
+        float4 vq[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          dq[t] = dg[uq[t]];
+          vq[t] = *reinterpret_cast<const float4*>(hr + static_cast<int64_t>(uq[t]) * h + fo);
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int j = j0 + t < n ? j0 + t : 0;
+          const int du = comp ? snu[j] - dq[t] : dq[t];
+          const float c = pq[t] ? __builtin_amdgcn_rsqf(1.0f + static_cast<float>(du)) : 0.f;
+          acc.x = fmaf(c, vq[t].x, acc.x);
+          acc.y = fmaf(c, vq[t].y, acc.y);
+          acc.z = fmaf(c, vq[t].z, acc.z);
+          acc.w = fmaf(c, vq[t].w, acc.w);
         }
       }
     }
