@@ -394,19 +394,20 @@ __global__ void __launch_bounds__(kBlockRows, 2) k_wide_l1(
           }
         }
       } else {
-        // the source's row under each coalition (a coalition without the
-        // player skips the load: its coefficient is 0)
+        // the source's row under the coalition that holds the player (the
+        // row itself, or with pairs its complement): one load, no branch, so
+        // the loads of the four row tiles go out together; the other
+        // coefficient is 0 and adds nothing
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct) {
-          if (cw[ct] != 0.f) {
-            const float4 zu = *reinterpret_cast<const float4*>(Zrow + (lr[ct] * n1 + u) * h + f);
-            D[ct][ft][0] = fmaf(cw[ct], zu.x, D[ct][ft][0]);
-            D[ct][ft][1] = fmaf(cw[ct], zu.y, D[ct][ft][1]);
-            D[ct][ft][2] = fmaf(cw[ct], zu.z, D[ct][ft][2]);
-            D[ct][ft][3] = fmaf(cw[ct], zu.w, D[ct][ft][3]);
-          }
-          if (PAIRS && cp[ct] != 0.f) {
-            const float4 zu = *reinterpret_cast<const float4*>(Zrow + ((lr[ct] + nloc) * n1 + u) * h + f);
+          const bool own = !PAIRS || cw[ct] != 0.f;
+          const float4 zu =
+              *reinterpret_cast<const float4*>(Zrow + ((own ? lr[ct] : lr[ct] + nloc) * n1 + u) * h + f);
+          D[ct][ft][0] = fmaf(cw[ct], zu.x, D[ct][ft][0]);
+          D[ct][ft][1] = fmaf(cw[ct], zu.y, D[ct][ft][1]);
+          D[ct][ft][2] = fmaf(cw[ct], zu.z, D[ct][ft][2]);
+          D[ct][ft][3] = fmaf(cw[ct], zu.w, D[ct][ft][3]);
+          if (PAIRS) {
             P[ct][ft][0] = fmaf(cp[ct], zu.x, P[ct][ft][0]);
             P[ct][ft][1] = fmaf(cp[ct], zu.y, P[ct][ft][1]);
             P[ct][ft][2] = fmaf(cp[ct], zu.z, P[ct][ft][2]);
