@@ -388,6 +388,9 @@ int gnnshap_explain_batch_workspace(const gnnshap_subgraph* sgs, const gnnshap_s
  * X, target_class and the model as for gnnshap_eval_coalitions.  Two-layer
  * models with X W_1 given and one-workgroup systems run batched; other
  * targets go through the single-target kernels in the same sequence.
+ * Systems factored by the multi-block Cholesky are set up one by one as
+ * their coalition values are queued and factored and solved in runs of up
+ * to 24 (one launch per step of the factorisation for the whole run).
  * Systems solved iteratively (more players than their plan's
  * iterative_threshold) run in two groups of up to three on the library's
  * side streams, each group advancing its systems together (one launch per
