@@ -1036,6 +1036,7 @@ int launch_wide3_t(const WideShape& s, const WideWs& w, const gnnshap_subgraph* 
   if (nloc > s.pass) return fail(GNNSHAP_EINVAL, "pass larger than the workspace's");
   if (nloc <= 0) return GNNSHAP_OK;
   const int64_t items = (pairs ? 2 : 1) * nloc * s.n2;
+  if (ceil_div(items * 64, 256) > INT32_MAX) return fail(GNNSHAP_EUNSUPPORTED, "evaluation grid too large");
   k_wide3_t<<<static_cast<unsigned>(ceil_div(items * 64, 256)), 256, 0, st>>>(
       masks, wpr, r0, nloc, pairs, pairs ? s.k / 2 : 0, sg->dst_ptr, s.n1, s.n2, w.deg, w.Z2, s.h2, b2, W3, s.C, ctl,
       s.k, w.t);
